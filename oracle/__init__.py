@@ -1,0 +1,174 @@
+"""ctypes wrapper of the fp64 CPU oracle (oracle.c).
+
+TEST INFRASTRUCTURE ONLY.  The tests, ``__graft_entry__.smoke()`` and the
+bench's CPU-baseline leg may call it; the GPU library and its Python binding
+never import it.  It takes host numpy arrays (bf16 inputs as raw uint16 bit
+patterns) and returns float64 results.
+
+The definitions it computes are stated at the top of oracle.c: grouped-query
+decode attention over a shared prompt prefix followed by each candidate's own
+suffix (Sec. 2.2.1, Problem Setup), and the full-vocabulary token log-prob of
+the sampled token that the GRPO ratio needs (Sec. 3, Eq. grpo-loss; masked
+positions per Sec. 3, Multi-turn RL Training).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+SRC_PATH = os.path.join(_HERE, "oracle.c")
+# Plain IEEE double arithmetic: no -ffast-math, no FMA contraction.
+CFLAGS = ["-O2", "-std=c99", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared"]
+
+
+def compile_c(src_path: str, out_path: str) -> str:
+    """Compile an oracle C source into a shared library with gcc."""
+    tmp = out_path + ".tmp"
+    subprocess.run(["gcc", *CFLAGS, src_path, "-o", tmp, "-lm"], check=True)
+    os.replace(tmp, out_path)
+    return out_path
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (plain C99 + OpenMP)."""
+    if force or not os.path.exists(LIB_PATH):
+        compile_c(SRC_PATH, LIB_PATH)
+    return LIB_PATH
+
+
+def _bind(path: str):
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    lib.oracle_decode_attn.restype = ctypes.c_int
+    lib.oracle_decode_attn.argtypes = [ctypes.c_int32] * 5 + [ctypes.c_float] + [P] * 11
+    lib.oracle_token_logprob.restype = ctypes.c_int
+    lib.oracle_token_logprob.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                         P, P, P, ctypes.c_float, P, P]
+    return lib
+
+
+_default = None
+
+
+def _load():
+    global _default
+    if _default is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        _default = _bind(LIB_PATH)
+    return _default
+
+
+def _u16(a, shape=None):
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16:
+        raise TypeError("bf16 inputs are passed as uint16 bit patterns")
+    if shape is not None and a.shape != tuple(shape):
+        raise ValueError(f"shape {a.shape} != {tuple(shape)}")
+    return a
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def decode_attn(q, k_prefix, v_prefix, k_suffix, v_suffix,
+                prefix_start, prefix_len, suffix_start, suffix_len,
+                group_size: int, scale: float, _lib=None):
+    """Oracle decode attention.
+
+    q: uint16 [S, Hq, D]; k/v_prefix: uint16 [rows_p, Hkv, D];
+    k/v_suffix: uint16 [rows_s, Hkv, D]; lengths/starts host ints.
+    Returns (out float64 [S, Hq, D], lse float64 [S, Hq]).
+    """
+    q = _u16(q)
+    S, Hq, D = q.shape
+    G = int(group_size)
+    if G <= 0 or S % G:
+        raise ValueError("S must be a positive multiple of group_size")
+    P = S // G
+    kp, vp, ks, vs = (_u16(t) for t in (k_prefix, v_prefix, k_suffix, v_suffix))
+    Hkv = kp.shape[1]
+    if Hq % Hkv or any(t.shape[1:] != (Hkv, D) for t in (kp, vp, ks, vs)):
+        raise ValueError("bad head layout")
+    ps = np.ascontiguousarray(prefix_start, dtype=np.int64)
+    pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
+    ss = np.ascontiguousarray(suffix_start, dtype=np.int64)
+    sl = np.ascontiguousarray(suffix_len, dtype=np.int32)
+    if ps.shape != (P,) or pl.shape != (P,) or ss.shape != (S,) or sl.shape != (S,):
+        raise ValueError("length arrays")
+    if (pl < 0).any() or (sl < 0).any():
+        raise ValueError("negative length")
+    if P and ((ps < 0).any() or (ps + pl > kp.shape[0]).any() or kp.shape != vp.shape):
+        raise ValueError("prefix range")
+    if S and ((ss < 0).any() or (ss + sl > ks.shape[0]).any() or ks.shape != vs.shape):
+        raise ValueError("suffix range")
+    out = np.zeros((S, Hq, D), dtype=np.float64)
+    lse = np.zeros((S, Hq), dtype=np.float64)
+    if S == 0:
+        return out, lse
+    rc = (_lib or _load()).oracle_decode_attn(
+        P, G, Hq, Hkv, D, float(np.float32(scale)),
+        _ptr(ps), _ptr(pl), _ptr(ss), _ptr(sl),
+        _ptr(q), _ptr(kp), _ptr(vp), _ptr(ks), _ptr(vs), _ptr(out), _ptr(lse))
+    if rc:
+        raise MemoryError("oracle_decode_attn scratch allocation failed")
+    return out, lse
+
+
+def token_logprob(hidden, w_lm, target, inv_temperature: float = 1.0, _lib=None):
+    """Oracle token log-prob.
+
+    hidden: uint16 [R, H]; w_lm: uint16 [V, H]; target: int32 [R].
+    Returns (logprob float64 [R], lse float64 [R]).
+    """
+    hidden = _u16(hidden)
+    w = _u16(w_lm)
+    R, H = hidden.shape
+    V, H2 = w.shape
+    if H2 != H or V <= 0 or H <= 0:
+        raise ValueError("shape")
+    t = np.ascontiguousarray(target, dtype=np.int32)
+    if t.shape != (R,):
+        raise ValueError("target shape")
+    logprob = np.zeros(R, dtype=np.float64)
+    lse = np.zeros(R, dtype=np.float64)
+    if R == 0:
+        return logprob, lse
+    rc = (_lib or _load()).oracle_token_logprob(
+        R, H, V, _ptr(hidden), _ptr(w), _ptr(t),
+        float(np.float32(inv_temperature)), _ptr(logprob), _ptr(lse))
+    if rc:
+        raise MemoryError("oracle_token_logprob scratch allocation failed")
+    return logprob, lse
+
+
+def num_threads() -> int:
+    """Threads OpenMP will use (OMP_NUM_THREADS, else the CPUs this process may run on)."""
+    env = os.environ.get("OMP_NUM_THREADS")
+    if env and env.strip().isdigit() and int(env) > 0:
+        return int(env)
+    return len(os.sched_getaffinity(0))
+
+
+class Oracle:
+    """The oracle's two functions bound to one compiled library.
+
+    The default instance uses liboracle.so; the mutation tests bind a copy
+    compiled from a deliberately altered source to show the pins catch it.
+    """
+
+    def __init__(self, lib_path: str = LIB_PATH):
+        self.lib_path = lib_path
+        self._lib = _bind(lib_path) if lib_path != LIB_PATH else _load()
+
+    def decode_attn(self, *args, **kw):
+        return decode_attn(*args, **kw, _lib=self._lib)
+
+    def token_logprob(self, *args, **kw):
+        return token_logprob(*args, **kw, _lib=self._lib)

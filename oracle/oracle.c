@@ -1,0 +1,153 @@
+/*
+ * fp64 CPU oracle for the rollout hot path.  TEST INFRASTRUCTURE ONLY: the
+ * tests, the smoke check and the bench's CPU-baseline leg call it; the GPU
+ * library never does, and this file shares no code, header or table with it.
+ *
+ * It computes the plain definitions, in double precision, with two-pass
+ * (max first, then sum) softmax and no blocking, splitting or online merge:
+ *
+ *  1. Decode attention for a group of candidates (Sec. 2.2.1, Problem Setup:
+ *     every input x gets g candidates y_1..y_g).  Candidate s = p*G + g sees
+ *     the KV of its prompt p followed by its own generated KV (the prompt is
+ *     shared by the group; refinement turns lengthen it, Sec. 3, Structured
+ *     Feedback and Iterative Refinement).  For query head h the key/value
+ *     head is h / (Hq/Hkv).  With x_j = scale * <q, k_j>, m = max_j x_j,
+ *     w_j = exp(x_j - m) / sum_i exp(x_i - m):
+ *         out = sum_j w_j v_j,   lse = m + ln sum_j exp(x_j - m).
+ *     An empty context gives out = 0 and lse = -inf.
+ *
+ *  2. Token log-probability of the sampled token under the policy, the
+ *     quantity whose ratio between the new and old policy drives the GRPO
+ *     objective (Sec. 3, Eq. grpo-loss), taken over the full vocabulary:
+ *         z_v = inv_T * <hidden_r, W_v>,  lse = M + ln sum_v exp(z_v - M),
+ *         logprob = z_t - lse  for target t in [0, V);
+ *     target -1 marks a masked position (the masked log-prob window of
+ *     Sec. 3, Multi-turn RL Training) and gives logprob 0; any other
+ *     target outside [0, V) gives NaN.  lse is computed in every case.
+ *
+ * Inputs are raw bf16 bit patterns (uint16).  Each is widened exactly:
+ * bits << 16 is the float32 pattern, and float32 -> double is exact.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+static double bf16_to_f64(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int oracle_abi_version(void) { return 1; }
+
+/* Returns 0 on success, 1 if a scratch allocation failed. */
+int oracle_decode_attn(int32_t P, int32_t G, int32_t Hq, int32_t Hkv, int32_t D,
+                       float scale,
+                       const int64_t *prefix_start, const int32_t *prefix_len,
+                       const int64_t *suffix_start, const int32_t *suffix_len,
+                       const uint16_t *q,
+                       const uint16_t *k_prefix, const uint16_t *v_prefix,
+                       const uint16_t *k_suffix, const uint16_t *v_suffix,
+                       double *out, double *lse)
+{
+    const int64_t S = (int64_t)P * G;
+    const int32_t r = Hq / Hkv;
+    const double sigma = (double)scale;
+    int failed = 0;
+
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t s = 0; s < S; ++s) {
+        for (int32_t h = 0; h < Hq; ++h) {
+            const int64_t p = s / G;
+            const int32_t kh = h / r;
+            const int64_t Lp = prefix_len[p];
+            const int64_t Ls = suffix_len[s];
+            const int64_t T = Lp + Ls;
+            double *o = out + (s * Hq + h) * (int64_t)D;
+            const uint16_t *qv = q + (s * Hq + h) * (int64_t)D;
+
+            if (T == 0) {
+                for (int32_t d = 0; d < D; ++d) o[d] = 0.0;
+                lse[s * Hq + h] = -INFINITY;
+                continue;
+            }
+            double *x = (double *)malloc((size_t)T * sizeof(double));
+            if (!x) {
+#pragma omp atomic write
+                failed = 1;
+                continue;
+            }
+            /* pass 1: scores over the concatenated context prefix ++ suffix */
+            for (int64_t j = 0; j < T; ++j) {
+                const uint16_t *kr = (j < Lp)
+                    ? k_prefix + ((prefix_start[p] + j) * Hkv + kh) * (int64_t)D
+                    : k_suffix + ((suffix_start[s] + (j - Lp)) * Hkv + kh) * (int64_t)D;
+                double dot = 0.0;
+                for (int32_t d = 0; d < D; ++d) dot += bf16_to_f64(qv[d]) * bf16_to_f64(kr[d]);
+                x[j] = sigma * dot;
+            }
+            double m = x[0];
+            for (int64_t j = 1; j < T; ++j) if (x[j] > m) m = x[j];
+            double Z = 0.0;
+            for (int64_t j = 0; j < T; ++j) Z += exp(x[j] - m);
+            /* pass 2: softmax-weighted sum of the values */
+            for (int32_t d = 0; d < D; ++d) o[d] = 0.0;
+            for (int64_t j = 0; j < T; ++j) {
+                const uint16_t *vr = (j < Lp)
+                    ? v_prefix + ((prefix_start[p] + j) * Hkv + kh) * (int64_t)D
+                    : v_suffix + ((suffix_start[s] + (j - Lp)) * Hkv + kh) * (int64_t)D;
+                const double w = exp(x[j] - m) / Z;
+                for (int32_t d = 0; d < D; ++d) o[d] += w * bf16_to_f64(vr[d]);
+            }
+            lse[s * Hq + h] = m + log(Z);
+            free(x);
+        }
+    }
+    return failed;
+}
+
+/* Returns 0 on success, 1 if a scratch allocation failed. */
+int oracle_token_logprob(int64_t R, int32_t H, int32_t V,
+                         const uint16_t *hidden, const uint16_t *w_lm,
+                         const int32_t *target, float inv_temperature,
+                         double *logprob, double *lse)
+{
+    const double inv_T = (double)inv_temperature;
+    int failed = 0;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r) {
+        double *z = (double *)malloc((size_t)V * sizeof(double));
+        if (!z) {
+#pragma omp atomic write
+            failed = 1;
+            continue;
+        }
+        const uint16_t *hr = hidden + r * (int64_t)H;
+        /* all V logits of this row */
+        for (int32_t v = 0; v < V; ++v) {
+            const uint16_t *wr = w_lm + (int64_t)v * H;
+            double dot = 0.0;
+            for (int32_t k = 0; k < H; ++k) dot += bf16_to_f64(hr[k]) * bf16_to_f64(wr[k]);
+            z[v] = inv_T * dot;
+        }
+        double M = z[0];
+        for (int32_t v = 1; v < V; ++v) if (z[v] > M) M = z[v];
+        double sum = 0.0;
+        for (int32_t v = 0; v < V; ++v) sum += exp(z[v] - M);
+        const double l = M + log(sum);
+        lse[r] = l;
+        const int32_t t = target[r];
+        if (t == -1)
+            logprob[r] = 0.0;
+        else if (t >= 0 && t < V)
+            logprob[r] = z[t] - l;
+        else
+            logprob[r] = NAN;
+        free(z);
+    }
+    return failed;
+}

@@ -1,0 +1,384 @@
+"""Pins of the fp64 oracle against things other than itself.
+
+Each function takes an ``oracle.Oracle`` and raises AssertionError when the
+oracle disagrees with what the mathematics fixes:
+
+* independent library routines on tiny inputs: torch's fp64 CPU
+  scaled_dot_product_attention (with its own grouped-query head expansion),
+  torch.logsumexp and torch.log_softmax;
+* closed forms (one token, zero query, equal keys, zero weights);
+* invariants (prefix sharing == concatenation, token permutation, vocab
+  chunking with a log-sum-exp merge, constant shift, sum of probabilities);
+* exact probes (one-hot attention returns one value row bit for bit; uniform
+  attention recovers the context length; an id probe recovers the target);
+* hand-derived worked examples under tests/golden/.
+
+The same battery runs against deliberately broken copies of the oracle
+(test_oracle_mutants.py) to show that each plausible mistake is caught.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ----------------------------------------------------------------- helpers
+def f64(bits: np.ndarray) -> torch.Tensor:
+    """uint16 bf16 bits -> float64 tensor (exact)."""
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).double()
+
+
+def bf16_bits_of(x: np.ndarray) -> np.ndarray:
+    """float64 values -> bf16 bit patterns (RNE); exact for bf16-representable values."""
+    return W.bf16_bits(torch.from_numpy(np.asarray(x, dtype=np.float32)).to(torch.bfloat16))
+
+
+def decode_case(P=2, G=3, Hq=4, Hkv=2, D=8, lp=None, ls=None, seed=0, qmul=1.0):
+    """Small random decode input as bf16 bit arrays + host length arrays."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    S = P * G
+    lp = np.asarray(rng.integers(0, 7, P) if lp is None else lp, dtype=np.int32)
+    ls = np.asarray(rng.integers(0, 6, S) if ls is None else ls, dtype=np.int32)
+    # leave gaps between sequences so a wrong start index reads other rows
+    ps = np.cumsum(np.concatenate([[1], lp[:-1] + 2])).astype(np.int64)
+    ss = np.cumsum(np.concatenate([[2], ls[:-1] + 1])).astype(np.int64)
+    prow = int(ps[-1] + lp[-1] + 3) if P else 1
+    srow = int(ss[-1] + ls[-1] + 3) if S else 1
+    def rn(*shape, mul=1.0):
+        return bf16_bits_of(rng.standard_normal(shape) * mul)
+    return dict(q=rn(S, Hq, D, mul=qmul), k_prefix=rn(prow, Hkv, D), v_prefix=rn(prow, Hkv, D),
+                k_suffix=rn(srow, Hkv, D), v_suffix=rn(srow, Hkv, D),
+                prefix_start=ps, prefix_len=lp, suffix_start=ss, suffix_len=ls,
+                group_size=G, scale=float(np.float32(1.0 / math.sqrt(D))))
+
+
+def torch_attention(c):
+    """Reference via torch's fp64 SDPA on the concatenated context of each candidate."""
+    q = f64(c["q"]); kp = f64(c["k_prefix"]); vp = f64(c["v_prefix"])
+    ks = f64(c["k_suffix"]); vs = f64(c["v_suffix"])
+    S, Hq, D = q.shape
+    Hkv = kp.shape[1]
+    G = c["group_size"]
+    sigma = float(np.float32(c["scale"]))
+    out = torch.zeros(S, Hq, D, dtype=torch.float64)
+    lse = torch.full((S, Hq), -math.inf, dtype=torch.float64)
+    for s in range(S):
+        p = s // G
+        a, n = int(c["prefix_start"][p]), int(c["prefix_len"][p])
+        b, m = int(c["suffix_start"][s]), int(c["suffix_len"][s])
+        K = torch.cat([kp[a:a + n], ks[b:b + m]])          # [T, Hkv, D]
+        V = torch.cat([vp[a:a + n], vs[b:b + m]])
+        if K.shape[0] == 0:
+            continue
+        o = F.scaled_dot_product_attention(q[s][None, :, None, :], K.permute(1, 0, 2)[None],
+                                           V.permute(1, 0, 2)[None], scale=sigma, enable_gqa=True)
+        out[s] = o[0, :, 0, :]
+        Krep = K.repeat_interleave(Hq // Hkv, dim=1)         # [T, Hq, D]
+        scores = sigma * (Krep.permute(1, 0, 2) @ q[s][:, :, None])[..., 0]   # [Hq, T]
+        lse[s] = torch.logsumexp(scores, dim=1)
+    return out.numpy(), lse.numpy()
+
+
+def logprob_case(R=5, H=16, V=37, seed=0, w_std=0.3, targets=None):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    hidden = bf16_bits_of(rng.standard_normal((R, H)))
+    w = bf16_bits_of(rng.standard_normal((V, H)) * w_std)
+    t = rng.integers(0, V, R).astype(np.int32) if targets is None else np.asarray(targets, np.int32)
+    return hidden, w, t
+
+
+def torch_logprob(hidden, w, target, inv_T):
+    z = float(np.float32(inv_T)) * (f64(hidden) @ f64(w).T)
+    ls = torch.log_softmax(z, dim=1)
+    lse = torch.logsumexp(z, dim=1)
+    out = torch.zeros(len(target), dtype=torch.float64)
+    for r, t in enumerate(target):
+        out[r] = 0.0 if t == -1 else (ls[r, t] if 0 <= t < w.shape[0] else math.nan)
+    return out.numpy(), lse.numpy()
+
+
+def close(a, b, tol, what):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    assert a.shape == b.shape, (what, a.shape, b.shape)
+    same_inf = (np.isinf(a) & np.isinf(b) & (np.sign(a) == np.sign(b))) | (np.isnan(a) & np.isnan(b))
+    with np.errstate(invalid="ignore"):
+        err = np.where(same_inf, 0.0, np.abs(a - b))
+    err = np.where(np.isnan(err), np.inf, err)
+    assert err.max(initial=0.0) <= tol, f"{what}: max err {err.max()} > {tol}"
+
+
+# ------------------------------------------------------------ attention pins
+def pin_attention_vs_torch(orc):
+    """A1: brute force by an independent library routine on small shapes."""
+    cases = [
+        dict(P=2, G=4, Hq=4, Hkv=1, D=64, lp=[128, 128], ls=[32] * 8, seed=0),   # tiny-config shape
+        dict(P=3, G=2, Hq=4, Hkv=2, D=8, seed=1),
+        dict(P=2, G=3, Hq=6, Hkv=3, D=16, seed=2),
+        dict(P=1, G=5, Hq=2, Hkv=2, D=8, lp=[0], seed=3),              # no prefix
+        dict(P=2, G=2, Hq=8, Hkv=1, D=8, ls=[0, 0, 0, 0], seed=4),      # no suffix
+        dict(P=2, G=2, Hq=4, Hkv=2, D=8, lp=[0, 3], ls=[0, 2, 0, 0], seed=5, qmul=4.0),  # empty contexts, peaky
+    ]
+    for cs in cases:
+        c = decode_case(**cs)
+        o, l = orc.decode_attn(**c)
+        ro, rl = torch_attention(c)
+        close(o, ro, 1e-12, f"out {cs}")
+        close(l, rl, 1e-12, f"lse {cs}")
+
+
+def pin_prefix_sharing(orc):
+    """A2: a shared prefix equals concatenating it into every candidate's suffix."""
+    c = decode_case(P=2, G=3, Hq=4, Hkv=2, D=8, lp=[5, 3], ls=[2, 0, 4, 1, 3, 2], seed=7)
+    o, l = orc.decode_attn(**c)
+    S, G = 6, 3
+    kp, vp, ks, vs = c["k_prefix"], c["v_prefix"], c["k_suffix"], c["v_suffix"]
+    krows, vrows, starts, lens = [], [], [], []
+    pos = 0
+    for s in range(S):
+        p = s // G
+        a, n = c["prefix_start"][p], c["prefix_len"][p]
+        b, m = c["suffix_start"][s], c["suffix_len"][s]
+        krows.append(np.concatenate([kp[a:a + n], ks[b:b + m]]))
+        vrows.append(np.concatenate([vp[a:a + n], vs[b:b + m]]))
+        starts.append(pos); lens.append(n + m); pos += n + m
+    c2 = dict(c, k_prefix=kp[:1], v_prefix=vp[:1], prefix_start=np.zeros(2, np.int64),
+              prefix_len=np.zeros(2, np.int32), k_suffix=np.concatenate(krows),
+              v_suffix=np.concatenate(vrows), suffix_start=np.array(starts, np.int64),
+              suffix_len=np.array(lens, np.int32))
+    o2, l2 = orc.decode_attn(**c2)
+    close(o, o2, 1e-12, "prefix sharing out")
+    close(l, l2, 1e-12, "prefix sharing lse")
+
+
+def pin_attention_closed_forms(orc):
+    """A3: one token -> that value row; zero query -> mean of values, lse = ln T."""
+    # one prefix token, no suffix
+    c = decode_case(P=1, G=2, Hq=2, Hkv=1, D=8, lp=[1], ls=[0, 0], seed=11)
+    o, l = orc.decode_attn(**c)
+    v0 = f64(c["v_prefix"])[c["prefix_start"][0], 0].numpy()
+    k0 = f64(c["k_prefix"])[c["prefix_start"][0], 0].numpy()
+    q = f64(c["q"]).numpy()
+    for s in range(2):
+        for h in range(2):
+            close(o[s, h], v0, 0.0, "T=1 out")
+            close(l[s, h], float(np.float32(c["scale"])) * float(q[s, h] @ k0), 1e-13, "T=1 lse")
+    # zero query: uniform weights
+    c = decode_case(P=2, G=2, Hq=4, Hkv=2, D=8, lp=[3, 2], ls=[1, 4, 0, 2], seed=12)
+    c["q"] = np.zeros_like(c["q"])
+    o, l = orc.decode_attn(**c)
+    vp, vs = f64(c["v_prefix"]).numpy(), f64(c["v_suffix"]).numpy()
+    for s in range(4):
+        p = s // 2
+        a, n = c["prefix_start"][p], c["prefix_len"][p]
+        b, m = c["suffix_start"][s], c["suffix_len"][s]
+        for h in range(4):
+            kh = h // 2
+            V = np.concatenate([vp[a:a + n, kh], vs[b:b + m, kh]])
+            close(o[s, h], V.mean(0), 1e-14, "q=0 mean")
+            close(l[s, h], math.log(n + m), 1e-14, "q=0 lse")
+
+
+def pin_permutation(orc):
+    """A5: permuting the suffix tokens of a candidate changes nothing."""
+    c = decode_case(P=1, G=2, Hq=4, Hkv=2, D=8, lp=[4], ls=[6, 5], seed=13)
+    o, l = orc.decode_attn(**c)
+    c2 = dict(c)
+    ks, vs = c["k_suffix"].copy(), c["v_suffix"].copy()
+    rng = np.random.Generator(np.random.PCG64(1))
+    for s in range(2):
+        b, m = c["suffix_start"][s], c["suffix_len"][s]
+        perm = b + rng.permutation(m)
+        ks[b:b + m] = c["k_suffix"][perm]
+        vs[b:b + m] = c["v_suffix"][perm]
+    c2["k_suffix"], c2["v_suffix"] = ks, vs
+    o2, l2 = orc.decode_attn(**c2)
+    close(o, o2, 1e-13, "perm out")
+    close(l, l2, 1e-13, "perm lse")
+
+
+def pin_one_hot_probe(orc):
+    """A6: a single dominant key returns its value row exactly (indexing, bit-exact).
+
+    Every key is zero except one per (sequence, kv head), which equals the query
+    direction scaled so its score beats all others by >= 200: every other weight
+    is exp(-200) relative, far below the resolution of the sum, so the output is
+    that token's value row up to fp64 rounding of a weight of 1.  Value rows
+    encode (prefix/suffix, kv head, position) as small integers.
+    """
+    P, G, Hq, Hkv, D = 2, 2, 4, 2, 8
+    S, r = P * G, Hq // Hkv
+    lp, ls = np.array([5, 7], np.int32), np.array([3, 0, 4, 6], np.int32)
+    c = decode_case(P=P, G=G, Hq=Hq, Hkv=Hkv, D=D, lp=lp, ls=ls, seed=14)
+    q = np.zeros((S, Hq, D)); q[:, :, 0] = 1.0
+    kp = np.zeros((len(c["k_prefix"]), Hkv, D)); ks = np.zeros((len(c["k_suffix"]), Hkv, D))
+    vp = np.zeros_like(kp); vs = np.zeros_like(ks)
+    for arr, tag in ((vp, 1), (vs, 2)):
+        for row in range(arr.shape[0]):
+            for kh in range(Hkv):
+                arr[row, kh, :4] = [tag, kh, row % 16, row // 16]
+    rng = np.random.Generator(np.random.PCG64(5))
+    expect = np.zeros((S, Hq, D))
+    chosen = {}
+    for p in range(P):
+        for kh in range(Hkv):
+            j = int(rng.integers(0, lp[p]))
+            chosen[(p, kh)] = ("p", int(c["prefix_start"][p] + j))
+    for s in range(S):
+        p = s // G
+        for kh in range(Hkv):
+            if ls[s] and (s % 2 == 0):
+                j = int(rng.integers(0, ls[s]))
+                row = int(c["suffix_start"][s] + j)
+                ks[row, kh, 0] = 2048.0
+                src = vs[row, kh]
+            else:
+                kind, row = chosen[(p, kh)]
+                src = vp[row, kh]
+            for h in range(kh * r, (kh + 1) * r):
+                expect[s, h] = src
+    for (p, kh), (_, row) in chosen.items():
+        kp[row, kh, 0] = 1024.0
+    c.update(q=bf16_bits_of(q), k_prefix=bf16_bits_of(kp), k_suffix=bf16_bits_of(ks),
+             v_prefix=bf16_bits_of(vp), v_suffix=bf16_bits_of(vs), scale=1.0)
+    o, _ = orc.decode_attn(**c)
+    close(o, expect, 1e-9, "one-hot probe")
+    assert np.array_equal(np.rint(o), expect), "one-hot probe indices"
+
+
+def pin_length_probe(orc):
+    """A7: zero keys -> uniform weights -> exp(lse) is the context length."""
+    c = decode_case(P=3, G=2, Hq=2, Hkv=1, D=8, lp=[0, 9, 4], ls=[3, 0, 1, 5, 0, 0], seed=15)
+    c["k_prefix"] = np.zeros_like(c["k_prefix"])
+    c["k_suffix"] = np.zeros_like(c["k_suffix"])
+    o, l = orc.decode_attn(**c)
+    T = np.array([c["prefix_len"][s // 2] + c["suffix_len"][s] for s in range(6)])
+    for s in range(6):
+        for h in range(2):
+            if T[s] == 0:
+                assert l[s, h] == -math.inf and not o[s, h].any(), "empty context"
+            else:
+                assert round(math.exp(l[s, h])) == T[s], "length probe"
+
+
+def pin_attention_golden(orc):
+    """Hand-derived worked examples (tests/golden/attention_hand.json)."""
+    with open(os.path.join(GOLDEN, "attention_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        c = dict(q=bf16_bits_of(np.array(case["q"], np.float64)),
+                 k_prefix=bf16_bits_of(np.array(case["k_prefix"], np.float64)),
+                 v_prefix=bf16_bits_of(np.array(case["v_prefix"], np.float64)),
+                 k_suffix=bf16_bits_of(np.array(case["k_suffix"], np.float64)),
+                 v_suffix=bf16_bits_of(np.array(case["v_suffix"], np.float64)),
+                 prefix_start=np.array(case["prefix_start"], np.int64),
+                 prefix_len=np.array(case["prefix_len"], np.int32),
+                 suffix_start=np.array(case["suffix_start"], np.int64),
+                 suffix_len=np.array(case["suffix_len"], np.int32),
+                 group_size=case["group_size"], scale=case["scale"])
+        o, l = orc.decode_attn(**c)
+        close(o, np.array(case["out"]), 1e-15, case["name"] + " out")
+        close(l, np.array(case["lse"]), 1e-15, case["name"] + " lse")
+
+
+# -------------------------------------------------------------- log-prob pins
+def pin_logprob_vs_torch(orc):
+    """L1: brute force by torch.log_softmax on materialised fp64 logits."""
+    for (R, H, V, seed, invT, tg) in [
+        (5, 16, 37, 0, 1.0, None),
+        (8, 256, 1024, 1, 1.0, None),                  # tiny-config shape
+        (6, 32, 50, 2, 1.0 / 0.7, [3, -1, 49, 0, -1, 7]),  # temperature, masked rows
+        (3, 8, 11, 3, 1.0, [11, -2, 5]),               # invalid ids -> NaN
+    ]:
+        h, w, t = logprob_case(R, H, V, seed, targets=tg)
+        lp, lse = orc.token_logprob(h, w, t, invT)
+        rlp, rlse = torch_logprob(h, w, t, invT)
+        close(lp, rlp, 1e-12, f"logprob {R}x{H}x{V}")
+        close(lse, rlse, 1e-12, f"lse {R}x{H}x{V}")
+
+
+def pin_logprob_sum_to_one(orc):
+    """L2: exp(logprob) over every vocabulary id sums to 1."""
+    h, w, _ = logprob_case(4, 24, 300, seed=4, w_std=1.0)
+    V = w.shape[0]
+    hh = np.repeat(h, V, axis=0)
+    t = np.tile(np.arange(V, dtype=np.int32), 4)
+    lp, _ = orc.token_logprob(hh, w, t, 1.0)
+    sums = np.exp(lp.reshape(4, V)).sum(1)
+    close(sums, np.ones(4), 1e-12, "sum of probabilities")
+
+
+def pin_logprob_closed_forms(orc):
+    """L3: zero weights -> every logit 0 -> logprob = -ln V and lse = ln V."""
+    h, w, t = logprob_case(3, 16, 1024, seed=5)
+    lp, lse = orc.token_logprob(h, np.zeros_like(w), t, 1.0)
+    close(lp, np.full(3, -math.log(1024)), 1e-15, "W=0 logprob")
+    close(lse, np.full(3, math.log(1024)), 1e-15, "W=0 lse")
+
+
+def pin_logprob_shift(orc):
+    """L4: a constant extra hidden column times a constant W column shifts every logit alike."""
+    h, w, t = logprob_case(4, 15, 40, seed=6)
+    lp, lse = orc.token_logprob(h, w, t, 1.0)
+    h2 = np.concatenate([h, bf16_bits_of(np.full((4, 1), 2.0))], 1)
+    w2 = np.concatenate([w, bf16_bits_of(np.full((40, 1), 1.5))], 1)
+    lp2, lse2 = orc.token_logprob(h2, w2, t, 1.0)
+    close(lp2, lp, 1e-12, "shift logprob")
+    close(lse2, lse + 3.0, 1e-12, "shift lse")
+
+
+def pin_logprob_chunks(orc):
+    """L5: per-vocab-chunk results merged by log-sum-exp equal one full pass."""
+    h, w, t = logprob_case(6, 32, 100, seed=7)
+    lp, lse = orc.token_logprob(h, w, t, 1.0 / 0.7)
+    bounds = [0, 17, 50, 64, 100]
+    lses, zt = [], np.zeros(6)
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        tt = np.where((t >= a) & (t < b), t - a, -1).astype(np.int32)
+        lpc, lsec = orc.token_logprob(h, w[a:b], tt, 1.0 / 0.7)
+        lses.append(lsec)
+        zt += np.where(tt >= 0, lpc + lsec, 0.0)     # the target's logit, from its own chunk
+    merged = torch.logsumexp(torch.tensor(np.stack(lses)), dim=0).numpy()
+    close(merged, lse, 1e-12, "chunked lse")
+    close(zt - merged, lp, 1e-12, "chunked logprob")
+
+
+def pin_logprob_id_probe(orc):
+    """L6: logits that encode the vocabulary id recover the gathered id exactly."""
+    R, H, V = 6, 8, 1000
+    rng = np.random.Generator(np.random.PCG64(8))
+    t = rng.integers(0, V, R).astype(np.int32)
+    for col, code in ((0, lambda v: (v % 251) / 16.0), (1, lambda v: (v // 251) / 16.0)):
+        h = np.zeros((R, H)); h[:, col] = 1.0
+        w = np.zeros((V, H)); w[:, col] = [code(v) for v in range(V)]
+        lp, lse = orc.token_logprob(bf16_bits_of(h), bf16_bits_of(w), t, 1.0)
+        got = (lp + lse) * 16.0
+        assert np.array_equal(np.rint(got), np.array([code(v) * 16 for v in t])), "id probe"
+        close(got, np.rint(got), 1e-9, "id probe exactness")
+
+
+def pin_logprob_golden(orc):
+    """Hand-derived worked examples (tests/golden/logprob_hand.json)."""
+    with open(os.path.join(GOLDEN, "logprob_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        lp, lse = orc.token_logprob(bf16_bits_of(np.array(case["hidden"], np.float64)),
+                                    bf16_bits_of(np.array(case["w_lm"], np.float64)),
+                                    np.array(case["target"], np.int32), case["inv_temperature"])
+        close(lp, np.array(case["logprob"], dtype=np.float64), 1e-15, case["name"] + " logprob")
+        close(lse, np.array(case["lse"]), 1e-15, case["name"] + " lse")
+
+
+ATTENTION_PINS = [pin_attention_vs_torch, pin_prefix_sharing, pin_attention_closed_forms,
+                  pin_permutation, pin_one_hot_probe, pin_length_probe, pin_attention_golden]
+LOGPROB_PINS = [pin_logprob_vs_torch, pin_logprob_sum_to_one, pin_logprob_closed_forms,
+                pin_logprob_shift, pin_logprob_chunks, pin_logprob_id_probe, pin_logprob_golden]
+ALL_PINS = ATTENTION_PINS + LOGPROB_PINS
