@@ -1,0 +1,231 @@
+#!/usr/bin/env python3
+"""Throughput of the rollout hot path on one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic input that is
+already resident in HBM: prefix-shared decode attention for all candidates of
+the batch, then the fused lm-head token log-prob of their rows.  The default
+workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
+/ 8 kv heads, head dim 128, shared prefix 1024, suffix lengths uniform in
+[256, 2048]; lm-head 512 rows x hidden 4096 x vocab 151936).
+
+Prints ONE JSON line.  `value` is decode attention's effective KV bandwidth
+(algorithmic bytes, the prefix counted once per prompt, over the measured
+decode time); the lm-head's TFLOP/s are reported beside it.  Per-operation
+durations come from HIP events recorded on the stream the kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 MFMA (256 CUs x 4096 flop/clk x 2.4 GHz)
+
+WORKLOADS = {
+    # name: (decode config or None, logprob config or None, description)
+    "8b": ("8b", "8b", "8B-class decode step: 64 prompts x G=8, 32/8 heads, D=128, prefix 1024, "
+                       "suffix U[256,2048]; lm-head 512 x 4096 x 151936"),
+    "32b": ("32b", "32b", "32B-class decode step: 16 prompts x G=16, 64/8 heads, D=128, prefix 2048, "
+                          "suffix U[512,8192]; lm-head 256 x 5120 x 151936"),
+    "longctx": ("longctx", None, "multi-turn long context: 4 prompts x G=8, 64/8 heads, D=128, "
+                                 "prefix 24576, suffix geometric mean 1024 cap 4096"),
+    "policy": (None, "policy", "policy-update log-prob pass: 262144 rows x 5120 x 151936"),
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def decode_bytes(x) -> int:
+    """Algorithmic HBM bytes of one decode-attention call: K and V of every
+    prefix token once per prompt and of every suffix token once, q read, out
+    written (bf16), lse written (fp32)."""
+    c = x.cfg
+    S = c.num_seqs
+    kv = 2 * 2 * c.head_dim * c.num_kv_heads * (int(x.prefix_len.sum()) + int(x.suffix_len.sum()))
+    return kv + 2 * (2 * S * c.num_q_heads * c.head_dim) + 4 * S * c.num_q_heads
+
+
+def lmhead_flops(cfg) -> int:
+    return 2 * cfg.rows * cfg.hidden * cfg.vocab
+
+
+def cpu_baseline_decode(x, budget_s: float):
+    """The fp64 oracle on the host, on the first n prompts (all their candidates)."""
+    import oracle
+    import workloads as W
+    c = x.cfg
+    G = c.group_size
+    q = x.q.cpu()
+    kp, vp, ks, vs = x.k_prefix.cpu(), x.v_prefix.cpu(), x.k_suffix.cpu(), x.v_suffix.cpu()
+    total_bytes, total_s, n = 0, 0.0, 0
+    while n < c.num_prompts and total_s < budget_s:
+        p = n
+        a, lp = int(x.prefix_start[p]), int(x.prefix_len[p])
+        sl = slice(p * G, (p + 1) * G)
+        ls = x.suffix_len[sl]
+        b0 = int(x.suffix_start[p * G])
+        rows_s = int(ls.sum())
+        args = (W.bf16_bits(q[sl]), W.bf16_bits(kp[a:a + lp]), W.bf16_bits(vp[a:a + lp]),
+                W.bf16_bits(ks[b0:b0 + rows_s]), W.bf16_bits(vs[b0:b0 + rows_s]),
+                np.array([0]), np.array([lp]), x.suffix_start[sl] - b0, ls, G, x.scale)
+        t0 = time.perf_counter()
+        oracle.decode_attn(*args)
+        total_s += time.perf_counter() - t0
+        total_bytes += (2 * 2 * c.head_dim * c.num_kv_heads * (lp + rows_s)
+                        + 2 * 2 * G * c.num_q_heads * c.head_dim + 4 * G * c.num_q_heads)
+        n += 1
+    return {"value": total_bytes / total_s / 1e9, "unit": "GB/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(total_s, 3),
+            "sample": f"decode attention of the first {n} of {c.num_prompts} prompts "
+                      f"({n * G} candidates), fp64 CPU oracle, {total_bytes / 1e9:.3f} GB of KV"}
+
+
+def cpu_baseline_logprob(y, budget_s: float):
+    import oracle
+    import workloads as W
+    c = y.cfg
+    w = W.bf16_bits(y.w_lm)
+    total_s, n = 0.0, 0
+    rows_per = 2
+    while n < c.rows and total_s < budget_s:
+        idx = slice(n, min(c.rows, n + rows_per))
+        t0 = time.perf_counter()
+        oracle.token_logprob(W.bf16_bits(y.hidden[idx]), w, y.target[idx].cpu().numpy(), y.inv_temperature)
+        total_s += time.perf_counter() - t0
+        n = idx.stop
+    flops = 2 * n * c.hidden * c.vocab
+    return {"value": flops / total_s / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(total_s, 3),
+            "sample": f"token log-prob of the first {n} of {c.rows} rows, fp64 CPU oracle"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle time for the CPU baseline (0 to skip)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the hot path on a single MI355X "
+              "and has no multi-GPU path (see DESIGN.md for how it would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2607_20908_amd as rk
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dname, lname, desc = WORKLOADS[args.workload]
+    x = W.make_decode_inputs(W.DECODE_CONFIGS[dname], dev) if dname else None
+    y = W.make_logprob_inputs(W.LOGPROB_CONFIGS[lname], dev) if lname else None
+
+    ops = []
+    if x is not None:
+        c = x.cfg
+        out = torch.empty((c.num_seqs, c.num_q_heads, c.head_dim), dtype=torch.bfloat16, device=dev)
+        lse = torch.empty((c.num_seqs, c.num_q_heads), dtype=torch.float32, device=dev)
+        need = rk.decode_attn_workspace_size(c.num_prompts, c.group_size, c.num_q_heads, c.num_kv_heads,
+                                             c.head_dim, x.prefix_start, x.prefix_len, x.suffix_start,
+                                             x.suffix_len, x.k_prefix.shape[0], x.k_suffix.shape[0],
+                                             x.scale)
+        ws_d = torch.empty(need, dtype=torch.uint8, device=dev)
+
+        def run_decode():
+            rk.decode_attn(x.q, x.k_prefix, x.v_prefix, x.k_suffix, x.v_suffix, x.prefix_start,
+                           x.prefix_len, x.suffix_start, x.suffix_len, c.group_size, scale=x.scale,
+                           out=out, lse=lse, workspace=ws_d, return_lse=True)
+        ops.append(("decode", run_decode))
+    if y is not None:
+        cl = y.cfg
+        lp = torch.empty(cl.rows, dtype=torch.float32, device=dev)
+        lse2 = torch.empty(cl.rows, dtype=torch.float32, device=dev)
+        ws_l = torch.empty(rk.token_logprob_workspace_size(cl.rows, cl.hidden, cl.vocab),
+                           dtype=torch.uint8, device=dev)
+
+        def run_logprob():
+            rk.token_logprob(y.hidden, y.w_lm, y.target, y.inv_temperature, logprob=lp, lse=lse2,
+                             workspace=ws_l)
+        ops.append(("lmhead", run_logprob))
+
+    stream = torch.cuda.current_stream()
+    log(f"bench: workload {args.workload}: warmup {args.warmup}")
+    for _ in range(args.warmup):
+        for _, f in ops:
+            f()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
+          for _ in range(args.steps)]
+    log(f"bench: timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        for j, (_, f) in enumerate(ops):
+            ev[k][j][0].record(stream)
+            f()
+            ev[k][j][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    op_ms = {name: float(np.mean([ev[k][j][0].elapsed_time(ev[k][j][1]) for k in range(args.steps)]))
+             for j, (name, _) in enumerate(ops)}
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"bench: {ms_per_step:.3f} ms/step; per op {op_ms}")
+
+    res = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, HBM-resident)",
+           "config": {"workload": desc}}
+    rooflines = []
+    if x is not None:
+        nbytes = decode_bytes(x)
+        gbs = nbytes / (op_ms["decode"] * 1e-3) / 1e9
+        res.update({"metric": "decode-attn effective KV GB/s (% HBM peak)", "value": round(gbs, 1),
+                    "unit": "GB/s", "decode_ms": round(op_ms["decode"], 4),
+                    "decode_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                    "decode_algorithmic_bytes": nbytes})
+        rooflines.append((op_ms["decode"], {"kernel": "decode attention (split + combine)", "bound": "hbm",
+                                            "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}))
+    if y is not None:
+        fl = lmhead_flops(y.cfg)
+        tf = fl / (op_ms["lmhead"] * 1e-3) / 1e12
+        res.update({"lmhead_ms": round(op_ms["lmhead"], 4), "lmhead_tflops": round(tf, 1),
+                    "lmhead_mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "lmhead_flops": fl})
+        if x is None:
+            res.update({"metric": "lm-head logprob TFLOP/s (% MFMA)", "value": round(tf, 1),
+                        "unit": "TFLOP/s"})
+        rooflines.append((op_ms["lmhead"], {"kernel": "lm-head log-prob (tile + combine)", "bound": "mfma",
+                                            "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                                            "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                                            "traffic": None}))
+    res["metric"] = "decode-attn effective KV GB/s (% HBM peak); lm-head logprob TFLOP/s (% MFMA)" \
+        if (x is not None and y is not None) else res["metric"]
+    res["roofline"] = max(rooflines, key=lambda t: t[0])[1]
+    if args.cpu_budget > 0:
+        log("bench: cpu baseline (fp64 oracle)")
+        res["cpu_baseline"] = (cpu_baseline_decode(x, args.cpu_budget) if x is not None
+                               else cpu_baseline_logprob(y, args.cpu_budget))
+    order = ["metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+             "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"]
+    line = {k: res[k] for k in order if k in res}
+    line.update({k: v for k, v in res.items() if k not in line})
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,193 @@
+/*
+ * rl_kernels.h - C ABI of librlkern.so, the MI355X (gfx950) rollout hot path.
+ *
+ * Two operations, both asynchronous on a caller-supplied HIP stream:
+ *
+ *  rl_decode_attn     one grouped-query decode step for a batch of prompts,
+ *                     each with a group of G sampled candidates (Sec. 2.2.1,
+ *                     Problem Setup: every input x gets g candidates).  The
+ *                     candidates of a prompt share its prefix KV (the prompt,
+ *                     including the refinement-turn feedback and summary of
+ *                     Sec. 3, Structured Feedback and Iterative Refinement) and
+ *                     each has its own suffix KV (its generated tokens, at most
+ *                     1536 per turn in Sec. 3, Multi-turn RL Training).
+ *
+ *  rl_token_logprob   log pi(o_t | q, o_<t) of each sampled token under the
+ *                     policy, the factor of the GRPO ratio (Sec. 3, Eq.
+ *                     grpo-loss), computed from the last hidden state and the
+ *                     lm-head weight over the full vocabulary without storing
+ *                     the logits; masked positions (Sec. 3, Multi-turn RL
+ *                     Training: masked log-probabilities) give 0.
+ *
+ * Plain C: no HIP or torch types.  `stream` is a hipStream_t passed as void*
+ * (NULL = the default stream).  "device" pointers must be device memory of the
+ * current HIP device; "host" pointers are read only during the call.
+ *
+ * Ownership: the caller owns every buffer, including the workspace.  The
+ * library allocates no device memory and keeps no state across calls except a
+ * thread-local error string.  Calls on different streams need distinct
+ * workspaces.
+ *
+ * Errors: a call that returns anything other than RL_OK has enqueued nothing
+ * and written no output; rl_last_error() then describes the problem.  Argument
+ * errors are detected on the host before any launch.  RL_OK means the work is
+ * enqueued: outputs are valid after the stream is synchronised, and inputs,
+ * outputs and workspace must stay alive until then.
+ */
+#ifndef RL_KERNELS_H
+#define RL_KERNELS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RL_ABI_VERSION 1
+
+typedef enum {
+    RL_OK = 0,
+    RL_ERR_NULL_POINTER = 1,   /* a required pointer is NULL */
+    RL_ERR_INVALID_SHAPE = 2,  /* sizes, lengths or ranges are inconsistent */
+    RL_ERR_UNSUPPORTED = 3,    /* valid, but outside what the kernels implement */
+    RL_ERR_MISALIGNED = 4,     /* a device pointer is not 16-byte aligned */
+    RL_ERR_WORKSPACE = 5,      /* workspace NULL or smaller than required */
+    RL_ERR_HIP = 6             /* the HIP runtime reported an error */
+} rl_status;
+
+/* ------------------------------------------------------------------------ */
+/* Decode attention                                                          */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t num_prompts;   /* P >= 0: prompts (inputs x) in the batch                     */
+    int32_t group_size;    /* G >= 1: candidates per prompt; sequence s = p*G + g          */
+    int32_t num_q_heads;   /* Hq >= 1                                                      */
+    int32_t num_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0; query head h reads kv head
+                              h / (Hq/Hkv) (consecutive query heads share a kv head)       */
+    int32_t head_dim;      /* D: 64 or 128                                                 */
+    float   softmax_scale; /* finite, > 0; scores are softmax_scale * <q, k>               */
+    int32_t split_tokens;  /* 0 = automatic; else the largest number of KV tokens one
+                              split-K work item covers (a multiple of 16, >= 16).  Results
+                              agree across splits to rounding, and are bitwise
+                              reproducible for a fixed split.                              */
+} rl_decode_shape;
+
+typedef struct {
+    const int64_t *prefix_start; /* host [P]:   first KV row of prompt p's prefix           */
+    const int32_t *prefix_len;   /* host [P]:   Lp[p] >= 0 tokens                           */
+    const int64_t *suffix_start; /* host [P*G]: first KV row of candidate s's suffix        */
+    const int32_t *suffix_len;   /* host [P*G]: Ls[s] >= 0 tokens                           */
+    int64_t prefix_rows;         /* rows allocated in k_prefix/v_prefix (range checks)      */
+    int64_t suffix_rows;         /* rows allocated in k_suffix/v_suffix                     */
+} rl_decode_lens;
+
+typedef struct {
+    const void *q;        /* device bf16 [P*G, Hq, D], contiguous                          */
+    const void *k_prefix; /* device bf16 [prefix_rows, Hkv, D]                             */
+    const void *v_prefix; /* device bf16 [prefix_rows, Hkv, D]                             */
+    const void *k_suffix; /* device bf16 [suffix_rows, Hkv, D]                             */
+    const void *v_suffix; /* device bf16 [suffix_rows, Hkv, D]                             */
+    void  *out;           /* device bf16 [P*G, Hq, D]: softmax-weighted sum of values,
+                             rounded to nearest even; 0 for an empty context               */
+    float *lse;           /* device fp32 [P*G, Hq] natural-log log-sum-exp of the scaled
+                             scores (-inf for an empty context), or NULL                   */
+} rl_decode_ptrs;
+
+/*
+ * Attention of candidate s = p*G + g, query head h, over the concatenated
+ * context: prefix rows [prefix_start[p], +Lp[p]) followed by suffix rows
+ * [suffix_start[s], +Ls[s]), both at kv head h / (Hq/Hkv).  The caller appends
+ * the current token's K/V to the suffix before the call; there is no causal
+ * mask inside one decode step.  The prefix KV of a prompt is read from HBM once
+ * for all G candidates when G*Hq/Hkv <= 128 (query rows per kv head), and once
+ * per block of 128 such rows beyond that.
+ *
+ * Rows outside the given ranges are never read.  P*G == 0 is a valid no-op.
+ * Status: NULL pointer -> RL_ERR_NULL_POINTER; negative sizes or lengths,
+ * Hq % Hkv != 0, a range past prefix_rows/suffix_rows, a non-finite or
+ * non-positive scale, a bad split_tokens -> RL_ERR_INVALID_SHAPE;
+ * D not in {64, 128} -> RL_ERR_UNSUPPORTED; a device pointer not 16-byte
+ * aligned -> RL_ERR_MISALIGNED; workspace NULL or short -> RL_ERR_WORKSPACE.
+ */
+rl_status rl_decode_attn_workspace_size(const rl_decode_shape *shape,
+                                        const rl_decode_lens *lens,
+                                        size_t *bytes);
+
+rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                         const rl_decode_ptrs *ptrs,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Token log-prob through the lm-head                                        */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For each row r:  z_v = inv_temperature * <hidden[r, :], w_lm[v, :]>  (v < V),
+ *                  lse[r] = ln sum_v exp(z_v),
+ *                  logprob[r] = z_t - lse[r]  for t = target[r] in [0, V),
+ *                             = 0             for t == -1 (masked position),
+ *                             = NaN           for any other t (lse is still computed).
+ * The [rows, V] logits are never written to memory.
+ *
+ *   hidden_states  device bf16 [rows, hidden], contiguous
+ *   w_lm           device bf16 [vocab, hidden], contiguous (row v gives logit v)
+ *   target         device int32 [rows]
+ *   inv_temperature finite, > 0 (1.0 for the plain policy)
+ *   logprob        device fp32 [rows]
+ *   lse            device fp32 [rows], or NULL
+ *
+ * rows == 0 is a valid no-op.  Status: NULL pointer -> RL_ERR_NULL_POINTER;
+ * rows < 0, hidden <= 0, vocab <= 0 or a bad temperature -> RL_ERR_INVALID_SHAPE;
+ * hidden % 64 != 0 -> RL_ERR_UNSUPPORTED; a device pointer not 16-byte
+ * aligned (target, logprob and lse: 4-byte) -> RL_ERR_MISALIGNED; workspace
+ * NULL or short -> RL_ERR_WORKSPACE.
+ */
+rl_status rl_token_logprob_workspace_size(int64_t rows, int32_t hidden, int32_t vocab,
+                                          size_t *bytes);
+
+rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab,
+                           const void *hidden_states, const void *w_lm,
+                           const int32_t *target, float inv_temperature,
+                           float *logprob, float *lse,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Diagnostics                                                               */
+/* ------------------------------------------------------------------------ */
+
+const char *rl_status_string(rl_status status); /* static text, never NULL          */
+const char *rl_last_error(void);                /* thread-local detail of the last
+                                                   failing call on this thread, ""
+                                                   if none; valid until the next call */
+int rl_abi_version(void);                       /* RL_ABI_VERSION                     */
+
+/*
+ * Host-only view of the split-K work list rl_decode_attn would launch for
+ * these arguments (no device access; for tests and tuning).  Each item covers
+ * tokens [tok_begin, tok_begin + tok_count) of one unit: the prefix of prompt
+ * `unit` (kind 0) or the suffix of candidate `unit` (kind 1), at one kv head.
+ * Writes at most `capacity` items and sets *num_items to the full count.
+ */
+typedef struct {
+    int32_t kind;        /* 0 = prefix of prompt `unit`, 1 = suffix of candidate `unit` */
+    int32_t unit;
+    int32_t kv_head;
+    int32_t chunk;       /* index of this chunk within its (unit, kv_head)              */
+    int64_t tok_begin;   /* first token of the chunk, relative to the unit's start      */
+    int32_t tok_count;   /* >= 1                                                        */
+    int32_t row_begin;   /* first query row served, of the unit's G*Hq/Hkv (prefix) or
+                            Hq/Hkv (suffix) rows at this kv head                         */
+    int32_t row_count;   /* query rows served: at most 128                               */
+    int32_t reserved;
+} rl_plan_item;
+
+rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                               rl_plan_item *items, int64_t capacity, int64_t *num_items);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RL_KERNELS_H */

@@ -1,0 +1,293 @@
+"""Python binding of librlkern.so, the MI355X rollout hot path.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels behind the C ABI (include/rl_kernels.h).  PyTorch provides device
+memory and the current stream.  There is no fallback: if the library is not
+built, importing this package raises.
+
+    decode_attn(...)    prefix-shared grouped-query decode attention for a
+                        batch of prompts with G candidates each (Sec. 2.2.1,
+                        Problem Setup)
+    token_logprob(...)  log-prob of each sampled token over the full
+                        vocabulary, through the lm-head, without storing the
+                        logits (the GRPO ratio's factor, Sec. 3, Eq. grpo-loss)
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import numpy as np
+import torch  # imported first so its HIP runtime is the one the library binds to
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librlkern.so")
+
+RL_OK = 0
+STATUS_NAMES = {0: "RL_OK", 1: "RL_ERR_NULL_POINTER", 2: "RL_ERR_INVALID_SHAPE",
+                3: "RL_ERR_UNSUPPORTED", 4: "RL_ERR_MISALIGNED", 5: "RL_ERR_WORKSPACE",
+                6: "RL_ERR_HIP"}
+
+
+class RLError(RuntimeError):
+    """A non-OK status from librlkern; ``status`` is the rl_status value."""
+
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {detail}")
+
+
+class DecodeShape(ctypes.Structure):
+    _fields_ = [("num_prompts", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("split_tokens", ctypes.c_int32)]
+
+
+class DecodeLens(ctypes.Structure):
+    _fields_ = [("prefix_start", ctypes.c_void_p), ("prefix_len", ctypes.c_void_p),
+                ("suffix_start", ctypes.c_void_p), ("suffix_len", ctypes.c_void_p),
+                ("prefix_rows", ctypes.c_int64), ("suffix_rows", ctypes.c_int64)]
+
+
+class DecodePtrs(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k_prefix", ctypes.c_void_p),
+                ("v_prefix", ctypes.c_void_p), ("k_suffix", ctypes.c_void_p),
+                ("v_suffix", ctypes.c_void_p), ("out", ctypes.c_void_p), ("lse", ctypes.c_void_p)]
+
+
+class PlanItem(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("unit", ctypes.c_int32), ("kv_head", ctypes.c_int32),
+                ("chunk", ctypes.c_int32), ("tok_begin", ctypes.c_int64),
+                ("tok_count", ctypes.c_int32), ("row_begin", ctypes.c_int32),
+                ("row_count", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_workspace_size",
+           "rl_token_logprob", "rl_status_string", "rl_last_error", "rl_abi_version",
+           "rl_decode_plan_debug"]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() or "
+                          "python paper_2607_20908_amd/build.py")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.rl_abi_version.restype = ctypes.c_int
+    lib.rl_status_string.restype = ctypes.c_char_p
+    lib.rl_status_string.argtypes = [ctypes.c_int]
+    lib.rl_last_error.restype = ctypes.c_char_p
+    lib.rl_decode_attn_workspace_size.restype = ctypes.c_int
+    lib.rl_decode_attn_workspace_size.argtypes = [P, P, ctypes.POINTER(SZ)]
+    lib.rl_decode_attn.restype = ctypes.c_int
+    lib.rl_decode_attn.argtypes = [P, P, P, P, SZ, P]
+    lib.rl_token_logprob_workspace_size.restype = ctypes.c_int
+    lib.rl_token_logprob_workspace_size.argtypes = [I64, I32, I32, ctypes.POINTER(SZ)]
+    lib.rl_token_logprob.restype = ctypes.c_int
+    lib.rl_token_logprob.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, SZ, P]
+    lib.rl_decode_plan_debug.restype = ctypes.c_int
+    lib.rl_decode_plan_debug.argtypes = [P, P, P, I64, ctypes.POINTER(I64)]
+    if lib.rl_abi_version() != 1:
+        raise ImportError("librlkern ABI version mismatch")
+    return lib
+
+
+_lib = _load()
+
+
+def lib() -> ctypes.CDLL:
+    return _lib
+
+
+def hip_runtimes_mapped() -> list[str]:
+    """Paths of every libamdhip64 mapped into this process (should be exactly one)."""
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) >= 6 and "libamdhip64" in parts[5]:
+                paths.add(os.path.realpath(parts[5]))
+    return sorted(paths)
+
+
+def _check(st: int, where: str):
+    if st != RL_OK:
+        raise RLError(st, where, _lib.rl_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        if torch.cuda.is_available():
+            return torch.cuda.current_stream().cuda_stream
+        return None
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _on_device(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor (the kernels read it on the GPU)")
+    return t
+
+
+def _bf16_dev(t: torch.Tensor, name: str) -> torch.Tensor:
+    _on_device(t, name)
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be bfloat16, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+class _DecodeArgs:
+    """Host-side ctypes structures for one decode call (kept alive by the caller)."""
+
+    def __init__(self, P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
+                 suffix_start, suffix_len, prefix_rows, suffix_rows):
+        self.ps = np.ascontiguousarray(prefix_start, dtype=np.int64)
+        self.pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
+        self.ss = np.ascontiguousarray(suffix_start, dtype=np.int64)
+        self.sl = np.ascontiguousarray(suffix_len, dtype=np.int32)
+        if self.ps.shape != (P,) or self.pl.shape != (P,) or self.ss.shape != (P * G,) \
+                or self.sl.shape != (P * G,):
+            raise ValueError("length arrays must be [P] (prefix) and [P*G] (suffix)")
+        self.shape = DecodeShape(P, G, Hq, Hkv, D, float(np.float32(scale)), int(split_tokens))
+        self.lens = DecodeLens(self.ps.ctypes.data, self.pl.ctypes.data, self.ss.ctypes.data,
+                               self.sl.ctypes.data, int(prefix_rows), int(suffix_rows))
+
+
+def decode_attn_workspace_size(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start,
+                               suffix_len, prefix_rows, suffix_rows, scale=None,
+                               split_tokens: int = 0) -> int:
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    a = _DecodeArgs(P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
+                    suffix_start, suffix_len, prefix_rows, suffix_rows)
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_decode_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens),
+                                              ctypes.byref(n)), "rl_decode_attn_workspace_size")
+    return n.value
+
+
+def decode_plan(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix_len,
+                prefix_rows, suffix_rows, scale=None, split_tokens: int = 0) -> np.ndarray:
+    """The split-K work list (host-only), as a numpy structured array in launch order."""
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    a = _DecodeArgs(P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
+                    suffix_start, suffix_len, prefix_rows, suffix_rows)
+    n = ctypes.c_int64(0)
+    _check(_lib.rl_decode_plan_debug(ctypes.byref(a.shape), ctypes.byref(a.lens), None, 0,
+                                     ctypes.byref(n)), "rl_decode_plan_debug")
+    buf = (PlanItem * max(1, n.value))()
+    _check(_lib.rl_decode_plan_debug(ctypes.byref(a.shape), ctypes.byref(a.lens), buf, n.value,
+                                     ctypes.byref(n)), "rl_decode_plan_debug")
+    dt = np.dtype([("kind", np.int32), ("unit", np.int32), ("kv_head", np.int32),
+                   ("chunk", np.int32), ("tok_begin", np.int64), ("tok_count", np.int32),
+                   ("row_begin", np.int32), ("row_count", np.int32), ("reserved", np.int32)])
+    return np.frombuffer(bytes(buf), dtype=dt, count=n.value).copy()
+
+
+def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
+                k_suffix: torch.Tensor, v_suffix: torch.Tensor,
+                prefix_start, prefix_len, suffix_start, suffix_len, group_size: int,
+                scale: Optional[float] = None, split_tokens: int = 0, return_lse: bool = False,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, stream=None):
+    """Decode attention of P*G candidates over their prompt's prefix KV ++ own suffix KV.
+
+    q [P*G, Hq, D] bf16; k/v_prefix [rows_p, Hkv, D] bf16; k/v_suffix [rows_s, Hkv, D]
+    bf16 (device); prefix_start/len [P], suffix_start/len [P*G] host integers.
+    Returns out [P*G, Hq, D] bf16 (and lse [P*G, Hq] fp32 natural log).
+    """
+    for t, n in ((q, "q"), (k_prefix, "k_prefix"), (v_prefix, "v_prefix"),
+                 (k_suffix, "k_suffix"), (v_suffix, "v_suffix")):
+        _bf16_dev(t, n)
+    S, Hq, D = q.shape
+    G = int(group_size)
+    if G <= 0 or S % G:
+        raise ValueError("q.shape[0] must be a positive multiple of group_size")
+    P = S // G
+    Hkv = k_prefix.shape[1]
+    for t in (k_prefix, v_prefix, k_suffix, v_suffix):
+        if t.dim() != 3 or t.shape[1] != Hkv or t.shape[2] != D:
+            raise ValueError("KV tensors must be [rows, Hkv, D]")
+    if k_prefix.shape != v_prefix.shape or k_suffix.shape != v_suffix.shape:
+        raise ValueError("K and V shapes differ")
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    a = _DecodeArgs(P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
+                    suffix_start, suffix_len, k_prefix.shape[0], k_suffix.shape[0])
+    if out is None:
+        out = torch.empty((S, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if return_lse and lse is None:
+        lse = torch.empty((S, Hq), dtype=torch.float32, device=q.device)
+    _bf16_dev(out, "out")
+    if out.shape != (S, Hq, D):
+        raise ValueError("out must be [P*G, Hq, D]")
+    if lse is not None:
+        _on_device(lse, "lse")
+        if lse.dtype != torch.float32 or lse.shape != (S, Hq) or not lse.is_contiguous():
+            raise ValueError("lse must be a contiguous fp32 [P*G, Hq] tensor")
+    need = ctypes.c_size_t(0)
+    _check(_lib.rl_decode_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens),
+                                              ctypes.byref(need)), "rl_decode_attn_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(max(need.value, 1), dtype=torch.uint8, device=q.device)
+    _on_device(workspace, "workspace")
+    ptrs = DecodePtrs(q.data_ptr(), k_prefix.data_ptr() if k_prefix.numel() else None,
+                      v_prefix.data_ptr() if v_prefix.numel() else None,
+                      k_suffix.data_ptr() if k_suffix.numel() else None,
+                      v_suffix.data_ptr() if v_suffix.numel() else None,
+                      out.data_ptr(), lse.data_ptr() if lse is not None else None)
+    _check(_lib.rl_decode_attn(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(ptrs),
+                               ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                               _stream_handle(stream)), "rl_decode_attn")
+    return (out, lse) if return_lse else out
+
+
+def token_logprob_workspace_size(rows: int, hidden: int, vocab: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_token_logprob_workspace_size(rows, hidden, vocab, ctypes.byref(n)),
+           "rl_token_logprob_workspace_size")
+    return n.value
+
+
+def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
+                  inv_temperature: float = 1.0, logprob: Optional[torch.Tensor] = None,
+                  lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                  stream=None):
+    """Log-prob of target[r] under softmax(inv_temperature * hidden[r] @ w_lm^T).
+
+    hidden [R, H] bf16, w_lm [V, H] bf16, target [R] int32 (device; -1 = masked).
+    Returns (logprob [R] fp32, lse [R] fp32).
+    """
+    _bf16_dev(hidden, "hidden")
+    _bf16_dev(w_lm, "w_lm")
+    _on_device(target, "target")
+    if target.dtype != torch.int32 or not target.is_contiguous():
+        raise TypeError("target must be a contiguous int32 tensor")
+    R, H = hidden.shape
+    V, H2 = w_lm.shape
+    if H2 != H or target.shape != (R,):
+        raise ValueError("shapes: hidden [R, H], w_lm [V, H], target [R]")
+    if logprob is None:
+        logprob = torch.empty(R, dtype=torch.float32, device=hidden.device)
+    if lse is None:
+        lse = torch.empty(R, dtype=torch.float32, device=hidden.device)
+    for t, n in ((logprob, "logprob"), (lse, "lse")):
+        _on_device(t, n)
+        if t.dtype != torch.float32 or t.shape != (R,) or not t.is_contiguous():
+            raise ValueError(f"{n} must be a contiguous fp32 [R] tensor")
+    need = token_logprob_workspace_size(R, H, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    _on_device(workspace, "workspace")
+    _check(_lib.rl_token_logprob(R, H, V, _ptr(hidden), _ptr(w_lm), _ptr(target),
+                                 float(inv_temperature), _ptr(logprob), _ptr(lse),
+                                 ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                 _stream_handle(stream)), "rl_token_logprob")
+    return logprob, lse

@@ -1,0 +1,370 @@
+// Prefix-shared split-K decode attention for gfx950.
+//
+// One workgroup (4 wave64s) runs one work item: a chunk of KV tokens of one
+// unit at one kv head, serving `rows` query rows:
+//   prefix item: the prompt's KV, for all G*r query rows of its candidates
+//                (r = Hq/Hkv), so the chunk crosses HBM once per group;
+//   suffix item: one candidate's own KV, for its r query rows.
+// The KV chunk streams through LDS in tiles of 64 tokens (coalesced 16-byte
+// loads, double-buffered, register prefetch of the next tile).  Per 16-token
+// sub-tile a wave computes scores S^T = K Q^T on MFMA 16x16x32 (tokens on the
+// M side, query rows on the N side), keeps an online softmax per query row in
+// fp32, rounds the probabilities to bf16 and accumulates O^T = V^T P^T on
+// MFMA 16x16x16, whose B operand is exactly the score tile's C layout.
+// Each item leaves, per query row, a partial (max m, sum l, weighted value
+// sum acc[D]) in log2 units; the combine kernel merges the partials of each
+// (sequence, head) by log-sum-exp and writes the bf16 output and fp32 lse.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace rlk {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kSub = 16;                          // tokens per MFMA sub-tile
+constexpr int kSubPerTile = kTileTokens / kSub;   // 4
+
+template <int D>
+struct DCfg {
+    static constexpr int CH = D / 8;             // 16-byte chunks per token row
+    static constexpr int KK = D / 32;            // k-steps of S^T = K Q^T
+    static constexpr int DT = D / 16;            // 16-wide d tiles of O^T
+    static constexpr int LDR = D + 8;            // LDS row pitch in bf16 (16-byte pad)
+    static constexpr int TILE = kTileTokens * LDR; // bf16 elements of one K or V tile
+    static constexpr int LD = kTileTokens * CH / kThreads;  // 16-byte chunks per thread per tensor
+    static constexpr int RED_STRIDE = D + 1;     // fp32 row stride of the merge area (bank spread)
+    static constexpr int KV_BYTES = 2 * 2 * TILE * 2;                  // 2 buffers x (K, V)
+    static constexpr int RED_BYTES = 4 * 2 * 16 * RED_STRIDE * 4;      // waves x ct x 16 rows
+    static constexpr int MAIN_BYTES = KV_BYTES > RED_BYTES ? KV_BYTES : RED_BYTES;
+    static constexpr int ML_BYTES = 4 * 2 * 16 * 2 * 4;
+};
+
+// Element offset of 16-byte chunk c of token t inside a K or V tile.  Rows are
+// padded by 16 bytes, so the lanes that read one chunk of 16 consecutive
+// tokens (K operand) or one d of 4 tokens 4 apart (V^T operand) spread over
+// the LDS banks, and every read of a lane sits at a constant offset from one
+// base address.
+template <int D>
+__device__ __forceinline__ int kv_off(int t, int c) {
+    return t * DCfg<D>::LDR + (c << 3);
+}
+
+// MAXC: column tiles (16 query rows each) per wave; 1 serves items of up to
+// 64 query rows, 2 serves up to 128.
+template <int D, int MAXC>
+__global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a, int item0) {
+    using C = DCfg<D>;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[C::MAIN_BYTES + C::ML_BYTES];
+    uint16_t *kv = reinterpret_cast<uint16_t *>(smem);
+    float *red_acc = reinterpret_cast<float *>(smem);
+    float *red_ml = reinterpret_cast<float *>(smem + C::MAIN_BYTES);
+
+    const DevItem it = a.items[item0 + blockIdx.x];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g4 = lane >> 4, l16 = lane & 15;
+    const int kh = it.kind_kh & 0xffff;
+    const bool is_suffix = (it.kind_kh >> 16) & 1;
+    const int M = is_suffix ? a.r : a.G * a.r;
+    const int rows = min(kMaxItemRows, M - it.row_begin);
+    const int n_ct = (rows + 15) >> 4;
+    const int Wc = n_ct == 1 ? 1 : (n_ct == 2 ? 2 : 4);
+    const int Wt = 4 / Wc;
+    const int nst = kSubPerTile / Wt;            // sub-tiles per wave per tile
+    const int wc = wave % Wc, wt = wave / Wc;
+    const int n_my = (wc < n_ct ? 1 : 0) + (MAXC > 1 && wc + Wc < n_ct ? 1 : 0);
+    const int ntok = it.ntok;
+    const int64_t tok_stride = static_cast<int64_t>(a.Hkv) * D;
+    const uint16_t *kg = (is_suffix ? a.k_suffix : a.k_prefix) + (it.kv_row0 * a.Hkv + kh) * D;
+    const uint16_t *vg = (is_suffix ? a.v_suffix : a.v_prefix) + (it.kv_row0 * a.Hkv + kh) * D;
+
+    // ---- query rows of this wave as MFMA B operands (Q^T, k = d) ----------
+    bf16x8 qb[MAXC][C::KK];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        const int i = (wc + c * Wc) * 16 + l16;      // row within the item
+        const bool ok = c < n_my && i < rows;
+        int64_t qoff = 0;
+        if (ok) {
+            const int ig = it.row_begin + i;         // row within the unit
+            int s, h;
+            if (is_suffix) { s = it.unit; h = kh * a.r + ig; }
+            else           { s = it.unit * a.G + ig / a.r; h = kh * a.r + ig % a.r; }
+            qoff = (static_cast<int64_t>(s) * a.Hq + h) * D;
+        }
+#pragma unroll
+        for (int kk = 0; kk < C::KK; ++kk) {
+            if (ok) qb[c][kk] = *reinterpret_cast<const bf16x8 *>(a.q + qoff + kk * 32 + g4 * 8);
+            else    qb[c][kk] = bf16x8{};
+        }
+    }
+
+    // ---- online softmax state --------------------------------------------
+    float m_run[MAXC], l_run[MAXC];           // l_run: this lane's share of the row sum
+    f32x4 acc[MAXC][C::DT];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        m_run[c] = -INFINITY;
+        l_run[c] = 0.f;
+    }
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt) acc[c][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- tile staging -----------------------------------------------------
+    u32x4 kr[C::LD], vr[C::LD];
+    auto load_tile = [&](int tile) {
+        const int t0 = tile * kTileTokens;
+#pragma unroll
+        for (int j = 0; j < C::LD; ++j) {
+            const int idx = tid + j * kThreads;
+            const int t = idx / C::CH, ch = idx % C::CH;
+            if (t0 + t < ntok) {
+                const int64_t off = static_cast<int64_t>(t0 + t) * tok_stride + ch * 8;
+                kr[j] = *reinterpret_cast<const u32x4 *>(kg + off);
+                vr[j] = *reinterpret_cast<const u32x4 *>(vg + off);
+            } else {
+                kr[j] = u32x4{0u, 0u, 0u, 0u};   // never read rows outside the chunk
+                vr[j] = u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+    };
+    auto store_tile = [&](int buf) {
+        uint16_t *kl = kv + buf * 2 * C::TILE;
+        uint16_t *vl = kl + C::TILE;
+#pragma unroll
+        for (int j = 0; j < C::LD; ++j) {
+            const int idx = tid + j * kThreads;
+            const int t = idx / C::CH, ch = idx % C::CH;
+            *reinterpret_cast<u32x4 *>(kl + kv_off<D>(t, ch)) = kr[j];
+            *reinterpret_cast<u32x4 *>(vl + kv_off<D>(t, ch)) = vr[j];
+        }
+    };
+
+    const int ntiles = (ntok + kTileTokens - 1) / kTileTokens;
+    load_tile(0);
+    store_tile(0);
+    if (ntiles > 1) load_tile(1);
+    __syncthreads();
+
+    for (int tile = 0; tile < ntiles; ++tile) {
+        const uint16_t *kl = kv + (tile & 1) * 2 * C::TILE;
+        const uint16_t *vl = kl + C::TILE;
+        const int t0 = tile * kTileTokens;
+        if (n_my > 0) {
+            // scores of my sub-tiles, log2 units, masked past the chunk end
+            float sc[MAXC][kSubPerTile][4];
+#pragma unroll
+            for (int k = 0; k < kSubPerTile; ++k) {
+                if (k < nst) {
+                    const int st = wt + k * Wt;
+                    f32x4 s[MAXC];
+#pragma unroll
+                    for (int c = 0; c < MAXC; ++c) s[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kk = 0; kk < C::KK; ++kk) {
+                        const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(
+                            kl + kv_off<D>(st * kSub + l16, kk * 4 + g4));
+                        s[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[0][kk], s[0], 0, 0, 0);
+                        if (MAXC > 1 && n_my > 1)
+                            s[MAXC - 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[MAXC - 1][kk],
+                                                                                  s[MAXC - 1], 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const bool valid = t0 + st * kSub + g4 * 4 + i < ntok;
+#pragma unroll
+                        for (int c = 0; c < MAXC; ++c)
+                            sc[c][k][i] = valid ? s[c][i] * a.score_scale_log2 : -INFINITY;
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int c = 0; c < MAXC; ++c) sc[c][k][i] = -INFINITY;
+                }
+            }
+            // online softmax update per column tile, probabilities to bf16
+            bf16x4 pb[MAXC][kSubPerTile];
+#pragma unroll
+            for (int c = 0; c < MAXC; ++c) {
+                if (c < n_my) {
+                    float mx = -INFINITY;
+#pragma unroll
+                    for (int k = 0; k < kSubPerTile; ++k)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[c][k][i]);
+                    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+                    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+                    const float m_new = fmaxf(m_run[c], mx);
+                    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+                    const float alpha = fast_exp2(m_run[c] - m_use);
+                    m_run[c] = m_new;
+                    float psum = 0.f;
+#pragma unroll
+                    for (int k = 0; k < kSubPerTile; ++k) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float p = fast_exp2(sc[c][k][i] - m_use);
+                            psum += p;
+                            pb[c][k][i] = static_cast<__bf16>(p);
+                        }
+                    }
+                    l_run[c] = l_run[c] * alpha + psum;
+                    // the running max rarely moves after the first tiles: skip the
+                    // rescale when it stayed put for every row of the wave
+                    if (__any(alpha != 1.f)) {
+#pragma unroll
+                        for (int dt = 0; dt < C::DT; ++dt) acc[c][dt] *= alpha;
+                    }
+                }
+            }
+            // O^T += V^T P^T; the V^T operand holds 4 consecutive tokens at one d
+#pragma unroll
+            for (int k = 0; k < kSubPerTile; ++k) {
+                if (k < nst) {
+                    const int st = wt + k * Wt;
+                    const int tb = st * kSub + g4 * 4;
+#pragma unroll
+                    for (int dt = 0; dt < C::DT; ++dt) {
+                        const int d = dt * 16 + l16;
+                        bf16x4 va;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const uint16_t bits = vl[kv_off<D>(tb + j, d >> 3) + (d & 7)];
+                            va[j] = __builtin_bit_cast(__bf16, bits);
+                        }
+                        acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0][k], acc[0][dt], 0, 0, 0);
+                        if (MAXC > 1 && n_my > 1)
+                            acc[MAXC - 1][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                                va, pb[MAXC - 1][k], acc[MAXC - 1][dt], 0, 0, 0);
+                    }
+                }
+            }
+        }
+        if (tile + 1 < ntiles) {
+            store_tile((tile + 1) & 1);
+            if (tile + 2 < ntiles) load_tile(tile + 2);
+        }
+        __syncthreads();
+    }
+
+    // ---- merge the waves' partials (same rows, disjoint tokens) ------------
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        l_run[c] += __shfl_xor(l_run[c], 16, 64);
+        l_run[c] += __shfl_xor(l_run[c], 32, 64);
+    }
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        if (c < n_my) {
+            const int slot = (wave * 2 + c) * 16 + l16;
+            if (lane < 16) {
+                red_ml[slot * 2 + 0] = m_run[c];
+                red_ml[slot * 2 + 1] = l_run[c];
+            }
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    red_acc[slot * C::RED_STRIDE + dt * 16 + g4 * 4 + i] = acc[c][dt][i];
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < rows * D; e += kThreads) {
+        const int i = e / D, d = e % D;
+        const int ct = i >> 4, q = i & 15;
+        const int wcx = ct % Wc, cl = ct / Wc;
+        float Mx = -INFINITY;
+        for (int w = 0; w < Wt; ++w) Mx = fmaxf(Mx, red_ml[((wcx + w * Wc) * 2 + cl) * 32 + q * 2]);
+        float L = 0.f, A = 0.f;
+        for (int w = 0; w < Wt; ++w) {
+            const int slot = ((wcx + w * Wc) * 2 + cl) * 16 + q;
+            const float f = fast_exp2(red_ml[slot * 2] - Mx);
+            L += f * red_ml[slot * 2 + 1];
+            A += f * red_acc[slot * C::RED_STRIDE + d];
+        }
+        const int64_t prow = it.partial_row0 + i;
+        a.pacc[prow * D + d] = A;
+        if (d == 0) {
+            a.pm[prow] = Mx;
+            a.pl[prow] = L;
+        }
+    }
+}
+
+// One wave per (sequence s, query head h): merge the partials of the prompt's
+// prefix chunks and the candidate's suffix chunks.
+template <int D>
+__global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) {
+    constexpr int PER_LANE = D / 64;
+    const int lane = threadIdx.x & 63;
+    const int64_t idx = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
+    const int64_t S = static_cast<int64_t>(a.P) * a.G;
+    if (idx >= S * a.Hq) return;
+    const int64_t s = idx / a.Hq;
+    const int h = static_cast<int>(idx % a.Hq);
+    const int64_t p = s / a.G;
+    const int g = static_cast<int>(s % a.G);
+    const int kh = h / a.r, hr = h % a.r;
+    const DevUnit pu = a.prefix_units[p * a.Hkv + kh];
+    const DevUnit su = a.suffix_units[s * a.Hkv + kh];
+    const int64_t Mp = static_cast<int64_t>(a.G) * a.r;
+    const int n = pu.nchunks + su.nchunks;
+    auto prow = [&](int j) -> int64_t {
+        return j < pu.nchunks ? pu.base + j * Mp + g * a.r + hr
+                              : su.base + static_cast<int64_t>(j - pu.nchunks) * a.r + hr;
+    };
+    float Mx = -INFINITY;
+    for (int j = lane; j < n; j += 64) Mx = fmaxf(Mx, a.pm[prow(j)]);
+    Mx = wave_max(Mx);
+    float L = 0.f, o[PER_LANE];
+#pragma unroll
+    for (int e = 0; e < PER_LANE; ++e) o[e] = 0.f;
+    for (int j = 0; j < n; ++j) {
+        const int64_t pr = prow(j);
+        const float f = fast_exp2(a.pm[pr] - Mx);
+        L += f * a.pl[pr];
+#pragma unroll
+        for (int e = 0; e < PER_LANE; ++e) o[e] += f * a.pacc[pr * D + lane * PER_LANE + e];
+    }
+    uint16_t *out = a.out + idx * D + lane * PER_LANE;
+    if (n == 0) {
+#pragma unroll
+        for (int e = 0; e < PER_LANE; ++e) out[e] = 0;
+        if (a.lse && lane == 0) a.lse[idx] = -INFINITY;
+        return;
+    }
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int e = 0; e < PER_LANE; ++e) out[e] = f32_to_bf16_bits(o[e] * inv);
+    if (a.lse && lane == 0) a.lse[idx] = (Mx + fast_log2(L)) * kLn2;
+}
+
+template <int D>
+hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
+    // The two-column-tile variant serves every item; with the LDS tile sizes
+    // both variants reach the same occupancy, so one launch covers all items.
+    if (a.n_items > 0) {
+        hipLaunchKernelGGL((decode_split_kernel<D, 2>), dim3(a.n_items), dim3(kThreads), 0, stream, a, 0);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const int64_t waves = static_cast<int64_t>(a.P) * a.G * a.Hq;
+    const int64_t blocks = (waves + 3) / 4;
+    hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream) {
+    switch (a.D) {
+        case 64: return launch_decode_d<64>(a, stream);
+        case 128: return launch_decode_d<128>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace rlk

@@ -1,0 +1,41 @@
+// Launch interface between the C ABI glue (abi.cpp) and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "plan.h"
+
+namespace rlk {
+
+struct DecodeArgs {
+    const uint16_t *q;
+    const uint16_t *k_prefix, *v_prefix, *k_suffix, *v_suffix;
+    uint16_t *out;
+    float *lse;                 // may be null
+    const DevItem *items;       // workspace: split-K work list
+    const DevUnit *prefix_units, *suffix_units;
+    float *pm, *pl, *pacc;      // workspace: partial max (log2 units), sum, weighted values
+    int32_t n_items;            // work items in the list
+    int32_t P, G, Hq, Hkv, r, D;
+    float score_scale_log2;     // softmax_scale * log2(e)
+};
+
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
+
+struct LogprobArgs {
+    const uint16_t *hidden;     // [R, H]
+    const uint16_t *w;          // [V, H]
+    const int32_t *target;      // [R]
+    float *logprob, *lse;       // [R], lse may be null
+    float *pm, *pl, *zt;        // workspace: [n_vocab_tiles, R] x2, [R]
+    int64_t R;
+    int32_t H, V;
+    int32_t n_vocab_tiles, n_row_tiles;
+    float inv_temperature;
+};
+
+hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream);
+
+}  // namespace rlk

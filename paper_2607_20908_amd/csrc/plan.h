@@ -1,0 +1,93 @@
+// Host-side argument validation and split-K planning for rl_decode_attn and
+// rl_token_logprob.  Plain C++17: no HIP calls, so every check here can be
+// exercised on a machine without a GPU.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "rl_kernels.h"
+
+namespace rlk {
+
+// Largest number of query rows one decode work item serves (16 per MFMA column
+// tile, at most 2 column tiles per wave, 4 waves).
+constexpr int kMaxItemRows = 128;
+// KV tokens staged per LDS tile in the split kernel.
+constexpr int kTileTokens = 64;
+// Vocabulary entries per lm-head work tile.
+constexpr int kVocabTile = 256;
+// Token rows per lm-head work tile.
+constexpr int kRowTile = 256;
+// Hidden-dimension step of the lm-head kernel.
+constexpr int kHiddenStep = 64;
+// Compute units of an MI355X; the automatic split size is planned for them.
+constexpr int kNumCUs = 256;
+constexpr float kLog2eHost = 1.4426950408889634f;
+
+// One split-K work item as the split kernel reads it (32 bytes).
+struct DevItem {
+    int64_t kv_row0;       // absolute KV row of the chunk's first token
+    int64_t partial_row0;  // partial row of the item's first query row
+    int32_t ntok;          // tokens in the chunk (>= 1)
+    int32_t kind_kh;       // kv head | (1 << 16 if suffix)
+    int32_t unit;          // prompt p (prefix) or candidate s (suffix)
+    int32_t row_begin;     // first query row served
+};
+static_assert(sizeof(DevItem) == 32, "DevItem layout");
+
+// Where the partial results of one (unit, kv head) live: chunk c's row i is
+// partial row base + c * rows_per_chunk + i.
+struct DevUnit {
+    int64_t base;
+    int32_t nchunks;
+    int32_t pad;
+};
+static_assert(sizeof(DevUnit) == 16, "DevUnit layout");
+
+struct DecodePlan {
+    // problem
+    int32_t P = 0, G = 0, Hq = 0, Hkv = 0, D = 0, r = 0;
+    float scale = 0.f;
+    int32_t split_prefix = 0, split_suffix = 0;  // chunk sizes used
+    // work list in launch order
+    std::vector<rl_plan_item> items;
+    std::vector<DevItem> dev_items;
+    std::vector<DevUnit> prefix_units;   // [P * Hkv]
+    std::vector<DevUnit> suffix_units;   // [S * Hkv]
+    int64_t partial_rows = 0;
+    // workspace layout (byte offsets; every section 256-byte aligned)
+    size_t off_items = 0, off_prefix_units = 0, off_suffix_units = 0;
+    size_t off_m = 0, off_l = 0, off_acc = 0;
+    size_t meta_bytes = 0;   // items + unit tables (uploaded from the host)
+    size_t total_bytes = 0;
+};
+
+// Validates shape and lengths (not device pointers) and builds the plan.
+// On failure returns the status and sets *err.
+rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                      DecodePlan *plan, std::string *err);
+
+// Validates the device pointers of a decode call against a built plan.
+rl_status check_decode_ptrs(const DecodePlan &plan, const rl_decode_lens *lens,
+                            const rl_decode_ptrs *ptrs, std::string *err);
+
+struct LogprobPlan {
+    int64_t R = 0;
+    int32_t H = 0, V = 0;
+    int64_t n_vocab_tiles = 0, n_row_tiles = 0;
+    size_t off_m = 0, off_l = 0, off_zt = 0, total_bytes = 0;
+};
+
+rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan *plan,
+                       std::string *err);
+
+rl_status check_logprob_args(const LogprobPlan &plan, const void *hidden_states,
+                             const void *w_lm, const int32_t *target, float inv_temperature,
+                             const float *logprob, const float *lse, std::string *err);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace rlk

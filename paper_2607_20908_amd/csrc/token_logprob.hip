@@ -1,0 +1,214 @@
+// Fused lm-head token log-prob for gfx950.
+//
+// Tile kernel: one workgroup (4 wave64s, 2 x 2) computes the 256 x 256 logit
+// tile  Z^T = W_tile * hidden_tile^T  (vocab entries on the M side, token rows
+// on the N side) on MFMA 32x32x16 bf16 with fp32 accumulation.  Both operands
+// are hidden-contiguous, so the hidden dimension streams through LDS in steps
+// of 64 (double-buffered, XOR-swizzled 16-byte chunks, register prefetch of
+// the next step).  The epilogue never stores the logits: per token row it
+// takes the max and the sum of exp2 over the tile's vocab entries (the vocab
+// index lives in the accumulator registers, so the reduction is in-lane plus
+// one cross-half shuffle), picks out the target's logit when the target falls
+// in the tile, and writes one (max, sum) partial per (vocab tile, row).
+// Combine kernel: per row, merge the partials of all vocab tiles into the
+// log-sum-exp and subtract it from the target logit.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace rlk {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kK = kHiddenStep;                 // 64 hidden entries per LDS stage
+constexpr int kTileElems = kVocabTile * kK;     // bf16 elements per operand per stage
+static_assert(kVocabTile == kRowTile, "square tiles assumed below");
+
+// Element offset of 16-byte chunk c (0..7) of tile row `row` in a stage buffer.
+__device__ __forceinline__ int op_off(int row, int c) { return row * kK + ((c ^ (row & 7)) << 3); }
+
+// Maps the launch index to a (vocab tile, row tile).  The hardware hands
+// consecutive workgroups to the 8 XCDs in turn; renumbering gives each XCD a
+// contiguous run of logical tiles, and inside a run 4 row tiles sweep the
+// vocabulary together, so a weight tile is fetched into an XCD's L2 once for
+// 4 row tiles and the row tiles stay resident in L2 / the MALL.
+__device__ __forceinline__ void tile_of(int64_t b, int64_t nvt, int64_t nrt, int64_t *vt, int64_t *rt) {
+    const int64_t total = nvt * nrt;
+    const int64_t full = total / 8 * 8;
+    const int64_t L = b < full ? (b % 8) * (total / 8) + b / 8 : b;
+    constexpr int64_t GR = 4;
+    const int64_t group = L / (GR * nvt);
+    const int64_t in = L % (GR * nvt);
+    const int64_t rows_in_group = min(GR, nrt - group * GR);
+    *rt = group * GR + in % rows_in_group;
+    *vt = in / rows_in_group;
+}
+
+__global__ __launch_bounds__(kThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * 2 * kTileElems];   // [buf][W, hidden]
+    __shared__ float red[2][kRowTile][2];                                        // [vocab half][row][m, l]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wv = wave & 1, wr = wave >> 1;     // vocab half, row half of the tile
+    const int l32 = lane & 31, h2 = lane >> 5;
+    int64_t vt, rt;
+    tile_of(blockIdx.x, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+    const int64_t v0 = vt * kVocabTile, r0 = rt * kRowTile;
+    const int64_t H = a.H;
+    const uint16_t *wg = a.w + v0 * H;
+    const uint16_t *hg = a.hidden + r0 * H;
+
+    // ---- staging: 8 chunks of W and 8 of hidden per thread per stage --------
+    u32x4 ra[8], rb[8];
+    auto load_stage = [&](int k0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int idx = tid + j * kThreads;
+            const int row = idx >> 3, c = idx & 7;
+            ra[j] = (v0 + row < a.V) ? *reinterpret_cast<const u32x4 *>(wg + row * H + k0 + c * 8)
+                                     : u32x4{0u, 0u, 0u, 0u};
+            rb[j] = (r0 + row < a.R) ? *reinterpret_cast<const u32x4 *>(hg + row * H + k0 + c * 8)
+                                     : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
+    auto store_stage = [&](int buf) {
+        uint16_t *as = smem + buf * 2 * kTileElems;
+        uint16_t *bs = as + kTileElems;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int idx = tid + j * kThreads;
+            const int row = idx >> 3, c = idx & 7;
+            *reinterpret_cast<u32x4 *>(as + op_off(row, c)) = ra[j];
+            *reinterpret_cast<u32x4 *>(bs + op_off(row, c)) = rb[j];
+        }
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = f32x16{};
+
+    const int nk = a.H / kK;
+    load_stage(0);
+    store_stage(0);
+    if (nk > 1) load_stage(kK);
+    __syncthreads();
+    for (int ks = 0; ks < nk; ++ks) {
+        const uint16_t *as = smem + (ks & 1) * 2 * kTileElems;
+        const uint16_t *bs = as + kTileElems;
+#pragma unroll
+        for (int kq = 0; kq < kK / 16; ++kq) {
+            const int c = kq * 2 + h2;
+            bf16x8 af[4], bf[4];
+#pragma unroll
+            for (int tm = 0; tm < 4; ++tm)
+                af[tm] = *reinterpret_cast<const bf16x8 *>(as + op_off(wv * 128 + tm * 32 + l32, c));
+#pragma unroll
+            for (int tn = 0; tn < 4; ++tn)
+                bf[tn] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wr * 128 + tn * 32 + l32, c));
+#pragma unroll
+            for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+                for (int tn = 0; tn < 4; ++tn)
+                    acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bf[tn], acc[tm][tn], 0, 0, 0);
+        }
+        if (ks + 1 < nk) {
+            store_stage((ks + 1) & 1);
+            if (ks + 2 < nk) load_stage((ks + 2) * kK);
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: per token row, max / sum of exp2 / target logit ---------
+    // acc[tm][tn][i] holds vocab v0 + wv*128 + tm*32 + 8*(i/4) + 4*h2 + i%4
+    // for token row r0 + wr*128 + tn*32 + l32.
+    const float c2 = a.inv_temperature * kLog2e;
+    const int64_t vbase = v0 + wv * 128;
+#pragma unroll
+    for (int tn = 0; tn < 4; ++tn) {
+        const int64_t rr = r0 + wr * 128 + tn * 32 + l32;
+        // target logit, if the target lies in this wave's 128 vocab entries
+        if (rr < a.R) {
+            const int64_t local = static_cast<int64_t>(a.target[rr]) - vbase;
+            if (local >= 0 && local < 128) {
+                const int tmt = static_cast<int>(local >> 5), rem = static_cast<int>(local & 31);
+                const int it = ((rem >> 3) << 2) | (rem & 3);
+                if (((rem >> 2) & 1) == h2) {
+                    float val = 0.f;
+#pragma unroll
+                    for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            if (tm == tmt && i == it) val = acc[tm][tn][i];
+                    a.zt[rr] = val * a.inv_temperature;
+                }
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int64_t v = vbase + tm * 32 + 8 * (i >> 2) + 4 * h2 + (i & 3);
+                const float x = v < a.V ? acc[tm][tn][i] * c2 : -INFINITY;
+                acc[tm][tn][i] = x;
+                mx = fmaxf(mx, x);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mu = mx == -INFINITY ? 0.f : mx;
+        float sum = 0.f;
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) sum += fast_exp2(acc[tm][tn][i] - mu);
+        sum += __shfl_xor(sum, 32, 64);
+        if (h2 == 0) {
+            red[wv][wr * 128 + tn * 32 + l32][0] = mx;
+            red[wv][wr * 128 + tn * 32 + l32][1] = sum;
+        }
+    }
+    __syncthreads();
+    {
+        const int row = tid;
+        const int64_t rr = r0 + row;
+        if (rr < a.R) {
+            const float m0 = red[0][row][0], m1 = red[1][row][0];
+            const float Mx = fmaxf(m0, m1);
+            const float L = red[0][row][1] * fast_exp2(m0 - Mx) + red[1][row][1] * fast_exp2(m1 - Mx);
+            a.pm[vt * a.R + rr] = Mx;
+            a.pl[vt * a.R + rr] = L;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void logprob_combine_kernel(LogprobArgs a) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    if (r >= a.R) return;
+    float Mx = -INFINITY;
+    for (int64_t vt = 0; vt < a.n_vocab_tiles; ++vt) Mx = fmaxf(Mx, a.pm[vt * a.R + r]);
+    float L = 0.f;
+    for (int64_t vt = 0; vt < a.n_vocab_tiles; ++vt)
+        L += a.pl[vt * a.R + r] * fast_exp2(a.pm[vt * a.R + r] - Mx);
+    const float lse = (Mx + fast_log2(L)) * kLn2;
+    const int32_t t = a.target[r];
+    float lp;
+    if (t == -1) lp = 0.f;
+    else if (t >= 0 && t < a.V) lp = a.zt[r] - lse;
+    else lp = __builtin_nanf("");
+    a.logprob[r] = lp;
+    if (a.lse) a.lse[r] = lse;
+}
+
+}  // namespace
+
+hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
+    const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
+    hipLaunchKernelGGL(logprob_tile_kernel, dim3(static_cast<uint32_t>(tiles)), dim3(kThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t blocks = (a.R + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(logprob_combine_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace rlk

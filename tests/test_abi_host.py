@@ -1,0 +1,197 @@
+"""The C ABI on the host: the library loads, exports what the header declares,
+and rejects bad arguments with the documented status before touching the GPU.
+
+No compute call reaches a kernel here: every call either fails validation or
+is a valid no-op, so these run without a GPU.  Device pointers are fake,
+suitably aligned integers that the library never dereferences on these paths.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_20908_amd as rk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rl_kernels.h")
+
+OK, NULLP, SHAPE, UNSUP, MISAL, WSPACE = 0, 1, 2, 3, 4, 5
+FAKE = 0x7f0000000000          # 256-byte aligned, never dereferenced
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rl_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    names = header_functions()
+    assert set(names) == set(rk.EXPORTS), names
+    lib = ctypes.CDLL(rk.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} not exported"
+
+
+def test_one_hip_runtime_mapped():
+    assert len(rk.hip_runtimes_mapped()) == 1, rk.hip_runtimes_mapped()
+
+
+def test_status_strings_and_version():
+    lib = rk.lib()
+    assert lib.rl_abi_version() == 1
+    for code, name in rk.STATUS_NAMES.items():
+        assert lib.rl_status_string(code).decode() == name
+    assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
+
+
+# ---------------------------------------------------------------- decode
+def decode_call(P=2, G=3, Hq=4, Hkv=2, D=128, scale=0.125, split=0, lp=None, ls=None,
+                prefix_rows=None, suffix_rows=None, ptrs=None, ws=None, ws_bytes=1 << 30,
+                null_shape=False, null_lens=False, null_ptrs=False, starts=None):
+    lib = rk.lib()
+    S = P * G
+    lp = np.full(P, 5, np.int32) if lp is None else np.asarray(lp, np.int32)
+    ls = np.full(S, 3, np.int32) if ls is None else np.asarray(ls, np.int32)
+    ps = (np.arange(P, dtype=np.int64) * 5) if starts is None else np.asarray(starts[0], np.int64)
+    ss = (np.arange(S, dtype=np.int64) * 3) if starts is None else np.asarray(starts[1], np.int64)
+    shape = rk.DecodeShape(P, G, Hq, Hkv, D, scale, split)
+    lens = rk.DecodeLens(ps.ctypes.data, lp.ctypes.data, ss.ctypes.data, ls.ctypes.data,
+                         5 * P if prefix_rows is None else prefix_rows,
+                         3 * S if suffix_rows is None else suffix_rows)
+    p = dict(q=FAKE, k_prefix=FAKE + 256, v_prefix=FAKE + 512, k_suffix=FAKE + 768,
+             v_suffix=FAKE + 1024, out=FAKE + 1280, lse=FAKE + 1536)
+    p.update(ptrs or {})
+    dp = rk.DecodePtrs(p["q"], p["k_prefix"], p["v_prefix"], p["k_suffix"], p["v_suffix"],
+                       p["out"], p["lse"])
+    st = lib.rl_decode_attn(None if null_shape else ctypes.byref(shape),
+                            None if null_lens else ctypes.byref(lens),
+                            None if null_ptrs else ctypes.byref(dp), ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(null_shape=True), NULLP),
+    (dict(null_lens=True), NULLP),
+    (dict(null_ptrs=True), NULLP),
+    (dict(ptrs=dict(q=None)), NULLP),
+    (dict(ptrs=dict(out=None)), NULLP),
+    (dict(ptrs=dict(k_prefix=None)), NULLP),
+    (dict(ptrs=dict(v_suffix=None)), NULLP),
+    (dict(G=0), SHAPE),
+    (dict(P=-1, lp=[], ls=[], starts=([], [])), SHAPE),
+    (dict(Hq=6, Hkv=4), SHAPE),
+    (dict(Hkv=0), SHAPE),
+    (dict(scale=0.0), SHAPE),
+    (dict(scale=float("nan")), SHAPE),
+    (dict(scale=float("inf")), SHAPE),
+    (dict(split=8), SHAPE),
+    (dict(split=40), SHAPE),
+    (dict(split=-16), SHAPE),
+    (dict(lp=[5, -1]), SHAPE),
+    (dict(ls=[3, 3, -2, 3, 3, 3]), SHAPE),
+    (dict(prefix_rows=9), SHAPE),             # prompt 1 needs rows [5, 10)
+    (dict(suffix_rows=17), SHAPE),            # candidate 5 needs rows [15, 18)
+    (dict(prefix_rows=-1), SHAPE),
+    (dict(starts=([0, -5], [0, 3, 6, 9, 12, 15])), SHAPE),
+    (dict(D=96), UNSUP),
+    (dict(D=256), UNSUP),
+    (dict(D=0), SHAPE),
+    (dict(ptrs=dict(q=FAKE + 8)), MISAL),
+    (dict(ptrs=dict(v_prefix=FAKE + 2)), MISAL),
+    (dict(ptrs=dict(out=FAKE + 4)), MISAL),
+    (dict(ptrs=dict(lse=FAKE + 2)), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws=FAKE, ws_bytes=64), WSPACE),
+])
+def test_decode_validation(kw, expect):
+    kw.setdefault("ws", FAKE)
+    st, msg = decode_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg, "a failing call must leave an error message"
+
+
+def test_decode_empty_batch_is_noop():
+    st, msg = decode_call(P=0, ws=None)
+    assert st == OK and msg == ""
+    # nullable pointers: no prefix anywhere -> prefix pointers may be NULL, but the
+    # call then proceeds to the workspace check (no device work before it)
+    st, _ = decode_call(lp=[0, 0], ptrs=dict(k_prefix=None, v_prefix=None), ws=None)
+    assert st == WSPACE
+
+
+def test_decode_workspace_size_queries():
+    args = (2, 3, 4, 2, 128, np.array([0, 5]), np.array([5, 5]), np.arange(6) * 3,
+            np.full(6, 3), 10, 18)
+    n = rk.decode_attn_workspace_size(*args)
+    assert n > 0 and n % 256 == 0
+    assert rk.decode_attn_workspace_size(*args) == n               # deterministic
+    with pytest.raises(rk.RLError) as e:
+        rk.decode_attn_workspace_size(2, 3, 4, 2, 96, *args[5:])
+    assert e.value.status == UNSUP
+    assert rk.decode_attn_workspace_size(0, 3, 4, 2, 128, [], [], [], [], 0, 0) == 0
+
+
+# --------------------------------------------------------------- logprob
+def logprob_call(R=8, H=256, V=1000, hs=FAKE, w=FAKE + 256, t=FAKE + 512, invT=1.0,
+                 lp=FAKE + 768, lse=FAKE + 1024, ws=FAKE, ws_bytes=1 << 30):
+    lib = rk.lib()
+    st = lib.rl_token_logprob(R, H, V, hs, w, t, invT, lp, lse, ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(hs=None), NULLP),
+    (dict(w=None), NULLP),
+    (dict(t=None), NULLP),
+    (dict(lp=None), NULLP),
+    (dict(R=-1), SHAPE),
+    (dict(H=0), SHAPE),
+    (dict(V=0), SHAPE),
+    (dict(V=-5), SHAPE),
+    (dict(invT=0.0), SHAPE),
+    (dict(invT=-1.0), SHAPE),
+    (dict(invT=float("nan")), SHAPE),
+    (dict(H=100), UNSUP),
+    (dict(H=32), UNSUP),
+    (dict(hs=FAKE + 8), MISAL),
+    (dict(w=FAKE + 4), MISAL),
+    (dict(t=FAKE + 2), MISAL),
+    (dict(lp=FAKE + 1), MISAL),
+    (dict(lse=FAKE + 2), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws_bytes=16), WSPACE),
+    (dict(ws=FAKE + 4), MISAL),
+])
+def test_logprob_validation(kw, expect):
+    st, msg = logprob_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg
+
+
+def test_logprob_empty_is_noop():
+    st, msg = logprob_call(R=0, hs=None, w=None, t=None, lp=None, lse=None, ws=None, ws_bytes=0)
+    assert st == OK and msg == ""
+
+
+def test_logprob_workspace_size():
+    # per (vocab tile of 256, row): max and sum; per row: the target logit
+    R, V = 1000, 151936
+    n = rk.token_logprob_workspace_size(R, 5120, V)
+    tiles = -(-V // 256)
+    assert n >= (2 * tiles * R + R) * 4
+    assert n < (2 * tiles * R + R) * 4 + 3 * 256
+    assert rk.token_logprob_workspace_size(0, 64, 10) == 0
+    with pytest.raises(rk.RLError):
+        rk.token_logprob_workspace_size(4, 100, 10)
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    x = torch.zeros(4, 64, dtype=torch.bfloat16)
+    w = torch.zeros(8, 64, dtype=torch.bfloat16)
+    t = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(ValueError, match="device tensor"):
+        rk.token_logprob(x, w, t)

@@ -1,0 +1,136 @@
+"""Token log-prob: the HIP path against the fp64 oracle on the same bits.
+
+Bar: log-prob and lse max-abs <= 2e-3; the gathered target id bit-exact
+(id probes), masked rows exactly 0, invalid targets NaN.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_20908_amd as rk
+import workloads as W
+from gpu_util import LOGPROB_TOL, dev, max_abs, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def rand_bits(rng, shape, std=1.0):
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32) * std)
+    return W.bf16_bits(x.to(torch.bfloat16))
+
+
+def run_gpu(h_bits, w_bits, target, inv_T=1.0):
+    h, w = to_dev(h_bits), to_dev(w_bits)
+    t = torch.from_numpy(np.ascontiguousarray(target, np.int32)).to(dev())
+    lp, lse = rk.token_logprob(h, w, t, inv_T)
+    torch.cuda.synchronize()
+    return lp.cpu().numpy(), lse.cpu().numpy()
+
+
+def check(h_bits, w_bits, target, inv_T=1.0, what=""):
+    say(f"logprob parity {what}")
+    lp, lse = run_gpu(h_bits, w_bits, target, inv_T)
+    rlp, rlse = oracle.token_logprob(h_bits, w_bits, target, inv_T)
+    e1, e2 = max_abs(lp, rlp), max_abs(lse, rlse)
+    assert e1 <= LOGPROB_TOL, f"{what}: logprob max-abs {e1}"
+    assert e2 <= LOGPROB_TOL, f"{what}: lse max-abs {e2}"
+    return lp, lse
+
+
+def test_tiny_config():
+    x = W.make_logprob_inputs(W.LOGPROB_CONFIGS["tiny"], "cpu")
+    check(W.bf16_bits(x.hidden), W.bf16_bits(x.w_lm), x.target.numpy(), what="tiny config")
+
+
+@pytest.mark.parametrize("R,H,V", [(300, 128, 1000),    # ragged rows and vocab, 2x4 tiles
+                                   (1, 64, 257),        # one row, one vocab entry past a tile
+                                   (513, 192, 511),
+                                   (256, 4096, 2048)])
+def test_ragged_shapes(R, H, V):
+    rng = np.random.Generator(np.random.PCG64(R + H + V))
+    h = rand_bits(rng, (R, H))
+    w = rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    check(h, w, t, what=f"{R}x{H}x{V}")
+
+
+def test_temperature_masking_and_invalid_targets():
+    rng = np.random.Generator(np.random.PCG64(7))
+    R, H, V = 400, 256, 1500
+    h = rand_bits(rng, (R, H))
+    w = rand_bits(rng, (V, H), 0.08)
+    t = rng.integers(0, V, R).astype(np.int32)
+    t[rng.random(R) < 0.1] = -1
+    t[[3, 50, 399]] = [V, -2, 1 << 30]
+    lp, lse = check(h, w, t, 1.0 / 0.7, "temperature+mask")
+    assert (lp[t == -1] == 0).all()
+    assert np.isnan(lp[[3, 50, 399]]).all() and np.isfinite(lse).all()
+
+
+def test_probabilities_sum_to_one():
+    x = W.make_logprob_inputs(W.LOGPROB_CONFIGS["tiny"], "cpu", w_std=0.5)
+    V = x.cfg.vocab
+    h = W.bf16_bits(x.hidden)
+    hh = np.repeat(h, V, axis=0)
+    t = np.tile(np.arange(V, dtype=np.int32), x.cfg.rows)
+    say("logprob sum to one")
+    lp, _ = run_gpu(hh, W.bf16_bits(x.w_lm), t)
+    sums = np.exp(lp.astype(np.float64).reshape(x.cfg.rows, V)).sum(1)
+    assert np.abs(sums - 1).max() <= 1e-3, sums
+
+
+def test_id_probe_bit_exact():
+    """Logits that encode the vocabulary id: the gathered logit names the target exactly."""
+    R, H, V = 700, 64, 151936
+    rng = np.random.Generator(np.random.PCG64(8))
+    t = rng.integers(0, V, R).astype(np.int32)
+    t[:4] = [0, V - 1, 255, 256]
+    for col, code in ((0, lambda v: (v % 251) / 16.0), (1, lambda v: (v // 251 % 256) / 16.0)):
+        h = np.zeros((R, H), np.float32); h[:, col] = 1.0
+        w = np.zeros((V, H), np.float32); w[:, col] = code(np.arange(V))
+        bits = lambda a: W.bf16_bits(torch.from_numpy(a).to(torch.bfloat16))
+        say(f"logprob id probe col {col}")
+        lp, lse = run_gpu(bits(h), bits(w), t)
+        z = (lp.astype(np.float64) + lse.astype(np.float64)) * 16.0
+        assert np.array_equal(np.rint(z), code(t) * 16.0), "gathered the wrong id"
+        assert np.abs(z - np.rint(z)).max() < 0.05
+
+
+def test_row_permutation_bitwise():
+    rng = np.random.Generator(np.random.PCG64(9))
+    R, H, V = 600, 128, 3000
+    h = rand_bits(rng, (R, H))
+    w = rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    perm = rng.permutation(R)
+    say("logprob permutation")
+    lp1, lse1 = run_gpu(h, w, t)
+    lp2, lse2 = run_gpu(h[perm], w, t[perm])
+    assert np.array_equal(lp1[perm].view(np.uint32), lp2.view(np.uint32))
+    assert np.array_equal(lse1[perm].view(np.uint32), lse2.view(np.uint32))
+    lp3, _ = run_gpu(h, w, t)
+    assert np.array_equal(lp1.view(np.uint32), lp3.view(np.uint32)), "not deterministic"
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,nsample", [("8b", 24), ("32b", 24), ("policy", 12)])
+def test_full_size_workloads(name, nsample):
+    """Full-size runs; the oracle recomputes a seeded sample of rows (first and last included)."""
+    cfg = W.LOGPROB_CONFIGS[name]
+    say(f"logprob full-size {name}: generating")
+    x = W.make_logprob_inputs(cfg, dev())
+    say(f"logprob full-size {name}: gpu")
+    lp, lse = rk.token_logprob(x.hidden, x.w_lm, x.target, x.inv_temperature)
+    torch.cuda.synchronize()
+    rng = np.random.Generator(np.random.PCG64(11))
+    rows = np.unique(np.concatenate([[0, cfg.rows - 1], rng.integers(0, cfg.rows, nsample - 2)]))
+    idx = torch.from_numpy(rows).to(dev())
+    say(f"logprob full-size {name}: oracle on {len(rows)} rows")
+    rlp, rlse = oracle.token_logprob(W.bf16_bits(x.hidden[idx]), W.bf16_bits(x.w_lm),
+                                     x.target[idx].cpu().numpy(), x.inv_temperature)
+    e1 = max_abs(lp[idx].cpu().numpy(), rlp)
+    e2 = max_abs(lse[idx].cpu().numpy(), rlse)
+    say(f"logprob full-size {name}: logprob max-abs {e1:.3g}, lse max-abs {e2:.3g}")
+    assert e1 <= LOGPROB_TOL and e2 <= LOGPROB_TOL
+    assert torch.isfinite(lp).all() and torch.isfinite(lse).all()
