@@ -33,9 +33,10 @@ def max_abs(a, b) -> float:
     assert a.shape == b.shape
     if a.size == 0:
         return 0.0
-    both_inf = np.isinf(a) & np.isinf(b) & (np.sign(a) == np.sign(b))
+    # equal infinities and NaN on both sides (e.g. an invalid target) agree
+    same = (np.isinf(a) & np.isinf(b) & (np.sign(a) == np.sign(b))) | (np.isnan(a) & np.isnan(b))
     with np.errstate(invalid="ignore"):
-        d = np.where(both_inf, 0.0, np.abs(a - b))
+        d = np.where(same, 0.0, np.abs(a - b))
     return float(np.nan_to_num(d, nan=np.inf).max())
 
 
