@@ -24,9 +24,11 @@
  * current HIP device; "host" pointers are read only during the call.
  *
  * Ownership: the caller owns every buffer, including the workspace.  The
- * library allocates no device memory and keeps no state across calls except a
- * thread-local error string.  Calls on different streams need distinct
- * workspaces.
+ * library allocates no device memory.  Across calls it keeps only per-thread
+ * state: the last error string and a ring of 4 pinned host buffers (grown on
+ * demand, never freed) from which rl_decode_attn uploads its work list without
+ * making the host wait for the stream.  Calls on different streams need
+ * distinct workspaces.
  *
  * Errors: a call that returns anything other than RL_OK has enqueued nothing
  * and written no output; rl_last_error() then describes the problem.  Argument

@@ -1,6 +1,7 @@
 // Exported C ABI of librlkern.so (declared in include/rl_kernels.h).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -23,6 +24,66 @@ rl_status hip_error(hipError_t e, const char *what) {
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Pinned host staging for the work-list upload.  A copy from pinned memory is
+// truly asynchronous, so the host never waits for the stream; each slot's
+// event guards its reuse until the copy that read it has run.  The slots are
+// never freed (plain thread-local pointers, no destructors to run after the
+// HIP runtime has shut down).
+struct StagingSlot {
+    unsigned char *host;
+    size_t cap;
+    hipEvent_t done;
+    int device;
+    bool pending;
+};
+constexpr int kStagingSlots = 4;
+thread_local StagingSlot g_staging[kStagingSlots];
+thread_local int g_staging_next;
+
+rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t stream) {
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+    StagingSlot &slot = g_staging[g_staging_next];
+    g_staging_next = (g_staging_next + 1) % kStagingSlots;
+    if (slot.pending) {
+        e = hipEventSynchronize(slot.done);
+        if (e != hipSuccess) return hip_error(e, "waiting for a staging slot");
+        slot.pending = false;
+    }
+    if (slot.done && slot.device != device) {
+        (void)hipEventDestroy(slot.done);
+        slot.done = nullptr;
+    }
+    if (!slot.done) {
+        e = hipEventCreateWithFlags(&slot.done, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_error(e, "creating a staging event");
+        slot.device = device;
+    }
+    if (slot.cap < plan.meta_bytes) {
+        if (slot.host) (void)hipHostFree(slot.host);
+        slot.host = nullptr;
+        slot.cap = 0;
+        const size_t cap = std::max<size_t>(plan.meta_bytes * 2, 1 << 16);
+        e = hipHostMalloc(reinterpret_cast<void **>(&slot.host), cap, hipHostMallocDefault);
+        if (e != hipSuccess) return hip_error(e, "allocating pinned staging memory");
+        slot.cap = cap;
+    }
+    std::memset(slot.host, 0, plan.meta_bytes);
+    std::memcpy(slot.host + plan.off_items, plan.dev_items.data(),
+                plan.dev_items.size() * sizeof(rlk::DevItem));
+    std::memcpy(slot.host + plan.off_prefix_units, plan.prefix_units.data(),
+                plan.prefix_units.size() * sizeof(rlk::DevUnit));
+    std::memcpy(slot.host + plan.off_suffix_units, plan.suffix_units.data(),
+                plan.suffix_units.size() * sizeof(rlk::DevUnit));
+    e = hipMemcpyAsync(dst, slot.host, plan.meta_bytes, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_error(e, "uploading the work list");
+    e = hipEventRecord(slot.done, stream);
+    if (e != hipSuccess) return hip_error(e, "recording the staging event");
+    slot.pending = true;
+    return RL_OK;
+}
 
 }  // namespace
 
@@ -91,18 +152,10 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
 
     // Work list and unit tables, uploaded in one copy on the caller's stream.
-    thread_local std::vector<unsigned char> meta;
-    meta.assign(plan.meta_bytes, 0);
-    std::memcpy(meta.data() + plan.off_items, plan.dev_items.data(),
-                plan.dev_items.size() * sizeof(rlk::DevItem));
-    std::memcpy(meta.data() + plan.off_prefix_units, plan.prefix_units.data(),
-                plan.prefix_units.size() * sizeof(rlk::DevUnit));
-    std::memcpy(meta.data() + plan.off_suffix_units, plan.suffix_units.data(),
-                plan.suffix_units.size() * sizeof(rlk::DevUnit));
     hipStream_t hs = static_cast<hipStream_t>(stream);
     unsigned char *ws = static_cast<unsigned char *>(workspace);
-    hipError_t e = hipMemcpyAsync(ws, meta.data(), plan.meta_bytes, hipMemcpyHostToDevice, hs);
-    if (e != hipSuccess) return hip_error(e, "uploading the work list");
+    st = stage_upload(plan, ws, hs);
+    if (st != RL_OK) return st;
 
     rlk::DecodeArgs a{};
     a.q = static_cast<const uint16_t *>(ptrs->q);
@@ -126,7 +179,7 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.r = plan.r;
     a.D = plan.D;
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
-    e = rlk::launch_decode(a, hs);
+    const hipError_t e = rlk::launch_decode(a, hs);
     if (e != hipSuccess) return hip_error(e, "launching decode attention");
     return RL_OK;
 }

@@ -181,15 +181,18 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_tile_kernel(LogprobArgs a
     }
 }
 
-__global__ __launch_bounds__(kThreads) void logprob_combine_kernel(LogprobArgs a) {
-    const int64_t r = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
-    if (r >= a.R) return;
-    float Mx = -INFINITY;
-    for (int64_t vt = 0; vt < a.n_vocab_tiles; ++vt) Mx = fmaxf(Mx, a.pm[vt * a.R + r]);
-    float L = 0.f;
-    for (int64_t vt = 0; vt < a.n_vocab_tiles; ++vt)
-        L += a.pl[vt * a.R + r] * fast_exp2(a.pm[vt * a.R + r] - Mx);
-    const float lse = (Mx + fast_log2(L)) * kLn2;
+// Online log-sum-exp merge of (max, sum) partials, both in log2 units.
+__device__ __forceinline__ void lse_merge(float &M, float &L, float m, float l) {
+    if (m > M) {
+        L = L * fast_exp2(M - m) + l;
+        M = m;
+    } else {
+        L += l * fast_exp2(m - M);
+    }
+}
+
+__device__ __forceinline__ void finish_row(const LogprobArgs &a, int64_t r, float M, float L) {
+    const float lse = (M + fast_log2(L)) * kLn2;
     const int32_t t = a.target[r];
     float lp;
     if (t == -1) lp = 0.f;
@@ -199,6 +202,39 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_kernel(LogprobArgs a
     if (a.lse) a.lse[r] = lse;
 }
 
+// Few rows: one wave per row, lanes stride over the vocab tiles.
+__global__ __launch_bounds__(kThreads) void logprob_combine_wave_kernel(LogprobArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
+    if (r >= a.R) return;
+    float M = -INFINITY, L = 0.f;
+    for (int64_t vt = lane; vt < a.n_vocab_tiles; vt += 64) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
+    const float Mw = wave_max(M);
+    const float Lw = wave_sum(M == -INFINITY ? 0.f : L * fast_exp2(M - Mw));
+    if (lane == 0) finish_row(a, r, Mw, Lw);
+}
+
+// Many rows: one thread per row; neighbouring threads read neighbouring rows
+// of each vocab tile's partials (coalesced).
+__global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobArgs a) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    if (r >= a.R) return;
+    float M = -INFINITY, L = 0.f;
+    int64_t vt = 0;
+    for (; vt + 4 <= a.n_vocab_tiles; vt += 4) {
+        float m[4], l[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            m[j] = a.pm[(vt + j) * a.R + r];
+            l[j] = a.pl[(vt + j) * a.R + r];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) lse_merge(M, L, m[j], l[j]);
+    }
+    for (; vt < a.n_vocab_tiles; ++vt) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
+    finish_row(a, r, M, L);
+}
+
 }  // namespace
 
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
@@ -206,8 +242,15 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
     hipLaunchKernelGGL(logprob_tile_kernel, dim3(static_cast<uint32_t>(tiles)), dim3(kThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t blocks = (a.R + kThreads - 1) / kThreads;
-    hipLaunchKernelGGL(logprob_combine_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream, a);
+    if (a.R < 32768) {
+        const int64_t blocks = (a.R + 3) / 4;
+        hipLaunchKernelGGL(logprob_combine_wave_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
+                           stream, a);
+    } else {
+        const int64_t blocks = (a.R + kThreads - 1) / kThreads;
+        hipLaunchKernelGGL(logprob_combine_row_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
+                           stream, a);
+    }
     return hipGetLastError();
 }
 
