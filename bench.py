@@ -47,6 +47,38 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+CSRC = os.path.join(ROOT, "paper_2607_20908_amd", "csrc")
+KERNEL_SOURCES = {"decode": "decode_attn.hip", "lmhead": "token_logprob.hip"}
+
+
+def source_sha256(op: str) -> str:
+    import hashlib
+    with open(os.path.join(CSRC, KERNEL_SOURCES[op]), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(op: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    op and workload, if that summary was taken on the current kernel source;
+    otherwise None.  The summary holds lines `source_sha256: ...` and
+    `hbm_bytes_per_launch: ...` (FETCH_SIZE + WRITE_SIZE, calibrated)."""
+    path = os.path.join(ROOT, "profiles", f"{op}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                fields[k.strip().strip("-* `")] = v.strip().strip("`")
+    if fields.get("source_sha256") != source_sha256(op):
+        return None
+    try:
+        return int(float(fields["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
 def decode_bytes(x) -> int:
     """Algorithmic HBM bytes of one decode-attention call: K and V of every
     prefix token once per prompt and of every suffix token once, q read, out
@@ -119,11 +151,14 @@ def main():
     ap.add_argument("--workload", default="8b", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 to skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 1 GiB device copy before the steps (outside the timed region) so a "
+                         "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs the hot path on a single MI355X "
-              "and has no multi-GPU path (see DESIGN.md for how it would shard).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library runs the hot path on a single MI355X "
+              "and has no multi-GPU path; run it without --gpus or with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import paper_2607_20908_amd as rk
@@ -164,6 +199,12 @@ def main():
         ops.append(("lmhead", run_logprob))
 
     stream = torch.cuda.current_stream()
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)      # 1 GiB
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     log(f"bench: workload {args.workload}: warmup {args.warmup}")
     for _ in range(args.warmup):
         for _, f in ops:
@@ -198,9 +239,11 @@ def main():
                     "unit": "GB/s", "decode_ms": round(op_ms["decode"], 4),
                     "decode_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
                     "decode_algorithmic_bytes": nbytes})
-        rooflines.append((op_ms["decode"], {"kernel": "decode attention (split + combine)", "bound": "hbm",
-                                            "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}))
+        rooflines.append((op_ms["decode"], {"kernel": "decode attention (split + combine kernels)",
+                                            "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                                            "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                                            "traffic": measured_traffic("decode", args.workload),
+                                            "algorithmic_bytes": nbytes}))
     if y is not None:
         fl = lmhead_flops(y.cfg)
         tf = fl / (op_ms["lmhead"] * 1e-3) / 1e12
@@ -209,13 +252,18 @@ def main():
         if x is None:
             res.update({"metric": "lm-head logprob TFLOP/s (% MFMA)", "value": round(tf, 1),
                         "unit": "TFLOP/s"})
-        rooflines.append((op_ms["lmhead"], {"kernel": "lm-head log-prob (tile + combine)", "bound": "mfma",
-                                            "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                                            "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                                            "traffic": None}))
+        rooflines.append((op_ms["lmhead"], {"kernel": "lm-head log-prob (tile + combine kernels)",
+                                            "bound": "mfma", "achieved": round(tf, 1),
+                                            "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                            "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                                            "traffic": measured_traffic("lmhead", args.workload),
+                                            "algorithmic_flops": fl}))
     res["metric"] = "decode-attn effective KV GB/s (% HBM peak); lm-head logprob TFLOP/s (% MFMA)" \
         if (x is not None and y is not None) else res["metric"]
-    res["roofline"] = max(rooflines, key=lambda t: t[0])[1]
+    rooflines.sort(key=lambda t: -t[0])
+    res["roofline"] = rooflines[0][1]            # the operation that takes the most time
+    if len(rooflines) > 1:
+        res["roofline_other"] = rooflines[1][1]
     if args.cpu_budget > 0:
         log("bench: cpu baseline (fp64 oracle)")
         res["cpu_baseline"] = (cpu_baseline_decode(x, args.cpu_budget) if x is not None
