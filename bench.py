@@ -11,7 +11,9 @@ workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
 Prints ONE JSON line.  `value` is decode attention's effective KV bandwidth
 (algorithmic bytes, the prefix counted once per prompt, over the measured
 decode time); the lm-head's TFLOP/s are reported beside it.  Per-operation
-durations come from HIP events recorded on the stream the kernels run on.
+durations come from HIP events recorded on the stream the kernels run on
+(created with a device-scope release, so recording one does not write back the
+L2 to system memory and the interval matches the kernels' own durations).
 """
 from __future__ import annotations
 
@@ -41,6 +43,45 @@ WORKLOADS = {
                                  "prefix 24576, suffix geometric mean 1024 cap 4096"),
     "policy": (None, "policy", "policy-update log-prob pass: 262144 rows x 5120 x 151936"),
 }
+
+
+class HipEvents:
+    """hipEventCreateWithFlags / Record / ElapsedTime through the HIP runtime the
+    process already uses, with hipEventReleaseToDevice: a timing event that only
+    needs device-scope ordering (torch.cuda.Event always fences at system scope)."""
+    RELEASE_TO_DEVICE = 0x40000000
+
+    def __init__(self, runtime_path: str):
+        import ctypes
+        self.ct = ctypes
+        self.lib = ctypes.CDLL(runtime_path)
+        self.lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        self.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = self.ct.c_void_p()
+        st = self.lib.hipEventCreateWithFlags(self.ct.byref(ev), self.RELEASE_TO_DEVICE)
+        if st != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({st})")
+        return ev
+
+    def record(self, ev, stream_handle: int):
+        st = self.lib.hipEventRecord(ev, self.ct.c_void_p(stream_handle))
+        if st != 0:
+            raise RuntimeError(f"hipEventRecord failed ({st})")
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = self.ct.c_float()
+        st = self.lib.hipEventElapsedTime(self.ct.byref(ms), a, b)
+        if st != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({st})")
+        return ms.value
+
+    def destroy(self, ev):
+        self.lib.hipEventDestroy(ev)
 
 
 def log(*a):
@@ -102,8 +143,8 @@ def cpu_baseline_decode(x, budget_s: float):
     c = x.cfg
     G = c.group_size
     q = W.bf16_bits(x.q)
-    kp, vp = W.bf16_bits(x.k_prefix), W.bf16_bits(x.v_prefix)
-    ks, vs = W.bf16_bits(x.k_suffix), W.bf16_bits(x.v_suffix)
+    kp, vp = W.bf16_bits(x.token_major(x.k_prefix)), W.bf16_bits(x.token_major(x.v_prefix))
+    ks, vs = W.bf16_bits(x.token_major(x.k_suffix)), W.bf16_bits(x.token_major(x.v_suffix))
     total_bytes, total_s, n = 0, 0.0, 0
     while total_s < budget_s and n < 64 * c.num_prompts:
         p = n % c.num_prompts
@@ -156,6 +197,8 @@ def main():
     ap.add_argument("--workload", default="8b", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle time per operation for the CPU baseline (0 to skip)")
+    ap.add_argument("--kv-layout", default="head", choices=["head", "token"],
+                    help="KV cache layout: head-major [Hkv, rows, D] (default) or token-major [rows, Hkv, D]")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy before the steps (outside the timed region) so a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -172,7 +215,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dname, lname, desc = WORKLOADS[args.workload]
-    x = W.make_decode_inputs(W.DECODE_CONFIGS[dname], dev) if dname else None
+    x = W.make_decode_inputs(W.DECODE_CONFIGS[dname], dev, kv_layout=args.kv_layout) if dname else None
     y = W.make_logprob_inputs(W.LOGPROB_CONFIGS[lname], dev) if lname else None
 
     ops = []
@@ -180,16 +223,17 @@ def main():
         c = x.cfg
         out = torch.empty((c.num_seqs, c.num_q_heads, c.head_dim), dtype=torch.bfloat16, device=dev)
         lse = torch.empty((c.num_seqs, c.num_q_heads), dtype=torch.float32, device=dev)
+        rdim = 1 if args.kv_layout == "head" else 0
         need = rk.decode_attn_workspace_size(c.num_prompts, c.group_size, c.num_q_heads, c.num_kv_heads,
                                              c.head_dim, x.prefix_start, x.prefix_len, x.suffix_start,
-                                             x.suffix_len, x.k_prefix.shape[0], x.k_suffix.shape[0],
-                                             x.scale)
+                                             x.suffix_len, x.k_prefix.shape[rdim], x.k_suffix.shape[rdim],
+                                             x.scale, kv_layout=args.kv_layout)
         ws_d = torch.empty(need, dtype=torch.uint8, device=dev)
 
         def run_decode():
             rk.decode_attn(x.q, x.k_prefix, x.v_prefix, x.k_suffix, x.v_suffix, x.prefix_start,
                            x.prefix_len, x.suffix_start, x.suffix_len, c.group_size, scale=x.scale,
-                           out=out, lse=lse, workspace=ws_d, return_lse=True)
+                           out=out, lse=lse, workspace=ws_d, return_lse=True, kv_layout=args.kv_layout)
         ops.append(("decode", run_decode))
     if y is not None:
         cl = y.cfg
@@ -215,27 +259,34 @@ def main():
         for _, f in ops:
             f()
     torch.cuda.synchronize()
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
-          for _ in range(args.steps)]
+    runtimes = rk.hip_runtimes_mapped()
+    if len(runtimes) != 1:
+        raise RuntimeError(f"expected one HIP runtime in the process, found {runtimes}")
+    hip = HipEvents(runtimes[0])
+    sh = stream.cuda_stream
+    ev = [[(hip.create(), hip.create()) for _ in ops] for _ in range(args.steps)]
     log(f"bench: timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         for j, (_, f) in enumerate(ops):
-            ev[k][j][0].record(stream)
+            hip.record(ev[k][j][0], sh)
             f()
-            ev[k][j][1].record(stream)
+            hip.record(ev[k][j][1], sh)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    op_ms = {name: float(np.mean([ev[k][j][0].elapsed_time(ev[k][j][1]) for k in range(args.steps)]))
+    op_ms = {name: float(np.mean([hip.elapsed_ms(*ev[k][j]) for k in range(args.steps)]))
              for j, (name, _) in enumerate(ops)}
+    for pair in (p for row in ev for p in row):
+        for e in pair:
+            hip.destroy(e)
     ms_per_step = wall * 1e3 / args.steps
     log(f"bench: {ms_per_step:.3f} ms/step; per op {op_ms}")
 
     res = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, HBM-resident)",
-           "config": {"workload": desc}}
+           "config": {"workload": desc, "kv_layout": args.kv_layout if x is not None else None}}
     rooflines = []
     if x is not None:
         nbytes = decode_bytes(x)

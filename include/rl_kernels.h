@@ -25,10 +25,11 @@
  *
  * Ownership: the caller owns every buffer, including the workspace.  The
  * library allocates no device memory.  Across calls it keeps only per-thread
- * state: the last error string and a ring of 4 pinned host buffers (grown on
- * demand, never freed) from which rl_decode_attn uploads its work list without
- * making the host wait for the stream.  Calls on different streams need
- * distinct workspaces.
+ * state: the last error string, a reusable planning buffer and a ring of 4
+ * pinned, device-mapped host buffers (grown on demand, never freed) that a
+ * small kernel on the caller's stream copies the work list from, so the host
+ * does not wait for the stream.  Calls on different streams need distinct
+ * workspaces.
  *
  * Errors: a call that returns anything other than RL_OK has enqueued nothing
  * and written no output; rl_last_error() then describes the problem.  Argument
@@ -46,7 +47,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 1
+#define RL_ABI_VERSION 2
 
 typedef enum {
     RL_OK = 0,
@@ -74,7 +75,14 @@ typedef struct {
                               split-K work item covers (a multiple of 16, >= 16).  Results
                               agree across splits to rounding, and are bitwise
                               reproducible for a fixed split.                              */
+    int32_t kv_layout;     /* RL_KV_TOKEN_MAJOR or RL_KV_HEAD_MAJOR (all four KV tensors)  */
 } rl_decode_shape;
+
+/* KV cache layouts.  Token-major keeps the kv heads of a token together; head-major
+ * keeps each kv head's rows contiguous, so one (sequence, kv head) streams as one
+ * contiguous range (the faster layout on MI355X). */
+#define RL_KV_TOKEN_MAJOR 0   /* [rows, Hkv, D] */
+#define RL_KV_HEAD_MAJOR 1    /* [Hkv, rows, D] */
 
 typedef struct {
     const int64_t *prefix_start; /* host [P]:   first KV row of prompt p's prefix           */
@@ -87,10 +95,10 @@ typedef struct {
 
 typedef struct {
     const void *q;        /* device bf16 [P*G, Hq, D], contiguous                          */
-    const void *k_prefix; /* device bf16 [prefix_rows, Hkv, D]                             */
-    const void *v_prefix; /* device bf16 [prefix_rows, Hkv, D]                             */
-    const void *k_suffix; /* device bf16 [suffix_rows, Hkv, D]                             */
-    const void *v_suffix; /* device bf16 [suffix_rows, Hkv, D]                             */
+    const void *k_prefix; /* device bf16 [prefix_rows, Hkv, D] or [Hkv, prefix_rows, D]    */
+    const void *v_prefix; /* device bf16, same layout as k_prefix                          */
+    const void *k_suffix; /* device bf16 [suffix_rows, Hkv, D] or [Hkv, suffix_rows, D]    */
+    const void *v_suffix; /* device bf16, same layout as k_suffix                          */
     void  *out;           /* device bf16 [P*G, Hq, D]: softmax-weighted sum of values,
                              rounded to nearest even; 0 for an empty context               */
     float *lse;           /* device fp32 [P*G, Hq] natural-log log-sum-exp of the scaled
@@ -109,7 +117,7 @@ typedef struct {
  * Rows outside the given ranges are never read.  P*G == 0 is a valid no-op.
  * Status: NULL pointer -> RL_ERR_NULL_POINTER; negative sizes or lengths,
  * Hq % Hkv != 0, a range past prefix_rows/suffix_rows, a non-finite or
- * non-positive scale, a bad split_tokens -> RL_ERR_INVALID_SHAPE;
+ * non-positive scale, a bad split_tokens or kv_layout -> RL_ERR_INVALID_SHAPE;
  * D not in {64, 128} -> RL_ERR_UNSUPPORTED; a device pointer not 16-byte
  * aligned -> RL_ERR_MISALIGNED; workspace NULL or short -> RL_ERR_WORKSPACE.
  */

@@ -43,7 +43,10 @@ class DecodeShape(ctypes.Structure):
     _fields_ = [("num_prompts", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-                ("split_tokens", ctypes.c_int32)]
+                ("split_tokens", ctypes.c_int32), ("kv_layout", ctypes.c_int32)]
+
+
+KV_LAYOUTS = {"token": 0, "head": 1}   # [rows, Hkv, D] / [Hkv, rows, D]
 
 
 class DecodeLens(ctypes.Structure):
@@ -90,7 +93,7 @@ def _load():
     lib.rl_token_logprob.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, SZ, P]
     lib.rl_decode_plan_debug.restype = ctypes.c_int
     lib.rl_decode_plan_debug.argtypes = [P, P, P, I64, ctypes.POINTER(I64)]
-    if lib.rl_abi_version() != 1:
+    if lib.rl_abi_version() != 2:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -149,7 +152,7 @@ class _DecodeArgs:
     """Host-side ctypes structures for one decode call (kept alive by the caller)."""
 
     def __init__(self, P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
-                 suffix_start, suffix_len, prefix_rows, suffix_rows):
+                 suffix_start, suffix_len, prefix_rows, suffix_rows, kv_layout="token"):
         self.ps = np.ascontiguousarray(prefix_start, dtype=np.int64)
         self.pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
         self.ss = np.ascontiguousarray(suffix_start, dtype=np.int64)
@@ -157,17 +160,20 @@ class _DecodeArgs:
         if self.ps.shape != (P,) or self.pl.shape != (P,) or self.ss.shape != (P * G,) \
                 or self.sl.shape != (P * G,):
             raise ValueError("length arrays must be [P] (prefix) and [P*G] (suffix)")
-        self.shape = DecodeShape(P, G, Hq, Hkv, D, float(np.float32(scale)), int(split_tokens))
+        if kv_layout not in KV_LAYOUTS:
+            raise ValueError(f"kv_layout must be one of {sorted(KV_LAYOUTS)}")
+        self.shape = DecodeShape(P, G, Hq, Hkv, D, float(np.float32(scale)), int(split_tokens),
+                                 KV_LAYOUTS[kv_layout])
         self.lens = DecodeLens(self.ps.ctypes.data, self.pl.ctypes.data, self.ss.ctypes.data,
                                self.sl.ctypes.data, int(prefix_rows), int(suffix_rows))
 
 
 def decode_attn_workspace_size(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start,
                                suffix_len, prefix_rows, suffix_rows, scale=None,
-                               split_tokens: int = 0) -> int:
+                               split_tokens: int = 0, kv_layout: str = "token") -> int:
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     a = _DecodeArgs(P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
-                    suffix_start, suffix_len, prefix_rows, suffix_rows)
+                    suffix_start, suffix_len, prefix_rows, suffix_rows, kv_layout)
     n = ctypes.c_size_t(0)
     _check(_lib.rl_decode_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens),
                                               ctypes.byref(n)), "rl_decode_attn_workspace_size")
@@ -197,11 +203,12 @@ def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
                 prefix_start, prefix_len, suffix_start, suffix_len, group_size: int,
                 scale: Optional[float] = None, split_tokens: int = 0, return_lse: bool = False,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-                workspace: Optional[torch.Tensor] = None, stream=None):
+                workspace: Optional[torch.Tensor] = None, stream=None, kv_layout: str = "token"):
     """Decode attention of P*G candidates over their prompt's prefix KV ++ own suffix KV.
 
-    q [P*G, Hq, D] bf16; k/v_prefix [rows_p, Hkv, D] bf16; k/v_suffix [rows_s, Hkv, D]
-    bf16 (device); prefix_start/len [P], suffix_start/len [P*G] host integers.
+    q [P*G, Hq, D] bf16; k/v_prefix and k/v_suffix bf16 device tensors laid out
+    [rows, Hkv, D] (kv_layout="token") or [Hkv, rows, D] (kv_layout="head");
+    prefix_start/len [P], suffix_start/len [P*G] host integers.
     Returns out [P*G, Hq, D] bf16 (and lse [P*G, Hq] fp32 natural log).
     """
     for t, n in ((q, "q"), (k_prefix, "k_prefix"), (v_prefix, "v_prefix"),
@@ -212,15 +219,17 @@ def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
     if G <= 0 or S % G:
         raise ValueError("q.shape[0] must be a positive multiple of group_size")
     P = S // G
-    Hkv = k_prefix.shape[1]
+    head_major = kv_layout == "head"
+    hdim, rdim = (0, 1) if head_major else (1, 0)
+    Hkv = k_prefix.shape[hdim]
     for t in (k_prefix, v_prefix, k_suffix, v_suffix):
-        if t.dim() != 3 or t.shape[1] != Hkv or t.shape[2] != D:
-            raise ValueError("KV tensors must be [rows, Hkv, D]")
+        if t.dim() != 3 or t.shape[hdim] != Hkv or t.shape[2] != D:
+            raise ValueError("KV tensors must be [rows, Hkv, D] (token) or [Hkv, rows, D] (head)")
     if k_prefix.shape != v_prefix.shape or k_suffix.shape != v_suffix.shape:
         raise ValueError("K and V shapes differ")
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     a = _DecodeArgs(P, G, Hq, Hkv, D, scale, split_tokens, prefix_start, prefix_len,
-                    suffix_start, suffix_len, k_prefix.shape[0], k_suffix.shape[0])
+                    suffix_start, suffix_len, k_prefix.shape[rdim], k_suffix.shape[rdim], kv_layout)
     if out is None:
         out = torch.empty((S, Hq, D), dtype=torch.bfloat16, device=q.device)
     if return_lse and lse is None:

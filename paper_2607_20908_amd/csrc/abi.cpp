@@ -25,13 +25,15 @@ rl_status hip_error(hipError_t e, const char *what) {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Pinned host staging for the work-list upload.  A copy from pinned memory is
-// truly asynchronous, so the host never waits for the stream; each slot's
-// event guards its reuse until the copy that read it has run.  The slots are
-// never freed (plain thread-local pointers, no destructors to run after the
-// HIP runtime has shut down).
+// Pinned host staging for the work-list upload.  The slots are coherent,
+// device-mapped host memory that a small kernel on the caller's stream reads
+// directly (no copy-engine hand-off in front of the split kernel), so the host
+// never waits for the stream; each slot's event guards its reuse until the
+// kernel that read it has run.  The slots are never freed (plain thread-local
+// pointers, no destructors to run after the HIP runtime has shut down).
 struct StagingSlot {
     unsigned char *host;
+    void *dev;                 // the same memory as the device sees it
     size_t cap;
     hipEvent_t done;
     int device;
@@ -40,6 +42,10 @@ struct StagingSlot {
 constexpr int kStagingSlots = 4;
 thread_local StagingSlot g_staging[kStagingSlots];
 thread_local int g_staging_next;
+
+// One plan object per thread, reused so that planning does not allocate once
+// its vectors have grown to the problem size.
+thread_local rlk::DecodePlan g_plan;
 
 rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t stream) {
     int device = 0;
@@ -57,7 +63,9 @@ rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t strea
         slot.done = nullptr;
     }
     if (!slot.done) {
-        e = hipEventCreateWithFlags(&slot.done, hipEventDisableTiming);
+        // completion only: the host reads nothing the GPU wrote, so no
+        // system-scope fence (an L2 write-back) is needed when it is recorded
+        e = hipEventCreateWithFlags(&slot.done, hipEventDisableTiming | hipEventDisableSystemFence);
         if (e != hipSuccess) return hip_error(e, "creating a staging event");
         slot.device = device;
     }
@@ -66,18 +74,25 @@ rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t strea
         slot.host = nullptr;
         slot.cap = 0;
         const size_t cap = std::max<size_t>(plan.meta_bytes * 2, 1 << 16);
-        e = hipHostMalloc(reinterpret_cast<void **>(&slot.host), cap, hipHostMallocDefault);
+        e = hipHostMalloc(reinterpret_cast<void **>(&slot.host), cap,
+                          hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) return hip_error(e, "allocating pinned staging memory");
+        e = hipHostGetDevicePointer(&slot.dev, slot.host, 0);
+        if (e != hipSuccess) return hip_error(e, "mapping pinned staging memory");
         slot.cap = cap;
     }
-    std::memset(slot.host, 0, plan.meta_bytes);
-    std::memcpy(slot.host + plan.off_items, plan.dev_items.data(),
-                plan.dev_items.size() * sizeof(rlk::DevItem));
-    std::memcpy(slot.host + plan.off_prefix_units, plan.prefix_units.data(),
-                plan.prefix_units.size() * sizeof(rlk::DevUnit));
-    std::memcpy(slot.host + plan.off_suffix_units, plan.suffix_units.data(),
-                plan.suffix_units.size() * sizeof(rlk::DevUnit));
-    e = hipMemcpyAsync(dst, slot.host, plan.meta_bytes, hipMemcpyHostToDevice, stream);
+    // the three sections, each followed by zeros up to the next section
+    auto put = [&](size_t off, const void *src, size_t n, size_t end) {
+        std::memcpy(slot.host + off, src, n);
+        std::memset(slot.host + off + n, 0, end - off - n);
+    };
+    put(plan.off_items, plan.dev_items.data(), plan.dev_items.size() * sizeof(rlk::DevItem),
+        plan.off_prefix_units);
+    put(plan.off_prefix_units, plan.prefix_units.data(),
+        plan.prefix_units.size() * sizeof(rlk::DevUnit), plan.off_suffix_units);
+    put(plan.off_suffix_units, plan.suffix_units.data(),
+        plan.suffix_units.size() * sizeof(rlk::DevUnit), plan.meta_bytes);
+    e = rlk::launch_plan_fetch(slot.dev, dst, plan.meta_bytes, stream);
     if (e != hipSuccess) return hip_error(e, "uploading the work list");
     e = hipEventRecord(slot.done, stream);
     if (e != hipSuccess) return hip_error(e, "recording the staging event");
@@ -110,11 +125,10 @@ rl_status rl_decode_attn_workspace_size(const rl_decode_shape *shape, const rl_d
                                         size_t *bytes) {
     g_last_error.clear();
     if (!bytes) return set_error(RL_ERR_NULL_POINTER, "bytes is NULL");
-    rlk::DecodePlan plan;
     std::string err;
-    const rl_status st = rlk::plan_decode(shape, lens, &plan, &err);
+    const rl_status st = rlk::plan_decode(shape, lens, &g_plan, &err, rlk::PlanDetail::kSizes);
     if (st != RL_OK) return set_error(st, err);
-    *bytes = plan.total_bytes;
+    *bytes = g_plan.total_bytes;
     return RL_OK;
 }
 
@@ -126,7 +140,7 @@ rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_len
     if (capacity > 0 && !items) return set_error(RL_ERR_NULL_POINTER, "items is NULL");
     rlk::DecodePlan plan;
     std::string err;
-    const rl_status st = rlk::plan_decode(shape, lens, &plan, &err);
+    const rl_status st = rlk::plan_decode(shape, lens, &plan, &err, rlk::PlanDetail::kDebug);
     if (st != RL_OK) return set_error(st, err);
     const int64_t n = static_cast<int64_t>(plan.items.size());
     for (int64_t i = 0; i < n && i < capacity; ++i) items[i] = plan.items[i];
@@ -138,9 +152,9 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
                          const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
                          void *stream) {
     g_last_error.clear();
-    rlk::DecodePlan plan;
+    rlk::DecodePlan &plan = g_plan;
     std::string err;
-    rl_status st = rlk::plan_decode(shape, lens, &plan, &err);
+    rl_status st = rlk::plan_decode(shape, lens, &plan, &err, rlk::PlanDetail::kDevice);
     if (st != RL_OK) return set_error(st, err);
     st = rlk::check_decode_ptrs(plan, lens, ptrs, &err);
     if (st != RL_OK) return set_error(st, err);
@@ -178,6 +192,9 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.Hkv = plan.Hkv;
     a.r = plan.r;
     a.D = plan.D;
+    a.kv_layout = plan.kv_layout;
+    a.prefix_rows = plan.prefix_rows;
+    a.suffix_rows = plan.suffix_rows;
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
     const hipError_t e = rlk::launch_decode(a, hs);
     if (e != hipSuccess) return hip_error(e, "launching decode attention");

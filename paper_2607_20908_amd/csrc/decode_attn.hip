@@ -14,6 +14,8 @@
 // Each item leaves, per query row, a partial (max m, sum l, weighted value
 // sum acc[D]) in log2 units; the combine kernel merges the partials of each
 // (sequence, head) by log-sum-exp and writes the bf16 output and fp32 lse.
+#include <algorithm>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -29,24 +31,45 @@ struct DCfg {
     static constexpr int CH = D / 8;             // 16-byte chunks per token row
     static constexpr int KK = D / 32;            // k-steps of S^T = K Q^T
     static constexpr int DT = D / 16;            // 16-wide d tiles of O^T
-    static constexpr int LDR = D + 8;            // LDS row pitch in bf16 (16-byte pad)
-    static constexpr int TILE = kTileTokens * LDR; // bf16 elements of one K or V tile
+    static constexpr int LDR = D + 8;            // K row pitch in bf16 (16-byte pad)
+    static constexpr int LDRV = D + 16;          // V row pitch in bf16 (32-byte pad)
+    static constexpr int TILE = kTileTokens * LDR;   // bf16 elements of one K tile
+    static constexpr int TILEV = kTileTokens * LDRV; // bf16 elements of one V tile
+    static constexpr int STAGE = TILE + TILEV;       // one K tile followed by one V tile
     static constexpr int LD = kTileTokens * CH / kThreads;  // 16-byte chunks per thread per tensor
     static constexpr int RED_STRIDE = D + 1;     // fp32 row stride of the merge area (bank spread)
-    static constexpr int KV_BYTES = 2 * 2 * TILE * 2;                  // 2 buffers x (K, V)
+    static constexpr int KV_BYTES = 2 * STAGE * 2;                     // 2 buffers x (K, V)
     static constexpr int RED_BYTES = 4 * 2 * 16 * RED_STRIDE * 4;      // waves x ct x 16 rows
     static constexpr int MAIN_BYTES = KV_BYTES > RED_BYTES ? KV_BYTES : RED_BYTES;
     static constexpr int ML_BYTES = 4 * 2 * 16 * 2 * 4;
 };
 
-// Element offset of 16-byte chunk c of token t inside a K or V tile.  Rows are
-// padded by 16 bytes, so the lanes that read one chunk of 16 consecutive
-// tokens (K operand) or one d of 4 tokens 4 apart (V^T operand) spread over
-// the LDS banks, and every read of a lane sits at a constant offset from one
-// base address.
+// Element offset of 16-byte chunk c of token t inside a K tile.  Rows are
+// padded by 16 bytes, so the 16 lanes that read one chunk of 16 consecutive
+// tokens (K operand) hit 16 disjoint groups of 4 banks, and every read of a
+// lane sits at a constant offset from one base address.
 template <int D>
 __device__ __forceinline__ int kv_off(int t, int c) {
     return t * DCfg<D>::LDR + (c << 3);
+}
+
+// Element offset of 16-byte chunk c of token t inside a V tile.  V rows are
+// padded by 32 bytes: the transposing reads of the V^T operand fetch 8 bytes
+// at 4 d-offsets of 8 consecutive tokens per half-wave, and a pitch of 8 banks
+// (mod 64) puts those 8 rows on disjoint banks.
+template <int D>
+__device__ __forceinline__ int v_off(int t, int c) {
+    return t * DCfg<D>::LDRV + (c << 3);
+}
+
+// gfx950 transposing LDS read: in each group of 16 lanes, lane s supplies the
+// address of 4 consecutive bf16; seen as a 4 x 16 block whose row k holds the
+// values of lanes 4k..4k+3 in order, lane n receives column n (rows 0..3).
+__device__ __forceinline__ bf16x4 lds_read_tr16(const uint16_t *p) {
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef s16x4 __attribute__((address_space(3))) *lds_s16x4;
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+    return __builtin_bit_cast(bf16x4, v);
 }
 
 // MAXC: column tiles (16 query rows each) per wave; 1 serves items of up to
@@ -73,9 +96,14 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
     const int wc = wave % Wc, wt = wave / Wc;
     const int n_my = (wc < n_ct ? 1 : 0) + (MAXC > 1 && wc + Wc < n_ct ? 1 : 0);
     const int ntok = it.ntok;
-    const int64_t tok_stride = static_cast<int64_t>(a.Hkv) * D;
-    const uint16_t *kg = (is_suffix ? a.k_suffix : a.k_prefix) + (it.kv_row0 * a.Hkv + kh) * D;
-    const uint16_t *vg = (is_suffix ? a.v_suffix : a.v_prefix) + (it.kv_row0 * a.Hkv + kh) * D;
+    // token-major [rows, Hkv, D]: rows of one kv head are Hkv*D apart;
+    // head-major [Hkv, rows, D]: they are contiguous
+    const bool head_major = a.kv_layout == RL_KV_HEAD_MAJOR;
+    const int64_t nrows = is_suffix ? a.suffix_rows : a.prefix_rows;
+    const int64_t tok_stride = head_major ? D : static_cast<int64_t>(a.Hkv) * D;
+    const int64_t base = head_major ? (kh * nrows + it.kv_row0) * D : (it.kv_row0 * a.Hkv + kh) * D;
+    const uint16_t *kg = (is_suffix ? a.k_suffix : a.k_prefix) + base;
+    const uint16_t *vg = (is_suffix ? a.v_suffix : a.v_prefix) + base;
 
     // ---- query rows of this wave as MFMA B operands (Q^T, k = d) ----------
     bf16x8 qb[MAXC][C::KK];
@@ -130,14 +158,14 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
         }
     };
     auto store_tile = [&](int buf) {
-        uint16_t *kl = kv + buf * 2 * C::TILE;
+        uint16_t *kl = kv + buf * C::STAGE;
         uint16_t *vl = kl + C::TILE;
 #pragma unroll
         for (int j = 0; j < C::LD; ++j) {
             const int idx = tid + j * kThreads;
             const int t = idx / C::CH, ch = idx % C::CH;
             *reinterpret_cast<u32x4 *>(kl + kv_off<D>(t, ch)) = kr[j];
-            *reinterpret_cast<u32x4 *>(vl + kv_off<D>(t, ch)) = vr[j];
+            *reinterpret_cast<u32x4 *>(vl + v_off<D>(t, ch)) = vr[j];
         }
     };
 
@@ -148,7 +176,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
     __syncthreads();
 
     for (int tile = 0; tile < ntiles; ++tile) {
-        const uint16_t *kl = kv + (tile & 1) * 2 * C::TILE;
+        const uint16_t *kl = kv + (tile & 1) * C::STAGE;
         const uint16_t *vl = kl + C::TILE;
         const int t0 = tile * kTileTokens;
         if (n_my > 0) {
@@ -219,21 +247,20 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
                     }
                 }
             }
-            // O^T += V^T P^T; the V^T operand holds 4 consecutive tokens at one d
+            // O^T += V^T P^T; lane (g4, l16) needs the 4 tokens st*16 + 4*g4 + 0..3
+            // at d = dt*16 + l16, which one transposing read delivers when source
+            // lane s of the 16-lane group points at token +s/4, d-offset 4*(s%4).
 #pragma unroll
             for (int k = 0; k < kSubPerTile; ++k) {
                 if (k < nst) {
                     const int st = wt + k * Wt;
-                    const int tb = st * kSub + g4 * 4;
+                    const uint16_t *vsrc = vl + (st * kSub + g4 * 4 + (l16 >> 2)) * C::LDRV + 4 * (l16 & 3);
+                    bf16x4 vt[C::DT];
+#pragma unroll
+                    for (int dt = 0; dt < C::DT; ++dt) vt[dt] = lds_read_tr16(vsrc + dt * 16);
 #pragma unroll
                     for (int dt = 0; dt < C::DT; ++dt) {
-                        const int d = dt * 16 + l16;
-                        bf16x4 va;
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            const uint16_t bits = vl[kv_off<D>(tb + j, d >> 3) + (d & 7)];
-                            va[j] = __builtin_bit_cast(__bf16, bits);
-                        }
+                        const bf16x4 va = vt[dt];
                         acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0][k], acc[0][dt], 0, 0, 0);
                         if (MAXC > 1 && n_my > 1)
                             acc[MAXC - 1][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
@@ -341,6 +368,13 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) 
     if (a.lse && lane == 0) a.lse[idx] = (Mx + fast_log2(L)) * kLn2;
 }
 
+__global__ __launch_bounds__(kThreads) void plan_fetch_kernel(const u32x4 *__restrict__ src,
+                                                              u32x4 *__restrict__ dst, int64_t n) {
+    const int64_t step = static_cast<int64_t>(gridDim.x) * kThreads;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n; i += step)
+        dst[i] = src[i];
+}
+
 template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
     // The two-column-tile variant serves every item; with the LDS tile sizes
@@ -358,6 +392,16 @@ hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
 }
 
 }  // namespace
+
+hipError_t launch_plan_fetch(const void *host_src, void *dst, size_t bytes, hipStream_t stream) {
+    if (bytes % 16 != 0) return hipErrorInvalidValue;
+    const int64_t n = static_cast<int64_t>(bytes / 16);
+    if (n == 0) return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((n + kThreads - 1) / kThreads, 256);
+    hipLaunchKernelGGL(plan_fetch_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream,
+                       static_cast<const u32x4 *>(host_src), static_cast<u32x4 *>(dst), n);
+    return hipGetLastError();
+}
 
 hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream) {
     switch (a.D) {

@@ -19,10 +19,17 @@ struct DecodeArgs {
     float *pm, *pl, *pacc;      // workspace: partial max (log2 units), sum, weighted values
     int32_t n_items;            // work items in the list
     int32_t P, G, Hq, Hkv, r, D;
+    int32_t kv_layout;          // RL_KV_TOKEN_MAJOR or RL_KV_HEAD_MAJOR
+    int64_t prefix_rows, suffix_rows;
     float score_scale_log2;     // softmax_scale * log2(e)
 };
 
 hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
+
+// Copies `bytes` (a multiple of 16) from device-mapped pinned host memory to
+// device memory with a kernel on `stream`, so the work list reaches the
+// workspace without a hand-off between the copy engine and the compute queue.
+hipError_t launch_plan_fetch(const void *host_src, void *dst, size_t bytes, hipStream_t stream);
 
 struct LogprobArgs {
     const uint16_t *hidden;     // [R, H]

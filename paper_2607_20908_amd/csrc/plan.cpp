@@ -29,10 +29,27 @@ int64_t round_up16(int64_t x) { return (x + 15) / 16 * 16; }
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Clears a plan but keeps the capacity of its vectors.
+void reset(DecodePlan *pl) {
+    std::vector<rl_plan_item> items = std::move(pl->items);
+    std::vector<DevItem> dev = std::move(pl->dev_items), tmp = std::move(pl->tmp_items);
+    std::vector<DevUnit> pu = std::move(pl->prefix_units), su = std::move(pl->suffix_units);
+    std::vector<uint64_t> k1 = std::move(pl->tmp_keys), k2 = std::move(pl->tmp_keys2);
+    *pl = DecodePlan{};
+    items.clear(); dev.clear(); tmp.clear(); pu.clear(); su.clear(); k1.clear(); k2.clear();
+    pl->items = std::move(items);
+    pl->dev_items = std::move(dev);
+    pl->tmp_items = std::move(tmp);
+    pl->prefix_units = std::move(pu);
+    pl->suffix_units = std::move(su);
+    pl->tmp_keys = std::move(k1);
+    pl->tmp_keys2 = std::move(k2);
+}
+
 }  // namespace
 
 rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
-                      DecodePlan *plan, std::string *err) {
+                      DecodePlan *plan, std::string *err, PlanDetail detail) {
     if (!shape) return fail(err, RL_ERR_NULL_POINTER, "shape is NULL");
     if (!lens) return fail(err, RL_ERR_NULL_POINTER, "lens is NULL");
     const rl_decode_shape &sh = *shape;
@@ -46,6 +63,8 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
         return fail(err, RL_ERR_INVALID_SHAPE, "softmax_scale must be finite and > 0");
     if (sh.split_tokens < 0 || (sh.split_tokens > 0 && (sh.split_tokens < 16 || sh.split_tokens % 16)))
         return fail(err, RL_ERR_INVALID_SHAPE, "split_tokens must be 0 or a positive multiple of 16");
+    if (sh.kv_layout != RL_KV_TOKEN_MAJOR && sh.kv_layout != RL_KV_HEAD_MAJOR)
+        return fail(err, RL_ERR_INVALID_SHAPE, "kv_layout must be RL_KV_TOKEN_MAJOR or RL_KV_HEAD_MAJOR");
     if (sh.head_dim <= 0) return fail(err, RL_ERR_INVALID_SHAPE, "head_dim must be > 0");
     if (sh.head_dim != 64 && sh.head_dim != 128)
         return fail(err, RL_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
@@ -53,7 +72,7 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
         return fail(err, RL_ERR_INVALID_SHAPE, "row counts must be >= 0");
 
     DecodePlan &pl = *plan;
-    pl = DecodePlan{};
+    reset(&pl);
     pl.P = sh.num_prompts;
     pl.G = sh.group_size;
     pl.Hq = sh.num_q_heads;
@@ -61,6 +80,9 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     pl.D = sh.head_dim;
     pl.r = sh.num_q_heads / sh.num_kv_heads;
     pl.scale = sh.softmax_scale;
+    pl.kv_layout = sh.kv_layout;
+    pl.prefix_rows = lens->prefix_rows;
+    pl.suffix_rows = lens->suffix_rows;
     const int64_t P = pl.P, G = pl.G, S = P * G, Hkv = pl.Hkv, r = pl.r;
     if (S > INT32_MAX / 2 || S * pl.Hq > INT32_MAX)
         return fail(err, RL_ERR_UNSUPPORTED, "too many sequences x heads");
@@ -106,79 +128,127 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     pl.split_prefix = static_cast<int32_t>(cp);
     pl.split_suffix = static_cast<int32_t>(cs);
 
-    // --- items in creation order, partial rows in unit order ---------------
-    std::vector<rl_plan_item> items;
-    std::vector<int64_t> item_prow;
+    // --- unit tables; partial rows in unit order ------------------------------
+    // A unit of L tokens splits into n = ceil(L / C) chunks of b = ceil(L / n)
+    // tokens rounded up to 16 (the last one shorter), each chunk into
+    // ceil(M / 128) items of at most 128 query rows.
     pl.prefix_units.assign(P * Hkv, DevUnit{0, 0, 0});
     pl.suffix_units.assign(S * Hkv, DevUnit{0, 0, 0});
-    int64_t prow = 0;
-    auto add_unit = [&](int32_t kind, int32_t unit, int32_t kh, int64_t L, int64_t C,
-                        int64_t M, DevUnit *du) {
+    int64_t prow = 0, n_items = 0;
+    auto size_unit = [&](int64_t L, int64_t C, int64_t M, DevUnit *du) {
         du->base = prow;
-        if (L == 0) { du->nchunks = 0; return; }
-        const int64_t n = ceil_div(L, C);
-        const int64_t b = round_up16(ceil_div(L, n));
+        const int64_t n = L == 0 ? 0 : ceil_div(L, C);
         du->nchunks = static_cast<int32_t>(n);
-        for (int64_t c = 0; c < n; ++c) {
-            const int64_t beg = c * b, cnt = std::min(b, L - beg);
-            for (int64_t rb = 0; rb < M; rb += kMaxItemRows) {
-                rl_plan_item it{};
-                it.kind = kind;
-                it.unit = unit;
-                it.kv_head = kh;
-                it.chunk = static_cast<int32_t>(c);
-                it.tok_begin = beg;
-                it.tok_count = static_cast<int32_t>(cnt);
-                it.row_begin = static_cast<int32_t>(rb);
-                it.row_count = static_cast<int32_t>(std::min<int64_t>(kMaxItemRows, M - rb));
-                items.push_back(it);
-                item_prow.push_back(prow + c * M + rb);
-            }
-        }
         prow += n * M;
+        n_items += n * ceil_div(M, kMaxItemRows);
     };
     for (int64_t p = 0; p < P; ++p)
         for (int64_t kh = 0; kh < Hkv; ++kh)
-            add_unit(0, (int32_t)p, (int32_t)kh, lens->prefix_len[p], cp, Mp,
-                     &pl.prefix_units[p * Hkv + kh]);
+            size_unit(lens->prefix_len[p], cp, Mp, &pl.prefix_units[p * Hkv + kh]);
     for (int64_t s = 0; s < S; ++s)
         for (int64_t kh = 0; kh < Hkv; ++kh)
-            add_unit(1, (int32_t)s, (int32_t)kh, lens->suffix_len[s], cs, r,
-                     &pl.suffix_units[s * Hkv + kh]);
+            size_unit(lens->suffix_len[s], cs, r, &pl.suffix_units[s * Hkv + kh]);
     pl.partial_rows = prow;
-
-    // --- launch order: longest work first (stable) -------------------------
-    const int64_t kv_bytes_per_tok = 4LL * pl.D;              // K + V, bf16
-    const int64_t partial_bytes_per_row = 2LL * (8 + 4LL * pl.D);  // written, then read
-    std::vector<int64_t> cost(items.size());
-    for (size_t i = 0; i < items.size(); ++i)
-        cost[i] = items[i].tok_count * kv_bytes_per_tok + items[i].row_count * partial_bytes_per_row;
-    std::vector<size_t> order(items.size());
-    std::iota(order.begin(), order.end(), 0);
-    std::stable_sort(order.begin(), order.end(),
-                     [&](size_t a, size_t b) { return cost[a] > cost[b]; });
-    pl.items.reserve(items.size());
-    pl.dev_items.reserve(items.size());
-    for (size_t i : order) {
-        const rl_plan_item &it = items[i];
-        pl.items.push_back(it);
-        DevItem d{};
-        const int64_t start = it.kind == 0 ? lens->prefix_start[it.unit] : lens->suffix_start[it.unit];
-        d.kv_row0 = start + it.tok_begin;
-        d.partial_row0 = item_prow[i];
-        d.ntok = it.tok_count;
-        d.kind_kh = it.kv_head | (it.kind << 16);
-        d.unit = it.unit;
-        d.row_begin = it.row_begin;
-        pl.dev_items.push_back(d);
-    }
-    if (pl.dev_items.size() > static_cast<size_t>(INT32_MAX))
+    pl.n_items = n_items;
+    if (n_items > static_cast<int64_t>(INT32_MAX))
         return fail(err, RL_ERR_UNSUPPORTED, "too many work items");
+
+    if (detail != PlanDetail::kSizes) {
+        // --- items in creation order with their cost -----------------------------
+        const uint64_t kv_bytes_per_tok = 4ull * pl.D;                // K + V, bf16
+        const uint64_t partial_bytes_per_row = 2ull * (8 + 4ull * pl.D);  // written, then read
+        std::vector<DevItem> &tmp = pl.tmp_items;
+        std::vector<uint64_t> &key = pl.tmp_keys;
+        tmp.resize(static_cast<size_t>(n_items));
+        key.resize(static_cast<size_t>(n_items));
+        size_t w = 0;
+        uint64_t max_cost = 0;
+        auto add_items = [&](int32_t kind, int32_t unit, int32_t kh, int64_t start, int64_t L,
+                             int64_t M, const DevUnit &du) {
+            const int64_t n = du.nchunks;
+            if (n == 0) return;
+            const int64_t b = round_up16(ceil_div(L, n));
+            for (int64_t c = 0; c < n; ++c) {
+                const int64_t beg = c * b, cnt = std::min(b, L - beg);
+                for (int64_t rb = 0; rb < M; rb += kMaxItemRows) {
+                    const int64_t rows = std::min<int64_t>(kMaxItemRows, M - rb);
+                    DevItem &d = tmp[w];
+                    d.kv_row0 = start + beg;
+                    d.partial_row0 = du.base + c * M + rb;
+                    d.ntok = static_cast<int32_t>(cnt);
+                    d.kind_kh = kh | (kind << 16);
+                    d.unit = unit;
+                    d.row_begin = static_cast<int32_t>(rb);
+                    const uint64_t cost = static_cast<uint64_t>(cnt) * kv_bytes_per_tok +
+                                          static_cast<uint64_t>(rows) * partial_bytes_per_row;
+                    key[w] = cost;
+                    max_cost = std::max(max_cost, cost);
+                    ++w;
+                }
+            }
+        };
+        for (int64_t p = 0; p < P; ++p)
+            for (int64_t kh = 0; kh < Hkv; ++kh)
+                add_items(0, (int32_t)p, (int32_t)kh, lens->prefix_start[p], lens->prefix_len[p], Mp,
+                          pl.prefix_units[p * Hkv + kh]);
+        for (int64_t s = 0; s < S; ++s)
+            for (int64_t kh = 0; kh < Hkv; ++kh)
+                add_items(1, (int32_t)s, (int32_t)kh, lens->suffix_start[s], lens->suffix_len[s], r,
+                          pl.suffix_units[s * Hkv + kh]);
+
+        // --- launch order: longest work first, ties in creation order ------------
+        // Stable LSD radix sort of (max_cost - cost) in 8-bit digits; the item
+        // index rides in the low 32 bits of each key.
+        std::vector<uint64_t> &k2 = pl.tmp_keys2;
+        k2.resize(key.size());
+        int digits = 0;
+        for (uint64_t m = max_cost; m; m >>= 8) ++digits;
+        if (digits > 4) {
+            // costs above 2^32 (a split of billions of tokens): fall back to a
+            // comparison sort on the full cost
+            std::vector<uint64_t> cost(key);
+            for (size_t i = 0; i < key.size(); ++i) key[i] = i;
+            std::stable_sort(key.begin(), key.end(),
+                             [&](uint64_t x, uint64_t y) { return cost[x] > cost[y]; });
+        } else {
+            for (size_t i = 0; i < key.size(); ++i) key[i] = ((max_cost - key[i]) << 32) | i;
+            for (int d = 0; d < digits; ++d) {
+                size_t count[257] = {0};
+                const int sh8 = 32 + 8 * d;
+                for (uint64_t v : key) ++count[((v >> sh8) & 255) + 1];
+                for (int i = 0; i < 256; ++i) count[i + 1] += count[i];
+                for (uint64_t v : key) k2[count[(v >> sh8) & 255]++] = v;
+                key.swap(k2);
+            }
+        }
+        pl.dev_items.resize(key.size());
+        for (size_t i = 0; i < key.size(); ++i) pl.dev_items[i] = tmp[key[i] & 0xffffffffu];
+        if (detail == PlanDetail::kDebug) {
+            pl.items.resize(pl.dev_items.size());
+            for (size_t i = 0; i < pl.dev_items.size(); ++i) {
+                const DevItem &d = pl.dev_items[i];
+                rl_plan_item &it = pl.items[i];
+                it = rl_plan_item{};
+                it.kind = (d.kind_kh >> 16) & 1;
+                it.unit = d.unit;
+                it.kv_head = d.kind_kh & 0xffff;
+                const DevUnit &du = it.kind == 0 ? pl.prefix_units[(int64_t)d.unit * Hkv + it.kv_head]
+                                                 : pl.suffix_units[(int64_t)d.unit * Hkv + it.kv_head];
+                const int64_t M = it.kind == 0 ? Mp : r;
+                const int64_t start = it.kind == 0 ? lens->prefix_start[d.unit] : lens->suffix_start[d.unit];
+                it.chunk = static_cast<int32_t>((d.partial_row0 - du.base) / M);
+                it.tok_begin = d.kv_row0 - start;
+                it.tok_count = d.ntok;
+                it.row_begin = d.row_begin;
+                it.row_count = static_cast<int32_t>(std::min<int64_t>(kMaxItemRows, M - d.row_begin));
+            }
+        }
+    }
 
     // --- workspace layout --------------------------------------------------
     size_t off = 0;
     pl.off_items = off;
-    off = align_up(off + pl.dev_items.size() * sizeof(DevItem), 256);
+    off = align_up(off + static_cast<size_t>(n_items) * sizeof(DevItem), 256);
     pl.off_prefix_units = off;
     off = align_up(off + pl.prefix_units.size() * sizeof(DevUnit), 256);
     pl.off_suffix_units = off;

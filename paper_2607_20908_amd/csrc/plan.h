@@ -47,12 +47,20 @@ struct DevUnit {
 };
 static_assert(sizeof(DevUnit) == 16, "DevUnit layout");
 
+// How much of the plan to build: the workspace size needs only the counts;
+// a launch needs the device work list; the debug export also wants the
+// rl_plan_item view of it.
+enum class PlanDetail { kSizes, kDevice, kDebug };
+
 struct DecodePlan {
     // problem
     int32_t P = 0, G = 0, Hq = 0, Hkv = 0, D = 0, r = 0;
     float scale = 0.f;
+    int32_t kv_layout = RL_KV_TOKEN_MAJOR;
+    int64_t prefix_rows = 0, suffix_rows = 0;
     int32_t split_prefix = 0, split_suffix = 0;  // chunk sizes used
-    // work list in launch order
+    // work list in launch order (items: kDebug only; dev_items: kDevice and up)
+    int64_t n_items = 0;
     std::vector<rl_plan_item> items;
     std::vector<DevItem> dev_items;
     std::vector<DevUnit> prefix_units;   // [P * Hkv]
@@ -63,12 +71,17 @@ struct DecodePlan {
     size_t off_m = 0, off_l = 0, off_acc = 0;
     size_t meta_bytes = 0;   // items + unit tables (uploaded from the host)
     size_t total_bytes = 0;
+    // scratch reused across calls when the same plan object is planned again
+    std::vector<DevItem> tmp_items;
+    std::vector<uint64_t> tmp_keys, tmp_keys2;
 };
 
-// Validates shape and lengths (not device pointers) and builds the plan.
+// Validates shape and lengths (not device pointers) and builds the plan to the
+// requested detail.  The plan object's vectors keep their capacity between
+// calls, so a caller that reuses one object plans without allocating.
 // On failure returns the status and sets *err.
 rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
-                      DecodePlan *plan, std::string *err);
+                      DecodePlan *plan, std::string *err, PlanDetail detail = PlanDetail::kDevice);
 
 // Validates the device pointers of a decode call against a built plan.
 rl_status check_decode_ptrs(const DecodePlan &plan, const rl_decode_lens *lens,

@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 1
+    assert lib.rl_abi_version() == 2
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -50,14 +50,14 @@ def test_status_strings_and_version():
 # ---------------------------------------------------------------- decode
 def decode_call(P=2, G=3, Hq=4, Hkv=2, D=128, scale=0.125, split=0, lp=None, ls=None,
                 prefix_rows=None, suffix_rows=None, ptrs=None, ws=None, ws_bytes=1 << 30,
-                null_shape=False, null_lens=False, null_ptrs=False, starts=None):
+                null_shape=False, null_lens=False, null_ptrs=False, starts=None, layout=0):
     lib = rk.lib()
     S = P * G
     lp = np.full(P, 5, np.int32) if lp is None else np.asarray(lp, np.int32)
     ls = np.full(S, 3, np.int32) if ls is None else np.asarray(ls, np.int32)
     ps = (np.arange(P, dtype=np.int64) * 5) if starts is None else np.asarray(starts[0], np.int64)
     ss = (np.arange(S, dtype=np.int64) * 3) if starts is None else np.asarray(starts[1], np.int64)
-    shape = rk.DecodeShape(P, G, Hq, Hkv, D, scale, split)
+    shape = rk.DecodeShape(P, G, Hq, Hkv, D, scale, split, layout)
     lens = rk.DecodeLens(ps.ctypes.data, lp.ctypes.data, ss.ctypes.data, ls.ctypes.data,
                          5 * P if prefix_rows is None else prefix_rows,
                          3 * S if suffix_rows is None else suffix_rows)
@@ -96,6 +96,8 @@ def decode_call(P=2, G=3, Hq=4, Hkv=2, D=128, scale=0.125, split=0, lp=None, ls=
     (dict(suffix_rows=17), SHAPE),            # candidate 5 needs rows [15, 18)
     (dict(prefix_rows=-1), SHAPE),
     (dict(starts=([0, -5], [0, 3, 6, 9, 12, 15])), SHAPE),
+    (dict(layout=2), SHAPE),
+    (dict(layout=-1), SHAPE),
     (dict(D=96), UNSUP),
     (dict(D=256), UNSUP),
     (dict(D=0), SHAPE),

@@ -18,12 +18,16 @@ from gpu_util import (ATTN_LSE_TOL, ATTN_OUT_TOL, decode_host_case, dev, max_abs
 pytestmark = pytest.mark.gpu
 
 
-def run_gpu(c, scale, split=0, workspace=None):
-    t = {k: to_dev(c[k]) for k in ("q", "k_prefix", "v_prefix", "k_suffix", "v_suffix")}
+def run_gpu(c, scale, split=0, workspace=None, layout="token"):
+    """GPU call on host-side token-major bits; layout "head" transposes the KV first."""
+    def kv(bits):
+        return to_dev(np.ascontiguousarray(np.transpose(bits, (1, 0, 2))) if layout == "head" else bits)
+    t = {k: kv(c[k]) for k in ("k_prefix", "v_prefix", "k_suffix", "v_suffix")}
+    t["q"] = to_dev(c["q"])
     out, lse = rk.decode_attn(t["q"], t["k_prefix"], t["v_prefix"], t["k_suffix"], t["v_suffix"],
                               c["prefix_start"], c["prefix_len"], c["suffix_start"], c["suffix_len"],
                               c["group_size"], scale=scale, split_tokens=split, return_lse=True,
-                              workspace=workspace)
+                              workspace=workspace, kv_layout=layout)
     torch.cuda.synchronize()
     return out.float().cpu().numpy(), lse.cpu().numpy(), W.bf16_bits(out)
 
@@ -34,9 +38,9 @@ def run_oracle(c, scale):
                               c["group_size"], scale)
 
 
-def check(c, scale, split=0, what=""):
-    say(f"decode parity {what} split={split}")
-    o, l, _ = run_gpu(c, scale, split)
+def check(c, scale, split=0, what="", layout="token"):
+    say(f"decode parity {what} split={split} layout={layout}")
+    o, l, _ = run_gpu(c, scale, split, layout=layout)
     ro, rl = run_oracle(c, scale)
     eo, el = max_abs(o, ro), max_abs(l, rl)
     assert eo <= ATTN_OUT_TOL, f"{what}: out max-abs {eo}"
@@ -54,15 +58,16 @@ def test_tiny_config():
     check(c, x.scale, what="tiny config")
 
 
+@pytest.mark.parametrize("layout", ["token", "head"])
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("split", [0, 16, 48, 64, 112])
-def test_ragged_multi_tile(D, split):
+def test_ragged_multi_tile(D, split, layout):
     # several 64-token tiles per unit, ragged tails, empty prefixes and suffixes
     P, G, Hq, Hkv = 3, 4, 16, 4
     lp = [300, 0, 129]
     ls = [200, 1, 0, 63, 64, 65, 0, 17, 250, 3, 128, 31]
     c = decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=D + split, gap=3)
-    check(c, 1.0 / math.sqrt(D), split, f"ragged D={D}")
+    check(c, 1.0 / math.sqrt(D), split, f"ragged D={D}", layout)
 
 
 @pytest.mark.parametrize("G,Hq,Hkv", [(16, 64, 8),   # 128 query rows per kv head: 2 column tiles per wave
@@ -76,7 +81,7 @@ def test_group_shapes(G, Hq, Hkv):
     ls = rng.integers(0, 160, P * G)
     c = decode_host_case(P, G, Hq, Hkv, 128, lp, ls, seed=G + Hq, gap=1)
     check(c, 1.0 / math.sqrt(128), 0, f"G={G} Hq={Hq} Hkv={Hkv}")
-    check(c, 1.0 / math.sqrt(128), 32, f"G={G} Hq={Hq} Hkv={Hkv}")
+    check(c, 1.0 / math.sqrt(128), 32, f"G={G} Hq={Hq} Hkv={Hkv}", "head")
 
 
 def test_peaky_scores():
@@ -93,11 +98,13 @@ def test_nan_poisoned_padding_and_workspace():
                                          c["suffix_start"], c["suffix_len"],
                                          c["k_prefix"].shape[0], c["k_suffix"].shape[0], scale)
     ws = torch.full((need // 4,), float("nan"), dtype=torch.float32, device=dev()).view(torch.uint8)
-    say("decode poisoned padding + workspace")
-    o, l, _ = run_gpu(c, scale, 0, workspace=ws)
-    assert np.isfinite(o).all() and np.isfinite(l).all()
     ro, rl = run_oracle(c, scale)
-    assert max_abs(o, ro) <= ATTN_OUT_TOL and max_abs(l, rl) <= ATTN_LSE_TOL
+    for layout in ("token", "head"):
+        say(f"decode poisoned padding + workspace, layout {layout}")
+        ws.view(torch.float32).fill_(float("nan"))
+        o, l, _ = run_gpu(c, scale, 0, workspace=ws, layout=layout)
+        assert np.isfinite(o).all() and np.isfinite(l).all()
+        assert max_abs(o, ro) <= ATTN_OUT_TOL and max_abs(l, rl) <= ATTN_LSE_TOL
 
 
 def test_bitwise_deterministic():
@@ -148,9 +155,9 @@ def test_one_hot_probe_bit_exact():
     bits = lambda a: W.bf16_bits(torch.from_numpy(a).to(torch.bfloat16))
     c.update(q=bits(q), k_prefix=bits(kp), v_prefix=bits(vp), k_suffix=bits(ks), v_suffix=bits(vs))
     say("decode one-hot probe")
-    for split in (0, 16, 64):
-        _, _, out_bits = run_gpu(c, 1.0, split)
-        assert np.array_equal(out_bits, bits(expect)), f"one-hot probe mismatch (split {split})"
+    for split, layout in ((0, "token"), (16, "token"), (64, "token"), (0, "head"), (16, "head")):
+        _, _, out_bits = run_gpu(c, 1.0, split, layout=layout)
+        assert np.array_equal(out_bits, bits(expect)), f"one-hot probe mismatch (split {split}, {layout})"
 
 
 def test_length_probe_exact():
@@ -164,7 +171,7 @@ def test_length_probe_exact():
     c["k_prefix"] = np.zeros_like(c["k_prefix"])
     c["k_suffix"] = np.zeros_like(c["k_suffix"])
     say("decode length probe")
-    o, l, _ = run_gpu(c, 1.0 / 8, 48)
+    o, l, _ = run_gpu(c, 1.0 / 8, 48, layout="head")
     T = np.array([lp[s // G] + ls[s] for s in range(P * G)])
     for s in range(P * G):
         if T[s] == 0:
@@ -211,22 +218,25 @@ def test_empty_batch_noop():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["8b", "32b", "longctx"])
-def test_full_size_workloads(name):
-    """The full-size decode workloads in the configuration the bench times."""
+@pytest.mark.parametrize("name,layout", [("8b", "head"), ("32b", "head"), ("longctx", "head"),
+                                         ("8b", "token")])
+def test_full_size_workloads(name, layout):
+    """The full-size decode workloads in the configuration the bench times (head-major KV),
+    and the 8B-class step in the token-major layout."""
     cfg = W.DECODE_CONFIGS[name]
-    say(f"decode full-size {name}: generating")
-    x = W.make_decode_inputs(cfg, dev())
-    say(f"decode full-size {name}: gpu")
+    say(f"decode full-size {name} {layout}: generating")
+    x = W.make_decode_inputs(cfg, dev(), kv_layout=layout)
+    say(f"decode full-size {name} {layout}: gpu")
     out, lse = rk.decode_attn(x.q, x.k_prefix, x.v_prefix, x.k_suffix, x.v_suffix,
                               x.prefix_start, x.prefix_len, x.suffix_start, x.suffix_len,
-                              cfg.group_size, scale=x.scale, return_lse=True)
+                              cfg.group_size, scale=x.scale, return_lse=True, kv_layout=layout)
     torch.cuda.synchronize()
     o = out.float().cpu().numpy()
     l = lse.cpu().numpy()
-    say(f"decode full-size {name}: oracle")
-    ro, rl = oracle.decode_attn(W.bf16_bits(x.q), W.bf16_bits(x.k_prefix), W.bf16_bits(x.v_prefix),
-                                W.bf16_bits(x.k_suffix), W.bf16_bits(x.v_suffix),
+    say(f"decode full-size {name} {layout}: oracle")
+    tm = x.token_major
+    ro, rl = oracle.decode_attn(W.bf16_bits(x.q), W.bf16_bits(tm(x.k_prefix)), W.bf16_bits(tm(x.v_prefix)),
+                                W.bf16_bits(tm(x.k_suffix)), W.bf16_bits(tm(x.v_suffix)),
                                 x.prefix_start, x.prefix_len, x.suffix_start, x.suffix_len,
                                 cfg.group_size, x.scale)
     eo, el = max_abs(o, ro), max_abs(l, rl)

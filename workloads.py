@@ -16,7 +16,9 @@ below; the paper's own datasets are not used (they stand in only as shapes).
 Layout conventions (shared with the C ABI):
   q        bf16 [S, Hq, D]            S = P*G, sequence s = p*G + g
   k/v_pfx  bf16 [prefix_rows, Hkv, D] prompt p owns rows [prefix_start[p], +Lp[p])
+           (or [Hkv, prefix_rows, D] with kv_layout="head")
   k/v_sfx  bf16 [suffix_rows, Hkv, D] candidate s owns rows [suffix_start[s], +Ls[s])
+           (or [Hkv, suffix_rows, D] with kv_layout="head")
   hidden   bf16 [R, H]
   w_lm     bf16 [V, H]                row v produces logit v (nn.Linear layout)
   target   int32 [R]                  -1 masks a row
@@ -122,6 +124,11 @@ class DecodeInputs:
     suffix_start: np.ndarray   # int64 [S]
     suffix_len: np.ndarray     # int32 [S]
     scale: float
+    kv_layout: str = "token"
+
+    def token_major(self, t: torch.Tensor) -> torch.Tensor:
+        """A KV tensor of this input as [rows, Hkv, D]."""
+        return t.transpose(0, 1).contiguous() if self.kv_layout == "head" else t
 
     @property
     def P(self): return self.cfg.num_prompts
@@ -140,7 +147,10 @@ def packed_starts(lengths: np.ndarray) -> np.ndarray:
 
 def make_decode_inputs(cfg: DecodeConfig, device="cpu", seed: int = 0,
                        suffix_len: Optional[np.ndarray] = None,
-                       prefix_len: Optional[np.ndarray] = None) -> DecodeInputs:
+                       prefix_len: Optional[np.ndarray] = None,
+                       kv_layout: str = "token") -> DecodeInputs:
+    """kv_layout "token": KV tensors [rows, Hkv, D]; "head": [Hkv, rows, D] holding
+    the same values (the token-major draw, transposed)."""
     P, G, Hq, Hkv, D = cfg.num_prompts, cfg.group_size, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
     S = P * G
     lp = (np.full(P, cfg.prefix_len, dtype=np.int32) if prefix_len is None
@@ -153,7 +163,11 @@ def make_decode_inputs(cfg: DecodeConfig, device="cpu", seed: int = 0,
     vp = _randn_bf16((prow, Hkv, D), seed + _SUB["vp"], device)
     ks = _randn_bf16((srow, Hkv, D), seed + _SUB["ks"], device)
     vs = _randn_bf16((srow, Hkv, D), seed + _SUB["vs"], device)
-    return DecodeInputs(cfg, q, kp, vp, ks, vs, ps, lp, ss, ls, cfg.softmax_scale)
+    if kv_layout == "head":
+        kp, vp, ks, vs = (t.transpose(0, 1).contiguous() for t in (kp, vp, ks, vs))
+    elif kv_layout != "token":
+        raise ValueError(kv_layout)
+    return DecodeInputs(cfg, q, kp, vp, ks, vs, ps, lp, ss, ls, cfg.softmax_scale, kv_layout)
 
 
 @dataclasses.dataclass
