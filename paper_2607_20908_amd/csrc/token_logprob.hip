@@ -1,19 +1,21 @@
 // Fused lm-head token log-prob for gfx950.
 //
-// Tile kernel: one workgroup (8 wave64s, 2 x 4, two per SIMD) computes the
-// 256 x 256 logit tile  Z^T = W_tile * hidden_tile^T  (vocab entries on the M
-// side, token rows on the N side); each wave owns 128 vocab x 64 rows as
-// 4 x 2 MFMA 32x32x16 bf16 tiles with fp32 accumulation.  Both operands are
-// hidden-contiguous.  The hidden dimension streams through two LDS stages of
-// 64 entries (XOR-swizzled 16-byte chunks); global loads run two stages ahead
-// in two alternating register sets, so each load has two compute phases to
-// land.  Rows past the vocabulary or the batch re-read the last valid row:
+// Tile kernel: one workgroup (4 wave64s, one per SIMD) computes the 256 x 256
+// logit tile  Z^T = W_tile * hidden_tile^T  (vocab entries on the M side,
+// token rows on the N side); each wave owns 128 vocab x 128 rows as 4 x 4
+// MFMA 32x32x16 bf16 tiles whose fp32 accumulators live in the AGPRs.  Both
+// operands are hidden-contiguous.  The hidden dimension streams through two
+// LDS stages of 64 entries, filled by direct global->LDS loads (no register
+// staging): the loads for stage s+2 are issued right after the barrier that
+// frees stage s's buffer, interleaved with the MFMAs of stage s's last k-step,
+// and the fragments of k-step q+1 are read from LDS while the MFMAs of k-step
+// q run.  Rows past the vocabulary or the batch re-read the last valid row:
 // their logits are masked (vocab) or never written (rows).
-// The epilogue never stores the logits: per token row it
-// takes the max and the sum of exp2 over the tile's vocab entries (the vocab
-// index lives in the accumulator registers, so the reduction is in-lane plus
-// one cross-half shuffle), picks out the target's logit when the target falls
-// in the tile, and writes one (max, sum) partial per (vocab tile, row).
+// The epilogue never stores the logits: per token row it takes the max and
+// the sum of exp2 over the tile's vocab entries (the vocab index lives in the
+// accumulator registers, so the reduction is in-lane plus one cross-half
+// shuffle), picks out the target's logit when the target falls in the tile,
+// and writes one (max, sum) partial per (vocab tile, row).
 // Combine kernel: per row, merge the partials of all vocab tiles into the
 // log-sum-exp and subtract it from the target logit.
 #include "device_common.h"
@@ -25,13 +27,17 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kK = kHiddenStep;                 // 64 hidden entries per LDS stage
 constexpr int kTileElems = kVocabTile * kK;     // bf16 elements per operand per stage
+constexpr int kStageElems = 2 * kTileElems;     // W tile then hidden tile
 static_assert(kVocabTile == kRowTile, "square tiles assumed below");
+constexpr int kTileThreads = 256;               // 4 waves
+constexpr int kBlocksPerWave = kTileElems / 512 / 4;   // 1 KB load blocks per wave per operand per stage
+static_assert(kBlocksPerWave == 8, "staging layout");
 
 // Element offset of 16-byte chunk c (0..7) of tile row `row` in a stage buffer.
 // Rows are 128 bytes, so two rows share one 256-byte window of the 64 LDS
 // banks; XOR-ing the chunk with row bits 1..3 gives the 16 rows that one
 // ds_read_b128 pass serves (same chunk, consecutive rows) 16 distinct 16-byte
-// slots of that window, and keeps the register-to-LDS stores conflict-free.
+// slots of that window.
 __device__ __forceinline__ int op_off(int row, int c) { return row * kK + ((c ^ ((row >> 1) & 7)) << 3); }
 
 // Maps the launch index to a (vocab tile, row tile).  The hardware hands
@@ -51,155 +57,204 @@ __device__ __forceinline__ void tile_of(int64_t b, int64_t nvt, int64_t nrt, int
     *vt = in / rows_in_group;
 }
 
-constexpr int kTileThreads = 512;
-constexpr int kLoadsPerOperand = kTileElems / 8 / kTileThreads;   // 16-byte chunks per thread
-static_assert(kLoadsPerOperand == 4, "staging layout");
+// 16 bytes global -> LDS, bypassing the registers.  Lane i of a wave writes
+// LDS bytes [base + 16 i, +16) (base in M0, wave-uniform), so one instruction
+// fills 1 KB contiguously.  Issued as inline assembly: the compiler then does
+// not know that it writes LDS and does not put a wait for all loads in flight
+// in front of every LDS read (it cannot tell the two stage buffers apart);
+// the kernel orders these loads against its LDS reads with explicit waits.
+__device__ __forceinline__ void load_lds16(const uint16_t *g, uint16_t *l) {
+    typedef __attribute__((address_space(3))) uint16_t lds_u16;
+    const uint32_t lds_addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l)));
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, off"
+        :
+        : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+        : "memory", "m0");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+// The global->LDS loads are tracked by this counter; the compiler does not see
+// when their LDS bytes are read, so the waits are explicit.
+template <int N>
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ void barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * 2 * kTileElems];   // [buf][W, hidden]
-    __shared__ float red[2][kRowTile][2];                                        // [vocab half][row][m, l]
+    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStageElems];   // [buf][W, hidden]
+    __shared__ float red[2][kRowTile][2];                                     // [vocab half][row][m, l]
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wv = wave & 1, wr = wave >> 1;     // vocab half (128 entries), row quarter (64 rows)
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;     // vocab half (128 entries), row half (128 rows)
     const int l32 = lane & 31, h2 = lane >> 5;
     int64_t vt, rt;
     tile_of(blockIdx.x, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
     const int64_t v0 = vt * kVocabTile, r0 = rt * kRowTile;
     const int64_t H = a.H;
+    const int nks = a.H / kK;
 
-    // ---- staging: per stage, 4 chunks of W and 4 of hidden per thread -------
-    // Rows past the vocabulary / the batch re-read the last valid row (the
-    // bounds are uniform; full tiles never clamp).
+    // ---- staging: each wave fills 8 blocks of 8 rows per operand per stage.
+    // Lane i of a block covers row 8*block + i/8 and LDS slot i%8 of that row,
+    // which holds chunk (i%8) ^ swizzle(row), so the LDS image is op_off's.
+    // Rows past the vocabulary / the batch re-read the last valid row.
     const uint16_t *wg = a.w + v0 * H;
     const uint16_t *hg = a.hidden + r0 * H;
     const int wlast = static_cast<int>(min(static_cast<int64_t>(kVocabTile - 1), a.V - 1 - v0));
     const int hlast = static_cast<int>(min(static_cast<int64_t>(kRowTile - 1), a.R - 1 - r0));
-    u32x4 ra0[kLoadsPerOperand], rb0[kLoadsPerOperand], ra1[kLoadsPerOperand], rb1[kLoadsPerOperand];
-    auto load_stage = [&](int ks, u32x4 *ra, u32x4 *rb) {
-        const int k0 = ks * kK;
+    // the swizzled chunk depends only on lane bits (row bits 1..3 = lane bits 4..5 and j)
+    auto issue = [&](int ks) {
+        uint16_t *st = smem + (ks & 1) * kStageElems;
+        const int64_t k0 = static_cast<int64_t>(ks) * kK;
 #pragma unroll
-        for (int j = 0; j < kLoadsPerOperand; ++j) {
-            const int idx = tid + j * kTileThreads;
-            const int row = idx >> 3, c = idx & 7;
-            ra[j] = *reinterpret_cast<const u32x4 *>(wg + min(row, wlast) * H + k0 + c * 8);
-            rb[j] = *reinterpret_cast<const u32x4 *>(hg + min(row, hlast) * H + k0 + c * 8);
-        }
-    };
-    auto store_stage = [&](int buf, const u32x4 *ra, const u32x4 *rb) {
-        uint16_t *as = smem + buf * 2 * kTileElems;
-        uint16_t *bs = as + kTileElems;
-#pragma unroll
-        for (int j = 0; j < kLoadsPerOperand; ++j) {
-            const int idx = tid + j * kTileThreads;
-            const int row = idx >> 3, c = idx & 7;
-            *reinterpret_cast<u32x4 *>(as + op_off(row, c)) = ra[j];
-            *reinterpret_cast<u32x4 *>(bs + op_off(row, c)) = rb[j];
+        for (int j = 0; j < kBlocksPerWave; ++j) {
+            const int blk = wave * kBlocksPerWave + j;
+            const int row = blk * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ ((row >> 1) & 7);
+            load_lds16(wg + min(row, wlast) * H + k0 + c * 8, st + blk * 512);
+            load_lds16(hg + min(row, hlast) * H + k0 + c * 8, st + kTileElems + blk * 512);
         }
     };
 
-    f32x16 acc[4][2];
+    f32x16 acc[4][4];
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) acc[tm][tn] = f32x16{};
-
-    auto compute_stage = [&](int buf) {
-        const uint16_t *as = smem + buf * 2 * kTileElems;
+        for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = f32x16{};
+    bf16x8 fa[2][4], fb[2][4];
+    auto read_frags = [&](int ks, int kq, int p) {
+        const uint16_t *as = smem + (ks & 1) * kStageElems;
         const uint16_t *bs = as + kTileElems;
+        const int c = kq * 2 + h2;
 #pragma unroll
-        for (int kq = 0; kq < kK / 16; ++kq) {
-            const int c = kq * 2 + h2;
-            bf16x8 af[4], bf[2];
+        for (int i = 0; i < 4; ++i) fa[p][i] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + i * 32 + l32, c));
 #pragma unroll
-            for (int tm = 0; tm < 4; ++tm)
-                af[tm] = *reinterpret_cast<const bf16x8 *>(as + op_off(wv * 128 + tm * 32 + l32, c));
+        for (int j = 0; j < 4; ++j) fb[p][j] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + j * 32 + l32, c));
+    };
+    auto mfma16 = [&](int p) {
 #pragma unroll
-            for (int tn = 0; tn < 2; ++tn)
-                bf[tn] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wr * 64 + tn * 32 + l32, c));
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int tm = 0; tm < 4; ++tm)
-#pragma unroll
-                for (int tn = 0; tn < 2; ++tn)
-                    acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bf[tn], acc[tm][tn], 0, 0, 0);
-        }
+            for (int j = 0; j < 4; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
     };
 
-    // Stage ks lives in LDS buffer ks % 2; odd stages pass through register set
-    // 0, even stages >= 2 through set 1, each loaded two stages ahead.
-    const int nk = a.H / kK;
-    load_stage(0, ra0, rb0);
-    store_stage(0, ra0, rb0);
-    if (nk > 1) load_stage(1, ra0, rb0);
-    if (nk > 2) load_stage(2, ra1, rb1);
-    __syncthreads();
-    for (int ks = 0; ks < nk; ks += 2) {
-        compute_stage(0);
-        if (ks + 1 < nk) {
-            store_stage(1, ra0, rb0);
-            if (ks + 3 < nk) load_stage(ks + 3, ra0, rb0);
-        }
-        __syncthreads();
-        if (ks + 1 < nk) {
-            compute_stage(1);
-            if (ks + 2 < nk) {
-                store_stage(0, ra1, rb1);
-                if (ks + 4 < nk) load_stage(ks + 4, ra1, rb1);
+    // Stage ks lives in LDS buffer ks % 2.  Loads past the last stage refill a
+    // buffer nobody reads any more (so the loop body has no branch and the
+    // scheduler can interleave loads, reads and MFMAs); the final wait makes
+    // sure none of them is still writing LDS when the epilogue starts.
+    issue(0);
+    issue(min(1, nks - 1));
+    wait_vm<2 * kBlocksPerWave>();               // stage 0 has landed
+    barrier();
+    read_frags(0, 0, 0);
+    for (int ks = 0; ks < nks; ++ks) {
+#pragma unroll
+        for (int kq = 0; kq < kK / 16 - 1; ++kq) {
+            read_frags(ks, kq + 1, (kq + 1) & 1);
+            mfma16(kq & 1);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
             }
-            __syncthreads();
+            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        }
+        // last k-step: stage ks+1 has landed and every wave is done reading
+        // stage ks, whose buffer takes stage ks+2
+        wait_vm<0>();
+        wait_lds();
+        barrier();
+        issue(min(ks + 2, nks - 1));
+        read_frags(ks + 1, 0, 0);
+        mfma16(1);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);   // global->LDS loads
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
     }
+    wait_vm<0>();
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- epilogue: per token row, max / sum of exp2 / target logit ---------
-    // acc[tm][tn][i] holds vocab v0 + wv*128 + tm*32 + 8*(i/4) + 4*h2 + i%4
-    // for token row r0 + wr*64 + tn*32 + l32.
+    // acc[tm][tn][i] holds vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4
+    // for token row r0 + wn*128 + tn*32 + l32.
     const float c2 = a.inv_temperature * kLog2e;
-    const int64_t vbase = v0 + wv * 128;
+    const int64_t vbase = v0 + wm * 128;
+    const bool full_vocab = vbase + 128 <= a.V;  // only the last vocab tile is masked
 #pragma unroll
-    for (int tn = 0; tn < 2; ++tn) {
-        const int64_t rr = r0 + wr * 64 + tn * 32 + l32;
-        // target logit, if the target lies in this wave's 128 vocab entries
+    for (int tn = 0; tn < 4; ++tn) {
+        const int row = wn * 128 + tn * 32 + l32;
+        const int64_t rr = r0 + row;
+        // the target's index among this wave's 128 vocab entries, shifted so
+        // that it compares against compile-time constants; -1 unless this
+        // lane's half of the accumulator rows (bit 2 of the index) holds it
+        int tsel = -1;
         if (rr < a.R) {
             const int64_t local = static_cast<int64_t>(a.target[rr]) - vbase;
-            if (local >= 0 && local < 128) {
-                const int tmt = static_cast<int>(local >> 5), rem = static_cast<int>(local & 31);
-                const int it = ((rem >> 3) << 2) | (rem & 3);
-                if (((rem >> 2) & 1) == h2) {
-                    float val = 0.f;
-#pragma unroll
-                    for (int tm = 0; tm < 4; ++tm)
-#pragma unroll
-                        for (int i = 0; i < 16; ++i)
-                            if (tm == tmt && i == it) val = acc[tm][tn][i];
-                    a.zt[rr] = val * a.inv_temperature;
-                }
-            }
+            if (local >= 0 && local < 128 && ((local >> 2) & 1) == h2) tsel = static_cast<int>(local) - 4 * h2;
         }
-        float mx = -INFINITY;
+        // one pass per 32-entry block: block max and sum, merged online into
+        // the row's (mx, sum); each accumulator register is read once
+        const int vlim = full_vocab ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
+        float mx = -INFINITY, sum = 0.f, zsel = 0.f;
 #pragma unroll
-        for (int tm = 0; tm < 4; ++tm)
+        for (int tm = 0; tm < 4; ++tm) {
+            const f32x16 z = acc[tm][tn];
+            float bm = -INFINITY;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int64_t v = vbase + tm * 32 + 8 * (i >> 2) + 4 * h2 + (i & 3);
-                const float x = v < a.V ? acc[tm][tn][i] * c2 : -INFINITY;
-                acc[tm][tn][i] = x;
-                mx = fmaxf(mx, x);
+                const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
+                bm = fmaxf(bm, loc < vlim ? z[i] : -INFINITY);
+                zsel = loc == tsel ? z[i] : zsel;
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mu = mx == -INFINITY ? 0.f : mx;
-        float sum = 0.f;
+            bm *= c2;                            // c2 > 0: scaling commutes with max
+            const float bmu = bm == -INFINITY ? 0.f : bm;
+            float bs = 0.f;
 #pragma unroll
-        for (int tm = 0; tm < 4; ++tm)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) sum += fast_exp2(acc[tm][tn][i] - mu);
-        sum += __shfl_xor(sum, 32, 64);
-        if (h2 == 0) {
-            red[wv][wr * 64 + tn * 32 + l32][0] = mx;
-            red[wv][wr * 64 + tn * 32 + l32][1] = sum;
+            for (int i = 0; i < 16; ++i) {
+                const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
+                bs += loc < vlim ? fast_exp2(z[i] * c2 - bmu) : 0.f;
+            }
+            // merge (bm, bs) into (mx, sum)
+            const float nm = fmaxf(mx, bm);
+            const float nmu = nm == -INFINITY ? 0.f : nm;
+            sum = sum * fast_exp2(mx - nmu) + bs * fast_exp2(bm - nmu);
+            mx = nm;
+            __builtin_amdgcn_sched_barrier(0);
         }
+        if (tsel >= 0) a.zt[rr] = zsel * a.inv_temperature;
+        // merge the two lane halves (same row, disjoint vocab entries)
+        {
+            const float om = __shfl_xor(mx, 32, 64), os = __shfl_xor(sum, 32, 64);
+            const float nm = fmaxf(mx, om);
+            const float nmu = nm == -INFINITY ? 0.f : nm;
+            sum = sum * fast_exp2(mx - nmu) + os * fast_exp2(om - nmu);
+            mx = nm;
+        }
+        if (h2 == 0) {
+            red[wm][row][0] = mx;
+            red[wm][row][1] = sum;
+        }
+        // keep each row block's accumulator copies local: hoisting the reads
+        // of all four blocks would need 256 more VGPRs
+        __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
-    if (tid < kRowTile) {
-        const int row = tid;
+    {
+        const int row = tid;                     // 256 threads, 256 rows
         const int64_t rr = r0 + row;
         if (rr < a.R) {
             const float m0 = red[0][row][0], m1 = red[1][row][0];
