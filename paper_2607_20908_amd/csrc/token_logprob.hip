@@ -174,15 +174,30 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         wait_vm<0>();
         wait_lds();
         barrier();
-        issue(min(ks + 2, nks - 1));
-        read_frags(ks + 1, 0, 0);
-        mfma16(1);
+        // eight groups of: one pair of global->LDS loads for stage ks+2, two
+        // MFMAs of this k-step, one fragment read of stage ks+1 (kept in this
+        // order: the loads are opaque to the scheduler)
+        {
+            const int ks2 = min(ks + 2, nks - 1);
+            uint16_t *st = smem + (ks2 & 1) * kStageElems;
+            const int64_t k0 = static_cast<int64_t>(ks2) * kK;
+            const uint16_t *as = smem + ((ks + 1) & 1) * kStageElems;
+            const uint16_t *bs = as + kTileElems;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);   // global->LDS loads
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            for (int g = 0; g < 8; ++g) {
+                const int blk = wave * kBlocksPerWave + g;
+                const int row = blk * 8 + (lane >> 3);
+                const int c = (lane & 7) ^ ((row >> 1) & 7);
+                load_lds16(wg + min(row, wlast) * H + k0 + c * 8, st + blk * 512);
+                load_lds16(hg + min(row, hlast) * H + k0 + c * 8, st + kTileElems + blk * 512);
+#pragma unroll
+                for (int m = 2 * g; m < 2 * g + 2; ++m)
+                    acc[m >> 2][m & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][m >> 2], fb[1][m & 3],
+                                                                                 acc[m >> 2][m & 3], 0, 0, 0);
+                if (g < 4) fa[0][g] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + g * 32 + l32, h2));
+                else fb[0][g - 4] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + (g - 4) * 32 + l32, h2));
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     }
     wait_vm<0>();
