@@ -27,7 +27,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kK = kHiddenStep;                 // 64 hidden entries per LDS stage
 constexpr int kTileElems = kVocabTile * kK;     // bf16 elements per operand per stage
-constexpr int kStageElems = 2 * kTileElems;     // W tile then hidden tile
+constexpr int kHStages = 2;                     // hidden ring: 2 stages
 static_assert(kVocabTile == kRowTile, "square tiles assumed below");
 constexpr int kTileThreads = 256;               // 4 waves
 constexpr int kBlocksPerWave = kTileElems / 512 / 4;   // 1 KB load blocks per wave per operand per stage
@@ -89,9 +89,17 @@ __device__ __forceinline__ void barrier() {
     asm volatile("" ::: "memory");
 }
 
+// WS: weight-ring depth.  With few row tiles the hidden rows stay in L2 and
+// only the weights stream from HBM; a third weight stage gives them two
+// stages to arrive (WS = 3 fills the whole 160 KB of LDS).  With many row
+// tiles both operands miss and WS = 2 measures better.
+template <int WS>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStageElems];   // [buf][W, hidden]
-    __shared__ float red[2][kRowTile][2];                                     // [vocab half][row][m, l]
+    // WS x 32 KB weight stages + 2 x 32 KB hidden stages; the epilogue's
+    // reduction area reuses the weight ring once the loop is done
+    __shared__ __attribute__((aligned(16))) uint16_t wring[WS * kTileElems];
+    __shared__ __attribute__((aligned(16))) uint16_t hring[kHStages * kTileElems];
+    float (*red)[kRowTile][2] = reinterpret_cast<float (*)[kRowTile][2]>(wring);   // [vocab half][row][m, l]
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -111,18 +119,24 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const uint16_t *hg = a.hidden + r0 * H;
     const int wlast = static_cast<int>(min(static_cast<int64_t>(kVocabTile - 1), a.V - 1 - v0));
     const int hlast = static_cast<int>(min(static_cast<int64_t>(kRowTile - 1), a.R - 1 - r0));
-    // the swizzled chunk depends only on lane bits (row bits 1..3 = lane bits 4..5 and j)
-    auto issue = [&](int ks) {
-        uint16_t *st = smem + (ks & 1) * kStageElems;
-        const int64_t k0 = static_cast<int64_t>(ks) * kK;
+    // Block j of stage `slot`'s buffer gets the data of stage min(slot, nks-1):
+    // past the last stage the loads refill a buffer nobody reads any more.
+    auto wbuf = [&](int ks) { return wring + (ks % WS) * kTileElems; };
+    auto hbuf = [&](int ks) { return hring + (ks & 1) * kTileElems; };
+    auto issue_block = [&](const uint16_t *g, int last, uint16_t *st, int slot, int j) {
+        const int blk = wave * kBlocksPerWave + j;
+        const int row = blk * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        const int64_t k0 = static_cast<int64_t>(min(slot, nks - 1)) * kK;
+        load_lds16(g + min(row, last) * H + k0 + c * 8, st + blk * 512);
+    };
+    auto issue_w = [&](int slot) {
 #pragma unroll
-        for (int j = 0; j < kBlocksPerWave; ++j) {
-            const int blk = wave * kBlocksPerWave + j;
-            const int row = blk * 8 + (lane >> 3);
-            const int c = (lane & 7) ^ ((row >> 1) & 7);
-            load_lds16(wg + min(row, wlast) * H + k0 + c * 8, st + blk * 512);
-            load_lds16(hg + min(row, hlast) * H + k0 + c * 8, st + kTileElems + blk * 512);
-        }
+        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(wg, wlast, wbuf(slot), slot, j);
+    };
+    auto issue_h = [&](int slot) {
+#pragma unroll
+        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(hg, hlast, hbuf(slot), slot, j);
     };
 
     f32x16 acc[4][4];
@@ -132,8 +146,8 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = f32x16{};
     bf16x8 fa[2][4], fb[2][4];
     auto read_frags = [&](int ks, int kq, int p) {
-        const uint16_t *as = smem + (ks & 1) * kStageElems;
-        const uint16_t *bs = as + kTileElems;
+        const uint16_t *as = wbuf(ks);
+        const uint16_t *bs = hbuf(ks);
         const int c = kq * 2 + h2;
 #pragma unroll
         for (int i = 0; i < 4; ++i) fa[p][i] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + i * 32 + l32, c));
@@ -148,13 +162,20 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
     };
 
-    // Stage ks lives in LDS buffer ks % 2.  Loads past the last stage refill a
-    // buffer nobody reads any more (so the loop body has no branch and the
-    // scheduler can interleave loads, reads and MFMAs); the final wait makes
-    // sure none of them is still writing LDS when the epilogue starts.
-    issue(0);
-    issue(min(1, nks - 1));
-    wait_vm<2 * kBlocksPerWave>();               // stage 0 has landed
+    // Stage ks lives in weight buffer ks % WS and hidden buffer ks % 2.  At
+    // the end of stage ks (once every wave is done reading it) the hidden rows
+    // of stage ks+2 and then the weights of stage ks+WS are issued, so the
+    // weights have WS-1 stages to arrive; the one wait per stage leaves only
+    // the newest weight stage in flight (WS = 3) or nothing (WS = 2).  Loads past the last stage
+    // refill a buffer nobody reads any more (so the loop body has no branch);
+    // the final wait makes sure none of them is still writing LDS when the
+    // epilogue starts.
+    issue_h(0);
+    issue_w(0);
+    issue_h(1);
+    issue_w(1);
+    if (WS == 3) issue_w(2);
+    wait_vm<(WS == 3 ? 3 : 2) * kBlocksPerWave>();   // stage 0 has landed
     barrier();
     read_frags(0, 0, 0);
     for (int ks = 0; ks < nks; ++ks) {
@@ -169,27 +190,27 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             }
             __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
         }
-        // last k-step: stage ks+1 has landed and every wave is done reading
-        // stage ks, whose buffer takes stage ks+2
-        wait_vm<0>();
+        // last k-step: stage ks+1 has landed (only the weights of stage ks+2
+        // may still be in flight) and every wave is done reading stage ks
+        wait_vm<(WS == 3 ? 1 : 0) * kBlocksPerWave>();
         wait_lds();
         barrier();
-        // eight groups of: one pair of global->LDS loads for stage ks+2, two
-        // MFMAs of this k-step, one fragment read of stage ks+1 (kept in this
-        // order: the loads are opaque to the scheduler)
+        // eight groups of: two global->LDS loads (hidden rows of stage ks+2
+        // in groups 0-3, weights of stage ks+WS in groups 4-7), two MFMAs of
+        // this k-step, one fragment read of stage ks+1 (kept in this order:
+        // the loads are opaque to the scheduler)
         {
-            const int ks2 = min(ks + 2, nks - 1);
-            uint16_t *st = smem + (ks2 & 1) * kStageElems;
-            const int64_t k0 = static_cast<int64_t>(ks2) * kK;
-            const uint16_t *as = smem + ((ks + 1) & 1) * kStageElems;
-            const uint16_t *bs = as + kTileElems;
+            const uint16_t *as = wbuf(ks + 1);
+            const uint16_t *bs = hbuf(ks + 1);
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
-                const int blk = wave * kBlocksPerWave + g;
-                const int row = blk * 8 + (lane >> 3);
-                const int c = (lane & 7) ^ ((row >> 1) & 7);
-                load_lds16(wg + min(row, wlast) * H + k0 + c * 8, st + blk * 512);
-                load_lds16(hg + min(row, hlast) * H + k0 + c * 8, st + kTileElems + blk * 512);
+                if (g < 4) {
+                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, 2 * g);
+                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, 2 * g + 1);
+                } else {
+                    issue_block(wg, wlast, wbuf(ks + WS), ks + WS, 2 * (g - 4));
+                    issue_block(wg, wlast, wbuf(ks + WS), ks + WS, 2 * (g - 4) + 1);
+                }
 #pragma unroll
                 for (int m = 2 * g; m < 2 * g + 2; ++m)
                     acc[m >> 2][m & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][m >> 2], fb[1][m & 3],
@@ -201,6 +222,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         }
     }
     wait_vm<0>();
+    barrier();                                   // the reduction area aliases the weight ring
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- epilogue: per token row, max / sum of exp2 / target logit ---------
@@ -339,7 +361,10 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
 
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
     const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
-    hipLaunchKernelGGL(logprob_tile_kernel, dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0, stream, a);
+    if (a.n_row_tiles <= 8)
+        hipLaunchKernelGGL(logprob_tile_kernel<3>, dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(logprob_tile_kernel<2>, dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.R < 32768) {

@@ -46,7 +46,10 @@ def test_tiny_config():
 @pytest.mark.parametrize("R,H,V", [(300, 128, 1000),    # ragged rows and vocab, 2x4 tiles
                                    (1, 64, 257),        # one row, one vocab entry past a tile
                                    (513, 192, 511),
-                                   (256, 4096, 2048)])
+                                   (256, 4096, 2048),
+                                   # more than 8 row tiles: the two-stage weight ring
+                                   (2305, 64, 700),     # one hidden stage, ragged rows and vocab
+                                   (2049, 192, 300)])   # three hidden stages, one row past a tile
 def test_ragged_shapes(R, H, V):
     rng = np.random.Generator(np.random.PCG64(R + H + V))
     h = rand_bits(rng, (R, H))
