@@ -7,9 +7,11 @@ patterns) and returns float64 results.
 
 The definitions it computes are stated at the top of oracle.c: grouped-query
 decode attention over a shared prompt prefix followed by each candidate's own
-suffix (Sec. 2.2.1, Problem Setup), and the full-vocabulary token log-prob of
+suffix (Sec. 2.2.1, Problem Setup), the full-vocabulary token log-prob of
 the sampled token that the GRPO ratio needs (Sec. 3, Eq. grpo-loss; masked
-positions per Sec. 3, Multi-turn RL Training).
+positions per Sec. 3, Multi-turn RL Training), the group-relative advantages
+and the clipped surrogate of Eq. grpo-loss with its gradient, and the
+gradient of the log-prob with respect to the hidden rows.
 """
 from __future__ import annotations
 
@@ -49,6 +51,17 @@ def _bind(path: str):
     lib.oracle_token_logprob.restype = ctypes.c_int
     lib.oracle_token_logprob.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                          P, P, P, ctypes.c_float, P, P]
+    lib.oracle_token_logprob_f64.restype = ctypes.c_int
+    lib.oracle_token_logprob_f64.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                             P, P, P, ctypes.c_float, P, P]
+    lib.oracle_grpo_advantage.restype = ctypes.c_int
+    lib.oracle_grpo_advantage.argtypes = [ctypes.c_int64, ctypes.c_int32, P, P]
+    lib.oracle_grpo_surrogate.restype = ctypes.c_int
+    lib.oracle_grpo_surrogate.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                          P, P, P, P, ctypes.c_double, P, P]
+    lib.oracle_token_logprob_backward.restype = ctypes.c_int
+    lib.oracle_token_logprob_backward.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                                  P, P, P, ctypes.c_float, P, P]
     return lib
 
 
@@ -148,6 +161,89 @@ def token_logprob(hidden, w_lm, target, inv_temperature: float = 1.0, _lib=None)
     return logprob, lse
 
 
+def token_logprob_f64(hidden, w_lm, target, inv_temperature: float = 1.0, _lib=None):
+    """Oracle token log-prob with float64 hidden rows (for finite differences).
+
+    hidden: float64 [R, H]; w_lm: uint16 [V, H]; target: int32 [R].
+    """
+    hidden = np.ascontiguousarray(hidden, dtype=np.float64)
+    w = _u16(w_lm)
+    R, H = hidden.shape
+    V, H2 = w.shape
+    if H2 != H or V <= 0 or H <= 0:
+        raise ValueError("shape")
+    t = np.ascontiguousarray(target, dtype=np.int32)
+    if t.shape != (R,):
+        raise ValueError("target shape")
+    logprob = np.zeros(R, dtype=np.float64)
+    lse = np.zeros(R, dtype=np.float64)
+    if R == 0:
+        return logprob, lse
+    rc = (_lib or _load()).oracle_token_logprob_f64(
+        R, H, V, _ptr(hidden), _ptr(w), _ptr(t),
+        float(np.float32(inv_temperature)), _ptr(logprob), _ptr(lse))
+    if rc:
+        raise MemoryError("oracle_token_logprob_f64 scratch allocation failed")
+    return logprob, lse
+
+
+def grpo_advantage(reward, group_size: int, _lib=None):
+    """Group-relative advantages: reward [P*G] -> float64 [P*G]."""
+    r = np.ascontiguousarray(reward, dtype=np.float64).reshape(-1)
+    G = int(group_size)
+    if G <= 0 or r.size % G:
+        raise ValueError("reward length must be a multiple of group_size")
+    adv = np.zeros_like(r)
+    if r.size:
+        (_lib or _load()).oracle_grpo_advantage(r.size // G, G, _ptr(r), _ptr(adv))
+    return adv
+
+
+def grpo_surrogate(logp_new, logp_old, seq, adv, group_size: int, eps: float = 0.2, _lib=None):
+    """Clipped GRPO surrogate loss and its gradient with respect to logp_new.
+
+    logp_new, logp_old: [R] (float64 values); seq: int32 [R], the candidate of
+    each token row or -1; adv: [P*G].  Returns (loss float, grad float64 [R]).
+    """
+    ln = np.ascontiguousarray(logp_new, dtype=np.float64)
+    lo = np.ascontiguousarray(logp_old, dtype=np.float64)
+    sq = np.ascontiguousarray(seq, dtype=np.int32)
+    a = np.ascontiguousarray(adv, dtype=np.float64)
+    G = int(group_size)
+    R = ln.shape[0]
+    if lo.shape != (R,) or sq.shape != (R,) or G <= 0 or a.size % G:
+        raise ValueError("shapes")
+    loss = np.zeros(1, dtype=np.float64)
+    grad = np.zeros(R, dtype=np.float64)
+    rc = (_lib or _load()).oracle_grpo_surrogate(R, a.size // G, G, _ptr(ln), _ptr(lo), _ptr(sq),
+                                                 _ptr(a), float(eps), _ptr(loss), _ptr(grad))
+    if rc:
+        raise MemoryError("oracle_grpo_surrogate scratch allocation failed")
+    return float(loss[0]), grad
+
+
+def token_logprob_backward(hidden, w_lm, target, grad_logprob, inv_temperature: float = 1.0, _lib=None):
+    """d(sum_r g_r logprob_r)/d hidden: float64 [R, H]."""
+    hidden = _u16(hidden)
+    w = _u16(w_lm)
+    R, H = hidden.shape
+    V, H2 = w.shape
+    if H2 != H or V <= 0 or H <= 0:
+        raise ValueError("shape")
+    t = np.ascontiguousarray(target, dtype=np.int32)
+    g = np.ascontiguousarray(grad_logprob, dtype=np.float64)
+    if t.shape != (R,) or g.shape != (R,):
+        raise ValueError("target / grad shape")
+    dh = np.zeros((R, H), dtype=np.float64)
+    if R == 0:
+        return dh
+    rc = (_lib or _load()).oracle_token_logprob_backward(
+        R, H, V, _ptr(hidden), _ptr(w), _ptr(t), float(np.float32(inv_temperature)), _ptr(g), _ptr(dh))
+    if rc:
+        raise MemoryError("oracle_token_logprob_backward scratch allocation failed")
+    return dh
+
+
 def num_threads() -> int:
     """Threads OpenMP will use (OMP_NUM_THREADS, else the CPUs this process may run on)."""
     env = os.environ.get("OMP_NUM_THREADS")
@@ -157,7 +253,7 @@ def num_threads() -> int:
 
 
 class Oracle:
-    """The oracle's two functions bound to one compiled library.
+    """The oracle's functions bound to one compiled library.
 
     The default instance uses liboracle.so; the mutation tests bind a copy
     compiled from a deliberately altered source to show the pins catch it.
@@ -172,3 +268,15 @@ class Oracle:
 
     def token_logprob(self, *args, **kw):
         return token_logprob(*args, **kw, _lib=self._lib)
+
+    def token_logprob_f64(self, *args, **kw):
+        return token_logprob_f64(*args, **kw, _lib=self._lib)
+
+    def grpo_advantage(self, *args, **kw):
+        return grpo_advantage(*args, **kw, _lib=self._lib)
+
+    def grpo_surrogate(self, *args, **kw):
+        return grpo_surrogate(*args, **kw, _lib=self._lib)
+
+    def token_logprob_backward(self, *args, **kw):
+        return token_logprob_backward(*args, **kw, _lib=self._lib)

@@ -25,6 +25,29 @@
  *     Sec. 3, Multi-turn RL Training) and gives logprob 0; any other
  *     target outside [0, V) gives NaN.  lse is computed in every case.
  *
+ *  3. Group-relative advantages (Sec. 3, the definition under Eq.
+ *     grpo-loss): for each prompt's group of G candidates with rewards r_i,
+ *         A_i = (r_i - mean(r)) / std(r),
+ *     std taken as the sample standard deviation (divisor G-1); a group whose
+ *     rewards are all equal (or G = 1) carries no signal and gets A_i = 0.
+ *
+ *  4. The clipped GRPO surrogate with beta * D_KL = 0 (Sec. 3, Eq.
+ *     grpo-loss), as a loss to minimise over a batch of P prompts:
+ *         rho = exp(logp_new - logp_old),
+ *         L = -(1/(P G)) sum_i (1/|o_i|) sum_t min(rho A_i, clip(rho, 1-eps, 1+eps) A_i),
+ *     |o_i| = the number of token rows of candidate i; rows of no candidate
+ *     (seq = -1) do not count.  dL/dlogp_new of a row is
+ *     -(1/(P G |o_i|)) rho A_i when the ratio term is the minimum (ties
+ *     included) and 0 when the clipped term is (clipping then holds the
+ *     ratio at a bound, so the term does not depend on logp_new).
+ *
+ *  5. The backward of the token log-probability with respect to the hidden
+ *     rows, given dL/dlogprob = g_r per row (the lm-head itself is frozen
+ *     under the paper's QLoRA fine-tuning, Sec. 3, Multi-turn RL Training):
+ *     with p_v = softmax_v(z),
+ *         dL/dhidden_r = g_r * inv_T * (W_t - sum_v p_v W_v);
+ *     a masked row (target -1) gets 0 and an invalid target NaN.
+ *
  * Inputs are raw bf16 bit patterns (uint16).  Each is widened exactly:
  * bits << 16 is the float32 pattern, and float32 -> double is exact.
  */
@@ -41,7 +64,7 @@ static double bf16_to_f64(uint16_t b)
     return (double)f;
 }
 
-int oracle_abi_version(void) { return 1; }
+int oracle_abi_version(void) { return 2; }
 
 /* Returns 0 on success, 1 if a scratch allocation failed. */
 int oracle_decode_attn(int32_t P, int32_t G, int32_t Hq, int32_t Hkv, int32_t D,
@@ -110,10 +133,37 @@ int oracle_decode_attn(int32_t P, int32_t G, int32_t Hq, int32_t Hkv, int32_t D,
 }
 
 /* Returns 0 on success, 1 if a scratch allocation failed. */
-int oracle_token_logprob(int64_t R, int32_t H, int32_t V,
-                         const uint16_t *hidden, const uint16_t *w_lm,
-                         const int32_t *target, float inv_temperature,
-                         double *logprob, double *lse)
+/* The V logits z_v = inv_T * <h, W_v> of one row whose hidden vector is
+ * given in double, and their log-sum-exp (max first, then the sum). */
+static double row_logits(int32_t H, int32_t V, const double *h, const uint16_t *w_lm,
+                         double inv_T, double *z)
+{
+    for (int32_t v = 0; v < V; ++v) {
+        const uint16_t *wr = w_lm + (int64_t)v * H;
+        double dot = 0.0;
+        for (int32_t k = 0; k < H; ++k) dot += h[k] * bf16_to_f64(wr[k]);
+        z[v] = inv_T * dot;
+    }
+    double M = z[0];
+    for (int32_t v = 1; v < V; ++v) if (z[v] > M) M = z[v];
+    double sum = 0.0;
+    for (int32_t v = 0; v < V; ++v) sum += exp(z[v] - M);
+    return M + log(sum);
+}
+
+static double target_logprob(int32_t V, int32_t t, const double *z, double l)
+{
+    if (t == -1) return 0.0;
+    if (t >= 0 && t < V) return z[t] - l;
+    return NAN;
+}
+
+/* Token log-prob with the hidden rows given in double (finite-difference
+ * checks of the backward perturb them). */
+int oracle_token_logprob_f64(int64_t R, int32_t H, int32_t V,
+                             const double *hidden, const uint16_t *w_lm,
+                             const int32_t *target, float inv_temperature,
+                             double *logprob, double *lse)
 {
     const double inv_T = (double)inv_temperature;
     int failed = 0;
@@ -126,28 +176,131 @@ int oracle_token_logprob(int64_t R, int32_t H, int32_t V,
             failed = 1;
             continue;
         }
-        const uint16_t *hr = hidden + r * (int64_t)H;
-        /* all V logits of this row */
-        for (int32_t v = 0; v < V; ++v) {
-            const uint16_t *wr = w_lm + (int64_t)v * H;
-            double dot = 0.0;
-            for (int32_t k = 0; k < H; ++k) dot += bf16_to_f64(hr[k]) * bf16_to_f64(wr[k]);
-            z[v] = inv_T * dot;
-        }
-        double M = z[0];
-        for (int32_t v = 1; v < V; ++v) if (z[v] > M) M = z[v];
-        double sum = 0.0;
-        for (int32_t v = 0; v < V; ++v) sum += exp(z[v] - M);
-        const double l = M + log(sum);
+        const double l = row_logits(H, V, hidden + r * (int64_t)H, w_lm, inv_T, z);
         lse[r] = l;
-        const int32_t t = target[r];
-        if (t == -1)
-            logprob[r] = 0.0;
-        else if (t >= 0 && t < V)
-            logprob[r] = z[t] - l;
-        else
-            logprob[r] = NAN;
+        logprob[r] = target_logprob(V, target[r], z, l);
         free(z);
+    }
+    return failed;
+}
+
+int oracle_token_logprob(int64_t R, int32_t H, int32_t V,
+                         const uint16_t *hidden, const uint16_t *w_lm,
+                         const int32_t *target, float inv_temperature,
+                         double *logprob, double *lse)
+{
+    const double inv_T = (double)inv_temperature;
+    int failed = 0;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r) {
+        double *z = (double *)malloc((size_t)V * sizeof(double));
+        double *h = (double *)malloc((size_t)H * sizeof(double));
+        if (!z || !h) {
+#pragma omp atomic write
+            failed = 1;
+            free(z);
+            free(h);
+            continue;
+        }
+        const uint16_t *hr = hidden + r * (int64_t)H;
+        for (int32_t k = 0; k < H; ++k) h[k] = bf16_to_f64(hr[k]);
+        const double l = row_logits(H, V, h, w_lm, inv_T, z);
+        lse[r] = l;
+        logprob[r] = target_logprob(V, target[r], z, l);
+        free(z);
+        free(h);
+    }
+    return failed;
+}
+
+int oracle_grpo_advantage(int64_t P, int32_t G, const double *reward, double *adv)
+{
+    for (int64_t p = 0; p < P; ++p) {
+        const double *r = reward + p * G;
+        double *a = adv + p * G;
+        double mean = 0.0;
+        for (int32_t i = 0; i < G; ++i) mean += r[i];
+        mean /= G;
+        double ss = 0.0;
+        for (int32_t i = 0; i < G; ++i) ss += (r[i] - mean) * (r[i] - mean);
+        const double sd = G > 1 ? sqrt(ss / (G - 1)) : 0.0;
+        for (int32_t i = 0; i < G; ++i) a[i] = sd > 0.0 ? (r[i] - mean) / sd : 0.0;
+    }
+    return 0;
+}
+
+int oracle_grpo_surrogate(int64_t R, int64_t P, int32_t G,
+                          const double *logp_new, const double *logp_old,
+                          const int32_t *seq, const double *adv, double eps,
+                          double *loss, double *grad)
+{
+    const int64_t S = P * G;
+    int64_t *count = (int64_t *)calloc((size_t)(S > 0 ? S : 1), sizeof(int64_t));
+    if (!count) return 1;
+    for (int64_t r = 0; r < R; ++r)
+        if (seq[r] >= 0 && seq[r] < S) count[seq[r]] += 1;
+    double total = 0.0;
+    for (int64_t r = 0; r < R; ++r) {
+        const int32_t i = seq[r];
+        grad[r] = 0.0;
+        if (i < 0 || i >= S) continue;
+        const double rho = exp(logp_new[r] - logp_old[r]);
+        const double clipped = rho < 1.0 - eps ? 1.0 - eps : (rho > 1.0 + eps ? 1.0 + eps : rho);
+        const double u = rho * adv[i], c = clipped * adv[i];
+        const double w = 1.0 / ((double)P * G * (double)count[i]);
+        total += (u <= c ? u : c) * w;
+        grad[r] = u <= c ? -w * rho * adv[i] : 0.0;
+    }
+    *loss = -total;
+    free(count);
+    return 0;
+}
+
+int oracle_token_logprob_backward(int64_t R, int32_t H, int32_t V,
+                                  const uint16_t *hidden, const uint16_t *w_lm,
+                                  const int32_t *target, float inv_temperature,
+                                  const double *grad_logprob, double *grad_hidden)
+{
+    const double inv_T = (double)inv_temperature;
+    int failed = 0;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r) {
+        double *dh = grad_hidden + r * (int64_t)H;
+        const int32_t t = target[r];
+        if (t == -1) {
+            for (int32_t k = 0; k < H; ++k) dh[k] = 0.0;
+            continue;
+        }
+        if (t < 0 || t >= V) {
+            for (int32_t k = 0; k < H; ++k) dh[k] = NAN;
+            continue;
+        }
+        double *z = (double *)malloc((size_t)V * sizeof(double));
+        double *h = (double *)malloc((size_t)H * sizeof(double));
+        if (!z || !h) {
+#pragma omp atomic write
+            failed = 1;
+            free(z);
+            free(h);
+            continue;
+        }
+        const uint16_t *hr = hidden + r * (int64_t)H;
+        for (int32_t k = 0; k < H; ++k) h[k] = bf16_to_f64(hr[k]);
+        const double l = row_logits(H, V, h, w_lm, inv_T, z);
+        /* expected weight row under the softmax, then the target row */
+        for (int32_t k = 0; k < H; ++k) dh[k] = 0.0;
+        for (int32_t v = 0; v < V; ++v) {
+            const double pv = exp(z[v] - l);
+            const uint16_t *wr = w_lm + (int64_t)v * H;
+            for (int32_t k = 0; k < H; ++k) dh[k] -= pv * bf16_to_f64(wr[k]);
+        }
+        const uint16_t *wt = w_lm + (int64_t)t * H;
+        const double scale = grad_logprob[r] * inv_T;
+        for (int32_t k = 0; k < H; ++k) dh[k] = scale * (bf16_to_f64(wt[k]) + dh[k]);
+        free(z);
+        free(h);
     }
     return failed;
 }

@@ -11,7 +11,11 @@ oracle disagrees with what the mathematics fixes:
   chunking with a log-sum-exp merge, constant shift, sum of probabilities);
 * exact probes (one-hot attention returns one value row bit for bit; uniform
   attention recovers the context length; an id probe recovers the target);
-* hand-derived worked examples under tests/golden/.
+* hand-derived worked examples under tests/golden/;
+* for the GRPO pieces and the backward: hand-worked regimes of the clipped
+  objective, the statistics that define the advantages, central finite
+  differences of the oracle's own loss / forward, the two-class logistic
+  gradient, and torch autograd in fp64.
 
 The same battery runs against deliberately broken copies of the oracle
 (test_oracle_mutants.py) to show that each plausible mistake is caught.
@@ -377,8 +381,174 @@ def pin_logprob_golden(orc):
         close(lse, np.array(case["lse"]), 1e-15, case["name"] + " lse")
 
 
+# ------------------------------------------------------------ GRPO pins
+# (Sec. 3, Eq. grpo-loss and the advantage definition under it)
+def pin_advantage_closed_form(orc):
+    """G1: rewards 1, 2, 3, 4: mean 2.5, sample variance 5/3 -> (r - 2.5) / sqrt(5/3);
+    a group of equal rewards and a group of one give 0."""
+    sd = math.sqrt(5.0 / 3.0)
+    got = orc.grpo_advantage([1.0, 2.0, 3.0, 4.0, 7.0, 7.0, 7.0, 7.0], 4)
+    close(got, [-1.5 / sd, -0.5 / sd, 0.5 / sd, 1.5 / sd, 0, 0, 0, 0], 1e-15, "advantage 1..4")
+    close(orc.grpo_advantage([3.0, -2.0], 1), [0.0, 0.0], 0.0, "group of one")
+
+
+def pin_advantage_invariants(orc):
+    """G2: per group the advantages sum to 0 and have sample variance 1; they do not
+    change under r -> a r + b (a > 0) and follow a permutation of the candidates."""
+    rng = np.random.Generator(np.random.PCG64(11))
+    P, G = 5, 16
+    r = rng.standard_normal(P * G) * 3.0 + 1.0
+    a = orc.grpo_advantage(r, G).reshape(P, G)
+    close(a.sum(1), np.zeros(P), 1e-12, "advantage sum")
+    close((a * a).sum(1) / (G - 1), np.ones(P), 1e-12, "advantage variance")
+    close(orc.grpo_advantage(2.5 * r + 7.0, G).reshape(P, G), a, 1e-12, "affine invariance")
+    perm = rng.permutation(G)
+    close(orc.grpo_advantage(r.reshape(P, G)[:, perm].reshape(-1), G).reshape(P, G), a[:, perm], 1e-15,
+          "permutation")
+
+
+def surrogate_case(seed=12, P=3, G=4, lo=1, hi=9, spread=0.15):
+    """Random token rows of P*G candidates (some rows belong to none) with ratios
+    exp(logp_new - logp_old) kept away from the clip bounds 0.8 and 1.2."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    S = P * G
+    counts = rng.integers(lo, hi, S)
+    seq = np.repeat(np.arange(S, dtype=np.int32), counts)
+    seq = np.concatenate([seq, np.full(5, -1, np.int32)])
+    rng.shuffle(seq)
+    R = len(seq)
+    old = rng.uniform(-6.0, -0.1, R)
+    d = rng.uniform(-spread, spread, R)
+    log_bounds = np.log([0.8, 1.2])
+    for b in log_bounds:                                  # at least 1e-3 from each bound
+        near = np.abs(d - b) < 1e-3
+        d[near] += 3e-3
+    adv = random_advantages(rng, P, G)
+    return old + d, old, seq, adv
+
+
+def random_advantages(rng, P, G):
+    a = rng.standard_normal((P, G))
+    return a.reshape(-1)
+
+
+def pin_surrogate_finite_differences(orc):
+    """G3: the returned gradient is the derivative of the returned loss (central
+    differences, every row, ratios inside, below and above the clip range)."""
+    for seed, spread in ((12, 0.1), (13, 0.6)):
+        new, old, seq, adv = surrogate_case(seed, spread=spread)
+        loss, grad = orc.grpo_surrogate(new, old, seq, adv, 4, 0.2)
+        h = 1e-6
+        fd = np.zeros_like(new)
+        for r in range(len(new)):
+            e = np.zeros_like(new); e[r] = h
+            lp, _ = orc.grpo_surrogate(new + e, old, seq, adv, 4, 0.2)
+            lm, _ = orc.grpo_surrogate(new - e, old, seq, adv, 4, 0.2)
+            fd[r] = (lp - lm) / (2 * h)
+        close(grad, fd, 1e-8, f"surrogate gradient (spread {spread})")
+
+
+def pin_surrogate_closed_forms(orc):
+    """G4: hand-worked cases.
+    * ratio 1 everywhere: L = -(1/(P G)) sum_i A_i (each candidate's token mean is A_i),
+      dL/dlogp = -A_i / (P G |o_i|);
+    * one candidate with one token per regime (A = +-1, ratio e^{+-0.5}, eps = 0.2):
+      A=+1, ratio 1.6487 -> clipped 1.2, gradient 0; A=-1, ratio 0.6065 -> clipped -0.8,
+      gradient 0; A=-1, ratio 1.6487 -> the ratio term -1.6487 is the minimum; A=+1,
+      ratio 0.6065 -> the ratio term 0.6065 is the minimum."""
+    P, G = 2, 3
+    seq = np.array([0, 0, 1, 2, 2, 2, 3, 5, 5, -1], np.int32)        # candidate 4 has no tokens
+    adv = np.array([1.0, -0.5, 2.0, 0.25, 3.0, -1.0])
+    z = np.full(len(seq), -2.0)
+    loss, grad = orc.grpo_surrogate(z, z, seq, adv, G, 0.2)
+    counts = np.bincount(seq[seq >= 0], minlength=6)
+    close(loss, -(adv[counts > 0].sum()) / (P * G), 1e-15, "ratio-1 loss")
+    want = np.array([-adv[i] / (P * G * counts[i]) if i >= 0 else 0.0 for i in seq])
+    close(grad, want, 1e-15, "ratio-1 gradient")
+    e = math.exp(0.5)
+    for a, d, term, g in ((1.0, 0.5, 1.2, 0.0), (-1.0, -0.5, -0.8, 0.0),
+                          (-1.0, 0.5, -e, e), (1.0, -0.5, 1 / e, -1 / e)):
+        loss, grad = orc.grpo_surrogate([d], [0.0], [0], [a], 1, 0.2)
+        close(loss, -term, 1e-15, f"regime A={a} d={d}")
+        close(grad, [g], 1e-15, f"regime gradient A={a} d={d}")
+
+
+def pin_surrogate_unowned_rows(orc):
+    """G5: rows of no candidate (seq = -1) change neither the loss nor the other
+    rows' gradients, and get gradient 0."""
+    new, old, seq, adv = surrogate_case(14)
+    keep = seq >= 0
+    l1, g1 = orc.grpo_surrogate(new, old, seq, adv, 4, 0.2)
+    l2, g2 = orc.grpo_surrogate(new[keep], old[keep], seq[keep], adv, 4, 0.2)
+    close(l1, l2, 1e-15, "loss without unowned rows")
+    close(g1[keep], g2, 1e-15, "gradients without unowned rows")
+    close(g1[~keep], np.zeros((~keep).sum()), 0.0, "unowned rows")
+
+
+# --------------------------------------------------------- backward pins
+def pin_backward_vs_torch(orc):
+    """B1: torch autograd in fp64 on the CPU (log_softmax, gather, sum g * logprob)."""
+    for R, H, V, seed, invT in ((4, 16, 37, 20, 1.0), (3, 24, 90, 21, 1 / 0.7)):
+        h, w, t = logprob_case(R, H, V, seed)
+        t[0] = -1
+        rng = np.random.Generator(np.random.PCG64(seed + 1))
+        g = rng.standard_normal(R)
+        dh = orc.token_logprob_backward(h, w, t, g, invT)
+        ht = f64(h).clone().requires_grad_(True)
+        z = float(np.float32(invT)) * (ht @ f64(w).T)
+        ls = torch.log_softmax(z, dim=1)
+        keep = torch.tensor(t >= 0)
+        tt = torch.tensor(np.where(t >= 0, t, 0).astype(np.int64))
+        picked = ls.gather(1, tt[:, None])[:, 0] * keep
+        (picked * torch.tensor(g)).sum().backward()
+        close(dh, ht.grad.numpy(), 1e-12, f"backward vs torch {R}x{H}x{V}")
+
+
+def pin_backward_finite_differences(orc):
+    """B2: central differences of sum_r g_r logprob_r with respect to every hidden entry."""
+    R, H, V = 3, 6, 13
+    h, w, t = logprob_case(R, H, V, seed=22)
+    g = np.array([0.7, -1.3, 2.0])
+    dh = orc.token_logprob_backward(h, w, t, g, 1.0 / 0.9)
+    hd = f64(h).numpy()
+    step = 1e-6
+    fd = np.zeros_like(hd)
+    for r in range(R):
+        for k in range(H):
+            e = np.zeros_like(hd); e[r, k] = step
+            lp, _ = orc.token_logprob_f64(hd + e, w, t, 1.0 / 0.9)
+            lm, _ = orc.token_logprob_f64(hd - e, w, t, 1.0 / 0.9)
+            fd[r, k] = (g * (lp - lm)).sum() / (2 * step)
+    close(dh, fd, 1e-7, "backward finite differences")
+
+
+def pin_backward_closed_forms(orc):
+    """B3: two classes: dlogp_t/dh = inv_T (1 - p_t)(W_t - W_o) with p_t the logistic
+    of the logit gap (the textbook logistic-regression gradient); equal weight rows give
+    0; a masked row gives 0 and an invalid target NaN."""
+    h, w, _ = logprob_case(2, 8, 2, seed=23, w_std=1.0)
+    t = np.array([0, 1], np.int32)
+    invT = 1.5
+    dh = orc.token_logprob_backward(h, w, t, np.ones(2), invT)
+    H, W2 = f64(h).numpy(), f64(w).numpy()
+    for r in range(2):
+        o = 1 - t[r]
+        gap = invT * (H[r] @ (W2[t[r]] - W2[o]))
+        pt = 1.0 / (1.0 + math.exp(-gap))
+        close(dh[r], invT * (1 - pt) * (W2[t[r]] - W2[o]), 1e-13, "two-class gradient")
+    weq = np.tile(w[:1], (9, 1))
+    h3, _, t3 = logprob_case(3, 8, 9, seed=24)
+    close(orc.token_logprob_backward(h3, weq, t3, np.ones(3), 1.0), np.zeros((3, 8)), 1e-14, "equal rows")
+    t4 = np.array([-1, 9, 4], np.int32)
+    dh4 = orc.token_logprob_backward(h3, weq, t4, np.ones(3), 1.0)
+    assert np.all(dh4[0] == 0.0) and np.all(np.isnan(dh4[1])), "masked / invalid rows"
+
+
 ATTENTION_PINS = [pin_attention_vs_torch, pin_prefix_sharing, pin_attention_closed_forms,
                   pin_permutation, pin_one_hot_probe, pin_length_probe, pin_attention_golden]
 LOGPROB_PINS = [pin_logprob_vs_torch, pin_logprob_sum_to_one, pin_logprob_closed_forms,
                 pin_logprob_shift, pin_logprob_chunks, pin_logprob_id_probe, pin_logprob_golden]
-ALL_PINS = ATTENTION_PINS + LOGPROB_PINS
+GRPO_PINS = [pin_advantage_closed_form, pin_advantage_invariants, pin_surrogate_finite_differences,
+             pin_surrogate_closed_forms, pin_surrogate_unowned_rows]
+BACKWARD_PINS = [pin_backward_vs_torch, pin_backward_finite_differences, pin_backward_closed_forms]
+ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS

@@ -26,15 +26,32 @@ MUTANTS = [
     ("query_index_swapped", "const uint16_t *qv = q + (s * Hq + h) * (int64_t)D;",
      "const uint16_t *qv = q + ((int64_t)h * S + s) * (int64_t)D;", "attn"),
     ("max_not_subtracted", "Z += exp(x[j] - m);", "Z += exp(x[j]);", "attn"),
-    ("logprob_sign", "logprob[r] = z[t] - l;", "logprob[r] = l - z[t];", "lp"),
-    ("transposed_weight", "dot += bf16_to_f64(hr[k]) * bf16_to_f64(wr[k]);",
-     "dot += bf16_to_f64(hr[k]) * bf16_to_f64(w_lm[(int64_t)k * V + v]);", "lp"),
+    ("logprob_sign", "if (t >= 0 && t < V) return z[t] - l;", "if (t >= 0 && t < V) return l - z[t];", "lp"),
+    ("transposed_weight", "for (int32_t k = 0; k < H; ++k) dot += h[k] * bf16_to_f64(wr[k]);",
+     "for (int32_t k = 0; k < H; ++k) dot += h[k] * bf16_to_f64(w_lm[(int64_t)k * V + v]);", "lp"),
     ("dropped_temperature", "z[v] = inv_T * dot;", "z[v] = dot;", "lp"),
-    ("lse_missing_max", "const double l = M + log(sum);", "const double l = log(sum);", "lp"),
-    ("masked_row_not_zero", "if (t == -1)\n            logprob[r] = 0.0;", "if (t == -1)\n            logprob[r] = -l;", "lp"),
-    ("gather_off_by_one", "logprob[r] = z[t] - l;", "logprob[r] = z[t > 0 ? t - 1 : 0] - l;", "lp"),
-    ("last_vocab_id_dropped", "for (int32_t v = 1; v < V; ++v) if (z[v] > M) M = z[v];\n        double sum = 0.0;\n        for (int32_t v = 0; v < V; ++v)",
-     "for (int32_t v = 1; v < V; ++v) if (z[v] > M) M = z[v];\n        double sum = 0.0;\n        for (int32_t v = 0; v < V - 1; ++v)", "lp"),
+    ("lse_missing_max", "return M + log(sum);", "return log(sum);", "lp"),
+    ("masked_row_not_zero", "if (t == -1) return 0.0;", "if (t == -1) return -l;", "lp"),
+    ("gather_off_by_one", "if (t >= 0 && t < V) return z[t] - l;", "if (t >= 0 && t < V) return z[t > 0 ? t - 1 : 0] - l;", "lp"),
+    ("last_vocab_id_dropped", "for (int32_t v = 0; v < V; ++v) sum += exp(z[v] - M);",
+     "for (int32_t v = 0; v < V - 1; ++v) sum += exp(z[v] - M);", "lp"),
+    # group-relative advantages and the clipped surrogate
+    ("adv_population_std", "sqrt(ss / (G - 1))", "sqrt(ss / G)", "grpo"),
+    ("adv_not_centred", "(r[i] - mean) / sd : 0.0;", "r[i] / sd : 0.0;", "grpo"),
+    ("adv_wrong_group_base", "const double *r = reward + p * G;", "const double *r = reward;", "grpo"),
+    ("clip_upper_bound", "(rho > 1.0 + eps ? 1.0 + eps : rho)", "(rho > 1.0 + eps ? 1.0 - eps : rho)", "grpo"),
+    ("max_not_min", "total += (u <= c ? u : c) * w;", "total += (u >= c ? u : c) * w;", "grpo"),
+    ("surrogate_grad_sign", "grad[r] = u <= c ? -w * rho * adv[i] : 0.0;", "grad[r] = u <= c ? w * rho * adv[i] : 0.0;", "grpo"),
+    ("grad_missing_ratio", "grad[r] = u <= c ? -w * rho * adv[i] : 0.0;", "grad[r] = u <= c ? -w * adv[i] : 0.0;", "grpo"),
+    ("no_token_mean", "const double w = 1.0 / ((double)P * G * (double)count[i]);", "const double w = 1.0 / ((double)P * G);", "grpo"),
+    ("ratio_inverted", "const double rho = exp(logp_new[r] - logp_old[r]);", "const double rho = exp(logp_old[r] - logp_new[r]);", "grpo"),
+    # log-prob backward
+    ("bwd_missing_temperature", "const double scale = grad_logprob[r] * inv_T;", "const double scale = grad_logprob[r];", "bwd"),
+    ("bwd_target_row_dropped", "dh[k] = scale * (bf16_to_f64(wt[k]) + dh[k]);", "dh[k] = scale * dh[k];", "bwd"),
+    ("bwd_unnormalised_p", "const double pv = exp(z[v] - l);", "const double pv = exp(z[v]);", "bwd"),
+    ("bwd_wrong_target_row", "const uint16_t *wt = w_lm + (int64_t)t * H;", "const uint16_t *wt = w_lm + (int64_t)(V - 1 - t) * H;", "bwd"),
+    ("bwd_masked_not_zero", "if (t == -1) {\n            for (int32_t k = 0; k < H; ++k) dh[k] = 0.0;",
+     "if (t == -1) {\n            for (int32_t k = 0; k < H; ++k) dh[k] = 1.0;", "bwd"),
 ]
 
 
@@ -51,7 +68,8 @@ def test_mutant_is_caught(tmp_path, source, name, old, new, battery):
     src.write_text(source.replace(old, new))
     lib = oracle.compile_c(str(src), str(tmp_path / f"liboracle_{name}.so"))
     orc = oracle.Oracle(lib)
-    battery_fns = pins.ATTENTION_PINS if battery == "attn" else pins.LOGPROB_PINS
+    battery_fns = {"attn": pins.ATTENTION_PINS, "lp": pins.LOGPROB_PINS, "grpo": pins.GRPO_PINS,
+                   "bwd": pins.BACKWARD_PINS}[battery]
     caught = []
     for pin in battery_fns:
         try:
