@@ -1,7 +1,7 @@
 /*
  * rl_kernels.h - C ABI of librlkern.so, the MI355X (gfx950) rollout hot path.
  *
- * Two operations, both asynchronous on a caller-supplied HIP stream:
+ * Operations, all asynchronous on a caller-supplied HIP stream:
  *
  *  rl_decode_attn     one grouped-query decode step for a batch of prompts,
  *                     each with a group of G sampled candidates (Sec. 2.2.1,
@@ -18,6 +18,13 @@
  *                     lm-head weight over the full vocabulary without storing
  *                     the logits; masked positions (Sec. 3, Multi-turn RL
  *                     Training: masked log-probabilities) give 0.
+ *
+ *  rl_grpo_advantage  group-relative advantages of the candidates' rewards
+ *                     (Sec. 3, the definition under Eq. grpo-loss).
+ *
+ *  rl_grpo_surrogate  the clipped GRPO surrogate of Eq. grpo-loss (beta = 0)
+ *                     over a batch of token rows, and its gradient with
+ *                     respect to the new policy's log-probs.
  *
  * Plain C: no HIP or torch types.  `stream` is a hipStream_t passed as void*
  * (NULL = the default stream).  "device" pointers must be device memory of the
@@ -47,7 +54,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 2
+#define RL_ABI_VERSION 3
 
 typedef enum {
     RL_OK = 0,
@@ -162,6 +169,58 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab,
                            const int32_t *target, float inv_temperature,
                            float *logprob, float *lse,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* GRPO advantages and clipped surrogate (Sec. 3, Eq. grpo-loss)             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For each prompt p's group of G candidates s = p*G + g with rewards r_s:
+ *   adv[s] = (r_s - mean_g r) / std_g r,
+ * std the sample standard deviation (divisor G - 1); a group whose rewards
+ * are all equal, or G == 1, gets adv = 0.
+ *
+ *   reward, adv    device fp32 [num_prompts * group_size]
+ *
+ * num_prompts == 0 is a valid no-op.  Status: NULL pointer ->
+ * RL_ERR_NULL_POINTER; num_prompts < 0 or group_size < 1 ->
+ * RL_ERR_INVALID_SHAPE; group_size > 1024 -> RL_ERR_UNSUPPORTED; a pointer not
+ * 4-byte aligned -> RL_ERR_MISALIGNED.
+ */
+rl_status rl_grpo_advantage(int64_t num_prompts, int32_t group_size, const float *reward, float *adv,
+                            void *stream);
+
+/*
+ * Over token rows r = 0 .. rows-1, each belonging to candidate seq[r] of the
+ * S = num_prompts * group_size candidates (seq[r] = -1: the row belongs to no
+ * candidate and is ignored), with rho_r = exp(logp_new[r] - logp_old[r]):
+ *   loss = -(1/(num_prompts * G)) * sum_s (1/|o_s|)
+ *          * sum_{r: seq[r] = s} min(rho_r adv[s], clip(rho_r, 1-eps, 1+eps) adv[s]),
+ * |o_s| the number of rows of candidate s.  grad[r] = dloss/dlogp_new[r]:
+ * -(1/(num_prompts * G |o_s|)) rho_r adv[s] where the ratio term is the minimum
+ * (ties included), 0 where the clipped term is smaller, 0 for ignored rows.
+ *
+ *   logp_new, logp_old  device fp32 [rows]
+ *   seq                 device int32 [rows], in [-1, S)
+ *   adv                 device fp32 [S]
+ *   eps                 clip range, finite, in [0, 1) (the paper uses 0.2)
+ *   loss                device fp32, one value
+ *   grad                device fp32 [rows]
+ *
+ * The loss is summed in a fixed order (bitwise reproducible).  rows == 0 or
+ * num_prompts == 0 writes loss 0.  Status: NULL pointer -> RL_ERR_NULL_POINTER;
+ * negative sizes, group_size < 1 or a bad eps -> RL_ERR_INVALID_SHAPE; a
+ * pointer not 4-byte aligned -> RL_ERR_MISALIGNED; workspace NULL or short ->
+ * RL_ERR_WORKSPACE.  A seq value outside [-1, S) is not checked on the host;
+ * such a row is ignored.
+ */
+rl_status rl_grpo_surrogate_workspace_size(int64_t rows, int64_t num_prompts, int32_t group_size,
+                                           size_t *bytes);
+
+rl_status rl_grpo_surrogate(int64_t rows, int64_t num_prompts, int32_t group_size,
+                            const float *logp_new, const float *logp_old, const int32_t *seq,
+                            const float *adv, float eps, float *loss, float *grad,
+                            void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Diagnostics                                                               */

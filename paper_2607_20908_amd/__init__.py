@@ -70,7 +70,8 @@ class PlanItem(ctypes.Structure):
 
 EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_workspace_size",
            "rl_token_logprob", "rl_status_string", "rl_last_error", "rl_abi_version",
-           "rl_decode_plan_debug"]
+           "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
+           "rl_grpo_surrogate"]
 
 
 def _load():
@@ -93,7 +94,13 @@ def _load():
     lib.rl_token_logprob.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, SZ, P]
     lib.rl_decode_plan_debug.restype = ctypes.c_int
     lib.rl_decode_plan_debug.argtypes = [P, P, P, I64, ctypes.POINTER(I64)]
-    if lib.rl_abi_version() != 2:
+    lib.rl_grpo_advantage.restype = ctypes.c_int
+    lib.rl_grpo_advantage.argtypes = [I64, I32, P, P, P]
+    lib.rl_grpo_surrogate_workspace_size.restype = ctypes.c_int
+    lib.rl_grpo_surrogate_workspace_size.argtypes = [I64, I64, I32, ctypes.POINTER(SZ)]
+    lib.rl_grpo_surrogate.restype = ctypes.c_int
+    lib.rl_grpo_surrogate.argtypes = [I64, I64, I32, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]
+    if lib.rl_abi_version() != 3:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -300,3 +307,71 @@ def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor
                                  ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                  _stream_handle(stream)), "rl_token_logprob")
     return logprob, lse
+
+
+def _f32_dev(t: torch.Tensor, name: str, shape) -> torch.Tensor:
+    _on_device(t, name)
+    if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be a contiguous fp32 device tensor of shape {tuple(shape)}")
+    return t
+
+
+def grpo_advantage(reward: torch.Tensor, group_size: int, adv: Optional[torch.Tensor] = None, stream=None):
+    """Group-relative advantages (r - mean) / std over each group of group_size rewards.
+
+    reward: fp32 [P*G] device tensor.  Returns adv fp32 [P*G].
+    """
+    G = int(group_size)
+    n = reward.numel()
+    if G <= 0 or n % G:
+        raise ValueError("reward length must be a positive multiple of group_size")
+    _f32_dev(reward, "reward", (n,))
+    if adv is None:
+        adv = torch.empty_like(reward)
+    _f32_dev(adv, "adv", (n,))
+    _check(_lib.rl_grpo_advantage(n // G, G, _ptr(reward), _ptr(adv), _stream_handle(stream)),
+           "rl_grpo_advantage")
+    return adv
+
+
+def grpo_surrogate_workspace_size(rows: int, num_prompts: int, group_size: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_grpo_surrogate_workspace_size(rows, num_prompts, group_size, ctypes.byref(n)),
+           "rl_grpo_surrogate_workspace_size")
+    return n.value
+
+
+def grpo_surrogate(logp_new: torch.Tensor, logp_old: torch.Tensor, seq: torch.Tensor, adv: torch.Tensor,
+                   group_size: int, eps: float = 0.2, loss: Optional[torch.Tensor] = None,
+                   grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):
+    """Clipped GRPO surrogate loss (beta = 0) and its gradient with respect to logp_new.
+
+    logp_new, logp_old: fp32 [R]; seq: int32 [R] (candidate of each row, -1 = none);
+    adv: fp32 [P*G].  Returns (loss fp32 [1], grad fp32 [R]).
+    """
+    G = int(group_size)
+    R = logp_new.numel()
+    S = adv.numel()
+    if G <= 0 or S % G:
+        raise ValueError("adv length must be a positive multiple of group_size")
+    _f32_dev(logp_new, "logp_new", (R,))
+    _f32_dev(logp_old, "logp_old", (R,))
+    _f32_dev(adv, "adv", (S,))
+    _on_device(seq, "seq")
+    if seq.dtype != torch.int32 or not seq.is_contiguous() or tuple(seq.shape) != (R,):
+        raise ValueError("seq must be a contiguous int32 device tensor of shape (R,)")
+    dev = logp_new.device
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+    if grad is None:
+        grad = torch.empty(R, dtype=torch.float32, device=dev)
+    _f32_dev(loss, "loss", (1,))
+    _f32_dev(grad, "grad", (R,))
+    need = grpo_surrogate_workspace_size(R, S // G, G)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _on_device(workspace, "workspace")
+    _check(_lib.rl_grpo_surrogate(R, S // G, G, _ptr(logp_new), _ptr(logp_old), _ptr(seq), _ptr(adv),
+                                  float(eps), _ptr(loss), _ptr(grad), ctypes.c_void_p(workspace.data_ptr()),
+                                  workspace.numel(), _stream_handle(stream)), "rl_grpo_surrogate")
+    return loss, grad

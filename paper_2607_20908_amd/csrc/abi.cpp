@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -246,6 +247,94 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
     a.inv_temperature = inv_temperature;
     const hipError_t e = rlk::launch_logprob(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_error(e, "launching token log-prob");
+    return RL_OK;
+}
+
+static bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+rl_status rl_grpo_advantage(int64_t num_prompts, int32_t group_size, const float *reward, float *adv,
+                            void *stream) {
+    g_last_error.clear();
+    if (num_prompts < 0) return set_error(RL_ERR_INVALID_SHAPE, "num_prompts < 0");
+    if (group_size < 1) return set_error(RL_ERR_INVALID_SHAPE, "group_size < 1");
+    if (group_size > 1024) return set_error(RL_ERR_UNSUPPORTED, "group_size must be <= 1024");
+    if (num_prompts == 0) return RL_OK;
+    if (!reward || !adv) return set_error(RL_ERR_NULL_POINTER, "reward and adv must not be NULL");
+    if (!aligned4(reward) || !aligned4(adv)) return set_error(RL_ERR_MISALIGNED, "reward/adv not 4-byte aligned");
+    const hipError_t e = rlk::launch_grpo_advantage(num_prompts, group_size, reward, adv,
+                                                    static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_error(e, "launching the GRPO advantages");
+    return RL_OK;
+}
+
+namespace {
+struct GrpoLayout {
+    size_t off_counts = 0, off_partials = 0, total = 0;
+};
+
+rl_status grpo_layout(int64_t rows, int64_t num_prompts, int32_t group_size, GrpoLayout *lay) {
+    if (rows < 0) return set_error(RL_ERR_INVALID_SHAPE, "rows < 0");
+    if (num_prompts < 0) return set_error(RL_ERR_INVALID_SHAPE, "num_prompts < 0");
+    if (group_size < 1) return set_error(RL_ERR_INVALID_SHAPE, "group_size < 1");
+    const int64_t S = num_prompts * group_size;
+    if (S > INT32_MAX) return set_error(RL_ERR_UNSUPPORTED, "too many candidates");
+    lay->off_counts = 0;
+    lay->off_partials = rlk::align_up(static_cast<size_t>(S) * 4, 256);
+    lay->total = rlk::align_up(lay->off_partials + static_cast<size_t>(rlk::grpo_term_blocks(rows)) * 8, 256);
+    if (lay->total == 0) lay->total = 256;
+    return RL_OK;
+}
+}  // namespace
+
+rl_status rl_grpo_surrogate_workspace_size(int64_t rows, int64_t num_prompts, int32_t group_size,
+                                           size_t *bytes) {
+    g_last_error.clear();
+    if (!bytes) return set_error(RL_ERR_NULL_POINTER, "bytes is NULL");
+    GrpoLayout lay;
+    const rl_status st = grpo_layout(rows, num_prompts, group_size, &lay);
+    if (st != RL_OK) return st;
+    *bytes = lay.total;
+    return RL_OK;
+}
+
+rl_status rl_grpo_surrogate(int64_t rows, int64_t num_prompts, int32_t group_size,
+                            const float *logp_new, const float *logp_old, const int32_t *seq,
+                            const float *adv, float eps, float *loss, float *grad,
+                            void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error.clear();
+    GrpoLayout lay;
+    const rl_status st = grpo_layout(rows, num_prompts, group_size, &lay);
+    if (st != RL_OK) return st;
+    if (!(std::isfinite(eps) && eps >= 0.f && eps < 1.f))
+        return set_error(RL_ERR_INVALID_SHAPE, "eps must be finite and in [0, 1)");
+    if (!loss) return set_error(RL_ERR_NULL_POINTER, "loss is NULL");
+    if (rows > 0 && (!logp_new || !logp_old || !seq || !grad))
+        return set_error(RL_ERR_NULL_POINTER, "logp_new, logp_old, seq and grad must not be NULL");
+    if (num_prompts > 0 && !adv) return set_error(RL_ERR_NULL_POINTER, "adv is NULL");
+    const void *ptrs[] = {logp_new, logp_old, seq, adv, loss, grad};
+    for (const void *p : ptrs)
+        if (p && !aligned4(p)) return set_error(RL_ERR_MISALIGNED, "a pointer is not 4-byte aligned");
+    if (!workspace || workspace_bytes < lay.total)
+        return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(lay.total) + " bytes, got " +
+                                               std::to_string(workspace_bytes));
+    if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+    unsigned char *ws = static_cast<unsigned char *>(workspace);
+    rlk::GrpoArgs a{};
+    a.rows = rows;
+    a.P = num_prompts;
+    a.G = group_size;
+    a.S = num_prompts * group_size;
+    a.eps = eps;
+    a.logp_new = logp_new;
+    a.logp_old = logp_old;
+    a.adv = adv;
+    a.seq = seq;
+    a.loss = loss;
+    a.grad = grad;
+    a.counts = reinterpret_cast<int32_t *>(ws + lay.off_counts);
+    a.partials = reinterpret_cast<double *>(ws + lay.off_partials);
+    const hipError_t e = rlk::launch_grpo_surrogate(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_error(e, "launching the GRPO surrogate");
     return RL_OK;
 }
 

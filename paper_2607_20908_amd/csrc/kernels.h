@@ -45,4 +45,21 @@ struct LogprobArgs {
 
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream);
 
+hipError_t launch_grpo_advantage(int64_t P, int32_t G, const float *reward, float *adv, hipStream_t stream);
+
+struct GrpoArgs {
+    int64_t rows, P, S;         // token rows, prompts, candidates (P * G)
+    int32_t G;
+    float eps;
+    const float *logp_new, *logp_old, *adv;
+    const int32_t *seq;
+    float *loss, *grad;
+    int32_t *counts;            // workspace: rows per candidate [S]
+    double *partials;           // workspace: per-workgroup term sums
+};
+
+// Workgroups of the per-row kernel (one partial sum each).
+int64_t grpo_term_blocks(int64_t rows);
+hipError_t launch_grpo_surrogate(const GrpoArgs &a, hipStream_t stream);
+
 }  // namespace rlk

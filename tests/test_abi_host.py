@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 2
+    assert lib.rl_abi_version() == 3
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -197,3 +197,78 @@ def test_binding_refuses_host_tensors():
     t = torch.zeros(4, dtype=torch.int32)
     with pytest.raises(ValueError, match="device tensor"):
         rk.token_logprob(x, w, t)
+
+
+# ------------------------------------------------------------------ GRPO
+def grpo_adv_call(P=4, G=8, r=FAKE, a=FAKE + 256):
+    lib = rk.lib()
+    st = lib.rl_grpo_advantage(P, G, r, a, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(r=None), NULLP),
+    (dict(a=None), NULLP),
+    (dict(P=-1), SHAPE),
+    (dict(G=0), SHAPE),
+    (dict(G=-3), SHAPE),
+    (dict(G=1025), UNSUP),
+    (dict(r=FAKE + 2), MISAL),
+    (dict(a=FAKE + 1), MISAL),
+])
+def test_grpo_advantage_validation(kw, expect):
+    st, msg = grpo_adv_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg
+
+
+def test_grpo_advantage_empty_is_noop():
+    st, msg = grpo_adv_call(P=0, r=None, a=None)
+    assert st == OK and msg == ""
+
+
+def grpo_sur_call(R=100, P=4, G=8, new=FAKE, old=FAKE + 1024, seq=FAKE + 2048, adv=FAKE + 4096,
+                  eps=0.2, loss=FAKE + 8192, grad=FAKE + 8448, ws=FAKE + 16384, ws_bytes=1 << 20):
+    lib = rk.lib()
+    st = lib.rl_grpo_surrogate(R, P, G, new, old, seq, adv, eps, loss, grad, ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(new=None), NULLP),
+    (dict(old=None), NULLP),
+    (dict(seq=None), NULLP),
+    (dict(adv=None), NULLP),
+    (dict(loss=None), NULLP),
+    (dict(grad=None), NULLP),
+    (dict(R=-1), SHAPE),
+    (dict(P=-2), SHAPE),
+    (dict(G=0), SHAPE),
+    (dict(eps=-0.1), SHAPE),
+    (dict(eps=1.0), SHAPE),
+    (dict(eps=float("inf")), SHAPE),
+    (dict(eps=float("nan")), SHAPE),
+    (dict(new=FAKE + 2), MISAL),
+    (dict(seq=FAKE + 2049), MISAL),
+    (dict(grad=FAKE + 8450), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws_bytes=16), WSPACE),
+    (dict(ws=FAKE + 16388), MISAL),
+])
+def test_grpo_surrogate_validation(kw, expect):
+    st, msg = grpo_sur_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg
+
+
+def test_grpo_surrogate_workspace_size():
+    # one int32 count per candidate, one fp64 partial per 256 rows
+    for R, P, G in [(262144, 4, 16), (0, 0, 1), (1, 1, 1), (1000, 4096, 16)]:
+        n = rk.grpo_surrogate_workspace_size(R, P, G)
+        assert n >= P * G * 4 + -(-R // 256) * 8
+        assert n % 256 == 0 and n > 0
+        assert n <= P * G * 4 + -(-R // 256) * 8 + 512
+    with pytest.raises(rk.RLError):
+        rk.grpo_surrogate_workspace_size(-1, 1, 1)
+    with pytest.raises(rk.RLError):
+        rk.grpo_surrogate_workspace_size(1, 1 << 30, 16)

@@ -205,3 +205,62 @@ def bf16_bits(x: torch.Tensor) -> np.ndarray:
 
 def bits_to_bf16(bits: np.ndarray, device="cpu") -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(device)
+
+
+# ----------------------------------------------------------------- GRPO update
+@dataclasses.dataclass(frozen=True)
+class GrpoConfig:
+    name: str
+    num_prompts: int     # P
+    group_size: int      # G
+    positions: int       # token positions per sequence (row r = s * positions + t)
+    max_response: int    # longest generated response; the rest of a row is prompt or padding
+
+
+# The policy-update pass as 4 prompts x 16 candidates = 64 sequences of 4096
+# positions (the log-prob pass's 262144 rows), each candidate with up to 1536
+# generated tokens; a small case of the same structure for exhaustive checks.
+GRPO_CONFIGS = {
+    "tiny": GrpoConfig("tiny", 3, 4, 48, 32),
+    "policy": GrpoConfig("policy", 4, 16, 4096, 1536),
+}
+
+
+@dataclasses.dataclass
+class GrpoInputs:
+    cfg: GrpoConfig
+    reward: torch.Tensor     # fp32 [P*G]
+    logp_old: torch.Tensor   # fp32 [R]  log-probs under the sampling policy
+    logp_new: torch.Tensor   # fp32 [R]  log-probs under the current policy
+    seq: torch.Tensor        # int32 [R] candidate of each row, -1 = prompt or padding
+    eps: float               # clip range, an exact float32 value
+
+
+def make_grpo_inputs(cfg: GrpoConfig, device="cpu", seed: int = 0, eps: float = 0.2,
+                     drift: float = 0.1, reward_levels: int = 5,
+                     equal_group: bool = True) -> GrpoInputs:
+    """Rows of P*G sequences laid end to end, `positions` rows each.  Sequence s
+    holds its prompt in the first positions - max_response rows (masked), then a
+    response of uniform length in [1, max_response] (rows tagged s), then
+    padding (masked).  Rewards are drawn from `reward_levels` evenly spaced
+    values in [0, 1], so ties occur; with equal_group, prompt 0's candidates all
+    get the same reward.  Old log-probs are -Exp(1); new ones add N(0, drift^2),
+    so ratios fall inside and on both sides of the clip range."""
+    P, G, T, M = cfg.num_prompts, cfg.group_size, cfg.positions, cfg.max_response
+    S = P * G
+    rng = np.random.Generator(np.random.PCG64(seed))
+    levels = np.linspace(0.0, 1.0, max(reward_levels, 1))
+    reward = levels[rng.integers(0, len(levels), S)].astype(np.float32)
+    if equal_group and P > 0 and G > 1:
+        reward[:G] = reward[0]
+    lens = rng.integers(1, M + 1, S)
+    seq = np.full((S, T), -1, np.int32)
+    start = T - M
+    for s in range(S):
+        seq[s, start:start + lens[s]] = s
+    seq = seq.reshape(-1)
+    R = seq.size
+    old = (-rng.exponential(1.0, R)).astype(np.float32)
+    new = (old + rng.normal(0.0, drift, R)).astype(np.float32)
+    dev = lambda a: torch.from_numpy(a).to(device)
+    return GrpoInputs(cfg, dev(reward), dev(old), dev(new), dev(seq), float(np.float32(eps)))
