@@ -19,6 +19,11 @@
  *                     the logits; masked positions (Sec. 3, Multi-turn RL
  *                     Training: masked log-probabilities) give 0.
  *
+ *  rl_token_logprob_backward
+ *                     d logprob / d hidden through the lm-head, scaled by
+ *                     the incoming gradient per row (the policy update's
+ *                     backward through the token log-probs, Sec. 3).
+ *
  *  rl_grpo_advantage  group-relative advantages of the candidates' rewards
  *                     (Sec. 3, the definition under Eq. grpo-loss).
  *
@@ -38,9 +43,11 @@
  * does not wait for the stream.  Calls on different streams need distinct
  * workspaces.
  *
- * Errors: a call that returns anything other than RL_OK has enqueued nothing
- * and written no output; rl_last_error() then describes the problem.  Argument
- * errors are detected on the host before any launch.  RL_OK means the work is
+ * Errors: rl_last_error() describes the problem of a failing call.  Argument
+ * errors are detected on the host before any launch: a call that returns
+ * any status but RL_OK or RL_ERR_HIP has enqueued nothing and written no
+ * output.  RL_ERR_HIP reports a failed kernel launch; launches of the same
+ * call before it may already be enqueued.  RL_OK means the work is
  * enqueued: outputs are valid after the stream is synchronised, and inputs,
  * outputs and workspace must stay alive until then.
  */
@@ -54,7 +61,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 3
+#define RL_ABI_VERSION 4
 
 typedef enum {
     RL_OK = 0,
@@ -169,6 +176,40 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab,
                            const int32_t *target, float inv_temperature,
                            float *logprob, float *lse,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Backward of rl_token_logprob with respect to the hidden rows, for the
+ * policy update through a frozen lm-head (Sec. 3, Eq. grpo-loss: the token
+ * ratio's gradient reaches the policy through log pi; the lm-head weight
+ * itself is not trained).  With p_v = exp(z_v - lse[r]) (z as above):
+ *   grad_hidden[r, :] = grad_logprob[r] * inv_temperature
+ *                       * (w_lm[t, :] - sum_v p_v w_lm[v, :])   t = target[r] in [0, V),
+ *                     = 0                                       t == -1,
+ *                     = NaN                                     any other t.
+ * The logits are recomputed; p is held in the workspace as bf16, one chunk
+ * of at most 16384 rows at a time, and never returned.
+ *
+ *   hidden_states, w_lm, target, inv_temperature   as for rl_token_logprob
+ *   lse            device fp32 [rows], the lse rl_token_logprob returned for
+ *                  the same inputs (read only for rows with a valid target)
+ *   grad_logprob   device fp32 [rows], d loss / d logprob[r]
+ *   grad_hidden    device fp32 [rows, hidden], written (not accumulated)
+ *
+ * The workspace holds chunk_rows x vocab (padded to 256) bf16 probabilities
+ * plus, when rows are few, fp32 partial sums of a vocabulary split; its size
+ * depends on (rows, hidden, vocab) only.  w_lm must be finite.  rows == 0 is
+ * a valid no-op.  Status: as rl_token_logprob; hidden_states, w_lm and
+ * grad_hidden 16-byte aligned, target, lse and grad_logprob 4-byte aligned.
+ */
+rl_status rl_token_logprob_backward_workspace_size(int64_t rows, int32_t hidden, int32_t vocab,
+                                                   size_t *bytes);
+
+rl_status rl_token_logprob_backward(int64_t rows, int32_t hidden, int32_t vocab,
+                                    const void *hidden_states, const void *w_lm,
+                                    const int32_t *target, float inv_temperature,
+                                    const float *lse, const float *grad_logprob,
+                                    float *grad_hidden,
+                                    void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* GRPO advantages and clipped surrogate (Sec. 3, Eq. grpo-loss)             */

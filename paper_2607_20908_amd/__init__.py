@@ -71,7 +71,7 @@ class PlanItem(ctypes.Structure):
 EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_workspace_size",
            "rl_token_logprob", "rl_status_string", "rl_last_error", "rl_abi_version",
            "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
-           "rl_grpo_surrogate"]
+           "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward"]
 
 
 def _load():
@@ -100,7 +100,11 @@ def _load():
     lib.rl_grpo_surrogate_workspace_size.argtypes = [I64, I64, I32, ctypes.POINTER(SZ)]
     lib.rl_grpo_surrogate.restype = ctypes.c_int
     lib.rl_grpo_surrogate.argtypes = [I64, I64, I32, P, P, P, P, ctypes.c_float, P, P, P, SZ, P]
-    if lib.rl_abi_version() != 3:
+    lib.rl_token_logprob_backward_workspace_size.restype = ctypes.c_int
+    lib.rl_token_logprob_backward_workspace_size.argtypes = [I64, I32, I32, ctypes.POINTER(SZ)]
+    lib.rl_token_logprob_backward.restype = ctypes.c_int
+    lib.rl_token_logprob_backward.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, P, SZ, P]
+    if lib.rl_abi_version() != 4:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -307,6 +311,47 @@ def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor
                                  ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                  _stream_handle(stream)), "rl_token_logprob")
     return logprob, lse
+
+
+def token_logprob_backward_workspace_size(rows: int, hidden: int, vocab: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_token_logprob_backward_workspace_size(rows, hidden, vocab, ctypes.byref(n)),
+           "rl_token_logprob_backward_workspace_size")
+    return n.value
+
+
+def token_logprob_backward(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
+                           lse: torch.Tensor, grad_logprob: torch.Tensor, inv_temperature: float = 1.0,
+                           grad_hidden: Optional[torch.Tensor] = None,
+                           workspace: Optional[torch.Tensor] = None, stream=None):
+    """d(sum_r grad_logprob[r] * logprob[r]) / d hidden, fp32 [R, H].
+
+    lse is the forward's lse for the same inputs (token_logprob's second output).
+    """
+    _bf16_dev(hidden, "hidden")
+    _bf16_dev(w_lm, "w_lm")
+    _on_device(target, "target")
+    if target.dtype != torch.int32 or not target.is_contiguous():
+        raise TypeError("target must be a contiguous int32 tensor")
+    R, H = hidden.shape
+    V, H2 = w_lm.shape
+    if H2 != H or target.shape != (R,):
+        raise ValueError("shapes: hidden [R, H], w_lm [V, H], target [R]")
+    _f32_dev(lse, "lse", (R,))
+    _f32_dev(grad_logprob, "grad_logprob", (R,))
+    if grad_hidden is None:
+        grad_hidden = torch.empty(R, H, dtype=torch.float32, device=hidden.device)
+    _f32_dev(grad_hidden, "grad_hidden", (R, H))
+    need = token_logprob_backward_workspace_size(R, H, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    _on_device(workspace, "workspace")
+    _check(_lib.rl_token_logprob_backward(R, H, V, _ptr(hidden), _ptr(w_lm), _ptr(target),
+                                          float(inv_temperature), _ptr(lse), _ptr(grad_logprob),
+                                          _ptr(grad_hidden), ctypes.c_void_p(workspace.data_ptr()),
+                                          workspace.numel(), _stream_handle(stream)),
+           "rl_token_logprob_backward")
+    return grad_hidden
 
 
 def _f32_dev(t: torch.Tensor, name: str, shape) -> torch.Tensor:

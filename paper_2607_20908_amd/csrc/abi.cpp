@@ -252,6 +252,86 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
 
 static bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
+rl_status rl_token_logprob_backward_workspace_size(int64_t rows, int32_t hidden, int32_t vocab, size_t *bytes) {
+    g_last_error.clear();
+    if (!bytes) return set_error(RL_ERR_NULL_POINTER, "bytes is NULL");
+    rlk::LogprobBwdPlan plan;
+    std::string err;
+    const rl_status st = rlk::plan_logprob_bwd(rows, hidden, vocab, &plan, &err);
+    if (st != RL_OK) return set_error(st, err);
+    *bytes = plan.total_bytes;
+    return RL_OK;
+}
+
+rl_status rl_token_logprob_backward(int64_t rows, int32_t hidden, int32_t vocab, const void *hidden_states,
+                                    const void *w_lm, const int32_t *target, float inv_temperature,
+                                    const float *lse, const float *grad_logprob, float *grad_hidden,
+                                    void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error.clear();
+    rlk::LogprobBwdPlan plan;
+    std::string err;
+    rl_status st = rlk::plan_logprob_bwd(rows, hidden, vocab, &plan, &err);
+    if (st != RL_OK) return set_error(st, err);
+    if (!(std::isfinite(inv_temperature) && inv_temperature > 0.f))
+        return set_error(RL_ERR_INVALID_SHAPE, "inv_temperature must be finite and > 0");
+    if (rows == 0) return RL_OK;
+    if (!hidden_states || !w_lm || !target || !lse || !grad_logprob || !grad_hidden)
+        return set_error(RL_ERR_NULL_POINTER,
+                         "hidden_states, w_lm, target, lse, grad_logprob and grad_hidden must not be NULL");
+    if (!aligned16(hidden_states) || !aligned16(w_lm) || !aligned16(grad_hidden))
+        return set_error(RL_ERR_MISALIGNED, "hidden_states, w_lm and grad_hidden must be 16-byte aligned");
+    if (!aligned4(target) || !aligned4(lse) || !aligned4(grad_logprob))
+        return set_error(RL_ERR_MISALIGNED, "target, lse and grad_logprob must be 4-byte aligned");
+    if (!workspace || workspace_bytes < plan.total_bytes)
+        return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(plan.total_bytes) +
+                                               " bytes, got " + std::to_string(workspace_bytes));
+    if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+    unsigned char *ws = static_cast<unsigned char *>(workspace);
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const uint16_t *hid = static_cast<const uint16_t *>(hidden_states);
+    const uint16_t *w = static_cast<const uint16_t *>(w_lm);
+    uint16_t *probs = reinterpret_cast<uint16_t *>(ws + plan.off_probs);
+    for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
+        const int64_t n = std::min(plan.chunk_rows, rows - c0);
+        const int32_t row_tiles = static_cast<int32_t>((n + rlk::kRowTile - 1) / rlk::kRowTile);
+        rlk::LogprobArgs f{};
+        f.hidden = hid + c0 * hidden;
+        f.w = w;
+        f.target = target + c0;
+        f.R = n;
+        f.H = hidden;
+        f.V = vocab;
+        f.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
+        f.n_row_tiles = row_tiles;
+        f.inv_temperature = inv_temperature;
+        f.lse_in = lse + c0;
+        f.probs = probs;
+        hipError_t e = rlk::launch_logprob_probs(f, hs);
+        if (e != hipSuccess) return hip_error(e, "launching the log-prob backward (probabilities)");
+        rlk::LogprobBwdArgs b{};
+        b.w = w;
+        b.target = target + c0;
+        b.grad = grad_logprob + c0;
+        b.dh = grad_hidden + c0 * hidden;
+        b.probs = probs;
+        b.dpart = plan.splits > 1 ? reinterpret_cast<float *>(ws + plan.off_part) : b.dh;
+        b.rows = n;
+        b.H = hidden;
+        b.V = vocab;
+        b.n_vsteps = plan.n_vsteps;
+        b.n_row_tiles = row_tiles;
+        b.n_h_tiles = plan.n_h_tiles;
+        b.splits = plan.splits;
+        b.steps_per_split = plan.steps_per_split;
+        b.inv_temperature = inv_temperature;
+        e = rlk::launch_logprob_bwd_gemm(b, hs);
+        if (e != hipSuccess) return hip_error(e, "launching the log-prob backward (GEMM)");
+        e = rlk::launch_logprob_bwd_finish(b, hs);
+        if (e != hipSuccess) return hip_error(e, "launching the log-prob backward (finish)");
+    }
+    return RL_OK;
+}
+
 rl_status rl_grpo_advantage(int64_t num_prompts, int32_t group_size, const float *reward, float *adv,
                             void *stream) {
     g_last_error.clear();

@@ -41,9 +41,40 @@ struct LogprobArgs {
     int32_t H, V;
     int32_t n_vocab_tiles, n_row_tiles;
     float inv_temperature;
+    // backward only: the forward's lse per row (input) and the probabilities
+    // p = exp(inv_T z - lse) as bf16 in the blocked layout of
+    // LogprobBwdArgs::probs (output); pm, pl, zt, logprob are then unused
+    const float *lse_in;
+    uint16_t *probs;
 };
 
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream);
+
+// Backward of the token log-prob with respect to the hidden rows, for one
+// chunk of rows at a time (the probabilities of a chunk live in the
+// workspace):
+//   dh[r] = g[r] inv_T (W[t_r] - sum_v p[r, v] W[v]).
+// probs: bf16, blocked: for row tile rt and vocab step ks (64 entries), a
+// 256 x 64 block at element ((rt * n_vsteps) + ks) * 16384 laid out as the
+// LDS stage image op_off(row, chunk); entries past the vocabulary and rows
+// without a valid target hold 0.
+struct LogprobBwdArgs {
+    const uint16_t *w;          // [V, H]
+    const int32_t *target;      // [R]  (chunk-relative pointers below)
+    const float *grad;          // [R]
+    float *dh;                  // [R, H] fp32
+    const uint16_t *probs;      // blocked probabilities of the chunk
+    float *dpart;               // [splits, rows_pad, H] fp32 partial sums
+    int64_t rows;               // rows in this chunk
+    int32_t H, V;
+    int32_t n_vsteps;           // vocab steps of 64 (padded vocabulary / 64)
+    int32_t n_row_tiles, n_h_tiles, splits, steps_per_split;
+    float inv_temperature;
+};
+
+hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream);
+hipError_t launch_logprob_bwd_gemm(const LogprobBwdArgs &a, hipStream_t stream);
+hipError_t launch_logprob_bwd_finish(const LogprobBwdArgs &a, hipStream_t stream);
 
 hipError_t launch_grpo_advantage(int64_t P, int32_t G, const float *reward, float *adv, hipStream_t stream);
 

@@ -316,6 +316,42 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
     return RL_OK;
 }
 
+rl_status plan_logprob_bwd(int64_t rows, int32_t hidden, int32_t vocab, LogprobBwdPlan *plan,
+                           std::string *err) {
+    LogprobPlan fwd;
+    const rl_status st = plan_logprob(rows, hidden, vocab, &fwd, err);
+    if (st != RL_OK) return st;
+    LogprobBwdPlan &pl = *plan;
+    pl = LogprobBwdPlan{};
+    pl.R = rows;
+    pl.H = hidden;
+    pl.V = vocab;
+    pl.n_vocab_tiles = ceil_div(vocab, kVocabTile);
+    pl.n_vsteps = static_cast<int32_t>(pl.n_vocab_tiles * (kVocabTile / kHiddenStep));
+    pl.n_h_tiles = static_cast<int32_t>(ceil_div(hidden, 256));
+    if (rows == 0) return RL_OK;
+    pl.chunk_rows = std::min<int64_t>(rows, kBwdChunkRows);
+    pl.n_chunks = ceil_div(rows, pl.chunk_rows);
+    pl.chunk_row_tiles = static_cast<int32_t>(ceil_div(pl.chunk_rows, kRowTile));
+    // Split the vocabulary when a chunk has fewer output tiles than the GPU
+    // has compute units, keeping at least 16 vocab steps per split.
+    const int64_t tiles = static_cast<int64_t>(pl.chunk_row_tiles) * pl.n_h_tiles;
+    int64_t splits = tiles >= 256 ? 1 : 256 / tiles;
+    splits = std::max<int64_t>(1, std::min<int64_t>(splits, pl.n_vsteps / 16));
+    pl.steps_per_split = static_cast<int32_t>(ceil_div(pl.n_vsteps, splits));
+    pl.splits = static_cast<int32_t>(ceil_div(pl.n_vsteps, pl.steps_per_split));
+    if (tiles * pl.splits > INT32_MAX || pl.n_vocab_tiles * pl.chunk_row_tiles > INT32_MAX)
+        return fail(err, RL_ERR_UNSUPPORTED, "too many tiles");
+    const size_t rows_pad = static_cast<size_t>(pl.chunk_row_tiles) * kRowTile;
+    size_t off = 0;
+    pl.off_probs = off;
+    off = align_up(off + rows_pad * static_cast<size_t>(pl.n_vsteps) * kHiddenStep * 2, 256);
+    pl.off_part = off;
+    if (pl.splits > 1) off = align_up(off + static_cast<size_t>(pl.splits) * rows_pad * hidden * 4, 256);
+    pl.total_bytes = off;
+    return RL_OK;
+}
+
 rl_status check_logprob_args(const LogprobPlan &pl, const void *hidden_states,
                              const void *w_lm, const int32_t *target, float inv_temperature,
                              const float *logprob, const float *lse, std::string *err) {

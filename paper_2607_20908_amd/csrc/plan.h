@@ -101,6 +101,28 @@ rl_status check_logprob_args(const LogprobPlan &plan, const void *hidden_states,
                              const void *w_lm, const int32_t *target, float inv_temperature,
                              const float *logprob, const float *lse, std::string *err);
 
+// Backward of the token log-prob: rows are processed in chunks whose bf16
+// probabilities (chunk rows x padded vocabulary) live in the workspace,
+// followed by the split partial sums when the GEMM is split over the
+// vocabulary.
+constexpr int64_t kBwdChunkRows = 16384;
+
+struct LogprobBwdPlan {
+    int64_t R = 0;
+    int32_t H = 0, V = 0;
+    int64_t chunk_rows = 0;          // rows per chunk (the last may have fewer)
+    int64_t n_chunks = 0;
+    int64_t n_vocab_tiles = 0;       // 256-entry vocab tiles
+    int32_t n_vsteps = 0;            // 64-entry vocab steps = 4 * n_vocab_tiles
+    int32_t chunk_row_tiles = 0;     // 256-row tiles of a full chunk
+    int32_t n_h_tiles = 0;           // 256-entry hidden tiles
+    int32_t splits = 1, steps_per_split = 0;
+    size_t off_probs = 0, off_part = 0, total_bytes = 0;
+};
+
+rl_status plan_logprob_bwd(int64_t rows, int32_t hidden, int32_t vocab, LogprobBwdPlan *plan,
+                           std::string *err);
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace rlk

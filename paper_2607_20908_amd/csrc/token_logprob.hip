@@ -20,6 +20,7 @@
 // log-sum-exp and subtract it from the target logit.
 #include "device_common.h"
 #include "kernels.h"
+#include "lds_stage.h"
 
 namespace rlk {
 namespace {
@@ -33,67 +34,13 @@ constexpr int kTileThreads = 256;               // 4 waves
 constexpr int kBlocksPerWave = kTileElems / 512 / 4;   // 1 KB load blocks per wave per operand per stage
 static_assert(kBlocksPerWave == 8, "staging layout");
 
-// Element offset of 16-byte chunk c (0..7) of tile row `row` in a stage buffer.
-// Rows are 128 bytes, so two rows share one 256-byte window of the 64 LDS
-// banks; XOR-ing the chunk with row bits 1..3 gives the 16 rows that one
-// ds_read_b128 pass serves (same chunk, consecutive rows) 16 distinct 16-byte
-// slots of that window.
-__device__ __forceinline__ int op_off(int row, int c) { return row * kK + ((c ^ ((row >> 1) & 7)) << 3); }
-
-// Maps the launch index to a (vocab tile, row tile).  The hardware hands
-// consecutive workgroups to the 8 XCDs in turn; renumbering gives each XCD a
-// contiguous run of logical tiles, and inside a run 4 row tiles sweep the
-// vocabulary together, so a weight tile is fetched into an XCD's L2 once for
-// 4 row tiles and the row tiles stay resident in L2 / the MALL.
-__device__ __forceinline__ void tile_of(int64_t b, int64_t nvt, int64_t nrt, int64_t *vt, int64_t *rt) {
-    const int64_t total = nvt * nrt;
-    const int64_t full = total / 8 * 8;
-    const int64_t L = b < full ? (b % 8) * (total / 8) + b / 8 : b;
-    constexpr int64_t GR = 4;
-    const int64_t group = L / (GR * nvt);
-    const int64_t in = L % (GR * nvt);
-    const int64_t rows_in_group = min(GR, nrt - group * GR);
-    *rt = group * GR + in % rows_in_group;
-    *vt = in / rows_in_group;
-}
-
-// 16 bytes global -> LDS, bypassing the registers.  Lane i of a wave writes
-// LDS bytes [base + 16 i, +16) (base in M0, wave-uniform), so one instruction
-// fills 1 KB contiguously.  Issued as inline assembly: the compiler then does
-// not know that it writes LDS and does not put a wait for all loads in flight
-// in front of every LDS read (it cannot tell the two stage buffers apart);
-// the kernel orders these loads against its LDS reads with explicit waits.
-__device__ __forceinline__ void load_lds16(const uint16_t *g, uint16_t *l) {
-    typedef __attribute__((address_space(3))) uint16_t lds_u16;
-    const uint32_t lds_addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l)));
-    asm volatile(
-        "s_mov_b32 m0, %1\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %0, off"
-        :
-        : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
-        : "memory", "m0");
-}
-
-// Wait until at most N vector-memory operations of this wave are outstanding.
-// The global->LDS loads are tracked by this counter; the compiler does not see
-// when their LDS bytes are read, so the waits are explicit.
-template <int N>
-__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
-
-__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-__device__ __forceinline__ void barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
 // WS: weight-ring depth.  With few row tiles the hidden rows stay in L2 and
 // only the weights stream from HBM; a third weight stage gives them two
 // stages to arrive (WS = 3 fills the whole 160 KB of LDS).  With many row
 // tiles both operands miss and WS = 2 measures better.
-template <int WS>
+// BWD: instead of the (max, sum) partials, write p = exp(inv_T z - lse) per
+// (row, vocab entry) as bf16 into the blocked probability buffer.
+template <int WS, bool BWD>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
     // WS x 32 KB weight stages + 2 x 32 KB hidden stages; the epilogue's
     // reduction area reuses the weight ring once the loop is done
@@ -224,6 +171,48 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     wait_vm<0>();
     barrier();                                   // the reduction area aliases the weight ring
     __builtin_amdgcn_sched_barrier(0);
+
+    if constexpr (BWD) {
+        // acc[tm][tn][i]: vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4,
+        // row r0 + wn*128 + tn*32 + l32.  The 4 consecutive entries i%4 are one
+        // 8-byte store into vocab step vt*4 + wm*2 + tm/2, chunk (tm%2)*4 + i/4.
+        const float c2 = a.inv_temperature * kLog2e;
+        const int64_t vbase = v0 + wm * 128;
+        const int vlim = vbase + 128 <= a.V ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
+        uint16_t *pb = a.probs + (rt * (a.n_vocab_tiles * 4LL) + vt * 4 + wm * 2) * kTileElems;
+#pragma unroll
+        for (int tn = 0; tn < 4; ++tn) {
+            const int row = wn * 128 + tn * 32 + l32;
+            const int64_t rr = r0 + row;
+            bool live = false;
+            float l2 = 0.f;
+            if (rr < a.R) {
+                const int32_t t = a.target[rr];
+                live = t >= 0 && t < a.V;
+                l2 = a.lse_in[rr] * kLog2e;
+            }
+#pragma unroll
+            for (int tm = 0; tm < 4; ++tm) {
+                const f32x16 z = acc[tm][tn];
+                uint16_t *blk = pb + (tm >> 1) * kTileElems;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t w2[2];
+#pragma unroll
+                    for (int e = 0; e < 4; e += 2) {
+                        const int loc = tm * 32 + 8 * q + e;
+                        const float p0 = live && loc < vlim ? fast_exp2(z[4 * q + e] * c2 - l2) : 0.f;
+                        const float p1 = live && loc + 1 < vlim ? fast_exp2(z[4 * q + e + 1] * c2 - l2) : 0.f;
+                        w2[e >> 1] = static_cast<uint32_t>(f32_to_bf16_bits(p0)) |
+                                     (static_cast<uint32_t>(f32_to_bf16_bits(p1)) << 16);
+                    }
+                    *reinterpret_cast<uint2 *>(blk + op_off(row, (tm & 1) * 4 + q) + 4 * h2) = make_uint2(w2[0], w2[1]);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        return;
+    }
 
     // ---- epilogue: per token row, max / sum of exp2 / target logit ---------
     // acc[tm][tn][i] holds vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4
@@ -362,9 +351,11 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
     const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
     if (a.n_row_tiles <= 8)
-        hipLaunchKernelGGL(logprob_tile_kernel<3>, dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0, stream, a);
+        hipLaunchKernelGGL((logprob_tile_kernel<3, false>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+                           stream, a);
     else
-        hipLaunchKernelGGL(logprob_tile_kernel<2>, dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0, stream, a);
+        hipLaunchKernelGGL((logprob_tile_kernel<2, false>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+                           stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.R < 32768) {
@@ -376,6 +367,17 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
         hipLaunchKernelGGL(logprob_combine_row_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
                            stream, a);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream) {
+    const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
+    if (a.n_row_tiles <= 8)
+        hipLaunchKernelGGL((logprob_tile_kernel<3, true>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((logprob_tile_kernel<2, true>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+                           stream, a);
     return hipGetLastError();
 }
 

@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 3
+    assert lib.rl_abi_version() == 4
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -272,3 +272,61 @@ def test_grpo_surrogate_workspace_size():
         rk.grpo_surrogate_workspace_size(-1, 1, 1)
     with pytest.raises(rk.RLError):
         rk.grpo_surrogate_workspace_size(1, 1 << 30, 16)
+
+
+# ------------------------------------------------------- log-prob backward
+def logprob_bwd_call(R=8, H=256, V=1000, hs=FAKE, w=FAKE + 256, t=FAKE + 512, invT=1.0,
+                     lse=FAKE + 768, g=FAKE + 1024, dh=FAKE + 2048, ws=FAKE, ws_bytes=1 << 30):
+    lib = rk.lib()
+    st = lib.rl_token_logprob_backward(R, H, V, hs, w, t, invT, lse, g, dh, ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(hs=None), NULLP),
+    (dict(w=None), NULLP),
+    (dict(t=None), NULLP),
+    (dict(lse=None), NULLP),
+    (dict(g=None), NULLP),
+    (dict(dh=None), NULLP),
+    (dict(R=-1), SHAPE),
+    (dict(H=0), SHAPE),
+    (dict(V=0), SHAPE),
+    (dict(invT=0.0), SHAPE),
+    (dict(invT=float("inf")), SHAPE),
+    (dict(H=100), UNSUP),
+    (dict(hs=FAKE + 8), MISAL),
+    (dict(w=FAKE + 4), MISAL),
+    (dict(dh=FAKE + 2056), MISAL),
+    (dict(t=FAKE + 2), MISAL),
+    (dict(lse=FAKE + 1), MISAL),
+    (dict(g=FAKE + 2), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws_bytes=16), WSPACE),
+    (dict(ws=FAKE + 4), MISAL),
+])
+def test_logprob_backward_validation(kw, expect):
+    st, msg = logprob_bwd_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg
+
+
+def test_logprob_backward_empty_is_noop():
+    st, msg = logprob_bwd_call(R=0, hs=None, w=None, t=None, lse=None, g=None, dh=None, ws=None, ws_bytes=0)
+    assert st == OK and msg == ""
+
+
+def test_logprob_backward_workspace_size():
+    V = 151936
+    vpad = -(-V // 256) * 256
+    # one chunk of probabilities (at most 16384 rows, padded to 256) in bf16
+    for R, H in [(262144, 5120), (16384, 5120), (20000, 4096)]:
+        n = rk.token_logprob_backward_workspace_size(R, H, V)
+        assert n == 16384 * vpad * 2
+    # few rows: the vocabulary is split and fp32 partial sums follow
+    n = rk.token_logprob_backward_workspace_size(512, 4096, V)
+    probs = 512 * vpad * 2
+    assert n > probs and (n - probs) % (512 * 4096 * 4) == 0
+    assert rk.token_logprob_backward_workspace_size(0, 64, 10) == 0
+    with pytest.raises(rk.RLError):
+        rk.token_logprob_backward_workspace_size(4, 100, 10)

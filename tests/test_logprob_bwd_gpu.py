@@ -1,0 +1,226 @@
+"""Backward of the token log-prob with respect to the hidden rows: the HIP path
+against the fp64 oracle on the same bits.
+
+Tolerance, derived from the arithmetic.  dh[r] = s_r (W[t] - sum_v p_v W[v])
+with s_r = g_r inv_T.  The GPU holds p in bf16 (relative rounding <= 2^-9)
+and recomputes it from fp32 logits and the forward's fp32 lse (relative
+error ~1e-5).  Since sum_v p_v = 1, the error of sum_v p_v W[v, h] is at most
+(2^-9 + 1e-4) max_v |W[v, h]|; the fp32 accumulation adds far less.  The test
+allows |dh_gpu - dh_oracle| <= |s_r| 2^-8 max|W| per row (about twice the
+bound), plus a relative Frobenius error <= 2e-3 over all valid rows.  Masked
+rows (target -1) are exactly 0, invalid targets NaN.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_20908_amd as rk
+import workloads as W
+from gpu_util import dev, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def rand_bits(rng, shape, std=1.0):
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32) * std)
+    return W.bf16_bits(x.to(torch.bfloat16))
+
+
+def bits_f64(bits):
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def gpu_backward(h, w, t, g, inv_T=1.0, lse=None):
+    """h, w: device bf16; t: device int32; g: device fp32.  lse from the GPU
+    forward unless given."""
+    if lse is None:
+        _, lse = rk.token_logprob(h, w, t, inv_T)
+    dh = rk.token_logprob_backward(h, w, t, lse, g, inv_T)
+    torch.cuda.synchronize()
+    return dh
+
+
+def check_rows(dh, ref, t, g, inv_T, wmax, V, what):
+    """dh, ref: [n, H] (GPU fp32, oracle fp64) for rows with targets t, grads g."""
+    dh = np.asarray(dh, np.float64)
+    valid = (t >= 0) & (t < V)
+    masked = t == -1
+    invalid = ~valid & ~masked
+    assert np.all(dh[masked] == 0), f"{what}: masked rows not 0"
+    assert np.all(np.isnan(dh[invalid])), f"{what}: invalid targets not NaN"
+    if not valid.any():
+        return 0.0
+    s = np.abs(np.asarray(g, np.float64)[valid]) * inv_T
+    err = np.abs(dh[valid] - ref[valid]).max(axis=1)
+    bound = s * 2.0 ** -8 * wmax
+    worst = float(np.max(err / np.maximum(bound, 1e-300)))
+    say(f"{what}: max err/bound {worst:.3g}")
+    assert np.all(err <= bound), f"{what}: row error {err.max():.3g} above bound"
+    num = np.linalg.norm(dh[valid] - ref[valid])
+    den = np.linalg.norm(ref[valid])
+    if den > 0:
+        assert num / den <= 2e-3, f"{what}: relative error {num / den:.3g}"
+    return worst
+
+
+def case(R, H, V, seed, hstd=1.0, wstd=0.05, inv_T=1.0, mask_frac=0.0, bad=(), gzero=0.0, what=""):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    hb = rand_bits(rng, (R, H), hstd)
+    wb = rand_bits(rng, (V, H), wstd)
+    t = rng.integers(0, V, R).astype(np.int32)
+    if mask_frac:
+        t[rng.random(R) < mask_frac] = -1
+    for i, val in bad:
+        t[i] = val
+    g = rng.standard_normal(R).astype(np.float32)
+    if gzero:
+        g[rng.random(R) < gzero] = 0.0
+    inv_T = float(np.float32(inv_T))
+    say(f"logprob backward {what} R={R} H={H} V={V}")
+    h, w = to_dev(hb), to_dev(wb)
+    td = torch.from_numpy(t).to(dev())
+    gd = torch.from_numpy(g).to(dev())
+    dh = gpu_backward(h, w, td, gd, inv_T).cpu().numpy()
+    ref = oracle.token_logprob_backward(hb, wb, t, g.astype(np.float64), inv_T)
+    wmax = float(np.abs(bits_f64(wb)).max())
+    check_rows(dh, ref, t, g, inv_T, wmax, V, what)
+    return dh, ref, hb, wb, t, g
+
+
+def test_tiny_config():
+    x = W.make_logprob_inputs(W.LOGPROB_CONFIGS["tiny"], "cpu")
+    hb, wb, t = W.bf16_bits(x.hidden), W.bf16_bits(x.w_lm), x.target.numpy()
+    g = np.random.Generator(np.random.PCG64(1)).standard_normal(len(t)).astype(np.float32)
+    say("logprob backward tiny config")
+    dh = gpu_backward(to_dev(hb), to_dev(wb), x.target.to(dev()), torch.from_numpy(g).to(dev())).cpu().numpy()
+    ref = oracle.token_logprob_backward(hb, wb, t, g.astype(np.float64))
+    check_rows(dh, ref, t, g, 1.0, float(np.abs(bits_f64(wb)).max()), x.cfg.vocab, "tiny config")
+
+
+@pytest.mark.parametrize("R,H,V", [(300, 128, 1000),     # ragged rows and vocab, half-used hidden tile
+                                   (1, 64, 257),         # one row, one vocab entry past a tile
+                                   (513, 192, 511),      # 192 of 256 hidden entries in the tile
+                                   (256, 4096, 2048),    # 16 hidden tiles, vocabulary split 2 ways
+                                   (256, 256, 8192),     # one output tile, vocabulary split 8 ways
+                                   (2305, 64, 700),      # more than 8 row tiles: two-stage ring
+                                   (2049, 320, 300)])    # two hidden tiles, the second ragged
+def test_ragged_shapes(R, H, V):
+    case(R, H, V, seed=R + H + V, what=f"ragged")
+
+
+def test_several_row_chunks():
+    # more rows than one chunk of probabilities (16384): three chunks, the last short
+    case(16384 * 2 + 300, 64, 300, seed=21, wstd=0.1, what="three chunks")
+
+
+def test_temperature_masking_invalid_and_zero_grads():
+    R, H, V = 400, 256, 1500
+    dh, *_ = case(R, H, V, seed=7, wstd=0.08, inv_T=1.0 / 0.7, mask_frac=0.1,
+                  bad=((3, V), (50, -2), (399, 1 << 30)), gzero=0.1, what="temperature+mask")
+
+
+def test_peaky_distribution_exercises_the_expectation_term():
+    # logits with std ~5: p is far from uniform, so sum_v p_v W[v] is large
+    # next to the tolerance and a wrong sign or a dropped term there fails
+    dh, ref, hb, wb, t, g = case(512, 256, 3000, seed=8, hstd=4.0, wstd=0.08, what="peaky")
+    W_t = bits_f64(wb)[t]
+    s = np.abs(g.astype(np.float64))
+    expect = np.abs(ref - g[:, None].astype(np.float64) * W_t).max(axis=1)
+    wmax = float(np.abs(bits_f64(wb)).max())
+    assert np.median(expect / (s * 2.0 ** -8 * wmax)) > 20
+
+
+def test_oracle_lse_and_gpu_lse_agree():
+    rng = np.random.Generator(np.random.PCG64(31))
+    R, H, V = 300, 192, 2000
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    g = rng.standard_normal(R).astype(np.float32)
+    h, w, td, gd = to_dev(hb), to_dev(wb), torch.from_numpy(t).to(dev()), torch.from_numpy(g).to(dev())
+    say("logprob backward with the oracle's lse")
+    _, rlse = oracle.token_logprob(hb, wb, t, 1.0)
+    dh_o = gpu_backward(h, w, td, gd, 1.0, torch.from_numpy(rlse.astype(np.float32)).to(dev())).cpu().numpy()
+    dh_g = gpu_backward(h, w, td, gd, 1.0).cpu().numpy()
+    ref = oracle.token_logprob_backward(hb, wb, t, g.astype(np.float64))
+    wmax = float(np.abs(bits_f64(wb)).max())
+    check_rows(dh_o, ref, t, g, 1.0, wmax, V, "oracle lse")
+    check_rows(dh_g, ref, t, g, 1.0, wmax, V, "gpu lse")
+
+
+def test_deterministic_and_row_permutation():
+    rng = np.random.Generator(np.random.PCG64(9))
+    R, H, V = 600, 128, 3000
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    g = rng.standard_normal(R).astype(np.float32)
+    perm = rng.permutation(R)
+    say("logprob backward determinism")
+    w = to_dev(wb)
+    run = lambda hh, tt, gg: gpu_backward(to_dev(hh), w, torch.from_numpy(tt).to(dev()),
+                                          torch.from_numpy(gg).to(dev())).cpu().numpy()
+    a = run(hb, t, g)
+    b = run(hb, t, g)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), "not deterministic"
+    c = run(hb[perm], t[perm], g[perm])
+    assert np.array_equal(a[perm].view(np.uint32), c.view(np.uint32))
+
+
+def test_workspace_reuse_and_nan_filled_workspace():
+    rng = np.random.Generator(np.random.PCG64(10))
+    R, H, V = 700, 256, 5000
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    g = rng.standard_normal(R).astype(np.float32)
+    h, w, td, gd = to_dev(hb), to_dev(wb), torch.from_numpy(t).to(dev()), torch.from_numpy(g).to(dev())
+    say("logprob backward NaN workspace")
+    _, lse = rk.token_logprob(h, w, td)
+    n = rk.token_logprob_backward_workspace_size(R, H, V)
+    ws = torch.full((n // 4,), float("nan"), dtype=torch.float32, device=dev()).view(torch.uint8)
+    out = torch.full((R, H), float("nan"), dtype=torch.float32, device=dev())
+    rk.token_logprob_backward(h, w, td, lse, gd, grad_hidden=out, workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.token_logprob_backward(hb, wb, t, g.astype(np.float64))
+    check_rows(out.cpu().numpy(), ref, t, g, 1.0, float(np.abs(bits_f64(wb)).max()), V, "NaN workspace")
+    # a second, smaller call on the same workspace
+    R2 = 130
+    dh2 = rk.token_logprob_backward(h[:R2].contiguous(), w, td[:R2].contiguous(), lse[:R2].contiguous(),
+                                    gd[:R2].contiguous(), workspace=ws)
+    torch.cuda.synchronize()
+    check_rows(dh2.cpu().numpy(), ref[:R2], t[:R2], g[:R2], 1.0, float(np.abs(bits_f64(wb)).max()), V,
+               "workspace reuse")
+
+
+def test_empty_rows():
+    w = torch.zeros(10, 64, dtype=torch.bfloat16, device=dev())
+    h = torch.zeros(0, 64, dtype=torch.bfloat16, device=dev())
+    t = torch.zeros(0, dtype=torch.int32, device=dev())
+    e = torch.zeros(0, dtype=torch.float32, device=dev())
+    dh = rk.token_logprob_backward(h, w, t, e, e)
+    torch.cuda.synchronize()
+    assert dh.shape == (0, 64)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,nsample", [("8b", 16), ("32b", 16), ("policy", 8)])
+def test_full_size_workloads(name, nsample):
+    """Full-size runs; the oracle recomputes a seeded sample of rows (first and last included)."""
+    cfg = W.LOGPROB_CONFIGS[name]
+    say(f"logprob backward full-size {name}: generating")
+    x = W.make_logprob_inputs(cfg, dev())
+    g = torch.from_numpy(np.random.Generator(np.random.PCG64(5)).standard_normal(cfg.rows)
+                         .astype(np.float32)).to(dev())
+    say(f"logprob backward full-size {name}: gpu")
+    dh = gpu_backward(x.hidden, x.w_lm, x.target, g, x.inv_temperature)
+    rng = np.random.Generator(np.random.PCG64(11))
+    rows = np.unique(np.concatenate([[0, cfg.rows - 1], rng.integers(0, cfg.rows, nsample - 2)]))
+    idx = torch.from_numpy(rows).to(dev())
+    say(f"logprob backward full-size {name}: oracle on {len(rows)} rows")
+    wb = W.bf16_bits(x.w_lm)
+    t = x.target[idx].cpu().numpy()
+    gs = g[idx].cpu().numpy()
+    ref = oracle.token_logprob_backward(W.bf16_bits(x.hidden[idx]), wb, t, gs.astype(np.float64),
+                                        x.inv_temperature)
+    check_rows(dh[idx].cpu().numpy(), ref, t, gs, x.inv_temperature, float(np.abs(bits_f64(wb)).max()),
+               cfg.vocab, f"full-size {name}")
+    assert torch.isfinite(dh).all()
