@@ -8,6 +8,11 @@ workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
 / 8 kv heads, head dim 128, shared prefix 1024, suffix lengths uniform in
 [256, 2048]; lm-head 512 rows x hidden 4096 x vocab 151936).
 
+After the timed steps, the policy-update operations are timed in a loop of
+their own (outside the step): the backward of the lm-head log-prob for the
+same rows, and the GRPO advantages and clipped surrogate over the policy
+pass's 262144 rows.  They are reported under "policy_update".
+
 Prints ONE JSON line.  `value` is decode attention's effective KV bandwidth
 (algorithmic bytes, the prefix counted once per prompt, over the measured
 decode time); the lm-head's TFLOP/s are reported beside it.  Per-operation
@@ -140,6 +145,15 @@ def lmhead_bytes(cfg) -> int:
     return 2 * cfg.vocab * cfg.hidden + 2 * cfg.rows * cfg.hidden + 4 * cfg.rows + 8 * cfg.rows
 
 
+def grpo_bytes(gx) -> int:
+    """Algorithmic HBM bytes of the GRPO advantages and surrogate: rewards read
+    and advantages written; per row logp_new, logp_old and seq read and grad
+    written; the loss written."""
+    S = gx.reward.numel()
+    R = gx.seq.numel()
+    return 8 * S + 16 * R + 4
+
+
 def cpu_baseline_decode(x, budget_s: float):
     """The fp64 oracle on the host over the workload's prompts (all their
     candidates), prompt by prompt, cycling through the batch until the time
@@ -205,6 +219,9 @@ def main():
                     help="seconds of oracle time per operation for the CPU baseline (0 to skip)")
     ap.add_argument("--kv-layout", default="head", choices=["head", "token"],
                     help="KV cache layout: head-major [Hkv, rows, D] (default) or token-major [rows, Hkv, D]")
+    ap.add_argument("--no-update", action="store_true",
+                    help="skip the policy-update operations (log-prob backward, GRPO surrogate), which "
+                         "are timed after the step in a loop of their own")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy before the steps (outside the timed region) so a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -289,6 +306,63 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     log(f"bench: {ms_per_step:.3f} ms/step; per op {op_ms}")
 
+    # ---- policy-update operations, timed on their own after the step: the
+    # backward of the lm-head log-prob for the same rows (incoming gradient
+    # seeded N(0, 1), lse from the forward above) and the GRPO surrogate over
+    # the policy pass's 262144 rows
+    update = None
+    if y is not None and not args.no_update:
+        cl = y.cfg
+        g_b = torch.from_numpy(np.random.Generator(np.random.PCG64(5)).standard_normal(cl.rows)
+                               .astype(np.float32)).to(dev)
+        dh = torch.empty((cl.rows, cl.hidden), dtype=torch.float32, device=dev)
+        ws_b = torch.empty(max(1, rk.token_logprob_backward_workspace_size(cl.rows, cl.hidden, cl.vocab)),
+                           dtype=torch.uint8, device=dev)
+        gx = W.make_grpo_inputs(W.GRPO_CONFIGS["policy"], dev)
+        G = gx.cfg.group_size
+        adv = rk.grpo_advantage(gx.reward, G)
+        gl = torch.empty(1, dtype=torch.float32, device=dev)
+        gg = torch.empty_like(gx.logp_new)
+        ws_g = torch.empty(rk.grpo_surrogate_workspace_size(gx.seq.numel(), adv.numel() // G, G),
+                           dtype=torch.uint8, device=dev)
+        uops = [("backward", lambda: rk.token_logprob_backward(y.hidden, y.w_lm, y.target, lse2, g_b,
+                                                               y.inv_temperature, grad_hidden=dh,
+                                                               workspace=ws_b)),
+                ("grpo", lambda: (rk.grpo_advantage(gx.reward, G, adv=adv),
+                                  rk.grpo_surrogate(gx.logp_new, gx.logp_old, gx.seq, adv, G, gx.eps,
+                                                    loss=gl, grad=gg, workspace=ws_g)))]
+        usteps = max(1, min(args.steps, 3 if cl.rows > 65536 else args.steps))
+        for _, f in uops:
+            f()
+        torch.cuda.synchronize()
+        uev = [[(hip.create(), hip.create()) for _ in uops] for _ in range(usteps)]
+        for k in range(usteps):
+            for j, (_, f) in enumerate(uops):
+                hip.record(uev[k][j][0], sh)
+                f()
+                hip.record(uev[k][j][1], sh)
+        torch.cuda.synchronize()
+        u_ms = {name: float(np.mean([hip.elapsed_ms(*uev[k][j]) for k in range(usteps)]))
+                for j, (name, _) in enumerate(uops)}
+        for pair in (p for row in uev for p in row):
+            for e in pair:
+                hip.destroy(e)
+        log(f"bench: policy update per op {u_ms}")
+        fl_b = 4 * cl.rows * cl.hidden * cl.vocab
+        tf_b = fl_b / (u_ms["backward"] * 1e-3) / 1e12
+        nb_g = grpo_bytes(gx)
+        update = {"steps": usteps,
+                  "lmhead_backward": {"kernel": "log-prob backward (probability tile + vocab GEMM + finish "
+                                                "kernels, per 16384-row chunk)",
+                                      "ms": round(u_ms["backward"], 4), "bound": "mfma",
+                                      "achieved": round(tf_b, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                                      "unit": "TFLOP/s", "frac": round(tf_b / MFMA_BF16_PEAK_TFLOPS, 4),
+                                      "algorithmic_flops": fl_b},
+                  "grpo": {"kernel": "GRPO advantages + clipped surrogate, 4 x G=16 sequences x 4096 rows",
+                           "us": round(u_ms["grpo"] * 1e3, 2), "bound": "hbm",
+                           "achieved": round(nb_g / (u_ms["grpo"] * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "algorithmic_bytes": nb_g}}
+
     res = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, HBM-resident)",
@@ -335,6 +409,8 @@ def main():
     res["roofline"] = rooflines[0][1]            # the operation that takes the most time
     if len(rooflines) > 1:
         res["roofline_other"] = rooflines[1][1]
+    if update is not None:
+        res["policy_update"] = update
     if args.cpu_budget > 0:
         log("bench: cpu baseline (fp64 oracle)")
         if x is not None:

@@ -47,11 +47,26 @@ __global__ __launch_bounds__(kThreads) void grpo_zero_counts_kernel(int32_t *cou
     if (i < S) counts[i] = 0;
 }
 
+// A candidate's rows are usually contiguous, so one atomic per row would
+// pile onto a few counters.  Each wave splits its 64 rows into runs of equal
+// candidate id; the first lane of a run adds the run's length.  Any row order
+// gives the same counts (every row belongs to exactly one run).
 __global__ __launch_bounds__(kThreads) void grpo_count_kernel(GrpoArgs a) {
     const int64_t r = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
-    if (r >= a.rows) return;
-    const int32_t s = a.seq[r];
-    if (s >= 0 && s < a.S) atomicAdd(a.counts + s, 1);
+    const int lane = threadIdx.x & 63;
+    int32_t s = -1;
+    if (r < a.rows) {
+        s = a.seq[r];
+        if (s < 0 || s >= a.S) s = -1;
+    }
+    const int32_t prev = __shfl_up(s, 1, 64);
+    const bool head = lane == 0 || prev != s;
+    const uint64_t heads = __ballot(head);
+    if (head && s >= 0) {
+        const uint64_t later = lane == 63 ? 0 : heads >> (lane + 1);
+        const int next = later ? lane + 1 + __builtin_ctzll(later) : 64;
+        atomicAdd(a.counts + s, next - lane);
+    }
 }
 
 // Per row: the clipped term (weighted) and the gradient; per workgroup: the
