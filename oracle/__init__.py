@@ -59,6 +59,9 @@ def _bind(path: str):
     lib.oracle_grpo_surrogate.restype = ctypes.c_int
     lib.oracle_grpo_surrogate.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                           P, P, P, P, ctypes.c_double, P, P]
+    lib.oracle_sample_top_p.restype = ctypes.c_int
+    lib.oracle_sample_top_p.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P,
+                                        ctypes.c_double, P, P, P, P]
     lib.oracle_token_logprob_backward.restype = ctypes.c_int
     lib.oracle_token_logprob_backward.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                                   P, P, P, ctypes.c_float, P, P]
@@ -244,6 +247,35 @@ def token_logprob_backward(hidden, w_lm, target, grad_logprob, inv_temperature: 
     return dh
 
 
+def sample_top_p(hidden, w_lm, inv_temperature, top_p: float, uniform, _lib=None):
+    """Nucleus sampling of one token per row.
+
+    hidden [R, H] and w_lm [V, H] bf16 bits; inv_temperature [R] (float32
+    values, one temperature per row); top_p in (0, 1]; uniform [R] in [0, 1).
+    Returns (token int32 [R], logprob float64 [R], margin float64 [R]).
+    """
+    hidden = _u16(hidden)
+    w = _u16(w_lm)
+    R, H = hidden.shape
+    V, H2 = w.shape
+    if H2 != H or V <= 0 or H <= 0:
+        raise ValueError("shape")
+    it = np.ascontiguousarray(inv_temperature, dtype=np.float32)
+    u = np.ascontiguousarray(uniform, dtype=np.float64)
+    if it.shape != (R,) or u.shape != (R,):
+        raise ValueError("inv_temperature / uniform shape")
+    token = np.zeros(R, dtype=np.int32)
+    lp = np.zeros(R, dtype=np.float64)
+    margin = np.zeros(R, dtype=np.float64)
+    if R == 0:
+        return token, lp, margin
+    rc = (_lib or _load()).oracle_sample_top_p(R, H, V, _ptr(hidden), _ptr(w), _ptr(it), float(top_p),
+                                               _ptr(u), _ptr(token), _ptr(lp), _ptr(margin))
+    if rc:
+        raise MemoryError("oracle_sample_top_p scratch allocation failed")
+    return token, lp, margin
+
+
 def num_threads() -> int:
     """Threads OpenMP will use (OMP_NUM_THREADS, else the CPUs this process may run on)."""
     env = os.environ.get("OMP_NUM_THREADS")
@@ -280,3 +312,6 @@ class Oracle:
 
     def token_logprob_backward(self, *args, **kw):
         return token_logprob_backward(*args, **kw, _lib=self._lib)
+
+    def sample_top_p(self, *args, **kw):
+        return sample_top_p(*args, **kw, _lib=self._lib)

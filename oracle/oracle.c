@@ -48,6 +48,22 @@
  *         dL/dhidden_r = g_r * inv_T * (W_t - sum_v p_v W_v);
  *     a masked row (target -1) gets 0 and an invalid target NaN.
  *
+ *  6. Nucleus (top-p) sampling of the next token of each row (Sec. 3,
+ *     Multi-turn RL Training: each turn draws its candidates by nucleus
+ *     sampling at a temperature).  With y_v = inv_T_r * <hidden_r, W_v> and
+ *     p_v = softmax_v(y):
+ *       - the tokens are ranked by p_v, largest first, equal p_v by the
+ *         smaller id first;
+ *       - the nucleus N is the shortest prefix of that ranking whose total
+ *         probability reaches top_p;
+ *       - given u_r in [0, 1), the sampled token is the smallest id t in N
+ *         with sum_{v in N, v <= t} p_v > u_r * sum_{v in N} p_v, i.e. the
+ *         inverse CDF of the renormalised nucleus taken in id order.
+ *     Also returned: the sampled token's log-prob under the full tempered
+ *     softmax (y_t - lse), and the row's decision margin (how far, in
+ *     probability, the inputs sit from a boundary that would change the
+ *     token), which lets tests tell robust rows from knife-edge ones.
+ *
  * Inputs are raw bf16 bit patterns (uint16).  Each is widened exactly:
  * bits << 16 is the float32 pattern, and float32 -> double is exact.
  */
@@ -64,7 +80,7 @@ static double bf16_to_f64(uint16_t b)
     return (double)f;
 }
 
-int oracle_abi_version(void) { return 2; }
+int oracle_abi_version(void) { return 3; }
 
 /* Returns 0 on success, 1 if a scratch allocation failed. */
 int oracle_decode_attn(int32_t P, int32_t G, int32_t Hq, int32_t Hkv, int32_t D,
@@ -301,6 +317,99 @@ int oracle_token_logprob_backward(int64_t R, int32_t H, int32_t V,
         for (int32_t k = 0; k < H; ++k) dh[k] = scale * (bf16_to_f64(wt[k]) + dh[k]);
         free(z);
         free(h);
+    }
+    return failed;
+}
+
+/* ---- 6. nucleus sampling --------------------------------------------- */
+
+typedef struct {
+    double y;
+    int32_t v;
+} ranked_token;
+
+/* Larger logit first (same order as p), equal logits by the smaller id. */
+static int rank_cmp(const void *a, const void *b)
+{
+    const ranked_token *x = (const ranked_token *)a, *y = (const ranked_token *)b;
+    if (x->y > y->y) return -1;
+    if (x->y < y->y) return 1;
+    return (x->v > y->v) - (x->v < y->v);
+}
+
+int oracle_sample_top_p(int64_t R, int32_t H, int32_t V,
+                        const uint16_t *hidden, const uint16_t *w_lm,
+                        const float *inv_temperature, double top_p,
+                        const double *uniform, int32_t *token,
+                        double *logprob, double *margin)
+{
+    int failed = 0;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r) {
+        double *y = (double *)malloc((size_t)V * sizeof(double));
+        double *h = (double *)malloc((size_t)H * sizeof(double));
+        ranked_token *rk = (ranked_token *)malloc((size_t)V * sizeof(ranked_token));
+        unsigned char *in_n = (unsigned char *)calloc((size_t)V, 1);
+        if (!y || !h || !rk || !in_n) {
+#pragma omp atomic write
+            failed = 1;
+            free(y);
+            free(h);
+            free(rk);
+            free(in_n);
+            continue;
+        }
+        const uint16_t *hr = hidden + r * (int64_t)H;
+        for (int32_t k = 0; k < H; ++k) h[k] = bf16_to_f64(hr[k]);
+        const double lse = row_logits(H, V, h, w_lm, (double)inv_temperature[r], y);
+
+        /* the ranking and the shortest prefix reaching top_p */
+        for (int32_t v = 0; v < V; ++v) {
+            rk[v].y = y[v];
+            rk[v].v = v;
+        }
+        qsort(rk, (size_t)V, sizeof(ranked_token), rank_cmp);
+        double before = 0.0, cum = 0.0;
+        int32_t n = 0;
+        while (n < V) {
+            before = cum;
+            cum += exp(rk[n].y - lse);
+            in_n[rk[n].v] = 1;
+            ++n;
+            if (cum >= top_p) break;
+        }
+        /* the boundaries of that decision (top_p < 1 only: with top_p = 1
+           every token is in): the mass just before and at the last member,
+           and the gap between the last member and the next token */
+        double m = INFINITY;
+        if (top_p < 1.0) {
+            m = fmin(top_p - before, cum - top_p);
+            if (n < V) m = fmin(m, exp(rk[n - 1].y - lse) - exp(rk[n].y - lse));
+        }
+
+        /* inverse CDF of the renormalised nucleus, in id order */
+        double zn = 0.0;
+        for (int32_t v = 0; v < V; ++v)
+            if (in_n[v]) zn += exp(y[v] - lse);
+        const double target = uniform[r] * zn;
+        double acc = 0.0, prev = 0.0;
+        int32_t t = -1;
+        for (int32_t v = 0; v < V; ++v) {
+            if (!in_n[v]) continue;
+            prev = acc;
+            acc += exp(y[v] - lse);
+            t = v;
+            if (acc > target) break;
+        }
+        m = fmin(m, fmin(acc - target, target - prev) / zn);
+        token[r] = t;
+        logprob[r] = y[t] - lse;
+        margin[r] = m;
+        free(y);
+        free(h);
+        free(rk);
+        free(in_n);
     }
     return failed;
 }

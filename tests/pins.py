@@ -15,7 +15,12 @@ oracle disagrees with what the mathematics fixes:
 * for the GRPO pieces and the backward: hand-worked regimes of the clipped
   objective, the statistics that define the advantages, central finite
   differences of the oracle's own loss / forward, the two-class logistic
-  gradient, and torch autograd in fp64.
+  gradient, and torch autograd in fp64;
+* for nucleus sampling: the top_p = 1 reduction to numpy's inverse CDF of
+  torch's softmax, the greedy limit (torch argmax), sample frequencies over a
+  uniform grid against the renormalised nucleus, ties broken by id, the
+  temperature / hidden-scale equivalence, the log-prob against torch's
+  log_softmax, and hand-worked cases.
 
 The same battery runs against deliberately broken copies of the oracle
 (test_oracle_mutants.py) to show that each plausible mistake is caught.
@@ -544,6 +549,122 @@ def pin_backward_closed_forms(orc):
     assert np.all(dh4[0] == 0.0) and np.all(np.isnan(dh4[1])), "masked / invalid rows"
 
 
+# ------------------------------------------------------- nucleus sampling
+# (Sec. 3, Multi-turn RL Training: candidates drawn by nucleus sampling with
+# p = 0.9 at temperatures 0.2 and 0.7)
+def sampling_case(R, H, V, seed, hstd=1.0, wstd=0.3):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    h = bf16_bits_of(rng.standard_normal((R, H)) * hstd)
+    w = bf16_bits_of(rng.standard_normal((V, H)) * wstd)
+    return h, w, rng
+
+
+def torch_probs(h, w, inv_t):
+    """softmax(inv_T * h W^T) in fp64 by torch (independent of the oracle)."""
+    z = f64(h) @ f64(w).T
+    return torch.softmax(z * torch.tensor(np.asarray(inv_t, np.float64))[:, None], dim=1).numpy()
+
+
+def pin_sampling_full_distribution(orc):
+    """S1: with top_p = 1 the nucleus is the whole vocabulary, so the sample is
+    the plain inverse CDF of softmax in id order: numpy searchsorted on the
+    cumulative sum of torch's softmax."""
+    R, H, V = 12, 16, 40
+    h, w, rng = sampling_case(R, H, V, seed=41)
+    it = np.float32(1 / 0.7) * np.ones(R, np.float32)
+    u = rng.random(R)
+    tok, _, _ = orc.sample_top_p(h, w, it, 1.0, u)
+    p = torch_probs(h, w, it)
+    want = np.array([np.searchsorted(np.cumsum(p[r]), u[r] * p[r].sum(), side="right") for r in range(R)])
+    assert np.array_equal(tok, want), (tok, want)
+
+
+def pin_sampling_greedy_limit(orc):
+    """S2: a tiny top_p keeps only the most probable token, whatever u is
+    (torch argmax; random logits have no ties)."""
+    R, H, V = 10, 16, 50
+    h, w, rng = sampling_case(R, H, V, seed=42)
+    it = np.full(R, 1 / 0.2, np.float32)
+    want = torch.argmax(f64(h) @ f64(w).T, dim=1).numpy()
+    for u in (np.zeros(R), rng.random(R), np.full(R, 0.999999)):
+        tok, _, _ = orc.sample_top_p(h, w, it, 1e-9, u)
+        assert np.array_equal(tok, want)
+
+
+def pin_sampling_frequencies(orc):
+    """S3: over a grid of M uniform values the oracle's samples follow the
+    renormalised nucleus: token v appears within 1 of M p_v / Z_N times, tokens
+    outside the nucleus never.  The nucleus (from torch's softmax) is the
+    shortest most-probable prefix reaching top_p: its mass reaches top_p and
+    dropping its least probable member falls short."""
+    R, H, V, M = 3, 16, 30, 4000
+    h, w, _ = sampling_case(R, H, V, seed=43)
+    it = np.array([1 / 0.7, 1 / 0.2, 1.0], np.float32)
+    p = torch_probs(h, w, it)
+    grid = (np.arange(M) + 0.5) / M
+    for top_p in (0.9, 0.5):
+        for r in range(R):
+            tok, _, _ = orc.sample_top_p(np.repeat(h[r:r + 1], M, 0), w, np.full(M, it[r], np.float32),
+                                         top_p, grid)
+            counts = np.bincount(tok, minlength=V)
+            members = np.flatnonzero(counts)
+            mass = p[r, members].sum()
+            assert mass >= top_p and mass - p[r, members].min() < top_p, "nucleus not minimal"
+            order = np.argsort(-p[r], kind="stable")
+            assert set(members) == set(order[:len(members)].tolist()), "nucleus not the most probable"
+            assert np.all(np.abs(counts[members] - M * p[r, members] / mass) <= 1.0), "frequencies"
+
+
+def pin_sampling_ties(orc):
+    """S4: ten equal logits (identical weight rows), top_p = 0.35: each token
+    has p = 0.1, so the nucleus is the four smallest ids (0.3 < 0.35 <= 0.4);
+    u = 0.6 puts the target at 0.24 of the nucleus mass 0.4: the third id."""
+    h = bf16_bits_of(np.array([[1.0, 2.0]]))
+    w = bf16_bits_of(np.tile([[0.5, -0.25]], (10, 1)))
+    for u, want in ((0.6, 2), (0.0, 0), (0.99, 3), (0.26, 1)):
+        tok, lp, _ = orc.sample_top_p(h, w, np.ones(1, np.float32), 0.35, np.array([u]))
+        assert tok[0] == want, (u, tok[0], want)
+        close(lp, [-math.log(10.0)], 1e-15, "tie log-prob")
+
+
+def pin_sampling_temperature_scale(orc):
+    """S5: inv_T = 2 on hidden h samples as inv_T = 1 on hidden 2h (the
+    doubling is exact in bf16), for the same u."""
+    R, H, V = 16, 8, 60
+    h, w, rng = sampling_case(R, H, V, seed=44, hstd=0.5)
+    u = rng.random(R)
+    a = orc.sample_top_p(h, w, np.full(R, 2.0, np.float32), 0.9, u)
+    b = orc.sample_top_p(bf16_bits_of(f64(h).numpy() * 2.0), w, np.ones(R, np.float32), 0.9, u)
+    assert np.array_equal(a[0], b[0])
+    close(a[1], b[1], 1e-12, "temperature scale log-prob")
+
+
+def pin_sampling_logprob(orc):
+    """S6: the returned log-prob is the full-vocabulary log-prob of the sampled
+    token (the pinned token_logprob, and torch's log_softmax)."""
+    R, H, V = 9, 16, 70
+    h, w, rng = sampling_case(R, H, V, seed=45)
+    inv_t = np.float32(1 / 0.7)
+    tok, lp, _ = orc.sample_top_p(h, w, np.full(R, inv_t, np.float32), 0.9, rng.random(R))
+    want, _ = orc.token_logprob(h, w, tok, float(inv_t))
+    close(lp, want, 1e-12, "sample log-prob vs token_logprob")
+    ls = torch.log_softmax(f64(h) @ f64(w).T * float(inv_t), dim=1).numpy()
+    close(lp, ls[np.arange(R), tok], 1e-12, "sample log-prob vs log_softmax")
+
+
+def pin_sampling_golden(orc):
+    """Hand-worked cases (tests/golden/sampling_hand.json)."""
+    with open(os.path.join(GOLDEN, "sampling_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        n = len(case["uniform"])
+        h = bf16_bits_of(np.tile(np.array(case["hidden"], np.float64), (n, 1)))
+        tok, _, _ = orc.sample_top_p(h, bf16_bits_of(np.array(case["w_lm"], np.float64)),
+                                     np.full(n, case["inv_temperature"], np.float32), case["top_p"],
+                                     np.array(case["uniform"], np.float64))
+        assert tok.tolist() == case["token"], (case["name"], tok.tolist(), case["token"])
+
+
 ATTENTION_PINS = [pin_attention_vs_torch, pin_prefix_sharing, pin_attention_closed_forms,
                   pin_permutation, pin_one_hot_probe, pin_length_probe, pin_attention_golden]
 LOGPROB_PINS = [pin_logprob_vs_torch, pin_logprob_sum_to_one, pin_logprob_closed_forms,
@@ -551,4 +672,6 @@ LOGPROB_PINS = [pin_logprob_vs_torch, pin_logprob_sum_to_one, pin_logprob_closed
 GRPO_PINS = [pin_advantage_closed_form, pin_advantage_invariants, pin_surrogate_finite_differences,
              pin_surrogate_closed_forms, pin_surrogate_unowned_rows]
 BACKWARD_PINS = [pin_backward_vs_torch, pin_backward_finite_differences, pin_backward_closed_forms]
-ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS
+SAMPLING_PINS = [pin_sampling_full_distribution, pin_sampling_greedy_limit, pin_sampling_frequencies,
+                 pin_sampling_ties, pin_sampling_temperature_scale, pin_sampling_logprob, pin_sampling_golden]
+ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS + SAMPLING_PINS

@@ -52,6 +52,16 @@ MUTANTS = [
     ("bwd_wrong_target_row", "const uint16_t *wt = w_lm + (int64_t)t * H;", "const uint16_t *wt = w_lm + (int64_t)(V - 1 - t) * H;", "bwd"),
     ("bwd_masked_not_zero", "if (t == -1) {\n            for (int32_t k = 0; k < H; ++k) dh[k] = 0.0;",
      "if (t == -1) {\n            for (int32_t k = 0; k < H; ++k) dh[k] = 1.0;", "bwd"),
+    # nucleus sampling
+    ("rank_ascending", "if (x->y > y->y) return -1;\n    if (x->y < y->y) return 1;",
+     "if (x->y > y->y) return 1;\n    if (x->y < y->y) return -1;", "samp"),
+    ("ties_larger_id_first", "return (x->v > y->v) - (x->v < y->v);", "return (x->v < y->v) - (x->v > y->v);", "samp"),
+    ("nucleus_drops_crossing_token", "in_n[rk[n].v] = 1;", "if (cum < top_p) in_n[rk[n].v] = 1;", "samp"),
+    ("nucleus_not_renormalised", "const double target = uniform[r] * zn;", "const double target = uniform[r];", "samp"),
+    ("cdf_in_rank_order", "for (int32_t v = 0; v < V; ++v) {\n            if (!in_n[v]) continue;",
+     "for (int32_t i = 0; i < V; ++i) {\n            const int32_t v = rk[i].v;\n            if (!in_n[v]) continue;", "samp"),
+    ("sampling_temperature_dropped", "(double)inv_temperature[r], y);", "1.0, y);", "samp"),
+    ("sample_logprob_unnormalised", "logprob[r] = y[t] - lse;", "logprob[r] = y[t];", "samp"),
 ]
 
 
@@ -69,7 +79,7 @@ def test_mutant_is_caught(tmp_path, source, name, old, new, battery):
     lib = oracle.compile_c(str(src), str(tmp_path / f"liboracle_{name}.so"))
     orc = oracle.Oracle(lib)
     battery_fns = {"attn": pins.ATTENTION_PINS, "lp": pins.LOGPROB_PINS, "grpo": pins.GRPO_PINS,
-                   "bwd": pins.BACKWARD_PINS}[battery]
+                   "bwd": pins.BACKWARD_PINS, "samp": pins.SAMPLING_PINS}[battery]
     caught = []
     for pin in battery_fns:
         try:
