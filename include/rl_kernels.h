@@ -24,6 +24,10 @@
  *                     the incoming gradient per row (the policy update's
  *                     backward through the token log-probs, Sec. 3).
  *
+ *  rl_sample_top_p    the next token of each row by nucleus sampling at a
+ *                     per-row temperature (Sec. 3, Multi-turn RL Training),
+ *                     through the lm-head.
+ *
  *  rl_grpo_advantage  group-relative advantages of the candidates' rewards
  *                     (Sec. 3, the definition under Eq. grpo-loss).
  *
@@ -61,7 +65,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 4
+#define RL_ABI_VERSION 5
 
 typedef enum {
     RL_OK = 0,
@@ -210,6 +214,52 @@ rl_status rl_token_logprob_backward(int64_t rows, int32_t hidden, int32_t vocab,
                                     const float *lse, const float *grad_logprob,
                                     float *grad_hidden,
                                     void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Nucleus (top-p) sampling head (Sec. 3, Multi-turn RL Training)            */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Draws the next token of each row: candidates are sampled with nucleus
+ * sampling at a temperature (the paper: p = 0.9, temperatures 0.2 and 0.7).
+ * With y_v = inv_temperature[r] * <hidden[r, :], w_lm[v, :]> and p = softmax(y):
+ *   - tokens are ranked by p, largest first, equal p by the smaller id;
+ *   - the nucleus N is the shortest ranked prefix whose mass reaches top_p;
+ *   - token[r] is the smallest id t in N whose nucleus mass in id order,
+ *     sum_{v in N, v <= t} p_v, exceeds uniform[r] * sum_{v in N} p_v.
+ * logprob[r] (if not NULL) is y_t - ln sum_v exp(y_v), the token's log-prob
+ * under the full tempered softmax.
+ *
+ * Precision: the logits are fp32 (bf16 MFMA, fp32 accumulation) and the
+ * probabilities are integer masses floor(2^40 exp(y_v - max y)), so all sums
+ * are exact and the result is deterministic; a token whose mass rounds to 0
+ * (p_v below 2^-40 of the most probable) is never drawn.
+ *
+ *   hidden_states, w_lm   as for rl_token_logprob
+ *   inv_temperature  device fp32 [rows], 1/T per row (finite, > 0: not
+ *                    checked, device memory)
+ *   top_p            in (0, 1]
+ *   uniform          device fp32 [rows], one draw in [0, 1) per row, from the
+ *                    caller's generator (values outside are clamped into
+ *                    the nucleus)
+ *   token            device int32 [rows]
+ *   logprob          device fp32 [rows], or NULL
+ *
+ * The workspace holds the tempered fp32 logits of up to 8192 rows at a time
+ * (rows x vocab padded to 256) and their per-tile maxima; no logits are
+ * returned.  rows == 0 is a valid no-op.  Status: NULL pointer ->
+ * RL_ERR_NULL_POINTER; bad sizes or top_p -> RL_ERR_INVALID_SHAPE; hidden %
+ * 64 != 0 or vocab > 2^21 -> RL_ERR_UNSUPPORTED; hidden_states, w_lm and the
+ * workspace not 16-byte aligned, the other pointers not 4-byte aligned ->
+ * RL_ERR_MISALIGNED; workspace NULL or short -> RL_ERR_WORKSPACE.
+ */
+rl_status rl_sample_top_p_workspace_size(int64_t rows, int32_t hidden, int32_t vocab, size_t *bytes);
+
+rl_status rl_sample_top_p(int64_t rows, int32_t hidden, int32_t vocab,
+                          const void *hidden_states, const void *w_lm,
+                          const float *inv_temperature, float top_p, const float *uniform,
+                          int32_t *token, float *logprob,
+                          void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* GRPO advantages and clipped surrogate (Sec. 3, Eq. grpo-loss)             */

@@ -62,6 +62,9 @@ def _bind(path: str):
     lib.oracle_sample_top_p.restype = ctypes.c_int
     lib.oracle_sample_top_p.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P,
                                         ctypes.c_double, P, P, P, P]
+    lib.oracle_top_p_interval.restype = ctypes.c_int
+    lib.oracle_top_p_interval.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P,
+                                          ctypes.c_double, P, P, P]
     lib.oracle_token_logprob_backward.restype = ctypes.c_int
     lib.oracle_token_logprob_backward.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                                   P, P, P, ctypes.c_float, P, P]
@@ -252,7 +255,9 @@ def sample_top_p(hidden, w_lm, inv_temperature, top_p: float, uniform, _lib=None
 
     hidden [R, H] and w_lm [V, H] bf16 bits; inv_temperature [R] (float32
     values, one temperature per row); top_p in (0, 1]; uniform [R] in [0, 1).
-    Returns (token int32 [R], logprob float64 [R], margin float64 [R]).
+    Returns (token int32 [R], logprob float64 [R], margin float64 [R, 3]); the
+    margin columns are the inverse-CDF margin, the nucleus margin and the mass
+    a nucleus change could move (see oracle.c).
     """
     hidden = _u16(hidden)
     w = _u16(w_lm)
@@ -266,7 +271,7 @@ def sample_top_p(hidden, w_lm, inv_temperature, top_p: float, uniform, _lib=None
         raise ValueError("inv_temperature / uniform shape")
     token = np.zeros(R, dtype=np.int32)
     lp = np.zeros(R, dtype=np.float64)
-    margin = np.zeros(R, dtype=np.float64)
+    margin = np.zeros((R, 3), dtype=np.float64)
     if R == 0:
         return token, lp, margin
     rc = (_lib or _load()).oracle_sample_top_p(R, H, V, _ptr(hidden), _ptr(w), _ptr(it), float(top_p),
@@ -274,6 +279,30 @@ def sample_top_p(hidden, w_lm, inv_temperature, top_p: float, uniform, _lib=None
     if rc:
         raise MemoryError("oracle_sample_top_p scratch allocation failed")
     return token, lp, margin
+
+
+def top_p_interval(hidden, w_lm, inv_temperature, top_p: float, token, _lib=None):
+    """For a given token per row, the range [lo, hi) of u that nucleus sampling
+    maps to it; (-1, -1) when the token is outside the nucleus."""
+    hidden = _u16(hidden)
+    w = _u16(w_lm)
+    R, H = hidden.shape
+    V, H2 = w.shape
+    if H2 != H or V <= 0 or H <= 0:
+        raise ValueError("shape")
+    it = np.ascontiguousarray(inv_temperature, dtype=np.float32)
+    t = np.ascontiguousarray(token, dtype=np.int32)
+    if it.shape != (R,) or t.shape != (R,):
+        raise ValueError("inv_temperature / token shape")
+    lo = np.zeros(R, dtype=np.float64)
+    hi = np.zeros(R, dtype=np.float64)
+    if R == 0:
+        return lo, hi
+    rc = (_lib or _load()).oracle_top_p_interval(R, H, V, _ptr(hidden), _ptr(w), _ptr(it), float(top_p),
+                                                 _ptr(t), _ptr(lo), _ptr(hi))
+    if rc:
+        raise MemoryError("oracle_top_p_interval scratch allocation failed")
+    return lo, hi
 
 
 def num_threads() -> int:
@@ -315,3 +344,6 @@ class Oracle:
 
     def sample_top_p(self, *args, **kw):
         return sample_top_p(*args, **kw, _lib=self._lib)
+
+    def top_p_interval(self, *args, **kw):
+        return top_p_interval(*args, **kw, _lib=self._lib)

@@ -60,9 +60,13 @@
  *         with sum_{v in N, v <= t} p_v > u_r * sum_{v in N} p_v, i.e. the
  *         inverse CDF of the renormalised nucleus taken in id order.
  *     Also returned: the sampled token's log-prob under the full tempered
- *     softmax (y_t - lse), and the row's decision margin (how far, in
- *     probability, the inputs sit from a boundary that would change the
- *     token), which lets tests tell robust rows from knife-edge ones.
+ *     softmax (y_t - lse), and three margins that let tests tell robust rows
+ *     from knife-edge ones: the distance of u * sum_N p from the ends of the
+ *     token's interval (as a fraction of the nucleus mass); how close the
+ *     nucleus is to changing (top_p against the mass before and at its last
+ *     member, and the probability gap to the next ranked token); and the
+ *     mass such a change could move (last member plus next token, over the
+ *     nucleus mass; infinite when the sample is one of them).
  *
  * Inputs are raw bf16 bit patterns (uint16).  Each is widened exactly:
  * bits << 16 is the float32 pattern, and float32 -> double is exact.
@@ -337,6 +341,36 @@ static int rank_cmp(const void *a, const void *b)
     return (x->v > y->v) - (x->v < y->v);
 }
 
+/* The nucleus of one row: logits y (and their lse), the ranking rk, the
+ * member flags in_n, and, through the out-pointers, the mass before and at
+ * the last member and the member count. */
+static double row_nucleus(int32_t H, int32_t V, const uint16_t *hr, const uint16_t *w_lm, double inv_T,
+                          double top_p, double *h, double *y, ranked_token *rk, unsigned char *in_n,
+                          double *before_out, double *cum_out, int32_t *n_out)
+{
+    for (int32_t k = 0; k < H; ++k) h[k] = bf16_to_f64(hr[k]);
+    const double lse = row_logits(H, V, h, w_lm, inv_T, y);
+    for (int32_t v = 0; v < V; ++v) {
+        rk[v].y = y[v];
+        rk[v].v = v;
+        in_n[v] = 0;
+    }
+    qsort(rk, (size_t)V, sizeof(ranked_token), rank_cmp);
+    double before = 0.0, cum = 0.0;
+    int32_t n = 0;
+    while (n < V) {
+        before = cum;
+        cum += exp(rk[n].y - lse);
+        in_n[rk[n].v] = 1;
+        ++n;
+        if (cum >= top_p) break;
+    }
+    *before_out = before;
+    *cum_out = cum;
+    *n_out = n;
+    return lse;
+}
+
 int oracle_sample_top_p(int64_t R, int32_t H, int32_t V,
                         const uint16_t *hidden, const uint16_t *w_lm,
                         const float *inv_temperature, double top_p,
@@ -350,7 +384,7 @@ int oracle_sample_top_p(int64_t R, int32_t H, int32_t V,
         double *y = (double *)malloc((size_t)V * sizeof(double));
         double *h = (double *)malloc((size_t)H * sizeof(double));
         ranked_token *rk = (ranked_token *)malloc((size_t)V * sizeof(ranked_token));
-        unsigned char *in_n = (unsigned char *)calloc((size_t)V, 1);
+        unsigned char *in_n = (unsigned char *)malloc((size_t)V);
         if (!y || !h || !rk || !in_n) {
 #pragma omp atomic write
             failed = 1;
@@ -360,33 +394,21 @@ int oracle_sample_top_p(int64_t R, int32_t H, int32_t V,
             free(in_n);
             continue;
         }
-        const uint16_t *hr = hidden + r * (int64_t)H;
-        for (int32_t k = 0; k < H; ++k) h[k] = bf16_to_f64(hr[k]);
-        const double lse = row_logits(H, V, h, w_lm, (double)inv_temperature[r], y);
-
-        /* the ranking and the shortest prefix reaching top_p */
-        for (int32_t v = 0; v < V; ++v) {
-            rk[v].y = y[v];
-            rk[v].v = v;
-        }
-        qsort(rk, (size_t)V, sizeof(ranked_token), rank_cmp);
-        double before = 0.0, cum = 0.0;
-        int32_t n = 0;
-        while (n < V) {
-            before = cum;
-            cum += exp(rk[n].y - lse);
-            in_n[rk[n].v] = 1;
-            ++n;
-            if (cum >= top_p) break;
-        }
-        /* the boundaries of that decision (top_p < 1 only: with top_p = 1
-           every token is in): the mass just before and at the last member,
-           and the gap between the last member and the next token */
-        double m = INFINITY;
+        double before, cum;
+        int32_t n;
+        const double lse = row_nucleus(H, V, hidden + r * (int64_t)H, w_lm, (double)inv_temperature[r], top_p,
+                                       h, y, rk, in_n, &before, &cum, &n);
+        /* how close the nucleus is to changing (top_p < 1 only: with
+           top_p = 1 every token is in): the mass just before and at the last
+           member, and the gap between the last member and the next token */
+        double nm = INFINITY;
         if (top_p < 1.0) {
-            m = fmin(top_p - before, cum - top_p);
-            if (n < V) m = fmin(m, exp(rk[n - 1].y - lse) - exp(rk[n].y - lse));
+            nm = fmin(top_p - before, cum - top_p);
+            if (n < V) nm = fmin(nm, exp(rk[n - 1].y - lse) - exp(rk[n].y - lse));
         }
+        /* what such a change could move: the last member and the next token */
+        const int32_t last = rk[n - 1].v, next = n < V ? rk[n].v : -1;
+        double bmass = exp(rk[n - 1].y - lse) + (n < V ? exp(rk[n].y - lse) : 0.0);
 
         /* inverse CDF of the renormalised nucleus, in id order */
         double zn = 0.0;
@@ -402,10 +424,62 @@ int oracle_sample_top_p(int64_t R, int32_t H, int32_t V,
             t = v;
             if (acc > target) break;
         }
-        m = fmin(m, fmin(acc - target, target - prev) / zn);
         token[r] = t;
         logprob[r] = y[t] - lse;
-        margin[r] = m;
+        margin[3 * r] = fmin(acc - target, target - prev) / zn;
+        margin[3 * r + 1] = nm;
+        margin[3 * r + 2] = (t == last || t == next) ? INFINITY : bmass / zn;
+        free(y);
+        free(h);
+        free(rk);
+        free(in_n);
+    }
+    return failed;
+}
+
+/* For a given token per row: the range [lo, hi) of u that samples it (its
+ * share of the renormalised nucleus, in id order), or lo = hi = -1 if the
+ * token is outside the nucleus or not a valid id. */
+int oracle_top_p_interval(int64_t R, int32_t H, int32_t V,
+                          const uint16_t *hidden, const uint16_t *w_lm,
+                          const float *inv_temperature, double top_p,
+                          const int32_t *token, double *lo, double *hi)
+{
+    int failed = 0;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r) {
+        double *y = (double *)malloc((size_t)V * sizeof(double));
+        double *h = (double *)malloc((size_t)H * sizeof(double));
+        ranked_token *rk = (ranked_token *)malloc((size_t)V * sizeof(ranked_token));
+        unsigned char *in_n = (unsigned char *)malloc((size_t)V);
+        if (!y || !h || !rk || !in_n) {
+#pragma omp atomic write
+            failed = 1;
+            free(y);
+            free(h);
+            free(rk);
+            free(in_n);
+            continue;
+        }
+        double before, cum;
+        int32_t n;
+        const double lse = row_nucleus(H, V, hidden + r * (int64_t)H, w_lm, (double)inv_temperature[r], top_p,
+                                       h, y, rk, in_n, &before, &cum, &n);
+        const int32_t t = token[r];
+        lo[r] = -1.0;
+        hi[r] = -1.0;
+        if (t >= 0 && t < V && in_n[t]) {
+            double zn = 0.0, below = 0.0;
+            for (int32_t v = 0; v < V; ++v) {
+                if (!in_n[v]) continue;
+                const double pv = exp(y[v] - lse);
+                if (v < t) below += pv;
+                zn += pv;
+            }
+            lo[r] = below / zn;
+            hi[r] = (below + exp(y[t] - lse)) / zn;
+        }
         free(y);
         free(h);
         free(rk);

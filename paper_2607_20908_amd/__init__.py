@@ -71,7 +71,8 @@ class PlanItem(ctypes.Structure):
 EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_workspace_size",
            "rl_token_logprob", "rl_status_string", "rl_last_error", "rl_abi_version",
            "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
-           "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward"]
+           "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
+           "rl_sample_top_p_workspace_size", "rl_sample_top_p"]
 
 
 def _load():
@@ -104,7 +105,11 @@ def _load():
     lib.rl_token_logprob_backward_workspace_size.argtypes = [I64, I32, I32, ctypes.POINTER(SZ)]
     lib.rl_token_logprob_backward.restype = ctypes.c_int
     lib.rl_token_logprob_backward.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, P, SZ, P]
-    if lib.rl_abi_version() != 4:
+    lib.rl_sample_top_p_workspace_size.restype = ctypes.c_int
+    lib.rl_sample_top_p_workspace_size.argtypes = [I64, I32, I32, ctypes.POINTER(SZ)]
+    lib.rl_sample_top_p.restype = ctypes.c_int
+    lib.rl_sample_top_p.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, P, SZ, P]
+    if lib.rl_abi_version() != 5:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -352,6 +357,50 @@ def token_logprob_backward(hidden: torch.Tensor, w_lm: torch.Tensor, target: tor
                                           workspace.numel(), _stream_handle(stream)),
            "rl_token_logprob_backward")
     return grad_hidden
+
+
+def sample_top_p_workspace_size(rows: int, hidden: int, vocab: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_sample_top_p_workspace_size(rows, hidden, vocab, ctypes.byref(n)),
+           "rl_sample_top_p_workspace_size")
+    return n.value
+
+
+def sample_top_p(hidden: torch.Tensor, w_lm: torch.Tensor, inv_temperature: torch.Tensor, top_p: float,
+                 uniform: torch.Tensor, token: Optional[torch.Tensor] = None,
+                 logprob: Optional[torch.Tensor] = None, want_logprob: bool = True,
+                 workspace: Optional[torch.Tensor] = None, stream=None):
+    """Nucleus sampling of one token per row at a per-row temperature.
+
+    hidden [R, H] bf16, w_lm [V, H] bf16, inv_temperature [R] fp32 (1/T per row),
+    uniform [R] fp32 draws in [0, 1).  Returns (token int32 [R], logprob fp32 [R] or None).
+    """
+    _bf16_dev(hidden, "hidden")
+    _bf16_dev(w_lm, "w_lm")
+    R, H = hidden.shape
+    V, H2 = w_lm.shape
+    if H2 != H:
+        raise ValueError("shapes: hidden [R, H], w_lm [V, H]")
+    _f32_dev(inv_temperature, "inv_temperature", (R,))
+    _f32_dev(uniform, "uniform", (R,))
+    if token is None:
+        token = torch.empty(R, dtype=torch.int32, device=hidden.device)
+    _on_device(token, "token")
+    if token.dtype != torch.int32 or token.shape != (R,) or not token.is_contiguous():
+        raise ValueError("token must be a contiguous int32 [R] tensor")
+    if logprob is None and want_logprob:
+        logprob = torch.empty(R, dtype=torch.float32, device=hidden.device)
+    if logprob is not None:
+        _f32_dev(logprob, "logprob", (R,))
+    need = sample_top_p_workspace_size(R, H, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    _on_device(workspace, "workspace")
+    _check(_lib.rl_sample_top_p(R, H, V, _ptr(hidden), _ptr(w_lm), _ptr(inv_temperature), float(top_p),
+                                _ptr(uniform), _ptr(token), _ptr(logprob),
+                                ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                _stream_handle(stream)), "rl_sample_top_p")
+    return token, logprob
 
 
 def _f32_dev(t: torch.Tensor, name: str, shape) -> torch.Tensor:

@@ -332,6 +332,78 @@ rl_status rl_token_logprob_backward(int64_t rows, int32_t hidden, int32_t vocab,
     return RL_OK;
 }
 
+rl_status rl_sample_top_p_workspace_size(int64_t rows, int32_t hidden, int32_t vocab, size_t *bytes) {
+    g_last_error.clear();
+    if (!bytes) return set_error(RL_ERR_NULL_POINTER, "bytes is NULL");
+    rlk::SamplePlan plan;
+    std::string err;
+    const rl_status st = rlk::plan_sample(rows, hidden, vocab, &plan, &err);
+    if (st != RL_OK) return set_error(st, err);
+    *bytes = plan.total_bytes;
+    return RL_OK;
+}
+
+rl_status rl_sample_top_p(int64_t rows, int32_t hidden, int32_t vocab, const void *hidden_states,
+                          const void *w_lm, const float *inv_temperature, float top_p, const float *uniform,
+                          int32_t *token, float *logprob, void *workspace, size_t workspace_bytes,
+                          void *stream) {
+    g_last_error.clear();
+    rlk::SamplePlan plan;
+    std::string err;
+    rl_status st = rlk::plan_sample(rows, hidden, vocab, &plan, &err);
+    if (st != RL_OK) return set_error(st, err);
+    if (!(std::isfinite(top_p) && top_p > 0.f && top_p <= 1.f))
+        return set_error(RL_ERR_INVALID_SHAPE, "top_p must be in (0, 1]");
+    if (rows == 0) return RL_OK;
+    if (!hidden_states || !w_lm || !inv_temperature || !uniform || !token)
+        return set_error(RL_ERR_NULL_POINTER, "hidden_states, w_lm, inv_temperature, uniform and token must not be NULL");
+    if (!aligned16(hidden_states) || !aligned16(w_lm))
+        return set_error(RL_ERR_MISALIGNED, "hidden_states and w_lm must be 16-byte aligned");
+    if (!aligned4(inv_temperature) || !aligned4(uniform) || !aligned4(token) || (logprob && !aligned4(logprob)))
+        return set_error(RL_ERR_MISALIGNED, "inv_temperature, uniform, token and logprob must be 4-byte aligned");
+    if (!workspace || workspace_bytes < plan.total_bytes)
+        return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(plan.total_bytes) +
+                                               " bytes, got " + std::to_string(workspace_bytes));
+    if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+    unsigned char *ws = static_cast<unsigned char *>(workspace);
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const uint16_t *hid = static_cast<const uint16_t *>(hidden_states);
+    float *logits = reinterpret_cast<float *>(ws + plan.off_logits);
+    float *pm = reinterpret_cast<float *>(ws + plan.off_pm);
+    for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
+        const int64_t n = std::min(plan.chunk_rows, rows - c0);
+        rlk::LogprobArgs f{};
+        f.hidden = hid + c0 * hidden;
+        f.w = static_cast<const uint16_t *>(w_lm);
+        f.R = n;
+        f.H = hidden;
+        f.V = vocab;
+        f.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
+        f.n_row_tiles = static_cast<int32_t>((n + rlk::kRowTile - 1) / rlk::kRowTile);
+        f.inv_temperature = 1.f;
+        f.inv_t_rows = inv_temperature + c0;
+        f.logits = logits;
+        f.ld = plan.ld;
+        f.pm = pm;
+        hipError_t e = rlk::launch_logits(f, hs);
+        if (e != hipSuccess) return hip_error(e, "launching the sampling head (logits)");
+        rlk::SampleArgs s{};
+        s.logits = logits;
+        s.pm = pm;
+        s.uniform = uniform + c0;
+        s.token = token + c0;
+        s.logprob = logprob ? logprob + c0 : nullptr;
+        s.rows = n;
+        s.ld = plan.ld;
+        s.V = vocab;
+        s.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
+        s.top_p = top_p;
+        e = rlk::launch_sample_top_p(s, hs);
+        if (e != hipSuccess) return hip_error(e, "launching the sampling head (selection)");
+    }
+    return RL_OK;
+}
+
 rl_status rl_grpo_advantage(int64_t num_prompts, int32_t group_size, const float *reward, float *adv,
                             void *stream) {
     g_last_error.clear();

@@ -46,6 +46,12 @@ struct LogprobArgs {
     // LogprobBwdArgs::probs (output); pm, pl, zt, logprob are then unused
     const float *lse_in;
     uint16_t *probs;
+    // sampling head only: per-row inverse temperatures (input) and the
+    // tempered logits y = inv_T[r] z, fp32 [R, ld] (output); pm then holds
+    // each (vocab tile, row)'s max of y
+    const float *inv_t_rows;
+    float *logits;
+    int64_t ld;
 };
 
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream);
@@ -73,6 +79,24 @@ struct LogprobBwdArgs {
 };
 
 hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream);
+hipError_t launch_logits(const LogprobArgs &a, hipStream_t stream);
+
+// Nucleus sampling over tempered logits already in memory (one chunk of
+// rows): per row, the max from the tile maxima, the nucleus of the top_p
+// most probable tokens and the inverse CDF of the renormalised nucleus in id
+// order at the row's uniform draw.
+struct SampleArgs {
+    const float *logits;        // [rows, ld] fp32 tempered logits
+    const float *pm;            // [n_vocab_tiles, rows] tile maxima of the logits
+    const float *uniform;       // [rows] in [0, 1)
+    int32_t *token;             // [rows]
+    float *logprob;             // [rows] or null
+    int64_t rows, ld;
+    int32_t V, n_vocab_tiles;
+    float top_p;
+};
+
+hipError_t launch_sample_top_p(const SampleArgs &a, hipStream_t stream);
 hipError_t launch_logprob_bwd_gemm(const LogprobBwdArgs &a, hipStream_t stream);
 hipError_t launch_logprob_bwd_finish(const LogprobBwdArgs &a, hipStream_t stream);
 

@@ -352,6 +352,30 @@ rl_status plan_logprob_bwd(int64_t rows, int32_t hidden, int32_t vocab, LogprobB
     return RL_OK;
 }
 
+rl_status plan_sample(int64_t rows, int32_t hidden, int32_t vocab, SamplePlan *plan, std::string *err) {
+    LogprobPlan fwd;
+    const rl_status st = plan_logprob(rows, hidden, vocab, &fwd, err);
+    if (st != RL_OK) return st;
+    if (vocab > kSampleMaxVocab) return fail(err, RL_ERR_UNSUPPORTED, "vocab must be <= 2097152");
+    SamplePlan &pl = *plan;
+    pl = SamplePlan{};
+    pl.R = rows;
+    pl.H = hidden;
+    pl.V = vocab;
+    pl.n_vocab_tiles = ceil_div(vocab, kVocabTile);
+    pl.ld = pl.n_vocab_tiles * kVocabTile;
+    if (rows == 0) return RL_OK;
+    pl.chunk_rows = std::min<int64_t>(rows, kSampleChunkRows);
+    const int64_t rows_pad = ceil_div(pl.chunk_rows, kRowTile) * kRowTile;
+    size_t off = 0;
+    pl.off_logits = off;
+    off = align_up(off + static_cast<size_t>(rows_pad) * pl.ld * 4, 256);
+    pl.off_pm = off;
+    off = align_up(off + static_cast<size_t>(pl.n_vocab_tiles) * pl.chunk_rows * 4, 256);
+    pl.total_bytes = off;
+    return RL_OK;
+}
+
 rl_status check_logprob_args(const LogprobPlan &pl, const void *hidden_states,
                              const void *w_lm, const int32_t *target, float inv_temperature,
                              const float *logprob, const float *lse, std::string *err) {

@@ -123,6 +123,22 @@ struct LogprobBwdPlan {
 rl_status plan_logprob_bwd(int64_t rows, int32_t hidden, int32_t vocab, LogprobBwdPlan *plan,
                            std::string *err);
 
+// Nucleus sampling: the tempered fp32 logits of a chunk of rows and their
+// per-tile maxima live in the workspace.
+constexpr int64_t kSampleChunkRows = 8192;
+constexpr int32_t kSampleMaxVocab = 1 << 21;
+
+struct SamplePlan {
+    int64_t R = 0;
+    int32_t H = 0, V = 0;
+    int64_t chunk_rows = 0;
+    int64_t n_vocab_tiles = 0;
+    int64_t ld = 0;                  // padded vocabulary (row stride of the logits)
+    size_t off_logits = 0, off_pm = 0, total_bytes = 0;
+};
+
+rl_status plan_sample(int64_t rows, int32_t hidden, int32_t vocab, SamplePlan *plan, std::string *err);
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace rlk

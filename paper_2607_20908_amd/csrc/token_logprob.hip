@@ -38,9 +38,13 @@ static_assert(kBlocksPerWave == 8, "staging layout");
 // only the weights stream from HBM; a third weight stage gives them two
 // stages to arrive (WS = 3 fills the whole 160 KB of LDS).  With many row
 // tiles both operands miss and WS = 2 measures better.
-// BWD: instead of the (max, sum) partials, write p = exp(inv_T z - lse) per
-// (row, vocab entry) as bf16 into the blocked probability buffer.
-template <int WS, bool BWD>
+// Epilogue modes: the forward's (max, sum) partials; the backward's
+// p = exp(inv_T z - lse) per (row, vocab entry) as bf16 into the blocked
+// probability buffer; or the sampling head's tempered fp32 logits (per-row
+// temperature) plus the tile's row maxima.
+enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2 };
+
+template <int WS, int MODE>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
     // WS x 32 KB weight stages + 2 x 32 KB hidden stages; the epilogue's
     // reduction area reuses the weight ring once the loop is done
@@ -172,7 +176,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     barrier();                                   // the reduction area aliases the weight ring
     __builtin_amdgcn_sched_barrier(0);
 
-    if constexpr (BWD) {
+    if constexpr (MODE == kBwdProbs) {
         // acc[tm][tn][i]: vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4,
         // row r0 + wn*128 + tn*32 + l32.  The 4 consecutive entries i%4 are one
         // 8-byte store into vocab step vt*4 + wm*2 + tm/2, chunk (tm%2)*4 + i/4.
@@ -211,6 +215,44 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        return;
+    }
+    if constexpr (MODE == kLogits) {
+        // acc[tm][tn][i]: vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4,
+        // row r0 + wn*128 + tn*32 + l32: 4 consecutive entries per store
+        const int64_t vbase = v0 + wm * 128;
+        const int vlim = vbase + 128 <= a.V ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
+#pragma unroll
+        for (int tn = 0; tn < 4; ++tn) {
+            const int row = wn * 128 + tn * 32 + l32;
+            const int64_t rr = r0 + row;
+            const bool live = rr < a.R;
+            const float it = live ? a.inv_t_rows[rr] : 0.f;
+            float *yrow = a.logits + (live ? rr : 0) * a.ld + vbase + 4 * h2;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int tm = 0; tm < 4; ++tm) {
+                const f32x16 z = acc[tm][tn];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float y[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        y[e] = z[4 * q + e] * it;
+                        y[e] = y[e] == 0.f ? 0.f : y[e];   // one key for +0 and -0
+                        if (tm * 32 + 8 * q + e < vlim) mx = fmaxf(mx, y[e]);
+                    }
+                    if (live)
+                        *reinterpret_cast<float4 *>(yrow + tm * 32 + 8 * q) = make_float4(y[0], y[1], y[2], y[3]);
+                }
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            if (h2 == 0) red[wm][row][0] = mx;
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __syncthreads();
+        const int64_t rr = r0 + tid;
+        if (rr < a.R) a.pm[vt * a.R + rr] = fmaxf(red[0][tid][0], red[1][tid][0]);
         return;
     }
 
@@ -351,10 +393,10 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
     const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
     if (a.n_row_tiles <= 8)
-        hipLaunchKernelGGL((logprob_tile_kernel<3, false>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
                            stream, a);
     else
-        hipLaunchKernelGGL((logprob_tile_kernel<2, false>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+        hipLaunchKernelGGL((logprob_tile_kernel<2, kFwd>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
                            stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -373,10 +415,21 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
 hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream) {
     const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
     if (a.n_row_tiles <= 8)
-        hipLaunchKernelGGL((logprob_tile_kernel<3, true>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kBwdProbs>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
                            stream, a);
     else
-        hipLaunchKernelGGL((logprob_tile_kernel<2, true>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+        hipLaunchKernelGGL((logprob_tile_kernel<2, kBwdProbs>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+                           stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_logits(const LogprobArgs &a, hipStream_t stream) {
+    const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
+    if (a.n_row_tiles <= 8)
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((logprob_tile_kernel<2, kLogits>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
                            stream, a);
     return hipGetLastError();
 }

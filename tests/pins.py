@@ -652,6 +652,27 @@ def pin_sampling_logprob(orc):
     close(lp, ls[np.arange(R), tok], 1e-12, "sample log-prob vs log_softmax")
 
 
+def pin_sampling_intervals(orc):
+    """S7: the intervals of u that map to each token tile [0, 1) in id order,
+    one per nucleus member, each as long as the member's share of the
+    nucleus mass (torch's softmax); the sampled token's interval holds u."""
+    H, V = 16, 40
+    h, w, rng = sampling_case(1, H, V, seed=46)
+    for inv_t, top_p in ((1 / 0.7, 0.9), (1 / 0.2, 0.9), (1.0, 0.5), (1.0, 1.0)):
+        it = np.float32(inv_t)
+        lo, hi = orc.top_p_interval(np.repeat(h, V, 0), w, np.full(V, it, np.float32), top_p,
+                                    np.arange(V, dtype=np.int32))
+        members = np.flatnonzero(lo >= 0)
+        p = torch_probs(h, w, [it])[0]
+        share = p[members] / p[members].sum()
+        close(hi[members] - lo[members], share, 1e-12, "interval lengths")
+        close(lo[members], np.concatenate([[0.0], np.cumsum(share)[:-1]]), 1e-12, "intervals in id order")
+        assert np.all(hi[lo < 0] == -1.0)
+        u = rng.random(8)
+        tok, _, _ = orc.sample_top_p(np.repeat(h, 8, 0), w, np.full(8, it, np.float32), top_p, u)
+        assert np.all((lo[tok] <= u) & (u < hi[tok])), "sample outside its interval"
+
+
 def pin_sampling_golden(orc):
     """Hand-worked cases (tests/golden/sampling_hand.json)."""
     with open(os.path.join(GOLDEN, "sampling_hand.json")) as f:
@@ -673,5 +694,6 @@ GRPO_PINS = [pin_advantage_closed_form, pin_advantage_invariants, pin_surrogate_
              pin_surrogate_closed_forms, pin_surrogate_unowned_rows]
 BACKWARD_PINS = [pin_backward_vs_torch, pin_backward_finite_differences, pin_backward_closed_forms]
 SAMPLING_PINS = [pin_sampling_full_distribution, pin_sampling_greedy_limit, pin_sampling_frequencies,
-                 pin_sampling_ties, pin_sampling_temperature_scale, pin_sampling_logprob, pin_sampling_golden]
+                 pin_sampling_ties, pin_sampling_temperature_scale, pin_sampling_logprob, pin_sampling_intervals,
+                 pin_sampling_golden]
 ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS + SAMPLING_PINS

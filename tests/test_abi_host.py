@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 4
+    assert lib.rl_abi_version() == 5
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -330,3 +330,58 @@ def test_logprob_backward_workspace_size():
     assert rk.token_logprob_backward_workspace_size(0, 64, 10) == 0
     with pytest.raises(rk.RLError):
         rk.token_logprob_backward_workspace_size(4, 100, 10)
+
+
+# ---------------------------------------------------------- sampling head
+def sample_call(R=8, H=256, V=1000, hs=FAKE, w=FAKE + 256, it=FAKE + 512, top_p=0.9, u=FAKE + 768,
+                tok=FAKE + 1024, lp=FAKE + 1280, ws=FAKE, ws_bytes=1 << 30):
+    lib = rk.lib()
+    st = lib.rl_sample_top_p(R, H, V, hs, w, it, top_p, u, tok, lp, ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(hs=None), NULLP),
+    (dict(w=None), NULLP),
+    (dict(it=None), NULLP),
+    (dict(u=None), NULLP),
+    (dict(tok=None), NULLP),
+    (dict(R=-1), SHAPE),
+    (dict(H=0), SHAPE),
+    (dict(V=0), SHAPE),
+    (dict(top_p=0.0), SHAPE),
+    (dict(top_p=-0.5), SHAPE),
+    (dict(top_p=1.5), SHAPE),
+    (dict(top_p=float("nan")), SHAPE),
+    (dict(H=100), UNSUP),
+    (dict(V=(1 << 21) + 1), UNSUP),
+    (dict(hs=FAKE + 8), MISAL),
+    (dict(w=FAKE + 4), MISAL),
+    (dict(it=FAKE + 2), MISAL),
+    (dict(u=FAKE + 1), MISAL),
+    (dict(tok=FAKE + 2), MISAL),
+    (dict(lp=FAKE + 3), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws_bytes=16), WSPACE),
+    (dict(ws=FAKE + 4), MISAL),
+])
+def test_sample_validation(kw, expect):
+    st, msg = sample_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg
+
+
+def test_sample_logprob_optional_and_empty():
+    st, msg = sample_call(R=0, hs=None, w=None, it=None, u=None, tok=None, lp=None, ws=None, ws_bytes=0)
+    assert st == OK and msg == ""
+
+
+def test_sample_workspace_size():
+    V = 151936
+    ld = -(-V // 256) * 256
+    tiles = ld // 256
+    # fp32 logits of up to 8192 rows (padded to 256) and their per-tile maxima
+    n = rk.sample_top_p_workspace_size(512, 4096, V)
+    assert n >= 512 * ld * 4 + tiles * 512 * 4 and n < 512 * ld * 4 + tiles * 512 * 4 + 512
+    assert rk.sample_top_p_workspace_size(100000, 4096, V) == rk.sample_top_p_workspace_size(8192, 4096, V)
+    assert rk.sample_top_p_workspace_size(0, 64, 10) == 0

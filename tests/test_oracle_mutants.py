@@ -60,7 +60,9 @@ MUTANTS = [
     ("nucleus_not_renormalised", "const double target = uniform[r] * zn;", "const double target = uniform[r];", "samp"),
     ("cdf_in_rank_order", "for (int32_t v = 0; v < V; ++v) {\n            if (!in_n[v]) continue;",
      "for (int32_t i = 0; i < V; ++i) {\n            const int32_t v = rk[i].v;\n            if (!in_n[v]) continue;", "samp"),
-    ("sampling_temperature_dropped", "(double)inv_temperature[r], y);", "1.0, y);", "samp"),
+    ("sampling_temperature_dropped", "const double lse = row_logits(H, V, h, w_lm, inv_T, y);",
+     "const double lse = row_logits(H, V, h, w_lm, 1.0, y);", "samp"),
+    ("interval_includes_own_mass", "if (v < t) below += pv;", "if (v <= t) below += pv;", "samp"),
     ("sample_logprob_unnormalised", "logprob[r] = y[t] - lse;", "logprob[r] = y[t];", "samp"),
 ]
 

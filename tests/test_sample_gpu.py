@@ -1,0 +1,219 @@
+"""Nucleus sampling head: the HIP path against the fp64 oracle on the same bits.
+
+The sample is an integer decided by floating point, so the bar is stated per
+row in terms of the exact (oracle) distribution.  The oracle gives the range
+[lo, hi) of u that maps to the token the GPU drew; the GPU's draw u must lie
+in it up to DELTA.  The GPU's fp32 logits (bf16 MFMA, fp32 accumulation) are
+off by about 1e-6 of a logit, times inv_T <= 5 at T = 0.2, and that moves
+every probability by a relative ~5e-6; DELTA = 5e-5 of the nucleus mass
+leaves ten times that.  Where the intervals are wider than DELTA (peaky or
+small vocabularies) this is an exact match except on knife-edge rows, and
+the tests also require the GPU token to equal the oracle's on every row whose
+margins (from the oracle) exceed DELTA.  A token the oracle's nucleus does not
+hold is accepted only if a nucleus DELTA larger holds it.  Log-probs of the
+drawn token are within 2e-3 of the oracle's.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_20908_amd as rk
+import workloads as W
+from gpu_util import LOGPROB_TOL, dev, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+DELTA = 5e-5
+
+
+def rand_bits(rng, shape, std=1.0):
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32) * std)
+    return W.bf16_bits(x.to(torch.bfloat16))
+
+
+def gpu_sample(hb, wb, inv_t, top_p, u):
+    tok, lp = rk.sample_top_p(to_dev(hb), to_dev(wb), torch.from_numpy(np.asarray(inv_t, np.float32)).to(dev()),
+                              top_p, torch.from_numpy(np.asarray(u, np.float32)).to(dev()))
+    torch.cuda.synchronize()
+    return tok.cpu().numpy(), lp.cpu().numpy()
+
+
+def check(hb, wb, inv_t, top_p, u, what, min_exact=0.0):
+    """Checks every row as described above; returns (tokens, exact-match fraction)."""
+    inv_t = np.asarray(inv_t, np.float32)
+    u = np.asarray(u, np.float32)
+    top_p = float(np.float32(top_p))
+    say(f"sampling {what}: R={hb.shape[0]} H={hb.shape[1]} V={wb.shape[0]} top_p={top_p}")
+    tok, lp = gpu_sample(hb, wb, inv_t, top_p, u)
+    V = wb.shape[0]
+    assert np.all((tok >= 0) & (tok < V)), "token out of range"
+    otok, olp, margin = oracle.sample_top_p(hb, wb, inv_t, top_p, u.astype(np.float64))
+    lo, hi = oracle.top_p_interval(hb, wb, inv_t, top_p, tok)
+    uu = u.astype(np.float64)
+    outside = lo < 0
+    if outside.any():
+        wide = min(1.0, top_p + DELTA)
+        lo2, hi2 = oracle.top_p_interval(hb[outside], wb, inv_t[outside], wide, tok[outside])
+        assert np.all(lo2 >= 0), f"{what}: token outside the nucleus at rows {np.flatnonzero(outside)[lo2 < 0]}"
+        lo[outside], hi[outside] = lo2, hi2
+    dev_u = np.maximum(lo - uu, uu - hi)             # <= 0 when u is inside
+    worst = float(dev_u.max())
+    assert worst <= DELTA, f"{what}: u misses the drawn token's interval by {worst:.3g}"
+    robust = (margin[:, 0] > DELTA) & ((margin[:, 1] > DELTA) | (margin[:, 0] > DELTA + margin[:, 2]))
+    bad = robust & (tok != otok)
+    assert not bad.any(), f"{what}: robust rows {np.flatnonzero(bad)[:8]} differ"
+    exact = float(np.mean(tok == otok))
+    # log-prob of the drawn token under the full tempered softmax
+    want = np.empty(len(tok))
+    for t in np.unique(inv_t):
+        rows = np.flatnonzero(inv_t == t)
+        want[rows], _ = oracle.token_logprob(hb[rows], wb, tok[rows], float(t))
+    err = float(np.abs(lp - want).max())
+    say(f"sampling {what}: exact {exact:.3f}, robust {robust.mean():.3f}, worst u offset {worst:.2e}, "
+        f"log-prob max-abs {err:.2e}")
+    assert err <= LOGPROB_TOL, f"{what}: log-prob max-abs {err}"
+    assert exact >= min_exact, f"{what}: only {exact:.3f} of rows match exactly"
+    return tok, exact
+
+
+def test_tiny_config():
+    x = W.make_sample_inputs(W.LOGPROB_CONFIGS["tiny"], "cpu")
+    check(W.bf16_bits(x.hidden), W.bf16_bits(x.w_lm), x.inv_temperature.numpy(), x.top_p, x.uniform.numpy(),
+          "tiny config")
+
+
+@pytest.mark.parametrize("R,H,V,wstd,top_p", [(300, 128, 1000, 0.3, 0.9),    # ragged rows, vocab
+                                              (1, 64, 257, 0.3, 0.9),        # one row, vocab past a tile
+                                              (513, 192, 511, 0.2, 0.5),
+                                              (256, 256, 5000, 0.1, 0.9),    # several chunks of ids
+                                              (2305, 64, 700, 0.3, 0.95),    # more than 8 row tiles
+                                              (200, 128, 3000, 0.3, 1.0)])   # the full distribution
+def test_shapes(R, H, V, wstd, top_p):
+    rng = np.random.Generator(np.random.PCG64(R + H + V))
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), wstd)
+    inv_t = np.where(np.arange(R) % 2 == 0, 1 / 0.2, 1 / 0.7).astype(np.float32)
+    check(hb, wb, inv_t, top_p, rng.random(R, dtype=np.float32), f"shape", min_exact=0.97)
+
+
+def test_greedy_limit():
+    # a tiny top_p keeps only the most probable token
+    rng = np.random.Generator(np.random.PCG64(3))
+    R, H, V = 256, 128, 4000
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.2)
+    tok, _ = check(hb, wb, np.ones(R, np.float32), 1e-6, rng.random(R, dtype=np.float32), "greedy")
+    z = (W.bits_to_bf16(hb).double() @ W.bits_to_bf16(wb).double().T).numpy()
+    top2 = np.sort(z, axis=1)[:, -2:]
+    clear = top2[:, 1] - top2[:, 0] > 1e-4
+    assert np.array_equal(tok[clear], np.argmax(z, axis=1)[clear])
+
+
+def test_ties_by_id():
+    # identical weight rows: every logit equal; the nucleus is the smallest ids
+    R, H, V = 64, 64, 1000
+    rng = np.random.Generator(np.random.PCG64(4))
+    hb = rand_bits(rng, (R, H))
+    wb = np.tile(rand_bits(rng, (1, H), 0.1), (V, 1))
+    u = ((np.arange(R) + 0.5) / R).astype(np.float32)
+    # top_p just under 0.5: the nucleus is 500 ids on both sides, away from the
+    # knife edge at exactly half the mass
+    tok, exact = check(hb, wb, np.ones(R, np.float32), 0.4995, u, "ties")
+    assert np.array_equal(tok, np.floor(u.astype(np.float64) * 500).astype(np.int32))
+
+
+def test_more_ties_than_the_candidate_list():
+    # 10000 equal logits: the tie group alone is larger than the sorted list
+    R, H, V = 16, 64, 10000
+    rng = np.random.Generator(np.random.PCG64(5))
+    hb = rand_bits(rng, (R, H))
+    wb = np.tile(rand_bits(rng, (1, H), 0.1), (V, 1))
+    u = ((np.arange(R) + 0.5) / R).astype(np.float32)
+    tok, _ = check(hb, wb, np.ones(R, np.float32), 0.29995, u, "tie overflow")
+    assert np.array_equal(tok, np.floor(u.astype(np.float64) * 3000).astype(np.int32))
+
+
+def test_dense_cluster_refinement():
+    # 20000 distinct logits within 1/64 of each other (one histogram bucket):
+    # the crossing bucket is refined by key digits before it is sorted.
+    # z = a + b/2^10 + c/2^16 is exact in fp32 for bf16 a in {1, 1+1/128},
+    # b, c in [1, 2).
+    R, H, V = 32, 64, 20000
+    rng = np.random.Generator(np.random.PCG64(6))
+    h = np.zeros((R, H))
+    h[:, 0], h[:, 1], h[:, 2] = 1.0, 2.0 ** -10, 2.0 ** -16
+    w = np.zeros((V, H))
+    w[:, 0] = 1.0 + rng.integers(0, 2, V) / 128.0
+    w[:, 1] = 1.0 + rng.integers(0, 128, V) / 128.0
+    w[:, 2] = 1.0 + rng.integers(0, 128, V) / 128.0
+    to_bits = lambda a: W.bf16_bits(torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16))
+    hb, wb = to_bits(h), to_bits(w)
+    for top_p in (0.3, 0.7):
+        check(hb, wb, np.ones(R, np.float32), top_p, rng.random(R, dtype=np.float32), "dense cluster",
+              min_exact=0.9)
+
+
+def test_several_row_chunks():
+    # more rows than one chunk of logits (8192)
+    rng = np.random.Generator(np.random.PCG64(7))
+    R, H, V = 8192 + 300, 64, 300
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.3)
+    inv_t = np.where(np.arange(R) % 2 == 0, 1 / 0.2, 1 / 0.7).astype(np.float32)
+    check(hb, wb, inv_t, 0.9, rng.random(R, dtype=np.float32), "two chunks", min_exact=0.97)
+
+
+def test_deterministic():
+    rng = np.random.Generator(np.random.PCG64(8))
+    R, H, V = 512, 128, 3000
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.1)
+    inv_t = np.full(R, 1 / 0.7, np.float32)
+    u = rng.random(R, dtype=np.float32)
+    say("sampling determinism")
+    a = gpu_sample(hb, wb, inv_t, 0.9, u)
+    b = gpu_sample(hb, wb, inv_t, 0.9, u)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1].view(np.uint32), b[1].view(np.uint32))
+
+
+def test_frequencies_follow_the_nucleus():
+    # one row repeated with a grid of draws: the GPU's sample counts follow the
+    # oracle's renormalised nucleus
+    rng = np.random.Generator(np.random.PCG64(9))
+    M, H, V = 4096, 64, 200
+    hb = np.repeat(rand_bits(rng, (1, H)), M, 0)
+    wb = rand_bits(rng, (V, H), 0.3)
+    u = ((np.arange(M) + 0.5) / M).astype(np.float32)
+    tok, _ = check(hb, wb, np.full(M, 1 / 0.7, np.float32), 0.9, u, "grid")
+    lo, hi = oracle.top_p_interval(hb[:V], wb, np.full(V, 1 / 0.7, np.float32), float(np.float32(0.9)),
+                                   np.arange(V, dtype=np.int32))
+    counts = np.bincount(tok, minlength=V)
+    share = np.where(lo >= 0, hi - lo, 0.0)
+    assert np.all(np.abs(counts - M * share) <= 1.0 + M * DELTA)
+
+
+def test_empty_rows():
+    w = torch.zeros(10, 64, dtype=torch.bfloat16, device=dev())
+    h = torch.zeros(0, 64, dtype=torch.bfloat16, device=dev())
+    e = torch.zeros(0, dtype=torch.float32, device=dev())
+    tok, lp = rk.sample_top_p(h, w, e, 0.9, e)
+    torch.cuda.synchronize()
+    assert tok.numel() == 0
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,nsample", [("8b", 16), ("32b", 16)])
+def test_full_size_decode_shapes(name, nsample):
+    """Full-size decode-step sampling (both temperatures); the oracle checks a
+    seeded sample of rows (first and last included)."""
+    cfg = W.LOGPROB_CONFIGS[name]
+    say(f"sampling full-size {name}: generating")
+    x = W.make_sample_inputs(cfg, dev())
+    say(f"sampling full-size {name}: gpu")
+    tok, lp = rk.sample_top_p(x.hidden, x.w_lm, x.inv_temperature, x.top_p, x.uniform)
+    torch.cuda.synchronize()
+    rng = np.random.Generator(np.random.PCG64(11))
+    rows = np.unique(np.concatenate([[0, cfg.rows - 1], rng.integers(0, cfg.rows, nsample - 2)]))
+    idx = torch.from_numpy(rows).to(dev())
+    hb, wb = W.bf16_bits(x.hidden[idx]), W.bf16_bits(x.w_lm)
+    it, u = x.inv_temperature[idx].cpu().numpy(), x.uniform[idx].cpu().numpy()
+    say(f"sampling full-size {name}: oracle on {len(rows)} rows")
+    got, _ = check(hb, wb, it, x.top_p, u, f"full-size {name} (rows recomputed)")
+    assert np.array_equal(got, tok[idx].cpu().numpy()), "row subset differs from the full batch"

@@ -264,3 +264,35 @@ def make_grpo_inputs(cfg: GrpoConfig, device="cpu", seed: int = 0, eps: float = 
     new = (old + rng.normal(0.0, drift, R)).astype(np.float32)
     dev = lambda a: torch.from_numpy(a).to(device)
     return GrpoInputs(cfg, dev(reward), dev(old), dev(new), dev(seq), float(np.float32(eps)))
+
+
+# ------------------------------------------------------------ sampling head
+# The rollout draws each turn's candidates by nucleus sampling with p = 0.9
+# at temperatures 0.2 and 0.7 (Sec. 3, Multi-turn RL Training); the rows of a
+# decode step alternate between the two.
+SAMPLE_TEMPERATURES = (0.2, 0.7)
+SAMPLE_TOP_P = 0.9
+
+
+@dataclasses.dataclass
+class SampleInputs:
+    cfg: LogprobConfig
+    hidden: torch.Tensor            # bf16 [R, H]
+    w_lm: torch.Tensor              # bf16 [V, H]
+    inv_temperature: torch.Tensor   # fp32 [R], 1/T per row
+    uniform: torch.Tensor           # fp32 [R], in [0, 1)
+    top_p: float
+
+
+def make_sample_inputs(cfg: LogprobConfig, device="cpu", seed: int = 0, top_p: float = SAMPLE_TOP_P,
+                       w_std: float = 0.02) -> SampleInputs:
+    """Hidden rows and lm-head weight as for the log-prob pass (same seeds);
+    row r samples at temperature SAMPLE_TEMPERATURES[r % 2]; one uniform draw
+    per row (PCG64, float32 in [0, 1))."""
+    R, H, V = cfg.rows, cfg.hidden, cfg.vocab
+    hidden = _randn_bf16((R, H), seed + _SUB["hidden"], device)
+    w = _randn_bf16((V, H), seed + _SUB["w"], device, std=w_std)
+    inv_t = np.array([1.0 / SAMPLE_TEMPERATURES[r % 2] for r in range(R)], dtype=np.float32)
+    u = np.random.Generator(np.random.PCG64(seed + 200)).random(R, dtype=np.float32)
+    return SampleInputs(cfg, hidden, w, torch.from_numpy(inv_t).to(device), torch.from_numpy(u).to(device),
+                        float(np.float32(top_p)))
