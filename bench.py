@@ -8,10 +8,11 @@ workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
 / 8 kv heads, head dim 128, shared prefix 1024, suffix lengths uniform in
 [256, 2048]; lm-head 512 rows x hidden 4096 x vocab 151936).
 
-After the timed steps, the policy-update operations are timed in a loop of
-their own (outside the step): the backward of the lm-head log-prob for the
-same rows, and the GRPO advantages and clipped surrogate over the policy
-pass's 262144 rows.  They are reported under "policy_update".
+After the timed steps, further operations are timed in a loop of their own
+(outside the step): the backward of the lm-head log-prob for the same rows,
+the GRPO advantages and clipped surrogate over the policy pass's 262144 rows,
+and (at decode shapes) the nucleus sampling head over the same rows.  They
+are reported under "extra_ops".
 
 Prints ONE JSON line.  `value` is decode attention's effective KV bandwidth
 (algorithmic bytes, the prefix counted once per prompt, over the measured
@@ -331,6 +332,18 @@ def main():
                 ("grpo", lambda: (rk.grpo_advantage(gx.reward, G, adv=adv),
                                   rk.grpo_surrogate(gx.logp_new, gx.logp_old, gx.seq, adv, G, gx.eps,
                                                     loss=gl, grad=gg, workspace=ws_g)))]
+        sx = None
+        if cl.rows <= 65536:
+            # the sampling head at the decode step's shape: rows alternate
+            # between the two temperatures, nucleus p = 0.9
+            sx = W.make_sample_inputs(cl, dev)
+            s_tok = torch.empty(cl.rows, dtype=torch.int32, device=dev)
+            s_lp = torch.empty(cl.rows, dtype=torch.float32, device=dev)
+            ws_s = torch.empty(rk.sample_top_p_workspace_size(cl.rows, cl.hidden, cl.vocab), dtype=torch.uint8,
+                               device=dev)
+            uops.append(("sample", lambda: rk.sample_top_p(sx.hidden, sx.w_lm, sx.inv_temperature, sx.top_p,
+                                                           sx.uniform, token=s_tok, logprob=s_lp,
+                                                           workspace=ws_s)))
         usteps = max(1, min(args.steps, 3 if cl.rows > 65536 else args.steps))
         for _, f in uops:
             f()
@@ -362,6 +375,14 @@ def main():
                            "us": round(u_ms["grpo"] * 1e3, 2), "bound": "hbm",
                            "achieved": round(nb_g / (u_ms["grpo"] * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                            "unit": "GB/s", "algorithmic_bytes": nb_g}}
+        if sx is not None:
+            fl_s = lmhead_flops(cl)
+            tf_s = fl_s / (u_ms["sample"] * 1e-3) / 1e12
+            update["sampling_head"] = {
+                "kernel": "nucleus sampling head (logits tile + per-row selection kernels), T in {0.2, 0.7}, "
+                          "top-p 0.9", "ms": round(u_ms["sample"], 4), "bound": "mfma",
+                "achieved": round(tf_s, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tf_s / MFMA_BF16_PEAK_TFLOPS, 4), "algorithmic_flops": fl_s}
 
     res = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
@@ -410,7 +431,7 @@ def main():
     if len(rooflines) > 1:
         res["roofline_other"] = rooflines[1][1]
     if update is not None:
-        res["policy_update"] = update
+        res["extra_ops"] = update
     if args.cpu_budget > 0:
         log("bench: cpu baseline (fp64 oracle)")
         if x is not None:

@@ -27,7 +27,8 @@
 namespace rlk {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 1024;          // 16 waves per row: the passes are issue-bound
+constexpr int kWaves = kThreads / 64;
 constexpr int kBuckets = 4096;
 constexpr float kBucketScale = 64.f;
 constexpr int kCap = 4096;              // candidates sorted in LDS
@@ -76,30 +77,40 @@ __device__ __forceinline__ T wave_incl_scan(T v, int lane) {
 }
 
 struct SelShared {
-    uint64_t hist[kBuckets];            // pass 1: bucket masses; pass 2: digit masses
-    uint64_t cand[kCap];                // (key << 32) | ~id of the candidates
-    uint64_t chunk_mass[kMaxChunks];    // nucleus mass above tau per chunk
-    uint32_t chunk_ties[kMaxChunks];    // tokens with key tau per chunk
-    uint32_t dcount[256];               // pass 2: digit counts
-    uint64_t part[kThreads];            // block scans
-    uint64_t zsum[kThreads / 64];
-    float fred[kThreads / 64];
+    union {
+        uint64_t hist[kBuckets];                    // bucket masses; later digit masses
+        struct {
+            uint64_t mass[kMaxChunks];              // nucleus mass above tau per chunk of ids
+            uint32_t ties[kMaxChunks];              // tokens with key tau per chunk
+        } chunk;                                    // (once the histograms are no longer read)
+    } a;
+    union {
+        uint32_t bcount[kBuckets];                  // tokens per bucket
+        uint64_t cand[kCap];                        // (key << 32) | ~id of the candidates
+    } b;
+    uint32_t dcount[256];                           // tokens per key digit
+    uint64_t part[kThreads];                        // block scans
+    uint64_t zsum[kWaves];
+    float fred[kWaves];
     uint32_t ncand;
 };
 
-// Exclusive scan of one value per thread (256 threads); returns the total.
+// Exclusive scan of one value per thread; returns the total.
 __device__ uint64_t block_excl_scan(SelShared &sh, uint64_t v, uint64_t *excl) {
     const int tid = threadIdx.x;
     sh.part[tid] = v;
     __syncthreads();
     if (tid < 64) {
-        uint64_t s4 = sh.part[4 * tid] + sh.part[4 * tid + 1] + sh.part[4 * tid + 2] + sh.part[4 * tid + 3];
-        const uint64_t inc = wave_incl_scan(s4, tid);
-        uint64_t run = inc - s4;
+        constexpr int kPerLane = kThreads / 64;
+        uint64_t sl = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint64_t x = sh.part[4 * tid + j];
-            sh.part[4 * tid + j] = run;
+        for (int j = 0; j < kPerLane; ++j) sl += sh.part[kPerLane * tid + j];
+        const uint64_t inc = wave_incl_scan(sl, tid);
+        uint64_t run = inc - sl;
+#pragma unroll
+        for (int j = 0; j < kPerLane; ++j) {
+            const uint64_t x = sh.part[kPerLane * tid + j];
+            sh.part[kPerLane * tid + j] = run;
             run += x;
         }
         if (tid == 63) sh.zsum[0] = inc;
@@ -111,6 +122,83 @@ __device__ uint64_t block_excl_scan(SelShared &sh, uint64_t v, uint64_t *excl) {
     return total;
 }
 
+// Calls f(v, y_v) for the ids of float4 groups g0, g0 + step, ... below g1
+// (ids < V only), with four groups' loads in flight: the passes are bound by
+// how many bytes each CU keeps in flight against the HBM latency.
+template <typename F>
+__device__ __forceinline__ void scan_groups(const float *y, int V, int g0, int g1, int step, F &&f) {
+    auto visit = [&](const float4 q4, int g) {
+        const float yy[4] = {q4.x, q4.y, q4.z, q4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (4 * g + e < V) f(4 * g + e, yy[e]);
+    };
+    int g = g0;
+    for (; g + 3 * step < g1; g += 4 * step) {
+        float4 q[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) q[j] = *reinterpret_cast<const float4 *>(y + 4 * (g + j * step));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) visit(q[j], g + j * step);
+    }
+    for (; g < g1; g += step) visit(*reinterpret_cast<const float4 *>(y + 4 * g), g);
+}
+
+// Sorts the ncand gathered candidates by (key desc, id asc) and walks their
+// masses from `above` to the first position reaching T: its key is tau and k
+// counts the key-tau candidates up to it.
+__device__ void sort_and_walk(SelShared &sh, uint32_t ncand, uint64_t above, uint64_t T, float m, uint32_t *tau,
+                              uint64_t *k) {
+    const int tid = threadIdx.x;
+    int n2 = 1;
+    while (n2 < static_cast<int>(ncand)) n2 <<= 1;
+    for (int i = static_cast<int>(ncand) + tid; i < n2; i += kThreads) sh.b.cand[i] = 0;   // sorts last
+    __syncthreads();
+    for (int size = 2; size <= n2; size <<= 1) {                   // bitonic, descending
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = tid; i < n2 / 2; i += kThreads) {
+                const int lo = 2 * i - (i & (stride - 1));
+                const int hi = lo + stride;
+                const bool desc = (lo & size) == 0;
+                const uint64_t x = sh.b.cand[lo], z = sh.b.cand[hi];
+                if ((x < z) == desc) {
+                    sh.b.cand[lo] = z;
+                    sh.b.cand[hi] = x;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    const int per = (static_cast<int>(ncand) + kThreads - 1) / kThreads;
+    const int i0 = tid * per, i1 = min(static_cast<int>(ncand), i0 + per);
+    uint64_t seg = 0;
+    for (int i = i0; i < i1; ++i) seg += qmass(key_to_float(static_cast<uint32_t>(sh.b.cand[i] >> 32)), m);
+    uint64_t segb;
+    block_excl_scan(sh, seg, &segb);
+    if (tid == 0) {                                                // defaults for a degenerate row
+        sh.part[0] = ncand ? static_cast<uint32_t>(sh.b.cand[ncand - 1] >> 32) : 0u;
+        sh.part[1] = 0;
+    }
+    __syncthreads();
+    if (i0 < i1 && above + segb < T && above + segb + seg >= T) {
+        uint64_t acc = above + segb;
+        int i = i0;
+        for (;; ++i) {
+            acc += qmass(key_to_float(static_cast<uint32_t>(sh.b.cand[i] >> 32)), m);
+            if (acc >= T || i == i1 - 1) break;
+        }
+        const uint32_t kt = static_cast<uint32_t>(sh.b.cand[i] >> 32);
+        int f = i;
+        while (f > 0 && static_cast<uint32_t>(sh.b.cand[f - 1] >> 32) == kt) --f;
+        sh.part[0] = kt;
+        sh.part[1] = static_cast<uint64_t>(i - f + 1);
+    }
+    __syncthreads();
+    *tau = static_cast<uint32_t>(sh.part[0]);
+    *k = sh.part[1];
+    __syncthreads();
+}
+
 __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     __shared__ SelShared sh;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -118,36 +206,36 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     const float *y = a.logits + r * a.ld;
     const int V = a.V;
     const int nvec = (V + 3) / 4;                 // float4 groups (the row is padded past V)
+    const int nchunks = (V + kChunk - 1) / kChunk;
 
     // ---- row max from the tile maxima
     float m = -INFINITY;
     for (int t = tid; t < a.n_vocab_tiles; t += kThreads) m = fmaxf(m, a.pm[static_cast<int64_t>(t) * a.rows + r]);
     m = wave_max(m);
     if (lane == 0) sh.fred[wave] = m;
-    for (int i = tid; i < kBuckets; i += kThreads) sh.hist[i] = 0;
-    __syncthreads();
-    m = fmaxf(fmaxf(sh.fred[0], sh.fred[1]), fmaxf(sh.fred[2], sh.fred[3]));
-
-    // ---- pass 1: bucket masses and the total
-    uint64_t zloc = 0;
-    for (int g = tid; g < nvec; g += kThreads) {
-        const float4 y4 = *reinterpret_cast<const float4 *>(y + 4 * g);
-        const float yy[4] = {y4.x, y4.y, y4.z, y4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            if (4 * g + e >= V) break;
-            const uint64_t q = qmass(yy[e], m);
-            if (q) {
-                atomicAdd(reinterpret_cast<unsigned long long *>(&sh.hist[bucket_of(yy[e], m)]),
-                          static_cast<unsigned long long>(q));
-                zloc += q;
-            }
-        }
+    for (int i = tid; i < kBuckets; i += kThreads) {
+        sh.a.hist[i] = 0;
+        sh.b.bcount[i] = 0;
     }
+    __syncthreads();
+    for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sh.fred[w]);
+
+    // ---- pass 1: bucket masses and counts, and the total mass
+    uint64_t zloc = 0;
+    scan_groups(y, V, tid, nvec, kThreads, [&](int, float yv) {
+        const int b = bucket_of(yv, m);
+        const uint64_t q = qmass(yv, m);
+        if (q) {
+            atomicAdd(reinterpret_cast<unsigned long long *>(&sh.a.hist[b]), static_cast<unsigned long long>(q));
+            zloc += q;
+        }
+        atomicAdd(&sh.b.bcount[b], 1u);
+    });
     zloc = wave_sum_int(zloc);
     if (lane == 0) sh.zsum[wave] = zloc;
     __syncthreads();
-    const uint64_t Z = sh.zsum[0] + sh.zsum[1] + sh.zsum[2] + sh.zsum[3];
+    uint64_t Z = 0;
+    for (int w = 0; w < kWaves; ++w) Z += sh.zsum[w];
     uint64_t T = a.top_p >= 1.f ? Z : static_cast<uint64_t>(ceil(static_cast<double>(a.top_p) * static_cast<double>(Z)));
     if (T < 1) T = 1;
     if (T > Z) T = Z;
@@ -156,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     constexpr int kPer = kBuckets / kThreads;
     uint64_t mine = 0;
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) mine += sh.hist[tid * kPer + j];
+    for (int j = 0; j < kPer; ++j) mine += sh.a.hist[tid * kPer + j];
     uint64_t before;
     block_excl_scan(sh, mine, &before);
     if (tid == 0) {                              // defaults, in range, for a degenerate row
@@ -167,188 +255,141 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     if (before < T && before + mine >= T) {
         uint64_t acc = before;
         int b = tid * kPer;
-        while (acc + sh.hist[b] < T) acc += sh.hist[b++];
+        while (acc + sh.a.hist[b] < T) acc += sh.a.hist[b++];
         sh.part[0] = acc;                        // mass above the bucket
         sh.zsum[0] = static_cast<uint64_t>(b);
     }
     __syncthreads();
     uint64_t above = sh.part[0];
     const int B = static_cast<int>(sh.zsum[0]);
-    __syncthreads();
+    uint32_t ncand = sh.b.bcount[B];
+    __syncthreads();                             // histograms and counts are free from here
 
-    // ---- refine by 8-bit key digits while the candidate set is too large
-    // (the set: bucket B, key >> shift == prefix)
-    int shift = 32;
-    uint32_t prefix = 0;
-    bool ties_only = false;
-    uint32_t ncand = 0;
-    for (;;) {
-        if (tid == 0) sh.ncand = 0;
-        __syncthreads();
-        // count the set
-        uint32_t cnt = 0;
-        for (int g = tid; g < nvec; g += kThreads) {
-            const float4 y4 = *reinterpret_cast<const float4 *>(y + 4 * g);
-            const float yy[4] = {y4.x, y4.y, y4.z, y4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (4 * g + e >= V) break;
-                const uint32_t k = fkey(yy[e]);
-                cnt += bucket_of(yy[e], m) == B && (shift == 32 || (k >> shift) == prefix);
-            }
-        }
-        cnt = wave_sum_int(cnt);
-        if (lane == 0) atomicAdd(&sh.ncand, cnt);
-        __syncthreads();
-        ncand = sh.ncand;
-        __syncthreads();
-        if (ncand <= kCap) break;
-        if (shift == 0) {
-            ties_only = true;                    // more than kCap tokens share one key
-            break;
-        }
-        // digit histogram of the set at the next 8 bits
-        const int s2 = shift - 8;
-        for (int i = tid; i < 256; i += kThreads) {
-            sh.hist[i] = 0;
-            sh.dcount[i] = 0;
-        }
-        __syncthreads();
-        for (int g = tid; g < nvec; g += kThreads) {
-            const float4 y4 = *reinterpret_cast<const float4 *>(y + 4 * g);
-            const float yy[4] = {y4.x, y4.y, y4.z, y4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (4 * g + e >= V) break;
-                const uint32_t k = fkey(yy[e]);
-                if (bucket_of(yy[e], m) == B && (shift == 32 || (k >> shift) == prefix)) {
-                    const int d = (k >> s2) & 255;
-                    atomicAdd(reinterpret_cast<unsigned long long *>(&sh.hist[d]),
-                              static_cast<unsigned long long>(qmass(yy[e], m)));
-                    atomicAdd(&sh.dcount[d], 1u);
-                }
-            }
-        }
-        __syncthreads();
-        if (tid == 0) {
-            // digits from the largest key down
-            uint64_t acc = above;
-            int d = 255;
-            while (d > 0 && (acc + sh.hist[d] < T || sh.dcount[d] == 0)) acc += sh.hist[d--];
-            sh.part[0] = acc;
-            sh.zsum[0] = static_cast<uint64_t>(d);
-        }
-        __syncthreads();
-        above = sh.part[0];
-        prefix = (shift == 32 ? 0u : (prefix << 8)) | static_cast<uint32_t>(sh.zsum[0]);
-        shift = s2;
-        __syncthreads();
-    }
-
-    // ---- tau (the last member's key) and k (members among the key-tau tokens)
     uint32_t tau;
     uint64_t k;
-    if (ties_only) {
-        tau = prefix;
-        const uint64_t qt = qmass(key_to_float(tau), m);
-        k = qt ? (T - above + qt - 1) / qt : ncand;
-        if (k > ncand) k = ncand;
-    } else {
-        // gather the set, sort it by (key desc, id asc), walk its masses
+    if (ncand <= kCap) {
+        // ---- fast path, one more pass: per chunk of ids the mass of the
+        // buckets above B, and the tokens of B gathered for sorting
         if (tid == 0) sh.ncand = 0;
         __syncthreads();
-        for (int g = tid; g < nvec; g += kThreads) {
-            const float4 y4 = *reinterpret_cast<const float4 *>(y + 4 * g);
-            const float yy[4] = {y4.x, y4.y, y4.z, y4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int v = 4 * g + e;
-                if (v >= V) break;
-                const uint32_t kk = fkey(yy[e]);
-                if (bucket_of(yy[e], m) == B && (shift == 32 || (kk >> shift) == prefix)) {
+        for (int c = wave; c < nchunks; c += kWaves) {
+            uint64_t ms = 0;
+            scan_groups(y, V, c * (kChunk / 4) + lane, min(nvec, (c + 1) * (kChunk / 4)), 64, [&](int v, float yv) {
+                const int b = bucket_of(yv, m);
+                if (b < B) {
+                    ms += qmass(yv, m);
+                } else if (b == B) {
                     const uint32_t slot = atomicAdd(&sh.ncand, 1u);
-                    sh.cand[slot] = (static_cast<uint64_t>(kk) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(v));
+                    sh.b.cand[slot] = (static_cast<uint64_t>(fkey(yv)) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(v));
                 }
+            });
+            ms = wave_sum_int(ms);
+            if (lane == 0) {
+                sh.a.chunk.mass[c] = ms;
+                sh.a.chunk.ties[c] = 0;
             }
         }
         __syncthreads();
-        int n2 = 1;
-        while (n2 < static_cast<int>(ncand)) n2 <<= 1;
-        for (int i = static_cast<int>(ncand) + tid; i < n2; i += kThreads) sh.cand[i] = 0;   // sorts last
+        sort_and_walk(sh, ncand, above, T, m, &tau, &k);
+        // the candidates complete the chunk masses (key above tau) and tie counts
+        for (int i = tid; i < static_cast<int>(ncand); i += kThreads) {
+            const uint32_t kk = static_cast<uint32_t>(sh.b.cand[i] >> 32);
+            const int c = static_cast<int>(~static_cast<uint32_t>(sh.b.cand[i])) / kChunk;
+            if (kk > tau)
+                atomicAdd(reinterpret_cast<unsigned long long *>(&sh.a.chunk.mass[c]),
+                          static_cast<unsigned long long>(qmass(key_to_float(kk), m)));
+            else if (kk == tau)
+                atomicAdd(&sh.a.chunk.ties[c], 1u);
+        }
         __syncthreads();
-        // bitonic sort, descending
-        for (int size = 2; size <= n2; size <<= 1) {
-            for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                for (int i = tid; i < n2 / 2; i += kThreads) {
-                    const int lo = 2 * i - (i & (stride - 1));
-                    const int hi = lo + stride;
-                    const bool desc = (lo & size) == 0;
-                    const uint64_t x = sh.cand[lo], z = sh.cand[hi];
-                    if ((x < z) == desc) {
-                        sh.cand[lo] = z;
-                        sh.cand[hi] = x;
-                    }
+    } else {
+        // ---- B holds more than kCap tokens: refine the set (bucket B, key >>
+        // shift == prefix) by 8-bit key digits until it fits or is one key
+        int shift = 32;
+        uint32_t prefix = 0;
+        bool ties_only = false;
+        for (;;) {
+            if (shift == 0) {
+                ties_only = true;                // more than kCap tokens share one key
+                break;
+            }
+            const int s2 = shift - 8;
+            for (int i = tid; i < 256; i += kThreads) {
+                sh.a.hist[i] = 0;
+                sh.dcount[i] = 0;
+            }
+            __syncthreads();
+            scan_groups(y, V, tid, nvec, kThreads, [&](int, float yv) {
+                const uint32_t kk = fkey(yv);
+                if (bucket_of(yv, m) == B && (shift == 32 || (kk >> shift) == prefix)) {
+                    const int d = (kk >> s2) & 255;
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&sh.a.hist[d]),
+                              static_cast<unsigned long long>(qmass(yv, m)));
+                    atomicAdd(&sh.dcount[d], 1u);
                 }
-                __syncthreads();
+            });
+            __syncthreads();
+            if (tid == 0) {
+                // digits from the largest key down
+                uint64_t acc = above;
+                int d = 255;
+                while (d > 0 && (acc + sh.a.hist[d] < T || sh.dcount[d] == 0)) acc += sh.a.hist[d--];
+                sh.part[0] = acc;
+                sh.zsum[0] = static_cast<uint64_t>(d);
+            }
+            __syncthreads();
+            above = sh.part[0];
+            const uint32_t d = static_cast<uint32_t>(sh.zsum[0]);
+            prefix = (shift == 32 ? 0u : (prefix << 8)) | d;
+            shift = s2;
+            ncand = sh.dcount[d];
+            __syncthreads();
+            if (ncand <= kCap) break;
+        }
+        if (ties_only) {
+            tau = prefix;
+            const uint64_t qt = qmass(key_to_float(tau), m);
+            k = qt ? (T - above + qt - 1) / qt : ncand;
+            if (k > ncand) k = ncand;
+        } else {
+            if (tid == 0) sh.ncand = 0;
+            __syncthreads();
+            scan_groups(y, V, tid, nvec, kThreads, [&](int v, float yv) {
+                const uint32_t kk = fkey(yv);
+                if (bucket_of(yv, m) == B && (kk >> shift) == prefix) {
+                    const uint32_t slot = atomicAdd(&sh.ncand, 1u);
+                    sh.b.cand[slot] = (static_cast<uint64_t>(kk) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(v));
+                }
+            });
+            __syncthreads();
+            sort_and_walk(sh, ncand, above, T, m, &tau, &k);
+        }
+        // per chunk: mass of members above tau and count of key-tau tokens
+        for (int c = wave; c < nchunks; c += kWaves) {
+            uint64_t ms = 0;
+            uint32_t nt = 0;
+            scan_groups(y, V, c * (kChunk / 4) + lane, min(nvec, (c + 1) * (kChunk / 4)), 64, [&](int, float yv) {
+                const uint32_t kk = fkey(yv);
+                if (kk > tau) ms += qmass(yv, m);
+                nt += kk == tau;
+            });
+            ms = wave_sum_int(ms);
+            nt = wave_sum_int(nt);
+            if (lane == 0) {
+                sh.a.chunk.mass[c] = ms;
+                sh.a.chunk.ties[c] = nt;
             }
         }
-        // walk: first position where above + prefix mass reaches T
-        const int per = (static_cast<int>(ncand) + kThreads - 1) / kThreads;
-        const int i0 = tid * per, i1 = min(static_cast<int>(ncand), i0 + per);
-        uint64_t seg = 0;
-        for (int i = i0; i < i1; ++i) seg += qmass(key_to_float(static_cast<uint32_t>(sh.cand[i] >> 32)), m);
-        uint64_t segb;
-        block_excl_scan(sh, seg, &segb);
-        if (i0 < i1 && above + segb < T && above + segb + seg >= T) {
-            uint64_t acc = above + segb;
-            int i = i0;
-            for (;; ++i) {
-                acc += qmass(key_to_float(static_cast<uint32_t>(sh.cand[i] >> 32)), m);
-                if (acc >= T || i == i1 - 1) break;
-            }
-            const uint32_t kt = static_cast<uint32_t>(sh.cand[i] >> 32);
-            int f = i;
-            while (f > 0 && static_cast<uint32_t>(sh.cand[f - 1] >> 32) == kt) --f;
-            sh.part[0] = kt;
-            sh.part[1] = static_cast<uint64_t>(i - f + 1);
-        }
-        __syncthreads();
-        tau = static_cast<uint32_t>(sh.part[0]);
-        k = sh.part[1];
         __syncthreads();
     }
 
-    // ---- per chunk: mass of members above tau and count of key-tau tokens
-    const int nchunks = (V + kChunk - 1) / kChunk;
-    for (int c = wave; c < nchunks; c += kThreads / 64) {
-        uint64_t ms = 0;
-        uint32_t nt = 0;
-        for (int g = c * (kChunk / 4) + lane; g < min(nvec, (c + 1) * (kChunk / 4)); g += 64) {
-            const float4 y4 = *reinterpret_cast<const float4 *>(y + 4 * g);
-            const float yy[4] = {y4.x, y4.y, y4.z, y4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (4 * g + e >= V) break;
-                const uint32_t kk = fkey(yy[e]);
-                if (kk > tau) ms += qmass(yy[e], m);
-                nt += kk == tau;
-            }
-        }
-        ms = wave_sum_int(ms);
-        nt = wave_sum_int(nt);
-        if (lane == 0) {
-            sh.chunk_mass[c] = ms;
-            sh.chunk_ties[c] = nt;
-        }
-    }
-    __syncthreads();
     const uint64_t qt = qmass(key_to_float(tau), m);
     if (tid == 0) {
         uint64_t zn = 0, tb = 0;
         for (int c = 0; c < nchunks; ++c) {
-            const uint64_t inc = min(static_cast<uint64_t>(sh.chunk_ties[c]), k > tb ? k - tb : 0);
-            zn += sh.chunk_mass[c] + inc * qt;
-            tb += sh.chunk_ties[c];
+            const uint64_t inc = min(static_cast<uint64_t>(sh.a.chunk.ties[c]), k > tb ? k - tb : 0);
+            zn += sh.a.chunk.mass[c] + inc * qt;
+            tb += sh.a.chunk.ties[c];
         }
         uint64_t U = static_cast<uint64_t>(floor(static_cast<double>(a.uniform[r]) * static_cast<double>(zn)));
         if (!(U < zn)) U = zn ? zn - 1 : 0;
@@ -358,8 +399,8 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
         int cs = nchunks - 1;
         uint64_t tb_cs = 0, cum_cs = 0;
         for (int c = 0; c < nchunks; ++c) {
-            const uint64_t inc = min(static_cast<uint64_t>(sh.chunk_ties[c]), k > tb ? k - tb : 0);
-            const uint64_t mc = sh.chunk_mass[c] + inc * qt;
+            const uint64_t inc = min(static_cast<uint64_t>(sh.a.chunk.ties[c]), k > tb ? k - tb : 0);
+            const uint64_t mc = sh.a.chunk.mass[c] + inc * qt;
             if (cum + mc > U) {
                 cs = c;
                 tb_cs = tb;
@@ -367,7 +408,7 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
                 break;
             }
             cum += mc;
-            tb += sh.chunk_ties[c];
+            tb += sh.a.chunk.ties[c];
             tb_cs = tb;
             cum_cs = cum;
         }
