@@ -9,7 +9,8 @@ workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
 [256, 2048]; lm-head 512 rows x hidden 4096 x vocab 151936).
 
 After the timed steps, further operations are timed in a loop of their own
-(outside the step): the backward of the lm-head log-prob for the same rows,
+(outside the step): the KV append of one token per candidate, the backward
+of the lm-head log-prob for the same rows,
 the GRPO advantages and clipped surrogate over the policy pass's 262144 rows,
 and (at decode shapes) the nucleus sampling head over the same rows.  They
 are reported under "extra_ops".
@@ -312,6 +313,40 @@ def main():
     # seeded N(0, 1), lse from the forward above) and the GRPO surrogate over
     # the policy pass's 262144 rows
     update = None
+    if x is not None and not args.no_update:
+        # the decode loop's cache update: one new token per candidate appended
+        # in place after its suffix (a cache with 16 free rows per candidate)
+        c = x.cfg
+        S = c.num_seqs
+        kn = torch.randn((S, c.num_kv_heads, c.head_dim), device=dev).to(torch.bfloat16)
+        vn = torch.randn_like(kn)
+        cshape = (c.num_kv_heads, S * 16, c.head_dim) if args.kv_layout == "head" else (S * 16, c.num_kv_heads,
+                                                                                       c.head_dim)
+        kc = torch.zeros(cshape, dtype=torch.bfloat16, device=dev)
+        vc = torch.zeros_like(kc)
+        a_ss, a_sl = np.arange(S, dtype=np.int64) * 16, np.zeros(S, np.int32)
+        a_ns, a_nl = np.arange(S, dtype=np.int64), np.ones(S, np.int32)
+        ws_a = torch.empty(max(256, 16 * S + 256), dtype=torch.uint8, device=dev)
+        run_append = lambda: rk.kv_append(kn, vn, kc, vc, a_ss, a_sl, a_ns, a_nl, c.group_size,
+                                          kv_layout=args.kv_layout, workspace=ws_a)
+        for _ in range(3):
+            run_append()
+        torch.cuda.synchronize()
+        aev = [(hip.create(), hip.create()) for _ in range(args.steps)]
+        for e0, e1 in aev:
+            hip.record(e0, sh)
+            run_append()
+            hip.record(e1, sh)
+        torch.cuda.synchronize()
+        a_ms = float(np.mean([hip.elapsed_ms(e0, e1) for e0, e1 in aev]))
+        for pair in aev:
+            for e in pair:
+                hip.destroy(e)
+        nb_a = 2 * 2 * (2 * S * c.num_kv_heads * c.head_dim)      # K and V, read and written
+        update = {"kv_append": {"kernel": "KV append, one token per candidate (fetch + copy kernels)",
+                                "us": round(a_ms * 1e3, 2), "bound": "hbm",
+                                "achieved": round(nb_a / (a_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                                "unit": "GB/s", "algorithmic_bytes": nb_a}}
     if y is not None and not args.no_update:
         cl = y.cfg
         g_b = torch.from_numpy(np.random.Generator(np.random.PCG64(5)).standard_normal(cl.rows)
@@ -364,7 +399,8 @@ def main():
         fl_b = 4 * cl.rows * cl.hidden * cl.vocab
         tf_b = fl_b / (u_ms["backward"] * 1e-3) / 1e12
         nb_g = grpo_bytes(gx)
-        update = {"steps": usteps,
+        update = dict(update or {})
+        update.update({"steps": usteps,
                   "lmhead_backward": {"kernel": "log-prob backward (probability tile + vocab GEMM + finish "
                                                 "kernels, per 16384-row chunk)",
                                       "ms": round(u_ms["backward"], 4), "bound": "mfma",
@@ -374,7 +410,7 @@ def main():
                   "grpo": {"kernel": "GRPO advantages + clipped surrogate, 4 x G=16 sequences x 4096 rows",
                            "us": round(u_ms["grpo"] * 1e3, 2), "bound": "hbm",
                            "achieved": round(nb_g / (u_ms["grpo"] * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
-                           "unit": "GB/s", "algorithmic_bytes": nb_g}}
+                           "unit": "GB/s", "algorithmic_bytes": nb_g}})
         if sx is not None:
             fl_s = lmhead_flops(cl)
             tf_s = fl_s / (u_ms["sample"] * 1e-3) / 1e12

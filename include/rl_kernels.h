@@ -12,6 +12,10 @@
  *                     each has its own suffix KV (its generated tokens, at most
  *                     1536 per turn in Sec. 3, Multi-turn RL Training).
  *
+ *  rl_kv_append       writes new tokens' keys and values after each
+ *                     candidate's suffix in place (the decode loop's cache
+ *                     update).
+ *
  *  rl_token_logprob   log pi(o_t | q, o_<t) of each sampled token under the
  *                     policy, the factor of the GRPO ratio (Sec. 3, Eq.
  *                     grpo-loss), computed from the last hidden state and the
@@ -65,7 +69,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 5
+#define RL_ABI_VERSION 6
 
 typedef enum {
     RL_OK = 0,
@@ -146,6 +150,51 @@ rl_status rl_decode_attn_workspace_size(const rl_decode_shape *shape,
 rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *lens,
                          const rl_decode_ptrs *ptrs,
                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Appending to the suffix KV cache                                          */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * A rollout adds one token per candidate per decode step (up to 1536
+ * generated tokens per turn, Sec. 3, Multi-turn RL Training).  rl_kv_append
+ * writes the new tokens' keys and values after each candidate's suffix in
+ * place, so a cache with a region of fixed capacity per candidate grows
+ * without repacking.  For candidate s and i < new_len[s], at every kv head:
+ *   suffix row suffix_start[s] + suffix_len[s] + i  <-  row new_start[s] + i
+ *   of k_new / v_new,
+ * in the cache layout shape->kv_layout.  k_new and v_new are token-major
+ * [new_rows, Hkv, D] bf16.  The suffix of s is then suffix_len[s] + new_len[s]
+ * tokens long; the caller keeps the lengths.  Only num_prompts, group_size,
+ * num_kv_heads, head_dim and kv_layout of the shape are used.
+ */
+typedef struct {
+    const int64_t *suffix_start;    /* host [P*G]: first row of candidate s's region      */
+    const int32_t *suffix_len;      /* host [P*G]: tokens already there                   */
+    const int32_t *suffix_capacity; /* host [P*G]: rows reserved for s, or NULL (then only
+                                       suffix_rows bounds the writes)                    */
+    const int64_t *new_start;       /* host [P*G]: first row of s's new tokens in k_new   */
+    const int32_t *new_len;         /* host [P*G] >= 0: tokens to append                  */
+    int64_t suffix_rows;            /* rows allocated in k_suffix / v_suffix              */
+    int64_t new_rows;               /* rows of k_new / v_new                              */
+} rl_kv_append_lens;
+
+/*
+ * The workspace holds the (source, destination) row pairs, 16 bytes per new
+ * token.  Status: NULL pointer -> RL_ERR_NULL_POINTER; negative lengths or
+ * starts, a write past suffix_rows or past a candidate's capacity, a source
+ * range past new_rows, or two candidates writing the same row ->
+ * RL_ERR_INVALID_SHAPE; head_dim not in {64, 128} or a bad kv_layout ->
+ * RL_ERR_UNSUPPORTED / RL_ERR_INVALID_SHAPE; a tensor not 16-byte aligned ->
+ * RL_ERR_MISALIGNED; workspace NULL or short -> RL_ERR_WORKSPACE.  No new
+ * tokens is a valid no-op.
+ */
+rl_status rl_kv_append_workspace_size(const rl_decode_shape *shape, const rl_kv_append_lens *lens,
+                                      size_t *bytes);
+
+rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *lens,
+                       const void *k_new, const void *v_new, void *k_suffix, void *v_suffix,
+                       void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Token log-prob through the lm-head                                        */

@@ -305,6 +305,28 @@ def top_p_interval(hidden, w_lm, inv_temperature, top_p: float, token, _lib=None
     return lo, hi
 
 
+def kv_append(k_suffix, v_suffix, k_new, v_new, suffix_start, suffix_len, new_start, new_len,
+              kv_layout: str = "token"):
+    """The suffix caches after appending: rows new_start[s] + i of k_new / v_new
+    ([new_rows, Hkv, D], token-major) become suffix rows suffix_start[s] +
+    suffix_len[s] + i, i < new_len[s], at every kv head; every other row is
+    unchanged.  Caches are [rows, Hkv, D] (token) or [Hkv, rows, D] (head);
+    any dtype (the copy moves bits).  Returns new arrays."""
+    ks, vs = np.array(k_suffix, copy=True), np.array(v_suffix, copy=True)
+    kn, vn = np.asarray(k_new), np.asarray(v_new)
+    for s in range(len(suffix_start)):
+        for i in range(int(new_len[s])):
+            src = int(new_start[s]) + i
+            dst = int(suffix_start[s]) + int(suffix_len[s]) + i
+            if kv_layout == "head":
+                ks[:, dst, :] = kn[src]
+                vs[:, dst, :] = vn[src]
+            else:
+                ks[dst] = kn[src]
+                vs[dst] = vn[src]
+    return ks, vs
+
+
 def num_threads() -> int:
     """Threads OpenMP will use (OMP_NUM_THREADS, else the CPUs this process may run on)."""
     env = os.environ.get("OMP_NUM_THREADS")

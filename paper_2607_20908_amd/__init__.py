@@ -55,6 +55,12 @@ class DecodeLens(ctypes.Structure):
                 ("prefix_rows", ctypes.c_int64), ("suffix_rows", ctypes.c_int64)]
 
 
+class KvAppendLens(ctypes.Structure):
+    _fields_ = [("suffix_start", ctypes.c_void_p), ("suffix_len", ctypes.c_void_p),
+                ("suffix_capacity", ctypes.c_void_p), ("new_start", ctypes.c_void_p),
+                ("new_len", ctypes.c_void_p), ("suffix_rows", ctypes.c_int64), ("new_rows", ctypes.c_int64)]
+
+
 class DecodePtrs(ctypes.Structure):
     _fields_ = [("q", ctypes.c_void_p), ("k_prefix", ctypes.c_void_p),
                 ("v_prefix", ctypes.c_void_p), ("k_suffix", ctypes.c_void_p),
@@ -72,7 +78,8 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_token_logprob", "rl_status_string", "rl_last_error", "rl_abi_version",
            "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
-           "rl_sample_top_p_workspace_size", "rl_sample_top_p"]
+           "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
+           "rl_kv_append"]
 
 
 def _load():
@@ -109,7 +116,11 @@ def _load():
     lib.rl_sample_top_p_workspace_size.argtypes = [I64, I32, I32, ctypes.POINTER(SZ)]
     lib.rl_sample_top_p.restype = ctypes.c_int
     lib.rl_sample_top_p.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, P, SZ, P]
-    if lib.rl_abi_version() != 5:
+    lib.rl_kv_append_workspace_size.restype = ctypes.c_int
+    lib.rl_kv_append_workspace_size.argtypes = [P, P, ctypes.POINTER(SZ)]
+    lib.rl_kv_append.restype = ctypes.c_int
+    lib.rl_kv_append.argtypes = [P, P, P, P, P, P, P, SZ, P]
+    if lib.rl_abi_version() != 6:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -212,6 +223,62 @@ def decode_plan(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix
                    ("chunk", np.int32), ("tok_begin", np.int64), ("tok_count", np.int32),
                    ("row_begin", np.int32), ("row_count", np.int32), ("reserved", np.int32)])
     return np.frombuffer(bytes(buf), dtype=dt, count=n.value).copy()
+
+
+class _AppendArgs:
+    """Host-side marshalling of rl_kv_append's shape and lengths (keeps the arrays alive)."""
+
+    def __init__(self, P, G, Hkv, D, suffix_start, suffix_len, new_start, new_len, suffix_rows, new_rows,
+                 suffix_capacity=None, kv_layout: str = "token"):
+        self.ss = np.ascontiguousarray(suffix_start, dtype=np.int64)
+        self.sl = np.ascontiguousarray(suffix_len, dtype=np.int32)
+        self.ns = np.ascontiguousarray(new_start, dtype=np.int64)
+        self.nl = np.ascontiguousarray(new_len, dtype=np.int32)
+        self.cap = None if suffix_capacity is None else np.ascontiguousarray(suffix_capacity, dtype=np.int32)
+        S = P * G
+        for arr, n in ((self.ss, "suffix_start"), (self.sl, "suffix_len"), (self.ns, "new_start"),
+                       (self.nl, "new_len")) + (((self.cap, "suffix_capacity"),) if self.cap is not None else ()):
+            if arr.shape != (S,):
+                raise ValueError(f"{n} must have P*G = {S} entries")
+        if kv_layout not in KV_LAYOUTS:
+            raise ValueError(f"kv_layout must be one of {sorted(KV_LAYOUTS)}")
+        self.shape = DecodeShape(P, G, 1, Hkv, D, 1.0, 0, KV_LAYOUTS[kv_layout])
+        self.lens = KvAppendLens(self.ss.ctypes.data, self.sl.ctypes.data,
+                                 None if self.cap is None else self.cap.ctypes.data,
+                                 self.ns.ctypes.data, self.nl.ctypes.data, int(suffix_rows), int(new_rows))
+
+
+def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_suffix: torch.Tensor, v_suffix: torch.Tensor,
+              suffix_start, suffix_len, new_start, new_len, group_size: int, suffix_capacity=None,
+              kv_layout: str = "token", workspace: Optional[torch.Tensor] = None, stream=None):
+    """Writes rows new_start[s] + i of k_new / v_new ([new_rows, Hkv, D]) to suffix rows
+    suffix_start[s] + suffix_len[s] + i of the caches, for i < new_len[s]."""
+    for t, n in ((k_new, "k_new"), (v_new, "v_new"), (k_suffix, "k_suffix"), (v_suffix, "v_suffix")):
+        _bf16_dev(t, n)
+    if k_new.dim() != 3 or v_new.shape != k_new.shape:
+        raise ValueError("k_new / v_new must be [new_rows, Hkv, D]")
+    new_rows, Hkv, D = k_new.shape
+    if k_suffix.shape != v_suffix.shape or k_suffix.dim() != 3:
+        raise ValueError("k_suffix / v_suffix must have the same 3-d shape")
+    rdim = 1 if kv_layout == "head" else 0
+    hdim = 0 if kv_layout == "head" else 1
+    if k_suffix.shape[hdim] != Hkv or k_suffix.shape[2] != D:
+        raise ValueError("suffix caches do not match k_new's heads / head_dim")
+    G = int(group_size)
+    S = len(np.asarray(suffix_start))
+    if G <= 0 or S % G:
+        raise ValueError("the number of candidates must be a multiple of group_size")
+    a = _AppendArgs(S // G, G, Hkv, D, suffix_start, suffix_len, new_start, new_len, k_suffix.shape[rdim],
+                    new_rows, suffix_capacity, kv_layout)
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_kv_append_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(n)),
+           "rl_kv_append_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(max(n.value, 1), dtype=torch.uint8, device=k_new.device)
+    _on_device(workspace, "workspace")
+    _check(_lib.rl_kv_append(ctypes.byref(a.shape), ctypes.byref(a.lens), _ptr(k_new), _ptr(v_new),
+                             _ptr(k_suffix), _ptr(v_suffix), ctypes.c_void_p(workspace.data_ptr()),
+                             workspace.numel(), _stream_handle(stream)), "rl_kv_append")
 
 
 def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,

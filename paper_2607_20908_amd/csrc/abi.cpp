@@ -48,7 +48,16 @@ thread_local int g_staging_next;
 // its vectors have grown to the problem size.
 thread_local rlk::DecodePlan g_plan;
 
-rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t stream) {
+struct Section {
+    size_t off;
+    const void *src;
+    size_t n;
+};
+
+// Copies the sections (each followed by zeros up to the next section's
+// offset, the last up to `total`) into the next staging slot and enqueues
+// the fetch of `total` bytes (a multiple of 16) into `dst` on `stream`.
+rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, hipStream_t stream) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_error(e, "hipGetDevice");
@@ -70,11 +79,11 @@ rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t strea
         if (e != hipSuccess) return hip_error(e, "creating a staging event");
         slot.device = device;
     }
-    if (slot.cap < plan.meta_bytes) {
+    if (slot.cap < total) {
         if (slot.host) (void)hipHostFree(slot.host);
         slot.host = nullptr;
         slot.cap = 0;
-        const size_t cap = std::max<size_t>(plan.meta_bytes * 2, 1 << 16);
+        const size_t cap = std::max<size_t>(total * 2, 1 << 16);
         e = hipHostMalloc(reinterpret_cast<void **>(&slot.host), cap,
                           hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) return hip_error(e, "allocating pinned staging memory");
@@ -82,23 +91,26 @@ rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t strea
         if (e != hipSuccess) return hip_error(e, "mapping pinned staging memory");
         slot.cap = cap;
     }
-    // the three sections, each followed by zeros up to the next section
-    auto put = [&](size_t off, const void *src, size_t n, size_t end) {
-        std::memcpy(slot.host + off, src, n);
-        std::memset(slot.host + off + n, 0, end - off - n);
-    };
-    put(plan.off_items, plan.dev_items.data(), plan.dev_items.size() * sizeof(rlk::DevItem),
-        plan.off_prefix_units);
-    put(plan.off_prefix_units, plan.prefix_units.data(),
-        plan.prefix_units.size() * sizeof(rlk::DevUnit), plan.off_suffix_units);
-    put(plan.off_suffix_units, plan.suffix_units.data(),
-        plan.suffix_units.size() * sizeof(rlk::DevUnit), plan.meta_bytes);
-    e = rlk::launch_plan_fetch(slot.dev, dst, plan.meta_bytes, stream);
+    for (int i = 0; i < nsec; ++i) {
+        const size_t end = i + 1 < nsec ? sec[i + 1].off : total;
+        if (sec[i].n) std::memcpy(slot.host + sec[i].off, sec[i].src, sec[i].n);
+        std::memset(slot.host + sec[i].off + sec[i].n, 0, end - sec[i].off - sec[i].n);
+    }
+    e = rlk::launch_plan_fetch(slot.dev, dst, total, stream);
     if (e != hipSuccess) return hip_error(e, "uploading the work list");
     e = hipEventRecord(slot.done, stream);
     if (e != hipSuccess) return hip_error(e, "recording the staging event");
     slot.pending = true;
     return RL_OK;
+}
+
+// The decode work list: items, then the prefix and suffix unit tables.
+rl_status stage_upload(const rlk::DecodePlan &plan, void *dst, hipStream_t stream) {
+    const Section sec[3] = {
+        {plan.off_items, plan.dev_items.data(), plan.dev_items.size() * sizeof(rlk::DevItem)},
+        {plan.off_prefix_units, plan.prefix_units.data(), plan.prefix_units.size() * sizeof(rlk::DevUnit)},
+        {plan.off_suffix_units, plan.suffix_units.data(), plan.suffix_units.size() * sizeof(rlk::DevUnit)}};
+    return stage_sections(sec, 3, plan.meta_bytes, dst, stream);
 }
 
 }  // namespace
@@ -251,6 +263,109 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
 }
 
 static bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+namespace {
+// Validates an append and builds its (source, destination) row pairs.
+thread_local std::vector<int64_t> g_append_rows;
+thread_local std::vector<std::pair<int64_t, int64_t>> g_append_ranges;
+
+rl_status plan_append(const rl_decode_shape *shape, const rl_kv_append_lens *lens, bool build, int64_t *n_new) {
+    if (!shape || !lens) return set_error(RL_ERR_NULL_POINTER, "shape and lens must not be NULL");
+    const int64_t P = shape->num_prompts, G = shape->group_size;
+    if (P < 0 || G < 1) return set_error(RL_ERR_INVALID_SHAPE, "num_prompts >= 0 and group_size >= 1 required");
+    if (shape->num_kv_heads < 1) return set_error(RL_ERR_INVALID_SHAPE, "num_kv_heads must be >= 1");
+    if (shape->head_dim != 64 && shape->head_dim != 128) return set_error(RL_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (shape->kv_layout != RL_KV_TOKEN_MAJOR && shape->kv_layout != RL_KV_HEAD_MAJOR)
+        return set_error(RL_ERR_INVALID_SHAPE, "kv_layout must be RL_KV_TOKEN_MAJOR or RL_KV_HEAD_MAJOR");
+    const int64_t S = P * G;
+    if (S > 0 && (!lens->suffix_start || !lens->suffix_len || !lens->new_start || !lens->new_len))
+        return set_error(RL_ERR_NULL_POINTER, "suffix_start, suffix_len, new_start and new_len must not be NULL");
+    if (lens->suffix_rows < 0 || lens->new_rows < 0) return set_error(RL_ERR_INVALID_SHAPE, "negative row counts");
+    int64_t total = 0;
+    g_append_ranges.clear();
+    for (int64_t s = 0; s < S; ++s) {
+        const int64_t st = lens->suffix_start[s], len = lens->suffix_len[s];
+        const int64_t ns = lens->new_start[s], nl = lens->new_len[s];
+        if (st < 0 || len < 0 || ns < 0 || nl < 0)
+            return set_error(RL_ERR_INVALID_SHAPE, "negative start or length at candidate " + std::to_string(s));
+        if (nl == 0) continue;
+        const int64_t end = st + len + nl;
+        if (end > lens->suffix_rows)
+            return set_error(RL_ERR_INVALID_SHAPE, "candidate " + std::to_string(s) + " writes past suffix_rows");
+        if (lens->suffix_capacity && len + nl > lens->suffix_capacity[s])
+            return set_error(RL_ERR_INVALID_SHAPE, "candidate " + std::to_string(s) + " exceeds its capacity");
+        if (ns + nl > lens->new_rows)
+            return set_error(RL_ERR_INVALID_SHAPE, "candidate " + std::to_string(s) + " reads past new_rows");
+        g_append_ranges.emplace_back(st + len, end);
+        total += nl;
+    }
+    std::sort(g_append_ranges.begin(), g_append_ranges.end());
+    for (size_t i = 1; i < g_append_ranges.size(); ++i)
+        if (g_append_ranges[i].first < g_append_ranges[i - 1].second)
+            return set_error(RL_ERR_INVALID_SHAPE, "two candidates write the same suffix rows");
+    *n_new = total;
+    if (build) {
+        g_append_rows.resize(static_cast<size_t>(2 * total));
+        int64_t t = 0;
+        for (int64_t s = 0; s < S; ++s) {
+            const int64_t nl = lens->new_len[s];
+            const int64_t dst0 = lens->suffix_start[s] + lens->suffix_len[s];
+            for (int64_t i = 0; i < nl; ++i, ++t) {
+                g_append_rows[2 * t] = lens->new_start[s] + i;
+                g_append_rows[2 * t + 1] = dst0 + i;
+            }
+        }
+    }
+    return RL_OK;
+}
+}  // namespace
+
+rl_status rl_kv_append_workspace_size(const rl_decode_shape *shape, const rl_kv_append_lens *lens, size_t *bytes) {
+    g_last_error.clear();
+    if (!bytes) return set_error(RL_ERR_NULL_POINTER, "bytes is NULL");
+    int64_t n = 0;
+    const rl_status st = plan_append(shape, lens, false, &n);
+    if (st != RL_OK) return st;
+    *bytes = rlk::align_up(static_cast<size_t>(n) * 16, 256);
+    return RL_OK;
+}
+
+rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *lens, const void *k_new,
+                       const void *v_new, void *k_suffix, void *v_suffix, void *workspace, size_t workspace_bytes,
+                       void *stream) {
+    g_last_error.clear();
+    int64_t n = 0;
+    rl_status st = plan_append(shape, lens, true, &n);
+    if (st != RL_OK) return st;
+    if (n == 0) return RL_OK;
+    if (!k_new || !v_new || !k_suffix || !v_suffix)
+        return set_error(RL_ERR_NULL_POINTER, "k_new, v_new, k_suffix and v_suffix must not be NULL");
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_suffix) || !aligned16(v_suffix))
+        return set_error(RL_ERR_MISALIGNED, "the KV tensors must be 16-byte aligned");
+    const size_t need = rlk::align_up(static_cast<size_t>(n) * 16, 256);
+    if (!workspace || workspace_bytes < need)
+        return set_error(RL_ERR_WORKSPACE,
+                         "workspace needs " + std::to_string(need) + " bytes, got " + std::to_string(workspace_bytes));
+    if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    const Section sec[1] = {{0, g_append_rows.data(), static_cast<size_t>(n) * 16}};
+    st = stage_sections(sec, 1, need, workspace, hs);
+    if (st != RL_OK) return st;
+    rlk::KvAppendArgs a{};
+    a.k_new = static_cast<const uint16_t *>(k_new);
+    a.v_new = static_cast<const uint16_t *>(v_new);
+    a.k_suffix = static_cast<uint16_t *>(k_suffix);
+    a.v_suffix = static_cast<uint16_t *>(v_suffix);
+    a.rows = static_cast<const int64_t *>(workspace);
+    a.n_new = n;
+    a.suffix_rows = lens->suffix_rows;
+    a.Hkv = shape->num_kv_heads;
+    a.D = shape->head_dim;
+    a.kv_layout = shape->kv_layout;
+    const hipError_t e = rlk::launch_kv_append(a, hs);
+    if (e != hipSuccess) return hip_error(e, "launching the KV append");
+    return RL_OK;
+}
 
 rl_status rl_token_logprob_backward_workspace_size(int64_t rows, int32_t hidden, int32_t vocab, size_t *bytes) {
     g_last_error.clear();

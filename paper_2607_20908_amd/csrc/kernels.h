@@ -31,6 +31,20 @@ hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
 // workspace without a hand-off between the copy engine and the compute queue.
 hipError_t launch_plan_fetch(const void *host_src, void *dst, size_t bytes, hipStream_t stream);
 
+// Appends new tokens to the suffix caches: rows[2t] is token t's row in
+// k_new / v_new ([rows, Hkv, D]), rows[2t + 1] its destination suffix row.
+struct KvAppendArgs {
+    const uint16_t *k_new, *v_new;
+    uint16_t *k_suffix, *v_suffix;
+    const int64_t *rows;        // workspace: (source, destination) per new token
+    int64_t n_new;
+    int64_t suffix_rows;
+    int32_t Hkv, D;
+    int32_t kv_layout;
+};
+
+hipError_t launch_kv_append(const KvAppendArgs &a, hipStream_t stream);
+
 struct LogprobArgs {
     const uint16_t *hidden;     // [R, H]
     const uint16_t *w;          // [V, H]

@@ -673,6 +673,24 @@ def pin_sampling_intervals(orc):
         assert np.all((lo[tok] <= u) & (u < hi[tok])), "sample outside its interval"
 
 
+# ------------------------------------------------------------ KV append
+def pin_kv_append_hand(orc=None):
+    """A1: two candidates, one kv head, D = 2, caches of 8 rows holding -1.
+    Candidate 0 (region from row 0, 2 tokens there) appends new rows 1 and 2;
+    candidate 1 (region from row 4, 1 token) appends new row 0: rows 2, 3 and
+    5 change, nothing else.  In the head-major cache the same rows change."""
+    import oracle as _o
+    new = np.array([[[10, 11]], [[20, 21]], [[30, 31]]], np.int64)      # [3, 1, 2]
+    cache = -np.ones((8, 1, 2), np.int64)
+    k, v = _o.kv_append(cache, cache, new, new + 100, [0, 4], [2, 1], [1, 0], [2, 1])
+    want = cache.copy()
+    want[2], want[3], want[5] = new[1], new[2], new[0]
+    assert np.array_equal(k, want) and np.array_equal(v, np.where(want == -1, -1, want + 100))
+    kh, _ = _o.kv_append(cache.transpose(1, 0, 2).copy(), cache.transpose(1, 0, 2).copy(), new, new,
+                         [0, 4], [2, 1], [1, 0], [2, 1], kv_layout="head")
+    assert np.array_equal(kh, want.transpose(1, 0, 2))
+
+
 def pin_sampling_golden(orc):
     """Hand-worked cases (tests/golden/sampling_hand.json)."""
     with open(os.path.join(GOLDEN, "sampling_hand.json")) as f:
@@ -696,4 +714,5 @@ BACKWARD_PINS = [pin_backward_vs_torch, pin_backward_finite_differences, pin_bac
 SAMPLING_PINS = [pin_sampling_full_distribution, pin_sampling_greedy_limit, pin_sampling_frequencies,
                  pin_sampling_ties, pin_sampling_temperature_scale, pin_sampling_logprob, pin_sampling_intervals,
                  pin_sampling_golden]
-ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS + SAMPLING_PINS
+APPEND_PINS = [pin_kv_append_hand]
+ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS + SAMPLING_PINS + APPEND_PINS

@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 5
+    assert lib.rl_abi_version() == 6
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -385,3 +385,47 @@ def test_sample_workspace_size():
     assert n >= 512 * ld * 4 + tiles * 512 * 4 and n < 512 * ld * 4 + tiles * 512 * 4 + 512
     assert rk.sample_top_p_workspace_size(100000, 4096, V) == rk.sample_top_p_workspace_size(8192, 4096, V)
     assert rk.sample_top_p_workspace_size(0, 64, 10) == 0
+
+
+# -------------------------------------------------------------- KV append
+def append_call(S=4, G=2, Hkv=2, D=128, ss=None, sl=None, cap=None, ns=None, nl=None, suffix_rows=64,
+                new_rows=8, layout=0, ptrs=True, ws=FAKE, ws_bytes=1 << 20):
+    lib = rk.lib()
+    ss = np.arange(S, dtype=np.int64) * 16 if ss is None else np.asarray(ss, np.int64)
+    sl = np.full(S, 3, np.int32) if sl is None else np.asarray(sl, np.int32)
+    ns = np.arange(S, dtype=np.int64) * 2 if ns is None else np.asarray(ns, np.int64)
+    nl = np.full(S, 2, np.int32) if nl is None else np.asarray(nl, np.int32)
+    capa = None if cap is None else np.asarray(cap, np.int32)
+    shape = rk.DecodeShape(S // G, G, 1, Hkv, D, 1.0, 0, layout)
+    lens = rk.KvAppendLens(ss.ctypes.data, sl.ctypes.data, None if capa is None else capa.ctypes.data,
+                           ns.ctypes.data, nl.ctypes.data, suffix_rows, new_rows)
+    p = [FAKE, FAKE + 4096, FAKE + 8192, FAKE + 12288] if ptrs is True else ptrs
+    st = lib.rl_kv_append(ctypes.byref(shape), ctypes.byref(lens), *p, ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(ptrs=[None, FAKE, FAKE, FAKE]), NULLP),
+    (dict(ptrs=[FAKE, FAKE, FAKE, None]), NULLP),
+    (dict(sl=[3, -1, 3, 3]), SHAPE),
+    (dict(nl=[2, 2, -2, 2]), SHAPE),
+    (dict(ss=[0, 16, 32, 62]), SHAPE),                 # 62 + 3 + 2 > 64 rows
+    (dict(cap=[8, 8, 4, 8]), SHAPE),                   # 3 + 2 > 4
+    (dict(ns=[0, 2, 4, 7]), SHAPE),                    # 7 + 2 > 8 new rows
+    (dict(ss=[0, 1, 32, 48], sl=[3, 3, 3, 3]), SHAPE), # rows 3-4 and 4-5 overlap
+    (dict(D=96), UNSUP),
+    (dict(layout=2), SHAPE),
+    (dict(ptrs=[FAKE + 8, FAKE, FAKE, FAKE]), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws_bytes=16), WSPACE),
+    (dict(ws=FAKE + 4), MISAL),
+])
+def test_kv_append_validation(kw, expect):
+    st, msg = append_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg
+
+
+def test_kv_append_nothing_to_do():
+    st, msg = append_call(nl=[0, 0, 0, 0], ptrs=[None, None, None, None], ws=None, ws_bytes=0)
+    assert st == OK and msg == ""
