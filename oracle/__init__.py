@@ -7,7 +7,9 @@ patterns) and returns float64 results.
 
 The definitions it computes are stated at the top of oracle.c: grouped-query
 decode attention over a shared prompt prefix followed by each candidate's own
-suffix (Sec. 2.2.1, Problem Setup), the full-vocabulary token log-prob of
+suffix (Sec. 2.2.1, Problem Setup) and the causal extend (prefill) of a
+refinement turn's new tokens over that context (Sec. 3, Structured Feedback
+and Iterative Refinement), the full-vocabulary token log-prob of
 the sampled token that the GRPO ratio needs (Sec. 3, Eq. grpo-loss; masked
 positions per Sec. 3, Multi-turn RL Training), the group-relative advantages
 and the clipped surrogate of Eq. grpo-loss with its gradient, and the
@@ -68,6 +70,8 @@ def _bind(path: str):
     lib.oracle_token_logprob_backward.restype = ctypes.c_int
     lib.oracle_token_logprob_backward.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                                   P, P, P, ctypes.c_float, P, P]
+    lib.oracle_extend_attn.restype = ctypes.c_int
+    lib.oracle_extend_attn.argtypes = [ctypes.c_int32] * 5 + [ctypes.c_float] + [P] * 13
     return lib
 
 
@@ -137,6 +141,60 @@ def decode_attn(q, k_prefix, v_prefix, k_suffix, v_suffix,
         _ptr(q), _ptr(kp), _ptr(vp), _ptr(ks), _ptr(vs), _ptr(out), _ptr(lse))
     if rc:
         raise MemoryError("oracle_decode_attn scratch allocation failed")
+    return out, lse
+
+
+def extend_attn(q, k_prefix, v_prefix, k_suffix, v_suffix,
+                prefix_start, prefix_len, suffix_start, suffix_len, new_len, q_start,
+                group_size: int, scale: float, _lib=None):
+    """Oracle extend (prefill) attention of a refinement turn.
+
+    The last new_len[s] tokens of candidate s's suffix are new; new token i
+    attends causally to the prompt's prefix and the candidate's suffix up to
+    and including itself.  q: uint16 [Q, Hq, D], its query rows q_start[s] + i;
+    k/v_prefix, k/v_suffix as in decode_attn (token-major).
+    Returns (out float64 [Q, Hq, D], lse float64 [Q, Hq]); rows of no
+    candidate stay 0.
+    """
+    q = _u16(q)
+    Q, Hq, D = q.shape
+    G = int(group_size)
+    S = len(suffix_len)
+    if G <= 0 or S % G:
+        raise ValueError("the number of candidates must be a positive multiple of group_size")
+    P = S // G
+    kp, vp, ks, vs = (_u16(t) for t in (k_prefix, v_prefix, k_suffix, v_suffix))
+    Hkv = kp.shape[1]
+    if Hq % Hkv or any(t.shape[1:] != (Hkv, D) for t in (kp, vp, ks, vs)):
+        raise ValueError("bad head layout")
+    ps = np.ascontiguousarray(prefix_start, dtype=np.int64)
+    pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
+    ss = np.ascontiguousarray(suffix_start, dtype=np.int64)
+    sl = np.ascontiguousarray(suffix_len, dtype=np.int32)
+    nl = np.ascontiguousarray(new_len, dtype=np.int32)
+    qs = np.ascontiguousarray(q_start, dtype=np.int64)
+    if ps.shape != (P,) or pl.shape != (P,) or any(a.shape != (S,) for a in (ss, sl, nl, qs)):
+        raise ValueError("length arrays")
+    if (pl < 0).any() or (sl < 0).any() or (nl < 0).any() or (nl > sl).any():
+        raise ValueError("lengths: need 0 <= new_len <= suffix_len")
+    if P and ((ps < 0).any() or (ps + pl > kp.shape[0]).any() or kp.shape != vp.shape):
+        raise ValueError("prefix range")
+    if S and ((ss < 0).any() or (ss + sl > ks.shape[0]).any() or ks.shape != vs.shape):
+        raise ValueError("suffix range")
+    if S and ((qs < 0).any() or (qs + nl > Q).any()):
+        raise ValueError("query range")
+    out = np.zeros((Q, Hq, D), dtype=np.float64)
+    lse = np.zeros((Q, Hq), dtype=np.float64)
+    if S == 0:
+        return out, lse
+    rc = (_lib or _load()).oracle_extend_attn(
+        P, G, Hq, Hkv, D, float(np.float32(scale)),
+        _ptr(ps), _ptr(pl), _ptr(ss), _ptr(sl), _ptr(nl), _ptr(qs),
+        _ptr(q), _ptr(kp), _ptr(vp), _ptr(ks), _ptr(vs), _ptr(out), _ptr(lse))
+    if rc == 1:
+        raise MemoryError("oracle_extend_attn scratch allocation failed")
+    if rc:
+        raise ValueError("oracle_extend_attn: new_len exceeds suffix_len")
     return out, lse
 
 
@@ -348,6 +406,9 @@ class Oracle:
 
     def decode_attn(self, *args, **kw):
         return decode_attn(*args, **kw, _lib=self._lib)
+
+    def extend_attn(self, *args, **kw):
+        return extend_attn(*args, **kw, _lib=self._lib)
 
     def token_logprob(self, *args, **kw):
         return token_logprob(*args, **kw, _lib=self._lib)

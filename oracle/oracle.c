@@ -68,6 +68,18 @@
  *     mass such a change could move (last member plus next token, over the
  *     nucleus mass; infinite when the sample is one of them).
  *
+ *  7. Extend (prefill) attention of a refinement turn (Sec. 3, Structured
+ *     Feedback and Iterative Refinement: each turn appends feedback and a
+ *     summary to the candidate's context, and the policy reads the whole
+ *     context before it generates).  Candidate s = p*G + g has the context
+ *     prefix(p) followed by suffix(s), Lp + Ls tokens, whose last n_s <= Ls
+ *     suffix tokens are new.  New token i (0 <= i < n_s) is at position
+ *     c_i = Lp + Ls - n_s + i of that sequence and attends causally: to
+ *     positions 0..c_i, itself included.  With that visible set in place of
+ *     the whole context, out and lse are those of definition 1.  Its query
+ *     and output rows are q_start[s] + i of a packed [rows, Hq, D] array.
+ *     With n_s = 1 this is definition 1 exactly.
+ *
  * Inputs are raw bf16 bit patterns (uint16).  Each is widened exactly:
  * bits << 16 is the float32 pattern, and float32 -> double is exact.
  */
@@ -84,7 +96,7 @@ static double bf16_to_f64(uint16_t b)
     return (double)f;
 }
 
-int oracle_abi_version(void) { return 3; }
+int oracle_abi_version(void) { return 4; }
 
 /* Returns 0 on success, 1 if a scratch allocation failed. */
 int oracle_decode_attn(int32_t P, int32_t G, int32_t Hq, int32_t Hkv, int32_t D,
@@ -484,6 +496,74 @@ int oracle_top_p_interval(int64_t R, int32_t H, int32_t V,
         free(h);
         free(rk);
         free(in_n);
+    }
+    return failed;
+}
+
+/* Definition 7.  Returns 0 on success, 1 if a scratch allocation failed, 2
+ * if some n_s exceeds Ls. */
+int oracle_extend_attn(int32_t P, int32_t G, int32_t Hq, int32_t Hkv, int32_t D,
+                       float scale,
+                       const int64_t *prefix_start, const int32_t *prefix_len,
+                       const int64_t *suffix_start, const int32_t *suffix_len,
+                       const int32_t *new_len, const int64_t *q_start,
+                       const uint16_t *q,
+                       const uint16_t *k_prefix, const uint16_t *v_prefix,
+                       const uint16_t *k_suffix, const uint16_t *v_suffix,
+                       double *out, double *lse)
+{
+    const int64_t n_cand = (int64_t)P * G;
+    const int32_t heads_per_kv = Hq / Hkv;
+    int failed = 0;
+
+    for (int64_t c = 0; c < n_cand; ++c)
+        if (new_len[c] < 0 || new_len[c] > suffix_len[c]) return 2;
+
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t c = 0; c < n_cand; ++c) {
+        for (int32_t head = 0; head < Hq; ++head) {
+            const int64_t prompt = c / G;
+            const int32_t kv_head = head / heads_per_kv;
+            const int64_t n_pre = prefix_len[prompt];
+            const int64_t n_suf = suffix_len[c];
+            const int64_t n_new = new_len[c];
+            double *score = (double *)malloc((size_t)(n_pre + n_suf + 1) * sizeof(double));
+            if (!score) {
+#pragma omp atomic write
+                failed = 1;
+                continue;
+            }
+            for (int64_t i = 0; i < n_new; ++i) {
+                const int64_t qrow = q_start[c] + i;
+                const uint16_t *qi = q + (qrow * Hq + head) * (int64_t)D;
+                double *oi = out + (qrow * Hq + head) * (int64_t)D;
+                /* new token i sits at position n_pre + n_suf - n_new + i of
+                 * prefix ++ suffix and sees positions 0 .. itself */
+                const int64_t visible = n_pre + (n_suf - n_new + i) + 1;
+                for (int64_t j = 0; j < visible; ++j) {
+                    const uint16_t *kj = (j < n_pre)
+                        ? k_prefix + ((prefix_start[prompt] + j) * Hkv + kv_head) * (int64_t)D
+                        : k_suffix + ((suffix_start[c] + (j - n_pre)) * Hkv + kv_head) * (int64_t)D;
+                    double qk = 0.0;
+                    for (int32_t d = 0; d < D; ++d) qk += bf16_to_f64(qi[d]) * bf16_to_f64(kj[d]);
+                    score[j] = (double)scale * qk;
+                }
+                double mx = score[0];
+                for (int64_t j = 1; j < visible; ++j) if (score[j] > mx) mx = score[j];
+                double zsum = 0.0;
+                for (int64_t j = 0; j < visible; ++j) zsum += exp(score[j] - mx);
+                for (int32_t d = 0; d < D; ++d) oi[d] = 0.0;
+                for (int64_t j = 0; j < visible; ++j) {
+                    const uint16_t *vj = (j < n_pre)
+                        ? v_prefix + ((prefix_start[prompt] + j) * Hkv + kv_head) * (int64_t)D
+                        : v_suffix + ((suffix_start[c] + (j - n_pre)) * Hkv + kv_head) * (int64_t)D;
+                    const double wj = exp(score[j] - mx) / zsum;
+                    for (int32_t d = 0; d < D; ++d) oi[d] += wj * bf16_to_f64(vj[d]);
+                }
+                lse[qrow * Hq + head] = mx + log(zsum);
+            }
+            free(score);
+        }
     }
     return failed;
 }

@@ -716,3 +716,166 @@ SAMPLING_PINS = [pin_sampling_full_distribution, pin_sampling_greedy_limit, pin_
                  pin_sampling_golden]
 APPEND_PINS = [pin_kv_append_hand]
 ALL_PINS = ATTENTION_PINS + LOGPROB_PINS + GRPO_PINS + BACKWARD_PINS + SAMPLING_PINS + APPEND_PINS
+
+
+# --------------------------------------------------------------- extend pins
+def extend_case(P=2, G=2, Hq=4, Hkv=2, D=8, lp=None, ls=None, nl=None, seed=0, qmul=1.0):
+    """Small random extend input: decode_case's caches plus the new-token counts
+    and a packed query array whose candidates come in reverse order, with gaps."""
+    c = decode_case(P=P, G=G, Hq=Hq, Hkv=Hkv, D=D, lp=lp, ls=ls, seed=seed, qmul=qmul)
+    rng = np.random.Generator(np.random.PCG64(seed + 1000))
+    S = P * G
+    ls_ = c["suffix_len"]
+    nl = np.asarray([int(rng.integers(0, l + 1)) for l in ls_] if nl is None else nl, np.int32)
+    qs = np.zeros(S, np.int64)
+    pos = 1
+    for s in reversed(range(S)):
+        qs[s] = pos
+        pos += int(nl[s]) + 1
+    q = bf16_bits_of(rng.standard_normal((pos + 1, Hq, D)) * qmul)
+    c.update(q=q, new_len=nl, q_start=qs)
+    return c
+
+
+def torch_extend(c):
+    """Reference via torch's fp64 SDPA with a lower-triangular boolean mask over
+    each candidate's concatenated sequence, keeping the rows of its last n tokens."""
+    q = f64(c["q"]); kp = f64(c["k_prefix"]); vp = f64(c["v_prefix"])
+    ks = f64(c["k_suffix"]); vs = f64(c["v_suffix"])
+    Q, Hq, D = q.shape
+    Hkv = kp.shape[1]
+    G = c["group_size"]
+    sigma = float(np.float32(c["scale"]))
+    out = torch.zeros(Q, Hq, D, dtype=torch.float64)
+    lse = torch.zeros(Q, Hq, dtype=torch.float64)
+    for s in range(len(c["suffix_len"])):
+        n = int(c["new_len"][s])
+        if n == 0:
+            continue
+        p = s // G
+        a, lp = int(c["prefix_start"][p]), int(c["prefix_len"][p])
+        b, ls = int(c["suffix_start"][s]), int(c["suffix_len"][s])
+        K = torch.cat([kp[a:a + lp], ks[b:b + ls]])          # [T, Hkv, D]
+        V = torch.cat([vp[a:a + lp], vs[b:b + ls]])
+        T = K.shape[0]
+        mask = torch.ones(T, T, dtype=torch.bool).tril()[T - n:]   # [n, T]
+        qs = int(c["q_start"][s])
+        Qs = q[qs:qs + n].permute(1, 0, 2)[None]              # [1, Hq, n, D]
+        o = F.scaled_dot_product_attention(Qs, K.permute(1, 0, 2)[None], V.permute(1, 0, 2)[None],
+                                           attn_mask=mask, scale=sigma, enable_gqa=True)
+        out[qs:qs + n] = o[0].permute(1, 0, 2)
+        Krep = K.repeat_interleave(Hq // Hkv, dim=1).permute(1, 0, 2)   # [Hq, T, D]
+        scores = sigma * (Qs[0] @ Krep.transpose(1, 2))                  # [Hq, n, T]
+        scores = scores.masked_fill(~mask, -math.inf)
+        lse[qs:qs + n] = torch.logsumexp(scores, dim=2).T
+    return out.numpy(), lse.numpy()
+
+
+def _extend_args(c):
+    return {k: c[k] for k in ("q", "k_prefix", "v_prefix", "k_suffix", "v_suffix", "prefix_start",
+                              "prefix_len", "suffix_start", "suffix_len", "new_len", "q_start",
+                              "group_size", "scale")}
+
+
+def pin_extend_vs_torch(orc):
+    """E1: brute force by torch's masked SDPA over the concatenated sequence."""
+    cases = [
+        dict(P=2, G=3, Hq=4, Hkv=2, D=8, seed=21),
+        dict(P=1, G=4, Hq=6, Hkv=3, D=16, lp=[9], ls=[7, 3, 5, 1], nl=[7, 1, 2, 0], seed=22),  # n = Ls, n = 0
+        dict(P=2, G=2, Hq=2, Hkv=2, D=8, lp=[0, 4], ls=[5, 3, 6, 2], nl=[5, 2, 1, 2], seed=23),  # no prefix
+        dict(P=2, G=2, Hq=8, Hkv=1, D=8, lp=[3, 6], ls=[4, 4, 5, 2], nl=[4, 3, 5, 1], seed=24, qmul=4.0),
+    ]
+    for cs in cases:
+        c = extend_case(**cs)
+        o, l = orc.extend_attn(**_extend_args(c))
+        ro, rl = torch_extend(c)
+        close(o, ro, 1e-12, f"extend out {cs}")
+        close(l, rl, 1e-12, f"extend lse {cs}")
+
+
+def pin_extend_decode_steps(orc):
+    """E2: new token i equals a decode step whose suffix ends at that token (a
+    decode loop that appends one token per step), through the pinned decode
+    definition; a single new token is exactly one decode step."""
+    c = extend_case(P=2, G=2, Hq=4, Hkv=2, D=8, lp=[5, 2], ls=[6, 4, 3, 5], nl=[6, 1, 3, 2], seed=25)
+    o, l = orc.extend_attn(**_extend_args(c))
+    S = 4
+    Hq, D = c["q"].shape[1:]
+    for i in range(int(c["new_len"].max())):
+        qd = np.zeros((S, Hq, D), np.uint16)
+        sl = c["suffix_len"].copy()
+        live = [s for s in range(S) if i < c["new_len"][s]]
+        for s in live:
+            qd[s] = c["q"][c["q_start"][s] + i]
+            sl[s] = c["suffix_len"][s] - c["new_len"][s] + i + 1
+        od, ld = orc.decode_attn(qd, c["k_prefix"], c["v_prefix"], c["k_suffix"], c["v_suffix"],
+                                 c["prefix_start"], c["prefix_len"], c["suffix_start"], sl,
+                                 c["group_size"], c["scale"])
+        for s in live:
+            row = c["q_start"][s] + i
+            close(o[row], od[s], 1e-13, f"extend step {i} out s={s}")
+            close(l[row], ld[s], 1e-13, f"extend step {i} lse s={s}")
+
+
+def pin_extend_future_independence(orc):
+    """E3: a new token's result does not depend on the tokens after it, and
+    does depend on the ones up to it (causality both ways)."""
+    c = extend_case(P=1, G=2, Hq=2, Hkv=1, D=8, lp=[3], ls=[6, 5], nl=[5, 4], seed=26)
+    o, l = orc.extend_attn(**_extend_args(c))
+    for s, cut in ((0, 2), (1, 1)):            # perturb suffix positions after new token `cut`
+        ks, vs = c["k_suffix"].copy(), c["v_suffix"].copy()
+        b, ls, n = int(c["suffix_start"][s]), int(c["suffix_len"][s]), int(c["new_len"][s])
+        first = b + ls - n + cut + 1
+        rng = np.random.Generator(np.random.PCG64(s))
+        ks[first:b + ls] = bf16_bits_of(rng.standard_normal(ks[first:b + ls].shape) * 3)
+        vs[first:b + ls] = bf16_bits_of(rng.standard_normal(vs[first:b + ls].shape) * 3)
+        o2, l2 = orc.extend_attn(**dict(_extend_args(c), k_suffix=ks, v_suffix=vs))
+        q0 = int(c["q_start"][s])
+        assert np.array_equal(o2[q0:q0 + cut + 1], o[q0:q0 + cut + 1]), "a later token leaked into an earlier one"
+        assert np.array_equal(l2[q0:q0 + cut + 1], l[q0:q0 + cut + 1])
+        assert not np.allclose(o2[q0 + cut + 1:q0 + n], o[q0 + cut + 1:q0 + n]), "later tokens must see the change"
+
+
+def pin_extend_prefix_sharing(orc):
+    """E4: a shared prefix equals concatenating it into every candidate's suffix."""
+    c = extend_case(P=2, G=3, Hq=4, Hkv=2, D=8, lp=[5, 3], ls=[2, 1, 4, 1, 3, 2], nl=[2, 0, 3, 1, 1, 2], seed=27)
+    o, l = orc.extend_attn(**_extend_args(c))
+    krows, vrows, starts, lens = [], [], [], []
+    pos = 0
+    for s in range(6):
+        p = s // 3
+        a, n = c["prefix_start"][p], c["prefix_len"][p]
+        b, m = c["suffix_start"][s], c["suffix_len"][s]
+        krows.append(np.concatenate([c["k_prefix"][a:a + n], c["k_suffix"][b:b + m]]))
+        vrows.append(np.concatenate([c["v_prefix"][a:a + n], c["v_suffix"][b:b + m]]))
+        starts.append(pos); lens.append(n + m); pos += n + m
+    c2 = dict(_extend_args(c), k_prefix=c["k_prefix"][:1], v_prefix=c["v_prefix"][:1],
+              prefix_start=np.zeros(2, np.int64), prefix_len=np.zeros(2, np.int32),
+              k_suffix=np.concatenate(krows), v_suffix=np.concatenate(vrows),
+              suffix_start=np.array(starts, np.int64), suffix_len=np.array(lens, np.int32))
+    o2, l2 = orc.extend_attn(**c2)
+    close(o, o2, 1e-12, "extend prefix sharing out")
+    close(l, l2, 1e-12, "extend prefix sharing lse")
+
+
+def pin_extend_golden(orc):
+    """Hand-derived worked examples (tests/golden/extend_hand.json)."""
+    with open(os.path.join(GOLDEN, "extend_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        c = {k: bf16_bits_of(np.array(case[k], np.float64))
+             for k in ("q", "k_prefix", "v_prefix", "k_suffix", "v_suffix")}
+        c.update(prefix_start=np.array(case["prefix_start"], np.int64),
+                 prefix_len=np.array(case["prefix_len"], np.int32),
+                 suffix_start=np.array(case["suffix_start"], np.int64),
+                 suffix_len=np.array(case["suffix_len"], np.int32),
+                 new_len=np.array(case["new_len"], np.int32), q_start=np.array(case["q_start"], np.int64),
+                 group_size=case["group_size"], scale=case["scale"])
+        o, l = orc.extend_attn(**c)
+        close(o, np.array(case["out"]), 1e-15, case["name"] + " out")
+        close(l, np.array(case["lse"]), 1e-15, case["name"] + " lse")
+
+
+EXTEND_PINS = [pin_extend_vs_torch, pin_extend_decode_steps, pin_extend_future_independence,
+               pin_extend_prefix_sharing, pin_extend_golden]
+ALL_PINS = ALL_PINS + EXTEND_PINS

@@ -64,6 +64,23 @@ MUTANTS = [
      "const double lse = row_logits(H, V, h, w_lm, 1.0, y);", "samp"),
     ("interval_includes_own_mass", "if (v < t) below += pv;", "if (v <= t) below += pv;", "samp"),
     ("sample_logprob_unnormalised", "logprob[r] = y[t] - lse;", "logprob[r] = y[t];", "samp"),
+    # extend (prefill) attention of a refinement turn
+    ("ext_excludes_self", "const int64_t visible = n_pre + (n_suf - n_new + i) + 1;",
+     "const int64_t visible = n_pre + (n_suf - n_new + i);", "ext"),
+    ("ext_new_at_suffix_start", "const int64_t visible = n_pre + (n_suf - n_new + i) + 1;",
+     "const int64_t visible = n_pre + i + 1;", "ext"),
+    ("ext_not_causal", "const int64_t visible = n_pre + (n_suf - n_new + i) + 1;",
+     "const int64_t visible = n_pre + n_suf;", "ext"),
+    ("ext_query_rows_reversed", "const int64_t qrow = q_start[c] + i;",
+     "const int64_t qrow = q_start[c] + (n_new - 1 - i);", "ext"),
+    ("ext_head_map", "const int32_t kv_head = head / heads_per_kv;", "const int32_t kv_head = head % Hkv;", "ext"),
+    ("ext_prompt_of_candidate", "const int64_t prompt = c / G;", "const int64_t prompt = c % P;", "ext"),
+    ("ext_dropped_scale", "score[j] = (double)scale * qk;", "score[j] = qk;", "ext"),
+    ("ext_lse_drops_max", "lse[qrow * Hq + head] = mx + log(zsum);", "lse[qrow * Hq + head] = log(zsum);", "ext"),
+    ("ext_suffix_row_index", "k_suffix + ((suffix_start[c] + (j - n_pre))", "k_suffix + ((suffix_start[c] + j)", "ext"),
+    ("ext_value_from_prefix_keys", "? v_prefix + ((prefix_start[prompt] + j)",
+     "? k_prefix + ((prefix_start[prompt] + j)", "ext"),
+    ("ext_unnormalised", "const double wj = exp(score[j] - mx) / zsum;", "const double wj = exp(score[j] - mx);", "ext"),
 ]
 
 
@@ -81,7 +98,8 @@ def test_mutant_is_caught(tmp_path, source, name, old, new, battery):
     lib = oracle.compile_c(str(src), str(tmp_path / f"liboracle_{name}.so"))
     orc = oracle.Oracle(lib)
     battery_fns = {"attn": pins.ATTENTION_PINS, "lp": pins.LOGPROB_PINS, "grpo": pins.GRPO_PINS,
-                   "bwd": pins.BACKWARD_PINS, "samp": pins.SAMPLING_PINS}[battery]
+                   "bwd": pins.BACKWARD_PINS, "samp": pins.SAMPLING_PINS,
+                   "ext": pins.EXTEND_PINS}[battery]
     caught = []
     for pin in battery_fns:
         try:

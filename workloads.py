@@ -296,3 +296,30 @@ def make_sample_inputs(cfg: LogprobConfig, device="cpu", seed: int = 0, top_p: f
     u = np.random.Generator(np.random.PCG64(seed + 200)).random(R, dtype=np.float32)
     return SampleInputs(cfg, hidden, w, torch.from_numpy(inv_t).to(device), torch.from_numpy(u).to(device),
                         float(np.float32(top_p)))
+
+
+@dataclasses.dataclass
+class ExtendInputs:
+    """A refinement turn's extend: the caches of a DecodeInputs (each candidate's
+    suffix already holds its new tokens' K/V at its end) plus the new tokens'
+    queries, packed [sum(new_len), Hq, D] with candidate s at rows
+    [q_start[s], +new_len[s])."""
+    dec: DecodeInputs
+    q: torch.Tensor
+    new_len: np.ndarray   # int32 [S], 0 <= new_len <= suffix_len
+    q_start: np.ndarray   # int64 [S]
+
+
+def make_extend_inputs(cfg: DecodeConfig, device="cpu", seed: int = 0,
+                       new_len: Optional[np.ndarray] = None,
+                       suffix_len: Optional[np.ndarray] = None,
+                       prefix_len: Optional[np.ndarray] = None,
+                       kv_layout: str = "token") -> ExtendInputs:
+    """Default new_len: the whole suffix is new (the turn's summary, feedback and
+    previous code are read in one pass against the shared prefix)."""
+    dec = make_decode_inputs(cfg, device, seed, suffix_len=suffix_len, prefix_len=prefix_len,
+                             kv_layout=kv_layout)
+    n = dec.suffix_len.copy() if new_len is None else np.asarray(new_len, dtype=np.int32)
+    qs = packed_starts(n)
+    q = _randn_bf16((int(n.sum()), cfg.num_q_heads, cfg.head_dim), seed + 8, device)
+    return ExtendInputs(dec, q, n, qs)
