@@ -12,6 +12,12 @@
  *                     each has its own suffix KV (its generated tokens, at most
  *                     1536 per turn in Sec. 3, Multi-turn RL Training).
  *
+ *  rl_extend_attn     the prefill of a refinement turn: each candidate's new
+ *                     tokens (the feedback and summary appended to its
+ *                     context, Sec. 3, Structured Feedback and Iterative
+ *                     Refinement) attend causally to the prompt's shared
+ *                     prefix and to the candidate's suffix up to themselves.
+ *
  *  rl_kv_append       writes new tokens' keys and values after each
  *                     candidate's suffix in place (the decode loop's cache
  *                     update).
@@ -69,7 +75,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 6
+#define RL_ABI_VERSION 7
 
 typedef enum {
     RL_OK = 0,
@@ -150,6 +156,60 @@ rl_status rl_decode_attn_workspace_size(const rl_decode_shape *shape,
 rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *lens,
                          const rl_decode_ptrs *ptrs,
                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Extend (prefill) attention of a refinement turn                           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Each refinement turn appends structured feedback (and a summary of the
+ * earlier turns) to a candidate's context before the policy generates again
+ * (Sec. 3, Structured Feedback and Iterative Refinement); the policy first
+ * reads those new tokens in one pass.  Candidate s = p*G + g has the context
+ * prefix(p) followed by suffix(s); the last new_len[s] tokens of its suffix
+ * are new, their K/V already in the cache.  New token i (0 <= i < n = new_len[s])
+ * is at suffix position Ls[s] - n + i and attends, at query head h and kv head
+ * h / (Hq/Hkv), to every prefix token and to suffix positions 0 .. Ls[s] - n + i
+ * (itself included): the causal mask of a prefill.  Its query and its output
+ * are row q_start[s] + i of q / out ([q_rows, Hq, D] bf16, contiguous), its
+ * log-sum-exp lse[(q_start[s] + i) * Hq + h] (fp32, natural log; lse may be
+ * NULL).  Rows of q / out that belong to no candidate are not written.
+ * With every new_len = 1 this is rl_decode_attn's result.
+ *
+ * The shape and the KV tensors are those of rl_decode_attn (both kv layouts;
+ * split_tokens is not used).  Work is cut into blocks of 256 query rows (token
+ * x query head of one candidate and kv head), each streaming its visible
+ * context through LDS; blocks of one prompt run together so its prefix is read
+ * from HBM about once per XCD.  The workspace holds the work list (48 bytes per
+ * block).
+ *
+ * Status: NULL pointers -> RL_ERR_NULL_POINTER; the checks of rl_decode_attn
+ * on the shape and the KV ranges, and new_len[s] < 0, new_len[s] > Ls[s], a
+ * query range outside [0, q_rows), or two candidates sharing a query row ->
+ * RL_ERR_INVALID_SHAPE; head_dim not in {64, 128} -> RL_ERR_UNSUPPORTED; a
+ * device pointer not 16-byte aligned -> RL_ERR_MISALIGNED; workspace NULL or
+ * short -> RL_ERR_WORKSPACE.  No new tokens is a valid no-op.
+ */
+typedef struct {
+    const int64_t *prefix_start; /* host [P]:   first KV row of prompt p's prefix           */
+    const int32_t *prefix_len;   /* host [P]:   Lp[p] >= 0                                  */
+    const int64_t *suffix_start; /* host [P*G]: first KV row of candidate s's suffix        */
+    const int32_t *suffix_len;   /* host [P*G]: Ls[s] >= 0 tokens, the new ones included     */
+    const int32_t *new_len;      /* host [P*G]: 0 <= n[s] <= Ls[s] new tokens at its end     */
+    const int64_t *q_start;      /* host [P*G]: row of s's first new token in q / out / lse */
+    int64_t prefix_rows;         /* rows allocated in k_prefix / v_prefix                   */
+    int64_t suffix_rows;         /* rows allocated in k_suffix / v_suffix                   */
+    int64_t q_rows;              /* rows of q and out                                       */
+} rl_extend_lens;
+
+rl_status rl_extend_attn_workspace_size(const rl_decode_shape *shape, const rl_extend_lens *lens,
+                                        size_t *bytes);
+
+/* ptrs: q / out are [q_rows, Hq, D], lse [q_rows, Hq] or NULL; the KV pointers
+ * as for rl_decode_attn. */
+rl_status rl_extend_attn(const rl_decode_shape *shape, const rl_extend_lens *lens,
+                         const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
+                         void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Appending to the suffix KV cache                                          */

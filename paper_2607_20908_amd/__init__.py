@@ -8,6 +8,9 @@ built, importing this package raises.
     decode_attn(...)    prefix-shared grouped-query decode attention for a
                         batch of prompts with G candidates each (Sec. 2.2.1,
                         Problem Setup)
+    extend_attn(...)    causal prefill of each candidate's new tokens over
+                        the shared prefix and its own suffix (Sec. 3,
+                        Structured Feedback and Iterative Refinement)
     token_logprob(...)  log-prob of each sampled token over the full
                         vocabulary, through the lm-head, without storing the
                         logits (the GRPO ratio's factor, Sec. 3, Eq. grpo-loss)
@@ -55,6 +58,13 @@ class DecodeLens(ctypes.Structure):
                 ("prefix_rows", ctypes.c_int64), ("suffix_rows", ctypes.c_int64)]
 
 
+class ExtendLens(ctypes.Structure):
+    _fields_ = [("prefix_start", ctypes.c_void_p), ("prefix_len", ctypes.c_void_p),
+                ("suffix_start", ctypes.c_void_p), ("suffix_len", ctypes.c_void_p),
+                ("new_len", ctypes.c_void_p), ("q_start", ctypes.c_void_p),
+                ("prefix_rows", ctypes.c_int64), ("suffix_rows", ctypes.c_int64), ("q_rows", ctypes.c_int64)]
+
+
 class KvAppendLens(ctypes.Structure):
     _fields_ = [("suffix_start", ctypes.c_void_p), ("suffix_len", ctypes.c_void_p),
                 ("suffix_capacity", ctypes.c_void_p), ("new_start", ctypes.c_void_p),
@@ -79,7 +89,7 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
-           "rl_kv_append"]
+           "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn"]
 
 
 def _load():
@@ -120,7 +130,11 @@ def _load():
     lib.rl_kv_append_workspace_size.argtypes = [P, P, ctypes.POINTER(SZ)]
     lib.rl_kv_append.restype = ctypes.c_int
     lib.rl_kv_append.argtypes = [P, P, P, P, P, P, P, SZ, P]
-    if lib.rl_abi_version() != 6:
+    lib.rl_extend_attn_workspace_size.restype = ctypes.c_int
+    lib.rl_extend_attn_workspace_size.argtypes = [P, P, ctypes.POINTER(SZ)]
+    lib.rl_extend_attn.restype = ctypes.c_int
+    lib.rl_extend_attn.argtypes = [P, P, P, P, SZ, P]
+    if lib.rl_abi_version() != 7:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -338,6 +352,103 @@ def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
     _check(_lib.rl_decode_attn(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(ptrs),
                                ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                _stream_handle(stream)), "rl_decode_attn")
+    return (out, lse) if return_lse else out
+
+
+class _ExtendArgs:
+    """Host-side ctypes structures for one extend call (kept alive by the caller)."""
+
+    def __init__(self, P, G, Hq, Hkv, D, scale, prefix_start, prefix_len, suffix_start, suffix_len,
+                 new_len, q_start, prefix_rows, suffix_rows, q_rows, kv_layout="token"):
+        self.ps = np.ascontiguousarray(prefix_start, dtype=np.int64)
+        self.pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
+        self.ss = np.ascontiguousarray(suffix_start, dtype=np.int64)
+        self.sl = np.ascontiguousarray(suffix_len, dtype=np.int32)
+        self.nl = np.ascontiguousarray(new_len, dtype=np.int32)
+        self.qs = np.ascontiguousarray(q_start, dtype=np.int64)
+        S = P * G
+        if self.ps.shape != (P,) or self.pl.shape != (P,) or \
+                any(x.shape != (S,) for x in (self.ss, self.sl, self.nl, self.qs)):
+            raise ValueError("length arrays must be [P] (prefix) and [P*G] (candidates)")
+        if kv_layout not in KV_LAYOUTS:
+            raise ValueError(f"kv_layout must be one of {sorted(KV_LAYOUTS)}")
+        self.shape = DecodeShape(P, G, Hq, Hkv, D, float(np.float32(scale)), 0, KV_LAYOUTS[kv_layout])
+        self.lens = ExtendLens(self.ps.ctypes.data, self.pl.ctypes.data, self.ss.ctypes.data,
+                               self.sl.ctypes.data, self.nl.ctypes.data, self.qs.ctypes.data,
+                               int(prefix_rows), int(suffix_rows), int(q_rows))
+
+
+def extend_attn_workspace_size(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix_len,
+                               new_len, q_start, prefix_rows, suffix_rows, q_rows, scale=None,
+                               kv_layout: str = "token") -> int:
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    a = _ExtendArgs(P, G, Hq, Hkv, D, scale, prefix_start, prefix_len, suffix_start, suffix_len,
+                    new_len, q_start, prefix_rows, suffix_rows, q_rows, kv_layout)
+    n = ctypes.c_size_t(0)
+    _check(_lib.rl_extend_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(n)),
+           "rl_extend_attn_workspace_size")
+    return n.value
+
+
+def extend_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
+                k_suffix: torch.Tensor, v_suffix: torch.Tensor,
+                prefix_start, prefix_len, suffix_start, suffix_len, new_len, q_start, group_size: int,
+                scale: Optional[float] = None, return_lse: bool = False,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, stream=None, kv_layout: str = "token"):
+    """Causal extend (prefill) attention of each candidate's new tokens.
+
+    The last new_len[s] tokens of candidate s's suffix are new; new token i
+    (query row q_start[s] + i of q) attends to the prompt's prefix and to the
+    suffix up to and including itself.  q [Q, Hq, D] bf16; KV tensors as for
+    decode_attn; length arrays on the host.  Returns out [Q, Hq, D] bf16 (and
+    lse [Q, Hq] fp32); rows of no candidate are left as allocated.
+    """
+    for t, n in ((q, "q"), (k_prefix, "k_prefix"), (v_prefix, "v_prefix"),
+                 (k_suffix, "k_suffix"), (v_suffix, "v_suffix")):
+        _bf16_dev(t, n)
+    Q, Hq, D = q.shape
+    G = int(group_size)
+    S = len(suffix_len)
+    if G <= 0 or S % G:
+        raise ValueError("the number of candidates must be a positive multiple of group_size")
+    P = S // G
+    head_major = kv_layout == "head"
+    hdim, rdim = (0, 1) if head_major else (1, 0)
+    Hkv = k_suffix.shape[hdim]
+    for t in (k_prefix, v_prefix, k_suffix, v_suffix):
+        if t.dim() != 3 or t.shape[hdim] != Hkv or t.shape[2] != D:
+            raise ValueError("KV tensors must be [rows, Hkv, D] (token) or [Hkv, rows, D] (head)")
+    if k_prefix.shape != v_prefix.shape or k_suffix.shape != v_suffix.shape:
+        raise ValueError("K and V shapes differ")
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    a = _ExtendArgs(P, G, Hq, Hkv, D, scale, prefix_start, prefix_len, suffix_start, suffix_len,
+                    new_len, q_start, k_prefix.shape[rdim], k_suffix.shape[rdim], Q, kv_layout)
+    if out is None:
+        out = torch.empty((Q, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if return_lse and lse is None:
+        lse = torch.empty((Q, Hq), dtype=torch.float32, device=q.device)
+    _bf16_dev(out, "out")
+    if out.shape != (Q, Hq, D):
+        raise ValueError("out must be [Q, Hq, D]")
+    if lse is not None:
+        _on_device(lse, "lse")
+        if lse.dtype != torch.float32 or lse.shape != (Q, Hq) or not lse.is_contiguous():
+            raise ValueError("lse must be a contiguous fp32 [Q, Hq] tensor")
+    need = ctypes.c_size_t(0)
+    _check(_lib.rl_extend_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(need)),
+           "rl_extend_attn_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(max(need.value, 1), dtype=torch.uint8, device=q.device)
+    _on_device(workspace, "workspace")
+    ptrs = DecodePtrs(q.data_ptr() if q.numel() else None, k_prefix.data_ptr() if k_prefix.numel() else None,
+                      v_prefix.data_ptr() if v_prefix.numel() else None,
+                      k_suffix.data_ptr() if k_suffix.numel() else None,
+                      v_suffix.data_ptr() if v_suffix.numel() else None,
+                      out.data_ptr() if out.numel() else None, lse.data_ptr() if lse is not None and lse.numel() else None)
+    _check(_lib.rl_extend_attn(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(ptrs),
+                               ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                               _stream_handle(stream)), "rl_extend_attn")
     return (out, lse) if return_lse else out
 
 

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "librlkern.so")
-SOURCES = ["plan.cpp", "abi.cpp", "decode_attn.hip", "kv_append.hip", "token_logprob.hip", "token_logprob_bwd.hip", "sample_top_p.hip", "grpo.hip"]
+SOURCES = ["plan.cpp", "abi.cpp", "decode_attn.hip", "extend_attn.hip", "kv_append.hip", "token_logprob.hip", "token_logprob_bwd.hip", "sample_top_p.hip", "grpo.hip"]
 ARCH = "gfx950"
 
 

@@ -47,6 +47,7 @@ thread_local int g_staging_next;
 // One plan object per thread, reused so that planning does not allocate once
 // its vectors have grown to the problem size.
 thread_local rlk::DecodePlan g_plan;
+thread_local rlk::ExtendPlan g_extend_plan;
 
 struct Section {
     size_t off;
@@ -211,6 +212,59 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
     const hipError_t e = rlk::launch_decode(a, hs);
     if (e != hipSuccess) return hip_error(e, "launching decode attention");
+    return RL_OK;
+}
+
+rl_status rl_extend_attn_workspace_size(const rl_decode_shape *shape, const rl_extend_lens *lens,
+                                        size_t *bytes) {
+    g_last_error.clear();
+    if (!bytes) return set_error(RL_ERR_NULL_POINTER, "bytes is NULL");
+    std::string err;
+    const rl_status st = rlk::plan_extend(shape, lens, &g_extend_plan, &err, false);
+    if (st != RL_OK) return set_error(st, err);
+    *bytes = g_extend_plan.total_bytes;
+    return RL_OK;
+}
+
+rl_status rl_extend_attn(const rl_decode_shape *shape, const rl_extend_lens *lens,
+                         const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
+                         void *stream) {
+    g_last_error.clear();
+    rlk::ExtendPlan &plan = g_extend_plan;
+    std::string err;
+    rl_status st = rlk::plan_extend(shape, lens, &plan, &err, true);
+    if (st != RL_OK) return set_error(st, err);
+    st = rlk::check_extend_ptrs(plan, ptrs, &err);
+    if (st != RL_OK) return set_error(st, err);
+    if (plan.n_items == 0) return RL_OK;
+    if (!workspace || workspace_bytes < plan.total_bytes)
+        return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(plan.total_bytes) +
+                                               " bytes, got " + std::to_string(workspace_bytes));
+    if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    const Section sec[1] = {{0, plan.items.data(), plan.items.size() * sizeof(rlk::ExtItem)}};
+    st = stage_sections(sec, 1, plan.total_bytes, workspace, hs);
+    if (st != RL_OK) return st;
+    rlk::ExtendArgs a{};
+    a.q = static_cast<const uint16_t *>(ptrs->q);
+    a.k_prefix = static_cast<const uint16_t *>(ptrs->k_prefix);
+    a.v_prefix = static_cast<const uint16_t *>(ptrs->v_prefix);
+    a.k_suffix = static_cast<const uint16_t *>(ptrs->k_suffix);
+    a.v_suffix = static_cast<const uint16_t *>(ptrs->v_suffix);
+    a.out = static_cast<uint16_t *>(ptrs->out);
+    a.lse = ptrs->lse;
+    a.items = static_cast<const rlk::ExtItem *>(workspace);
+    a.n_items = static_cast<int32_t>(plan.n_items);
+    a.Hq = plan.Hq;
+    a.Hkv = plan.Hkv;
+    a.r = plan.r;
+    a.D = plan.D;
+    a.kv_layout = plan.kv_layout;
+    a.prefix_rows = plan.prefix_rows;
+    a.suffix_rows = plan.suffix_rows;
+    a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
+    const hipError_t e = rlk::launch_extend(a, hs);
+    if (e != hipSuccess) return hip_error(e, "launching extend attention");
     return RL_OK;
 }
 

@@ -62,16 +62,6 @@ __device__ __forceinline__ int v_off(int t, int c) {
     return t * DCfg<D>::LDRV + (c << 3);
 }
 
-// gfx950 transposing LDS read: in each group of 16 lanes, lane s supplies the
-// address of 4 consecutive bf16; seen as a 4 x 16 block whose row k holds the
-// values of lanes 4k..4k+3 in order, lane n receives column n (rows 0..3).
-__device__ __forceinline__ bf16x4 lds_read_tr16(const uint16_t *p) {
-    typedef short s16x4 __attribute__((ext_vector_type(4)));
-    typedef s16x4 __attribute__((address_space(3))) *lds_s16x4;
-    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
-    return __builtin_bit_cast(bf16x4, v);
-}
-
 // MAXC: column tiles (16 query rows each) per wave; 1 serves items of up to
 // 64 query rows, 2 serves up to 128.
 template <int D, int MAXC>

@@ -26,6 +26,22 @@ struct DecodeArgs {
 
 hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
 
+// Causal extend attention: one workgroup per ExtItem block of query rows.
+struct ExtendArgs {
+    const uint16_t *q;
+    const uint16_t *k_prefix, *v_prefix, *k_suffix, *v_suffix;
+    uint16_t *out;
+    float *lse;                 // may be null
+    const ExtItem *items;       // workspace: the work list
+    int32_t n_items;
+    int32_t Hq, Hkv, r, D;
+    int32_t kv_layout;
+    int64_t prefix_rows, suffix_rows;
+    float score_scale_log2;     // softmax_scale * log2(e)
+};
+
+hipError_t launch_extend(const ExtendArgs &a, hipStream_t stream);
+
 // Copies `bytes` (a multiple of 16) from device-mapped pinned host memory to
 // device memory with a kernel on `stream`, so the work list reaches the
 // workspace without a hand-off between the copy engine and the compute queue.

@@ -46,13 +46,8 @@ void reset(DecodePlan *pl) {
     pl->tmp_keys2 = std::move(k2);
 }
 
-}  // namespace
-
-rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
-                      DecodePlan *plan, std::string *err, PlanDetail detail) {
-    if (!shape) return fail(err, RL_ERR_NULL_POINTER, "shape is NULL");
-    if (!lens) return fail(err, RL_ERR_NULL_POINTER, "lens is NULL");
-    const rl_decode_shape &sh = *shape;
+// The checks of a decode shape that every attention entry point shares.
+rl_status check_shape(const rl_decode_shape &sh, std::string *err) {
     if (sh.num_prompts < 0) return fail(err, RL_ERR_INVALID_SHAPE, "num_prompts < 0");
     if (sh.group_size < 1) return fail(err, RL_ERR_INVALID_SHAPE, "group_size < 1");
     if (sh.num_q_heads < 1 || sh.num_kv_heads < 1)
@@ -68,6 +63,43 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     if (sh.head_dim <= 0) return fail(err, RL_ERR_INVALID_SHAPE, "head_dim must be > 0");
     if (sh.head_dim != 64 && sh.head_dim != 128)
         return fail(err, RL_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+    return RL_OK;
+}
+
+// Prefix ranges of P prompts and suffix ranges of S candidates inside the
+// allocated rows.
+rl_status check_ranges(int64_t P, int64_t S, const int64_t *prefix_start, const int32_t *prefix_len,
+                       int64_t prefix_rows, const int64_t *suffix_start, const int32_t *suffix_len,
+                       int64_t suffix_rows, int64_t *sum_lp, int64_t *sum_ls, std::string *err) {
+    *sum_lp = *sum_ls = 0;
+    for (int64_t p = 0; p < P; ++p) {
+        const int64_t st = prefix_start[p], n = prefix_len[p];
+        if (n < 0) return fail(err, RL_ERR_INVALID_SHAPE, "prefix_len[" + std::to_string(p) + "] < 0");
+        if (n > 0 && (st < 0 || st > prefix_rows - n))
+            return fail(err, RL_ERR_INVALID_SHAPE,
+                        "prefix range of prompt " + std::to_string(p) + " exceeds prefix_rows");
+        *sum_lp += n;
+    }
+    for (int64_t s = 0; s < S; ++s) {
+        const int64_t st = suffix_start[s], n = suffix_len[s];
+        if (n < 0) return fail(err, RL_ERR_INVALID_SHAPE, "suffix_len[" + std::to_string(s) + "] < 0");
+        if (n > 0 && (st < 0 || st > suffix_rows - n))
+            return fail(err, RL_ERR_INVALID_SHAPE,
+                        "suffix range of candidate " + std::to_string(s) + " exceeds suffix_rows");
+        *sum_ls += n;
+    }
+    return RL_OK;
+}
+
+}  // namespace
+
+rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                      DecodePlan *plan, std::string *err, PlanDetail detail) {
+    if (!shape) return fail(err, RL_ERR_NULL_POINTER, "shape is NULL");
+    if (!lens) return fail(err, RL_ERR_NULL_POINTER, "lens is NULL");
+    const rl_decode_shape &sh = *shape;
+    rl_status st0 = check_shape(sh, err);
+    if (st0 != RL_OK) return st0;
     if (lens->prefix_rows < 0 || lens->suffix_rows < 0)
         return fail(err, RL_ERR_INVALID_SHAPE, "row counts must be >= 0");
 
@@ -91,22 +123,9 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     if (!lens->prefix_start || !lens->prefix_len || !lens->suffix_start || !lens->suffix_len)
         return fail(err, RL_ERR_NULL_POINTER, "length arrays must not be NULL when P*G > 0");
     int64_t sum_lp = 0, sum_ls = 0;
-    for (int64_t p = 0; p < P; ++p) {
-        const int64_t st = lens->prefix_start[p], n = lens->prefix_len[p];
-        if (n < 0) return fail(err, RL_ERR_INVALID_SHAPE, "prefix_len[" + std::to_string(p) + "] < 0");
-        if (n > 0 && (st < 0 || st > lens->prefix_rows - n))
-            return fail(err, RL_ERR_INVALID_SHAPE,
-                        "prefix range of prompt " + std::to_string(p) + " exceeds prefix_rows");
-        sum_lp += n;
-    }
-    for (int64_t s = 0; s < S; ++s) {
-        const int64_t st = lens->suffix_start[s], n = lens->suffix_len[s];
-        if (n < 0) return fail(err, RL_ERR_INVALID_SHAPE, "suffix_len[" + std::to_string(s) + "] < 0");
-        if (n > 0 && (st < 0 || st > lens->suffix_rows - n))
-            return fail(err, RL_ERR_INVALID_SHAPE,
-                        "suffix range of candidate " + std::to_string(s) + " exceeds suffix_rows");
-        sum_ls += n;
-    }
+    st0 = check_ranges(P, S, lens->prefix_start, lens->prefix_len, lens->prefix_rows, lens->suffix_start,
+                       lens->suffix_len, lens->suffix_rows, &sum_lp, &sum_ls, err);
+    if (st0 != RL_OK) return st0;
 
     // --- split sizes --------------------------------------------------------
     const int64_t Mp = G * r;                       // query rows per prefix unit
@@ -285,6 +304,142 @@ rl_status check_decode_ptrs(const DecodePlan &pl, const rl_decode_lens *lens,
             return fail(err, RL_ERR_MISALIGNED, std::string(names[i]) + " is not 16-byte aligned");
     if (ptrs->lse && !aligned(ptrs->lse, 4))
         return fail(err, RL_ERR_MISALIGNED, "lse is not 4-byte aligned");
+    return RL_OK;
+}
+
+rl_status plan_extend(const rl_decode_shape *shape, const rl_extend_lens *lens, ExtendPlan *plan,
+                      std::string *err, bool build) {
+    if (!shape) return fail(err, RL_ERR_NULL_POINTER, "shape is NULL");
+    if (!lens) return fail(err, RL_ERR_NULL_POINTER, "lens is NULL");
+    const rl_decode_shape &sh = *shape;
+    rl_status st = check_shape(sh, err);
+    if (st != RL_OK) return st;
+    if (lens->prefix_rows < 0 || lens->suffix_rows < 0 || lens->q_rows < 0)
+        return fail(err, RL_ERR_INVALID_SHAPE, "row counts must be >= 0");
+    ExtendPlan &pl = *plan;
+    pl.P = sh.num_prompts;
+    pl.G = sh.group_size;
+    pl.Hq = sh.num_q_heads;
+    pl.Hkv = sh.num_kv_heads;
+    pl.D = sh.head_dim;
+    pl.r = sh.num_q_heads / sh.num_kv_heads;
+    pl.scale = sh.softmax_scale;
+    pl.kv_layout = sh.kv_layout;
+    pl.prefix_rows = lens->prefix_rows;
+    pl.suffix_rows = lens->suffix_rows;
+    pl.q_rows = lens->q_rows;
+    pl.n_items = 0;
+    pl.any_prefix = false;
+    pl.ctx_tokens = 0;
+    pl.total_bytes = 0;
+    pl.items.clear();
+    const int64_t P = pl.P, G = pl.G, S = P * G, r = pl.r;
+    if (S > INT32_MAX / 2 || S * pl.Hq > INT32_MAX)
+        return fail(err, RL_ERR_UNSUPPORTED, "too many sequences x heads");
+    if (S == 0) return RL_OK;
+    if (!lens->prefix_start || !lens->prefix_len || !lens->suffix_start || !lens->suffix_len ||
+        !lens->new_len || !lens->q_start)
+        return fail(err, RL_ERR_NULL_POINTER, "length arrays must not be NULL when P*G > 0");
+    int64_t sum_lp = 0, sum_ls = 0;
+    st = check_ranges(P, S, lens->prefix_start, lens->prefix_len, lens->prefix_rows, lens->suffix_start,
+                      lens->suffix_len, lens->suffix_rows, &sum_lp, &sum_ls, err);
+    if (st != RL_OK) return st;
+    // new tokens and their query rows; two candidates must not write one row
+    pl.tmp_ranges.clear();
+    for (int64_t s = 0; s < S; ++s) {
+        const int64_t n = lens->new_len[s], q0 = lens->q_start[s];
+        if (n < 0 || n > lens->suffix_len[s])
+            return fail(err, RL_ERR_INVALID_SHAPE,
+                        "new_len[" + std::to_string(s) + "] must be in [0, suffix_len]");
+        if (n == 0) continue;
+        if (n * r > INT32_MAX) return fail(err, RL_ERR_UNSUPPORTED, "new_len x Hq/Hkv too large");
+        if (q0 < 0 || q0 > lens->q_rows - n)
+            return fail(err, RL_ERR_INVALID_SHAPE,
+                        "query rows of candidate " + std::to_string(s) + " exceed q_rows");
+        pl.tmp_ranges.emplace_back(q0, q0 + n);
+    }
+    std::sort(pl.tmp_ranges.begin(), pl.tmp_ranges.end());
+    for (size_t i = 1; i < pl.tmp_ranges.size(); ++i)
+        if (pl.tmp_ranges[i].first < pl.tmp_ranges[i - 1].second)
+            return fail(err, RL_ERR_INVALID_SHAPE, "two candidates share query rows");
+
+    // blocks: per (prompt, kv head) unit, per candidate, kExtBlockRows unit rows each
+    const int64_t Hkv = pl.Hkv;
+    int64_t n_items = 0;
+    double ctx = 0;
+    for (int64_t s = 0; s < S; ++s) {
+        const int64_t n = lens->new_len[s];
+        if (n == 0) continue;
+        n_items += ceil_div(n * r, kExtBlockRows) * Hkv;
+        pl.any_prefix |= lens->prefix_len[s / G] > 0;
+        const int64_t base = lens->prefix_len[s / G] + lens->suffix_len[s] - n;
+        ctx += static_cast<double>(Hkv * r) * (static_cast<double>(n) * base + 0.5 * n * (n + 1));
+    }
+    pl.n_items = n_items;
+    pl.ctx_tokens = ctx;
+    pl.total_bytes = align_up(static_cast<size_t>(n_items) * sizeof(ExtItem), 256);
+    if (n_items > INT32_MAX) return fail(err, RL_ERR_UNSUPPORTED, "too many work blocks");
+    if (!build || n_items == 0) return RL_OK;
+
+    // units by work, largest first; blocks inside a unit by visible context, longest first
+    pl.tmp_units.clear();
+    for (int64_t p = 0; p < P; ++p) {
+        int64_t work = 0;
+        for (int64_t g = 0; g < G; ++g) {
+            const int64_t s = p * G + g, n = lens->new_len[s];
+            work += n * (lens->prefix_len[p] + lens->suffix_len[s]);
+        }
+        if (work > 0)
+            for (int64_t kh = 0; kh < Hkv; ++kh) pl.tmp_units.emplace_back(-work, p * Hkv + kh);
+    }
+    std::stable_sort(pl.tmp_units.begin(), pl.tmp_units.end());
+    pl.items.reserve(static_cast<size_t>(n_items));
+    for (const auto &u : pl.tmp_units) {
+        const int64_t p = u.second / Hkv, kh = u.second % Hkv;
+        pl.tmp_items.clear();
+        for (int64_t g = 0; g < G; ++g) {
+            const int64_t s = p * G + g, n = lens->new_len[s];
+            for (int64_t rb = 0; rb < n * r; rb += kExtBlockRows) {
+                ExtItem it{};
+                it.prefix_row0 = lens->prefix_len[p] > 0 ? lens->prefix_start[p] : 0;
+                it.suffix_row0 = lens->suffix_start[s];
+                it.q_row0 = lens->q_start[s];
+                it.Lp = lens->prefix_len[p];
+                it.Ls = lens->suffix_len[s];
+                it.n = static_cast<int32_t>(n);
+                it.kh = static_cast<int32_t>(kh);
+                it.row_begin = static_cast<int32_t>(rb);
+                // visible context of the block's last token, kept in pad for the sort
+                const int64_t i_hi = std::min<int64_t>(rb + kExtBlockRows, n * r) - 1;
+                it.pad = static_cast<int32_t>(std::min<int64_t>(INT32_MAX, it.Lp + it.Ls - n + i_hi / r + 1));
+                pl.tmp_items.push_back(it);
+            }
+        }
+        std::stable_sort(pl.tmp_items.begin(), pl.tmp_items.end(),
+                         [](const ExtItem &a, const ExtItem &b) { return a.pad > b.pad; });
+        for (ExtItem &it : pl.tmp_items) {
+            it.pad = 0;
+            pl.items.push_back(it);
+        }
+    }
+    return RL_OK;
+}
+
+rl_status check_extend_ptrs(const ExtendPlan &pl, const rl_decode_ptrs *ptrs, std::string *err) {
+    if (!ptrs) return fail(err, RL_ERR_NULL_POINTER, "ptrs is NULL");
+    if (pl.n_items == 0) return RL_OK;
+    if (!ptrs->q) return fail(err, RL_ERR_NULL_POINTER, "q is NULL");
+    if (!ptrs->out) return fail(err, RL_ERR_NULL_POINTER, "out is NULL");
+    // every candidate with new tokens has a non-empty suffix; the prefix may be empty
+    if (!ptrs->k_suffix || !ptrs->v_suffix) return fail(err, RL_ERR_NULL_POINTER, "k_suffix/v_suffix is NULL");
+    if (pl.any_prefix && (!ptrs->k_prefix || !ptrs->v_prefix))
+        return fail(err, RL_ERR_NULL_POINTER, "k_prefix/v_prefix is NULL");
+    const void *a16[] = {ptrs->q, ptrs->k_prefix, ptrs->v_prefix, ptrs->k_suffix, ptrs->v_suffix, ptrs->out};
+    const char *names[] = {"q", "k_prefix", "v_prefix", "k_suffix", "v_suffix", "out"};
+    for (int i = 0; i < 6; ++i)
+        if (a16[i] && !aligned(a16[i], 16))
+            return fail(err, RL_ERR_MISALIGNED, std::string(names[i]) + " is not 16-byte aligned");
+    if (ptrs->lse && !aligned(ptrs->lse, 4)) return fail(err, RL_ERR_MISALIGNED, "lse is not 4-byte aligned");
     return RL_OK;
 }
 

@@ -1,5 +1,5 @@
-// Host-side argument validation and split-K planning for rl_decode_attn and
-// rl_token_logprob.  Plain C++17: no HIP calls, so every check here can be
+// Host-side argument validation and planning for rl_decode_attn,
+// rl_extend_attn and rl_token_logprob.  Plain C++17: no HIP calls, so every check here can be
 // exercised on a machine without a GPU.
 #pragma once
 
@@ -138,6 +138,46 @@ struct SamplePlan {
 };
 
 rl_status plan_sample(int64_t rows, int32_t hidden, int32_t vocab, SamplePlan *plan, std::string *err);
+
+// Extend attention: one block of at most kExtBlockRows query rows (new token x
+// query head of one candidate at one kv head) per workgroup.
+constexpr int kExtBlockRows = 256;
+
+struct ExtItem {
+    int64_t prefix_row0;   // first prefix row of the prompt (0 when Lp = 0)
+    int64_t suffix_row0;   // first suffix row of the candidate
+    int64_t q_row0;        // query / output row of the candidate's first new token
+    int32_t Lp, Ls, n;     // prefix length, suffix length (new tokens included), new tokens
+    int32_t kh;            // kv head
+    int32_t row_begin;     // first unit row of the block (unit row = token * r + head in group)
+    int32_t pad;
+};
+static_assert(sizeof(ExtItem) == 48, "ExtItem layout");
+
+struct ExtendPlan {
+    int32_t P = 0, G = 0, Hq = 0, Hkv = 0, D = 0, r = 0;
+    float scale = 0.f;
+    int32_t kv_layout = RL_KV_TOKEN_MAJOR;
+    int64_t prefix_rows = 0, suffix_rows = 0, q_rows = 0;
+    int64_t n_items = 0;
+    bool any_prefix = false;           // some block reads prefix rows
+    double ctx_tokens = 0;             // sum over query rows of visible tokens (flop count / 4D)
+    std::vector<ExtItem> items;        // launch order (built when requested)
+    size_t total_bytes = 0;            // workspace: the work list
+    // scratch kept between calls
+    std::vector<std::pair<int64_t, int64_t>> tmp_ranges;
+    std::vector<std::pair<int64_t, int64_t>> tmp_units;
+    std::vector<ExtItem> tmp_items;
+};
+
+// Validates an extend call (shape, lengths, query ranges; not device pointers)
+// and, with build = true, lays out the work list: the blocks of one (prompt,
+// kv head) are consecutive, units with more work first, and inside a unit the
+// blocks with the longest visible context first.
+rl_status plan_extend(const rl_decode_shape *shape, const rl_extend_lens *lens, ExtendPlan *plan,
+                      std::string *err, bool build);
+
+rl_status check_extend_ptrs(const ExtendPlan &plan, const rl_decode_ptrs *ptrs, std::string *err);
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

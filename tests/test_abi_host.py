@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 6
+    assert lib.rl_abi_version() == 7
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -429,3 +429,85 @@ def test_kv_append_validation(kw, expect):
 def test_kv_append_nothing_to_do():
     st, msg = append_call(nl=[0, 0, 0, 0], ptrs=[None, None, None, None], ws=None, ws_bytes=0)
     assert st == OK and msg == ""
+
+
+# ---------------------------------------------------------------- extend
+def extend_call(P=2, G=2, Hq=4, Hkv=2, D=128, scale=0.125, lp=None, ls=None, nl=None, qs=None,
+                prefix_rows=None, suffix_rows=None, q_rows=None, ptrs=None, ws=None, ws_bytes=1 << 30,
+                null_shape=False, null_lens=False, null_ptrs=False, layout=0, size_only=False):
+    lib = rk.lib()
+    S = P * G
+    lp = np.full(P, 5, np.int32) if lp is None else np.asarray(lp, np.int32)
+    ls = np.full(S, 4, np.int32) if ls is None else np.asarray(ls, np.int32)
+    nl = np.full(S, 2, np.int32) if nl is None else np.asarray(nl, np.int32)
+    qs = (np.arange(S, dtype=np.int64) * 2) if qs is None else np.asarray(qs, np.int64)
+    ps = np.arange(P, dtype=np.int64) * 5
+    ss = np.arange(S, dtype=np.int64) * 4
+    shape = rk.DecodeShape(P, G, Hq, Hkv, D, scale, 0, layout)
+    lens = rk.ExtendLens(ps.ctypes.data, lp.ctypes.data, ss.ctypes.data, ls.ctypes.data, nl.ctypes.data,
+                         qs.ctypes.data, 5 * P if prefix_rows is None else prefix_rows,
+                         4 * S if suffix_rows is None else suffix_rows, 2 * S if q_rows is None else q_rows)
+    if size_only:
+        n = ctypes.c_size_t(0)
+        st = lib.rl_extend_attn_workspace_size(ctypes.byref(shape), ctypes.byref(lens), ctypes.byref(n))
+        return st, n.value
+    p = dict(q=FAKE, k_prefix=FAKE + 256, v_prefix=FAKE + 512, k_suffix=FAKE + 768,
+             v_suffix=FAKE + 1024, out=FAKE + 1280, lse=FAKE + 1536)
+    p.update(ptrs or {})
+    dp = rk.DecodePtrs(p["q"], p["k_prefix"], p["v_prefix"], p["k_suffix"], p["v_suffix"], p["out"], p["lse"])
+    st = lib.rl_extend_attn(None if null_shape else ctypes.byref(shape), None if null_lens else ctypes.byref(lens),
+                            None if null_ptrs else ctypes.byref(dp), ws, ws_bytes, None)
+    return st, lib.rl_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(null_shape=True), NULLP),
+    (dict(null_lens=True), NULLP),
+    (dict(null_ptrs=True), NULLP),
+    (dict(ptrs=dict(q=None)), NULLP),
+    (dict(ptrs=dict(out=None)), NULLP),
+    (dict(ptrs=dict(k_suffix=None)), NULLP),
+    (dict(ptrs=dict(v_prefix=None)), NULLP),
+    (dict(G=0), SHAPE),
+    (dict(Hq=6, Hkv=4), SHAPE),
+    (dict(scale=0.0), SHAPE),
+    (dict(layout=3), SHAPE),
+    (dict(nl=[2, 2, 5, 2]), SHAPE),          # more new tokens than the suffix holds
+    (dict(nl=[2, -1, 2, 2]), SHAPE),
+    (dict(qs=[0, 2, 3, 6]), SHAPE),          # candidates 1 and 2 share query row 3
+    (dict(qs=[0, 2, 4, 7]), SHAPE),          # candidate 3 needs rows [7, 9) of 8
+    (dict(qs=[-1, 2, 4, 6]), SHAPE),
+    (dict(q_rows=-1), SHAPE),
+    (dict(prefix_rows=9), SHAPE),
+    (dict(suffix_rows=15), SHAPE),
+    (dict(ls=[4, 4, -1, 4], nl=[2, 2, 0, 2]), SHAPE),
+    (dict(D=96), UNSUP),
+    (dict(ptrs=dict(q=FAKE + 8)), MISAL),
+    (dict(ptrs=dict(k_prefix=FAKE + 4)), MISAL),
+    (dict(ptrs=dict(lse=FAKE + 2)), MISAL),
+    (dict(ws=None), WSPACE),
+    (dict(ws=FAKE, ws_bytes=64), WSPACE),
+    (dict(ws=FAKE + 8), MISAL),
+])
+def test_extend_validation(kw, expect):
+    kw.setdefault("ws", FAKE)
+    st, msg = extend_call(**kw)
+    assert st == expect, (st, msg)
+    assert msg, "a failing call must leave an error message"
+
+
+def test_extend_noops_and_sizes():
+    # no new tokens anywhere: valid, nothing enqueued, no workspace needed
+    st, msg = extend_call(nl=[0, 0, 0, 0], ws=None, ptrs=dict(q=None, out=None))
+    assert st == OK and msg == ""
+    st, msg = extend_call(P=0, lp=[], ls=[], nl=[], qs=[], ws=None)
+    assert st == OK and msg == ""
+    # no prefix at all: the prefix pointers may be NULL
+    st, n = extend_call(lp=[0, 0], prefix_rows=0, size_only=True)
+    assert st == OK
+    # 48 bytes per block of 256 query rows, rounded up to 256: 4 candidates x 2 kv heads x 1 block
+    st, n = extend_call(size_only=True)
+    assert st == OK and n == 512
+    st, n = extend_call(Hq=8, Hkv=1, ls=[200] * 4, nl=[100] * 4, qs=[0, 100, 200, 300], suffix_rows=800,
+                        q_rows=400, size_only=True)
+    assert st == OK and n == ((4 * 4 * 48 + 255) // 256) * 256   # 100 tokens x 8 heads = 4 blocks each
