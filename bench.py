@@ -9,7 +9,9 @@ workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
 [256, 2048]; lm-head 512 rows x hidden 4096 x vocab 151936).
 
 After the timed steps, further operations are timed in a loop of their own
-(outside the step): the KV append of one token per candidate, the backward
+(outside the step): the KV append of one token per candidate, the extend
+(prefill) of a refinement turn at the same shape with every suffix token new,
+the backward
 of the lm-head log-prob for the same rows,
 the GRPO advantages and clipped surrogate over the policy pass's 262144 rows,
 and (at decode shapes) the nucleus sampling head over the same rows.  They
@@ -156,6 +158,18 @@ def grpo_bytes(gx) -> int:
     return 8 * S + 16 * R + 4
 
 
+def extend_flops(xe) -> int:
+    """Algorithmic flops of one extend call: 2 D for the score and 2 D for the
+    value sum of every (new token, query head, visible token)."""
+    c = xe.dec.cfg
+    vis = 0
+    for s in range(c.num_seqs):
+        n = int(xe.new_len[s])
+        base = int(xe.dec.prefix_len[s // c.group_size]) + int(xe.dec.suffix_len[s]) - n
+        vis += n * base + n * (n + 1) // 2
+    return 4 * c.head_dim * c.num_q_heads * vis
+
+
 def cpu_baseline_decode(x, budget_s: float):
     """The fp64 oracle on the host over the workload's prompts (all their
     candidates), prompt by prompt, cycling through the batch until the time
@@ -224,6 +238,8 @@ def main():
     ap.add_argument("--no-update", action="store_true",
                     help="skip the policy-update operations (log-prob backward, GRPO surrogate), which "
                          "are timed after the step in a loop of their own")
+    ap.add_argument("--no-extend", action="store_true",
+                    help="skip the extend (prefill) of a refinement turn, timed after the step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy before the steps (outside the timed region) so a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -347,6 +363,48 @@ def main():
                                 "us": round(a_ms * 1e3, 2), "bound": "hbm",
                                 "achieved": round(nb_a / (a_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                                 "unit": "GB/s", "algorithmic_bytes": nb_a}}
+        del kc, vc
+    if x is not None and not args.no_extend:
+        c = x.cfg
+        # a refinement turn's extend at the same shape: every candidate's whole
+        # suffix is new and is read causally against the shared prefix
+        xe = W.make_extend_inputs(c, dev, kv_layout=args.kv_layout)
+        de = xe.dec
+        e_out = torch.empty(xe.q.shape, dtype=torch.bfloat16, device=dev)
+        e_lse = torch.empty(xe.q.shape[:2], dtype=torch.float32, device=dev)
+        rdim = 1 if args.kv_layout == "head" else 0
+        ws_e = torch.empty(max(256, rk.extend_attn_workspace_size(
+            c.num_prompts, c.group_size, c.num_q_heads, c.num_kv_heads, c.head_dim, de.prefix_start,
+            de.prefix_len, de.suffix_start, de.suffix_len, xe.new_len, xe.q_start, de.k_prefix.shape[rdim],
+            de.k_suffix.shape[rdim], xe.q.shape[0], de.scale, kv_layout=args.kv_layout)),
+            dtype=torch.uint8, device=dev)
+        run_extend = lambda: rk.extend_attn(xe.q, de.k_prefix, de.v_prefix, de.k_suffix, de.v_suffix,
+                                            de.prefix_start, de.prefix_len, de.suffix_start, de.suffix_len,
+                                            xe.new_len, xe.q_start, c.group_size, scale=de.scale, out=e_out,
+                                            lse=e_lse, workspace=ws_e, return_lse=True, kv_layout=args.kv_layout)
+        run_extend()
+        torch.cuda.synchronize()
+        esteps = max(1, min(args.steps, 5))
+        eev = [(hip.create(), hip.create()) for _ in range(esteps)]
+        for e0, e1 in eev:
+            hip.record(e0, sh)
+            run_extend()
+            hip.record(e1, sh)
+        torch.cuda.synchronize()
+        e_ms = float(np.mean([hip.elapsed_ms(e0, e1) for e0, e1 in eev]))
+        for pair in eev:
+            for e in pair:
+                hip.destroy(e)
+        fl_e = extend_flops(xe)
+        tf_e = fl_e / (e_ms * 1e-3) / 1e12
+        log(f"bench: extend {e_ms:.3f} ms, {tf_e:.1f} TFLOP/s")
+        update = dict(update or {})
+        update["extend"] = {"kernel": "extend (prefill) attention of a refinement turn, every suffix token new "
+                                      f"({int(xe.new_len.sum())} tokens)", "ms": round(e_ms, 4), "steps": esteps,
+                            "bound": "mfma", "achieved": round(tf_e, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                            "unit": "TFLOP/s", "frac": round(tf_e / MFMA_BF16_PEAK_TFLOPS, 4),
+                            "algorithmic_flops": fl_e}
+        del xe, de, e_out, e_lse, ws_e
     if y is not None and not args.no_update:
         cl = y.cfg
         g_b = torch.from_numpy(np.random.Generator(np.random.PCG64(5)).standard_normal(cl.rows)

@@ -29,7 +29,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBN = 64;        // KV tokens per tile
-constexpr int kStages = 3;     // LDS ring depth
+constexpr int kStages = 4;     // LDS ring depth
 
 template <int D>
 struct ECfg {
@@ -59,6 +59,12 @@ template <int D>
 __device__ __forceinline__ int kv_elem(int t, int d) {
     return t * D + ((((d >> 3) ^ swz<D>(t))) << 3) + (d & 7);
 }
+
+// Rows keep the max they exponentiate against until a new score exceeds it by
+// more than this many log2 units: probabilities stay below 2^8 (exact in
+// fp32, in range for bf16), the accumulators are rescaled only when the max
+// really moves, and out = acc / l and lse = m + log2 l are unchanged.
+constexpr float kRescaleLog2 = 8.f;
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) {
@@ -110,140 +116,202 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
     // ---- tile t of the context into ring stage t % kStages -------------------
     // Lane i of load instruction j writes the 16-byte slot i of the 1 KB block
     // j, i.e. row (64j + i) / CH, slot (64j + i) % CH; it fetches the chunk that
-    // the swizzle stores there.  Rows past the tile's tokens re-read its last
-    // token (never a row outside the range); their scores are masked.
+    // the swizzle stores there.  In a ragged last tile, rows past its tokens
+    // re-read its last token (never a row outside the range); their scores are
+    // masked.
+    // per-lane byte offsets of this wave's loads in a full tile (token row x
+    // stride + swizzled chunk); a ragged last tile clamps the token row
+    uint32_t ld_off[C::LPW];
+    int ld_tok[C::LPW], ld_chk[C::LPW];
+#pragma unroll
+    for (int j = 0; j < C::LPW; ++j) {
+        const int e = (wave * C::LPW + j) * 64 + lane;
+        const int tt = e / C::CH, slot = e % C::CH;
+        ld_tok[j] = tt;
+        ld_chk[j] = (slot ^ swz<D>(tt)) << 3;
+        ld_off[j] = static_cast<uint32_t>((tt * tok_stride + ld_chk[j]) * 2);
+    }
+    auto tile_tok0 = [&](int t) { return (t < np ? t : t - np) * kBN; };
+    auto tile_cnt = [&](int t) { return min(kBN, (t < np ? it.Lp : suf_ctx) - tile_tok0(t)); };
     auto issue = [&](int t) {
         uint16_t *kl = ring + (t % kStages) * 2 * C::TILE;
         uint16_t *vl = kl + C::TILE;
         const bool pre = t < np;
-        const int tok0 = (pre ? t : t - np) * kBN;
-        const int cnt = min(kBN, (pre ? it.Lp : suf_ctx) - tok0);
-        const uint16_t *kg = pre ? kpre : ksuf;
-        const uint16_t *vg = pre ? vpre : vsuf;
+        const int tok0 = tile_tok0(t), cnt = tile_cnt(t);
+        const uint16_t *kg = (pre ? kpre : ksuf) + tok0 * tok_stride;
+        const uint16_t *vg = (pre ? vpre : vsuf) + tok0 * tok_stride;
+        if (cnt == kBN) {
 #pragma unroll
-        for (int j = 0; j < C::LPW; ++j) {
-            const int inst = wave * C::LPW + j;
-            const int e = inst * 64 + lane;
-            const int tt = e / C::CH, slot = e % C::CH;
-            const int64_t off = static_cast<int64_t>(tok0 + min(tt, cnt - 1)) * tok_stride +
-                                ((slot ^ swz<D>(tt)) << 3);
-            load_lds16(kg + off, kl + inst * 512);
-        }
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, ld_off[j], kl + (wave * C::LPW + j) * 512);
 #pragma unroll
-        for (int j = 0; j < C::LPW; ++j) {
-            const int inst = wave * C::LPW + j;
-            const int e = inst * 64 + lane;
-            const int tt = e / C::CH, slot = e % C::CH;
-            const int64_t off = static_cast<int64_t>(tok0 + min(tt, cnt - 1)) * tok_stride +
-                                ((slot ^ swz<D>(tt)) << 3);
-            load_lds16(vg + off, vl + inst * 512);
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(vg, ld_off[j], vl + (wave * C::LPW + j) * 512);
+        } else {
+            uint32_t off[C::LPW];
+#pragma unroll
+            for (int j = 0; j < C::LPW; ++j)
+                off[j] = static_cast<uint32_t>((min(ld_tok[j], cnt - 1) * tok_stride + ld_chk[j]) * 2);
+#pragma unroll
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, off[j], kl + (wave * C::LPW + j) * 512);
+#pragma unroll
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(vg, off[j], vl + (wave * C::LPW + j) * 512);
         }
     };
+    auto stage_k = [&](int t) -> const uint16_t * { return ring + (t % kStages) * 2 * C::TILE; };
 
-    float m_run[2] = {-INFINITY, -INFINITY};      // running max, log2 units
-    float l_run[2] = {0.f, 0.f};                  // this lane's share of the row sum
+    // Per-lane LDS read offsets inside a tile.  The swizzle of row t depends
+    // on t mod 16 only, so the 32-token half (K) and the 16-token k-step (V)
+    // add compile-time offsets to these.
+    int koff[C::KK];
+#pragma unroll
+    for (int kk = 0; kk < C::KK; ++kk) koff[kk] = kv_elem<D>(l32, kk * 16 + h2 * 8);
+    const int tA = 4 * h2 + (l16 >> 2);
+    const int dA = 16 * g16 + 4 * (l16 & 3);
+    int voff[2][C::DT];
+#pragma unroll
+    for (int sel = 0; sel < 2; ++sel)
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt) voff[sel][dt] = C::TILE + kv_elem<D>(8 * sel + tA, 32 * dt + dA);
+
+    // S^T of the 32-token half tm of the tile in stage kl: sc[tn][v] is token
+    // 32 tm + 8 (v/4) + 4 h2 + v%4 of row tn*32 + l32
+    auto scores = [&](const uint16_t *kl, int tm, f32x16 (&sc)[2]) {
+        sc[0] = f32x16{};
+        sc[1] = f32x16{};
+#pragma unroll
+        for (int kk = 0; kk < C::KK; ++kk) {
+            const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kl + koff[kk] + 32 * tm * D);
+            sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][kk], sc[0], 0, 0, 0);
+            sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[1][kk], sc[1], 0, 0, 0);
+        }
+    };
+    // tokens past the tile's count, and suffix tokens after a row's own
+    // position: a row sees the first vis tokens of the tile
+    auto mask = [&](f32x16 (&sc)[2], int tm, int t) {
+        const int tok0 = tile_tok0(t), cnt = tile_cnt(t);
+#pragma unroll
+        for (int tn = 0; tn < 2; ++tn) {
+            const int vis = (t < np ? cnt : min(cnt, lim[tn] - tok0 + 1)) - 32 * tm - 4 * h2;
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                sc[tn][v] = 8 * (v >> 2) + (v & 3) < vis ? sc[tn][v] : -INFINITY;
+        }
+    };
+    auto masked_tile = [&](int t) {
+        return tile_cnt(t) < kBN || (t >= np && tile_tok0(t) + kBN - 1 > base_pos + i_lo);
+    };
+    // O^T += V^T P^T over half tm.  Lane (l32, h2) needs V[16 ks + 4 h2 + 0..3]
+    // [32 dt + l32] and V[16 ks + 8 + 4 h2 + 0..3][32 dt + l32]: one transposing
+    // read each, source lane s of a 16-lane group pointing at token +s/4, d + 4 (s%4).
     f32x16 acc[C::DT][2];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
         for (int tn = 0; tn < 2; ++tn) acc[dt][tn] = f32x16{};
+    auto values = [&](const uint16_t *kl, int tm, const bf16x8 (&pb)[2][2]) {
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh) {
+            const int ks = 2 * tm + kh;
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt) {
+                const bf16x4 lo = lds_read_tr16(kl + voff[0][dt] + 16 * ks * D);
+                const bf16x4 hi = lds_read_tr16(kl + voff[1][dt] + 16 * ks * D);
+                const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                acc[dt][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[0][kh], acc[dt][0], 0, 0, 0);
+                acc[dt][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[1][kh], acc[dt][1], 0, 0, 0);
+            }
+        }
+    };
+
+    float m_ref[2] = {-INFINITY, -INFINITY};      // reference max per row, log2 units
+    float l_run[2] = {0.f, 0.f};                  // this lane's share of the row sum
+    float mx[2];                                  // the current half's row max, log2 units
     const float c2 = a.score_scale_log2;
+    f32x16 s_cur[2], s_next[2];
+
+    // One half-step (tile t, half h) on s_cur: mask, row max, and unless the
+    // max moved past the reference (then it returns false having changed
+    // nothing), the probabilities, the next half's scores and this half's
+    // value products.  Nothing here touches the accumulators with VALU work,
+    // so they stay in the MFMA accumulator registers.
+    auto step = [&](int t, int h) -> bool {
+        if (masked_tile(t)) mask(s_cur, h, t);
+        bool mv = false;
+#pragma unroll
+        for (int tn = 0; tn < 2; ++tn) {
+            float m = -INFINITY;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) m = fmaxf(m, s_cur[tn][v]);
+            mx[tn] = fmaxf(m, __shfl_xor(m, 32, 64)) * c2;
+            mv |= mx[tn] > m_ref[tn] + kRescaleLog2;
+        }
+        if (__any(mv)) return false;
+        if (h == 1 && t + 1 < ntiles) {
+            // tile t+1 must have landed (only tile t+2's loads may be in flight);
+            // the barrier also frees stage (t+3) % 4, last read for tile t-1
+            if (t + 2 < ntiles) wait_vm<2 * C::LPW>();
+            else wait_vm<0>();
+            barrier();
+            if (t + 3 < ntiles) issue(t + 3);
+        }
+        // probabilities as bf16 (the operand of the value MFMA); the row sum
+        // in fp32, so lse keeps fp32 accuracy
+        bf16x8 pb[2][2];
+#pragma unroll
+        for (int tn = 0; tn < 2; ++tn) {
+            float ps = 0.f;
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float p = fast_exp2(fmaf(s_cur[tn][8 * kh + e], c2, -m_ref[tn]));
+                    ps += p;
+                    pb[tn][kh][e] = static_cast<__bf16>(p);
+                }
+            l_run[tn] += ps;
+        }
+        // the next half's scores: tile t's second half, or tile t+1's first
+        // (past the last tile this reads a stale stage; the result is unused)
+        scores(stage_k(h == 0 ? t : t + 1), h == 0 ? 1 : 0, s_next);
+        values(stage_k(t), h, pb);
+        s_cur[0] = s_next[0];
+        s_cur[1] = s_next[1];
+        return true;
+    };
 
     issue(0);
     if (ntiles > 1) issue(1);
-    for (int t = 0; t < ntiles; ++t) {
-        // tile t has landed once only tile t+1's loads may still be in flight;
-        // the barrier also frees stage (t+2) % 3, last read for tile t-1
-        if (t + 1 < ntiles) wait_vm<2 * C::LPW>();
-        else wait_vm<0>();
-        barrier();
-        if (t + 2 < ntiles) issue(t + 2);
-        const uint16_t *kl = ring + (t % kStages) * 2 * C::TILE;
-        const uint16_t *vl = kl + C::TILE;
-        const bool pre = t < np;
-        const int tok0 = (pre ? t : t - np) * kBN;
-        const int cnt = min(kBN, (pre ? it.Lp : suf_ctx) - tok0);
+    if (ntiles > 2) issue(2);
+    if (ntiles > 2) wait_vm<4 * C::LPW>();
+    else if (ntiles > 1) wait_vm<2 * C::LPW>();
+    else wait_vm<0>();
+    barrier();
+    scores(stage_k(0), 0, s_cur);
 
-        // S^T: sc[tm][tn][v] is token 32 tm + 8 (v/4) + 4 h2 + v%4 of row tn*32 + l32
-        f32x16 sc[2][2];
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm)
-#pragma unroll
-            for (int tn = 0; tn < 2; ++tn) sc[tm][tn] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < C::KK; ++kk) {
-            const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(kl + kv_elem<D>(l32, kk * 16 + h2 * 8));
-            const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(kl + kv_elem<D>(32 + l32, kk * 16 + h2 * 8));
-            sc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[0][kk], sc[0][0], 0, 0, 0);
-            sc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[1][kk], sc[0][1], 0, 0, 0);
-            sc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[0][kk], sc[1][0], 0, 0, 0);
-            sc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[1][kk], sc[1][1], 0, 0, 0);
+    int t = 0, h_start = 0;
+    for (;;) {
+        bool bail = false;
+        for (; t < ntiles; ++t) {
+            if (h_start == 0 && !step(t, 0)) { bail = true; break; }
+            if (!step(t, 1)) { h_start = 1; bail = true; break; }
+            h_start = 0;
         }
-        // tokens past the tile, and suffix tokens after a row's own position
-        if (cnt < kBN || (!pre && tok0 + kBN - 1 > base_pos + i_lo)) {
-#pragma unroll
-            for (int tm = 0; tm < 2; ++tm)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int tok = 32 * tm + 8 * (v >> 2) + 4 * h2 + (v & 3);
-#pragma unroll
-                    for (int tn = 0; tn < 2; ++tn) {
-                        const bool vis = tok < cnt && (pre || tok0 + tok <= lim[tn]);
-                        if (!vis) sc[tm][tn][v] = -INFINITY;
-                    }
-                }
-        }
-        // online softmax; pb[tn][ks] slot e (of lane half h2) is token
-        // 16 ks + 8 (e/4) + 4 h2 + e%4, i.e. score sc[ks/2][tn][8 (ks%2) + e]
-        bf16x8 pb[2][4];
-        float alpha[2];
+        if (!bail) break;
+        // A row's max moved by more than the threshold (always on the first
+        // half-step): move the reference to the new max and rescale what the
+        // row has accumulated, then redo the step.
+        float al[2];
 #pragma unroll
         for (int tn = 0; tn < 2; ++tn) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int tm = 0; tm < 2; ++tm)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[tm][tn][v]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float m_new = fmaxf(m_run[tn], mx * c2);
-            const float m_use = m_new == -INFINITY ? 0.f : m_new;
-            alpha[tn] = fast_exp2(m_run[tn] - m_use);
-            m_run[tn] = m_new;
-            float ps = 0.f;
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float p = fast_exp2(fmaf(sc[ks >> 1][tn][8 * (ks & 1) + e], c2, -m_use));
-                    ps += p;
-                    pb[tn][ks][e] = static_cast<__bf16>(p);
-                }
-            l_run[tn] = l_run[tn] * alpha[tn] + ps;
+            const bool up = mx[tn] > m_ref[tn] + kRescaleLog2;
+            const float m_new = up ? mx[tn] : m_ref[tn];
+            al[tn] = up ? fast_exp2(m_ref[tn] - m_new) : 1.f;
+            m_ref[tn] = m_new;
+            l_run[tn] *= al[tn];
         }
-        // the running max rarely moves after the first tiles: rescale only when
-        // it moved for some row of the wave
-        if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
 #pragma unroll
-            for (int dt = 0; dt < C::DT; ++dt) {
-                acc[dt][0] *= alpha[0];
-                acc[dt][1] *= alpha[1];
-            }
-        }
-        // O^T += V^T P^T.  Lane (l32, h2) needs V[16 ks + 4 h2 + 0..3][32 dt + l32]
-        // and V[16 ks + 8 + 4 h2 + 0..3][32 dt + l32]: one transposing read each,
-        // source lane s of a 16-lane group pointing at token +s/4, d + 4 (s%4).
-        const int tA = 4 * h2 + (l16 >> 2);
-        const int dA = 16 * g16 + 4 * (l16 & 3);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-            for (int dt = 0; dt < C::DT; ++dt) {
-                const bf16x4 lo = lds_read_tr16(vl + kv_elem<D>(16 * ks + tA, 32 * dt + dA));
-                const bf16x4 hi = lds_read_tr16(vl + kv_elem<D>(16 * ks + 8 + tA, 32 * dt + dA));
-                const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                acc[dt][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[0][ks], acc[dt][0], 0, 0, 0);
-                acc[dt][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[1][ks], acc[dt][1], 0, 0, 0);
-            }
+        for (int dt = 0; dt < C::DT; ++dt) {
+            acc[dt][0] *= al[0];
+            acc[dt][1] *= al[1];
         }
     }
 
@@ -267,7 +335,7 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
                     for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[dt][tn][4 * q4 + e] * inv);
                     *reinterpret_cast<bf16x4 *>(o + 32 * dt + 8 * q4) = w;
                 }
-            if (h2 == 0 && a.lse) a.lse[orow] = (m_run[tn] + fast_log2(l)) * kLn2;
+            if (h2 == 0 && a.lse) a.lse[orow] = (m_ref[tn] + fast_log2(l)) * kLn2;
         }
     }
 }

@@ -24,6 +24,20 @@ __device__ __forceinline__ void load_lds16(const uint16_t *g, uint16_t *l) {
         : "memory", "m0");
 }
 
+// The same with a wave-uniform base in SGPRs and a per-lane 32-bit byte offset
+// (the global_load_lds "saddr" form): no 64-bit address arithmetic per lane.
+__device__ __forceinline__ void load_lds16_s(const void *base, uint32_t voff, uint16_t *l) {
+    typedef __attribute__((address_space(3))) uint16_t lds_u16;
+    const uint32_t lds_addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l)));
+    asm volatile(
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, %1"
+        :
+        : "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+        : "memory", "m0");
+}
+
 // Wait until at most N vector-memory operations of this wave are outstanding.
 // The global->LDS loads are tracked by this counter; the compiler does not see
 // when their LDS bytes are read, so the waits are explicit.
