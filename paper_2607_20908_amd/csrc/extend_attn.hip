@@ -27,17 +27,21 @@
 namespace rlk {
 namespace {
 
-constexpr int kThreads = 256;
 constexpr int kBN = 64;        // KV tokens per tile
 constexpr int kStages = 4;     // LDS ring depth
 
-template <int D>
+// NT: 32-row MFMA column tiles per wave; the workgroup's 256 rows take 8 / NT
+// waves.
+template <int D, int NT>
 struct ECfg {
+    static constexpr int WAVES = 8 / NT;
+    static constexpr int THREADS = 64 * WAVES;
     static constexpr int CH = D / 8;              // 16-byte chunks per token row
     static constexpr int TILE = kBN * D;          // bf16 elements of one K or V tile
     static constexpr int KK = D / 16;             // k-steps of S^T = K Q^T
     static constexpr int DT = D / 32;             // 32-wide d tiles of O^T
-    static constexpr int LPW = TILE / 512 / 4;    // 1 KB direct loads per wave per tensor per tile
+    static constexpr int LPW = TILE / 512 / WAVES;  // 1 KB direct loads per wave per tensor per tile
+    static_assert(LPW >= 1 && LPW * 512 * WAVES == TILE, "load split");
 };
 
 // Chunk swizzle of token row t.  D = 128: rows are 256 bytes (one window of
@@ -66,9 +70,9 @@ __device__ __forceinline__ int kv_elem(int t, int d) {
 // really moves, and out = acc / l and lse = m + log2 l are unchanged.
 constexpr float kRescaleLog2 = 8.f;
 
-template <int D>
-__global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) {
-    using C = ECfg<D>;
+template <int D, int NT>
+__global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArgs a) {
+    using C = ECfg<D, NT>;
     __shared__ __attribute__((aligned(16))) uint16_t ring[kStages * 2 * C::TILE];
 
     const ExtItem it = a.items[blockIdx.x];
@@ -98,11 +102,11 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
     const uint16_t *vsuf = a.v_suffix + soff;
 
     // ---- this wave's query rows as MFMA B operands (Q^T, k = d) -------------
-    bf16x8 qf[2][C::KK];
-    int lim[2];                                   // last visible suffix position per row
+    bf16x8 qf[NT][C::KK];
+    int lim[NT];                                  // last visible suffix position per row
 #pragma unroll
-    for (int tn = 0; tn < 2; ++tn) {
-        const int row = wave * 64 + tn * 32 + l32;
+    for (int tn = 0; tn < NT; ++tn) {
+        const int row = wave * 32 * NT + tn * 32 + l32;
         const bool ok = row < rows;
         const int u = it.row_begin + (ok ? row : rows - 1);
         const int i = u / r, hr = u - i * r;
@@ -174,22 +178,23 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
 
     // S^T of the 32-token half tm of the tile in stage kl: sc[tn][v] is token
     // 32 tm + 8 (v/4) + 4 h2 + v%4 of row tn*32 + l32
-    auto scores = [&](const uint16_t *kl, int tm, f32x16 (&sc)[2]) {
-        sc[0] = f32x16{};
-        sc[1] = f32x16{};
+    auto scores = [&](const uint16_t *kl, int tm, f32x16 (&sc)[NT]) {
+#pragma unroll
+        for (int tn = 0; tn < NT; ++tn) sc[tn] = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < C::KK; ++kk) {
             const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kl + koff[kk] + 32 * tm * D);
-            sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][kk], sc[0], 0, 0, 0);
-            sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[1][kk], sc[1], 0, 0, 0);
+#pragma unroll
+            for (int tn = 0; tn < NT; ++tn)
+                sc[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[tn][kk], sc[tn], 0, 0, 0);
         }
     };
     // tokens past the tile's count, and suffix tokens after a row's own
     // position: a row sees the first vis tokens of the tile
-    auto mask = [&](f32x16 (&sc)[2], int tm, int t) {
+    auto mask = [&](f32x16 (&sc)[NT], int tm, int t) {
         const int tok0 = tile_tok0(t), cnt = tile_cnt(t);
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) {
+        for (int tn = 0; tn < NT; ++tn) {
             const int vis = (t < np ? cnt : min(cnt, lim[tn] - tok0 + 1)) - 32 * tm - 4 * h2;
 #pragma unroll
             for (int v = 0; v < 16; ++v)
@@ -202,12 +207,12 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
     // O^T += V^T P^T over half tm.  Lane (l32, h2) needs V[16 ks + 4 h2 + 0..3]
     // [32 dt + l32] and V[16 ks + 8 + 4 h2 + 0..3][32 dt + l32]: one transposing
     // read each, source lane s of a 16-lane group pointing at token +s/4, d + 4 (s%4).
-    f32x16 acc[C::DT][2];
+    f32x16 acc[C::DT][NT];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) acc[dt][tn] = f32x16{};
-    auto values = [&](const uint16_t *kl, int tm, const bf16x8 (&pb)[2][2]) {
+        for (int tn = 0; tn < NT; ++tn) acc[dt][tn] = f32x16{};
+    auto values = [&](const uint16_t *kl, int tm, const bf16x8 (&pb)[NT][2]) {
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh) {
             const int ks = 2 * tm + kh;
@@ -216,17 +221,22 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
                 const bf16x4 lo = lds_read_tr16(kl + voff[0][dt] + 16 * ks * D);
                 const bf16x4 hi = lds_read_tr16(kl + voff[1][dt] + 16 * ks * D);
                 const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                acc[dt][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[0][kh], acc[dt][0], 0, 0, 0);
-                acc[dt][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[1][kh], acc[dt][1], 0, 0, 0);
+#pragma unroll
+                for (int tn = 0; tn < NT; ++tn)
+                    acc[dt][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[tn][kh], acc[dt][tn], 0, 0, 0);
             }
         }
     };
 
-    float m_ref[2] = {-INFINITY, -INFINITY};      // reference max per row, log2 units
-    float l_run[2] = {0.f, 0.f};                  // this lane's share of the row sum
-    float mx[2];                                  // the current half's row max, log2 units
+    float m_ref[NT], l_run[NT];                   // reference max (log2 units); this lane's
+    float mx[NT];                                 // share of the row sum; the half's row max
+#pragma unroll
+    for (int tn = 0; tn < NT; ++tn) {
+        m_ref[tn] = -INFINITY;
+        l_run[tn] = 0.f;
+    }
     const float c2 = a.score_scale_log2;
-    f32x16 s_cur[2], s_next[2];
+    f32x16 s_cur[NT], s_next[NT];
 
     // One half-step (tile t, half h) on s_cur: mask, row max, and unless the
     // max moved past the reference (then it returns false having changed
@@ -237,7 +247,7 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
         if (masked_tile(t)) mask(s_cur, h, t);
         bool mv = false;
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) {
+        for (int tn = 0; tn < NT; ++tn) {
             float m = -INFINITY;
 #pragma unroll
             for (int v = 0; v < 16; ++v) m = fmaxf(m, s_cur[tn][v]);
@@ -255,9 +265,9 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
         }
         // probabilities as bf16 (the operand of the value MFMA); the row sum
         // in fp32, so lse keeps fp32 accuracy
-        bf16x8 pb[2][2];
+        bf16x8 pb[NT][2];
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) {
+        for (int tn = 0; tn < NT; ++tn) {
             float ps = 0.f;
 #pragma unroll
             for (int kh = 0; kh < 2; ++kh)
@@ -273,8 +283,8 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
         // (past the last tile this reads a stale stage; the result is unused)
         scores(stage_k(h == 0 ? t : t + 1), h == 0 ? 1 : 0, s_next);
         values(stage_k(t), h, pb);
-        s_cur[0] = s_next[0];
-        s_cur[1] = s_next[1];
+#pragma unroll
+        for (int tn = 0; tn < NT; ++tn) s_cur[tn] = s_next[tn];
         return true;
     };
 
@@ -299,9 +309,9 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
         // A row's max moved by more than the threshold (always on the first
         // half-step): move the reference to the new max and rescale what the
         // row has accumulated, then redo the step.
-        float al[2];
+        float al[NT];
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) {
+        for (int tn = 0; tn < NT; ++tn) {
             const bool up = mx[tn] > m_ref[tn] + kRescaleLog2;
             const float m_new = up ? mx[tn] : m_ref[tn];
             al[tn] = up ? fast_exp2(m_ref[tn] - m_new) : 1.f;
@@ -309,17 +319,16 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
             l_run[tn] *= al[tn];
         }
 #pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt) {
-            acc[dt][0] *= al[0];
-            acc[dt][1] *= al[1];
-        }
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+            for (int tn = 0; tn < NT; ++tn) acc[dt][tn] *= al[tn];
     }
 
     // ---- normalise and write: acc[dt][tn][v] is d = 32 dt + 8 (v/4) + 4 h2 + v%4
 #pragma unroll
-    for (int tn = 0; tn < 2; ++tn) {
+    for (int tn = 0; tn < NT; ++tn) {
         const float l = l_run[tn] + __shfl_xor(l_run[tn], 32, 64);
-        const int row = wave * 64 + tn * 32 + l32;
+        const int row = wave * 32 * NT + tn * 32 + l32;
         if (row < rows) {
             const int u = it.row_begin + row;
             const int i = u / r, hr = u - i * r;
@@ -340,11 +349,15 @@ __global__ __launch_bounds__(kThreads, 1) void extend_attn_kernel(ExtendArgs a) 
     }
 }
 
+// One 32-row column tile per wave, 8 waves: two waves per SIMD, so one
+// wave's softmax and LDS waits overlap the other's MFMAs.
+constexpr int kNT = 1;
+
 template <int D>
 hipError_t launch_extend_d(const ExtendArgs &a, hipStream_t stream) {
     if (a.n_items == 0) return hipSuccess;
-    hipLaunchKernelGGL(extend_attn_kernel<D>, dim3(static_cast<uint32_t>(a.n_items)), dim3(kThreads), 0, stream,
-                       a);
+    hipLaunchKernelGGL((extend_attn_kernel<D, kNT>), dim3(static_cast<uint32_t>(a.n_items)),
+                       dim3(ECfg<D, kNT>::THREADS), 0, stream, a);
     return hipGetLastError();
 }
 
