@@ -316,8 +316,14 @@ def main():
             hip.record(ev[k][j][1], sh)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    op_ms = {name: float(np.mean([hip.elapsed_ms(*ev[k][j]) for k in range(args.steps)]))
-             for j, (name, _) in enumerate(ops)}
+    # per-operation duration: the median over the timed steps (p10 and p90
+    # reported beside it).  The first step's interval also holds the host's
+    # planning of that call, since the GPU has drained before the timed region.
+    op_all = {name: np.array([hip.elapsed_ms(*ev[k][j]) for k in range(args.steps)])
+              for j, (name, _) in enumerate(ops)}
+    op_ms = {name: float(np.median(v)) for name, v in op_all.items()}
+    op_pct = {name: [round(float(np.percentile(v, 10)), 4), round(float(np.percentile(v, 90)), 4)]
+              for name, v in op_all.items()}
     for pair in (p for row in ev for p in row):
         for e in pair:
             hip.destroy(e)
@@ -488,6 +494,7 @@ def main():
         gbs = nbytes / (op_ms["decode"] * 1e-3) / 1e9
         res.update({"metric": "decode-attn effective KV GB/s (% HBM peak)", "value": round(gbs, 1),
                     "unit": "GB/s", "decode_ms": round(op_ms["decode"], 4),
+                    "decode_ms_p10_p90": op_pct["decode"],
                     "decode_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
                     "decode_algorithmic_bytes": nbytes})
         rooflines.append((op_ms["decode"], {"kernel": "decode attention (split + combine kernels)",
@@ -498,7 +505,8 @@ def main():
     if y is not None:
         fl = lmhead_flops(y.cfg)
         tf = fl / (op_ms["lmhead"] * 1e-3) / 1e12
-        res.update({"lmhead_ms": round(op_ms["lmhead"], 4), "lmhead_tflops": round(tf, 1),
+        res.update({"lmhead_ms": round(op_ms["lmhead"], 4), "lmhead_ms_p10_p90": op_pct["lmhead"],
+                    "lmhead_tflops": round(tf, 1),
                     "lmhead_mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "lmhead_flops": fl})
         if x is None:
             res.update({"metric": "lm-head logprob TFLOP/s (% MFMA)", "value": round(tf, 1),

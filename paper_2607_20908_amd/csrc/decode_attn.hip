@@ -1,12 +1,14 @@
 // Prefix-shared split-K decode attention for gfx950.
 //
 // One workgroup (4 wave64s) runs one work item: a chunk of KV tokens of one
-// unit at one kv head, serving `rows` query rows:
-//   prefix item: the prompt's KV, for all G*r query rows of its candidates
-//                (r = Hq/Hkv), so the chunk crosses HBM once per group;
+// unit at one kv head, serving up to 64 query rows:
+//   prefix item: the prompt's KV, for the G*r query rows of its candidates
+//                (r = Hq/Hkv; wider groups take one item per 64 rows), so the
+//                chunk crosses HBM once per group of up to 64 rows;
 //   suffix item: one candidate's own KV, for its r query rows.
-// The KV chunk streams through LDS in tiles of 64 tokens (coalesced 16-byte
-// loads, double-buffered, register prefetch of the next tile).  Per 16-token
+// The KV chunk streams through LDS in tiles of 64 tokens: coalesced 16-byte
+// loads into registers one tile ahead and a single LDS stage, so three
+// workgroups fit on a CU, each with a tile's loads in flight.  Per 16-token
 // sub-tile a wave computes scores S^T = K Q^T on MFMA 16x16x32 (tokens on the
 // M side, query rows on the N side), keeps an online softmax per query row in
 // fp32, rounds the probabilities to bf16 and accumulates O^T = V^T P^T on
@@ -23,6 +25,9 @@ namespace rlk {
 namespace {
 
 constexpr int kThreads = 256;
+// Three workgroups per CU (LDS: one ~36 KB stage each; registers: at most 168
+// per lane), each with one tile's loads in flight.
+constexpr int kSplitBlocksPerCU = 3;
 constexpr int kSub = 16;                          // tokens per MFMA sub-tile
 constexpr int kSubPerTile = kTileTokens / kSub;   // 4
 
@@ -38,10 +43,10 @@ struct DCfg {
     static constexpr int STAGE = TILE + TILEV;       // one K tile followed by one V tile
     static constexpr int LD = kTileTokens * CH / kThreads;  // 16-byte chunks per thread per tensor
     static constexpr int RED_STRIDE = D + 1;     // fp32 row stride of the merge area (bank spread)
-    static constexpr int KV_BYTES = 2 * STAGE * 2;                     // 2 buffers x (K, V)
-    static constexpr int RED_BYTES = 4 * 2 * 16 * RED_STRIDE * 4;      // waves x ct x 16 rows
+    static constexpr int KV_BYTES = STAGE * 2;                         // one LDS stage (K, V)
+    static constexpr int RED_BYTES = 4 * 16 * RED_STRIDE * 4;          // waves x 16 rows
     static constexpr int MAIN_BYTES = KV_BYTES > RED_BYTES ? KV_BYTES : RED_BYTES;
-    static constexpr int ML_BYTES = 4 * 2 * 16 * 2 * 4;
+    static constexpr int ML_BYTES = 4 * 16 * 2 * 4;
 };
 
 // Element offset of 16-byte chunk c of token t inside a K tile.  Rows are
@@ -62,17 +67,18 @@ __device__ __forceinline__ int v_off(int t, int c) {
     return t * DCfg<D>::LDRV + (c << 3);
 }
 
-// MAXC: column tiles (16 query rows each) per wave; 1 serves items of up to
-// 64 query rows, 2 serves up to 128.
-template <int D, int MAXC>
-__global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a, int item0) {
+// Items serve at most 64 query rows: 4 MFMA column tiles of 16, one per wave.
+// Items of up to 16 rows split each tile's 4 sub-tiles over the 4 waves, items
+// of up to 32 rows over 2; those waves' partials are merged through LDS.
+template <int D>
+__global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kernel(DecodeArgs a) {
     using C = DCfg<D>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::MAIN_BYTES + C::ML_BYTES];
     uint16_t *kv = reinterpret_cast<uint16_t *>(smem);
     float *red_acc = reinterpret_cast<float *>(smem);
     float *red_ml = reinterpret_cast<float *>(smem + C::MAIN_BYTES);
 
-    const DevItem it = a.items[item0 + blockIdx.x];
+    const DevItem it = a.items[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g4 = lane >> 4, l16 = lane & 15;
     const int kh = it.kind_kh & 0xffff;
@@ -84,7 +90,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
     const int Wt = 4 / Wc;
     const int nst = kSubPerTile / Wt;            // sub-tiles per wave per tile
     const int wc = wave % Wc, wt = wave / Wc;
-    const int n_my = (wc < n_ct ? 1 : 0) + (MAXC > 1 && wc + Wc < n_ct ? 1 : 0);
+    const bool mine = wc < n_ct;                 // this wave has a column tile
     const int ntok = it.ntok;
     // token-major [rows, Hkv, D]: rows of one kv head are Hkv*D apart;
     // head-major [Hkv, rows, D]: they are contiguous
@@ -96,11 +102,10 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
     const uint16_t *vg = (is_suffix ? a.v_suffix : a.v_prefix) + base;
 
     // ---- query rows of this wave as MFMA B operands (Q^T, k = d) ----------
-    bf16x8 qb[MAXC][C::KK];
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-        const int i = (wc + c * Wc) * 16 + l16;      // row within the item
-        const bool ok = c < n_my && i < rows;
+    bf16x8 qb[C::KK];
+    {
+        const int i = wc * 16 + l16;                 // row within the item
+        const bool ok = mine && i < rows;
         int64_t qoff = 0;
         if (ok) {
             const int ig = it.row_begin + i;         // row within the unit
@@ -111,23 +116,16 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
         }
 #pragma unroll
         for (int kk = 0; kk < C::KK; ++kk) {
-            if (ok) qb[c][kk] = *reinterpret_cast<const bf16x8 *>(a.q + qoff + kk * 32 + g4 * 8);
-            else    qb[c][kk] = bf16x8{};
+            if (ok) qb[kk] = *reinterpret_cast<const bf16x8 *>(a.q + qoff + kk * 32 + g4 * 8);
+            else    qb[kk] = bf16x8{};
         }
     }
 
     // ---- online softmax state --------------------------------------------
-    float m_run[MAXC], l_run[MAXC];           // l_run: this lane's share of the row sum
-    f32x4 acc[MAXC][C::DT];
+    float m_run = -INFINITY, l_run = 0.f;        // l_run: this lane's share of the row sum
+    f32x4 acc[C::DT];
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-        m_run[c] = -INFINITY;
-        l_run[c] = 0.f;
-    }
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-#pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt) acc[c][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int dt = 0; dt < C::DT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // ---- tile staging -----------------------------------------------------
     u32x4 kr[C::LD], vr[C::LD];
@@ -147,8 +145,8 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
             }
         }
     };
-    auto store_tile = [&](int buf) {
-        uint16_t *kl = kv + buf * C::STAGE;
+    auto store_tile = [&]() {
+        uint16_t *kl = kv;
         uint16_t *vl = kl + C::TILE;
 #pragma unroll
         for (int j = 0; j < C::LD; ++j) {
@@ -161,81 +159,67 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
 
     const int ntiles = (ntok + kTileTokens - 1) / kTileTokens;
     load_tile(0);
-    store_tile(0);
+    store_tile();
     if (ntiles > 1) load_tile(1);
     __syncthreads();
 
+    const uint16_t *kl = kv;
+    const uint16_t *vl = kl + C::TILE;
     for (int tile = 0; tile < ntiles; ++tile) {
-        const uint16_t *kl = kv + (tile & 1) * C::STAGE;
-        const uint16_t *vl = kl + C::TILE;
         const int t0 = tile * kTileTokens;
-        if (n_my > 0) {
+        if (mine) {
             // scores of my sub-tiles, log2 units, masked past the chunk end
-            float sc[MAXC][kSubPerTile][4];
+            float sc[kSubPerTile][4];
 #pragma unroll
             for (int k = 0; k < kSubPerTile; ++k) {
                 if (k < nst) {
                     const int st = wt + k * Wt;
-                    f32x4 s[MAXC];
-#pragma unroll
-                    for (int c = 0; c < MAXC; ++c) s[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    f32x4 sv = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int kk = 0; kk < C::KK; ++kk) {
                         const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(
                             kl + kv_off<D>(st * kSub + l16, kk * 4 + g4));
-                        s[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[0][kk], s[0], 0, 0, 0);
-                        if (MAXC > 1 && n_my > 1)
-                            s[MAXC - 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[MAXC - 1][kk],
-                                                                                  s[MAXC - 1], 0, 0, 0);
+                        sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[kk], sv, 0, 0, 0);
                     }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const bool valid = t0 + st * kSub + g4 * 4 + i < ntok;
-#pragma unroll
-                        for (int c = 0; c < MAXC; ++c)
-                            sc[c][k][i] = valid ? s[c][i] * a.score_scale_log2 : -INFINITY;
+                        sc[k][i] = valid ? sv[i] * a.score_scale_log2 : -INFINITY;
                     }
                 } else {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
-#pragma unroll
-                        for (int c = 0; c < MAXC; ++c) sc[c][k][i] = -INFINITY;
+                    for (int i = 0; i < 4; ++i) sc[k][i] = -INFINITY;
                 }
             }
-            // online softmax update per column tile, probabilities to bf16
-            bf16x4 pb[MAXC][kSubPerTile];
+            // online softmax update, probabilities to bf16
+            bf16x4 pb[kSubPerTile];
+            float mx = -INFINITY;
 #pragma unroll
-            for (int c = 0; c < MAXC; ++c) {
-                if (c < n_my) {
-                    float mx = -INFINITY;
+            for (int k = 0; k < kSubPerTile; ++k)
 #pragma unroll
-                    for (int k = 0; k < kSubPerTile; ++k)
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[k][i]);
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float m_new = fmaxf(m_run, mx);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = fast_exp2(m_run - m_use);
+            m_run = m_new;
+            float psum = 0.f;
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[c][k][i]);
-                    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-                    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-                    const float m_new = fmaxf(m_run[c], mx);
-                    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-                    const float alpha = fast_exp2(m_run[c] - m_use);
-                    m_run[c] = m_new;
-                    float psum = 0.f;
+            for (int k = 0; k < kSubPerTile; ++k) {
 #pragma unroll
-                    for (int k = 0; k < kSubPerTile; ++k) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float p = fast_exp2(sc[c][k][i] - m_use);
-                            psum += p;
-                            pb[c][k][i] = static_cast<__bf16>(p);
-                        }
-                    }
-                    l_run[c] = l_run[c] * alpha + psum;
-                    // the running max rarely moves after the first tiles: skip the
-                    // rescale when it stayed put for every row of the wave
-                    if (__any(alpha != 1.f)) {
-#pragma unroll
-                        for (int dt = 0; dt < C::DT; ++dt) acc[c][dt] *= alpha;
-                    }
+                for (int i = 0; i < 4; ++i) {
+                    const float p = fast_exp2(sc[k][i] - m_use);
+                    psum += p;
+                    pb[k][i] = static_cast<__bf16>(p);
                 }
+            }
+            l_run = l_run * alpha + psum;
+            // the running max rarely moves after the first tiles: skip the
+            // rescale when it stayed put for every row of the wave
+            if (__any(alpha != 1.f)) {
+#pragma unroll
+                for (int dt = 0; dt < C::DT; ++dt) acc[dt] *= alpha;
             }
             // O^T += V^T P^T; lane (g4, l16) needs the 4 tokens st*16 + 4*g4 + 0..3
             // at d = dt*16 + l16, which one transposing read delivers when source
@@ -249,54 +233,61 @@ __global__ __launch_bounds__(kThreads, 2) void decode_split_kernel(DecodeArgs a,
 #pragma unroll
                     for (int dt = 0; dt < C::DT; ++dt) vt[dt] = lds_read_tr16(vsrc + dt * 16);
 #pragma unroll
-                    for (int dt = 0; dt < C::DT; ++dt) {
-                        const bf16x4 va = vt[dt];
-                        acc[0][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0][k], acc[0][dt], 0, 0, 0);
-                        if (MAXC > 1 && n_my > 1)
-                            acc[MAXC - 1][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-                                va, pb[MAXC - 1][k], acc[MAXC - 1][dt], 0, 0, 0);
-                    }
+                    for (int dt = 0; dt < C::DT; ++dt)
+                        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[dt], pb[k], acc[dt], 0, 0, 0);
                 }
             }
         }
-        if (tile + 1 < ntiles) {
-            store_tile((tile + 1) & 1);
-            if (tile + 2 < ntiles) load_tile(tile + 2);
-        }
+        // one LDS stage: once every wave has read it, tile+1 moves in from the
+        // registers and tile+2's loads are issued
         __syncthreads();
+        if (tile + 1 < ntiles) {
+            store_tile();
+            if (tile + 2 < ntiles) load_tile(tile + 2);
+            __syncthreads();
+        }
     }
 
-    // ---- merge the waves' partials (same rows, disjoint tokens) ------------
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-        l_run[c] += __shfl_xor(l_run[c], 16, 64);
-        l_run[c] += __shfl_xor(l_run[c], 32, 64);
-    }
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-        if (c < n_my) {
-            const int slot = (wave * 2 + c) * 16 + l16;
-            if (lane < 16) {
-                red_ml[slot * 2 + 0] = m_run[c];
-                red_ml[slot * 2 + 1] = l_run[c];
-            }
+    // ---- the item's partials ------------------------------------------------
+    l_run += __shfl_xor(l_run, 16, 64);
+    l_run += __shfl_xor(l_run, 32, 64);
+    if (Wt == 1) {
+        // every row belongs to one wave: write its partial from the registers
+        const int i = wc * 16 + l16;
+        if (mine && i < rows) {
+            const int64_t prow = it.partial_row0 + i;
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    red_acc[slot * C::RED_STRIDE + dt * 16 + g4 * 4 + i] = acc[c][dt][i];
+                *reinterpret_cast<f32x4 *>(a.pacc + prow * D + dt * 16 + g4 * 4) = acc[dt];
+            if (g4 == 0) {
+                a.pm[prow] = m_run;
+                a.pl[prow] = l_run;
+            }
         }
+        return;
+    }
+    // Wt waves hold partials of the same rows over disjoint tokens: merge them
+    // through LDS (the stage is free after the loop's last barrier)
+    {
+        const int slot = wave * 16 + l16;
+        if (lane < 16) {
+            red_ml[slot * 2 + 0] = m_run;
+            red_ml[slot * 2 + 1] = l_run;
+        }
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red_acc[slot * C::RED_STRIDE + dt * 16 + g4 * 4 + i] = acc[dt][i];
     }
     __syncthreads();
     for (int e = tid; e < rows * D; e += kThreads) {
         const int i = e / D, d = e % D;
         const int ct = i >> 4, q = i & 15;
-        const int wcx = ct % Wc, cl = ct / Wc;
         float Mx = -INFINITY;
-        for (int w = 0; w < Wt; ++w) Mx = fmaxf(Mx, red_ml[((wcx + w * Wc) * 2 + cl) * 32 + q * 2]);
+        for (int w = 0; w < Wt; ++w) Mx = fmaxf(Mx, red_ml[((ct + w * Wc) * 16 + q) * 2]);
         float L = 0.f, A = 0.f;
         for (int w = 0; w < Wt; ++w) {
-            const int slot = ((wcx + w * Wc) * 2 + cl) * 16 + q;
+            const int slot = (ct + w * Wc) * 16 + q;
             const float f = fast_exp2(red_ml[slot * 2] - Mx);
             L += f * red_ml[slot * 2 + 1];
             A += f * red_acc[slot * C::RED_STRIDE + d];
@@ -367,10 +358,8 @@ __global__ __launch_bounds__(kThreads) void plan_fetch_kernel(const u32x4 *__res
 
 template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
-    // The two-column-tile variant serves every item; with the LDS tile sizes
-    // both variants reach the same occupancy, so one launch covers all items.
     if (a.n_items > 0) {
-        hipLaunchKernelGGL((decode_split_kernel<D, 2>), dim3(a.n_items), dim3(kThreads), 0, stream, a, 0);
+        hipLaunchKernelGGL(decode_split_kernel<D>, dim3(a.n_items), dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -130,7 +130,7 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     // --- split sizes --------------------------------------------------------
     const int64_t Mp = G * r;                       // query rows per prefix unit
     const int64_t ncg = ceil_div(Mp, kMaxItemRows); // column groups per prefix chunk
-    if (r > kMaxItemRows) return fail(err, RL_ERR_UNSUPPORTED, "Hq/Hkv must be <= 128");
+    if (r > kMaxHeadsPerKv) return fail(err, RL_ERR_UNSUPPORTED, "Hq/Hkv must be <= 128");
     int64_t cs, cp;
     if (sh.split_tokens > 0) {
         cs = cp = sh.split_tokens;
@@ -150,7 +150,7 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     // --- unit tables; partial rows in unit order ------------------------------
     // A unit of L tokens splits into n = ceil(L / C) chunks of b = ceil(L / n)
     // tokens rounded up to 16 (the last one shorter), each chunk into
-    // ceil(M / 128) items of at most 128 query rows.
+    // ceil(M / kMaxItemRows) items of at most kMaxItemRows query rows.
     pl.prefix_units.assign(P * Hkv, DevUnit{0, 0, 0});
     pl.suffix_units.assign(S * Hkv, DevUnit{0, 0, 0});
     int64_t prow = 0, n_items = 0;

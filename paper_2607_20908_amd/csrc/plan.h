@@ -13,8 +13,10 @@
 namespace rlk {
 
 // Largest number of query rows one decode work item serves (16 per MFMA column
-// tile, at most 2 column tiles per wave, 4 waves).
-constexpr int kMaxItemRows = 128;
+// tile, one column tile per wave, 4 waves).
+constexpr int kMaxItemRows = 64;
+// Largest Hq / Hkv the decode path accepts.
+constexpr int kMaxHeadsPerKv = 128;
 // KV tokens staged per LDS tile in the split kernel.
 constexpr int kTileTokens = 64;
 // Vocabulary entries per lm-head work tile.

@@ -25,7 +25,7 @@ def check_cover(items, P, G, Hq, Hkv, lp, ls, split=None):
     r = Hq // Hkv
     S = P * G
     assert (items["tok_count"] >= 1).all()
-    assert (items["row_count"] >= 1).all() and (items["row_count"] <= 128).all()
+    assert (items["row_count"] >= 1).all() and (items["row_count"] <= 64).all()
     if split:
         assert (items["tok_count"] <= split).all()
     # exact coverage: every (kind, unit, kh, token, row) exactly once
@@ -71,12 +71,13 @@ def test_workload_plans_cover_and_balance():
             # enough items to spread over 256 compute units, none dominating
             assert len(items) >= 512, (name, len(items))
             assert c.max() <= 0.6 * c.sum() / 256, (name, c.max(), c.sum() / 256)
-    # the prefix is one pass per group for <= 128 query rows per kv head
+    # a prefix chunk serves its group's query rows in items of at most 64 rows:
+    # G*r = 16*8 = 128 rows -> two items per chunk, rows [0, 64) and [64, 128)
     cfg = W.DECODE_CONFIGS["32b"]
     items, _, _ = plan_for(cfg.num_prompts, cfg.group_size, cfg.num_q_heads, cfg.num_kv_heads,
                            cfg.head_dim, np.full(16, 2048), W.suffix_lengths(cfg, 0))
     pre = items[items["kind"] == 0]
-    assert (pre["row_count"] == 128).all() and (pre["row_begin"] == 0).all()
+    assert (pre["row_count"] == 64).all() and sorted(set(pre["row_begin"])) == [0, 64]
 
 
 @pytest.mark.parametrize("lengths", ["equal", "one_giant", "geometric", "zeros"])
@@ -105,11 +106,11 @@ def test_forced_split():
 
 
 def test_wide_groups_split_rows():
-    # G*r = 32*8 = 256 query rows per kv head -> two row blocks per prefix chunk
+    # G*r = 32*8 = 256 query rows per kv head -> four row blocks per prefix chunk
     items, lp, ls = plan_for(1, 32, 16, 2, 128, [300], np.full(32, 5))
     check_cover(items, 1, 32, 16, 2, lp, ls)
     pre = items[items["kind"] == 0]
-    assert sorted(set(pre["row_begin"])) == [0, 128]
+    assert sorted(set(pre["row_begin"])) == [0, 64, 128, 192]
 
 
 @settings(max_examples=60, deadline=None)
