@@ -324,17 +324,50 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) 
                               : su.base + static_cast<int64_t>(j - pu.nchunks) * a.r + hr;
     };
     float Mx = -INFINITY;
-    for (int j = lane; j < n; j += 64) Mx = fmaxf(Mx, a.pm[prow(j)]);
-    Mx = wave_max(Mx);
     float L = 0.f, o[PER_LANE];
 #pragma unroll
     for (int e = 0; e < PER_LANE; ++e) o[e] = 0.f;
-    for (int j = 0; j < n; ++j) {
-        const int64_t pr = prow(j);
-        const float f = fast_exp2(a.pm[pr] - Mx);
-        L += f * a.pl[pr];
+    if (n <= 64) {
+        // lane j holds partial j's (m, l): one load latency for all of them;
+        // the value rows then load 8 at a time, each weight taken by readlane
+        float mj = -INFINITY, lj = 0.f;
+        if (lane < n) {
+            const int64_t pr = prow(lane);
+            mj = a.pm[pr];
+            lj = a.pl[pr];
+        }
+        Mx = wave_max(mj);
+        const float fj = lane < n ? fast_exp2(mj - Mx) : 0.f;
+        L = wave_sum(fj * lj);
+        for (int j0 = 0; j0 < n; j0 += 8) {
+            float v[8][PER_LANE];
 #pragma unroll
-        for (int e = 0; e < PER_LANE; ++e) o[e] += f * a.pacc[pr * D + lane * PER_LANE + e];
+            for (int u = 0; u < 8; ++u) {
+                if (j0 + u < n) {
+                    const int64_t pr = prow(j0 + u);
+#pragma unroll
+                    for (int e = 0; e < PER_LANE; ++e) v[u][e] = a.pacc[pr * D + lane * PER_LANE + e];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                if (j0 + u < n) {
+                    const float f = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fj), j0 + u));
+#pragma unroll
+                    for (int e = 0; e < PER_LANE; ++e) o[e] += f * v[u][e];
+                }
+            }
+        }
+    } else {
+        for (int j = lane; j < n; j += 64) Mx = fmaxf(Mx, a.pm[prow(j)]);
+        Mx = wave_max(Mx);
+        for (int j = 0; j < n; ++j) {
+            const int64_t pr = prow(j);
+            const float f = fast_exp2(a.pm[pr] - Mx);
+            L += f * a.pl[pr];
+#pragma unroll
+            for (int e = 0; e < PER_LANE; ++e) o[e] += f * a.pacc[pr * D + lane * PER_LANE + e];
+        }
     }
     uint16_t *out = a.out + idx * D + lane * PER_LANE;
     if (n == 0) {
