@@ -3,7 +3,9 @@
 
 #include <algorithm>
 #include <cmath>
+#include <chrono>
 #include <cstring>
+#include <thread>
 #include <string>
 #include <vector>
 
@@ -29,16 +31,24 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // Pinned host staging for the work-list upload.  The slots are coherent,
 // device-mapped host memory that a small kernel on the caller's stream reads
 // directly (no copy-engine hand-off in front of the split kernel), so the host
-// never waits for the stream; each slot's event guards its reuse until the
-// kernel that read it has run.  The slots are never freed (plain thread-local
-// pointers, no destructors to run after the HIP runtime has shut down).
+// never waits for the stream.  A slot is reused once the kernel that read it
+// has run: the operation's last kernel stores the slot's sequence number into
+// a pinned word (no marker packet on the stream, which would hold the next
+// kernel back by a few microseconds), or, if that kernel did not launch, an
+// event recorded behind the fetch says so.  The slots are never freed (plain
+// thread-local pointers, no destructors to run after the HIP runtime has shut
+// down).
 struct StagingSlot {
     unsigned char *host;
     void *dev;                 // the same memory as the device sees it
     size_t cap;
     hipEvent_t done;
     int device;
-    bool pending;
+    bool pending;              // a kernel may still read the slot
+    bool by_flag;              // pending until *flag reaches expect (else until `done`)
+    uint64_t *flag;            // pinned word, stored into by the device
+    uint64_t *flag_dev;
+    uint64_t expect;
 };
 constexpr int kStagingSlots = 4;
 thread_local StagingSlot g_staging[kStagingSlots];
@@ -55,9 +65,15 @@ struct Section {
     size_t n;
 };
 
+thread_local StagingSlot *g_staged_slot;     // the slot of the last upload, until committed
+
 // Copies the sections (each followed by zeros up to the next section's
 // offset, the last up to `total`) into the next staging slot and enqueues
 // the fetch of `total` bytes (a multiple of 16) into `dst` on `stream`.
+// The caller then enqueues the kernels that read the upload and calls
+// stage_commit, which records the slot's reuse event behind them: an event
+// recorded between the fetch and the next kernel would hold that kernel back
+// by the few microseconds the command processor takes for the marker.
 rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, hipStream_t stream) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
@@ -65,8 +81,19 @@ rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, 
     StagingSlot &slot = g_staging[g_staging_next];
     g_staging_next = (g_staging_next + 1) % kStagingSlots;
     if (slot.pending) {
-        e = hipEventSynchronize(slot.done);
-        if (e != hipSuccess) return hip_error(e, "waiting for a staging slot");
+        if (slot.by_flag) {
+            const auto t0 = std::chrono::steady_clock::now();
+            for (uint32_t i = 1; __atomic_load_n(slot.flag, __ATOMIC_ACQUIRE) < slot.expect; ++i) {
+                if (i < 256) continue;
+                std::this_thread::yield();
+                if ((i & 4095) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60))
+                    return set_error(RL_ERR_HIP, "waiting for a staging slot: the kernel that reads it has "
+                                                 "not run for 60 s");
+            }
+        } else {
+            e = hipEventSynchronize(slot.done);
+            if (e != hipSuccess) return hip_error(e, "waiting for a staging slot");
+        }
         slot.pending = false;
     }
     if (slot.done && slot.device != device) {
@@ -78,6 +105,13 @@ rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, 
         // system-scope fence (an L2 write-back) is needed when it is recorded
         e = hipEventCreateWithFlags(&slot.done, hipEventDisableTiming | hipEventDisableSystemFence);
         if (e != hipSuccess) return hip_error(e, "creating a staging event");
+        if (!slot.flag) {
+            e = hipHostMalloc(reinterpret_cast<void **>(&slot.flag), 64, hipHostMallocMapped | hipHostMallocCoherent);
+            if (e != hipSuccess) return hip_error(e, "allocating the staging flag");
+            __atomic_store_n(slot.flag, slot.expect, __ATOMIC_RELEASE);
+        }
+        e = hipHostGetDevicePointer(reinterpret_cast<void **>(&slot.flag_dev), slot.flag, 0);
+        if (e != hipSuccess) return hip_error(e, "mapping the staging flag");
         slot.device = device;
     }
     if (slot.cap < total) {
@@ -99,10 +133,45 @@ rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, 
     }
     e = rlk::launch_plan_fetch(slot.dev, dst, total, stream);
     if (e != hipSuccess) return hip_error(e, "uploading the work list");
-    e = hipEventRecord(slot.done, stream);
-    if (e != hipSuccess) return hip_error(e, "recording the staging event");
-    slot.pending = true;
+    g_staged_slot = &slot;
     return RL_OK;
+}
+
+// The release word of the last upload's slot and the value that the
+// operation's last kernel stores into it (system scope, thread 0 of block 0).
+rlk::StageRelease stage_release() {
+    StagingSlot *slot = g_staged_slot;
+    if (!slot) return rlk::StageRelease{nullptr, 0};
+    return rlk::StageRelease{reinterpret_cast<unsigned long long *>(slot->flag_dev),
+                             static_cast<unsigned long long>(slot->expect + 1)};
+}
+
+// Marks the last upload's slot as in use until its reader has run: by the
+// release word when the kernels enqueued since launched (`st` is RL_OK and
+// `released_by_kernel`), otherwise by an event recorded on `stream` behind
+// them.  `st` is the status of those launches and is passed through unless
+// recording the event fails.
+rl_status stage_commit(hipStream_t stream, rl_status st, bool released_by_kernel = false) {
+    StagingSlot *slot = g_staged_slot;
+    g_staged_slot = nullptr;
+    if (!slot) return st;
+    if (st == RL_OK && released_by_kernel) {
+        slot->expect += 1;
+        slot->by_flag = true;
+        slot->pending = true;
+        return st;
+    }
+    slot->by_flag = false;
+    const hipError_t e = hipEventRecord(slot->done, stream);
+    if (e != hipSuccess) {
+        // the slot stays unguarded: drop it, so the next upload allocates afresh
+        slot->host = nullptr;
+        slot->cap = 0;
+        slot->pending = false;
+        return st != RL_OK ? st : hip_error(e, "recording the staging event");
+    }
+    slot->pending = true;
+    return st;
 }
 
 // The decode work list: items, then the prefix and suffix unit tables.
@@ -210,9 +279,9 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.prefix_rows = plan.prefix_rows;
     a.suffix_rows = plan.suffix_rows;
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
+    a.release = stage_release();
     const hipError_t e = rlk::launch_decode(a, hs);
-    if (e != hipSuccess) return hip_error(e, "launching decode attention");
-    return RL_OK;
+    return stage_commit(hs, e != hipSuccess ? hip_error(e, "launching decode attention") : RL_OK, true);
 }
 
 rl_status rl_extend_attn_workspace_size(const rl_decode_shape *shape, const rl_extend_lens *lens,
@@ -263,9 +332,9 @@ rl_status rl_extend_attn(const rl_decode_shape *shape, const rl_extend_lens *len
     a.prefix_rows = plan.prefix_rows;
     a.suffix_rows = plan.suffix_rows;
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
+    a.release = stage_release();
     const hipError_t e = rlk::launch_extend(a, hs);
-    if (e != hipSuccess) return hip_error(e, "launching extend attention");
-    return RL_OK;
+    return stage_commit(hs, e != hipSuccess ? hip_error(e, "launching extend attention") : RL_OK, true);
 }
 
 rl_status rl_token_logprob_workspace_size(int64_t rows, int32_t hidden, int32_t vocab, size_t *bytes) {
@@ -416,9 +485,9 @@ rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *le
     a.Hkv = shape->num_kv_heads;
     a.D = shape->head_dim;
     a.kv_layout = shape->kv_layout;
+    a.release = stage_release();
     const hipError_t e = rlk::launch_kv_append(a, hs);
-    if (e != hipSuccess) return hip_error(e, "launching the KV append");
-    return RL_OK;
+    return stage_commit(hs, e != hipSuccess ? hip_error(e, "launching the KV append") : RL_OK, true);
 }
 
 rl_status rl_token_logprob_backward_workspace_size(int64_t rows, int32_t hidden, int32_t vocab, size_t *bytes) {

@@ -305,6 +305,7 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
 // prefix chunks and the candidate's suffix chunks.
 template <int D>
 __global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) {
+    release_staging(a.release);
     constexpr int PER_LANE = D / 64;
     const int lane = threadIdx.x & 63;
     const int64_t idx = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);

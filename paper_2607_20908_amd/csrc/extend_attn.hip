@@ -75,6 +75,7 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
     using C = ECfg<D, NT>;
     __shared__ __attribute__((aligned(16))) uint16_t ring[kStages * 2 * C::TILE];
 
+    release_staging(a.release);
     const ExtItem it = a.items[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);

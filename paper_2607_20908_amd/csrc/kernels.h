@@ -9,6 +9,19 @@
 
 namespace rlk {
 
+// Release of the pinned staging slot an operation's work list was fetched
+// from: thread 0 of block 0 of the operation's last kernel (which runs after
+// the fetch) stores `value` into `flag` at system scope.  flag may be null.
+struct StageRelease {
+    unsigned long long *flag;
+    unsigned long long value;
+};
+
+__device__ __forceinline__ void release_staging(const StageRelease &r) {
+    if (r.flag && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(r.flag, r.value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 struct DecodeArgs {
     const uint16_t *q;
     const uint16_t *k_prefix, *v_prefix, *k_suffix, *v_suffix;
@@ -22,6 +35,7 @@ struct DecodeArgs {
     int32_t kv_layout;          // RL_KV_TOKEN_MAJOR or RL_KV_HEAD_MAJOR
     int64_t prefix_rows, suffix_rows;
     float score_scale_log2;     // softmax_scale * log2(e)
+    StageRelease release;       // stored by the combine kernel
 };
 
 hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
@@ -38,6 +52,7 @@ struct ExtendArgs {
     int32_t kv_layout;
     int64_t prefix_rows, suffix_rows;
     float score_scale_log2;     // softmax_scale * log2(e)
+    StageRelease release;
 };
 
 hipError_t launch_extend(const ExtendArgs &a, hipStream_t stream);
@@ -57,6 +72,7 @@ struct KvAppendArgs {
     int64_t suffix_rows;
     int32_t Hkv, D;
     int32_t kv_layout;
+    StageRelease release;
 };
 
 hipError_t launch_kv_append(const KvAppendArgs &a, hipStream_t stream);

@@ -12,6 +12,7 @@ namespace {
 constexpr int kThreads = 256;
 
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(KvAppendArgs a) {
+    release_staging(a.release);
     const int chunks = a.D / 8;
     const int64_t per_tok = static_cast<int64_t>(a.Hkv) * chunks;
     const int64_t idx = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
