@@ -380,6 +380,10 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
     a.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
     a.n_row_tiles = static_cast<int32_t>(plan.n_row_tiles);
     a.inv_temperature = inv_temperature;
+    a.dp_tiles = plan.n_dp_tiles;
+    a.tail_tiles = plan.n_tail_tiles;
+    a.splits = plan.tail_splits;
+    a.part = reinterpret_cast<float *>(ws + plan.off_part);
     const hipError_t e = rlk::launch_logprob(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_error(e, "launching token log-prob");
     return RL_OK;

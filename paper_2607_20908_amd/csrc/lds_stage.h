@@ -71,14 +71,15 @@ __device__ __forceinline__ void tile_of_logical(int64_t L, int64_t nnt, int64_t 
     *nt = in / rows_in_group;
 }
 
-// Launch index -> (n-tile, m-tile).  The hardware hands consecutive
-// workgroups to the 8 XCDs in turn; renumbering gives each XCD a contiguous
-// run of logical tiles, so the sharing above happens inside one XCD's L2.
-__device__ __forceinline__ void tile_of(int64_t b, int64_t nnt, int64_t nmt, int64_t *nt, int64_t *mt) {
-    const int64_t total = nnt * nmt;
-    const int64_t full = total / 8 * 8;
-    const int64_t L = b < full ? (b % 8) * (total / 8) + b / 8 : b;
-    tile_of_logical(L, nnt, nmt, nt, mt);
+// Launch index -> (n-tile, m-tile) for a launch over logical tiles [base,
+// base + count).  The hardware hands consecutive workgroups to the 8 XCDs in
+// turn; renumbering gives each XCD a contiguous run of logical tiles, so the
+// sharing above happens inside one XCD's L2.
+__device__ __forceinline__ void tile_of(int64_t b, int64_t count, int64_t base, int64_t nnt, int64_t nmt,
+                                        int64_t *nt, int64_t *mt) {
+    const int64_t full = count / 8 * 8;
+    const int64_t L = b < full ? (b % 8) * (count / 8) + b / 8 : b;
+    tile_of_logical(base + L, nnt, nmt, nt, mt);
 }
 
 }  // namespace rlk

@@ -460,6 +460,22 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
     if (pl.n_vocab_tiles * pl.n_row_tiles > INT32_MAX)
         return fail(err, RL_ERR_UNSUPPORTED, "too many rows x vocab tiles");
     if (rows == 0) return RL_OK;
+    // Whole rounds of tiles over the CUs run as they are.  A last round that
+    // would leave at least half of the CUs idle is split over the hidden
+    // dimension instead, as many ways as fit one round (up to 4, at least 4
+    // hidden steps per part), so that it takes a fraction of a tile's time.
+    const int64_t tiles = pl.n_vocab_tiles * pl.n_row_tiles;
+    const int64_t dp = tiles / kNumCUs * kNumCUs, tail = tiles - dp;
+    const int64_t nks = hidden / kHiddenStep;
+    pl.n_dp_tiles = tiles;
+    if (dp > 0 && tail > 0 && 2 * tail <= kNumCUs) {
+        const int64_t s = std::min<int64_t>(std::min<int64_t>(kMaxTailSplits, kNumCUs / tail), nks / 4);
+        if (s >= 2) {
+            pl.n_dp_tiles = dp;
+            pl.n_tail_tiles = tail;
+            pl.tail_splits = static_cast<int32_t>(s);
+        }
+    }
     size_t off = 0;
     pl.off_m = off;
     off = align_up(off + static_cast<size_t>(pl.n_vocab_tiles) * rows * 4, 256);
@@ -467,6 +483,8 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
     off = align_up(off + static_cast<size_t>(pl.n_vocab_tiles) * rows * 4, 256);
     pl.off_zt = off;
     off = align_up(off + static_cast<size_t>(rows) * 4, 256);
+    pl.off_part = off;
+    off += static_cast<size_t>(pl.n_tail_tiles) * pl.tail_splits * kVocabTile * kRowTile * 4;
     pl.total_bytes = off;
     return RL_OK;
 }

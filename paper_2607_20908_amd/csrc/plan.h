@@ -89,11 +89,20 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
 rl_status check_decode_ptrs(const DecodePlan &plan, const rl_decode_lens *lens,
                             const rl_decode_ptrs *ptrs, std::string *err);
 
+// A last round of lm-head tiles that would leave at least half the CUs idle
+// is split over the hidden dimension into up to this many parts.
+constexpr int kMaxTailSplits = 4;
+
 struct LogprobPlan {
     int64_t R = 0;
     int32_t H = 0, V = 0;
     int64_t n_vocab_tiles = 0, n_row_tiles = 0;
-    size_t off_m = 0, off_l = 0, off_zt = 0, total_bytes = 0;
+    // tiles [0, n_dp_tiles) run whole; the n_tail_tiles after them run as
+    // tail_splits hidden-dimension parts whose fp32 accumulators (one
+    // 256 x 256 tile each, at off_part) a reduce kernel sums
+    int64_t n_dp_tiles = 0, n_tail_tiles = 0;
+    int32_t tail_splits = 1;
+    size_t off_m = 0, off_l = 0, off_zt = 0, off_part = 0, total_bytes = 0;
 };
 
 rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan *plan,

@@ -42,7 +42,104 @@ static_assert(kBlocksPerWave == 8, "staging layout");
 // p = exp(inv_T z - lse) per (row, vocab entry) as bf16 into the blocked
 // probability buffer; or the sampling head's tempered fp32 logits (per-row
 // temperature) plus the tile's row maxima.
-enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2 };
+enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2, kPartialK = 3 };
+
+// Forward epilogue of one 32-row column of a 256 x 256 logit tile, as one
+// lane of a wave holds it: z(tm)[i] is vocab vbase + tm*32 + 8*(i/4) + 4*h2 +
+// i%4 for token row rr (vbase = v0 + 128 * the wave's vocab half).  Returns
+// the row's max and sum of exp2 over the wave's 128 vocab entries (both lane
+// halves merged) and writes the target's logit if it falls among them.
+template <class Z>
+__device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t rr, int64_t vbase, int h2,
+                                            float &mx_out, float &sum_out) {
+    const float c2 = a.inv_temperature * kLog2e;
+    const bool full_vocab = vbase + 128 <= a.V;  // only the last vocab tile is masked
+    // the target's index among the wave's 128 vocab entries, shifted so that
+    // it compares against compile-time constants; -1 unless this lane's half
+    // of the accumulator rows (bit 2 of the index) holds it
+    int tsel = -1;
+    if (rr < a.R) {
+        const int64_t local = static_cast<int64_t>(a.target[rr]) - vbase;
+        if (local >= 0 && local < 128 && ((local >> 2) & 1) == h2) tsel = static_cast<int>(local) - 4 * h2;
+    }
+    // one pass per 32-entry block: block max and sum, merged online into the
+    // row's (mx, sum); each accumulator register is read once
+    const int vlim = full_vocab ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
+    float mx = -INFINITY, sum = 0.f, zsel = 0.f;
+#pragma unroll
+    for (int tm = 0; tm < 4; ++tm) {
+        const f32x16 zz = z(tm);
+        float bm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
+            bm = fmaxf(bm, loc < vlim ? zz[i] : -INFINITY);
+            zsel = loc == tsel ? zz[i] : zsel;
+        }
+        bm *= c2;                                // c2 > 0: scaling commutes with max
+        const float bmu = bm == -INFINITY ? 0.f : bm;
+        float bs = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
+            bs += loc < vlim ? fast_exp2(zz[i] * c2 - bmu) : 0.f;
+        }
+        // merge (bm, bs) into (mx, sum)
+        const float nm = fmaxf(mx, bm);
+        const float nmu = nm == -INFINITY ? 0.f : nm;
+        sum = sum * fast_exp2(mx - nmu) + bs * fast_exp2(bm - nmu);
+        mx = nm;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (tsel >= 0) a.zt[rr] = zsel * a.inv_temperature;
+    // merge the two lane halves (same row, disjoint vocab entries)
+    const float om = __shfl_xor(mx, 32, 64), os = __shfl_xor(sum, 32, 64);
+    const float nm = fmaxf(mx, om);
+    const float nmu = nm == -INFINITY ? 0.f : nm;
+    sum_out = sum * fast_exp2(mx - nmu) + os * fast_exp2(om - nmu);
+    mx_out = nm;
+}
+
+// Writes the (max, sum) partial of (vocab tile vt, row rr) from the two vocab
+// halves' partials.
+__device__ __forceinline__ void write_partial(const LogprobArgs &a, int64_t vt, int64_t rr, float m0, float l0,
+                                              float m1, float l1) {
+    const float Mx = fmaxf(m0, m1);
+    a.pm[vt * a.R + rr] = Mx;
+    a.pl[vt * a.R + rr] = l0 * fast_exp2(m0 - Mx) + l1 * fast_exp2(m1 - Mx);
+}
+
+// Forward epilogue of one 256 x 256 logit tile held in the registers of the
+// workgroup's 4 waves (acc[tm][tn][i] of wave (wm, wn), lane (h2, l32) holds
+// vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4 for token row
+// r0 + wn*128 + tn*32 + l32): per token row the max and the sum of exp2 over
+// the tile's vocab entries and, if the target falls in the tile, its logit.
+// `red` is 4 KB of LDS that the caller no longer uses.
+__device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 (&acc)[4][4], int64_t vt,
+                                             int64_t rt, float (*red)[kRowTile][2]) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;
+    const int l32 = lane & 31, h2 = lane >> 5;
+    const int64_t r0 = rt * kRowTile;
+    const int64_t vbase = vt * kVocabTile + wm * 128;
+#pragma unroll
+    for (int tn = 0; tn < 4; ++tn) {
+        const int row = wn * 128 + tn * 32 + l32;
+        float mx, sum;
+        row_partial(a, [&](int tm) -> const f32x16 & { return acc[tm][tn]; }, r0 + row, vbase, h2, mx, sum);
+        if (h2 == 0) {
+            red[wm][row][0] = mx;
+            red[wm][row][1] = sum;
+        }
+        // keep each row block's accumulator copies local: hoisting the reads
+        // of all four blocks would need 256 more VGPRs
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    const int64_t rr = r0 + tid;                 // 256 threads, 256 rows
+    if (rr < a.R) write_partial(a, vt, rr, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
+}
 
 template <int WS, int MODE>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
@@ -57,10 +154,22 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const int wm = wave & 1, wn = wave >> 1;     // vocab half (128 entries), row half (128 rows)
     const int l32 = lane & 31, h2 = lane >> 5;
     int64_t vt, rt;
-    tile_of(blockIdx.x, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+    int kb = 0, nks = a.H / kK;                  // hidden steps [kb, kb + nks)
+    if constexpr (MODE == kPartialK) {
+        // part s of tail tile j covers hidden steps [s n / S, (s + 1) n / S)
+        const int64_t j = blockIdx.x / a.splits;
+        const int sp = static_cast<int>(blockIdx.x % a.splits);
+        tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+        kb = sp * nks / a.splits;
+        nks = (sp + 1) * nks / a.splits - kb;
+    } else if constexpr (MODE == kFwd) {
+        tile_of(blockIdx.x, a.tile_count, a.tile_base, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+    } else {
+        tile_of(blockIdx.x, static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles, 0, a.n_vocab_tiles,
+                a.n_row_tiles, &vt, &rt);
+    }
     const int64_t v0 = vt * kVocabTile, r0 = rt * kRowTile;
     const int64_t H = a.H;
-    const int nks = a.H / kK;
 
     // ---- staging: each wave fills 8 blocks of 8 rows per operand per stage.
     // Lane i of a block covers row 8*block + i/8 and LDS slot i%8 of that row,
@@ -78,7 +187,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         const int blk = wave * kBlocksPerWave + j;
         const int row = blk * 8 + (lane >> 3);
         const int c = (lane & 7) ^ ((row >> 1) & 7);
-        const int64_t k0 = static_cast<int64_t>(min(slot, nks - 1)) * kK;
+        const int64_t k0 = static_cast<int64_t>(kb + min(slot, nks - 1)) * kK;
         load_lds16(g + min(row, last) * H + k0 + c * 8, st + blk * 512);
     };
     auto issue_w = [&](int slot) {
@@ -256,81 +365,71 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         return;
     }
 
-    // ---- epilogue: per token row, max / sum of exp2 / target logit ---------
-    // acc[tm][tn][i] holds vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4
-    // for token row r0 + wn*128 + tn*32 + l32.
-    const float c2 = a.inv_temperature * kLog2e;
-    const int64_t vbase = v0 + wm * 128;
-    const bool full_vocab = vbase + 128 <= a.V;  // only the last vocab tile is masked
+    if constexpr (MODE == kPartialK) {
+        // one part of a tail tile: its fp32 accumulators, in register order
+        // (each store writes 1 KB contiguously), for the reduce kernel
+        float *dst = a.part + static_cast<int64_t>(blockIdx.x) * (kVocabTile * kRowTile);
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-        const int row = wn * 128 + tn * 32 + l32;
-        const int64_t rr = r0 + row;
-        // the target's index among this wave's 128 vocab entries, shifted so
-        // that it compares against compile-time constants; -1 unless this
-        // lane's half of the accumulator rows (bit 2 of the index) holds it
-        int tsel = -1;
-        if (rr < a.R) {
-            const int64_t local = static_cast<int64_t>(a.target[rr]) - vbase;
-            if (local >= 0 && local < 128 && ((local >> 2) & 1) == h2) tsel = static_cast<int>(local) - 4 * h2;
-        }
-        // one pass per 32-entry block: block max and sum, merged online into
-        // the row's (mx, sum); each accumulator register is read once
-        const int vlim = full_vocab ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
-        float mx = -INFINITY, sum = 0.f, zsel = 0.f;
+        for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
-        for (int tm = 0; tm < 4; ++tm) {
-            const f32x16 z = acc[tm][tn];
-            float bm = -INFINITY;
+            for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
-                bm = fmaxf(bm, loc < vlim ? z[i] : -INFINITY);
-                zsel = loc == tsel ? z[i] : zsel;
-            }
-            bm *= c2;                            // c2 > 0: scaling commutes with max
-            const float bmu = bm == -INFINITY ? 0.f : bm;
-            float bs = 0.f;
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 v = {acc[tm][tn][4 * q], acc[tm][tn][4 * q + 1], acc[tm][tn][4 * q + 2],
+                                     acc[tm][tn][4 * q + 3]};
+                    *reinterpret_cast<f32x4 *>(dst + (((wave * 16 + tm * 4 + tn) * 4 + q) * 64 + lane) * 4) = v;
+                }
+        return;
+    }
+    fwd_epilogue(a, acc, vt, rt, red);
+}
+
+// Sums the hidden-dimension parts of the tail tiles (in a fixed order) and
+// runs the forward epilogue on the sums.  One workgroup of 2 waves per
+// (tail tile, 32-row column tn of row half wn): wave wm holds what lane (h2,
+// l32) of tile-kernel wave (wm, wn) held for that column, 8 workgroups per
+// tile, so the parts are read by many CUs at once.
+__global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a) {
+    __shared__ float red[2][32][2];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t j = blockIdx.x >> 3;
+    const int wn = (blockIdx.x >> 2) & 1, tn = blockIdx.x & 3;
+    const int l32 = lane & 31, h2 = lane >> 5;
+    int64_t vt, rt;
+    tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+    const int wave = wn * 2 + wm;                // the tile kernel's wave index
+    const float *src = a.part + j * a.splits * (kVocabTile * kRowTile);
+    f32x16 z[4];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
-                bs += loc < vlim ? fast_exp2(z[i] * c2 - bmu) : 0.f;
-            }
-            // merge (bm, bs) into (mx, sum)
-            const float nm = fmaxf(mx, bm);
-            const float nmu = nm == -INFINITY ? 0.f : nm;
-            sum = sum * fast_exp2(mx - nmu) + bs * fast_exp2(bm - nmu);
-            mx = nm;
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        if (tsel >= 0) a.zt[rr] = zsel * a.inv_temperature;
-        // merge the two lane halves (same row, disjoint vocab entries)
-        {
-            const float om = __shfl_xor(mx, 32, 64), os = __shfl_xor(sum, 32, 64);
-            const float nm = fmaxf(mx, om);
-            const float nmu = nm == -INFINITY ? 0.f : nm;
-            sum = sum * fast_exp2(mx - nmu) + os * fast_exp2(om - nmu);
-            mx = nm;
-        }
-        if (h2 == 0) {
-            red[wm][row][0] = mx;
-            red[wm][row][1] = sum;
-        }
-        // keep each row block's accumulator copies local: hoisting the reads
-        // of all four blocks would need 256 more VGPRs
-        __builtin_amdgcn_sched_barrier(0);
+    for (int tm = 0; tm < 4; ++tm) z[tm] = f32x16{};
+    for (int sp = 0; sp < a.splits; ++sp) {
+        const float *p = src + static_cast<int64_t>(sp) * (kVocabTile * kRowTile);
+        f32x4 v[4][4];
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                v[tm][q] = *reinterpret_cast<const f32x4 *>(p + (((wave * 16 + tm * 4 + tn) * 4 + q) * 64 + lane) * 4);
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) z[tm][4 * q + e] += v[tm][q][e];
+    }
+    const int row = tn * 32 + l32;               // within the row half
+    const int64_t rr = rt * kRowTile + wn * 128 + row;
+    float mx, sum;
+    row_partial(a, [&](int tm) -> const f32x16 & { return z[tm]; }, rr, vt * kVocabTile + wm * 128, h2, mx, sum);
+    if (h2 == 0) {
+        red[wm][l32][0] = mx;
+        red[wm][l32][1] = sum;
     }
     __syncthreads();
-    {
-        const int row = tid;                     // 256 threads, 256 rows
-        const int64_t rr = r0 + row;
-        if (rr < a.R) {
-            const float m0 = red[0][row][0], m1 = red[1][row][0];
-            const float Mx = fmaxf(m0, m1);
-            const float L = red[0][row][1] * fast_exp2(m0 - Mx) + red[1][row][1] * fast_exp2(m1 - Mx);
-            a.pm[vt * a.R + rr] = Mx;
-            a.pl[vt * a.R + rr] = L;
-        }
+    if (tid < 32) {
+        const int64_t r = rt * kRowTile + wn * 128 + tn * 32 + tid;
+        if (r < a.R) write_partial(a, vt, r, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
     }
 }
 
@@ -391,15 +490,35 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
 }  // namespace
 
 hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
-    const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
+    // whole tiles [0, dp_tiles)
+    LogprobArgs d = a;
+    d.tile_base = 0;
+    d.tile_count = a.dp_tiles;
     if (a.n_row_tiles <= 8)
-        hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
-                           stream, a);
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd>), dim3(static_cast<uint32_t>(d.tile_count)),
+                           dim3(kTileThreads), 0, stream, d);
     else
-        hipLaunchKernelGGL((logprob_tile_kernel<2, kFwd>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
-                           stream, a);
+        hipLaunchKernelGGL((logprob_tile_kernel<2, kFwd>), dim3(static_cast<uint32_t>(d.tile_count)),
+                           dim3(kTileThreads), 0, stream, d);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (a.tail_tiles > 0) {
+        // the tail: `splits` hidden-dimension parts per tile, then their sum
+        LogprobArgs t = a;
+        t.tile_base = a.dp_tiles;
+        t.tile_count = a.tail_tiles;
+        const uint32_t parts = static_cast<uint32_t>(a.tail_tiles * a.splits);
+        if (a.n_row_tiles <= 8)
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+        else
+            hipLaunchKernelGGL((logprob_tile_kernel<2, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(logprob_tail_reduce_kernel, dim3(static_cast<uint32_t>(a.tail_tiles * 8)), dim3(128), 0,
+                           stream, t);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (a.R < 32768) {
         const int64_t blocks = (a.R + 3) / 4;
         hipLaunchKernelGGL(logprob_combine_wave_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,

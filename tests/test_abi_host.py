@@ -178,13 +178,34 @@ def test_logprob_empty_is_noop():
     assert st == OK and msg == ""
 
 
+def tail_part_bytes(R, H, V, cus=256, max_splits=4):
+    """fp32 accumulators of the hidden-dimension parts of a short last round
+    of 256 x 256 tiles (at most half the CUs busy): tail x splits x 256 KB."""
+    tiles = -(-V // 256) * -(-R // 256)
+    dp, tail = tiles // cus * cus, tiles % cus
+    if dp == 0 or tail == 0 or 2 * tail > cus:
+        return 0
+    s = min(max_splits, cus // tail, H // 64 // 4)
+    if s < 2:
+        return 0
+    return tail * s * 256 * 256 * 4
+
+
 def test_logprob_workspace_size():
-    # per (vocab tile of 256, row): max and sum; per row: the target logit
-    R, V = 1000, 151936
-    n = rk.token_logprob_workspace_size(R, 5120, V)
-    tiles = -(-V // 256)
-    assert n >= (2 * tiles * R + R) * 4
-    assert n < (2 * tiles * R + R) * 4 + 3 * 256
+    # per (vocab tile of 256, row): max and sum; per row: the target logit;
+    # the tail's partial accumulators when the last round is split
+    for R, H, V in ((1000, 5120, 151936), (256, 5120, 151936), (512, 4096, 151936), (40, 64, 1000),
+                    (256, 256, 76800), (262144, 5120, 151936)):
+        n = rk.token_logprob_workspace_size(R, H, V)
+        tiles = -(-V // 256)
+        base = (2 * tiles * R + R) * 4 + tail_part_bytes(R, H, V)
+        assert base <= n < base + 3 * 256, (R, H, V)
+    # the 32B-class decode step (594 tiles: 2 rounds + 82) splits its tail
+    # 3 ways; the 8B-class one (1188 tiles: 4 rounds + 164) does not split
+    assert tail_part_bytes(256, 5120, 151936) == 82 * 3 * 256 * 256 * 4
+    assert tail_part_bytes(512, 4096, 151936) == 0
+    assert tail_part_bytes(256, 256, 76800) == 0      # too few hidden steps
+    assert tail_part_bytes(256, 768, 66048) == 2 * 3 * 256 * 256 * 4   # 12 hidden steps: 3 parts
     assert rk.token_logprob_workspace_size(0, 64, 10) == 0
     with pytest.raises(rk.RLError):
         rk.token_logprob_workspace_size(4, 100, 10)

@@ -58,6 +58,23 @@ def test_ragged_shapes(R, H, V):
     check(h, w, t, what=f"{R}x{H}x{V}")
 
 
+@pytest.mark.parametrize("R,H,V", [(200, 1024, 75739),    # 296 vocab tiles: 256 whole, 40 in 4 hidden parts
+                                   (300, 1024, 38395),    # 2 x 150 tiles: 256 whole, 44 in 4 parts
+                                   (256, 768, 66048)])    # 258 tiles: 256 whole, 2 in 3 parts
+def test_split_tail(R, H, V):
+    """A short last round of tiles runs as hidden-dimension parts summed by a
+    reduce kernel; the tail holds the highest vocab tiles, so targets there
+    (the last ids included), masks and invalid ids go through it."""
+    rng = np.random.Generator(np.random.PCG64(R * 7 + V))
+    h = rand_bits(rng, (R, H))
+    w = rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    t[: R // 4] = rng.integers(V - 40 * 256, V, R // 4)
+    t[[0, 1, 2, 3]] = [V - 1, V - 256, -1, V]
+    lp, lse = check(h, w, t, 1.0 / 0.7, f"split tail {R}x{H}x{V}")
+    assert lp[2] == 0 and np.isnan(lp[3])
+
+
 def test_temperature_masking_and_invalid_targets():
     rng = np.random.Generator(np.random.PCG64(7))
     R, H, V = 400, 256, 1500
