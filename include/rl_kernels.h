@@ -138,16 +138,18 @@ typedef struct {
  * context: prefix rows [prefix_start[p], +Lp[p]) followed by suffix rows
  * [suffix_start[s], +Ls[s]), both at kv head h / (Hq/Hkv).  The caller appends
  * the current token's K/V to the suffix before the call; there is no causal
- * mask inside one decode step.  The prefix KV of a prompt is read from HBM once
- * for all G candidates when G*Hq/Hkv <= 128 (query rows per kv head), and once
- * per block of 128 such rows beyond that.
+ * mask inside one decode step.  The prefix KV of a prompt is read once for all
+ * G candidates when G*Hq/Hkv <= 64 (query rows per kv head); wider groups take
+ * one work item per block of 64 such rows on the same chunk, launched side by
+ * side, so the repeated reads mostly hit the last-level cache.
  *
  * Rows outside the given ranges are never read.  P*G == 0 is a valid no-op.
  * Status: NULL pointer -> RL_ERR_NULL_POINTER; negative sizes or lengths,
  * Hq % Hkv != 0, a range past prefix_rows/suffix_rows, a non-finite or
  * non-positive scale, a bad split_tokens or kv_layout -> RL_ERR_INVALID_SHAPE;
- * D not in {64, 128} -> RL_ERR_UNSUPPORTED; a device pointer not 16-byte
- * aligned -> RL_ERR_MISALIGNED; workspace NULL or short -> RL_ERR_WORKSPACE.
+ * D not in {64, 128} or Hq/Hkv > 128 -> RL_ERR_UNSUPPORTED; a device pointer
+ * not 16-byte aligned -> RL_ERR_MISALIGNED; workspace NULL or short ->
+ * RL_ERR_WORKSPACE.
  */
 rl_status rl_decode_attn_workspace_size(const rl_decode_shape *shape,
                                         const rl_decode_lens *lens,
@@ -280,6 +282,12 @@ rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *le
  * hidden % 64 != 0 -> RL_ERR_UNSUPPORTED; a device pointer not 16-byte
  * aligned (target, logprob and lse: 4-byte) -> RL_ERR_MISALIGNED; workspace
  * NULL or short -> RL_ERR_WORKSPACE.
+ *
+ * The workspace holds a (max, sum) partial per (256-entry vocab tile, row)
+ * and the target logit per row; when the last round of 256 x 256 tiles would
+ * leave at least half of the 256 CUs idle, those tiles run as 2-4 parts of
+ * the hidden dimension and the workspace also holds their fp32 accumulators
+ * (256 KB per part).
  */
 rl_status rl_token_logprob_workspace_size(int64_t rows, int32_t hidden, int32_t vocab,
                                           size_t *bytes);
@@ -448,7 +456,7 @@ typedef struct {
     int32_t tok_count;   /* >= 1                                                        */
     int32_t row_begin;   /* first query row served, of the unit's G*Hq/Hkv (prefix) or
                             Hq/Hkv (suffix) rows at this kv head                         */
-    int32_t row_count;   /* query rows served: at most 128                               */
+    int32_t row_count;   /* query rows served: at most 64                                */
     int32_t reserved;
 } rl_plan_item;
 
