@@ -101,6 +101,7 @@ def decode_call(P=2, G=3, Hq=4, Hkv=2, D=128, scale=0.125, split=0, lp=None, ls=
     (dict(D=96), UNSUP),
     (dict(D=256), UNSUP),
     (dict(D=0), SHAPE),
+    (dict(Hq=258, Hkv=2), UNSUP),             # Hq/Hkv = 129 > 128
     (dict(ptrs=dict(q=FAKE + 8)), MISAL),
     (dict(ptrs=dict(v_prefix=FAKE + 2)), MISAL),
     (dict(ptrs=dict(out=FAKE + 4)), MISAL),
