@@ -70,10 +70,12 @@ def test_ragged_multi_tile(D, split, layout):
     check(c, 1.0 / math.sqrt(D), split, f"ragged D={D}", layout)
 
 
-@pytest.mark.parametrize("G,Hq,Hkv", [(16, 64, 8),   # 128 query rows per kv head: 2 column tiles per wave
-                                       (20, 16, 2),   # 160 rows: two row blocks per prefix chunk
+@pytest.mark.parametrize("G,Hq,Hkv", [(16, 64, 8),   # 128 query rows per kv head: two 64-row items per chunk
+                                       (20, 16, 2),   # 160 rows: three row blocks per prefix chunk
                                        (5, 12, 4),    # 15 rows: one partial column tile
-                                       (3, 24, 2)])   # r = 12 per candidate
+                                       (3, 24, 2),    # r = 12 per candidate
+                                       (2, 160, 2),   # r = 80: two row blocks per suffix chunk too
+                                       (1, 128, 1)])  # r = 128, the largest: G = 1
 def test_group_shapes(G, Hq, Hkv):
     P = 2
     rng = np.random.Generator(np.random.PCG64(G * 100 + Hq))
