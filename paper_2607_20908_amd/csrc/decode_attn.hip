@@ -330,18 +330,16 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) 
     for (int e = 0; e < PER_LANE; ++e) o[e] = 0.f;
     if (n <= 64) {
         // lane j holds partial j's (m, l): one load latency for all of them;
-        // the value rows then load 8 at a time, each weight taken by readlane
+        // the value rows load 8 at a time (the first 8 alongside the (m, l),
+        // as they do not depend on the weights), each weight taken by readlane
         float mj = -INFINITY, lj = 0.f;
         if (lane < n) {
             const int64_t pr = prow(lane);
             mj = a.pm[pr];
             lj = a.pl[pr];
         }
-        Mx = wave_max(mj);
-        const float fj = lane < n ? fast_exp2(mj - Mx) : 0.f;
-        L = wave_sum(fj * lj);
-        for (int j0 = 0; j0 < n; j0 += 8) {
-            float v[8][PER_LANE];
+        float v[8][PER_LANE];
+        auto load_rows = [&](int j0) {
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
                 if (j0 + u < n) {
@@ -350,6 +348,13 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) 
                     for (int e = 0; e < PER_LANE; ++e) v[u][e] = a.pacc[pr * D + lane * PER_LANE + e];
                 }
             }
+        };
+        load_rows(0);
+        Mx = wave_max(mj);
+        const float fj = lane < n ? fast_exp2(mj - Mx) : 0.f;
+        L = wave_sum(fj * lj);
+        for (int j0 = 0; j0 < n; j0 += 8) {
+            if (j0 > 0) load_rows(j0);
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
                 if (j0 + u < n) {
