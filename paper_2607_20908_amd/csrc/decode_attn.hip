@@ -42,7 +42,7 @@ struct DCfg {
     static constexpr int TILEV = kTileTokens * LDRV; // bf16 elements of one V tile
     static constexpr int STAGE = TILE + TILEV;       // one K tile followed by one V tile
     static constexpr int LD = kTileTokens * CH / kThreads;  // 16-byte chunks per thread per tensor
-    static constexpr int RED_STRIDE = D + 1;     // fp32 row stride of the merge area (bank spread)
+    static constexpr int RED_STRIDE = D + 4;     // fp32 row stride of the merge area (16-byte rows, bank spread)
     static constexpr int KV_BYTES = STAGE * 2;                         // one LDS stage (K, V)
     static constexpr int RED_BYTES = 4 * 16 * RED_STRIDE * 4;          // waves x 16 rows
     static constexpr int MAIN_BYTES = KV_BYTES > RED_BYTES ? KV_BYTES : RED_BYTES;
@@ -267,17 +267,17 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
         return;
     }
     // Wt waves hold partials of the same rows over disjoint tokens: merge them
-    // through LDS (the stage is free after the loop's last barrier)
-    {
+    // through LDS (the stage is free after the loop's last barrier); only the
+    // item's rows are written (a suffix item has r of a column tile's 16)
+    if (wc * 16 + l16 < rows) {
         const int slot = wave * 16 + l16;
-        if (lane < 16) {
+        if (g4 == 0) {
             red_ml[slot * 2 + 0] = m_run;
             red_ml[slot * 2 + 1] = l_run;
         }
 #pragma unroll
         for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) red_acc[slot * C::RED_STRIDE + dt * 16 + g4 * 4 + i] = acc[dt][i];
+            *reinterpret_cast<f32x4 *>(red_acc + slot * C::RED_STRIDE + dt * 16 + g4 * 4) = acc[dt];
     }
     __syncthreads();
     for (int e = tid; e < rows * D; e += kThreads) {

@@ -63,35 +63,66 @@ __device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t r
         if (local >= 0 && local < 128 && ((local >> 2) & 1) == h2) tsel = static_cast<int>(local) - 4 * h2;
     }
     // one pass per 32-entry block: block max and sum, merged online into the
-    // row's (mx, sum); each accumulator register is read once
-    const int vlim = full_vocab ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
-    float mx = -INFINITY, sum = 0.f, zsel = 0.f;
-#pragma unroll
-    for (int tm = 0; tm < 4; ++tm) {
-        const f32x16 zz = z(tm);
-        float bm = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
-            bm = fmaxf(bm, loc < vlim ? zz[i] : -INFINITY);
-            zsel = loc == tsel ? zz[i] : zsel;
-        }
-        bm *= c2;                                // c2 > 0: scaling commutes with max
-        const float bmu = bm == -INFINITY ? 0.f : bm;
-        float bs = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
-            bs += loc < vlim ? fast_exp2(zz[i] * c2 - bmu) : 0.f;
-        }
-        // merge (bm, bs) into (mx, sum)
+    // row's (mx, sum); each accumulator register is read once.  Only the last
+    // vocab tile masks entries past the vocabulary: the other tiles take a
+    // path without per-entry compares (the branch is uniform over the wave).
+    float mx = -INFINITY, sum = 0.f;
+    auto merge = [&](float bm, float bs) {
         const float nm = fmaxf(mx, bm);
         const float nmu = nm == -INFINITY ? 0.f : nm;
         sum = sum * fast_exp2(mx - nmu) + bs * fast_exp2(bm - nmu);
         mx = nm;
-        __builtin_amdgcn_sched_barrier(0);
+    };
+    if (full_vocab) {
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm) {
+            const f32x16 zz = z(tm);
+            float bm = fmaxf(fmaxf(zz[0], zz[1]), zz[2]);
+#pragma unroll
+            for (int i = 3; i < 15; i += 2) bm = fmaxf(fmaxf(bm, zz[i]), zz[i + 1]);
+            bm = fmaxf(bm, zz[15]) * c2;         // c2 > 0: scaling commutes with max
+            const float bmu = bm == -INFINITY ? 0.f : bm;
+            float bs = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) bs += fast_exp2(zz[i] * c2 - bmu);
+            merge(bm, bs);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+        const int vlim = static_cast<int>(a.V - vbase) - 4 * h2;
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm) {
+            const f32x16 zz = z(tm);
+            float bm = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
+                bm = fmaxf(bm, loc < vlim ? zz[i] : -INFINITY);
+            }
+            bm *= c2;
+            const float bmu = bm == -INFINITY ? 0.f : bm;
+            float bs = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int loc = tm * 32 + 8 * (i >> 2) + (i & 3);
+                bs += loc < vlim ? fast_exp2(zz[i] * c2 - bmu) : 0.f;
+            }
+            merge(bm, bs);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
-    if (tsel >= 0) a.zt[rr] = zsel * a.inv_temperature;
+    // the target's logit: a tile holds a given row's target with probability
+    // 256 / V, so the search runs only when some lane of the wave needs it
+    if (__any(tsel >= 0)) {
+        float zsel = 0.f;
+#pragma unroll
+        for (int tm = 0; tm < 4; ++tm) {
+            const f32x16 zz = z(tm);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) zsel = tm * 32 + 8 * (i >> 2) + (i & 3) == tsel ? zz[i] : zsel;
+        }
+        if (tsel >= 0) a.zt[rr] = zsel * a.inv_temperature;
+    }
     // merge the two lane halves (same row, disjoint vocab entries)
     const float om = __shfl_xor(mx, 32, 64), os = __shfl_xor(sum, 32, 64);
     const float nm = fmaxf(mx, om);
