@@ -283,11 +283,13 @@ rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *le
  * aligned (target, logprob and lse: 4-byte) -> RL_ERR_MISALIGNED; workspace
  * NULL or short -> RL_ERR_WORKSPACE.
  *
- * The workspace holds a (max, sum) partial per (256-entry vocab tile, row)
- * and the target logit per row; when the last round of 256 x 256 tiles would
- * leave at least half of the 256 CUs idle, those tiles run as 2-4 parts of
- * the hidden dimension and the workspace also holds their fp32 accumulators
- * (256 KB per part).
+ * The workspace holds a (max, sum) partial per (vocab tile, row) and the
+ * target logit per row.  When the last round of 256 x 256 tiles would leave
+ * at least half of the 256 CUs idle, those tiles run as 2-4 parts of the
+ * hidden dimension and the workspace also holds their fp32 accumulators
+ * (256 KB per part).  When it is more than half full and there are at most 4
+ * row tiles, the vocabulary past the full rounds runs as tiles 192 entries
+ * wide instead (if they fit in one round), each with its own partial slot.
  */
 rl_status rl_token_logprob_workspace_size(int64_t rows, int32_t hidden, int32_t vocab,
                                           size_t *bytes);

@@ -384,6 +384,10 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
     a.tail_tiles = plan.n_tail_tiles;
     a.splits = plan.tail_splits;
     a.part = reinterpret_cast<float *>(ws + plan.off_part);
+    a.narrow_v0 = plan.narrow_v0;
+    a.narrow_tiles = plan.narrow_tiles;
+    a.narrow_slot0 = plan.narrow_slot0;
+    a.n_partials = plan.n_partials;
     const hipError_t e = rlk::launch_logprob(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_error(e, "launching token log-prob");
     return RL_OK;

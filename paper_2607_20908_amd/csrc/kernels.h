@@ -82,7 +82,7 @@ struct LogprobArgs {
     const uint16_t *w;          // [V, H]
     const int32_t *target;      // [R]
     float *logprob, *lse;       // [R], lse may be null
-    float *pm, *pl, *zt;        // workspace: [n_vocab_tiles, R] x2, [R]
+    float *pm, *pl, *zt;        // workspace: [n_partials, R] x2, [R]
     int64_t R;
     int32_t H, V;
     int32_t n_vocab_tiles, n_row_tiles;
@@ -96,6 +96,10 @@ struct LogprobArgs {
     int32_t splits;
     float *part;
     int64_t tile_base, tile_count;
+    // forward only: the last round as narrow tiles of 192 vocab entries,
+    // narrow tile j covering [narrow_v0 + 192 j, + 192) with its partials in
+    // slot narrow_slot0 + j; the combine merges n_partials slots per row
+    int64_t narrow_v0, narrow_tiles, narrow_slot0, n_partials;
     // backward only: the forward's lse per row (input) and the probabilities
     // p = exp(inv_T z - lse) as bf16 in the blocked layout of
     // LogprobBwdArgs::probs (output); pm, pl, zt, logprob are then unused

@@ -468,6 +468,7 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
     const int64_t dp = tiles / kNumCUs * kNumCUs, tail = tiles - dp;
     const int64_t nks = hidden / kHiddenStep;
     pl.n_dp_tiles = tiles;
+    pl.n_partials = pl.n_vocab_tiles;
     if (dp > 0 && tail > 0 && 2 * tail <= kNumCUs) {
         const int64_t s = std::min<int64_t>(std::min<int64_t>(kMaxTailSplits, kNumCUs / tail), nks / 4);
         if (s >= 2) {
@@ -476,11 +477,27 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
             pl.tail_splits = static_cast<int32_t>(s);
         }
     }
+    // A last round more than half full: with at most 4 row tiles (the tiles
+    // of one vocab tile are neighbours in launch order), the whole vocab
+    // tiles of the full rounds run as they are and the rest of the
+    // vocabulary runs as one round of tiles 192 entries wide, if they fit on
+    // the CUs (a round of them takes about 3/4 of a round of whole tiles).
+    if (pl.n_tail_tiles == 0 && dp > 0 && tail > 0 && pl.n_row_tiles <= kNarrowMaxRowTiles) {
+        const int64_t vt0 = dp / pl.n_row_tiles;
+        const int64_t n = ceil_div(vocab - vt0 * kVocabTile, kNarrowWidth);
+        if (n * pl.n_row_tiles <= kNumCUs) {
+            pl.n_dp_tiles = vt0 * pl.n_row_tiles;
+            pl.narrow_v0 = vt0 * kVocabTile;
+            pl.narrow_tiles = n;
+            pl.narrow_slot0 = vt0;
+            pl.n_partials = vt0 + n;
+        }
+    }
     size_t off = 0;
     pl.off_m = off;
-    off = align_up(off + static_cast<size_t>(pl.n_vocab_tiles) * rows * 4, 256);
+    off = align_up(off + static_cast<size_t>(pl.n_partials) * rows * 4, 256);
     pl.off_l = off;
-    off = align_up(off + static_cast<size_t>(pl.n_vocab_tiles) * rows * 4, 256);
+    off = align_up(off + static_cast<size_t>(pl.n_partials) * rows * 4, 256);
     pl.off_zt = off;
     off = align_up(off + static_cast<size_t>(rows) * 4, 256);
     pl.off_part = off;

@@ -92,6 +92,11 @@ rl_status check_decode_ptrs(const DecodePlan &plan, const rl_decode_lens *lens,
 // A last round of lm-head tiles that would leave at least half the CUs idle
 // is split over the hidden dimension into up to this many parts.
 constexpr int kMaxTailSplits = 4;
+// Narrow last-round tiles are this many vocab entries wide; they need every
+// row tile of a vocab tile next to each other in launch order, which holds
+// for at most kNarrowMaxRowTiles row tiles.
+constexpr int64_t kNarrowWidth = 192;
+constexpr int64_t kNarrowMaxRowTiles = 4;
 
 struct LogprobPlan {
     int64_t R = 0;
@@ -102,6 +107,11 @@ struct LogprobPlan {
     // 256 x 256 tile each, at off_part) a reduce kernel sums
     int64_t n_dp_tiles = 0, n_tail_tiles = 0;
     int32_t tail_splits = 1;
+    // or: a last round more than half full runs as narrow_tiles tiles of
+    // kNarrowWidth vocab entries over [narrow_v0, V) (per row tile), their
+    // partials in slots narrow_slot0.. after the whole tiles' slots
+    int64_t narrow_v0 = 0, narrow_tiles = 0, narrow_slot0 = 0;
+    int64_t n_partials = 0;          // (max, sum) partial slots per row
     size_t off_m = 0, off_l = 0, off_zt = 0, off_part = 0, total_bytes = 0;
 };
 

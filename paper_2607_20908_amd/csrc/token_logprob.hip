@@ -42,25 +42,27 @@ static_assert(kBlocksPerWave == 8, "staging layout");
 // p = exp(inv_T z - lse) per (row, vocab entry) as bf16 into the blocked
 // probability buffer; or the sampling head's tempered fp32 logits (per-row
 // temperature) plus the tile's row maxima.
-enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2, kPartialK = 3 };
+// kNarrow is the forward over the narrow tiles of a last round (TM < 4).
+enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2, kPartialK = 3, kNarrow = 4 };
 
-// Forward epilogue of one 32-row column of a 256 x 256 logit tile, as one
+// Forward epilogue of one 32-row column of a (64 TM) x 256 logit tile, as one
 // lane of a wave holds it: z(tm)[i] is vocab vbase + tm*32 + 8*(i/4) + 4*h2 +
-// i%4 for token row rr (vbase = v0 + 128 * the wave's vocab half).  Returns
-// the row's max and sum of exp2 over the wave's 128 vocab entries (both lane
+// i%4 for token row rr (vbase = v0 + 32 TM * the wave's vocab half).  Returns
+// the row's max and sum of exp2 over the wave's 32 TM vocab entries (both lane
 // halves merged) and writes the target's logit if it falls among them.
-template <class Z>
+template <int TM, class Z>
 __device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t rr, int64_t vbase, int h2,
                                             float &mx_out, float &sum_out) {
+    constexpr int SPAN = 32 * TM;                // vocab entries per wave
     const float c2 = a.inv_temperature * kLog2e;
-    const bool full_vocab = vbase + 128 <= a.V;  // only the last vocab tile is masked
-    // the target's index among the wave's 128 vocab entries, shifted so that
+    const bool full_vocab = vbase + SPAN <= a.V;  // only the last vocab tile is masked
+    // the target's index among the wave's vocab entries, shifted so that
     // it compares against compile-time constants; -1 unless this lane's half
     // of the accumulator rows (bit 2 of the index) holds it
     int tsel = -1;
     if (rr < a.R) {
         const int64_t local = static_cast<int64_t>(a.target[rr]) - vbase;
-        if (local >= 0 && local < 128 && ((local >> 2) & 1) == h2) tsel = static_cast<int>(local) - 4 * h2;
+        if (local >= 0 && local < SPAN && ((local >> 2) & 1) == h2) tsel = static_cast<int>(local) - 4 * h2;
     }
     // one pass per 32-entry block: block max and sum, merged online into the
     // row's (mx, sum); each accumulator register is read once.  Only the last
@@ -75,7 +77,7 @@ __device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t r
     };
     if (full_vocab) {
 #pragma unroll
-        for (int tm = 0; tm < 4; ++tm) {
+        for (int tm = 0; tm < TM; ++tm) {
             const f32x16 zz = z(tm);
             float bm = fmaxf(fmaxf(zz[0], zz[1]), zz[2]);
 #pragma unroll
@@ -91,7 +93,7 @@ __device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t r
     } else {
         const int vlim = static_cast<int>(a.V - vbase) - 4 * h2;
 #pragma unroll
-        for (int tm = 0; tm < 4; ++tm) {
+        for (int tm = 0; tm < TM; ++tm) {
             const f32x16 zz = z(tm);
             float bm = -INFINITY;
 #pragma unroll
@@ -116,7 +118,7 @@ __device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t r
     if (__any(tsel >= 0)) {
         float zsel = 0.f;
 #pragma unroll
-        for (int tm = 0; tm < 4; ++tm) {
+        for (int tm = 0; tm < TM; ++tm) {
             const f32x16 zz = z(tm);
 #pragma unroll
             for (int i = 0; i < 16; ++i) zsel = tm * 32 + 8 * (i >> 2) + (i & 3) == tsel ? zz[i] : zsel;
@@ -131,7 +133,7 @@ __device__ __forceinline__ void row_partial(const LogprobArgs &a, Z z, int64_t r
     mx_out = nm;
 }
 
-// Writes the (max, sum) partial of (vocab tile vt, row rr) from the two vocab
+// Writes the (max, sum) partial of (partial slot vt, row rr) from the two vocab
 // halves' partials.
 __device__ __forceinline__ void write_partial(const LogprobArgs &a, int64_t vt, int64_t rr, float m0, float l0,
                                               float m1, float l1) {
@@ -140,25 +142,27 @@ __device__ __forceinline__ void write_partial(const LogprobArgs &a, int64_t vt, 
     a.pl[vt * a.R + rr] = l0 * fast_exp2(m0 - Mx) + l1 * fast_exp2(m1 - Mx);
 }
 
-// Forward epilogue of one 256 x 256 logit tile held in the registers of the
-// workgroup's 4 waves (acc[tm][tn][i] of wave (wm, wn), lane (h2, l32) holds
-// vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4 for token row
+// Forward epilogue of one (64 TM) x 256 logit tile held in the registers of
+// the workgroup's 4 waves (acc[tm][tn][i] of wave (wm, wn), lane (h2, l32)
+// holds vocab v0 + wm*32*TM + tm*32 + 8*(i/4) + 4*h2 + i%4 for token row
 // r0 + wn*128 + tn*32 + l32): per token row the max and the sum of exp2 over
 // the tile's vocab entries and, if the target falls in the tile, its logit.
-// `red` is 4 KB of LDS that the caller no longer uses.
-__device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 (&acc)[4][4], int64_t vt,
-                                             int64_t rt, float (*red)[kRowTile][2]) {
+// The partial goes to slot `slot`.  `red` is 4 KB of LDS that the caller no
+// longer uses.
+template <int TM>
+__device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 (&acc)[TM][4], int64_t v0,
+                                             int64_t slot, int64_t rt, float (*red)[kRowTile][2]) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave & 1, wn = wave >> 1;
     const int l32 = lane & 31, h2 = lane >> 5;
     const int64_t r0 = rt * kRowTile;
-    const int64_t vbase = vt * kVocabTile + wm * 128;
+    const int64_t vbase = v0 + wm * 32 * TM;
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn) {
         const int row = wn * 128 + tn * 32 + l32;
         float mx, sum;
-        row_partial(a, [&](int tm) -> const f32x16 & { return acc[tm][tn]; }, r0 + row, vbase, h2, mx, sum);
+        row_partial<TM>(a, [&](int tm) -> const f32x16 & { return acc[tm][tn]; }, r0 + row, vbase, h2, mx, sum);
         if (h2 == 0) {
             red[wm][row][0] = mx;
             red[wm][row][1] = sum;
@@ -169,24 +173,41 @@ __device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 
     }
     __syncthreads();
     const int64_t rr = r0 + tid;                 // 256 threads, 256 rows
-    if (rr < a.R) write_partial(a, vt, rr, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
+    if (rr < a.R) write_partial(a, slot, rr, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
 }
 
-template <int WS, int MODE>
+// TM: 32-entry vocab blocks per wave; a tile spans 64 TM vocab entries (4:
+// the 256 x 256 tiles; 3: the narrow tiles of a last round, kNarrow).
+template <int WS, int MODE, int TM = 4>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
-    // WS x 32 KB weight stages + 2 x 32 KB hidden stages; the epilogue's
-    // reduction area reuses the weight ring once the loop is done
-    __shared__ __attribute__((aligned(16))) uint16_t wring[WS * kTileElems];
+    static_assert(TM == 4 || MODE == kNarrow, "narrow tiles are forward-only");
+    constexpr int VW = 64 * TM;                  // vocab entries per tile
+    constexpr int WELEMS = VW * kK;              // bf16 elements of one weight stage
+    constexpr int WBLK = VW / 32;                // 1 KB weight blocks per wave per stage
+    // WS weight stages + 2 x 32 KB hidden stages; the epilogue's reduction
+    // area reuses the weight ring once the loop is done
+    __shared__ __attribute__((aligned(16))) uint16_t wring[WS * WELEMS];
     __shared__ __attribute__((aligned(16))) uint16_t hring[kHStages * kTileElems];
     float (*red)[kRowTile][2] = reinterpret_cast<float (*)[kRowTile][2]>(wring);   // [vocab half][row][m, l]
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;     // vocab half (128 entries), row half (128 rows)
+    const int wm = wave & 1, wn = wave >> 1;     // vocab half (32 TM entries), row half (128 rows)
     const int l32 = lane & 31, h2 = lane >> 5;
-    int64_t vt, rt;
+    int64_t vt, rt, v0;                          // vt: the partial slot of the tile
     int kb = 0, nks = a.H / kK;                  // hidden steps [kb, kb + nks)
-    if constexpr (MODE == kPartialK) {
+    if constexpr (MODE == kNarrow) {
+        // narrow tile j covers vocab [narrow_v0 + j VW, + VW) for row tile
+        // rt; the row tiles of one j are neighbours in launch order, which
+        // gives each XCD a contiguous run as tile_of does
+        const int64_t count = a.narrow_tiles * a.n_row_tiles, b = blockIdx.x;
+        const int64_t full = count / 8 * 8;
+        const int64_t L = b < full ? (b % 8) * (count / 8) + b / 8 : b;
+        const int64_t j = L / a.n_row_tiles;
+        rt = L % a.n_row_tiles;
+        vt = a.narrow_slot0 + j;
+        v0 = a.narrow_v0 + j * VW;
+    } else if constexpr (MODE == kPartialK) {
         // part s of tail tile j covers hidden steps [s n / S, (s + 1) n / S)
         const int64_t j = blockIdx.x / a.splits;
         const int sp = static_cast<int>(blockIdx.x % a.splits);
@@ -199,23 +220,24 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         tile_of(blockIdx.x, static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles, 0, a.n_vocab_tiles,
                 a.n_row_tiles, &vt, &rt);
     }
-    const int64_t v0 = vt * kVocabTile, r0 = rt * kRowTile;
+    if constexpr (MODE != kNarrow) v0 = vt * kVocabTile;
+    const int64_t r0 = rt * kRowTile;
     const int64_t H = a.H;
 
-    // ---- staging: each wave fills 8 blocks of 8 rows per operand per stage.
+    // ---- staging: each wave fills 2 TM blocks of 8 weight rows and 8 blocks
+    // of 8 hidden rows per stage.
     // Lane i of a block covers row 8*block + i/8 and LDS slot i%8 of that row,
     // which holds chunk (i%8) ^ swizzle(row), so the LDS image is op_off's.
     // Rows past the vocabulary / the batch re-read the last valid row.
     const uint16_t *wg = a.w + v0 * H;
     const uint16_t *hg = a.hidden + r0 * H;
-    const int wlast = static_cast<int>(min(static_cast<int64_t>(kVocabTile - 1), a.V - 1 - v0));
+    const int wlast = static_cast<int>(min(static_cast<int64_t>(VW - 1), a.V - 1 - v0));
     const int hlast = static_cast<int>(min(static_cast<int64_t>(kRowTile - 1), a.R - 1 - r0));
     // Block j of stage `slot`'s buffer gets the data of stage min(slot, nks-1):
     // past the last stage the loads refill a buffer nobody reads any more.
-    auto wbuf = [&](int ks) { return wring + (ks % WS) * kTileElems; };
+    auto wbuf = [&](int ks) { return wring + (ks % WS) * WELEMS; };
     auto hbuf = [&](int ks) { return hring + (ks & 1) * kTileElems; };
-    auto issue_block = [&](const uint16_t *g, int last, uint16_t *st, int slot, int j) {
-        const int blk = wave * kBlocksPerWave + j;
+    auto issue_block = [&](const uint16_t *g, int last, uint16_t *st, int slot, int blk) {
         const int row = blk * 8 + (lane >> 3);
         const int c = (lane & 7) ^ ((row >> 1) & 7);
         const int64_t k0 = static_cast<int64_t>(kb + min(slot, nks - 1)) * kK;
@@ -223,31 +245,32 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     };
     auto issue_w = [&](int slot) {
 #pragma unroll
-        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(wg, wlast, wbuf(slot), slot, j);
+        for (int j = 0; j < WBLK; ++j) issue_block(wg, wlast, wbuf(slot), slot, wave * WBLK + j);
     };
     auto issue_h = [&](int slot) {
 #pragma unroll
-        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(hg, hlast, hbuf(slot), slot, j);
+        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(hg, hlast, hbuf(slot), slot, wave * kBlocksPerWave + j);
     };
 
-    f32x16 acc[4][4];
+    f32x16 acc[TM][4];
 #pragma unroll
-    for (int tm = 0; tm < 4; ++tm)
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = f32x16{};
-    bf16x8 fa[2][4], fb[2][4];
+    bf16x8 fa[2][TM], fb[2][4];
     auto read_frags = [&](int ks, int kq, int p) {
         const uint16_t *as = wbuf(ks);
         const uint16_t *bs = hbuf(ks);
         const int c = kq * 2 + h2;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) fa[p][i] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + i * 32 + l32, c));
+        for (int i = 0; i < TM; ++i)
+            fa[p][i] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 32 * TM + i * 32 + l32, c));
 #pragma unroll
         for (int j = 0; j < 4; ++j) fb[p][j] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + j * 32 + l32, c));
     };
     auto mfma16 = [&](int p) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
@@ -266,7 +289,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     issue_h(1);
     issue_w(1);
     if (WS == 3) issue_w(2);
-    wait_vm<(WS == 3 ? 3 : 2) * kBlocksPerWave>();   // stage 0 has landed
+    wait_vm<kBlocksPerWave + (WS == 3 ? 2 : 1) * WBLK>();   // stage 0 has landed
     barrier();
     read_frags(0, 0, 0);
     for (int ks = 0; ks < nks; ++ks) {
@@ -275,15 +298,15 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             read_frags(ks, kq + 1, (kq + 1) & 1);
             mfma16(kq & 1);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
+            for (int i = 0; i < TM + 4; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4 * TM - (TM + 4), 0);
         }
         // last k-step: stage ks+1 has landed (only the weights of stage ks+2
         // may still be in flight) and every wave is done reading stage ks
-        wait_vm<(WS == 3 ? 1 : 0) * kBlocksPerWave>();
+        wait_vm<(WS == 3 ? 1 : 0) * WBLK>();
         wait_lds();
         barrier();
         // eight groups of: two global->LDS loads (hidden rows of stage ks+2
@@ -296,18 +319,22 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
                 if (g < 4) {
-                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, 2 * g);
-                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, 2 * g + 1);
+                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g);
+                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g + 1);
                 } else {
-                    issue_block(wg, wlast, wbuf(ks + WS), ks + WS, 2 * (g - 4));
-                    issue_block(wg, wlast, wbuf(ks + WS), ks + WS, 2 * (g - 4) + 1);
+#pragma unroll
+                    for (int jj = 2 * (g - 4); jj < 2 * (g - 4) + 2; ++jj)
+                        if (jj < WBLK) issue_block(wg, wlast, wbuf(ks + WS), ks + WS, wave * WBLK + jj);
                 }
 #pragma unroll
                 for (int m = 2 * g; m < 2 * g + 2; ++m)
-                    acc[m >> 2][m & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][m >> 2], fb[1][m & 3],
-                                                                                 acc[m >> 2][m & 3], 0, 0, 0);
-                if (g < 4) fa[0][g] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + g * 32 + l32, h2));
-                else fb[0][g - 4] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + (g - 4) * 32 + l32, h2));
+                    if (m < 4 * TM)
+                        acc[m >> 2][m & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][m >> 2], fb[1][m & 3],
+                                                                                     acc[m >> 2][m & 3], 0, 0, 0);
+                if (g < TM)
+                    fa[0][g] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 32 * TM + g * 32 + l32, h2));
+                else if (g >= 4)
+                    fb[0][g - 4] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + (g - 4) * 32 + l32, h2));
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -412,7 +439,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 }
         return;
     }
-    fwd_epilogue(a, acc, vt, rt, red);
+    fwd_epilogue<TM>(a, acc, v0, vt, rt, red);
 }
 
 // Sums the hidden-dimension parts of the tail tiles (in a fixed order) and
@@ -452,7 +479,7 @@ __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a)
     const int row = tn * 32 + l32;               // within the row half
     const int64_t rr = rt * kRowTile + wn * 128 + row;
     float mx, sum;
-    row_partial(a, [&](int tm) -> const f32x16 & { return z[tm]; }, rr, vt * kVocabTile + wm * 128, h2, mx, sum);
+    row_partial<4>(a, [&](int tm) -> const f32x16 & { return z[tm]; }, rr, vt * kVocabTile + wm * 128, h2, mx, sum);
     if (h2 == 0) {
         red[wm][l32][0] = mx;
         red[wm][l32][1] = sum;
@@ -491,7 +518,7 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_wave_kernel(LogprobA
     const int64_t r = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
     if (r >= a.R) return;
     float M = -INFINITY, L = 0.f;
-    for (int64_t vt = lane; vt < a.n_vocab_tiles; vt += 64) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
+    for (int64_t vt = lane; vt < a.n_partials; vt += 64) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
     const float Mw = wave_max(M);
     const float Lw = wave_sum(M == -INFINITY ? 0.f : L * fast_exp2(M - Mw));
     if (lane == 0) finish_row(a, r, Mw, Lw);
@@ -504,7 +531,7 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
     if (r >= a.R) return;
     float M = -INFINITY, L = 0.f;
     int64_t vt = 0;
-    for (; vt + 4 <= a.n_vocab_tiles; vt += 4) {
+    for (; vt + 4 <= a.n_partials; vt += 4) {
         float m[4], l[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -514,7 +541,7 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
 #pragma unroll
         for (int j = 0; j < 4; ++j) lse_merge(M, L, m[j], l[j]);
     }
-    for (; vt < a.n_vocab_tiles; ++vt) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
+    for (; vt < a.n_partials; ++vt) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
     finish_row(a, r, M, L);
 }
 
@@ -533,6 +560,16 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
                            dim3(kTileThreads), 0, stream, d);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (a.narrow_tiles > 0) {
+        // the last round as narrow tiles, 192 vocab entries wide (the plan
+        // allows them only for at most 4 row tiles, so the 3-stage weight
+        // ring applies)
+        static_assert(kNarrowWidth == 64 * 3, "narrow tile width");
+        const uint32_t blocks = static_cast<uint32_t>(a.narrow_tiles * a.n_row_tiles);
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (a.tail_tiles > 0) {
         // the tail: `splits` hidden-dimension parts per tile, then their sum
         LogprobArgs t = a;

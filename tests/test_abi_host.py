@@ -192,15 +192,44 @@ def tail_part_bytes(R, H, V, cus=256, max_splits=4):
     return tail * s * 256 * 256 * 4
 
 
+def narrow_tiles(R, H, V, cus=256, width=192):
+    """(whole vocab tiles before the narrow region, narrow tiles per row
+    tile) when a last round of 256 x 256 tiles more than half full runs as
+    192-wide tiles (at most 4 row tiles, one round of them), else None."""
+    nrt = -(-R // 256)
+    tiles = -(-V // 256) * nrt
+    dp, tail = tiles // cus * cus, tiles % cus
+    if dp == 0 or tail == 0 or tail_part_bytes(R, H, V) or nrt > 4:
+        return None
+    vt0 = dp // nrt
+    n = -(-(V - vt0 * 256) // width)
+    return (vt0, n) if n * nrt <= cus else None
+
+
 def test_logprob_workspace_size():
-    # per (vocab tile of 256, row): max and sum; per row: the target logit;
-    # the tail's partial accumulators when the last round is split
+    # per (partial slot, row): max and sum, one slot per vocab tile (the
+    # narrow tiles of a last round have their own); per row: the target
+    # logit; the tail's partial accumulators when the last round is split
     for R, H, V in ((1000, 5120, 151936), (256, 5120, 151936), (512, 4096, 151936), (40, 64, 1000),
-                    (256, 256, 76800), (262144, 5120, 151936)):
+                    (256, 256, 76800), (262144, 5120, 151936), (300, 512, 51001), (600, 512, 35700),
+                    (1000, 512, 25500)):
         n = rk.token_logprob_workspace_size(R, H, V)
-        tiles = -(-V // 256)
-        base = (2 * tiles * R + R) * 4 + tail_part_bytes(R, H, V)
+        nt = narrow_tiles(R, H, V)
+        slots = -(-V // 256) if nt is None else nt[0] + nt[1]
+        base = (2 * slots * R + R) * 4 + tail_part_bytes(R, H, V)
         assert base <= n < base + 3 * 256, (R, H, V)
+    # the 8B-class step (1188 tiles: 4 rounds + 164) runs its last round as
+    # 109 x 2 tiles 192 wide over vocab [131072, 151936); the 32B-class one
+    # (594 tiles: 2 rounds + 82) splits its tail instead; the policy pass
+    # has no partial round; 5 row tiles are too many for narrow tiles
+    assert narrow_tiles(512, 4096, 151936) == (512, 109)
+    assert narrow_tiles(256, 5120, 151936) is None
+    assert narrow_tiles(262144, 5120, 151936) is None
+    assert narrow_tiles(300, 512, 51001) == (128, 95)
+    assert narrow_tiles(600, 512, 35700) == (85, 73)      # 255 whole tiles: 85 per row tile
+    assert narrow_tiles(1000, 512, 25500) == (64, 48)
+    assert narrow_tiles(1200, 512, 20000) is None         # 5 row tiles
+    assert narrow_tiles(200, 512, 55000) is None          # 215 tiles: no full round
     # the 32B-class decode step (594 tiles: 2 rounds + 82) splits its tail
     # 3 ways; the 8B-class one (1188 tiles: 4 rounds + 164) does not split
     assert tail_part_bytes(256, 5120, 151936) == 82 * 3 * 256 * 256 * 4
