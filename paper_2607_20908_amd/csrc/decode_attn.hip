@@ -301,91 +301,111 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
     }
 }
 
-// One wave per (sequence s, query head h): merge the partials of the prompt's
-// prefix chunks and the candidate's suffix chunks.
-template <int D>
-__global__ __launch_bounds__(kThreads) void decode_combine_kernel(DecodeArgs a) {
+// Merges, per (sequence s, query head h) row, the partials of the prompt's
+// prefix chunks and the candidate's suffix chunks.  RPW rows per wave, 64 /
+// RPW lanes per row (row x of a wave in lanes x 64/RPW ..); the cross-lane
+// reductions stay inside a row's lanes.  Two rows per wave put an 8B- or
+// 32B-class step's 16384 rows in one round of resident waves; with few rows
+// one row per wave keeps more waves, and loads, in flight.
+// NB: value rows loaded per batch.  NB = 4 at D = 128 keeps the two-row
+// kernel within 64 VGPRs, so 8 waves fit on a SIMD.
+template <int D, int RPW, int NB>
+__global__ __launch_bounds__(kThreads, NB == 4 ? 8 : 1) void decode_combine_kernel(DecodeArgs a) {
     release_staging(a.release);
-    constexpr int PER_LANE = D / 64;
+    constexpr int LPR = 64 / RPW;                // lanes per row
+    constexpr int PER_LANE = D / LPR;
+    typedef float fvec __attribute__((ext_vector_type(PER_LANE)));
     const int lane = threadIdx.x & 63;
-    const int64_t idx = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
-    const int64_t S = static_cast<int64_t>(a.P) * a.G;
-    if (idx >= S * a.Hq) return;
-    const int64_t s = idx / a.Hq;
-    const int h = static_cast<int>(idx % a.Hq);
+    const int slot = lane / LPR, hl = lane % LPR;
+    const int64_t rows = static_cast<int64_t>(a.P) * a.G * a.Hq;
+    const int64_t idx = (static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6)) * RPW + slot;
+    const bool live = idx < rows;                // the last wave's second row may be past the end
+    const int64_t ix = live ? idx : 0;
+    const int64_t s = ix / a.Hq;
+    const int h = static_cast<int>(ix % a.Hq);
     const int64_t p = s / a.G;
     const int g = static_cast<int>(s % a.G);
     const int kh = h / a.r, hr = h % a.r;
     const DevUnit pu = a.prefix_units[p * a.Hkv + kh];
     const DevUnit su = a.suffix_units[s * a.Hkv + kh];
     const int64_t Mp = static_cast<int64_t>(a.G) * a.r;
-    const int n = pu.nchunks + su.nchunks;
+    const int n = live ? pu.nchunks + su.nchunks : 0;
     auto prow = [&](int j) -> int64_t {
         return j < pu.nchunks ? pu.base + j * Mp + g * a.r + hr
                               : su.base + static_cast<int64_t>(j - pu.nchunks) * a.r + hr;
     };
-    float Mx = -INFINITY;
-    float L = 0.f, o[PER_LANE];
+    auto row_max = [](float v) {
 #pragma unroll
-    for (int e = 0; e < PER_LANE; ++e) o[e] = 0.f;
-    if (n <= 64) {
-        // lane j holds partial j's (m, l): one load latency for all of them;
-        // the value rows load 8 at a time (the first 8 alongside the (m, l),
-        // as they do not depend on the weights), each weight taken by readlane
+        for (int o = LPR / 2; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+        return v;
+    };
+    auto row_sum = [](float v) {
+#pragma unroll
+        for (int o = LPR / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+        return v;
+    };
+    // the largest partial count of the wave's rows, the same in every lane
+    const int nw = __builtin_amdgcn_readfirstlane(RPW == 2 ? max(n, __shfl_xor(n, 32, 64)) : n);
+    float Mx = -INFINITY, L = 0.f;
+    fvec o = {};
+    if (nw <= LPR) {
+        // lane j of a row holds partial j's (m, l): one load latency for all of
+        // them; the value rows load NB at a time (the first NB alongside the
+        // (m, l), as they do not depend on the weights), each weight taken by
+        // readlane from the row's own lanes
         float mj = -INFINITY, lj = 0.f;
-        if (lane < n) {
-            const int64_t pr = prow(lane);
+        if (hl < n) {
+            const int64_t pr = prow(hl);
             mj = a.pm[pr];
             lj = a.pl[pr];
         }
-        float v[8][PER_LANE];
+        fvec v[NB];
         auto load_rows = [&](int j0) {
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (j0 + u < n) {
-                    const int64_t pr = prow(j0 + u);
-#pragma unroll
-                    for (int e = 0; e < PER_LANE; ++e) v[u][e] = a.pacc[pr * D + lane * PER_LANE + e];
-                }
-            }
+            for (int u = 0; u < NB; ++u)
+                if (j0 + u < n) v[u] = *reinterpret_cast<const fvec *>(a.pacc + prow(j0 + u) * D + hl * PER_LANE);
         };
         load_rows(0);
-        Mx = wave_max(mj);
-        const float fj = lane < n ? fast_exp2(mj - Mx) : 0.f;
-        L = wave_sum(fj * lj);
-        for (int j0 = 0; j0 < n; j0 += 8) {
+        Mx = row_max(mj);
+        const float fj = hl < n ? fast_exp2(mj - Mx) : 0.f;
+        L = row_sum(fj * lj);
+        for (int j0 = 0; j0 < nw; j0 += NB) {
             if (j0 > 0) load_rows(j0);
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (j0 + u < n) {
-                    const float f = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fj), j0 + u));
-#pragma unroll
-                    for (int e = 0; e < PER_LANE; ++e) o[e] += f * v[u][e];
+            for (int u = 0; u < NB; ++u) {
+                if (j0 + u < nw) {               // uniform: the lanes read below are < 64
+                    const float f0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fj), j0 + u));
+                    float f = f0;
+                    if constexpr (RPW == 2) {
+                        const float f1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fj), 32 + j0 + u));
+                        f = slot ? f1 : f0;
+                    }
+                    if (j0 + u < n) o += f * v[u];
                 }
             }
         }
     } else {
-        for (int j = lane; j < n; j += 64) Mx = fmaxf(Mx, a.pm[prow(j)]);
-        Mx = wave_max(Mx);
+        for (int j = hl; j < n; j += LPR) Mx = fmaxf(Mx, a.pm[prow(j)]);
+        Mx = row_max(Mx);
         for (int j = 0; j < n; ++j) {
             const int64_t pr = prow(j);
             const float f = fast_exp2(a.pm[pr] - Mx);
             L += f * a.pl[pr];
-#pragma unroll
-            for (int e = 0; e < PER_LANE; ++e) o[e] += f * a.pacc[pr * D + lane * PER_LANE + e];
+            o += f * *reinterpret_cast<const fvec *>(a.pacc + pr * D + hl * PER_LANE);
         }
     }
-    uint16_t *out = a.out + idx * D + lane * PER_LANE;
+    if (!live) return;
+    uint16_t *out = a.out + idx * D + hl * PER_LANE;
     if (n == 0) {
 #pragma unroll
         for (int e = 0; e < PER_LANE; ++e) out[e] = 0;
-        if (a.lse && lane == 0) a.lse[idx] = -INFINITY;
+        if (a.lse && hl == 0) a.lse[idx] = -INFINITY;
         return;
     }
     const float inv = 1.f / L;
 #pragma unroll
     for (int e = 0; e < PER_LANE; ++e) out[e] = f32_to_bf16_bits(o[e] * inv);
-    if (a.lse && lane == 0) a.lse[idx] = (Mx + fast_log2(L)) * kLn2;
+    if (a.lse && hl == 0) a.lse[idx] = (Mx + fast_log2(L)) * kLn2;
 }
 
 __global__ __launch_bounds__(kThreads) void plan_fetch_kernel(const u32x4 *__restrict__ src,
@@ -402,10 +422,18 @@ hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const int64_t waves = static_cast<int64_t>(a.P) * a.G * a.Hq;
-    const int64_t blocks = (waves + 3) / 4;
-    hipLaunchKernelGGL(decode_combine_kernel<D>, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
-                       stream, a);
+    // one row per wave while the rows fit one round of resident waves (8 per
+    // SIMD), two per wave (NB = 4 at D = 128, 8 waves per SIMD) beyond
+    const int64_t rows = static_cast<int64_t>(a.P) * a.G * a.Hq;
+    if (rows > 8 * 4 * kNumCUs) {
+        const int64_t blocks = ((rows + 1) / 2 + 3) / 4;
+        hipLaunchKernelGGL((decode_combine_kernel<D, 2, D == 128 ? 4 : 8>), dim3(static_cast<uint32_t>(blocks)),
+                           dim3(kThreads), 0, stream, a);
+    } else {
+        const int64_t blocks = (rows + 3) / 4;
+        hipLaunchKernelGGL((decode_combine_kernel<D, 1, 8>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
+                           stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -86,6 +86,20 @@ def test_group_shapes(G, Hq, Hkv):
     check(c, 1.0 / math.sqrt(128), 32, f"G={G} Hq={Hq} Hkv={Hkv}", "head")
 
 
+@pytest.mark.parametrize("D", [64, 128])
+def test_many_rows_many_partials(D):
+    """More rows than one round of one-row waves (16384 > 8192), so the
+    combine runs two rows per wave, with 16-token chunks, so rows merge 10 to
+    about 40 partials: the value batches (4 rows at D = 128) and the path for
+    more than 32 partials of that launch both run."""
+    P, G, Hq, Hkv = 16, 8, 128, 8
+    rng = np.random.Generator(np.random.PCG64(4242 + D))
+    lp = rng.integers(150, 220, P)
+    ls = rng.integers(1, 420, P * G)
+    c = decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=77 + D, gap=2)
+    check(c, 1.0 / math.sqrt(D), 16, f"16384 rows, 16-token chunks, D={D}", "head")
+
+
 def test_peaky_scores():
     c = decode_host_case(2, 4, 8, 2, 128, [200, 77], [40, 0, 90, 5, 66, 1, 0, 130], seed=9,
                          qmul=4.0, gap=2)
