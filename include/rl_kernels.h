@@ -147,9 +147,15 @@ typedef struct {
  * Status: NULL pointer -> RL_ERR_NULL_POINTER; negative sizes or lengths,
  * Hq % Hkv != 0, a range past prefix_rows/suffix_rows, a non-finite or
  * non-positive scale, a bad split_tokens or kv_layout -> RL_ERR_INVALID_SHAPE;
- * D not in {64, 128} or Hq/Hkv > 128 -> RL_ERR_UNSUPPORTED; a device pointer
- * not 16-byte aligned -> RL_ERR_MISALIGNED; workspace NULL or short ->
- * RL_ERR_WORKSPACE.
+ * D not in {64, 128}, Hq/Hkv > 128, Hkv > 256, G*Hq/Hkv > 16384, or
+ * prefix_rows / suffix_rows of 2^32 or more -> RL_ERR_UNSUPPORTED (the work
+ * list uploaded on every call packs these into 16 bytes per item); a device
+ * pointer not 16-byte aligned -> RL_ERR_MISALIGNED; workspace NULL or short ->
+ * RL_ERR_WORKSPACE.  A split_tokens above 16384 acts as 16384.
+ *
+ * The workspace holds the work list (16 bytes per item, 8 bytes per prompt and
+ * per candidate) and the split partials (max, sum and D fp32 values per
+ * query row of each item).
  */
 rl_status rl_decode_attn_workspace_size(const rl_decode_shape *shape,
                                         const rl_decode_lens *lens,

@@ -81,23 +81,25 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
     const DevItem it = a.items[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g4 = lane >> 4, l16 = lane & 15;
-    const int kh = it.kind_kh & 0xffff;
-    const bool is_suffix = (it.kind_kh >> 16) & 1;
+    const int kh = (it.meta >> 16) & 255;
+    const bool is_suffix = (it.meta >> 15) & 1;
+    const int row_begin = static_cast<int>(it.meta >> 24) * kMaxItemRows;
     const int M = is_suffix ? a.r : a.G * a.r;
-    const int rows = min(kMaxItemRows, M - it.row_begin);
+    const int rows = min(kMaxItemRows, M - row_begin);
     const int n_ct = (rows + 15) >> 4;
     const int Wc = n_ct == 1 ? 1 : (n_ct == 2 ? 2 : 4);
     const int Wt = 4 / Wc;
     const int nst = kSubPerTile / Wt;            // sub-tiles per wave per tile
     const int wc = wave % Wc, wt = wave / Wc;
     const bool mine = wc < n_ct;                 // this wave has a column tile
-    const int ntok = it.ntok;
+    const int ntok = static_cast<int>(it.meta & 0x7fff);
     // token-major [rows, Hkv, D]: rows of one kv head are Hkv*D apart;
     // head-major [Hkv, rows, D]: they are contiguous
     const bool head_major = a.kv_layout == RL_KV_HEAD_MAJOR;
     const int64_t nrows = is_suffix ? a.suffix_rows : a.prefix_rows;
     const int64_t tok_stride = head_major ? D : static_cast<int64_t>(a.Hkv) * D;
-    const int64_t base = head_major ? (kh * nrows + it.kv_row0) * D : (it.kv_row0 * a.Hkv + kh) * D;
+    const int64_t kv_row0 = it.kv_row0;
+    const int64_t base = head_major ? (kh * nrows + kv_row0) * D : (kv_row0 * a.Hkv + kh) * D;
     const uint16_t *kg = (is_suffix ? a.k_suffix : a.k_prefix) + base;
     const uint16_t *vg = (is_suffix ? a.v_suffix : a.v_prefix) + base;
 
@@ -108,7 +110,7 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
         const bool ok = mine && i < rows;
         int64_t qoff = 0;
         if (ok) {
-            const int ig = it.row_begin + i;         // row within the unit
+            const int ig = row_begin + i;            // row within the unit
             int s, h;
             if (is_suffix) { s = it.unit; h = kh * a.r + ig; }
             else           { s = it.unit * a.G + ig / a.r; h = kh * a.r + ig % a.r; }
@@ -255,7 +257,7 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
         // every row belongs to one wave: write its partial from the registers
         const int i = wc * 16 + l16;
         if (mine && i < rows) {
-            const int64_t prow = it.partial_row0 + i;
+            const int64_t prow = static_cast<int64_t>(it.partial_row0) + i;
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt)
                 *reinterpret_cast<f32x4 *>(a.pacc + prow * D + dt * 16 + g4 * 4) = acc[dt];
@@ -292,7 +294,7 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
             L += f * red_ml[slot * 2 + 1];
             A += f * red_acc[slot * C::RED_STRIDE + d];
         }
-        const int64_t prow = it.partial_row0 + i;
+        const int64_t prow = static_cast<int64_t>(it.partial_row0) + i;
         a.pacc[prow * D + d] = A;
         if (d == 0) {
             a.pm[prow] = Mx;
@@ -326,13 +328,16 @@ __global__ __launch_bounds__(kThreads, NB == 4 ? 8 : 1) void decode_combine_kern
     const int64_t p = s / a.G;
     const int g = static_cast<int>(s % a.G);
     const int kh = h / a.r, hr = h % a.r;
-    const DevUnit pu = a.prefix_units[p * a.Hkv + kh];
-    const DevUnit su = a.suffix_units[s * a.Hkv + kh];
+    const DevUnit pu = a.prefix_units[p];
+    const DevUnit su = a.suffix_units[s];
     const int64_t Mp = static_cast<int64_t>(a.G) * a.r;
-    const int n = live ? pu.nchunks + su.nchunks : 0;
+    const int pn = static_cast<int>(pu.nchunks);
+    const int n = live ? pn + static_cast<int>(su.nchunks) : 0;
+    // this kv head's partial rows of the prompt's prefix and the candidate's suffix
+    const int64_t pbase = pu.base + static_cast<int64_t>(kh) * pu.nchunks * Mp + g * a.r + hr;
+    const int64_t sbase = su.base + static_cast<int64_t>(kh) * su.nchunks * a.r + hr;
     auto prow = [&](int j) -> int64_t {
-        return j < pu.nchunks ? pu.base + j * Mp + g * a.r + hr
-                              : su.base + static_cast<int64_t>(j - pu.nchunks) * a.r + hr;
+        return j < pn ? pbase + j * Mp : sbase + static_cast<int64_t>(j - pn) * a.r;
     };
     auto row_max = [](float v) {
 #pragma unroll

@@ -131,6 +131,10 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     const int64_t Mp = G * r;                       // query rows per prefix unit
     const int64_t ncg = ceil_div(Mp, kMaxItemRows); // column groups per prefix chunk
     if (r > kMaxHeadsPerKv) return fail(err, RL_ERR_UNSUPPORTED, "Hq/Hkv must be <= 128");
+    if (Hkv > kMaxDecodeKvHeads) return fail(err, RL_ERR_UNSUPPORTED, "num_kv_heads must be <= 256");
+    if (Mp > kMaxUnitRows) return fail(err, RL_ERR_UNSUPPORTED, "group_size * Hq/Hkv must be <= 16384");
+    if (lens->prefix_rows > kMaxDecodeRows || lens->suffix_rows > kMaxDecodeRows)
+        return fail(err, RL_ERR_UNSUPPORTED, "prefix_rows and suffix_rows must be < 2^32");
     int64_t cs, cp;
     if (sh.split_tokens > 0) {
         cs = cp = sh.split_tokens;
@@ -144,6 +148,10 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
         cp = std::max<int64_t>(cs, round_up16(32 * std::min<int64_t>(Mp, kMaxItemRows)));
         cp = std::min<int64_t>(cp, 16384);
     }
+    // a forced split above the item limit covers fewer tokens per item,
+    // which the split bound allows
+    cp = std::min<int64_t>(cp, kMaxItemTokens);
+    cs = std::min<int64_t>(cs, kMaxItemTokens);
     pl.split_prefix = static_cast<int32_t>(cp);
     pl.split_suffix = static_cast<int32_t>(cs);
 
@@ -151,26 +159,25 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     // A unit of L tokens splits into n = ceil(L / C) chunks of b = ceil(L / n)
     // tokens rounded up to 16 (the last one shorter), each chunk into
     // ceil(M / kMaxItemRows) items of at most kMaxItemRows query rows.
-    pl.prefix_units.assign(P * Hkv, DevUnit{0, 0, 0});
-    pl.suffix_units.assign(S * Hkv, DevUnit{0, 0, 0});
+    // The kv heads of a unit follow each other, so one table entry per unit
+    // serves them all.
+    pl.prefix_units.assign(P, DevUnit{0, 0});
+    pl.suffix_units.assign(S, DevUnit{0, 0});
     int64_t prow = 0, n_items = 0;
     auto size_unit = [&](int64_t L, int64_t C, int64_t M, DevUnit *du) {
-        du->base = prow;
         const int64_t n = L == 0 ? 0 : ceil_div(L, C);
-        du->nchunks = static_cast<int32_t>(n);
-        prow += n * M;
-        n_items += n * ceil_div(M, kMaxItemRows);
+        du->base = static_cast<uint32_t>(std::min(prow, kMaxDecodeRows));   // checked below
+        du->nchunks = static_cast<uint32_t>(n);
+        prow += Hkv * n * M;
+        n_items += Hkv * n * ceil_div(M, kMaxItemRows);
     };
-    for (int64_t p = 0; p < P; ++p)
-        for (int64_t kh = 0; kh < Hkv; ++kh)
-            size_unit(lens->prefix_len[p], cp, Mp, &pl.prefix_units[p * Hkv + kh]);
-    for (int64_t s = 0; s < S; ++s)
-        for (int64_t kh = 0; kh < Hkv; ++kh)
-            size_unit(lens->suffix_len[s], cs, r, &pl.suffix_units[s * Hkv + kh]);
+    for (int64_t p = 0; p < P; ++p) size_unit(lens->prefix_len[p], cp, Mp, &pl.prefix_units[p]);
+    for (int64_t s = 0; s < S; ++s) size_unit(lens->suffix_len[s], cs, r, &pl.suffix_units[s]);
     pl.partial_rows = prow;
     pl.n_items = n_items;
     if (n_items > static_cast<int64_t>(INT32_MAX))
         return fail(err, RL_ERR_UNSUPPORTED, "too many work items");
+    if (prow > kMaxDecodeRows) return fail(err, RL_ERR_UNSUPPORTED, "too many partial rows (2^32 or more)");
 
     if (detail != PlanDetail::kSizes) {
         // --- items in creation order with their cost -----------------------------
@@ -187,17 +194,17 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
             const int64_t n = du.nchunks;
             if (n == 0) return;
             const int64_t b = round_up16(ceil_div(L, n));
+            const int64_t base = du.base + kh * n * M;
             for (int64_t c = 0; c < n; ++c) {
                 const int64_t beg = c * b, cnt = std::min(b, L - beg);
                 for (int64_t rb = 0; rb < M; rb += kMaxItemRows) {
                     const int64_t rows = std::min<int64_t>(kMaxItemRows, M - rb);
                     DevItem &d = tmp[w];
-                    d.kv_row0 = start + beg;
-                    d.partial_row0 = du.base + c * M + rb;
-                    d.ntok = static_cast<int32_t>(cnt);
-                    d.kind_kh = kh | (kind << 16);
+                    d.kv_row0 = static_cast<uint32_t>(start + beg);
+                    d.partial_row0 = static_cast<uint32_t>(base + c * M + rb);
                     d.unit = unit;
-                    d.row_begin = static_cast<int32_t>(rb);
+                    d.meta = static_cast<uint32_t>(cnt) | (static_cast<uint32_t>(kind) << 15) |
+                             (static_cast<uint32_t>(kh) << 16) | (static_cast<uint32_t>(rb / kMaxItemRows) << 24);
                     const uint64_t cost = static_cast<uint64_t>(cnt) * kv_bytes_per_tok +
                                           static_cast<uint64_t>(rows) * partial_bytes_per_row;
                     key[w] = cost;
@@ -209,11 +216,11 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
         for (int64_t p = 0; p < P; ++p)
             for (int64_t kh = 0; kh < Hkv; ++kh)
                 add_items(0, (int32_t)p, (int32_t)kh, lens->prefix_start[p], lens->prefix_len[p], Mp,
-                          pl.prefix_units[p * Hkv + kh]);
+                          pl.prefix_units[p]);
         for (int64_t s = 0; s < S; ++s)
             for (int64_t kh = 0; kh < Hkv; ++kh)
                 add_items(1, (int32_t)s, (int32_t)kh, lens->suffix_start[s], lens->suffix_len[s], r,
-                          pl.suffix_units[s * Hkv + kh]);
+                          pl.suffix_units[s]);
 
         // --- launch order: longest work first, ties in creation order ------------
         // Stable LSD radix sort of (max_cost - cost) in 8-bit digits; the item
@@ -248,18 +255,18 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
                 const DevItem &d = pl.dev_items[i];
                 rl_plan_item &it = pl.items[i];
                 it = rl_plan_item{};
-                it.kind = (d.kind_kh >> 16) & 1;
+                it.kind = (d.meta >> 15) & 1;
                 it.unit = d.unit;
-                it.kv_head = d.kind_kh & 0xffff;
-                const DevUnit &du = it.kind == 0 ? pl.prefix_units[(int64_t)d.unit * Hkv + it.kv_head]
-                                                 : pl.suffix_units[(int64_t)d.unit * Hkv + it.kv_head];
+                it.kv_head = (d.meta >> 16) & 255;
+                const DevUnit &du = it.kind == 0 ? pl.prefix_units[d.unit] : pl.suffix_units[d.unit];
                 const int64_t M = it.kind == 0 ? Mp : r;
                 const int64_t start = it.kind == 0 ? lens->prefix_start[d.unit] : lens->suffix_start[d.unit];
-                it.chunk = static_cast<int32_t>((d.partial_row0 - du.base) / M);
-                it.tok_begin = d.kv_row0 - start;
-                it.tok_count = d.ntok;
-                it.row_begin = d.row_begin;
-                it.row_count = static_cast<int32_t>(std::min<int64_t>(kMaxItemRows, M - d.row_begin));
+                const int64_t base = du.base + static_cast<int64_t>(it.kv_head) * du.nchunks * M;
+                it.chunk = static_cast<int32_t>((static_cast<int64_t>(d.partial_row0) - base) / M);
+                it.tok_begin = static_cast<int64_t>(d.kv_row0) - start;
+                it.tok_count = static_cast<int32_t>(d.meta & 0x7fff);
+                it.row_begin = static_cast<int32_t>((d.meta >> 24) * kMaxItemRows);
+                it.row_count = static_cast<int32_t>(std::min<int64_t>(kMaxItemRows, M - it.row_begin));
             }
         }
     }

@@ -29,25 +29,32 @@ constexpr int kHiddenStep = 64;
 constexpr int kNumCUs = 256;
 constexpr float kLog2eHost = 1.4426950408889634f;
 
-// One split-K work item as the split kernel reads it (32 bytes).
+// One split-K work item as the split kernel reads it (16 bytes; the work list
+// is uploaded over PCIe on every call, so it is kept small).
 struct DevItem {
-    int64_t kv_row0;       // absolute KV row of the chunk's first token
-    int64_t partial_row0;  // partial row of the item's first query row
-    int32_t ntok;          // tokens in the chunk (>= 1)
-    int32_t kind_kh;       // kv head | (1 << 16 if suffix)
-    int32_t unit;          // prompt p (prefix) or candidate s (suffix)
-    int32_t row_begin;     // first query row served
+    uint32_t kv_row0;       // KV row of the chunk's first token in its buffer
+    uint32_t partial_row0;  // partial row of the item's first query row
+    int32_t unit;           // prompt p (prefix) or candidate s (suffix)
+    uint32_t meta;          // tokens (bits 0-14, >= 1) | suffix (bit 15) | kv head (bits 16-23)
+                            // | first query row / kMaxItemRows (bits 24-31)
 };
-static_assert(sizeof(DevItem) == 32, "DevItem layout");
+static_assert(sizeof(DevItem) == 16, "DevItem layout");
 
-// Where the partial results of one (unit, kv head) live: chunk c's row i is
-// partial row base + c * rows_per_chunk + i.
+// Where the partial results of one unit (prompt or candidate) live: at kv
+// head kh, chunk c's row i is partial row base + (kh * nchunks + c) *
+// rows_per_chunk + i.
 struct DevUnit {
-    int64_t base;
-    int32_t nchunks;
-    int32_t pad;
+    uint32_t base;
+    uint32_t nchunks;
 };
-static_assert(sizeof(DevUnit) == 16, "DevUnit layout");
+static_assert(sizeof(DevUnit) == 8, "DevUnit layout");
+
+// Limits of that encoding: tokens per item, kv heads, query rows per prefix
+// unit (G * Hq / Hkv, 256 blocks of kMaxItemRows), and KV or partial rows.
+constexpr int64_t kMaxItemTokens = 16384;
+constexpr int64_t kMaxDecodeKvHeads = 256;
+constexpr int64_t kMaxUnitRows = 16384;
+constexpr int64_t kMaxDecodeRows = 0xffffffffLL;
 
 // How much of the plan to build: the workspace size needs only the counts;
 // a launch needs the device work list; the debug export also wants the
@@ -65,8 +72,8 @@ struct DecodePlan {
     int64_t n_items = 0;
     std::vector<rl_plan_item> items;
     std::vector<DevItem> dev_items;
-    std::vector<DevUnit> prefix_units;   // [P * Hkv]
-    std::vector<DevUnit> suffix_units;   // [S * Hkv]
+    std::vector<DevUnit> prefix_units;   // [P]
+    std::vector<DevUnit> suffix_units;   // [S]
     int64_t partial_rows = 0;
     // workspace layout (byte offsets; every section 256-byte aligned)
     size_t off_items = 0, off_prefix_units = 0, off_suffix_units = 0;

@@ -102,6 +102,10 @@ def decode_call(P=2, G=3, Hq=4, Hkv=2, D=128, scale=0.125, split=0, lp=None, ls=
     (dict(D=256), UNSUP),
     (dict(D=0), SHAPE),
     (dict(Hq=258, Hkv=2), UNSUP),             # Hq/Hkv = 129 > 128
+    (dict(Hq=514, Hkv=257), UNSUP),           # more than 256 kv heads (the work item holds 8 bits)
+    (dict(G=129, Hq=256, Hkv=2, ls=np.full(258, 3)), UNSUP),   # G * Hq/Hkv = 16512 > 16384 rows
+    (dict(prefix_rows=1 << 32), UNSUP),       # KV rows are 32-bit in the work list
+    (dict(suffix_rows=1 << 32), UNSUP),
     (dict(ptrs=dict(q=FAKE + 8)), MISAL),
     (dict(ptrs=dict(v_prefix=FAKE + 2)), MISAL),
     (dict(ptrs=dict(out=FAKE + 4)), MISAL),
@@ -114,6 +118,21 @@ def test_decode_validation(kw, expect):
     st, msg = decode_call(**kw)
     assert st == expect, (st, msg)
     assert msg, "a failing call must leave an error message"
+
+
+def test_decode_split_above_item_limit():
+    """A forced split above 16384 tokens acts as 16384 (items may cover fewer
+    tokens than the bound): a 40000-token prefix becomes 3 chunks."""
+    lp = np.array([40000], np.int32)
+    ls = np.array([20, 0], np.int32)
+    it = rk.decode_plan(1, 2, 4, 2, 128, np.array([0], np.int64), lp, np.array([0, 20], np.int64), ls,
+                        40000, 20, split_tokens=32768)
+    pre = it[it["kind"] == 0]
+    assert pre["tok_count"].max() <= 16384
+    for kh in range(2):
+        mine = np.sort(pre[pre["kv_head"] == kh], order="tok_begin")
+        assert len(mine) == 3 and mine["tok_count"].sum() == 40000
+        assert np.array_equal(mine["tok_begin"][1:], np.cumsum(mine["tok_count"])[:-1])
 
 
 def test_decode_empty_batch_is_noop():
