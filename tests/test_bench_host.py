@@ -1,0 +1,83 @@
+"""bench.py's host-side pieces on the CPU: the algorithmic byte and flop
+counts its rooflines divide by, the counter summaries it reads traffic from
+(only while the kernel source is unchanged), the CPU-baseline sampler, and
+the refusal of more than one GPU."""
+import os
+import subprocess
+import sys
+import types
+
+import numpy as np
+import pytest
+
+import bench
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_decode_bytes_match_the_workload_sizes():
+    # the 8B-class step: prefix 64 x 1024 tokens once, every suffix token once,
+    # K and V of 8 kv heads x 128 dims in bf16, plus q, out (bf16) and lse (fp32)
+    cfg = W.DECODE_CONFIGS["8b"]
+    x = types.SimpleNamespace(cfg=cfg, prefix_len=np.full(64, 1024, np.int32),
+                              suffix_len=W.suffix_lengths(cfg, seed=0))
+    kv_tokens = 64 * 1024 + int(x.suffix_len.sum())
+    expect = kv_tokens * 8 * 128 * 2 * 2 + 2 * 512 * 32 * 128 * 2 + 512 * 32 * 4
+    assert bench.decode_bytes(x) == expect
+    # the seeded suffix lengths of the bench workload (mean 1152 expected)
+    assert expect == 2771460096
+
+
+def test_lmhead_counts():
+    cfg = W.LOGPROB_CONFIGS["8b"]
+    assert bench.lmhead_flops(cfg) == 2 * 512 * 4096 * 151936 == 637265772544
+    # W and the hidden rows once, target in, log-prob and lse out
+    assert bench.lmhead_bytes(cfg) == 2 * 151936 * 4096 + 2 * 512 * 4096 + 4 * 512 + 8 * 512
+
+
+def test_extend_flops_count_visible_pairs():
+    # one candidate whose 3 new tokens see a prefix of 5 and 2 earlier suffix
+    # tokens: visible pairs 7+1, 7+2, 7+3 = 27; 4 D Hq flops per pair
+    cfg = W.DecodeConfig("t", 1, 1, 2, 1, 64, 5, "const", 5, 5)
+
+    class Dec:
+        pass
+
+    class Ext:
+        pass
+    d = Dec()
+    d.cfg = cfg
+    d.prefix_len = np.array([5])
+    d.suffix_len = np.array([5])
+    e = Ext()
+    e.dec = d
+    e.new_len = np.array([3])
+    assert bench.extend_flops(e) == 4 * 64 * 2 * 27
+
+
+@pytest.mark.parametrize("op", ["decode", "lmhead"])
+def test_traffic_read_only_for_the_current_source(op, tmp_path, monkeypatch):
+    path = os.path.join(ROOT, "profiles", f"{op}_8b_traffic.md")
+    assert os.path.exists(path), "the counter summary of the 8B-class step is committed"
+    text = open(path).read()
+    assert "hbm_bytes_per_launch:" in text and "source_sha256:" in text
+    # a summary taken on another source is ignored
+    fake = tmp_path / "profiles"
+    fake.mkdir()
+    (fake / f"{op}_8b_traffic.md").write_text(
+        "\n".join(l if not l.startswith("- source_sha256:") else "- source_sha256: 0" for l in text.splitlines()))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic(op, "8b") is None
+    # the same lines with the current hash are read back as an integer
+    (fake / f"{op}_8b_traffic.md").write_text(
+        "- source_sha256: " + bench.source_sha256(op) + "\n- hbm_bytes_per_launch: 1234\n")
+    assert bench.measured_traffic(op, "8b") == 1234
+    assert bench.measured_traffic(op, "32b") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=300, cwd=ROOT)
+    assert r.returncode != 0
+    assert "one GPU" in r.stderr and r.stdout == ""
