@@ -512,6 +512,31 @@ __device__ __forceinline__ void finish_row(const LogprobArgs &a, int64_t r, floa
     if (a.lse) a.lse[r] = lse;
 }
 
+// Very few rows (a decode step): one workgroup per row, each thread merging
+// at most a few of the row's partial slots, so all of the row's loads are in
+// flight at once; the (max, sum) pairs then merge across the waves in LDS.
+__global__ __launch_bounds__(kThreads) void logprob_combine_block_kernel(LogprobArgs a) {
+    __shared__ float ml[kThreads / 64][2];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t r = blockIdx.x;
+    float M = -INFINITY, L = 0.f;
+    for (int64_t vt = tid; vt < a.n_partials; vt += kThreads) lse_merge(M, L, a.pm[vt * a.R + r], a.pl[vt * a.R + r]);
+    const float Mw = wave_max(M);
+    const float Lw = wave_sum(M == -INFINITY ? 0.f : L * fast_exp2(M - Mw));
+    if (lane == 0) {
+        ml[wave][0] = Mw;
+        ml[wave][1] = Lw;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float Mb = -INFINITY, Lb = 0.f;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w)
+            if (ml[w][0] != -INFINITY) lse_merge(Mb, Lb, ml[w][0], ml[w][1]);
+        finish_row(a, r, Mb, Lb);
+    }
+}
+
 // Few rows: one wave per row, lanes stride over the vocab tiles.
 __global__ __launch_bounds__(kThreads) void logprob_combine_wave_kernel(LogprobArgs a) {
     const int lane = threadIdx.x & 63;
@@ -587,7 +612,10 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (a.R < 32768) {
+    if (a.R <= 4096) {
+        hipLaunchKernelGGL(logprob_combine_block_kernel, dim3(static_cast<uint32_t>(a.R)), dim3(kThreads), 0, stream,
+                           a);
+    } else if (a.R < 32768) {
         const int64_t blocks = (a.R + 3) / 4;
         hipLaunchKernelGGL(logprob_combine_wave_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
                            stream, a);

@@ -49,7 +49,11 @@ def test_tiny_config():
                                    (256, 4096, 2048),
                                    # more than 8 row tiles: the two-stage weight ring
                                    (2305, 64, 700),     # one hidden stage, ragged rows and vocab
-                                   (2049, 192, 300)])   # three hidden stages, one row past a tile
+                                   (2049, 192, 300),    # three hidden stages, one row past a tile
+                                   # the combine: one workgroup per row up to 4096 rows,
+                                   # one wave per row above
+                                   (4096, 64, 1500),
+                                   (5000, 64, 1500)])
 def test_ragged_shapes(R, H, V):
     rng = np.random.Generator(np.random.PCG64(R + H + V))
     h = rand_bits(rng, (R, H))
