@@ -631,6 +631,12 @@ rl_status rl_sample_top_p(int64_t rows, int32_t hidden, int32_t vocab, const voi
         f.logits = logits;
         f.ld = plan.ld;
         f.pm = pm;
+        const rlk::TileRounds tr = rlk::plan_tile_rounds(n, vocab);
+        f.dp_tiles = tr.dp_tiles;
+        f.narrow_v0 = tr.narrow_v0;
+        f.narrow_tiles = tr.narrow_tiles;
+        f.narrow_slot0 = tr.narrow_slot0;
+        f.n_partials = tr.n_partials;
         hipError_t e = rlk::launch_logits(f, hs);
         if (e != hipSuccess) return hip_error(e, "launching the sampling head (logits)");
         rlk::SampleArgs s{};
@@ -642,7 +648,7 @@ rl_status rl_sample_top_p(int64_t rows, int32_t hidden, int32_t vocab, const voi
         s.rows = n;
         s.ld = plan.ld;
         s.V = vocab;
-        s.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
+        s.n_partials = static_cast<int32_t>(tr.n_partials);
         s.top_p = top_p;
         e = rlk::launch_sample_top_p(s, hs);
         if (e != hipSuccess) return hip_error(e, "launching the sampling head (selection)");

@@ -146,12 +146,12 @@ hipError_t launch_logits(const LogprobArgs &a, hipStream_t stream);
 // order at the row's uniform draw.
 struct SampleArgs {
     const float *logits;        // [rows, ld] fp32 tempered logits
-    const float *pm;            // [n_vocab_tiles, rows] tile maxima of the logits
+    const float *pm;            // [n_partials, rows] tile maxima of the logits
     const float *uniform;       // [rows] in [0, 1)
     int32_t *token;             // [rows]
     float *logprob;             // [rows] or null
     int64_t rows, ld;
-    int32_t V, n_vocab_tiles;
+    int32_t V, n_partials;      // n_partials: row-maximum slots (whole and narrow tiles)
     float top_p;
 };
 

@@ -450,6 +450,32 @@ rl_status check_extend_ptrs(const ExtendPlan &pl, const rl_decode_ptrs *ptrs, st
     return RL_OK;
 }
 
+TileRounds plan_tile_rounds(int64_t rows, int32_t vocab) {
+    // With at most 4 row tiles (the tiles of one vocab tile are neighbours in
+    // launch order), the whole vocab tiles of the full rounds run as they are
+    // and the rest of the vocabulary runs as one round of tiles 192 entries
+    // wide, if they fit on the CUs (a round of them takes about 3/4 of a
+    // round of whole tiles).
+    TileRounds tr;
+    const int64_t nvt = ceil_div(vocab, kVocabTile), nrt = ceil_div(rows, kRowTile);
+    const int64_t tiles = nvt * nrt;
+    const int64_t dp = tiles / kNumCUs * kNumCUs, tail = tiles - dp;
+    tr.dp_tiles = tiles;
+    tr.n_partials = nvt;
+    if (dp > 0 && tail > 0 && nrt <= kNarrowMaxRowTiles) {
+        const int64_t vt0 = dp / nrt;
+        const int64_t n = ceil_div(vocab - vt0 * kVocabTile, kNarrowWidth);
+        if (n * nrt <= kNumCUs) {
+            tr.dp_tiles = vt0 * nrt;
+            tr.narrow_v0 = vt0 * kVocabTile;
+            tr.narrow_tiles = n;
+            tr.narrow_slot0 = vt0;
+            tr.n_partials = vt0 + n;
+        }
+    }
+    return tr;
+}
+
 rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan *plan,
                        std::string *err) {
     if (rows < 0) return fail(err, RL_ERR_INVALID_SHAPE, "rows < 0");
@@ -484,21 +510,14 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
             pl.tail_splits = static_cast<int32_t>(s);
         }
     }
-    // A last round more than half full: with at most 4 row tiles (the tiles
-    // of one vocab tile are neighbours in launch order), the whole vocab
-    // tiles of the full rounds run as they are and the rest of the
-    // vocabulary runs as one round of tiles 192 entries wide, if they fit on
-    // the CUs (a round of them takes about 3/4 of a round of whole tiles).
-    if (pl.n_tail_tiles == 0 && dp > 0 && tail > 0 && pl.n_row_tiles <= kNarrowMaxRowTiles) {
-        const int64_t vt0 = dp / pl.n_row_tiles;
-        const int64_t n = ceil_div(vocab - vt0 * kVocabTile, kNarrowWidth);
-        if (n * pl.n_row_tiles <= kNumCUs) {
-            pl.n_dp_tiles = vt0 * pl.n_row_tiles;
-            pl.narrow_v0 = vt0 * kVocabTile;
-            pl.narrow_tiles = n;
-            pl.narrow_slot0 = vt0;
-            pl.n_partials = vt0 + n;
-        }
+    // A last round more than half full: narrow tiles, when they fit.
+    if (pl.n_tail_tiles == 0) {
+        const TileRounds tr = plan_tile_rounds(rows, vocab);
+        pl.n_dp_tiles = tr.dp_tiles;
+        pl.narrow_v0 = tr.narrow_v0;
+        pl.narrow_tiles = tr.narrow_tiles;
+        pl.narrow_slot0 = tr.narrow_slot0;
+        pl.n_partials = tr.n_partials;
     }
     size_t off = 0;
     pl.off_m = off;
@@ -560,15 +579,22 @@ rl_status plan_sample(int64_t rows, int32_t hidden, int32_t vocab, SamplePlan *p
     pl.H = hidden;
     pl.V = vocab;
     pl.n_vocab_tiles = ceil_div(vocab, kVocabTile);
-    pl.ld = pl.n_vocab_tiles * kVocabTile;
+    // one tile of padding past the vocab tiles: a narrow last round's tiles
+    // (192 wide from a whole tile's edge) end at most 191 entries past V
+    pl.ld = (pl.n_vocab_tiles + 1) * kVocabTile;
     if (rows == 0) return RL_OK;
     pl.chunk_rows = std::min<int64_t>(rows, kSampleChunkRows);
     const int64_t rows_pad = ceil_div(pl.chunk_rows, kRowTile) * kRowTile;
     size_t off = 0;
     pl.off_logits = off;
     off = align_up(off + static_cast<size_t>(rows_pad) * pl.ld * 4, 256);
+    // row-maximum slots: the whole tiles' and, per chunk, those of its narrow
+    // last round (at most 4/3 as many tiles cover the rest of the vocabulary)
+    pl.pm_slots = std::max(pl.n_vocab_tiles, plan_tile_rounds(pl.chunk_rows, vocab).n_partials);
+    if (rows % pl.chunk_rows)
+        pl.pm_slots = std::max(pl.pm_slots, plan_tile_rounds(rows % pl.chunk_rows, vocab).n_partials);
     pl.off_pm = off;
-    off = align_up(off + static_cast<size_t>(pl.n_vocab_tiles) * pl.chunk_rows * 4, 256);
+    off = align_up(off + static_cast<size_t>(pl.pm_slots) * pl.chunk_rows * 4, 256);
     pl.total_bytes = off;
     return RL_OK;
 }

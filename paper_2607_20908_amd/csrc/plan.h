@@ -125,6 +125,17 @@ struct LogprobPlan {
 rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan *plan,
                        std::string *err);
 
+// The tiles of one lm-head pass over `rows` rows: logical tiles [0,
+// dp_tiles) whole, then (when narrow_tiles > 0) the vocabulary from
+// narrow_v0 on as one round of kNarrowWidth-wide tiles per row tile, with
+// partial slots narrow_slot0.. ; n_partials slots per row in all.  Narrow
+// tiles are taken when the tiles leave a partial last round, there are at
+// most kNarrowMaxRowTiles row tiles and the narrow tiles fit in one round.
+struct TileRounds {
+    int64_t dp_tiles = 0, narrow_v0 = 0, narrow_tiles = 0, narrow_slot0 = 0, n_partials = 0;
+};
+TileRounds plan_tile_rounds(int64_t rows, int32_t vocab);
+
 rl_status check_logprob_args(const LogprobPlan &plan, const void *hidden_states,
                              const void *w_lm, const int32_t *target, float inv_temperature,
                              const float *logprob, const float *lse, std::string *err);
@@ -161,7 +172,8 @@ struct SamplePlan {
     int32_t H = 0, V = 0;
     int64_t chunk_rows = 0;
     int64_t n_vocab_tiles = 0;
-    int64_t ld = 0;                  // padded vocabulary (row stride of the logits)
+    int64_t pm_slots = 0;            // row-maximum slots per row (whole and narrow tiles)
+    int64_t ld = 0;                  // row stride of the logits: the vocab tiles plus one tile of padding
     size_t off_logits = 0, off_pm = 0, total_bytes = 0;
 };
 

@@ -210,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
 
     // ---- row max from the tile maxima
     float m = -INFINITY;
-    for (int t = tid; t < a.n_vocab_tiles; t += kThreads) m = fmaxf(m, a.pm[static_cast<int64_t>(t) * a.rows + r]);
+    for (int t = tid; t < a.n_partials; t += kThreads) m = fmaxf(m, a.pm[static_cast<int64_t>(t) * a.rows + r]);
     m = wave_max(m);
     if (lane == 0) sh.fred[wave] = m;
     for (int i = tid; i < kBuckets; i += kThreads) {

@@ -177,10 +177,11 @@ __device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 
 }
 
 // TM: 32-entry vocab blocks per wave; a tile spans 64 TM vocab entries (4:
-// the 256 x 256 tiles; 3: the narrow tiles of a last round, kNarrow).
+// the 256 x 256 tiles; 3: the narrow tiles of a last round, for the forward
+// (kNarrow) and the sampling head's logits (kLogits)).
 template <int WS, int MODE, int TM = 4>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
-    static_assert(TM == 4 || MODE == kNarrow, "narrow tiles are forward-only");
+    static_assert(TM == 4 || MODE == kNarrow || MODE == kLogits, "narrow tiles: forward and logits only");
     constexpr int VW = 64 * TM;                  // vocab entries per tile
     constexpr int WELEMS = VW * kK;              // bf16 elements of one weight stage
     constexpr int WBLK = VW / 32;                // 1 KB weight blocks per wave per stage
@@ -196,7 +197,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const int l32 = lane & 31, h2 = lane >> 5;
     int64_t vt, rt, v0;                          // vt: the partial slot of the tile
     int kb = 0, nks = a.H / kK;                  // hidden steps [kb, kb + nks)
-    if constexpr (MODE == kNarrow) {
+    if constexpr (TM != 4) {
         // narrow tile j covers vocab [narrow_v0 + j VW, + VW) for row tile
         // rt; the row tiles of one j are neighbours in launch order, which
         // gives each XCD a contiguous run as tile_of does
@@ -214,13 +215,13 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
         kb = sp * nks / a.splits;
         nks = (sp + 1) * nks / a.splits - kb;
-    } else if constexpr (MODE == kFwd) {
+    } else if constexpr (MODE == kFwd || MODE == kLogits) {
         tile_of(blockIdx.x, a.tile_count, a.tile_base, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
     } else {
         tile_of(blockIdx.x, static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles, 0, a.n_vocab_tiles,
                 a.n_row_tiles, &vt, &rt);
     }
-    if constexpr (MODE != kNarrow) v0 = vt * kVocabTile;
+    if constexpr (TM == 4) v0 = vt * kVocabTile;
     const int64_t r0 = rt * kRowTile;
     const int64_t H = a.H;
 
@@ -385,10 +386,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         return;
     }
     if constexpr (MODE == kLogits) {
-        // acc[tm][tn][i]: vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4,
+        // acc[tm][tn][i]: vocab v0 + wm*32*TM + tm*32 + 8*(i/4) + 4*h2 + i%4,
         // row r0 + wn*128 + tn*32 + l32: 4 consecutive entries per store
-        const int64_t vbase = v0 + wm * 128;
-        const int vlim = vbase + 128 <= a.V ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
+        const int64_t vbase = v0 + wm * 32 * TM;
+        const int vlim = vbase + 32 * TM <= a.V ? 32 * TM : static_cast<int>(a.V - vbase) - 4 * h2;
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) {
             const int row = wn * 128 + tn * 32 + l32;
@@ -398,7 +399,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             float *yrow = a.logits + (live ? rr : 0) * a.ld + vbase + 4 * h2;
             float mx = -INFINITY;
 #pragma unroll
-            for (int tm = 0; tm < 4; ++tm) {
+            for (int tm = 0; tm < TM; ++tm) {
                 const f32x16 z = acc[tm][tn];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
@@ -639,13 +640,25 @@ hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream) {
 }
 
 hipError_t launch_logits(const LogprobArgs &a, hipStream_t stream) {
-    const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
-    if (a.n_row_tiles <= 8)
-        hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
-                           stream, a);
-    else
-        hipLaunchKernelGGL((logprob_tile_kernel<2, kLogits>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
-                           stream, a);
+    // whole tiles [0, dp_tiles), then the last round's narrow tiles if any
+    LogprobArgs d = a;
+    d.tile_base = 0;
+    d.tile_count = a.dp_tiles;
+    if (d.tile_count > 0) {
+        if (a.n_row_tiles <= 8)
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits>), dim3(static_cast<uint32_t>(d.tile_count)),
+                               dim3(kTileThreads), 0, stream, d);
+        else
+            hipLaunchKernelGGL((logprob_tile_kernel<2, kLogits>), dim3(static_cast<uint32_t>(d.tile_count)),
+                               dim3(kTileThreads), 0, stream, d);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (a.narrow_tiles > 0) {
+        static_assert(kNarrowWidth == 64 * 3, "narrow tile width");
+        const uint32_t blocks = static_cast<uint32_t>(a.narrow_tiles * a.n_row_tiles);
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, a);
+    }
     return hipGetLastError();
 }
 

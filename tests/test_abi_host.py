@@ -448,11 +448,14 @@ def test_sample_logprob_optional_and_empty():
 
 def test_sample_workspace_size():
     V = 151936
-    ld = -(-V // 256) * 256
-    tiles = ld // 256
-    # fp32 logits of up to 8192 rows (padded to 256) and their per-tile maxima
+    tiles = -(-V // 256)
+    ld = (tiles + 1) * 256      # one tile of padding: narrow tiles end up to 191 entries past V
+    # fp32 logits of up to 8192 rows (padded to 256) and their per-tile maxima;
+    # at 512 rows the last round runs as 109 x 2 narrow tiles: 512 + 109 slots
+    slots = 512 + 109
+    assert narrow_tiles(512, 4096, V) == (512, 109)
     n = rk.sample_top_p_workspace_size(512, 4096, V)
-    assert n >= 512 * ld * 4 + tiles * 512 * 4 and n < 512 * ld * 4 + tiles * 512 * 4 + 512
+    assert n >= 512 * ld * 4 + slots * 512 * 4 and n < 512 * ld * 4 + slots * 512 * 4 + 512
     assert rk.sample_top_p_workspace_size(100000, 4096, V) == rk.sample_top_p_workspace_size(8192, 4096, V)
     assert rk.sample_top_p_workspace_size(0, 64, 10) == 0
 

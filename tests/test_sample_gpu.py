@@ -88,7 +88,11 @@ def test_tiny_config():
                                               (513, 192, 511, 0.2, 0.5),
                                               (256, 256, 5000, 0.1, 0.9),    # several chunks of ids
                                               (2305, 64, 700, 0.3, 0.95),    # more than 8 row tiles
-                                              (200, 128, 3000, 0.3, 1.0)])   # the full distribution
+                                              (200, 128, 3000, 0.3, 1.0),    # the full distribution
+                                              # narrow last rounds: 95 x 2 tiles 192 wide, the last
+                                              # ending 64 entries past V (a multiple of 256); 48 x 4
+                                              (300, 128, 50944, 0.3, 0.9),
+                                              (1000, 64, 25500, 0.3, 0.9)])
 def test_shapes(R, H, V, wstd, top_p):
     rng = np.random.Generator(np.random.PCG64(R + H + V))
     hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), wstd)
