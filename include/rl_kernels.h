@@ -285,9 +285,9 @@ rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *le
  *
  * rows == 0 is a valid no-op.  Status: NULL pointer -> RL_ERR_NULL_POINTER;
  * rows < 0, hidden <= 0, vocab <= 0 or a bad temperature -> RL_ERR_INVALID_SHAPE;
- * hidden % 64 != 0 -> RL_ERR_UNSUPPORTED; a device pointer not 16-byte
- * aligned (target, logprob and lse: 4-byte) -> RL_ERR_MISALIGNED; workspace
- * NULL or short -> RL_ERR_WORKSPACE.
+ * hidden % 64 != 0 or hidden > 4194304 -> RL_ERR_UNSUPPORTED; a device
+ * pointer not 16-byte aligned (target, logprob and lse: 4-byte) ->
+ * RL_ERR_MISALIGNED; workspace NULL or short -> RL_ERR_WORKSPACE.
  *
  * The workspace holds a (max, sum) partial per (vocab tile, row) and the
  * target logit per row.  When the last round of 256 x 256 tiles would leave

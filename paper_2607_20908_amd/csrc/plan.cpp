@@ -483,6 +483,8 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
     if (vocab <= 0) return fail(err, RL_ERR_INVALID_SHAPE, "vocab must be > 0");
     if (hidden % kHiddenStep)
         return fail(err, RL_ERR_UNSUPPORTED, "hidden must be a multiple of 64");
+    if (hidden > kMaxHidden)
+        return fail(err, RL_ERR_UNSUPPORTED, "hidden must be <= 4194304");
     LogprobPlan &pl = *plan;
     pl = LogprobPlan{};
     pl.R = rows;

@@ -99,6 +99,9 @@ rl_status check_decode_ptrs(const DecodePlan &plan, const rl_decode_lens *lens,
 // A last round of lm-head tiles that would leave at least half the CUs idle
 // is split over the hidden dimension into up to this many parts.
 constexpr int kMaxTailSplits = 4;
+// The tile kernels address a weight or hidden row of a tile as a 32-bit byte
+// offset from the tile's first row (255 rows of 2 * hidden bytes).
+constexpr int64_t kMaxHidden = 1 << 22;
 // Narrow last-round tiles are this many vocab entries wide; they need every
 // row tile of a vocab tile next to each other in launch order, which holds
 // for at most kNarrowMaxRowTiles row tiles.

@@ -242,7 +242,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         const int row = blk * 8 + (lane >> 3);
         const int c = (lane & 7) ^ ((row >> 1) & 7);
         const int64_t k0 = static_cast<int64_t>(kb + min(slot, nks - 1)) * kK;
-        load_lds16(g + min(row, last) * H + k0 + c * 8, st + blk * 512);
+        // wave-uniform base (SGPRs) plus a per-lane byte offset that stays
+        // the same from stage to stage
+        const uint32_t voff = static_cast<uint32_t>((min(row, last) * H + c * 8) * 2);
+        load_lds16_s(g + k0, voff, st + blk * 512);
     };
     auto issue_w = [&](int slot) {
 #pragma unroll

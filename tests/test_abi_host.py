@@ -177,6 +177,7 @@ def logprob_call(R=8, H=256, V=1000, hs=FAKE, w=FAKE + 256, t=FAKE + 512, invT=1
     (dict(invT=-1.0), SHAPE),
     (dict(invT=float("nan")), SHAPE),
     (dict(H=100), UNSUP),
+    (dict(H=(1 << 22) + 64), UNSUP),      # 32-bit byte offsets within a tile's rows
     (dict(H=32), UNSUP),
     (dict(hs=FAKE + 8), MISAL),
     (dict(w=FAKE + 4), MISAL),
@@ -365,6 +366,7 @@ def logprob_bwd_call(R=8, H=256, V=1000, hs=FAKE, w=FAKE + 256, t=FAKE + 512, in
     (dict(invT=0.0), SHAPE),
     (dict(invT=float("inf")), SHAPE),
     (dict(H=100), UNSUP),
+    (dict(H=(1 << 22) + 64), UNSUP),      # 32-bit byte offsets within a tile's rows
     (dict(hs=FAKE + 8), MISAL),
     (dict(w=FAKE + 4), MISAL),
     (dict(dh=FAKE + 2056), MISAL),
@@ -424,6 +426,7 @@ def sample_call(R=8, H=256, V=1000, hs=FAKE, w=FAKE + 256, it=FAKE + 512, top_p=
     (dict(top_p=1.5), SHAPE),
     (dict(top_p=float("nan")), SHAPE),
     (dict(H=100), UNSUP),
+    (dict(H=(1 << 22) + 64), UNSUP),      # 32-bit byte offsets within a tile's rows
     (dict(V=(1 << 21) + 1), UNSUP),
     (dict(hs=FAKE + 8), MISAL),
     (dict(w=FAKE + 4), MISAL),
