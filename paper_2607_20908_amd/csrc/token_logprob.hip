@@ -16,7 +16,11 @@
 // accumulator registers, so the reduction is in-lane plus one cross-half
 // shuffle), picks out the target's logit when the target falls in the tile,
 // and writes one (max, sum) partial per (vocab tile, row).
-// Combine kernel: per row, merge the partials of all vocab tiles into the
+// A last round of tiles runs either as hidden-dimension parts summed by a
+// reduce kernel (at most half the CUs busy) or as tiles 192 vocab entries
+// wide (more than half busy, at most 4 row tiles), each with a partial slot
+// of its own.
+// Combine kernel: per row, merge the partials of all slots into the
 // log-sum-exp and subtract it from the target logit.
 #include "device_common.h"
 #include "kernels.h"
@@ -42,7 +46,8 @@ static_assert(kBlocksPerWave == 8, "staging layout");
 // p = exp(inv_T z - lse) per (row, vocab entry) as bf16 into the blocked
 // probability buffer; or the sampling head's tempered fp32 logits (per-row
 // temperature) plus the tile's row maxima.
-// kNarrow is the forward over the narrow tiles of a last round (TM < 4).
+// kNarrow is the forward over the narrow tiles of a last round (TM < 4); the
+// sampling head's kLogits takes narrow tiles as well.
 enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2, kPartialK = 3, kNarrow = 4 };
 
 // Forward epilogue of one 32-row column of a (64 TM) x 256 logit tile, as one
