@@ -7,7 +7,8 @@
 //                chunk crosses HBM once per group of up to 64 rows;
 //   suffix item: one candidate's own KV, for its r query rows.
 // The KV chunk streams through LDS in tiles of 64 tokens: coalesced 16-byte
-// loads into registers one tile ahead and a single LDS stage, so three
+// buffer loads (rows past the chunk read as zeros through the descriptor's
+// range) into registers one tile ahead and a single LDS stage, so three
 // workgroups fit on a CU, each with a tile's loads in flight.  Per 16-token
 // sub-tile a wave computes scores S^T = K Q^T on MFMA 16x16x32 (tokens on the
 // M side, query rows on the N side), keeps an online softmax per query row in
@@ -131,20 +132,28 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
 
     // ---- tile staging -----------------------------------------------------
     u32x4 kr[C::LD], vr[C::LD];
+    // Buffer loads: a descriptor per tile covers the chunk's rows from the
+    // tile's first token to the end of the chunk's last row, so rows past the
+    // chunk fall outside it and read as zeros; each lane's byte offset inside
+    // a tile is fixed (tokens x row pitch < 2^23 bytes, ranges < 2^31).
+    uint32_t voff[C::LD];
+#pragma unroll
+    for (int j = 0; j < C::LD; ++j) {
+        const int idx = tid + j * kThreads;
+        voff[j] = static_cast<uint32_t>((idx / C::CH) * tok_stride * 2 + (idx % C::CH) * 16);
+    }
     auto load_tile = [&](int tile) {
         const int t0 = tile * kTileTokens;
+        const int64_t first = static_cast<int64_t>(t0) * tok_stride;
+        const int range = static_cast<int>((static_cast<int64_t>(ntok - t0 - 1) * tok_stride + D) * 2);
+        const __amdgpu_buffer_rsrc_t rk =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(kg + first), 0, range, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rv =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(vg + first), 0, range, 0x00020000);
 #pragma unroll
         for (int j = 0; j < C::LD; ++j) {
-            const int idx = tid + j * kThreads;
-            const int t = idx / C::CH, ch = idx % C::CH;
-            if (t0 + t < ntok) {
-                const int64_t off = static_cast<int64_t>(t0 + t) * tok_stride + ch * 8;
-                kr[j] = *reinterpret_cast<const u32x4 *>(kg + off);
-                vr[j] = *reinterpret_cast<const u32x4 *>(vg + off);
-            } else {
-                kr[j] = u32x4{0u, 0u, 0u, 0u};   // never read rows outside the chunk
-                vr[j] = u32x4{0u, 0u, 0u, 0u};
-            }
+            kr[j] = __builtin_amdgcn_raw_buffer_load_b128(rk, voff[j], 0, 0);
+            vr[j] = __builtin_amdgcn_raw_buffer_load_b128(rv, voff[j], 0, 0);
         }
     };
     auto store_tile = [&]() {
@@ -188,9 +197,6 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
                         const bool valid = t0 + st * kSub + g4 * 4 + i < ntok;
                         sc[k][i] = valid ? sv[i] * a.score_scale_log2 : -INFINITY;
                     }
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) sc[k][i] = -INFINITY;
                 }
             }
             // online softmax update, probabilities to bf16
@@ -198,17 +204,20 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
             float mx = -INFINITY;
 #pragma unroll
             for (int k = 0; k < kSubPerTile; ++k)
+                if (k < nst)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[k][i]);
+                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[k][i]);
             mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
             mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
             const float m_new = fmaxf(m_run, mx);
             const float m_use = m_new == -INFINITY ? 0.f : m_new;
             const float alpha = fast_exp2(m_run - m_use);
             m_run = m_new;
+            // only the wave's own sub-tiles (one of four in a 4-row suffix item)
             float psum = 0.f;
 #pragma unroll
             for (int k = 0; k < kSubPerTile; ++k) {
+                if (k >= nst) continue;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float p = fast_exp2(sc[k][i] - m_use);
