@@ -276,6 +276,7 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.r = plan.r;
     a.D = plan.D;
     a.kv_layout = plan.kv_layout;
+    a.deep_prefetch = plan.deep_prefetch;
     a.prefix_rows = plan.prefix_rows;
     a.suffix_rows = plan.suffix_rows;
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;

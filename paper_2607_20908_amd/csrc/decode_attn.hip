@@ -27,8 +27,10 @@ namespace {
 
 constexpr int kThreads = 256;
 // Three workgroups per CU (LDS: one ~36 KB stage each; registers: at most 168
-// per lane), each with one tile's loads in flight.
+// per lane), each with one tile's loads in flight; with two tiles in flight
+// (two register sets) two workgroups fit.
 constexpr int kSplitBlocksPerCU = 3;
+constexpr int kSplitBlocksPerCUDeep = 2;
 constexpr int kSub = 16;                          // tokens per MFMA sub-tile
 constexpr int kSubPerTile = kTileTokens / kSub;   // 4
 
@@ -71,8 +73,10 @@ __device__ __forceinline__ int v_off(int t, int c) {
 // Items serve at most 64 query rows: 4 MFMA column tiles of 16, one per wave.
 // Items of up to 16 rows split each tile's 4 sub-tiles over the 4 waves, items
 // of up to 32 rows over 2; those waves' partials are merged through LDS.
-template <int D>
-__global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kernel(DecodeArgs a) {
+// PF: tiles whose loads are in flight while a tile is computed (1 or 2).
+template <int D, int PF>
+__global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitBlocksPerCU) void decode_split_kernel(
+    DecodeArgs a) {
     using C = DCfg<D>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::MAIN_BYTES + C::ML_BYTES];
     uint16_t *kv = reinterpret_cast<uint16_t *>(smem);
@@ -131,7 +135,7 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
     for (int dt = 0; dt < C::DT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // ---- tile staging -----------------------------------------------------
-    u32x4 kr[C::LD], vr[C::LD];
+    u32x4 kA[C::LD], vA[C::LD], kB[C::LD], vB[C::LD];
     // Buffer loads: a descriptor per tile covers the chunk's rows from the
     // tile's first token to the end of the chunk's last row, so rows past the
     // chunk fall outside it and read as zeros; each lane's byte offset inside
@@ -142,10 +146,13 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
         const int idx = tid + j * kThreads;
         voff[j] = static_cast<uint32_t>((idx / C::CH) * tok_stride * 2 + (idx % C::CH) * 16);
     }
-    auto load_tile = [&](int tile) {
+    auto load_tile = [&](int tile, u32x4 (&kr)[C::LD], u32x4 (&vr)[C::LD]) {
+        // a tile past the chunk gets an empty range: its loads touch no memory
+        // and return zeros, so every step issues the same loads
         const int t0 = tile * kTileTokens;
-        const int64_t first = static_cast<int64_t>(t0) * tok_stride;
-        const int range = static_cast<int>((static_cast<int64_t>(ntok - t0 - 1) * tok_stride + D) * 2);
+        const bool in = t0 < ntok;
+        const int64_t first = in ? static_cast<int64_t>(t0) * tok_stride : 0;
+        const int range = in ? static_cast<int>((static_cast<int64_t>(ntok - t0 - 1) * tok_stride + D) * 2) : 0;
         const __amdgpu_buffer_rsrc_t rk =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(kg + first), 0, range, 0x00020000);
         const __amdgpu_buffer_rsrc_t rv =
@@ -156,7 +163,7 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
             vr[j] = __builtin_amdgcn_raw_buffer_load_b128(rv, voff[j], 0, 0);
         }
     };
-    auto store_tile = [&]() {
+    auto store_tile = [&](const u32x4 (&kr)[C::LD], const u32x4 (&vr)[C::LD]) {
         uint16_t *kl = kv;
         uint16_t *vl = kl + C::TILE;
 #pragma unroll
@@ -169,14 +176,10 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
     };
 
     const int ntiles = (ntok + kTileTokens - 1) / kTileTokens;
-    load_tile(0);
-    store_tile();
-    if (ntiles > 1) load_tile(1);
-    __syncthreads();
 
     const uint16_t *kl = kv;
     const uint16_t *vl = kl + C::TILE;
-    for (int tile = 0; tile < ntiles; ++tile) {
+    auto step = [&](int tile, u32x4 (&kc)[C::LD], u32x4 (&vc)[C::LD]) {
         const int t0 = tile * kTileTokens;
         if (mine) {
             // scores of my sub-tiles, log2 units, masked past the chunk end
@@ -249,13 +252,40 @@ __global__ __launch_bounds__(kThreads, kSplitBlocksPerCU) void decode_split_kern
                 }
             }
         }
-        // one LDS stage: once every wave has read it, tile+1 moves in from the
-        // registers and tile+2's loads are issued
+        // one LDS stage: once every wave has read it, the next tile moves in
+        // from its register set, which then takes the loads PF + 1 tiles ahead
         __syncthreads();
-        if (tile + 1 < ntiles) {
-            store_tile();
-            if (tile + 2 < ntiles) load_tile(tile + 2);
+        if constexpr (PF == 1) {
+            if (tile + 1 < ntiles) {
+                store_tile(kc, vc);
+                if (tile + 2 < ntiles) load_tile(tile + 2, kc, vc);
+                __syncthreads();
+            }
+        } else {
+            // unconditional: every step issues the same loads (past the chunk
+            // they are empty), so the wait before the store covers only the
+            // older register set
+            store_tile(kc, vc);
+            load_tile(tile + 3, kc, vc);
             __syncthreads();
+        }
+    };
+    if constexpr (PF == 1) {
+        load_tile(0, kA, vA);
+        store_tile(kA, vA);
+        if (ntiles > 1) load_tile(1, kA, vA);
+        __syncthreads();
+        for (int tile = 0; tile < ntiles; ++tile) step(tile, kA, vA);
+    } else {
+        // set A holds the odd tiles' loads, set B the even ones'
+        load_tile(0, kB, vB);
+        load_tile(1, kA, vA);
+        store_tile(kB, vB);
+        load_tile(2, kB, vB);
+        __syncthreads();
+        for (int tile = 0; tile < ntiles; tile += 2) {
+            step(tile, kA, vA);
+            if (tile + 1 < ntiles) step(tile + 1, kB, vB);
         }
     }
 
@@ -432,7 +462,10 @@ __global__ __launch_bounds__(kThreads) void plan_fetch_kernel(const u32x4 *__res
 template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
     if (a.n_items > 0) {
-        hipLaunchKernelGGL(decode_split_kernel<D>, dim3(a.n_items), dim3(kThreads), 0, stream, a);
+        if (a.deep_prefetch)
+            hipLaunchKernelGGL((decode_split_kernel<D, 2>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL((decode_split_kernel<D, 1>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -33,6 +33,7 @@ struct DecodeArgs {
     int32_t n_items;            // work items in the list
     int32_t P, G, Hq, Hkv, r, D;
     int32_t kv_layout;          // RL_KV_TOKEN_MAJOR or RL_KV_HEAD_MAJOR
+    int32_t deep_prefetch;      // split kernel with two tiles in flight per workgroup
     int64_t prefix_rows, suffix_rows;
     float score_scale_log2;     // softmax_scale * log2(e)
     StageRelease release;       // stored by the combine kernel

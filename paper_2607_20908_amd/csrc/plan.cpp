@@ -163,9 +163,11 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     // serves them all.
     pl.prefix_units.assign(P, DevUnit{0, 0});
     pl.suffix_units.assign(S, DevUnit{0, 0});
-    int64_t prow = 0, n_items = 0;
+    int64_t prow = 0, n_items = 0, item_tokens = 0, wide_tokens = 0;
     auto size_unit = [&](int64_t L, int64_t C, int64_t M, DevUnit *du) {
         const int64_t n = L == 0 ? 0 : ceil_div(L, C);
+        item_tokens += L * ceil_div(M, kMaxItemRows);
+        wide_tokens += L * (M / kMaxItemRows + (M % kMaxItemRows > 48 ? 1 : 0));
         du->base = static_cast<uint32_t>(std::min(prow, kMaxDecodeRows));   // checked below
         du->nchunks = static_cast<uint32_t>(n);
         prow += Hkv * n * M;
@@ -175,6 +177,7 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
     for (int64_t s = 0; s < S; ++s) size_unit(lens->suffix_len[s], cs, r, &pl.suffix_units[s]);
     pl.partial_rows = prow;
     pl.n_items = n_items;
+    pl.deep_prefetch = 2 * wide_tokens > item_tokens ? 1 : 0;
     if (n_items > static_cast<int64_t>(INT32_MAX))
         return fail(err, RL_ERR_UNSUPPORTED, "too many work items");
     if (prow > kMaxDecodeRows) return fail(err, RL_ERR_UNSUPPORTED, "too many partial rows (2^32 or more)");

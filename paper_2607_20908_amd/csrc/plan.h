@@ -75,6 +75,10 @@ struct DecodePlan {
     std::vector<DevUnit> prefix_units;   // [P]
     std::vector<DevUnit> suffix_units;   // [S]
     int64_t partial_rows = 0;
+    // nonzero when items of more than 48 query rows (four sub-tiles per wave)
+    // hold most of the KV tokens: the split kernel then keeps two tiles in
+    // flight per workgroup
+    int32_t deep_prefetch = 0;
     // workspace layout (byte offsets; every section 256-byte aligned)
     size_t off_items = 0, off_prefix_units = 0, off_suffix_units = 0;
     size_t off_m = 0, off_l = 0, off_acc = 0;

@@ -70,6 +70,21 @@ def test_ragged_multi_tile(D, split, layout):
     check(c, 1.0 / math.sqrt(D), split, f"ragged D={D}", layout)
 
 
+@pytest.mark.parametrize("layout", ["token", "head"])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("split", [0, 16, 64, 112, 176])
+def test_wide_items_two_tiles_in_flight(D, split, layout):
+    """Prefix items of 64 query rows (G * r = 64) hold most of the KV tokens
+    (893 of about 1300), so the split kernel keeps two tiles in flight per
+    workgroup; chunks of one to three tiles with ragged ends exercise the
+    empty loads issued past a chunk's last tile."""
+    P, G, Hq, Hkv = 3, 8, 16, 2
+    lp = [700, 0, 193]
+    ls = ([5, 0, 17, 64, 1, 65, 0, 30] + [3, 9, 0, 2, 40, 1, 0, 12] + [63, 0, 1, 2, 3, 4, 5, 6])
+    c = decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=D * 7 + split, gap=2)
+    check(c, 1.0 / math.sqrt(D), split, f"wide items D={D}", layout)
+
+
 @pytest.mark.parametrize("G,Hq,Hkv", [(16, 64, 8),   # 128 query rows per kv head: two 64-row items per chunk
                                        (20, 16, 2),   # 160 rows: three row blocks per prefix chunk
                                        (5, 12, 4),    # 15 rows: one partial column tile
