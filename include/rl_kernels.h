@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 7
+#define RL_ABI_VERSION 8
 
 typedef enum {
     RL_OK = 0,
@@ -470,6 +470,38 @@ typedef struct {
 
 rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_lens *lens,
                                rl_plan_item *items, int64_t capacity, int64_t *num_items);
+
+/*
+ * Host-only replay of the global memory accesses that rl_token_logprob
+ * (op = 0) or rl_token_logprob_backward (op = 1) would make for these sizes:
+ * every launch of the call, every workgroup and lane, with the kernel
+ * arguments the entry point builds and the kernels' own index arithmetic;
+ * each load and store is checked against the allocation (or workspace
+ * section) it must fall in, sized as the entry point requires.  No device
+ * access; for tests.  Staged loads are checked at the first and last stage
+ * (each address is affine and non-decreasing in the stage), or at every
+ * stage when every_stage != 0.  shrink_region >= 0 makes that allocation or
+ * section (numbered in the order listed below) 16 bytes smaller than the
+ * entry point requires, to test the checker: every one that the kernels use
+ * up to its last byte must then report a violation.  Regions: op 0: hidden,
+ * w_lm, target, logprob, lse, workspace, and the workspace's partial max,
+ * partial sum, target logit and tail part sections; op 1: hidden, w_lm,
+ * target, lse, grad_logprob, grad_hidden, workspace, and the workspace's
+ * probability and (split GEMMs only) split-sum sections.  Returns the plan's
+ * status for invalid sizes, RL_ERR_NULL_POINTER for a NULL report and
+ * RL_ERR_INVALID_SHAPE for an unknown op; otherwise RL_OK with the counts in
+ * *report.
+ */
+typedef struct {
+    uint64_t accesses;          /* lane accesses checked                         */
+    uint64_t violations;        /* accesses outside their allocation             */
+    int32_t  launches;          /* kernel launches replayed                      */
+    int32_t  regions;           /* allocations and sections checked              */
+    char     first_violation[256]; /* the first one found, "" if none            */
+} rl_bounds_report;
+
+rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t hidden, int32_t vocab,
+                                  int32_t every_stage, int32_t shrink_region, rl_bounds_report *report);
 
 #ifdef __cplusplus
 }

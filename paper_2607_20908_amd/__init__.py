@@ -84,12 +84,17 @@ class PlanItem(ctypes.Structure):
                 ("row_count", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class BoundsReport(ctypes.Structure):
+    _fields_ = [("accesses", ctypes.c_uint64), ("violations", ctypes.c_uint64), ("launches", ctypes.c_int32),
+                ("regions", ctypes.c_int32), ("first_violation", ctypes.c_char * 256)]
+
+
 EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_workspace_size",
            "rl_token_logprob", "rl_status_string", "rl_last_error", "rl_abi_version",
            "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
-           "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn"]
+           "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds"]
 
 
 def _load():
@@ -134,7 +139,9 @@ def _load():
     lib.rl_extend_attn_workspace_size.argtypes = [P, P, ctypes.POINTER(SZ)]
     lib.rl_extend_attn.restype = ctypes.c_int
     lib.rl_extend_attn.argtypes = [P, P, P, P, SZ, P]
-    if lib.rl_abi_version() != 7:
+    lib.rl_debug_logprob_bounds.restype = ctypes.c_int
+    lib.rl_debug_logprob_bounds.argtypes = [I32, I64, I32, I32, I32, I32, ctypes.POINTER(BoundsReport)]
+    if lib.rl_abi_version() != 8:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -494,6 +501,16 @@ def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor
                                  ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                  _stream_handle(stream)), "rl_token_logprob")
     return logprob, lse
+
+
+def logprob_bounds(op: int, rows: int, hidden: int, vocab: int, every_stage: bool = False,
+                   shrink_region: int = -1) -> BoundsReport:
+    """Host replay of the global accesses of rl_token_logprob (op 0) or
+    rl_token_logprob_backward (op 1) at these sizes (no device access)."""
+    rep = BoundsReport()
+    _check(_lib.rl_debug_logprob_bounds(op, rows, hidden, vocab, int(bool(every_stage)), shrink_region,
+                                        ctypes.byref(rep)), "rl_debug_logprob_bounds")
+    return rep
 
 
 def token_logprob_backward_workspace_size(rows: int, hidden: int, vocab: int) -> int:

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "logprob_args.h"
 #include "plan.h"
 #include "rl_kernels.h"
 
@@ -365,30 +366,8 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
         return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(plan.total_bytes) +
                                                " bytes, got " + std::to_string(workspace_bytes));
     if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
-    unsigned char *ws = static_cast<unsigned char *>(workspace);
-    rlk::LogprobArgs a{};
-    a.hidden = static_cast<const uint16_t *>(hidden_states);
-    a.w = static_cast<const uint16_t *>(w_lm);
-    a.target = target;
-    a.logprob = logprob;
-    a.lse = lse;
-    a.pm = reinterpret_cast<float *>(ws + plan.off_m);
-    a.pl = reinterpret_cast<float *>(ws + plan.off_l);
-    a.zt = reinterpret_cast<float *>(ws + plan.off_zt);
-    a.R = rows;
-    a.H = hidden;
-    a.V = vocab;
-    a.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
-    a.n_row_tiles = static_cast<int32_t>(plan.n_row_tiles);
-    a.inv_temperature = inv_temperature;
-    a.dp_tiles = plan.n_dp_tiles;
-    a.tail_tiles = plan.n_tail_tiles;
-    a.splits = plan.tail_splits;
-    a.part = reinterpret_cast<float *>(ws + plan.off_part);
-    a.narrow_v0 = plan.narrow_v0;
-    a.narrow_tiles = plan.narrow_tiles;
-    a.narrow_slot0 = plan.narrow_slot0;
-    a.n_partials = plan.n_partials;
+    const rlk::LogprobArgs a = rlk::logprob_args(plan, hidden_states, w_lm, target, inv_temperature, logprob, lse,
+                                                 static_cast<unsigned char *>(workspace));
     const hipError_t e = rlk::launch_logprob(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_error(e, "launching token log-prob");
     return RL_OK;
@@ -537,40 +516,13 @@ rl_status rl_token_logprob_backward(int64_t rows, int32_t hidden, int32_t vocab,
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     const uint16_t *hid = static_cast<const uint16_t *>(hidden_states);
     const uint16_t *w = static_cast<const uint16_t *>(w_lm);
-    uint16_t *probs = reinterpret_cast<uint16_t *>(ws + plan.off_probs);
     for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
-        const int64_t n = std::min(plan.chunk_rows, rows - c0);
-        const int32_t row_tiles = static_cast<int32_t>((n + rlk::kRowTile - 1) / rlk::kRowTile);
-        rlk::LogprobArgs f{};
-        f.hidden = hid + c0 * hidden;
-        f.w = w;
-        f.target = target + c0;
-        f.R = n;
-        f.H = hidden;
-        f.V = vocab;
-        f.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
-        f.n_row_tiles = row_tiles;
-        f.inv_temperature = inv_temperature;
-        f.lse_in = lse + c0;
-        f.probs = probs;
+        rlk::LogprobArgs f;
+        rlk::LogprobBwdArgs b;
+        rlk::logprob_bwd_chunk_args(plan, c0, hid, w, target, inv_temperature, lse, grad_logprob, grad_hidden, ws, &f,
+                                    &b);
         hipError_t e = rlk::launch_logprob_probs(f, hs);
         if (e != hipSuccess) return hip_error(e, "launching the log-prob backward (probabilities)");
-        rlk::LogprobBwdArgs b{};
-        b.w = w;
-        b.target = target + c0;
-        b.grad = grad_logprob + c0;
-        b.dh = grad_hidden + c0 * hidden;
-        b.probs = probs;
-        b.dpart = plan.splits > 1 ? reinterpret_cast<float *>(ws + plan.off_part) : b.dh;
-        b.rows = n;
-        b.H = hidden;
-        b.V = vocab;
-        b.n_vsteps = plan.n_vsteps;
-        b.n_row_tiles = row_tiles;
-        b.n_h_tiles = plan.n_h_tiles;
-        b.splits = plan.splits;
-        b.steps_per_split = plan.steps_per_split;
-        b.inv_temperature = inv_temperature;
         e = rlk::launch_logprob_bwd_gemm(b, hs);
         if (e != hipSuccess) return hip_error(e, "launching the log-prob backward (GEMM)");
         e = rlk::launch_logprob_bwd_finish(b, hs);

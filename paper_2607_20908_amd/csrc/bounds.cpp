@@ -1,0 +1,454 @@
+// Host replay of the global memory accesses of the lm-head log-prob kernels
+// (rl_token_logprob and rl_token_logprob_backward), for tests: every launch
+// of a call is replayed workgroup by workgroup and lane by lane with the
+// arguments the entry point builds (logprob_args.h) and the index arithmetic
+// the kernels use (tile_index.h), and every load and store is checked to lie
+// inside the allocation, or workspace section, it must fall in.  Allocations
+// get disjoint fake base addresses; nothing touches device memory.
+//
+// Staged loads: a workgroup loads stage min(slot, nks - 1) for every slot it
+// issues, and each address is affine and non-decreasing in that clamped stage
+// index, so the first and last stage bound every stage's access; with
+// every_stage set, every issued slot is replayed instead.  Data-dependent
+// accesses (the target's weight row in the finish kernel, the target logit's
+// store) are checked at both ends of the range the kernel's guard admits.
+#include <algorithm>
+#include <atomic>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "kernels.h"
+#include "logprob_args.h"
+#include "plan.h"
+#include "rl_kernels.h"
+#include "tile_index.h"
+
+namespace rlk {
+namespace {
+
+struct Region {
+    const char *name;
+    uint64_t base, size;   // fake address and bytes
+};
+
+class Replay {
+  public:
+    // shrink: index of the region (in the order added) to make 16 bytes
+    // smaller than the entry point requires, or -1
+    Replay(bool every_stage, int shrink) : every_stage_(every_stage), shrink_(shrink) {}
+
+    int add(const char *name, uint64_t size) {
+        const uint64_t base = static_cast<uint64_t>(regions_.size() + 1) << 44;
+        return push({name, base, size});
+    }
+    // a section [off, off + size) of region `parent`, checked on its own
+    int section(const char *name, int parent, uint64_t off, uint64_t size) {
+        return push({name, regions_[parent].base + off, size});
+    }
+    int regions() const { return static_cast<int>(regions_.size()); }
+    uint64_t base(int r) const { return regions_[r].base; }
+    template <class T>
+    T *ptr(int r) const {
+        return reinterpret_cast<T *>(static_cast<uintptr_t>(regions_[r].base));
+    }
+    static uint64_t addr(const void *p) { return static_cast<uint64_t>(reinterpret_cast<uintptr_t>(p)); }
+    bool every_stage() const { return every_stage_; }
+
+    // Replays blocks [0, blocks) of one launch on the host's cores.
+    template <class F>
+    void launch(const char *kernel, int64_t blocks, F body) {
+        ++launches_;
+        const int nt = static_cast<int>(std::max<unsigned>(1u, std::min<unsigned>(8u, std::thread::hardware_concurrency())));
+        std::atomic<int64_t> next{0};
+        auto work = [&]() {
+            Lane ln{this, kernel, 0, 0, 0, 0};
+            for (;;) {
+                const int64_t b0 = next.fetch_add(64);
+                if (b0 >= blocks) break;
+                for (int64_t b = b0; b < std::min(blocks, b0 + 64); ++b) {
+                    ln.block = b;
+                    body(b, ln);
+                }
+            }
+            accesses_ += ln.n;
+            violations_ += ln.bad;
+        };
+        std::vector<std::thread> ts;
+        for (int i = 1; i < nt; ++i) ts.emplace_back(work);
+        work();
+        for (auto &t : ts) t.join();
+    }
+
+    // Per-host-thread checker of one launch.
+    struct Lane {
+        Replay *rp;
+        const char *kernel;
+        int64_t block;
+        int thread;
+        uint64_t n, bad;
+        void check(int region, uint64_t a, uint64_t bytes, const char *what) {
+            ++n;
+            const Region &r = rp->regions_[region];
+            if (a >= r.base && bytes <= r.size && a - r.base <= r.size - bytes) return;
+            ++bad;
+            rp->note(kernel, block, thread, what, r, a, bytes);
+        }
+    };
+
+    void report(rl_bounds_report *rep) const {
+        rep->accesses = accesses_;
+        rep->violations = violations_;
+        rep->launches = launches_;
+        rep->regions = static_cast<int32_t>(regions_.size());
+        std::snprintf(rep->first_violation, sizeof(rep->first_violation), "%s", first_.c_str());
+    }
+
+  private:
+    int push(Region r) {
+        if (static_cast<int>(regions_.size()) == shrink_) r.size = r.size >= 16 ? r.size - 16 : 0;
+        regions_.push_back(r);
+        return static_cast<int>(regions_.size()) - 1;
+    }
+    void note(const char *kernel, int64_t block, int thread, const char *what, const Region &r, uint64_t a,
+              uint64_t bytes) {
+        std::lock_guard<std::mutex> g(mu_);
+        if (!first_.empty()) return;
+        char buf[256];
+        std::snprintf(buf, sizeof(buf), "%s block %lld thread %d: %s of %llu bytes at offset %lld of %s (%llu bytes)",
+                      kernel, static_cast<long long>(block), thread, what, static_cast<unsigned long long>(bytes),
+                      static_cast<long long>(a - r.base), r.name, static_cast<unsigned long long>(r.size));
+        first_ = buf;
+    }
+
+    bool every_stage_;
+    int shrink_;
+    std::vector<Region> regions_;
+    std::atomic<uint64_t> accesses_{0}, violations_{0};
+    int launches_ = 0;
+    std::mutex mu_;
+    std::string first_;
+};
+
+// The stage slots a workgroup issues for one operand: slots 0 .. last_slot
+// (each loading stage min(slot, nks - 1)), or the two that load the first and
+// the last stage.
+std::vector<int> stage_slots(const Replay &rp, int nks, int last_slot) {
+    std::vector<int> s;
+    if (rp.every_stage()) {
+        for (int i = 0; i <= last_slot; ++i) s.push_back(i);
+    } else {
+        s.push_back(0);
+        if (nks - 1 > 0) s.push_back(nks - 1);
+    }
+    return s;
+}
+
+struct TileRegions {
+    int hidden, w, target, pm, pl, zt, part, lse_in, probs;
+};
+
+// logprob_tile_kernel<WS, MODE, TM> over `blocks` workgroups of 256 threads.
+void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const LogprobArgs &a, int64_t blocks,
+                 const TileRegions &rg) {
+    rp.launch(name, blocks, [&](int64_t b, Replay::Lane &ln) {
+        const TileCoord tc = tile_coord(mode, TM, b, a);
+        const int VW = 64 * TM, WBLK = VW / 32;
+        const int64_t H = a.H, r0 = tc.rt * kRowTile;
+        const int wlast = stage_last(VW, a.V, tc.v0), hlast = stage_last(kRowTile, a.R, r0);
+        ln.thread = 0;
+        if (tc.nks < 1 || wlast < 0 || hlast < 0) {
+            ln.check(rg.w, 0, 1, "tile with no hidden step, vocab entry or row");
+            return;
+        }
+        const uint64_t wg = Replay::addr(a.w) + static_cast<uint64_t>(tc.v0 * H) * 2;
+        const uint64_t hg = Replay::addr(a.hidden) + static_cast<uint64_t>(r0 * H) * 2;
+        // the hidden rows of slots 0 .. nks + 1, the weights of 0 .. nks - 1 + WS
+        const std::vector<int> hs = stage_slots(rp, tc.nks, tc.nks + 1), ws = stage_slots(rp, tc.nks, tc.nks - 1 + WS);
+        for (int wave = 0; wave < 4; ++wave)
+            for (int lane = 0; lane < 64; ++lane) {
+                ln.thread = wave * 64 + lane;
+                for (int j = 0; j < WBLK; ++j) {
+                    const int row = stage_row(wave * WBLK + j, lane);
+                    const uint32_t voff = stage_voff(row, wlast, H, stage_chunk(row, lane));
+                    for (int slot : ws) ln.check(rg.w, wg + stage_k0(tc.kb, slot, tc.nks) * 2 + voff, 16, "weight stage load");
+                }
+                for (int j = 0; j < 8; ++j) {
+                    const int row = stage_row(wave * 8 + j, lane);
+                    const uint32_t voff = stage_voff(row, hlast, H, stage_chunk(row, lane));
+                    for (int slot : hs) ln.check(rg.hidden, hg + stage_k0(tc.kb, slot, tc.nks) * 2 + voff, 16, "hidden stage load");
+                }
+            }
+        // epilogues
+        const uint64_t tgt = Replay::addr(a.target);
+        for (int wave = 0; wave < 4; ++wave) {
+            const int wm = wave & 1, wn = wave >> 1;
+            for (int lane = 0; lane < 64; ++lane) {
+                ln.thread = wave * 64 + lane;
+                const int l32 = lane & 31, h2 = lane >> 5;
+                if (mode == kPartialK) {
+                    for (int tm = 0; tm < 4; ++tm)
+                        for (int tn = 0; tn < 4; ++tn)
+                            for (int q = 0; q < 4; ++q)
+                                ln.check(rg.part, Replay::addr(a.part) + part_elem(b, wave, tm, tn, q, lane) * 4, 16,
+                                         "tail part store");
+                    continue;
+                }
+                for (int tn = 0; tn < 4; ++tn) {
+                    const int row = wn * 128 + tn * 32 + l32;
+                    const int64_t rr = r0 + row;
+                    if (mode == kBwdProbs) {
+                        if (rr < a.R) {
+                            ln.check(rg.target, tgt + rr * 4, 4, "target load");
+                            ln.check(rg.lse_in, Replay::addr(a.lse_in) + rr * 4, 4, "lse load");
+                        }
+                        const uint64_t pb = Replay::addr(a.probs) +
+                                            probs_block(tc.rt, a.n_vocab_tiles * 4LL, tc.vt * 4 + wm * 2) * 2;
+                        for (int tm = 0; tm < 4; ++tm)
+                            for (int q = 0; q < 4; ++q)
+                                ln.check(rg.probs, pb + probs_store_off(tm, q, row, h2) * 2, 8, "probability store");
+                    } else if (rr < a.R) {   // forward: the row's target, and its logit if the tile holds it
+                        ln.check(rg.target, tgt + rr * 4, 4, "target load");
+                        ln.check(rg.zt, Replay::addr(a.zt) + rr * 4, 4, "target logit store");
+                    }
+                }
+            }
+        }
+        if (mode == kFwd || mode == kNarrow)
+            for (int tid = 0; tid < 256; ++tid) {
+                ln.thread = tid;
+                const int64_t rr = r0 + tid;
+                if (rr < a.R) {
+                    ln.check(rg.pm, Replay::addr(a.pm) + (tc.vt * a.R + rr) * 4, 4, "partial max store");
+                    ln.check(rg.pl, Replay::addr(a.pl) + (tc.vt * a.R + rr) * 4, 4, "partial sum store");
+                }
+            }
+    });
+}
+
+// logprob_tail_reduce_kernel: 8 workgroups of 128 threads per tail tile.
+void replay_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegions &rg) {
+    rp.launch("logprob_tail_reduce_kernel", t.tail_tiles * 8, [&](int64_t b, Replay::Lane &ln) {
+        const int64_t j = b >> 3;
+        const int wn = (b >> 2) & 1, tn = b & 3;
+        int64_t vt, rt;
+        tile_of_logical(t.tile_base + j, t.n_vocab_tiles, t.n_row_tiles, &vt, &rt);
+        for (int tid = 0; tid < 128; ++tid) {
+            ln.thread = tid;
+            const int wm = tid >> 6, lane = tid & 63, l32 = lane & 31;
+            const int wave = wn * 2 + wm;
+            for (int sp = 0; sp < t.splits; ++sp)
+                for (int tm = 0; tm < 4; ++tm)
+                    for (int q = 0; q < 4; ++q)
+                        ln.check(rg.part, Replay::addr(t.part) + part_elem(j * t.splits + sp, wave, tm, tn, q, lane) * 4,
+                                 16, "tail part load");
+            const int64_t rr = rt * kRowTile + wn * 128 + tn * 32 + l32;
+            if (rr < t.R) {
+                ln.check(rg.target, Replay::addr(t.target) + rr * 4, 4, "target load");
+                ln.check(rg.zt, Replay::addr(t.zt) + rr * 4, 4, "target logit store");
+            }
+            if (tid < 32) {
+                const int64_t r = rt * kRowTile + wn * 128 + tn * 32 + tid;
+                if (r < t.R) {
+                    ln.check(rg.pm, Replay::addr(t.pm) + (vt * t.R + r) * 4, 4, "partial max store");
+                    ln.check(rg.pl, Replay::addr(t.pl) + (vt * t.R + r) * 4, 4, "partial sum store");
+                }
+            }
+        }
+    });
+}
+
+// The combine kernel launch_logprob picks for a.R rows.
+void replay_combine(Replay &rp, const LogprobArgs &a, const TileRegions &rg, int logprob_r, int lse_r) {
+    const int kind = logprob_combine_kind(a.R);
+    const int64_t blocks = kind == kCombineBlock ? a.R : kind == kCombineWave ? (a.R + 3) / 4 : (a.R + 255) / 256;
+    rp.launch(kind == kCombineBlock ? "logprob_combine_block_kernel"
+                                    : kind == kCombineWave ? "logprob_combine_wave_kernel" : "logprob_combine_row_kernel",
+              blocks, [&](int64_t b, Replay::Lane &ln) {
+                  for (int tid = 0; tid < 256; ++tid) {
+                      ln.thread = tid;
+                      int64_t r, vt0, step;
+                      bool finisher;
+                      if (kind == kCombineBlock) {
+                          r = b, vt0 = tid, step = 256, finisher = tid == 0;
+                      } else if (kind == kCombineWave) {
+                          r = b * 4 + (tid >> 6), vt0 = tid & 63, step = 64, finisher = (tid & 63) == 0;
+                      } else {
+                          r = b * 256 + tid, vt0 = 0, step = 1, finisher = true;
+                      }
+                      if (r >= a.R) continue;
+                      for (int64_t vt = vt0; vt < a.n_partials; vt += step) {
+                          ln.check(rg.pm, Replay::addr(a.pm) + (vt * a.R + r) * 4, 4, "partial max load");
+                          ln.check(rg.pl, Replay::addr(a.pl) + (vt * a.R + r) * 4, 4, "partial sum load");
+                      }
+                      if (finisher) {
+                          ln.check(rg.target, Replay::addr(a.target) + r * 4, 4, "target load");
+                          ln.check(rg.zt, Replay::addr(a.zt) + r * 4, 4, "target logit load");
+                          ln.check(logprob_r, Replay::addr(a.logprob) + r * 4, 4, "logprob store");
+                          if (a.lse) ln.check(lse_r, Replay::addr(a.lse) + r * 4, 4, "lse store");
+                      }
+                  }
+              });
+}
+
+// logprob_bwd_gemm_kernel<WS>.
+void replay_bwd_gemm(Replay &rp, const LogprobBwdArgs &a, int probs_r, int w_r, int out_r) {
+    const int WS = tile_weight_stages(a.n_row_tiles);
+    rp.launch("logprob_bwd_gemm_kernel", bwd_gemm_blocks(a), [&](int64_t b, Replay::Lane &ln) {
+        int split, ht, rt;
+        gemm_tile_of(b, a.n_h_tiles, a.n_row_tiles, a.splits, &split, &ht, &rt);
+        const int H = a.H, h0 = ht * 256;
+        const int ks0 = split * a.steps_per_split;
+        const int nks = std::min(a.steps_per_split, a.n_vsteps - ks0);
+        ln.thread = 0;
+        if (nks < 1 || rt >= a.n_row_tiles || h0 >= H) {
+            ln.check(out_r, 0, 1, "workgroup outside the vocabulary, rows or hidden size");
+            return;
+        }
+        const int clast = bwd_clast(H, h0);
+        const std::vector<int> as = stage_slots(rp, nks, nks + 1), bs = stage_slots(rp, nks, nks - 1 + WS);
+        for (int wave = 0; wave < 4; ++wave)
+            for (int lane = 0; lane < 64; ++lane) {
+                ln.thread = wave * 64 + lane;
+                for (int j = 0; j < 8; ++j) {
+                    const int blk = wave * 8 + j;
+                    for (int slot : as)
+                        ln.check(probs_r, Replay::addr(a.probs) + bwd_a_elem(rt, a.n_vsteps, ks0, slot, nks, blk, lane) * 2,
+                                 16, "probability stage load");
+                    const int row = bwd_b_row(blk, lane);
+                    for (int slot : bs)
+                        ln.check(w_r,
+                                 Replay::addr(a.w) +
+                                     bwd_b_elem(ks0, slot, nks, row, bwd_b_chunk(row, lane), clast, a.V, H, h0) * 2,
+                                 16, "weight stage load");
+                }
+            }
+        const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;
+        const uint64_t out = Replay::addr(a.dpart) + bwd_out_base(split, rows_pad, rt, H, h0) * 4;
+        const int64_t rlim = a.rows - static_cast<int64_t>(rt) * 256;
+        for (int wave = 0; wave < 4; ++wave) {
+            const int wm = wave & 1, wn = wave >> 1;
+            for (int lane = 0; lane < 64; ++lane) {
+                ln.thread = wave * 64 + lane;
+                const int l32 = lane & 31, h2 = lane >> 5;
+                for (int tn = 0; tn < 4; ++tn) {
+                    const int h = wn * 128 + tn * 32 + l32;
+                    if (h0 + h >= H) continue;
+                    for (int tm = 0; tm < 4; ++tm)
+                        for (int i = 0; i < 16; ++i) {
+                            const int row = wm * 128 + tm * 32 + 8 * (i >> 2) + 4 * h2 + (i & 3);
+                            if (row < rlim) ln.check(out_r, out + bwd_out_off(row, H, h) * 4, 4, "partial sum store");
+                        }
+                }
+            }
+        }
+    });
+}
+
+// logprob_bwd_finish_kernel: one thread per 4 hidden entries of a row.
+void replay_bwd_finish(Replay &rp, const LogprobBwdArgs &a, int part_r, int w_r, int target_r, int grad_r, int dh_r) {
+    const int64_t per_row = a.H / 4;
+    rp.launch("logprob_bwd_finish_kernel", bwd_finish_blocks(a), [&](int64_t b, Replay::Lane &ln) {
+        const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;
+        for (int tid = 0; tid < kBwdFinishThreads; ++tid) {
+            ln.thread = tid;
+            const int64_t idx = b * kBwdFinishThreads + tid;
+            if (idx >= a.rows * per_row) continue;
+            const int64_t r = idx / per_row;
+            const int h = static_cast<int>(idx % per_row) * 4;
+            ln.check(target_r, Replay::addr(a.target) + r * 4, 4, "target load");
+            // a valid target t in [0, V): the split sums, W[t] and the gradient
+            for (int sp = 0; sp < a.splits; ++sp)
+                ln.check(part_r, Replay::addr(a.dpart) + bwd_part_elem(sp, rows_pad, r, a.H, h) * 4, 16,
+                         "partial sum load");
+            for (int64_t t : {static_cast<int64_t>(0), static_cast<int64_t>(a.V - 1)})
+                ln.check(w_r, Replay::addr(a.w) + (t * a.H + h) * 2, 8, "target weight load");
+            ln.check(grad_r, Replay::addr(a.grad) + r * 4, 4, "gradient load");
+            ln.check(dh_r, Replay::addr(a.dh) + (r * a.H + h) * 4, 16, "gradient store");
+        }
+    });
+}
+
+}  // namespace
+}  // namespace rlk
+
+extern "C" rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t hidden, int32_t vocab,
+                                             int32_t every_stage, int32_t shrink_region, rl_bounds_report *report) {
+    using namespace rlk;
+    if (!report) return RL_ERR_NULL_POINTER;
+    std::memset(report, 0, sizeof(*report));
+    std::string err;
+    Replay rp(every_stage != 0, shrink_region);
+    if (op == 0) {
+        LogprobPlan plan;
+        const rl_status st = plan_logprob(rows, hidden, vocab, &plan, &err);
+        if (st != RL_OK) return st;
+        if (rows == 0) return RL_OK;
+        TileRegions rg{};
+        rg.hidden = rp.add("hidden", static_cast<uint64_t>(rows) * hidden * 2);
+        rg.w = rp.add("w_lm", static_cast<uint64_t>(vocab) * hidden * 2);
+        rg.target = rp.add("target", static_cast<uint64_t>(rows) * 4);
+        const int lp = rp.add("logprob", static_cast<uint64_t>(rows) * 4);
+        const int ls = rp.add("lse", static_cast<uint64_t>(rows) * 4);
+        const int ws = rp.add("workspace", plan.total_bytes);
+        rg.pm = rp.section("workspace partial max", ws, plan.off_m, static_cast<uint64_t>(plan.n_partials) * rows * 4);
+        rg.pl = rp.section("workspace partial sum", ws, plan.off_l, static_cast<uint64_t>(plan.n_partials) * rows * 4);
+        rg.zt = rp.section("workspace target logits", ws, plan.off_zt, static_cast<uint64_t>(rows) * 4);
+        rg.part = rp.section("workspace tail parts", ws, plan.off_part, plan.total_bytes - plan.off_part);
+        const LogprobArgs a = logprob_args(plan, rp.ptr<void>(rg.hidden), rp.ptr<void>(rg.w), rp.ptr<int32_t>(rg.target),
+                                           1.f, rp.ptr<float>(lp), rp.ptr<float>(ls), rp.ptr<unsigned char>(ws));
+        // the launches of launch_logprob, in order
+        LogprobArgs d = a;
+        d.tile_base = 0;
+        d.tile_count = a.dp_tiles;
+        replay_tile(rp, "logprob_tile_kernel<kFwd>", kFwd, 4, tile_weight_stages(a.n_row_tiles), d, d.tile_count, rg);
+        if (a.narrow_tiles > 0)
+            replay_tile(rp, "logprob_tile_kernel<kNarrow>", kNarrow, 3, 3, a, a.narrow_tiles * a.n_row_tiles, rg);
+        if (a.tail_tiles > 0) {
+            LogprobArgs t = a;
+            t.tile_base = a.dp_tiles;
+            t.tile_count = a.tail_tiles;
+            replay_tile(rp, "logprob_tile_kernel<kPartialK>", kPartialK, 4, tile_weight_stages(a.n_row_tiles), t,
+                        a.tail_tiles * a.splits, rg);
+            replay_tail_reduce(rp, t, rg);
+        }
+        replay_combine(rp, a, rg, lp, ls);
+    } else if (op == 1) {
+        LogprobBwdPlan plan;
+        const rl_status st = plan_logprob_bwd(rows, hidden, vocab, &plan, &err);
+        if (st != RL_OK) return st;
+        if (rows == 0) return RL_OK;
+        TileRegions rg{};
+        rg.hidden = rp.add("hidden", static_cast<uint64_t>(rows) * hidden * 2);
+        rg.w = rp.add("w_lm", static_cast<uint64_t>(vocab) * hidden * 2);
+        rg.target = rp.add("target", static_cast<uint64_t>(rows) * 4);
+        rg.lse_in = rp.add("lse", static_cast<uint64_t>(rows) * 4);
+        const int grad = rp.add("grad_logprob", static_cast<uint64_t>(rows) * 4);
+        const int dh = rp.add("grad_hidden", static_cast<uint64_t>(rows) * hidden * 4);
+        const int ws = rp.add("workspace", plan.total_bytes);
+        const uint64_t rows_pad = static_cast<uint64_t>(plan.chunk_row_tiles) * kRowTile;
+        rg.probs = rp.section("workspace probabilities", ws, plan.off_probs,
+                              rows_pad * static_cast<uint64_t>(plan.n_vsteps) * kHiddenStep * 2);
+        const int part = plan.splits > 1 ? rp.section("workspace split sums", ws, plan.off_part,
+                                                      static_cast<uint64_t>(plan.splits) * rows_pad * hidden * 4)
+                                         : dh;
+        for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
+            LogprobArgs f;
+            LogprobBwdArgs b;
+            logprob_bwd_chunk_args(plan, c0, rp.ptr<uint16_t>(rg.hidden), rp.ptr<uint16_t>(rg.w),
+                                   rp.ptr<int32_t>(rg.target), 1.f, rp.ptr<float>(rg.lse_in), rp.ptr<float>(grad),
+                                   rp.ptr<float>(dh), rp.ptr<unsigned char>(ws), &f, &b);
+            replay_tile(rp, "logprob_tile_kernel<kBwdProbs>", kBwdProbs, 4, tile_weight_stages(f.n_row_tiles), f,
+                        static_cast<int64_t>(f.n_vocab_tiles) * f.n_row_tiles, rg);
+            replay_bwd_gemm(rp, b, rg.probs, rg.w, part);
+            replay_bwd_finish(rp, b, part, rg.w, rg.target, grad, dh);
+        }
+    } else {
+        return RL_ERR_INVALID_SHAPE;
+    }
+    rp.report(report);
+    return RL_OK;
+}

@@ -3,6 +3,7 @@
 #pragma once
 
 #include "device_common.h"
+#include "tile_index.h"
 
 namespace rlk {
 
@@ -12,30 +13,51 @@ namespace rlk {
 // not know that it writes LDS and does not put a wait for all loads in flight
 // in front of every LDS read (it cannot tell the stage buffers apart); the
 // kernels order these loads against their LDS reads with explicit waits.
-__device__ __forceinline__ void load_lds16(const uint16_t *g, uint16_t *l) {
+// M0 is an input operand ("{m0}"), so the compiler itself writes it and knows
+// that it holds the LDS base; the asm only reads it.  The leading s_nop is
+// the one wait state the ISA requires between an SALU write of M0 and an LDS
+// DMA instruction that reads it (the compiler's hazard tracking does not look
+// inside the asm).
+__device__ __forceinline__ uint32_t lds_base_u32(uint16_t *l) {
     typedef __attribute__((address_space(3))) uint16_t lds_u16;
-    const uint32_t lds_addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l)));
+    return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l))));
+}
+
+// A value the same in every lane of the wave, read first-lane so the compiler
+// keeps it (and what is computed from it) in SGPRs.  The tile coordinates come
+// out of 64-bit divisions the compiler expands on the VALU.  The builtin
+// returns a signed int: each half goes through uint32_t before widening, or
+// a low half with bit 31 set would sign-extend into the high half.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+    const uint64_t u = static_cast<uint64_t>(x);
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(u))));
+    const uint32_t hi =
+        static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(u >> 32))));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+__device__ __forceinline__ void load_lds16(const uint16_t *g, uint16_t *l) {
     asm volatile(
-        "s_mov_b32 m0, %1\n\t"
         "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, off"
         :
-        : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
-        : "memory", "m0");
+        : "v"(g), "{m0}"(lds_base_u32(l))
+        : "memory");
 }
 
 // The same with a wave-uniform base in SGPRs and a per-lane 32-bit byte offset
 // (the global_load_lds "saddr" form): no 64-bit address arithmetic per lane.
+// The base must be computed on the scalar unit: the compiler's hazard
+// tracking does not see that the asm's VMEM instruction reads those SGPRs, so
+// a VALU write of them (a v_readfirstlane) right before it would need 5 wait
+// states it does not get.  build.py checks the gfx950 assembly for that.
 __device__ __forceinline__ void load_lds16_s(const void *base, uint32_t voff, uint16_t *l) {
-    typedef __attribute__((address_space(3))) uint16_t lds_u16;
-    const uint32_t lds_addr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l)));
     asm volatile(
-        "s_mov_b32 m0, %2\n\t"
         "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, %1"
         :
-        : "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
-        : "memory", "m0");
+        : "v"(voff), "s"(base), "{m0}"(lds_base_u32(l))
+        : "memory");
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
@@ -50,36 +72,6 @@ __device__ __forceinline__ void barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-}
-
-// Element offset of 16-byte chunk c (0..7) of row `row` in a [rows][64] bf16
-// stage image.  Rows are 128 bytes, so two rows share one 256-byte window of
-// the 64 LDS banks; XOR-ing the chunk with row bits 1..3 gives the 16 rows
-// that one ds_read_b128 pass serves (same chunk, consecutive rows) 16 distinct
-// 16-byte slots of that window.
-__device__ __forceinline__ int op_off(int row, int c) { return row * 64 + ((c ^ ((row >> 1) & 7)) << 3); }
-
-// Logical tile index -> (n-tile, m-tile): groups of 4 m-tiles sweep the
-// n-tiles together, so an n-tile's operand is fetched into an L2 once for 4
-// m-tiles while the m-tiles' operand stays resident in L2 / the MALL.
-__device__ __forceinline__ void tile_of_logical(int64_t L, int64_t nnt, int64_t nmt, int64_t *nt, int64_t *mt) {
-    constexpr int64_t GR = 4;
-    const int64_t group = L / (GR * nnt);
-    const int64_t in = L % (GR * nnt);
-    const int64_t rows_in_group = min(GR, nmt - group * GR);
-    *mt = group * GR + in % rows_in_group;
-    *nt = in / rows_in_group;
-}
-
-// Launch index -> (n-tile, m-tile) for a launch over logical tiles [base,
-// base + count).  The hardware hands consecutive workgroups to the 8 XCDs in
-// turn; renumbering gives each XCD a contiguous run of logical tiles, so the
-// sharing above happens inside one XCD's L2.
-__device__ __forceinline__ void tile_of(int64_t b, int64_t count, int64_t base, int64_t nnt, int64_t nmt,
-                                        int64_t *nt, int64_t *mt) {
-    const int64_t full = count / 8 * 8;
-    const int64_t L = b < full ? (b % 8) * (count / 8) + b / 8 : b;
-    tile_of_logical(base + L, nnt, nmt, nt, mt);
 }
 
 }  // namespace rlk

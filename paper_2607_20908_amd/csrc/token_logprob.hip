@@ -42,13 +42,8 @@ static_assert(kBlocksPerWave == 8, "staging layout");
 // only the weights stream from HBM; a third weight stage gives them two
 // stages to arrive (WS = 3 fills the whole 160 KB of LDS).  With many row
 // tiles both operands miss and WS = 2 measures better.
-// Epilogue modes: the forward's (max, sum) partials; the backward's
-// p = exp(inv_T z - lse) per (row, vocab entry) as bf16 into the blocked
-// probability buffer; or the sampling head's tempered fp32 logits (per-row
-// temperature) plus the tile's row maxima.
-// kNarrow is the forward over the narrow tiles of a last round (TM < 4); the
-// sampling head's kLogits takes narrow tiles as well.
-enum : int { kFwd = 0, kBwdProbs = 1, kLogits = 2, kPartialK = 3, kNarrow = 4 };
+// The epilogue modes (kFwd, kBwdProbs, kLogits, kPartialK, kNarrow) and
+// the tile each workgroup computes are defined with the index arithmetic.
 
 // Forward epilogue of one 32-row column of a (64 TM) x 256 logit tile, as one
 // lane of a wave holds it: z(tm)[i] is vocab vbase + tm*32 + 8*(i/4) + 4*h2 +
@@ -200,33 +195,9 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave & 1, wn = wave >> 1;     // vocab half (32 TM entries), row half (128 rows)
     const int l32 = lane & 31, h2 = lane >> 5;
-    int64_t vt, rt, v0;                          // vt: the partial slot of the tile
-    int kb = 0, nks = a.H / kK;                  // hidden steps [kb, kb + nks)
-    if constexpr (TM != 4) {
-        // narrow tile j covers vocab [narrow_v0 + j VW, + VW) for row tile
-        // rt; the row tiles of one j are neighbours in launch order, which
-        // gives each XCD a contiguous run as tile_of does
-        const int64_t count = a.narrow_tiles * a.n_row_tiles, b = blockIdx.x;
-        const int64_t full = count / 8 * 8;
-        const int64_t L = b < full ? (b % 8) * (count / 8) + b / 8 : b;
-        const int64_t j = L / a.n_row_tiles;
-        rt = L % a.n_row_tiles;
-        vt = a.narrow_slot0 + j;
-        v0 = a.narrow_v0 + j * VW;
-    } else if constexpr (MODE == kPartialK) {
-        // part s of tail tile j covers hidden steps [s n / S, (s + 1) n / S)
-        const int64_t j = blockIdx.x / a.splits;
-        const int sp = static_cast<int>(blockIdx.x % a.splits);
-        tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
-        kb = sp * nks / a.splits;
-        nks = (sp + 1) * nks / a.splits - kb;
-    } else if constexpr (MODE == kFwd || MODE == kLogits) {
-        tile_of(blockIdx.x, a.tile_count, a.tile_base, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
-    } else {
-        tile_of(blockIdx.x, static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles, 0, a.n_vocab_tiles,
-                a.n_row_tiles, &vt, &rt);
-    }
-    if constexpr (TM == 4) v0 = vt * kVocabTile;
+    const TileCoord tc = tile_coord(MODE, TM, blockIdx.x, a);
+    const int64_t vt = uniform64(tc.vt), rt = uniform64(tc.rt), v0 = uniform64(tc.v0);   // vt: the tile's partial slot
+    const int kb = tc.kb, nks = tc.nks;                 // hidden steps [kb, kb + nks)
     const int64_t r0 = rt * kRowTile;
     const int64_t H = a.H;
 
@@ -237,20 +208,17 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     // Rows past the vocabulary / the batch re-read the last valid row.
     const uint16_t *wg = a.w + v0 * H;
     const uint16_t *hg = a.hidden + r0 * H;
-    const int wlast = static_cast<int>(min(static_cast<int64_t>(VW - 1), a.V - 1 - v0));
-    const int hlast = static_cast<int>(min(static_cast<int64_t>(kRowTile - 1), a.R - 1 - r0));
+    const int wlast = stage_last(VW, a.V, v0);
+    const int hlast = stage_last(kRowTile, a.R, r0);
     // Block j of stage `slot`'s buffer gets the data of stage min(slot, nks-1):
     // past the last stage the loads refill a buffer nobody reads any more.
     auto wbuf = [&](int ks) { return wring + (ks % WS) * WELEMS; };
     auto hbuf = [&](int ks) { return hring + (ks & 1) * kTileElems; };
     auto issue_block = [&](const uint16_t *g, int last, uint16_t *st, int slot, int blk) {
-        const int row = blk * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ ((row >> 1) & 7);
-        const int64_t k0 = static_cast<int64_t>(kb + min(slot, nks - 1)) * kK;
+        const int row = stage_row(blk, lane);
         // wave-uniform base (SGPRs) plus a per-lane byte offset that stays
         // the same from stage to stage
-        const uint32_t voff = static_cast<uint32_t>((min(row, last) * H + c * 8) * 2);
-        load_lds16_s(g + k0, voff, st + blk * 512);
+        load_lds16_s(g + stage_k0(kb, slot, nks), stage_voff(row, last, H, stage_chunk(row, lane)), st + blk * 512);
     };
     auto issue_w = [&](int slot) {
 #pragma unroll
@@ -359,7 +327,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         const float c2 = a.inv_temperature * kLog2e;
         const int64_t vbase = v0 + wm * 128;
         const int vlim = vbase + 128 <= a.V ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
-        uint16_t *pb = a.probs + (rt * (a.n_vocab_tiles * 4LL) + vt * 4 + wm * 2) * kTileElems;
+        uint16_t *pb = a.probs + probs_block(rt, a.n_vocab_tiles * 4LL, vt * 4 + wm * 2);
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) {
             const int row = wn * 128 + tn * 32 + l32;
@@ -374,7 +342,6 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 #pragma unroll
             for (int tm = 0; tm < 4; ++tm) {
                 const f32x16 z = acc[tm][tn];
-                uint16_t *blk = pb + (tm >> 1) * kTileElems;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     uint32_t w2[2];
@@ -386,7 +353,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                         w2[e >> 1] = static_cast<uint32_t>(f32_to_bf16_bits(p0)) |
                                      (static_cast<uint32_t>(f32_to_bf16_bits(p1)) << 16);
                     }
-                    *reinterpret_cast<uint2 *>(blk + op_off(row, (tm & 1) * 4 + q) + 4 * h2) = make_uint2(w2[0], w2[1]);
+                    *reinterpret_cast<uint2 *>(pb + probs_store_off(tm, q, row, h2)) = make_uint2(w2[0], w2[1]);
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -435,7 +402,6 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     if constexpr (MODE == kPartialK) {
         // one part of a tail tile: its fp32 accumulators, in register order
         // (each store writes 1 KB contiguously), for the reduce kernel
-        float *dst = a.part + static_cast<int64_t>(blockIdx.x) * (kVocabTile * kRowTile);
 #pragma unroll
         for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
@@ -444,7 +410,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 for (int q = 0; q < 4; ++q) {
                     const f32x4 v = {acc[tm][tn][4 * q], acc[tm][tn][4 * q + 1], acc[tm][tn][4 * q + 2],
                                      acc[tm][tn][4 * q + 3]};
-                    *reinterpret_cast<f32x4 *>(dst + (((wave * 16 + tm * 4 + tn) * 4 + q) * 64 + lane) * 4) = v;
+                    *reinterpret_cast<f32x4 *>(a.part + part_elem(blockIdx.x, wave, tm, tn, q, lane)) = v;
                 }
         return;
     }
@@ -466,18 +432,16 @@ __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a)
     int64_t vt, rt;
     tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
     const int wave = wn * 2 + wm;                // the tile kernel's wave index
-    const float *src = a.part + j * a.splits * (kVocabTile * kRowTile);
     f32x16 z[4];
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm) z[tm] = f32x16{};
     for (int sp = 0; sp < a.splits; ++sp) {
-        const float *p = src + static_cast<int64_t>(sp) * (kVocabTile * kRowTile);
         f32x4 v[4][4];
 #pragma unroll
         for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                v[tm][q] = *reinterpret_cast<const f32x4 *>(p + (((wave * 16 + tm * 4 + tn) * 4 + q) * 64 + lane) * 4);
+                v[tm][q] = *reinterpret_cast<const f32x4 *>(a.part + part_elem(j * a.splits + sp, wave, tm, tn, q, lane));
 #pragma unroll
         for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
@@ -586,7 +550,7 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
     LogprobArgs d = a;
     d.tile_base = 0;
     d.tile_count = a.dp_tiles;
-    if (a.n_row_tiles <= 8)
+    if (tile_weight_stages(a.n_row_tiles) == 3)
         hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd>), dim3(static_cast<uint32_t>(d.tile_count)),
                            dim3(kTileThreads), 0, stream, d);
     else
@@ -610,7 +574,7 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
         t.tile_base = a.dp_tiles;
         t.tile_count = a.tail_tiles;
         const uint32_t parts = static_cast<uint32_t>(a.tail_tiles * a.splits);
-        if (a.n_row_tiles <= 8)
+        if (tile_weight_stages(a.n_row_tiles) == 3)
             hipLaunchKernelGGL((logprob_tile_kernel<3, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
         else
             hipLaunchKernelGGL((logprob_tile_kernel<2, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
@@ -621,10 +585,11 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (a.R <= 4096) {
+    const int combine = logprob_combine_kind(a.R);
+    if (combine == kCombineBlock) {
         hipLaunchKernelGGL(logprob_combine_block_kernel, dim3(static_cast<uint32_t>(a.R)), dim3(kThreads), 0, stream,
                            a);
-    } else if (a.R < 32768) {
+    } else if (combine == kCombineWave) {
         const int64_t blocks = (a.R + 3) / 4;
         hipLaunchKernelGGL(logprob_combine_wave_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0,
                            stream, a);
@@ -638,7 +603,7 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
 
 hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream) {
     const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
-    if (a.n_row_tiles <= 8)
+    if (tile_weight_stages(a.n_row_tiles) == 3)
         hipLaunchKernelGGL((logprob_tile_kernel<3, kBwdProbs>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
                            stream, a);
     else
@@ -653,7 +618,7 @@ hipError_t launch_logits(const LogprobArgs &a, hipStream_t stream) {
     d.tile_base = 0;
     d.tile_count = a.dp_tiles;
     if (d.tile_count > 0) {
-        if (a.n_row_tiles <= 8)
+        if (tile_weight_stages(a.n_row_tiles) == 3)
             hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits>), dim3(static_cast<uint32_t>(d.tile_count)),
                                dim3(kTileThreads), 0, stream, d);
         else

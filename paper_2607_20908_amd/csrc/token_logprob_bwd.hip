@@ -40,27 +40,6 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const uint16_t *p) {
     return __builtin_bit_cast(bf16x4, v);
 }
 
-// W band image: row v (0..63) holds 256 hidden entries as 32 chunks of 8;
-// chunk c sits in slot c ^ (4 * (v % 4)).  One transposing read pass (32
-// lanes) touches 4 consecutive rows x 4 consecutive chunks (c0 = 0 mod 4);
-// the XOR spreads them over the 16 slots of a 256-byte bank window.
-__device__ __forceinline__ int band_off(int v, int c) { return v * 256 + ((c ^ (4 * (v & 3))) << 3); }
-
-// Launch index -> (split, h tile, row tile).  XCD renumbering as in tile_of;
-// splits are outermost, so the workgroups of one XCD share a vocabulary
-// range, and inside a split 4 row tiles sweep the h tiles together.
-__device__ __forceinline__ void gemm_tile_of(int64_t b, const LogprobBwdArgs &a, int *split, int *ht, int *rt) {
-    const int64_t per_split = static_cast<int64_t>(a.n_h_tiles) * a.n_row_tiles;
-    const int64_t total = per_split * a.splits;
-    const int64_t full = total / 8 * 8;
-    const int64_t L = b < full ? (b % 8) * (total / 8) + b / 8 : b;
-    *split = static_cast<int>(L / per_split);
-    int64_t nt, mt;
-    tile_of_logical(L % per_split, a.n_h_tiles, a.n_row_tiles, &nt, &mt);
-    *ht = static_cast<int>(nt);
-    *rt = static_cast<int>(mt);
-}
-
 // S[rows, h] over one vocabulary range; one workgroup per 256 x 256 output
 // tile, each wave 128 rows x 128 hidden entries as 4 x 4 MFMA 32x32x16 tiles.
 template <int WS>
@@ -73,7 +52,7 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
     const int wm = wave & 1, wn = wave >> 1;     // row half, hidden half
     const int l32 = lane & 31, h2 = lane >> 5;
     int split, ht, rt;
-    gemm_tile_of(blockIdx.x, a, &split, &ht, &rt);
+    gemm_tile_of(blockIdx.x, a.n_h_tiles, a.n_row_tiles, a.splits, &split, &ht, &rt);
     const int H = a.H;
     const int h0 = ht * 256;
     const int ks0 = split * a.steps_per_split;
@@ -85,21 +64,18 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
     // 2 blk + i / 32 with chunk slot ^ (4 * (row % 4)).  Rows past the
     // vocabulary re-read the last row (their probabilities are 0); columns
     // past the hidden size re-read the last chunk (never stored).
-    const uint16_t *pg = a.probs + static_cast<int64_t>(rt) * a.n_vsteps * kTileElems;
-    const int clast = min(256, H - h0) / 8 - 1;
+    const int clast = bwd_clast(H, h0);
     auto abuf = [&](int s) { return aring + (s & 1) * kTileElems; };
     auto bbuf = [&](int s) { return bring + (s % WS) * kTileElems; };
     auto issue_a = [&](int slot, int j) {
         const int blk = wave * kBlocksPerWave + j;
-        const int64_t ks = ks0 + min(slot, nks - 1);
-        load_lds16(pg + ks * kTileElems + blk * 512 + lane * 8, abuf(slot) + blk * 512);
+        load_lds16(a.probs + bwd_a_elem(rt, a.n_vsteps, ks0, slot, nks, blk, lane), abuf(slot) + blk * 512);
     };
     auto issue_b = [&](int slot, int j) {
         const int blk = wave * kBlocksPerWave + j;
-        const int row = 2 * blk + (lane >> 5);
-        const int c = (lane & 31) ^ (4 * (row & 3));
-        const int64_t v = min(static_cast<int64_t>(ks0 + min(slot, nks - 1)) * 64 + row, static_cast<int64_t>(a.V - 1));
-        load_lds16(a.w + v * H + h0 + 8 * min(c, clast), bbuf(slot) + blk * 512);
+        const int row = bwd_b_row(blk, lane);
+        load_lds16(a.w + bwd_b_elem(ks0, slot, nks, row, bwd_b_chunk(row, lane), clast, a.V, H, h0),
+                   bbuf(slot) + blk * 512);
     };
 
     f32x16 acc[4][4];
@@ -202,7 +178,7 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
     // ---- epilogue: acc[tm][tn][i] is S at row wm*128 + tm*32 + 8*(i/4) +
     // 4*h2 + i%4 of the tile, hidden entry wn*128 + tn*32 + l32.
     const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;
-    float *out = a.dpart + (split * rows_pad + static_cast<int64_t>(rt) * 256) * H + h0;
+    float *out = a.dpart + bwd_out_base(split, rows_pad, rt, H, h0);
     const int64_t rlim = a.rows - static_cast<int64_t>(rt) * 256;
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn) {
@@ -213,7 +189,7 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int row = wm * 128 + tm * 32 + 8 * (i >> 2) + 4 * h2 + (i & 3);
-                if (row < rlim) out[static_cast<int64_t>(row) * H + h] = acc[tm][tn][i];
+                if (row < rlim) out[bwd_out_off(row, H, h)] = acc[tm][tn][i];
             }
     }
 }
@@ -234,9 +210,9 @@ __global__ __launch_bounds__(kThreads) void logprob_bwd_finish_kernel(LogprobBwd
         o = make_float4(nan, nan, nan, nan);
     } else {
         const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;
-        float4 sacc = *reinterpret_cast<const float4 *>(a.dpart + r * a.H + h);
+        float4 sacc = *reinterpret_cast<const float4 *>(a.dpart + bwd_part_elem(0, rows_pad, r, a.H, h));
         for (int sp = 1; sp < a.splits; ++sp) {
-            const float4 x = *reinterpret_cast<const float4 *>(a.dpart + (sp * rows_pad + r) * a.H + h);
+            const float4 x = *reinterpret_cast<const float4 *>(a.dpart + bwd_part_elem(sp, rows_pad, r, a.H, h));
             sacc.x += x.x;
             sacc.y += x.y;
             sacc.z += x.z;
@@ -254,8 +230,8 @@ __global__ __launch_bounds__(kThreads) void logprob_bwd_finish_kernel(LogprobBwd
 }  // namespace
 
 hipError_t launch_logprob_bwd_gemm(const LogprobBwdArgs &a, hipStream_t stream) {
-    const int64_t blocks = static_cast<int64_t>(a.n_row_tiles) * a.n_h_tiles * a.splits;
-    if (a.n_row_tiles <= 8)
+    const int64_t blocks = bwd_gemm_blocks(a);
+    if (tile_weight_stages(a.n_row_tiles) == 3)
         hipLaunchKernelGGL(logprob_bwd_gemm_kernel<3>, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream,
                            a);
     else
@@ -265,10 +241,10 @@ hipError_t launch_logprob_bwd_gemm(const LogprobBwdArgs &a, hipStream_t stream) 
 }
 
 hipError_t launch_logprob_bwd_finish(const LogprobBwdArgs &a, hipStream_t stream) {
-    const int64_t n = a.rows * (a.H / 4);
-    if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(logprob_bwd_finish_kernel, dim3(static_cast<uint32_t>((n + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, stream, a);
+    const int64_t blocks = bwd_finish_blocks(a);
+    if (blocks == 0) return hipSuccess;
+    static_assert(kBwdFinishThreads == kThreads, "finish launch shape");
+    hipLaunchKernelGGL(logprob_bwd_finish_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

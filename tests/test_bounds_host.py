@@ -1,0 +1,110 @@
+"""Host replay of the lm-head log-prob kernels' global accesses (no GPU).
+
+rl_debug_logprob_bounds replays every launch of rl_token_logprob (op 0) and
+rl_token_logprob_backward (op 1), workgroup by workgroup and lane by lane, with
+the arguments the entry points build and the kernels' own index functions, and
+checks each load and store against the allocation or workspace section it must
+fall in.  The shapes are the ones the bench and the parity tests run (the
+8B-class and 32B-class decode-step rows, one full 16384-row backward chunk,
+the 262144-row policy pass) plus ragged small shapes replayed at every stage.
+
+A call's accesses depend only on (rows, hidden, vocab) and its own pointers:
+neither entry point keeps state between calls, so a sequence of calls (one
+forward, then many backward calls at one shape, then at another) is covered by
+replaying each shape once.
+
+The shrink checks make one allocation 16 bytes smaller than the entry point
+requires: every allocation the kernels use up to its last byte must then
+report a violation, which shows that the checker sees overruns and that each
+allocation is exactly as large as the kernels need.
+"""
+import ctypes
+
+import pytest
+
+import paper_2607_20908_amd as rk
+
+_f = rk.lib().rl_debug_logprob_bounds
+
+V = 151936
+# (rows, hidden, vocab, every_stage)
+SHAPES = [
+    (512, 4096, V, 0),        # 8B-class decode step: whole tiles + narrow last round; backward split 8 ways
+    (256, 5120, V, 0),        # 32B-class decode step
+    (16384, 5120, V, 0),      # one full backward chunk, unsplit
+    (262144, 5120, V, 0),     # policy pass: 16 backward chunks, one-thread-per-row combine
+    (300, 128, 1000, 1),      # ragged rows and vocab
+    (40000, 64, 700, 1),      # ragged last backward chunk; row combine; split hidden
+    (1, 64, 1, 1),            # one row, one vocab entry
+    (4097, 192, 77777, 0),    # wave combine; ragged vocab tile
+    (8000, 4096, 2500, 0),    # tail parts: 320 tiles, the last 64 split 4 ways over the hidden dimension
+]
+
+
+def replay(op, rows, hidden, vocab, every=0, shrink=-1):
+    return rk.logprob_bounds(op, rows, hidden, vocab, every_stage=bool(every), shrink_region=shrink)
+
+
+@pytest.mark.parametrize("op", [0, 1], ids=["forward", "backward"])
+@pytest.mark.parametrize("rows,hidden,vocab,every", SHAPES)
+def test_every_access_inside_its_allocation(op, rows, hidden, vocab, every):
+    rep = replay(op, rows, hidden, vocab, every)
+    assert rep.accesses > 0 and rep.launches >= 2
+    assert rep.violations == 0, rep.first_violation.decode()
+
+
+def test_backward_launch_count_per_chunk():
+    # three launches (probabilities, GEMM, finish) per 16384-row chunk
+    assert replay(1, 262144, 5120, V).launches == 3 * 16
+    assert replay(1, 40000, 64, 700).launches == 3 * 3
+
+
+def test_forward_launches_follow_the_plan():
+    # 8B-class: whole tiles, narrow last round, combine;
+    # 8000 x 4096 x 2500 has a hidden-split tail (tile parts + reduce)
+    assert replay(0, 512, 4096, V).launches == 3
+    assert replay(0, 8000, 4096, 2500).launches == 4
+
+
+# region indices (in the order the replay allocates them) that the kernels
+# use up to their last byte; the parent workspace allocation itself is only
+# checked through its sections
+FWD_TIGHT = {"hidden": 0, "w_lm": 1, "target": 2, "logprob": 3, "lse": 4, "partial max": 6, "partial sum": 7,
+             "target logits": 8}
+BWD_TIGHT = {"hidden": 0, "w_lm": 1, "target": 2, "lse": 3, "grad_logprob": 4, "grad_hidden": 5, "probabilities": 7}
+
+
+@pytest.mark.parametrize("rows,hidden,vocab", [(512, 4096, V), (300, 128, 1000), (8000, 4096, 2500)])
+def test_shrunk_allocation_is_caught_forward(rows, hidden, vocab):
+    n = replay(0, rows, hidden, vocab).regions
+    for name, i in FWD_TIGHT.items():
+        rep = replay(0, rows, hidden, vocab, shrink=i)
+        assert rep.violations > 0, f"shrinking {name} went unnoticed"
+    assert replay(0, rows, hidden, vocab, shrink=5).violations == 0   # the workspace's own extent
+    # tail parts exist only with a hidden-split last round
+    tail = replay(0, rows, hidden, vocab, shrink=9).violations
+    assert (tail > 0) == (rows == 8000)
+    assert n == 10
+
+
+@pytest.mark.parametrize("rows,hidden,vocab,splits", [(512, 4096, V, True), (16384, 5120, V, False),
+                                                      (300, 128, 1000, False), (300, 128, 20000, True)])
+def test_shrunk_allocation_is_caught_backward(rows, hidden, vocab, splits):
+    rep0 = replay(1, rows, hidden, vocab)
+    for name, i in BWD_TIGHT.items():
+        rep = replay(1, rows, hidden, vocab, shrink=i)
+        assert rep.violations > 0, f"shrinking {name} went unnoticed"
+    assert replay(1, rows, hidden, vocab, shrink=6).violations == 0   # the workspace's own extent
+    assert rep0.regions == (9 if splits else 8)
+    if splits:
+        # the split sums are padded to whole 256-row tiles: used to the last
+        # byte only when the rows fill their last tile
+        assert (replay(1, rows, hidden, vocab, shrink=8).violations > 0) == (rows % 256 == 0)
+
+
+def test_invalid_arguments():
+    rep = rk.BoundsReport()
+    assert _f(2, 8, 64, 100, 0, -1, ctypes.byref(rep)) == 2          # unknown op
+    assert _f(0, 8, 96, 100, 0, -1, ctypes.byref(rep)) == 3          # hidden not a multiple of 64
+    assert _f(1, 8, 64, 100, 0, -1, None) == 1
+    assert replay(0, 0, 64, 100).launches == 0
