@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 8
+#define RL_ABI_VERSION 9
 
 typedef enum {
     RL_OK = 0,
@@ -305,6 +305,28 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab,
                            const int32_t *target, float inv_temperature,
                            float *logprob, float *lse,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * rl_token_logprob without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  It calls no hipMalloc, hipFree or other
+ * allocating routine.  The workspace rl_token_logprob_workspace_size reports
+ * lives instead in a static device array of RL_NOALLOC_SCRATCH_BYTES
+ * (128 MiB), one per GPU the library runs on, held until the process ends;
+ * its address is looked up once per device on the first call there.  Sizes
+ * whose workspace exceeds it return RL_ERR_UNSUPPORTED before any launch
+ * (the decode-step shapes fit; at a 151936-entry vocabulary, rows up to about
+ * 28000 when no hidden-split tail is planned); the other arguments, results,
+ * statuses and kernels are rl_token_logprob's.  Every call on one GPU shares
+ * that GPU's array: calls whose executions overlap on one GPU (other
+ * streams, or other threads) race and give wrong results; calls in order on
+ * one stream are safe.  Nothing in the array needs clearing between calls.
+ */
+#define RL_NOALLOC_SCRATCH_BYTES (128u << 20)
+rl_status rl_token_logprob_noalloc(int64_t rows, int32_t hidden, int32_t vocab,
+                                   const void *hidden_states, const void *w_lm,
+                                   const int32_t *target, float inv_temperature,
+                                   float *logprob, float *lse, void *stream);
 
 /*
  * Backward of rl_token_logprob with respect to the hidden rows, for the

@@ -94,7 +94,8 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_decode_plan_debug", "rl_grpo_advantage", "rl_grpo_surrogate_workspace_size",
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
-           "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds"]
+           "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds",
+           "rl_token_logprob_noalloc"]
 
 
 def _load():
@@ -141,7 +142,9 @@ def _load():
     lib.rl_extend_attn.argtypes = [P, P, P, P, SZ, P]
     lib.rl_debug_logprob_bounds.restype = ctypes.c_int
     lib.rl_debug_logprob_bounds.argtypes = [I32, I64, I32, I32, I32, I32, ctypes.POINTER(BoundsReport)]
-    if lib.rl_abi_version() != 8:
+    lib.rl_token_logprob_noalloc.restype = ctypes.c_int
+    lib.rl_token_logprob_noalloc.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P]
+    if lib.rl_abi_version() != 9:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -500,6 +503,37 @@ def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor
                                  float(inv_temperature), _ptr(logprob), _ptr(lse),
                                  ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                  _stream_handle(stream)), "rl_token_logprob")
+    return logprob, lse
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def token_logprob_noalloc(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
+                          logprob: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                          inv_temperature: float = 1.0, stream=None):
+    """token_logprob through rl_token_logprob_noalloc: no workspace, and
+    nothing allocated here either (the caller passes the outputs).  Its
+    scratch is one static device array per GPU, so calls that overlap on a GPU
+    race; sizes whose workspace exceeds NOALLOC_SCRATCH_BYTES raise."""
+    _bf16_dev(hidden, "hidden")
+    _bf16_dev(w_lm, "w_lm")
+    _on_device(target, "target")
+    if target.dtype != torch.int32 or not target.is_contiguous():
+        raise TypeError("target must be a contiguous int32 tensor")
+    R, H = hidden.shape
+    V, H2 = w_lm.shape
+    if H2 != H or target.shape != (R,):
+        raise ValueError("shapes: hidden [R, H], w_lm [V, H], target [R]")
+    for t, n in ((logprob, "logprob"), (lse, "lse")):
+        if t is None and n == "lse":
+            continue
+        _on_device(t, n)
+        if t.dtype != torch.float32 or t.shape != (R,) or not t.is_contiguous():
+            raise ValueError(f"{n} must be a contiguous fp32 [R] tensor")
+    _check(_lib.rl_token_logprob_noalloc(R, H, V, _ptr(hidden), _ptr(w_lm), _ptr(target), float(inv_temperature),
+                                         _ptr(logprob), _ptr(lse) if lse is not None else None,
+                                         _stream_handle(stream)), "rl_token_logprob_noalloc")
     return logprob, lse
 
 

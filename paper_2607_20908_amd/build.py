@@ -26,7 +26,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "librlkern.so")
-SOURCES = ["plan.cpp", "abi.cpp", "bounds.cpp", "decode_attn.hip", "extend_attn.hip", "kv_append.hip", "token_logprob.hip", "token_logprob_bwd.hip", "sample_top_p.hip", "grpo.hip"]
+SOURCES = ["plan.cpp", "abi.cpp", "bounds.cpp", "decode_attn.hip", "extend_attn.hip", "kv_append.hip", "token_logprob.hip", "token_logprob_bwd.hip", "sample_top_p.hip", "grpo.hip", "noalloc.hip"]
 ARCH = "gfx950"
 # sources whose kernels stage tiles through the inline-asm global->LDS loads
 STAGING_ASM = ["extend_attn.hip", "token_logprob.hip", "token_logprob_bwd.hip"]

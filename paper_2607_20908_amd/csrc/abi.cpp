@@ -9,6 +9,7 @@
 #include <string>
 #include <vector>
 
+#include "abi_error.h"
 #include "kernels.h"
 #include "logprob_args.h"
 #include "plan.h"
@@ -28,6 +29,16 @@ rl_status hip_error(hipError_t e, const char *what) {
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+namespace rlk {
+void abi_clear_error() { g_last_error.clear(); }
+rl_status abi_fail(rl_status st, const std::string &msg) { return set_error(st, msg); }
+rl_status abi_hip_fail(hipError_t e, const char *what) { return hip_error(e, what); }
+}  // namespace rlk
+
+namespace {
 
 // Pinned host staging for the work-list upload.  The slots are coherent,
 // device-mapped host memory that a small kernel on the caller's stream reads

@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 8
+    assert lib.rl_abi_version() == 9
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -587,3 +587,23 @@ def test_extend_noops_and_sizes():
     st, n = extend_call(Hq=8, Hkv=1, ls=[200] * 4, nl=[100] * 4, qs=[0, 100, 200, 300], suffix_rows=800,
                         q_rows=400, size_only=True)
     assert st == OK and n == ((4 * 4 * 48 + 255) // 256) * 256   # 100 tokens x 8 heads = 4 blocks each
+
+
+# ---------------------------------------------------------------- no-alloc variant
+def test_noalloc_validation_before_any_hip_call():
+    lib = rk.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    # rows 0: a valid no-op
+    assert lib.rl_token_logprob_noalloc(0, 64, 100, None, None, None, 1.0, None, None, None) == 0
+    # NULL target
+    assert lib.rl_token_logprob_noalloc(4, 64, 100, fake, fake, None, 1.0, fake, None, None) == 1
+    # hidden not a multiple of 64
+    assert lib.rl_token_logprob_noalloc(4, 96, 100, fake, fake, fake, 1.0, fake, None, None) == 3
+    # a workspace larger than the static scratch
+    R, H, V = 65536, 64, 151936
+    assert rk.token_logprob_workspace_size(R, H, V) > rk.NOALLOC_SCRATCH_BYTES
+    assert lib.rl_token_logprob_noalloc(R, H, V, fake, fake, fake, 1.0, fake, fake, None) == 3
+    assert b"scratch" in lib.rl_last_error()
+    # the 8B-class and 32B-class decode-step rows fit
+    assert rk.token_logprob_workspace_size(512, 4096, 151936) <= rk.NOALLOC_SCRATCH_BYTES
+    assert rk.token_logprob_workspace_size(256, 5120, 151936) <= rk.NOALLOC_SCRATCH_BYTES
