@@ -4,25 +4,38 @@
 A step is one pass of the whole path over one batch of synthetic input that is
 already resident in HBM: prefix-shared decode attention for all candidates of
 the batch, then the fused lm-head token log-prob of their rows.  The default
-workload is the 8B-class single-layer decode step (64 prompts x G=8, 32 query
-/ 8 kv heads, head dim 128, shared prefix 1024, suffix lengths uniform in
-[256, 2048]; lm-head 512 rows x hidden 4096 x vocab 151936).
+(headline) workload is the 32B-class single-layer decode step, the largest
+configuration with both halves of the path: 16 prompts x G=16, 64 query / 8
+kv heads, head dim 128, shared prefix 2048, suffix lengths uniform in [512,
+8192]; lm-head 256 rows x hidden 5120 x vocab 151936.  `value` is its decode
+attention's effective KV bandwidth (algorithmic bytes, the prefix counted once
+per prompt, over the measured decode time); `roofline` is the entry of the
+operation that takes the most time, `roofline_other` the other one's.
 
-After the timed steps, further operations are timed in a loop of their own
-(outside the step): the KV append of one token per candidate, the extend
-(prefill) of a refinement turn at the same shape with every suffix token new,
-the backward
-of the lm-head log-prob for the same rows,
-the GRPO advantages and clipped surrogate over the policy pass's 262144 rows,
-and (at decode shapes) the nucleus sampling head over the same rows.  They
-are reported under "extra_ops".
+The same run then measures the other configurations (--also, by default the
+8B-class step, the multi-turn long context and the 262144-row policy pass),
+each reported under "configs" with its own roofline entries, host time per
+call and CPU baseline.  They are not part of the headline's timed steps.
 
-Prints ONE JSON line.  `value` is decode attention's effective KV bandwidth
-(algorithmic bytes, the prefix counted once per prompt, over the measured
-decode time); the lm-head's TFLOP/s are reported beside it.  Per-operation
-durations come from HIP events recorded on the stream the kernels run on
-(created with a device-scope release, so recording one does not write back the
-L2 to system memory and the interval matches the kernels' own durations).
+Before every timed operation a 1 GiB buffer is read (outside the events), so
+no operation finds its inputs in the 256 MB MALL or the L2 from the previous
+one.  It is read, not written: a written buffer leaves the MALL full of
+dirty lines, and their write-back would land inside the next timed
+operation.  Per-operation durations are the medians of HIP events recorded on
+the stream the kernels run on (created with a device-scope release, so
+recording one does not write back the L2 to system memory and the interval
+matches the kernels' own durations).  host_us is the wall time of the host
+side of one call with the GPU idle (the binding's marshalling, the library's
+planning and the launches), the median of a separate loop.
+
+After the headline's steps, further operations at its shape are timed in
+loops of their own and reported under "extra_ops": the KV append of one
+token per candidate, the extend (prefill) of a refinement turn with every
+suffix token new, the backward of the lm-head log-prob for the same rows, the
+GRPO advantages and clipped surrogate over the policy pass's 262144 rows, and
+the nucleus sampling head over the same rows.
+
+Prints ONE JSON line.
 """
 from __future__ import annotations
 
@@ -101,10 +114,29 @@ CSRC = os.path.join(ROOT, "paper_2607_20908_amd", "csrc")
 KERNEL_SOURCES = {"decode": "decode_attn.hip", "lmhead": "token_logprob.hip"}
 
 
+def _local_sources(name: str, seen=None) -> list:
+    """The kernel source and every header of the package it includes, in a
+    fixed order."""
+    import re
+    seen = [] if seen is None else seen
+    if name in seen or not os.path.exists(os.path.join(CSRC, name)):
+        return seen
+    seen.append(name)
+    with open(os.path.join(CSRC, name)) as f:
+        for inc in re.findall(r'^#include "([^"]+)"', f.read(), re.M):
+            _local_sources(inc, seen)
+    return seen
+
+
 def source_sha256(op: str) -> str:
+    """sha256 of the op's kernel source followed by the package headers it
+    includes (so a change in a shared header also retires old counters)."""
     import hashlib
-    with open(os.path.join(CSRC, KERNEL_SOURCES[op]), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for name in _local_sources(KERNEL_SOURCES[op]):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(op: str, workload: str):
@@ -197,143 +229,210 @@ def cpu_baseline_decode(x, budget_s: float):
         total_bytes += (2 * 2 * c.head_dim * c.num_kv_heads * (lp + rows_s)
                         + 2 * 2 * G * c.num_q_heads * c.head_dim + 4 * G * c.num_q_heads)
         n += 1
-    return {"value": round(total_bytes / total_s / 1e9, 3), "unit": "GB/s", "cores": oracle.num_threads(),
+    # the oracle spreads a call over (candidate, query head) pairs
+    cores = min(oracle.num_threads(), G * c.num_q_heads)
+    return {"value": round(total_bytes / total_s / 1e9, 3), "unit": "GB/s", "cores": cores,
             "kind": "oracle", "seconds": round(total_s, 3),
             "sample": f"decode attention of {n} prompt groups ({n // c.num_prompts} full passes over the "
                       f"{c.num_prompts} prompts + {n % c.num_prompts}), {G} candidates each, fp64 CPU oracle, "
                       f"{total_bytes / 1e9:.2f} GB of algorithmic KV bytes"}
 
 
-def cpu_baseline_logprob(y, budget_s: float):
-    """The fp64 oracle on the host over the first rows of the workload, two rows
-    at a time, until the time budget is spent."""
+def subsample_rows(R: int, n: int, seed: int = 0) -> np.ndarray:
+    """n distinct rows of R, seeded, rows 0 and R - 1 included, ascending."""
+    if n >= R:
+        return np.arange(R)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    mid = rng.choice(np.arange(1, R - 1), size=n - 2, replace=False)
+    return np.sort(np.concatenate([[0, R - 1], mid]))
+
+
+def cpu_baseline_logprob(y, budget_s: float, fixed_rows: int = 0):
+    """The fp64 oracle on the host.  The oracle spreads a call over its rows,
+    so each call takes as many rows as it has threads.  With fixed_rows, a
+    seeded subsample of that many rows (rows 0 and R - 1 included) runs to the
+    end and the full pass's time is extrapolated from it; otherwise the first
+    rows run until the time budget is spent."""
     import oracle
     import workloads as W
     c = y.cfg
     w = W.bf16_bits(y.w_lm)
+    threads = oracle.num_threads()
+    rows = subsample_rows(c.rows, fixed_rows) if fixed_rows else np.arange(c.rows)
     total_s, n = 0.0, 0
-    rows_per = 2
-    while n < c.rows and total_s < budget_s:
-        idx = slice(n, min(c.rows, n + rows_per))
+    while n < len(rows) and (fixed_rows or total_s < budget_s):
+        idx = rows[n:n + threads]
+        h = W.bf16_bits(y.hidden[torch.from_numpy(idx).to(y.hidden.device)])
         t0 = time.perf_counter()
-        oracle.token_logprob(W.bf16_bits(y.hidden[idx]), w, y.target[idx].cpu().numpy(), y.inv_temperature)
+        oracle.token_logprob(h, w, y.target[torch.from_numpy(idx).to(y.target.device)].cpu().numpy(),
+                             y.inv_temperature)
         total_s += time.perf_counter() - t0
-        n = idx.stop
+        n += len(idx)
     flops = 2 * n * c.hidden * c.vocab
-    return {"value": round(flops / total_s / 1e12, 5), "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "seconds": round(total_s, 3),
-            "sample": f"token log-prob of the first {n} of {c.rows} rows (full vocabulary), fp64 CPU oracle"}
+    res = {"value": round(flops / total_s / 1e12, 5), "unit": "TFLOP/s", "cores": min(threads, n),
+           "kind": "oracle", "seconds": round(total_s, 3)}
+    if fixed_rows:
+        res["sample"] = (f"token log-prob of a seeded subsample of {n} of {c.rows} rows (rows 0 and "
+                         f"{c.rows - 1} included; full vocabulary), fp64 CPU oracle, {threads} rows per call")
+        res["rows_per_s"] = round(n / total_s, 3)
+        res["extrapolated_full_pass_s"] = round(c.rows * total_s / n, 1)
+    else:
+        res["sample"] = (f"token log-prob of the first {n} of {c.rows} rows (full vocabulary), fp64 CPU "
+                         f"oracle, {threads} rows per call")
+    return res
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="8b", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-budget", type=float, default=10.0,
-                    help="seconds of oracle time per operation for the CPU baseline (0 to skip)")
-    ap.add_argument("--kv-layout", default="head", choices=["head", "token"],
-                    help="KV cache layout: head-major [Hkv, rows, D] (default) or token-major [rows, Hkv, D]")
-    ap.add_argument("--no-update", action="store_true",
-                    help="skip the policy-update operations (log-prob backward, GRPO surrogate), which "
-                         "are timed after the step in a loop of their own")
-    ap.add_argument("--no-extend", action="store_true",
-                    help="skip the extend (prefill) of a refinement turn, timed after the step")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="run one 1 GiB device copy before the steps (outside the timed region) so a "
-                         "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: the library runs the hot path on a single MI355X "
-              "and has no multi-GPU path; run it without --gpus or with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
+class Timer:
+    """Times a list of operations on one stream with HIP events, medians over
+    `steps` repetitions after `warmup`, each operation behind an eviction
+    write (outside its events)."""
 
-    import paper_2607_20908_amd as rk
-    import workloads as W
+    def __init__(self, hip, stream, evict):
+        self.hip, self.sh, self.evict = hip, stream.cuda_stream, evict
 
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    dname, lname, desc = WORKLOADS[args.workload]
+    def run(self, ops, steps: int, warmup: int):
+        for _ in range(warmup):
+            for _, f in ops:
+                self.evict()
+                f()
+        torch.cuda.synchronize()
+        hip, sh = self.hip, self.sh
+        ev = [[(hip.create(), hip.create()) for _ in ops] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(steps):
+            for j, (name, f) in enumerate(ops):
+                self.evict()
+                hip.record(ev[k][j][0], sh)
+                f()
+                hip.record(ev[k][j][1], sh)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = {name: np.array([hip.elapsed_ms(*ev[k][j]) for k in range(steps)]) for j, (name, _) in enumerate(ops)}
+        for pair in (p for row in ev for p in row):
+            for e in pair:
+                hip.destroy(e)
+        # the host side of one call with the GPU idle: marshalling, planning
+        # and the launches (in the loop above the host runs ahead of the GPU)
+        host = {name: [] for name, _ in ops}
+        for _ in range(min(steps, 10)):
+            for name, f in ops:
+                torch.cuda.synchronize()
+                h0 = time.perf_counter()
+                f()
+                host[name].append(time.perf_counter() - h0)
+        torch.cuda.synchronize()
+        return {"ms": {n: float(np.median(v)) for n, v in ms.items()},
+                "p10_p90": {n: [round(float(np.percentile(v, 10)), 4), round(float(np.percentile(v, 90)), 4)]
+                            for n, v in ms.items()},
+                "host_us": {n: round(float(np.median(v)) * 1e6, 1) for n, v in host.items()},
+                "wall_s": wall}
+
+
+def decode_setup(rk, x, kv_layout, dev):
+    c = x.cfg
+    out = torch.empty((c.num_seqs, c.num_q_heads, c.head_dim), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((c.num_seqs, c.num_q_heads), dtype=torch.float32, device=dev)
+    rdim = 1 if kv_layout == "head" else 0
+    need = rk.decode_attn_workspace_size(c.num_prompts, c.group_size, c.num_q_heads, c.num_kv_heads,
+                                         c.head_dim, x.prefix_start, x.prefix_len, x.suffix_start,
+                                         x.suffix_len, x.k_prefix.shape[rdim], x.k_suffix.shape[rdim],
+                                         x.scale, kv_layout=kv_layout)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+
+    def run():
+        rk.decode_attn(x.q, x.k_prefix, x.v_prefix, x.k_suffix, x.v_suffix, x.prefix_start,
+                       x.prefix_len, x.suffix_start, x.suffix_len, c.group_size, scale=x.scale,
+                       out=out, lse=lse, workspace=ws, return_lse=True, kv_layout=kv_layout)
+    return run
+
+
+def logprob_setup(rk, y, dev):
+    cl = y.cfg
+    lp = torch.empty(cl.rows, dtype=torch.float32, device=dev)
+    lse = torch.empty(cl.rows, dtype=torch.float32, device=dev)
+    ws = torch.empty(rk.token_logprob_workspace_size(cl.rows, cl.hidden, cl.vocab), dtype=torch.uint8, device=dev)
+
+    def run():
+        rk.token_logprob(y.hidden, y.w_lm, y.target, y.inv_temperature, logprob=lp, lse=lse, workspace=ws)
+    return run, lse
+
+
+def decode_entry(x, ms, workload):
+    nbytes = decode_bytes(x)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": "decode attention (work-list fetch + split + combine kernels)", "bound": "hbm",
+            "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic("decode", workload), "algorithmic_bytes": nbytes}
+
+
+def lmhead_entry(cfg, ms, workload):
+    """The bound is the resource whose peak allows the longer time: MFMA at
+    the 8B-class and policy shapes, HBM (the weights) at 256 rows."""
+    fl = lmhead_flops(cfg)
+    nb = lmhead_bytes(cfg)
+    tf = fl / (ms * 1e-3) / 1e12
+    e = {"kernel": "lm-head log-prob (tile + combine kernels)"}
+    if nb / (HBM_PEAK_GBS * 1e9) > fl / (MFMA_BF16_PEAK_TFLOPS * 1e12):
+        gbs = nb / (ms * 1e-3) / 1e9
+        e.update({"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic("lmhead", workload),
+                  "algorithmic_bytes": nb, "tflops": round(tf, 1),
+                  "mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)})
+    else:
+        e.update({"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                  "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic("lmhead", workload),
+                  "algorithmic_flops": fl})
+    return e
+
+
+def measure_workload(rk, W, name, args, timer, dev, steps, warmup, cpu_budget, keep=False):
+    """Times one workload's operations and builds its report; with keep, also
+    returns its inputs for the extra operations."""
+    dname, lname, desc = WORKLOADS[name]
     x = W.make_decode_inputs(W.DECODE_CONFIGS[dname], dev, kv_layout=args.kv_layout) if dname else None
     y = W.make_logprob_inputs(W.LOGPROB_CONFIGS[lname], dev) if lname else None
-
-    ops = []
+    ops, lse_l = [], None
     if x is not None:
-        c = x.cfg
-        out = torch.empty((c.num_seqs, c.num_q_heads, c.head_dim), dtype=torch.bfloat16, device=dev)
-        lse = torch.empty((c.num_seqs, c.num_q_heads), dtype=torch.float32, device=dev)
-        rdim = 1 if args.kv_layout == "head" else 0
-        need = rk.decode_attn_workspace_size(c.num_prompts, c.group_size, c.num_q_heads, c.num_kv_heads,
-                                             c.head_dim, x.prefix_start, x.prefix_len, x.suffix_start,
-                                             x.suffix_len, x.k_prefix.shape[rdim], x.k_suffix.shape[rdim],
-                                             x.scale, kv_layout=args.kv_layout)
-        ws_d = torch.empty(need, dtype=torch.uint8, device=dev)
-
-        def run_decode():
-            rk.decode_attn(x.q, x.k_prefix, x.v_prefix, x.k_suffix, x.v_suffix, x.prefix_start,
-                           x.prefix_len, x.suffix_start, x.suffix_len, c.group_size, scale=x.scale,
-                           out=out, lse=lse, workspace=ws_d, return_lse=True, kv_layout=args.kv_layout)
-        ops.append(("decode", run_decode))
+        ops.append(("decode", decode_setup(rk, x, args.kv_layout, dev)))
     if y is not None:
-        cl = y.cfg
-        lp = torch.empty(cl.rows, dtype=torch.float32, device=dev)
-        lse2 = torch.empty(cl.rows, dtype=torch.float32, device=dev)
-        ws_l = torch.empty(rk.token_logprob_workspace_size(cl.rows, cl.hidden, cl.vocab),
-                           dtype=torch.uint8, device=dev)
+        run_l, lse_l = logprob_setup(rk, y, dev)
+        ops.append(("lmhead", run_l))
+    log(f"bench: workload {name}: warmup {warmup}, timing {steps} steps")
+    t = timer.run(ops, steps, warmup)
+    log(f"bench: {name}: per op {t['ms']} ms, host {t['host_us']} us")
+    rep = {"workload": desc, "steps": steps, "ms_per_step": round(t["wall_s"] * 1e3 / steps, 4),
+           "ops": {}}
+    entries = []
+    if x is not None:
+        e = decode_entry(x, t["ms"]["decode"], name)
+        rep["ops"]["decode"] = {"ms": round(t["ms"]["decode"], 4), "ms_p10_p90": t["p10_p90"]["decode"],
+                                "host_us": t["host_us"]["decode"], "roofline": e}
+        entries.append((t["ms"]["decode"], e))
+    if y is not None:
+        e = lmhead_entry(y.cfg, t["ms"]["lmhead"], name)
+        rep["ops"]["lmhead"] = {"ms": round(t["ms"]["lmhead"], 4), "ms_p10_p90": t["p10_p90"]["lmhead"],
+                                "host_us": t["host_us"]["lmhead"], "roofline": e}
+        entries.append((t["ms"]["lmhead"], e))
+    entries.sort(key=lambda p: -p[0])
+    rep["roofline"] = entries[0][1]
+    if cpu_budget > 0:
+        log(f"bench: {name}: cpu baseline (fp64 oracle)")
+        if x is not None:
+            rep["ops"]["decode"]["cpu_baseline"] = cpu_baseline_decode(x, cpu_budget)
+        if y is not None:
+            fixed = 1024 if y.cfg.rows > 65536 else 0
+            rep["ops"]["lmhead"]["cpu_baseline"] = cpu_baseline_logprob(y, cpu_budget, fixed_rows=fixed)
+        rep["cpu_baseline"] = rep["ops"]["decode" if x is not None else "lmhead"]["cpu_baseline"]
+    if keep:
+        return rep, t, (x, y, ops, lse_l)
+    del x, y, ops
+    torch.cuda.empty_cache()
+    return rep, t, None
 
-        def run_logprob():
-            rk.token_logprob(y.hidden, y.w_lm, y.target, y.inv_temperature, logprob=lp, lse=lse2,
-                             workspace=ws_l)
-        ops.append(("lmhead", run_logprob))
 
-    stream = torch.cuda.current_stream()
-    if args.copy_calibration:
-        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)      # 1 GiB
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-    log(f"bench: workload {args.workload}: warmup {args.warmup}")
-    for _ in range(args.warmup):
-        for _, f in ops:
-            f()
-    torch.cuda.synchronize()
-    runtimes = rk.hip_runtimes_mapped()
-    if len(runtimes) != 1:
-        raise RuntimeError(f"expected one HIP runtime in the process, found {runtimes}")
-    hip = HipEvents(runtimes[0])
-    sh = stream.cuda_stream
-    ev = [[(hip.create(), hip.create()) for _ in ops] for _ in range(args.steps)]
-    log(f"bench: timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        for j, (_, f) in enumerate(ops):
-            hip.record(ev[k][j][0], sh)
-            f()
-            hip.record(ev[k][j][1], sh)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    # per-operation duration: the median over the timed steps (p10 and p90
-    # reported beside it).  The first step's interval also holds the host's
-    # planning of that call, since the GPU has drained before the timed region.
-    op_all = {name: np.array([hip.elapsed_ms(*ev[k][j]) for k in range(args.steps)])
-              for j, (name, _) in enumerate(ops)}
-    op_ms = {name: float(np.median(v)) for name, v in op_all.items()}
-    op_pct = {name: [round(float(np.percentile(v, 10)), 4), round(float(np.percentile(v, 90)), 4)]
-              for name, v in op_all.items()}
-    for pair in (p for row in ev for p in row):
-        for e in pair:
-            hip.destroy(e)
-    ms_per_step = wall * 1e3 / args.steps
-    log(f"bench: {ms_per_step:.3f} ms/step; per op {op_ms}")
-
-    # ---- policy-update operations, timed on their own after the step: the
-    # backward of the lm-head log-prob for the same rows (incoming gradient
-    # seeded N(0, 1), lse from the forward above) and the GRPO surrogate over
-    # the policy pass's 262144 rows
+def extra_ops(rk, W, args, x, y, lse2, ops, hip, sh, dev):
+    """The operations timed after the headline's steps at its shape."""
     update = None
     if x is not None and not args.no_update:
         # the decode loop's cache update: one new token per candidate appended
@@ -471,16 +570,16 @@ def main():
         nb_g = grpo_bytes(gx)
         update = dict(update or {})
         update.update({"steps": usteps,
-                  "lmhead_backward": {"kernel": "log-prob backward (probability tile + vocab GEMM + finish "
-                                                "kernels, per 16384-row chunk)",
-                                      "ms": round(u_ms["backward"], 4), "bound": "mfma",
-                                      "achieved": round(tf_b, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                                      "unit": "TFLOP/s", "frac": round(tf_b / MFMA_BF16_PEAK_TFLOPS, 4),
-                                      "algorithmic_flops": fl_b},
-                  "grpo": {"kernel": "GRPO advantages + clipped surrogate, 4 x G=16 sequences x 4096 rows",
-                           "us": round(u_ms["grpo"] * 1e3, 2), "bound": "hbm",
-                           "achieved": round(nb_g / (u_ms["grpo"] * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
-                           "unit": "GB/s", "algorithmic_bytes": nb_g}})
+                       "lmhead_backward": {"kernel": "log-prob backward (probability tile + vocab GEMM + finish "
+                                                     "kernels, per 16384-row chunk)",
+                                           "ms": round(u_ms["backward"], 4), "bound": "mfma",
+                                           "achieved": round(tf_b, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                                           "unit": "TFLOP/s", "frac": round(tf_b / MFMA_BF16_PEAK_TFLOPS, 4),
+                                           "algorithmic_flops": fl_b},
+                       "grpo": {"kernel": "GRPO advantages + clipped surrogate, 4 x G=16 sequences x 4096 rows",
+                                "us": round(u_ms["grpo"] * 1e3, 2), "bound": "hbm",
+                                "achieved": round(nb_g / (u_ms["grpo"] * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                                "unit": "GB/s", "algorithmic_bytes": nb_g}})
         if sx is not None:
             fl_s = lmhead_flops(cl)
             tf_s = fl_s / (u_ms["sample"] * 1e-3) / 1e12
@@ -489,65 +588,116 @@ def main():
                           "top-p 0.9", "ms": round(u_ms["sample"], 4), "bound": "mfma",
                 "achieved": round(tf_s, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tf_s / MFMA_BF16_PEAK_TFLOPS, 4), "algorithmic_flops": fl_s}
+    return update
 
-    res = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-           "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="32b", choices=sorted(WORKLOADS),
+                    help="the headline workload (value, roofline, extra operations)")
+    ap.add_argument("--also", default="8b,longctx,policy",
+                    help="comma-separated workloads measured after the headline, reported under configs "
+                         "('' for none)")
+    ap.add_argument("--cpu-budget", type=float, default=10.0,
+                    help="seconds of oracle time per headline operation for the CPU baseline (0 to skip); "
+                         "the other workloads get half")
+    ap.add_argument("--kv-layout", default="head", choices=["head", "token"],
+                    help="KV cache layout: head-major [Hkv, rows, D] (default) or token-major [rows, Hkv, D]")
+    ap.add_argument("--evict-mb", type=int, default=1024,
+                    help="MiB read before every timed operation, outside its events (0: none)")
+    ap.add_argument("--no-update", action="store_true",
+                    help="skip the policy-update operations (log-prob backward, GRPO surrogate, sampling head), "
+                         "which are timed after the step in a loop of their own")
+    ap.add_argument("--no-extend", action="store_true",
+                    help="skip the extend (prefill) of a refinement turn, timed after the step")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 1 GiB device copy before the steps (outside the timed region) so a "
+                         "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the library runs the hot path on a single MI355X "
+              "and has no multi-GPU path; run it without --gpus or with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    also = [w for w in args.also.split(",") if w and w != args.workload]
+    for w in also:
+        if w not in WORKLOADS:
+            sys.exit(f"unknown workload {w}")
+
+    import paper_2607_20908_amd as rk
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    evict_buf = torch.zeros((max(1, args.evict_mb) << 20) // 4, dtype=torch.float32, device=dev) \
+        if args.evict_mb else None
+
+    def evict():
+        if evict_buf is not None:
+            torch.amax(evict_buf)             # a read of the whole buffer; the result is not used
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)      # 1 GiB
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    runtimes = rk.hip_runtimes_mapped()
+    if len(runtimes) != 1:
+        raise RuntimeError(f"expected one HIP runtime in the process, found {runtimes}")
+    hip = HipEvents(runtimes[0])
+    timer = Timer(hip, stream, evict)
+
+    head, t, (x, y, ops, lse2) = measure_workload(rk, W, args.workload, args, timer, dev, args.steps, args.warmup,
+                                                  args.cpu_budget, keep=True)
+    update = extra_ops(rk, W, args, x, y, lse2, ops, hip, stream.cuda_stream, dev)
+    del x, y, ops, lse2
+    torch.cuda.empty_cache()
+    configs = {args.workload: head}
+    for w in also:
+        steps = min(args.steps, 5) if w == "policy" else args.steps
+        rep, _, _ = measure_workload(rk, W, w, args, timer, dev, steps, min(args.warmup, 2) if w == "policy"
+                                     else args.warmup, args.cpu_budget / 2)
+        configs[w] = rep
+
+    hops = head["ops"]
+    both = "decode" in hops and "lmhead" in hops
+    res = {"metric": "decode-attn effective KV GB/s (% HBM peak); lm-head logprob TFLOP/s (% MFMA)" if both else
+           ("decode-attn effective KV GB/s (% HBM peak)" if "decode" in hops else "lm-head logprob TFLOP/s (% MFMA)"),
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, HBM-resident)",
-           "config": {"workload": desc, "kv_layout": args.kv_layout if x is not None else None}}
-    rooflines = []
-    if x is not None:
-        nbytes = decode_bytes(x)
-        gbs = nbytes / (op_ms["decode"] * 1e-3) / 1e9
-        res.update({"metric": "decode-attn effective KV GB/s (% HBM peak)", "value": round(gbs, 1),
-                    "unit": "GB/s", "decode_ms": round(op_ms["decode"], 4),
-                    "decode_ms_p10_p90": op_pct["decode"],
-                    "decode_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
-                    "decode_algorithmic_bytes": nbytes})
-        rooflines.append((op_ms["decode"], {"kernel": "decode attention (split + combine kernels)",
-                                            "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
-                                            "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                            "traffic": measured_traffic("decode", args.workload),
-                                            "algorithmic_bytes": nbytes}))
-    if y is not None:
-        fl = lmhead_flops(y.cfg)
-        tf = fl / (op_ms["lmhead"] * 1e-3) / 1e12
-        res.update({"lmhead_ms": round(op_ms["lmhead"], 4), "lmhead_ms_p10_p90": op_pct["lmhead"],
-                    "lmhead_tflops": round(tf, 1),
-                    "lmhead_mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "lmhead_flops": fl})
-        if x is None:
-            res.update({"metric": "lm-head logprob TFLOP/s (% MFMA)", "value": round(tf, 1),
-                        "unit": "TFLOP/s"})
-        # the bound is the resource whose peak allows the longer time: MFMA
-        # at the 8B-class and policy shapes, HBM (the weights) at 256 rows
-        nb = lmhead_bytes(y.cfg)
-        if nb / (HBM_PEAK_GBS * 1e9) > fl / (MFMA_BF16_PEAK_TFLOPS * 1e12):
-            gbs_l = nb / (op_ms["lmhead"] * 1e-3) / 1e9
-            entry = {"kernel": "lm-head log-prob (tile + combine kernels)", "bound": "hbm",
-                     "achieved": round(gbs_l, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gbs_l / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("lmhead", args.workload), "algorithmic_bytes": nb}
-        else:
-            entry = {"kernel": "lm-head log-prob (tile + combine kernels)", "bound": "mfma",
-                     "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic("lmhead", args.workload), "algorithmic_flops": fl}
-        rooflines.append((op_ms["lmhead"], entry))
-    res["metric"] = "decode-attn effective KV GB/s (% HBM peak); lm-head logprob TFLOP/s (% MFMA)" \
-        if (x is not None and y is not None) else res["metric"]
-    rooflines.sort(key=lambda t: -t[0])
-    res["roofline"] = rooflines[0][1]            # the operation that takes the most time
-    if len(rooflines) > 1:
-        res["roofline_other"] = rooflines[1][1]
+           "config": {"workload": head["workload"], "kv_layout": args.kv_layout if "decode" in hops else None,
+                      "evict_mib_between_ops": args.evict_mb}}
+    if "decode" in hops:
+        d = hops["decode"]
+        res.update({"value": d["roofline"]["achieved"], "unit": "GB/s", "decode_ms": d["ms"],
+                    "decode_ms_p10_p90": d["ms_p10_p90"], "decode_host_us": d["host_us"],
+                    "decode_hbm_frac": d["roofline"]["frac"],
+                    "decode_algorithmic_bytes": d["roofline"]["algorithmic_bytes"]})
+    if "lmhead" in hops:
+        l = hops["lmhead"]
+        fl = lmhead_flops(W.LOGPROB_CONFIGS[WORKLOADS[args.workload][1]])
+        tf = fl / (l["ms"] * 1e-3) / 1e12
+        res.update({"lmhead_ms": l["ms"], "lmhead_ms_p10_p90": l["ms_p10_p90"], "lmhead_host_us": l["host_us"],
+                    "lmhead_tflops": round(tf, 1), "lmhead_mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                    "lmhead_flops": fl})
+        if "decode" not in hops:
+            res.update({"value": round(tf, 1), "unit": "TFLOP/s"})
+    res["roofline"] = head["roofline"]
+    other = [o["roofline"] for n, o in hops.items() if o["roofline"] is not head["roofline"]]
+    if other:
+        res["roofline_other"] = other[0]
+    if "cpu_baseline" in head:
+        res["cpu_baseline"] = head["cpu_baseline"]
+        if both:
+            res["cpu_baseline_lmhead"] = hops["lmhead"]["cpu_baseline"]
     if update is not None:
         res["extra_ops"] = update
-    if args.cpu_budget > 0:
-        log("bench: cpu baseline (fp64 oracle)")
-        if x is not None:
-            res["cpu_baseline"] = cpu_baseline_decode(x, args.cpu_budget)
-            if y is not None:
-                res["cpu_baseline_lmhead"] = cpu_baseline_logprob(y, args.cpu_budget)
-        else:
-            res["cpu_baseline"] = cpu_baseline_logprob(y, args.cpu_budget)
+    res["configs"] = configs
     order = ["metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
              "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"]
     line = {k: res[k] for k in order if k in res}

@@ -50,12 +50,17 @@
  * current HIP device; "host" pointers are read only during the call.
  *
  * Ownership: the caller owns every buffer, including the workspace.  The
- * library allocates no device memory.  Across calls it keeps only per-thread
- * state: the last error string, a reusable planning buffer and a ring of 4
- * pinned, device-mapped host buffers (grown on demand, never freed) that a
- * small kernel on the caller's stream copies the work list from, so the host
- * does not wait for the stream.  Calls on different streams need distinct
- * workspaces.
+ * library allocates no device memory (rl_token_logprob_noalloc's static
+ * array aside).  Across calls it keeps only per-thread state: the last error
+ * string, a reusable planning buffer and up to 64 pinned, device-mapped host
+ * buffers that a small kernel on the caller's stream copies a work list from
+ * (rl_decode_attn, rl_extend_attn and rl_kv_append upload one per call).
+ * Buffers are added and enlarged on demand and never freed: an outgrown
+ * buffer is kept and one at least twice its size taken.  Such a call does not
+ * wait for the stream unless 64 earlier ones on the same thread still wait
+ * for the kernel that reads their buffer to run; it then waits for the oldest
+ * of them, for at most 60 s, and returns RL_ERR_HIP if it has not run by
+ * then.  Calls on different streams need distinct workspaces.
  *
  * Errors: rl_last_error() describes the problem of a failing call.  Argument
  * errors are detected on the host before any launch: a call that returns
@@ -487,7 +492,9 @@ typedef struct {
     int32_t row_begin;   /* first query row served, of the unit's G*Hq/Hkv (prefix) or
                             Hq/Hkv (suffix) rows at this kv head                         */
     int32_t row_count;   /* query rows served: at most 64                                */
-    int32_t reserved;
+    int32_t split_variant; /* split kernel the call launches, the same in every item: 0 = one
+                              KV tile in flight per workgroup, 1 = two (chosen when items of
+                              more than 48 query rows hold most of the KV tokens)          */
 } rl_plan_item;
 
 rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_lens *lens,

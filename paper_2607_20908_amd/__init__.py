@@ -81,7 +81,7 @@ class PlanItem(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("unit", ctypes.c_int32), ("kv_head", ctypes.c_int32),
                 ("chunk", ctypes.c_int32), ("tok_begin", ctypes.c_int64),
                 ("tok_count", ctypes.c_int32), ("row_begin", ctypes.c_int32),
-                ("row_count", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("row_count", ctypes.c_int32), ("split_variant", ctypes.c_int32)]
 
 
 class BoundsReport(ctypes.Structure):
@@ -245,7 +245,7 @@ def decode_plan(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix
                                      ctypes.byref(n)), "rl_decode_plan_debug")
     dt = np.dtype([("kind", np.int32), ("unit", np.int32), ("kv_head", np.int32),
                    ("chunk", np.int32), ("tok_begin", np.int64), ("tok_count", np.int32),
-                   ("row_begin", np.int32), ("row_count", np.int32), ("reserved", np.int32)])
+                   ("row_begin", np.int32), ("row_count", np.int32), ("split_variant", np.int32)])
     return np.frombuffer(bytes(buf), dtype=dt, count=n.value).copy()
 
 

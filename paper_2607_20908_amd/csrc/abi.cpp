@@ -47,9 +47,13 @@ namespace {
 // has run: the operation's last kernel stores the slot's sequence number into
 // a pinned word (no marker packet on the stream, which would hold the next
 // kernel back by a few microseconds), or, if that kernel did not launch, an
-// event recorded behind the fetch says so.  The slots are never freed (plain
-// thread-local pointers, no destructors to run after the HIP runtime has shut
-// down).
+// event recorded behind the fetch says so.  A call takes any slot whose
+// reader has run; if there is none it adds a slot, up to kStagingSlots per
+// thread, and only then waits for the oldest.  Nothing is ever freed: a slot
+// that needs more room keeps its old buffer and takes one at least twice as
+// large (so a slot's retired buffers total less than its current one), and
+// the slots are plain thread-local storage with no destructors to run after
+// the HIP runtime has shut down.  (hipHostFree could wait for the device.)
 struct StagingSlot {
     unsigned char *host;
     void *dev;                 // the same memory as the device sees it
@@ -61,10 +65,24 @@ struct StagingSlot {
     uint64_t *flag;            // pinned word, stored into by the device
     uint64_t *flag_dev;
     uint64_t expect;
+    uint64_t last_use;         // call number of the slot's last upload
 };
-constexpr int kStagingSlots = 4;
+constexpr int kStagingSlots = 64;
 thread_local StagingSlot g_staging[kStagingSlots];
-thread_local int g_staging_next;
+thread_local int g_staging_count;      // slots created so far on this thread
+thread_local uint64_t g_staging_calls;
+
+// True once the slot's reader has run (no waiting).
+bool slot_released(StagingSlot &slot) {
+    if (!slot.pending) return true;
+    const bool done = slot.by_flag ? __atomic_load_n(slot.flag, __ATOMIC_ACQUIRE) >= slot.expect
+                                   : hipEventQuery(slot.done) == hipSuccess;
+    if (done) slot.pending = false;
+    return done;
+}
+
+// Waits until the slot's reader has run (60 s limit).
+rl_status wait_slot(StagingSlot &slot);
 
 // One plan object per thread, reused so that planning does not allocate once
 // its vectors have grown to the problem size.
@@ -86,28 +104,56 @@ thread_local StagingSlot *g_staged_slot;     // the slot of the last upload, unt
 // stage_commit, which records the slot's reuse event behind them: an event
 // recorded between the fetch and the next kernel would hold that kernel back
 // by the few microseconds the command processor takes for the marker.
+rl_status wait_slot(StagingSlot &slot) {
+    if (!slot.pending) return RL_OK;
+    if (slot.by_flag) {
+        const auto t0 = std::chrono::steady_clock::now();
+        for (uint32_t i = 1; __atomic_load_n(slot.flag, __ATOMIC_ACQUIRE) < slot.expect; ++i) {
+            if (i < 256) continue;
+            std::this_thread::yield();
+            if ((i & 4095) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60))
+                return set_error(RL_ERR_HIP, "waiting for a staging slot: the kernel that reads it has "
+                                             "not run for 60 s");
+        }
+    } else {
+        const hipError_t e = hipEventSynchronize(slot.done);
+        if (e != hipSuccess) return hip_error(e, "waiting for a staging slot");
+    }
+    slot.pending = false;
+    return RL_OK;
+}
+
+// A slot whose reader has run: a free existing one, else a new one while
+// fewer than kStagingSlots exist, else the least recently used, waited for.
+rl_status next_slot(StagingSlot **out) {
+    StagingSlot *lru = nullptr;
+    for (int i = 0; i < g_staging_count; ++i) {
+        StagingSlot &s = g_staging[i];
+        if (slot_released(s)) {
+            *out = &s;
+            return RL_OK;
+        }
+        if (!lru || s.last_use < lru->last_use) lru = &s;
+    }
+    if (g_staging_count < kStagingSlots) {
+        *out = &g_staging[g_staging_count++];
+        return RL_OK;
+    }
+    const rl_status st = wait_slot(*lru);
+    if (st != RL_OK) return st;
+    *out = lru;
+    return RL_OK;
+}
+
 rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, hipStream_t stream) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_error(e, "hipGetDevice");
-    StagingSlot &slot = g_staging[g_staging_next];
-    g_staging_next = (g_staging_next + 1) % kStagingSlots;
-    if (slot.pending) {
-        if (slot.by_flag) {
-            const auto t0 = std::chrono::steady_clock::now();
-            for (uint32_t i = 1; __atomic_load_n(slot.flag, __ATOMIC_ACQUIRE) < slot.expect; ++i) {
-                if (i < 256) continue;
-                std::this_thread::yield();
-                if ((i & 4095) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60))
-                    return set_error(RL_ERR_HIP, "waiting for a staging slot: the kernel that reads it has "
-                                                 "not run for 60 s");
-            }
-        } else {
-            e = hipEventSynchronize(slot.done);
-            if (e != hipSuccess) return hip_error(e, "waiting for a staging slot");
-        }
-        slot.pending = false;
-    }
+    StagingSlot *sp = nullptr;
+    const rl_status st = next_slot(&sp);
+    if (st != RL_OK) return st;
+    StagingSlot &slot = *sp;
+    slot.last_use = ++g_staging_calls;
     if (slot.done && slot.device != device) {
         (void)hipEventDestroy(slot.done);
         slot.done = nullptr;
@@ -127,10 +173,10 @@ rl_status stage_sections(const Section *sec, int nsec, size_t total, void *dst, 
         slot.device = device;
     }
     if (slot.cap < total) {
-        if (slot.host) (void)hipHostFree(slot.host);
+        // the old buffer is retired, not freed (see above)
         slot.host = nullptr;
+        const size_t cap = std::max<size_t>(std::max<size_t>(total, 2 * slot.cap), 1 << 16);
         slot.cap = 0;
-        const size_t cap = std::max<size_t>(total * 2, 1 << 16);
         e = hipHostMalloc(reinterpret_cast<void **>(&slot.host), cap,
                           hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) return hip_error(e, "allocating pinned staging memory");

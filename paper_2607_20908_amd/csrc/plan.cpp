@@ -270,6 +270,7 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
                 it.tok_count = static_cast<int32_t>(d.meta & 0x7fff);
                 it.row_begin = static_cast<int32_t>((d.meta >> 24) * kMaxItemRows);
                 it.row_count = static_cast<int32_t>(std::min<int64_t>(kMaxItemRows, M - it.row_begin));
+                it.split_variant = pl.deep_prefetch;
             }
         }
     }

@@ -81,3 +81,20 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=300, cwd=ROOT)
     assert r.returncode != 0
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_cpu_baseline_subsample_rows():
+    r = bench.subsample_rows(262144, 1024, seed=0)
+    assert len(r) == 1024 and len(np.unique(r)) == 1024
+    assert r[0] == 0 and r[-1] == 262143 and np.all(np.diff(r) > 0)
+    assert np.array_equal(r, bench.subsample_rows(262144, 1024, seed=0))
+    # at least 64 distinct 256-row tiles, the last one included
+    assert len(np.unique(r // 256)) >= 64 and (262143 // 256) in set(r // 256)
+    assert np.array_equal(bench.subsample_rows(10, 50), np.arange(10))
+
+
+def test_source_hash_covers_included_headers():
+    names = bench._local_sources("token_logprob.hip")
+    assert names[0] == "token_logprob.hip"
+    assert {"lds_stage.h", "tile_index.h", "kernels.h"} <= set(names)
+    assert "decode_attn.hip" in bench._local_sources("decode_attn.hip")

@@ -82,7 +82,27 @@ def test_wide_items_two_tiles_in_flight(D, split, layout):
     lp = [700, 0, 193]
     ls = ([5, 0, 17, 64, 1, 65, 0, 30] + [3, 9, 0, 2, 40, 1, 0, 12] + [63, 0, 1, 2, 3, 4, 5, 6])
     c = decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=D * 7 + split, gap=2)
+    assert set(plan_of(c, Hq, Hkv, D, split)["split_variant"]) == {1}, "two tiles in flight expected"
     check(c, 1.0 / math.sqrt(D), split, f"wide items D={D}", layout)
+
+
+def plan_of(c, Hq, Hkv, D, split=0):
+    P = len(c["prefix_len"])
+    return rk.decode_plan(P, c["group_size"], Hq, Hkv, D, c["prefix_start"], c["prefix_len"], c["suffix_start"],
+                          c["suffix_len"], c["k_prefix"].shape[0], c["k_suffix"].shape[0], split_tokens=split)
+
+
+@pytest.mark.parametrize("layout", ["token", "head"])
+@pytest.mark.parametrize("D", [64, 128])
+def test_one_query_head_per_kv_head(D, layout):
+    """Hq = Hkv (r = 1): plain multi-head attention, each candidate's suffix
+    item serving one query row per kv head; the prefix items serve G rows."""
+    P, G, Hq, Hkv = 3, 5, 8, 8
+    lp = [257, 0, 64]
+    ls = [1, 0, 130, 64, 17] + [0, 5, 300, 2, 63] + [65, 1, 0, 128, 40]
+    c = decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=11 * D, gap=3)
+    check(c, 1.0 / math.sqrt(D), 0, f"r=1 D={D}", layout)
+    check(c, 1.0 / math.sqrt(D), 32, f"r=1 D={D}", layout)
 
 
 @pytest.mark.parametrize("G,Hq,Hkv", [(16, 64, 8),   # 128 query rows per kv head: two 64-row items per chunk
@@ -136,6 +156,55 @@ def test_nan_poisoned_padding_and_workspace():
         o, l, _ = run_gpu(c, scale, 0, workspace=ws, layout=layout)
         assert np.isfinite(o).all() and np.isfinite(l).all()
         assert max_abs(o, ro) <= ATTN_OUT_TOL and max_abs(l, rl) <= ATTN_LSE_TOL
+
+
+def test_nan_poisoned_two_tiles_in_flight():
+    """The two-tiles-in-flight variant (items of G * r = 64 query rows hold
+    most of the KV) against NaN gap rows and a NaN workspace: the empty loads
+    past a chunk's last tile and the final merge must touch neither."""
+    P, G, Hq, Hkv, D = 2, 8, 16, 2, 128
+    lp, ls = [450, 129], [3, 0, 64, 1, 17, 2, 0, 65, 5, 1, 0, 33, 2, 64, 1, 0]
+    c = decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=21, gap=4, poison=True)
+    scale = 1.0 / math.sqrt(D)
+    assert set(plan_of(c, Hq, Hkv, D)["split_variant"]) == {1}
+    need = rk.decode_attn_workspace_size(P, G, Hq, Hkv, D, c["prefix_start"], c["prefix_len"], c["suffix_start"],
+                                         c["suffix_len"], c["k_prefix"].shape[0], c["k_suffix"].shape[0], scale)
+    ws = torch.full((need // 4 + 1,), float("nan"), dtype=torch.float32, device=dev()).view(torch.uint8)
+    ro, rl = run_oracle(c, scale)
+    for layout in ("token", "head"):
+        say(f"decode poisoned padding + workspace, two tiles in flight, layout {layout}")
+        ws.view(torch.float32).fill_(float("nan"))
+        o, l, _ = run_gpu(c, scale, 0, workspace=ws, layout=layout)
+        assert np.isfinite(o).all() and np.isfinite(l).all()
+        assert max_abs(o, ro) <= ATTN_OUT_TOL and max_abs(l, rl) <= ATTN_LSE_TOL
+
+
+def test_many_calls_in_flight():
+    """100 calls enqueued without a synchronisation, four problems in turn:
+    more calls than the 64 pinned staging buffers, so buffers are reused (or
+    waited for) while earlier calls are still queued.  Every output must match
+    the oracle; a work list overwritten before its fetch ran would not."""
+    D = 128
+    cases = [decode_host_case(2, 4, 8, 2, D, [100 + 37 * i, 64], [(i * 13 + 7 * j) % 90 for j in range(8)],
+                              seed=40 + i, gap=1) for i in range(4)]
+    scale = 1.0 / math.sqrt(D)
+    refs = [run_oracle(c, scale) for c in cases]
+    dev_in = []
+    for c in cases:
+        t = {k: to_dev(c[k]) for k in ("q", "k_prefix", "v_prefix", "k_suffix", "v_suffix")}
+        dev_in.append(t)
+    say("decode: 100 calls in flight")
+    outs = []
+    for n in range(100):
+        c, t = cases[n % 4], dev_in[n % 4]
+        outs.append(rk.decode_attn(t["q"], t["k_prefix"], t["v_prefix"], t["k_suffix"], t["v_suffix"],
+                                   c["prefix_start"], c["prefix_len"], c["suffix_start"], c["suffix_len"],
+                                   c["group_size"], scale=scale, return_lse=True))
+    torch.cuda.synchronize()
+    for n, (o, l) in enumerate(outs):
+        ro, rl = refs[n % 4]
+        assert max_abs(o.float().cpu().numpy(), ro) <= ATTN_OUT_TOL, f"call {n}"
+        assert max_abs(l.cpu().numpy(), rl) <= ATTN_LSE_TOL, f"call {n}"
 
 
 def test_bitwise_deterministic():

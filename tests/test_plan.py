@@ -122,3 +122,21 @@ def test_cover_fuzz(P, G, Hkv, r, split, data):
     ls = data.draw(st.lists(st.integers(0, 300), min_size=S, max_size=S))
     items, lp, ls = plan_for(P, G, Hkv * r, Hkv, 64, lp, ls, split=split)
     check_cover(items, P, G, Hkv * r, Hkv, lp, ls, split=split or None)
+
+
+def test_split_variant_follows_item_widths():
+    # prompts shared by G * r = 64 query rows dominating the KV: two tiles in flight
+    P, G, Hq, Hkv = 3, 8, 16, 2
+    lp = np.array([700, 0, 193], np.int32)
+    ls = np.array([5, 0, 17, 64, 1, 65, 0, 30] + [3, 9, 0, 2, 40, 1, 0, 12] + [63, 0, 1, 2, 3, 4, 5, 6], np.int32)
+    ps = np.array([0, 700, 700], np.int64)
+    ss = np.concatenate([[0], np.cumsum(ls)[:-1]]).astype(np.int64)
+    it = rk.decode_plan(P, G, Hq, Hkv, 128, ps, lp, ss, ls, 1000, int(ls.sum()))
+    assert set(it["split_variant"]) == {1}
+    # the 8B-class step: 4-row suffix items hold most of the KV
+    cfg = W.DECODE_CONFIGS["8b"]
+    sl = W.suffix_lengths(cfg, seed=0).astype(np.int32)
+    ss = np.concatenate([[0], np.cumsum(sl)[:-1]]).astype(np.int64)
+    it = rk.decode_plan(64, 8, 32, 8, 128, np.arange(64, dtype=np.int64) * 1024, np.full(64, 1024, np.int32),
+                        ss, sl, 65536, int(sl.sum()))
+    assert set(it["split_variant"]) == {0}
