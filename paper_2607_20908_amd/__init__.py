@@ -18,6 +18,7 @@ built, importing this package raises.
 from __future__ import annotations
 
 import ctypes
+import functools
 import math
 import os
 from typing import Optional
@@ -184,6 +185,21 @@ def _stream_handle(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
+def _on_call_stream(fn):
+    """Runs a wrapper whose caller passed stream= with that stream current, so
+    the workspace and outputs it allocates belong to that stream in torch's
+    caching allocator: once dropped, they are reused only by later work on the
+    same stream, never while the library's kernels there may still use them."""
+    @functools.wraps(fn)
+    def call(*args, stream=None, **kw):
+        if stream is None:
+            return fn(*args, stream=None, **kw)
+        s = stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.ExternalStream(_stream_handle(stream))
+        with torch.cuda.stream(s):
+            return fn(*args, stream=stream, **kw)
+    return call
+
+
 def _on_device(t: torch.Tensor, name: str) -> torch.Tensor:
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor (the kernels read it on the GPU)")
@@ -272,6 +288,7 @@ class _AppendArgs:
                                  self.ns.ctypes.data, self.nl.ctypes.data, int(suffix_rows), int(new_rows))
 
 
+@_on_call_stream
 def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_suffix: torch.Tensor, v_suffix: torch.Tensor,
               suffix_start, suffix_len, new_start, new_len, group_size: int, suffix_capacity=None,
               kv_layout: str = "token", workspace: Optional[torch.Tensor] = None, stream=None):
@@ -305,6 +322,7 @@ def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_suffix: torch.Tensor, 
                              workspace.numel(), _stream_handle(stream)), "rl_kv_append")
 
 
+@_on_call_stream
 def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
                 k_suffix: torch.Tensor, v_suffix: torch.Tensor,
                 prefix_start, prefix_len, suffix_start, suffix_len, group_size: int,
@@ -400,6 +418,7 @@ def extend_attn_workspace_size(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffi
     return n.value
 
 
+@_on_call_stream
 def extend_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
                 k_suffix: torch.Tensor, v_suffix: torch.Tensor,
                 prefix_start, prefix_len, suffix_start, suffix_len, new_len, q_start, group_size: int,
@@ -469,6 +488,7 @@ def token_logprob_workspace_size(rows: int, hidden: int, vocab: int) -> int:
     return n.value
 
 
+@_on_call_stream
 def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
                   inv_temperature: float = 1.0, logprob: Optional[torch.Tensor] = None,
                   lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
@@ -509,6 +529,7 @@ def token_logprob(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor
 NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
+@_on_call_stream
 def token_logprob_noalloc(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
                           logprob: torch.Tensor, lse: Optional[torch.Tensor] = None,
                           inv_temperature: float = 1.0, stream=None):
@@ -554,6 +575,7 @@ def token_logprob_backward_workspace_size(rows: int, hidden: int, vocab: int) ->
     return n.value
 
 
+@_on_call_stream
 def token_logprob_backward(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
                            lse: torch.Tensor, grad_logprob: torch.Tensor, inv_temperature: float = 1.0,
                            grad_hidden: Optional[torch.Tensor] = None,
@@ -595,6 +617,7 @@ def sample_top_p_workspace_size(rows: int, hidden: int, vocab: int) -> int:
     return n.value
 
 
+@_on_call_stream
 def sample_top_p(hidden: torch.Tensor, w_lm: torch.Tensor, inv_temperature: torch.Tensor, top_p: float,
                  uniform: torch.Tensor, token: Optional[torch.Tensor] = None,
                  logprob: Optional[torch.Tensor] = None, want_logprob: bool = True,
@@ -639,6 +662,7 @@ def _f32_dev(t: torch.Tensor, name: str, shape) -> torch.Tensor:
     return t
 
 
+@_on_call_stream
 def grpo_advantage(reward: torch.Tensor, group_size: int, adv: Optional[torch.Tensor] = None, stream=None):
     """Group-relative advantages (r - mean) / std over each group of group_size rewards.
 
@@ -664,6 +688,7 @@ def grpo_surrogate_workspace_size(rows: int, num_prompts: int, group_size: int) 
     return n.value
 
 
+@_on_call_stream
 def grpo_surrogate(logp_new: torch.Tensor, logp_old: torch.Tensor, seq: torch.Tensor, adv: torch.Tensor,
                    group_size: int, eps: float = 0.2, loss: Optional[torch.Tensor] = None,
                    grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):

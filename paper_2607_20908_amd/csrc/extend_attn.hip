@@ -1,13 +1,15 @@
 // Causal extend (prefill) attention over a prompt-shared prefix for gfx950.
 //
-// One workgroup (4 wave64s, one per SIMD) serves one block of up to 256 query
-// rows of one candidate at one kv head.  Unit row u = token * r + head in the
-// group, so the r query heads of a token sit side by side and share its causal
-// limit.  Wave w owns rows 64w .. 64w+63 as two 32-row MFMA column tiles.
+// One workgroup serves one block of up to 256 query rows of one candidate at
+// one kv head.  Unit row u = token * r + head in the group, so the r query
+// heads of a token sit side by side and share its causal limit.  The kernel
+// is templated on NT, the 32-row MFMA column tiles per wave; the launched
+// variant has NT = 1: 8 wave64s (two per SIMD, so one wave's softmax and LDS
+// waits overlap the other's MFMAs), wave w owning rows 32w .. 32w+31.
 //
 // The visible context (the prompt's prefix, then the candidate's suffix up to
-// the block's last token) streams through a 3-stage LDS ring in tiles of 64
-// tokens.  Direct global->LDS loads fill it two tiles ahead.  Per tile a wave:
+// the block's last token) streams through a 4-stage LDS ring in tiles of 64
+// tokens.  Direct global->LDS loads fill it three tiles ahead.  Per tile a wave:
 //  - computes S^T = K Q^T on MFMA 32x32x16 bf16, tokens on M and query rows on
 //    N, so each lane holds 32 scores of one row and the row max and sum are
 //    in-lane plus one shuffle across the lane halves;

@@ -79,3 +79,14 @@ def decode_host_case(P, G, Hq, Hkv, D, lp, ls, seed=0, qmul=1.0, gap=0, poison=F
             arr[mask] = nan
     return dict(q=q, k_prefix=kp, v_prefix=vp, k_suffix=ks, v_suffix=vs,
                 prefix_start=ps, prefix_len=lp, suffix_start=ss, suffix_len=ls, group_size=G)
+
+
+def tile_sample(R: int, ntiles: int, seed: int = 0, tile: int = 256) -> np.ndarray:
+    """Rows 0 and R - 1 plus one seeded row in each of ntiles distinct
+    tile-row blocks (the last block included), ascending and distinct."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    nt = (R + tile - 1) // tile
+    tiles = rng.choice(np.arange(nt - 1), size=min(ntiles, nt) - 1, replace=False) if nt > 1 else np.array([], int)
+    tiles = np.concatenate([tiles, [nt - 1]])
+    rows = [min(R - 1, int(t) * tile + int(rng.integers(0, tile))) for t in tiles]
+    return np.unique(np.concatenate([[0, R - 1], rows]).astype(np.int64))

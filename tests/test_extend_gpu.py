@@ -158,26 +158,26 @@ def test_reproducible_and_no_new_tokens():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("layout", ["head", "token"])
-def test_full_size_long_context_turn(layout):
-    """The refinement-turn extend at full size: 4 prompts x G=8, 64/8 heads,
-    D=128, shared prefix 24576, each candidate's whole suffix (geometric, mean
-    1024, cap 4096) new.  The oracle checks sampled tokens one by one: a token
-    of a candidate, at every head, is the call with that candidate's suffix
-    ending at the token and one new token."""
-    cfg = W.DECODE_CONFIGS["longctx"]
+@pytest.mark.parametrize("name,layout", [("longctx", "head"), ("longctx", "token"), ("8b", "head")])
+def test_full_size_turn(name, layout):
+    """The refinement-turn extend at full size, every candidate's whole
+    suffix new: the long context (4 prompts x G=8, 64/8 heads, D=128, shared
+    prefix 24576, suffixes geometric with mean 1024, cap 4096) in both
+    layouts, and the 8B-class shape bench.py times (64 prompts x G=8, 32/8
+    heads, prefix 1024, suffixes uniform in [256, 2048]: 609026 new tokens).
+    The oracle checks the first, the last and a random new token of every
+    candidate, at every head: a token is the call with that candidate's
+    suffix ending at the token and one new token."""
+    cfg = W.DECODE_CONFIGS[name]
     x = W.make_extend_inputs(cfg, dev(), kv_layout=layout)
     d = x.dec
-    say(f"extend full size longctx layout={layout}: {int(x.new_len.sum())} new tokens")
+    say(f"extend full size {name} layout={layout}: {int(x.new_len.sum())} new tokens")
     out, lse = rk.extend_attn(x.q, d.k_prefix, d.v_prefix, d.k_suffix, d.v_suffix, d.prefix_start,
                               d.prefix_len, d.suffix_start, d.suffix_len, x.new_len, x.q_start,
                               cfg.group_size, scale=d.scale, return_lse=True, kv_layout=layout)
     torch.cuda.synchronize()
     assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
     kp, vp, ks, vs = (W.bf16_bits(d.token_major(t)) for t in (d.k_prefix, d.v_prefix, d.k_suffix, d.v_suffix))
-    qb = W.bf16_bits(x.q)
-    ob = out.float().cpu().numpy()
-    lb = lse.cpu().numpy()
     rng = np.random.Generator(np.random.PCG64(3))
     S = cfg.num_seqs
     for rep in range(3):
@@ -185,9 +185,12 @@ def test_full_size_long_context_turn(layout):
         pick = [0 if rep == 0 else (int(x.new_len[s]) - 1 if rep == 1 else int(rng.integers(0, x.new_len[s])))
                 for s in range(S)]
         sl = np.array([d.suffix_len[s] - x.new_len[s] + pick[s] + 1 for s in range(S)], np.int32)
-        rows = np.array([x.q_start[s] + pick[s] for s in range(S)])
-        ro, rl = oracle.extend_attn(qb[rows], kp, vp, ks, vs, d.prefix_start, d.prefix_len, d.suffix_start, sl,
-                                    np.ones(S, np.int32), np.arange(S, dtype=np.int64), cfg.group_size, d.scale)
-        eo, el = max_abs(ob[rows], ro), max_abs(lb[rows], rl)
+        rows = np.array([x.q_start[s] + pick[s] for s in range(S)], np.int64)
+        idx = torch.from_numpy(rows).to(dev())
+        ro, rl = oracle.extend_attn(W.bf16_bits(x.q[idx]), kp, vp, ks, vs, d.prefix_start, d.prefix_len,
+                                    d.suffix_start, sl, np.ones(S, np.int32), np.arange(S, dtype=np.int64),
+                                    cfg.group_size, d.scale)
+        eo = max_abs(out[idx].float().cpu().numpy(), ro)
+        el = max_abs(lse[idx].cpu().numpy(), rl)
         say(f"  sample {rep}: out max-abs {eo:.2e} lse max-abs {el:.2e}")
         assert eo <= ATTN_OUT_TOL and el <= ATTN_LSE_TOL

@@ -17,7 +17,7 @@ import torch
 import oracle
 import paper_2607_20908_amd as rk
 import workloads as W
-from gpu_util import dev, say, to_dev
+from gpu_util import dev, say, tile_sample, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -110,8 +110,9 @@ def test_ragged_shapes(R, H, V):
 
 
 def test_several_row_chunks():
-    # more rows than one chunk of probabilities (16384): three chunks, the last short
-    case(16384 * 2 + 300, 64, 300, seed=21, wstd=0.1, what="three chunks")
+    # 40000 rows, compared on every row: three chunks of probabilities
+    # (16384, 16384, 7232), 64 row tiles in the full ones (two-stage ring)
+    case(40000, 64, 700, seed=21, wstd=0.1, mask_frac=0.05, what="three chunks, 40000 rows")
 
 
 def test_temperature_masking_invalid_and_zero_grads():
@@ -202,9 +203,11 @@ def test_empty_rows():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name,nsample", [("8b", 16), ("32b", 16), ("policy", 8)])
-def test_full_size_workloads(name, nsample):
-    """Full-size runs; the oracle recomputes a seeded sample of rows (first and last included)."""
+@pytest.mark.parametrize("name,ntiles", [("8b", 16), ("32b", 16), ("policy", 64)])
+def test_full_size_workloads(name, ntiles):
+    """Full-size runs; the oracle recomputes rows 0 and R - 1 and one seeded
+    row in each of `ntiles` distinct 256-row tiles (the last included): 64 of
+    the policy pass's 1024 tiles, in 16 different 16384-row chunks."""
     cfg = W.LOGPROB_CONFIGS[name]
     say(f"logprob backward full-size {name}: generating")
     x = W.make_logprob_inputs(cfg, dev())
@@ -212,8 +215,9 @@ def test_full_size_workloads(name, nsample):
                          .astype(np.float32)).to(dev())
     say(f"logprob backward full-size {name}: gpu")
     dh = gpu_backward(x.hidden, x.w_lm, x.target, g, x.inv_temperature)
-    rng = np.random.Generator(np.random.PCG64(11))
-    rows = np.unique(np.concatenate([[0, cfg.rows - 1], rng.integers(0, cfg.rows, nsample - 2)]))
+    rows = tile_sample(cfg.rows, ntiles, seed=11)
+    if cfg.rows <= 512:
+        rows = np.unique(np.concatenate([rows, np.arange(0, cfg.rows, 16)]))
     idx = torch.from_numpy(rows).to(dev())
     say(f"logprob backward full-size {name}: oracle on {len(rows)} rows")
     wb = W.bf16_bits(x.w_lm)

@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2607_20908_amd as rk
 import workloads as W
-from gpu_util import LOGPROB_TOL, dev, max_abs, say, to_dev
+from gpu_util import LOGPROB_TOL, dev, max_abs, say, tile_sample, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -157,18 +157,36 @@ def test_row_permutation_bitwise():
     assert np.array_equal(lp1.view(np.uint32), lp3.view(np.uint32)), "not deterministic"
 
 
+def test_many_rows_every_row():
+    """40000 rows (more than 32768: the one-thread-per-row combine; 157 row
+    tiles: the two-stage weight ring), small hidden size and vocabulary, so
+    the oracle checks every row."""
+    rng = np.random.Generator(np.random.PCG64(12))
+    R, H, V = 40000, 64, 700
+    h = rand_bits(rng, (R, H))
+    w = rand_bits(rng, (V, H), 0.1)
+    t = rng.integers(0, V, R).astype(np.int32)
+    t[rng.random(R) < 0.05] = -1
+    lp, _ = check(h, w, t, 1.0, "40000 rows, every row")
+    assert (lp[t == -1] == 0).all()
+
+
 @pytest.mark.slow
-@pytest.mark.parametrize("name,nsample", [("8b", 24), ("32b", 24), ("policy", 12)])
-def test_full_size_workloads(name, nsample):
-    """Full-size runs; the oracle recomputes a seeded sample of rows (first and last included)."""
+@pytest.mark.parametrize("name,ntiles", [("8b", 64), ("32b", 64), ("policy", 126)])
+def test_full_size_workloads(name, ntiles):
+    """Full-size runs; the oracle recomputes rows 0 and R - 1 and one seeded
+    row in each of `ntiles` distinct 256-row tiles (the last included; all the
+    tiles of the 8B- and 32B-class rows, 127 of the policy pass's 1024 tiles:
+    128 rows, about 4 s of oracle time on 16 cores)."""
     cfg = W.LOGPROB_CONFIGS[name]
     say(f"logprob full-size {name}: generating")
     x = W.make_logprob_inputs(cfg, dev())
     say(f"logprob full-size {name}: gpu")
     lp, lse = rk.token_logprob(x.hidden, x.w_lm, x.target, x.inv_temperature)
     torch.cuda.synchronize()
-    rng = np.random.Generator(np.random.PCG64(11))
-    rows = np.unique(np.concatenate([[0, cfg.rows - 1], rng.integers(0, cfg.rows, nsample - 2)]))
+    rows = tile_sample(cfg.rows, ntiles, seed=11)
+    if cfg.rows <= 512:
+        rows = np.unique(np.concatenate([rows, np.arange(0, cfg.rows, 8)]))   # a row in every 8
     idx = torch.from_numpy(rows).to(dev())
     say(f"logprob full-size {name}: oracle on {len(rows)} rows")
     rlp, rlse = oracle.token_logprob(W.bf16_bits(x.hidden[idx]), W.bf16_bits(x.w_lm),
