@@ -31,6 +31,21 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// max / sum of v and its value in lane l ^ 32 (the other half of the wave):
+// one v_permlane32_swap on the VALU instead of an LDS permute, whose round
+// trip the next instruction would wait for.  After the swap every lane holds
+// its own value and its partner's, one in each register, so both halves get
+// the same result bit for bit.
+__device__ __forceinline__ float half_swap_max(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float half_swap_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // gfx950 transposing LDS read: in each group of 16 lanes, lane s supplies the
 // address of 4 consecutive bf16; seen as a 4 x 16 block whose row k holds the
 // values of lanes 4k..4k+3 in order, lane n receives column n (rows 0..3).

@@ -254,7 +254,7 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
             float m = -INFINITY;
 #pragma unroll
             for (int v = 0; v < 16; ++v) m = fmaxf(m, s_cur[tn][v]);
-            mx[tn] = fmaxf(m, __shfl_xor(m, 32, 64)) * c2;
+            mx[tn] = half_swap_max(m) * c2;
             mv |= mx[tn] > m_ref[tn] + kRescaleLog2;
         }
         if (__any(mv)) return false;
@@ -330,7 +330,7 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
     // ---- normalise and write: acc[dt][tn][v] is d = 32 dt + 8 (v/4) + 4 h2 + v%4
 #pragma unroll
     for (int tn = 0; tn < NT; ++tn) {
-        const float l = l_run[tn] + __shfl_xor(l_run[tn], 32, 64);
+        const float l = half_swap_sum(l_run[tn]);
         const int row = wave * 32 * NT + tn * 32 + l32;
         if (row < rows) {
             const int u = it.row_begin + row;
