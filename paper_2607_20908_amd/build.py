@@ -70,6 +70,9 @@ def _device_asm(src: str) -> str:
 
 
 def _sgprs(tok: str) -> set:
+    """Scalar registers named by one operand (M0 as "m0")."""
+    if tok == "m0":
+        return {"m0"}
     m = re.match(r"s\[(\d+):(\d+)\]$", tok)
     if m:
         return set(range(int(m.group(1)), int(m.group(2)) + 1))
@@ -80,20 +83,61 @@ def _sgprs(tok: str) -> set:
 # VALU instructions that also write an SGPR pair as their second operand (carry out)
 _CARRY_OUT = ("v_mad_u64_u32", "v_mad_i64_i32", "v_add_co_u32", "v_sub_co_u32", "v_addc_co_u32", "v_subb_co_u32",
               "v_subrev_co_u32", "v_subbrev_co_u32", "v_div_scale")
+# instructions after which execution never falls through to the next line
+_NO_FALLTHROUGH = ("s_branch", "s_endpgm", "s_setpc_b64")
+_WAIT_STATES = 5
 
 
 def staging_hazards(asm: str) -> tuple[int, list]:
     """Checks every global_load_lds of a gfx950 assembly listing: returns the
-    number of loads and a description of each that may read a base SGPR fewer
-    than 5 wait states after a VALU write of it (or takes a VGPR base).
-    Walking back from a load, the first writer of each base SGPR decides; a
-    block start reached within 5 wait states counts as a hazard, since a
-    writer in another block is not seen."""
+    number of loads and a description of each that may read a base SGPR or M0
+    fewer than 5 wait states after a VALU write of it (or takes a VGPR base).
+
+    From each load the check walks back along every path that reaches it: at
+    a label it continues into the fall-through predecessor and into every
+    branch to that label, with the wait states counted so far.  On each path
+    the first writer of a register decides; a path that starts at a kernel's
+    entry within the window has no writer."""
     body = []
     for line in asm.splitlines():
         t = line.split(";")[0].strip()
         if t and (not t.startswith(".") or t.endswith(":")):   # instructions and labels, no directives
             body.append(t)
+    branches = {}
+    for k, ins in enumerate(body):
+        parts = ins.split(None, 1)
+        if parts[0].startswith(("s_branch", "s_cbranch")) and len(parts) > 1:
+            branches.setdefault(parts[1].strip(), []).append(k)
+
+    def walk(j, need, ws, ins, via, errs, seen):
+        while j >= 0 and need and ws < _WAIT_STATES:
+            prev = body[j]
+            if prev.endswith(":"):
+                key = (j, ws, frozenset(need))
+                if key in seen:
+                    return
+                seen.add(key)
+                preds = list(branches.get(prev[:-1], []))
+                if j > 0 and (body[j - 1].endswith(":") or body[j - 1].split()[0] not in _NO_FALLTHROUGH):
+                    preds.append(j - 1)
+                for pj in preds:
+                    walk(pj, set(need), ws, ins, via + [prev[:-1]], errs, seen)
+                return
+            parts = prev.split(None, 1)
+            op = parts[0]
+            pops = [o.strip() for o in parts[1].split(",")] if len(parts) > 1 else []
+            written = (_sgprs(pops[0]) if pops else set())
+            if op.startswith(_CARRY_OUT) and len(pops) > 1:
+                written |= _sgprs(pops[1])
+            written &= need
+            if written:
+                if op.startswith("v_"):
+                    path = f" (through {', '.join(via)})" if via else ""
+                    errs.append(f"VALU write {ws} wait states before the load{path}: {prev} -> {ins}")
+                need -= written
+            ws += (int(pops[0]) + 1 if pops else 1) if op == "s_nop" else 1
+            j -= 1
+
     loads, errs = 0, []
     for k, ins in enumerate(body):
         if not ins.startswith("global_load_lds"):
@@ -103,30 +147,10 @@ def staging_hazards(asm: str) -> tuple[int, list]:
         if len(ops) > 1 and ops[1].startswith("v"):
             errs.append(f"VGPR base: {ins}")
             continue
-        need = set()
+        need = {"m0"}
         for o in ops[1:]:
             need |= _sgprs(o)
-        ws = 0
-        for j in range(k - 1, -1, -1):
-            prev = body[j]
-            if prev.endswith(":"):
-                if need and ws < 5:
-                    errs.append(f"base written in another block, within {ws} wait states: {ins}")
-                break
-            parts = prev.split(None, 1)
-            op = parts[0]
-            pops = [o.strip() for o in parts[1].split(",")] if len(parts) > 1 else []
-            written = (_sgprs(pops[0]) if pops else set())
-            if op.startswith(_CARRY_OUT) and len(pops) > 1:
-                written |= _sgprs(pops[1])
-            written &= need
-            if written:
-                if op.startswith("v_") and ws < 5:
-                    errs.append(f"VALU write {ws} wait states before the load: {prev} -> {ins}")
-                need -= written
-            if not need or ws >= 5:
-                break
-            ws += (int(pops[0]) + 1 if pops else 1) if op == "s_nop" else 1
+        walk(k - 1, need, 0, ins, [], errs, set())
     return loads, errs
 
 

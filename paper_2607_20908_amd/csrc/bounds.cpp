@@ -316,14 +316,22 @@ void replay_bwd_gemm(Replay &rp, const LogprobBwdArgs &a, int probs_r, int w_r, 
                 for (int j = 0; j < 8; ++j) {
                     const int blk = wave * 8 + j;
                     for (int slot : as)
-                        ln.check(probs_r, Replay::addr(a.probs) + bwd_a_elem(rt, a.n_vsteps, ks0, slot, nks, blk, lane) * 2,
+                        ln.check(probs_r,
+                                 Replay::addr(a.probs) + bwd_a_base(rt, a.n_vsteps, ks0, slot, nks, blk) * 2 +
+                                     bwd_a_voff(lane),
                                  16, "probability stage load");
                     const int row = bwd_b_row(blk, lane);
-                    for (int slot : bs)
-                        ln.check(w_r,
-                                 Replay::addr(a.w) +
-                                     bwd_b_elem(ks0, slot, nks, row, bwd_b_chunk(row, lane), clast, a.V, H, h0) * 2,
-                                 16, "weight stage load");
+                    const int c = bwd_b_chunk(row, lane);
+                    for (int slot : bs) {
+                        const int64_t first = bwd_b_first(ks0, slot, nks, blk);
+                        const uint64_t base = Replay::addr(a.w) + (bwd_b_base_row(first, a.V) * H + h0) * 2;
+                        const uint32_t voff = bwd_b_voff(lane, bwd_b_pair(first, a.V), c, clast, H);
+                        ln.check(w_r, base + voff, 16, "weight stage load");
+                        // the row the lane must read: its band row, clamped to the vocabulary
+                        const int64_t want = std::min<int64_t>(first + (lane >> 5), a.V - 1);
+                        if (base + voff != Replay::addr(a.w) + (want * H + h0 + 8 * std::min(c, clast)) * 2)
+                            ln.check(w_r, 0, static_cast<uint64_t>(1) << 63, "weight load not at its clamped row");
+                    }
                 }
             }
         const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;

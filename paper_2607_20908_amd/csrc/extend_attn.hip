@@ -140,27 +140,28 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
     }
     auto tile_tok0 = [&](int t) { return (t < np ? t : t - np) * kBN; };
     auto tile_cnt = [&](int t) { return min(kBN, (t < np ? it.Lp : suf_ctx) - tile_tok0(t)); };
+    const uint32_t ring_l = lds_addr(ring);
     auto issue = [&](int t) {
-        uint16_t *kl = ring + (t % kStages) * 2 * C::TILE;
-        uint16_t *vl = kl + C::TILE;
+        const uint32_t kl = ring_l + (t % kStages) * (2 * C::TILE * 2);
+        const uint32_t vl = kl + C::TILE * 2;
         const bool pre = t < np;
         const int tok0 = tile_tok0(t), cnt = tile_cnt(t);
         const uint16_t *kg = (pre ? kpre : ksuf) + tok0 * tok_stride;
         const uint16_t *vg = (pre ? vpre : vsuf) + tok0 * tok_stride;
         if (cnt == kBN) {
 #pragma unroll
-            for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, ld_off[j], kl + (wave * C::LPW + j) * 512);
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, ld_off[j], kl + (wave * C::LPW + j) * 1024);
 #pragma unroll
-            for (int j = 0; j < C::LPW; ++j) load_lds16_s(vg, ld_off[j], vl + (wave * C::LPW + j) * 512);
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(vg, ld_off[j], vl + (wave * C::LPW + j) * 1024);
         } else {
             uint32_t off[C::LPW];
 #pragma unroll
             for (int j = 0; j < C::LPW; ++j)
                 off[j] = static_cast<uint32_t>((min(ld_tok[j], cnt - 1) * tok_stride + ld_chk[j]) * 2);
 #pragma unroll
-            for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, off[j], kl + (wave * C::LPW + j) * 512);
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, off[j], kl + (wave * C::LPW + j) * 1024);
 #pragma unroll
-            for (int j = 0; j < C::LPW; ++j) load_lds16_s(vg, off[j], vl + (wave * C::LPW + j) * 512);
+            for (int j = 0; j < C::LPW; ++j) load_lds16_s(vg, off[j], vl + (wave * C::LPW + j) * 1024);
         }
     };
     auto stage_k = [&](int t) -> const uint16_t * { return ring + (t % kStages) * 2 * C::TILE; };

@@ -18,9 +18,14 @@ namespace rlk {
 // the one wait state the ISA requires between an SALU write of M0 and an LDS
 // DMA instruction that reads it (the compiler's hazard tracking does not look
 // inside the asm).
-__device__ __forceinline__ uint32_t lds_base_u32(uint16_t *l) {
-    typedef __attribute__((address_space(3))) uint16_t lds_u16;
-    return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u16 *)(l))));
+//
+// LDS destinations are passed as 32-bit LDS byte addresses: the address of a
+// __shared__ array is taken once (lds_addr) and each load adds a wave-uniform
+// offset on the scalar unit.  Converting a generic pointer at every load
+// would cost a 64-bit add, a null check and a select per load.
+__device__ __forceinline__ uint32_t lds_addr(const void *l) {
+    typedef __attribute__((address_space(3))) const unsigned char lds_u8;
+    return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8 *)(l))));
 }
 
 // A value the same in every lane of the wave, read first-lane so the compiler
@@ -36,27 +41,19 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
     return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-__device__ __forceinline__ void load_lds16(const uint16_t *g, uint16_t *l) {
-    asm volatile(
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %0, off"
-        :
-        : "v"(g), "{m0}"(lds_base_u32(l))
-        : "memory");
-}
-
-// The same with a wave-uniform base in SGPRs and a per-lane 32-bit byte offset
+// A wave-uniform global base in SGPRs plus a per-lane 32-bit byte offset
 // (the global_load_lds "saddr" form): no 64-bit address arithmetic per lane.
 // The base must be computed on the scalar unit: the compiler's hazard
 // tracking does not see that the asm's VMEM instruction reads those SGPRs, so
 // a VALU write of them (a v_readfirstlane) right before it would need 5 wait
 // states it does not get.  build.py checks the gfx950 assembly for that.
-__device__ __forceinline__ void load_lds16_s(const void *base, uint32_t voff, uint16_t *l) {
+// `lds` is the destination's LDS byte address (lds_addr + offset).
+__device__ __forceinline__ void load_lds16_s(const void *base, uint32_t voff, uint32_t lds) {
     asm volatile(
         "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, %1"
         :
-        : "v"(voff), "s"(base), "{m0}"(lds_base_u32(l))
+        : "v"(voff), "s"(base), "{m0}"(lds)
         : "memory");
 }
 

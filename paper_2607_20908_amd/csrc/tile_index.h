@@ -162,20 +162,31 @@ RLK_HD void gemm_tile_of(int64_t b, int n_h_tiles, int n_row_tiles, int splits, 
 }
 
 // Probability operand: block blk (0..31) of stage `slot` is the 1 KB at this
-// element offset from the chunk's blocked buffer (lane: 8 elements).
-RLK_HD int64_t bwd_a_elem(int rt, int n_vsteps, int ks0, int slot, int nks, int blk, int lane) {
-    return probs_block(rt, n_vsteps, ks0 + mini(slot, nks - 1)) + blk * 512 + lane * 8;
+// element offset from the chunk's blocked buffer, lane i's 16 bytes at byte
+// offset 16 i from it (the saddr form: a wave-uniform base plus a fixed
+// per-lane offset).
+RLK_HD int64_t bwd_a_base(int rt, int n_vsteps, int ks0, int slot, int nks, int blk) {
+    return probs_block(rt, n_vsteps, ks0 + mini(slot, nks - 1)) + blk * 512;
 }
+RLK_HD uint32_t bwd_a_voff(int lane) { return static_cast<uint32_t>(lane) * 16; }
 
 // W operand: block blk holds band rows 2 blk and 2 blk + 1; lane i fills slot
 // i % 32 of row 2 blk + i / 32 with chunk slot ^ (4 (row % 4)).  Rows past
 // the vocabulary re-read the last row (their probabilities are 0); columns
-// past the hidden size re-read the last chunk (never stored).
+// past the hidden size re-read the last chunk (never stored).  In the saddr
+// form the wave-uniform base is the block's first row, clamped to V - 1, and
+// lanes i >= 32 add one row only while that row exists (`pair`, the same for
+// the whole wave), which clamps every lane's row to V - 1 exactly as
+// min(first row + i / 32, V - 1) would.
 RLK_HD int bwd_b_row(int blk, int lane) { return 2 * blk + (lane >> 5); }
 RLK_HD int bwd_b_chunk(int row, int lane) { return (lane & 31) ^ (4 * (row & 3)); }
-RLK_HD int64_t bwd_b_elem(int ks0, int slot, int nks, int row, int c, int clast, int V, int64_t H, int h0) {
-    const int64_t v = min64(static_cast<int64_t>(ks0 + mini(slot, nks - 1)) * 64 + row, static_cast<int64_t>(V - 1));
-    return v * H + h0 + 8 * mini(c, clast);
+RLK_HD int64_t bwd_b_first(int ks0, int slot, int nks, int blk) {
+    return static_cast<int64_t>(ks0 + mini(slot, nks - 1)) * 64 + 2 * blk;
+}
+RLK_HD int64_t bwd_b_base_row(int64_t first, int V) { return min64(first, static_cast<int64_t>(V - 1)); }
+RLK_HD bool bwd_b_pair(int64_t first, int V) { return first + 1 <= static_cast<int64_t>(V - 1); }
+RLK_HD uint32_t bwd_b_voff(int lane, bool pair, int c, int clast, int64_t H) {
+    return static_cast<uint32_t>(((pair ? (lane >> 5) : 0) * H + 8 * mini(c, clast)) * 2);
 }
 RLK_HD int bwd_clast(int H, int h0) { return mini(256, H - h0) / 8 - 1; }
 

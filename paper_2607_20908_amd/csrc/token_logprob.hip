@@ -214,19 +214,24 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     // past the last stage the loads refill a buffer nobody reads any more.
     auto wbuf = [&](int ks) { return wring + (ks % WS) * WELEMS; };
     auto hbuf = [&](int ks) { return hring + (ks & 1) * kTileElems; };
-    auto issue_block = [&](const uint16_t *g, int last, uint16_t *st, int slot, int blk) {
+    const uint32_t wring_l = lds_addr(wring), hring_l = lds_addr(hring);
+    auto issue_block = [&](const uint16_t *g, int last, uint32_t st, int slot, int blk) {
         const int row = stage_row(blk, lane);
         // wave-uniform base (SGPRs) plus a per-lane byte offset that stays
         // the same from stage to stage
-        load_lds16_s(g + stage_k0(kb, slot, nks), stage_voff(row, last, H, stage_chunk(row, lane)), st + blk * 512);
+        load_lds16_s(g + stage_k0(kb, slot, nks), stage_voff(row, last, H, stage_chunk(row, lane)), st + blk * 1024);
     };
+    auto wbuf_l = [&](int ks) { return wring_l + (ks % WS) * (WELEMS * 2); };
+    auto hbuf_l = [&](int ks) { return hring_l + (ks & 1) * (kTileElems * 2); };
     auto issue_w = [&](int slot) {
+        const uint32_t st = wbuf_l(slot);
 #pragma unroll
-        for (int j = 0; j < WBLK; ++j) issue_block(wg, wlast, wbuf(slot), slot, wave * WBLK + j);
+        for (int j = 0; j < WBLK; ++j) issue_block(wg, wlast, st, slot, wave * WBLK + j);
     };
     auto issue_h = [&](int slot) {
+        const uint32_t st = hbuf_l(slot);
 #pragma unroll
-        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(hg, hlast, hbuf(slot), slot, wave * kBlocksPerWave + j);
+        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(hg, hlast, st, slot, wave * kBlocksPerWave + j);
     };
 
     f32x16 acc[TM][4];
@@ -296,12 +301,12 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
                 if (g < 4) {
-                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g);
-                    issue_block(hg, hlast, hbuf(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g + 1);
+                    issue_block(hg, hlast, hbuf_l(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g);
+                    issue_block(hg, hlast, hbuf_l(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g + 1);
                 } else {
 #pragma unroll
                     for (int jj = 2 * (g - 4); jj < 2 * (g - 4) + 2; ++jj)
-                        if (jj < WBLK) issue_block(wg, wlast, wbuf(ks + WS), ks + WS, wave * WBLK + jj);
+                        if (jj < WBLK) issue_block(wg, wlast, wbuf_l(ks + WS), ks + WS, wave * WBLK + jj);
                 }
 #pragma unroll
                 for (int m = 2 * g; m < 2 * g + 2; ++m)

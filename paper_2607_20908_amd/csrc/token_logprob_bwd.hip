@@ -67,15 +67,29 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
     const int clast = bwd_clast(H, h0);
     auto abuf = [&](int s) { return aring + (s & 1) * kTileElems; };
     auto bbuf = [&](int s) { return bring + (s % WS) * kTileElems; };
+    // saddr-form loads: wave-uniform bases (scalar arithmetic only) and
+    // per-lane byte offsets fixed for the whole loop; for W, one table for
+    // blocks whose second row exists and one for the last rows
+    const uint32_t aring_l = lds_addr(aring), bring_l = lds_addr(bring);
+    const uint32_t avoff = bwd_a_voff(lane);
+    uint32_t bvoff_pair[kBlocksPerWave], bvoff_same[kBlocksPerWave];
+#pragma unroll
+    for (int j = 0; j < kBlocksPerWave; ++j) {
+        const int row = bwd_b_row(wave * kBlocksPerWave + j, lane);
+        const int c = bwd_b_chunk(row, lane);
+        bvoff_pair[j] = bwd_b_voff(lane, true, c, clast, H);
+        bvoff_same[j] = bwd_b_voff(lane, false, c, clast, H);
+    }
     auto issue_a = [&](int slot, int j) {
         const int blk = wave * kBlocksPerWave + j;
-        load_lds16(a.probs + bwd_a_elem(rt, a.n_vsteps, ks0, slot, nks, blk, lane), abuf(slot) + blk * 512);
+        load_lds16_s(a.probs + bwd_a_base(rt, a.n_vsteps, ks0, slot, nks, blk), avoff,
+                     aring_l + ((slot & 1) * kTileElems + blk * 512) * 2);
     };
     auto issue_b = [&](int slot, int j) {
         const int blk = wave * kBlocksPerWave + j;
-        const int row = bwd_b_row(blk, lane);
-        load_lds16(a.w + bwd_b_elem(ks0, slot, nks, row, bwd_b_chunk(row, lane), clast, a.V, H, h0),
-                   bbuf(slot) + blk * 512);
+        const int64_t first = bwd_b_first(ks0, slot, nks, blk);
+        load_lds16_s(a.w + bwd_b_base_row(first, a.V) * H + h0, bwd_b_pair(first, a.V) ? bvoff_pair[j] : bvoff_same[j],
+                     bring_l + ((slot % WS) * kTileElems + blk * 512) * 2);
     };
 
     f32x16 acc[4][4];

@@ -42,10 +42,41 @@ def test_carry_out_of_a_valu_op_is_a_write():
     assert len(errs) == 1
 
 
-def test_block_start_within_five_wait_states_is_flagged():
-    n, errs = scan(".LBB0_3:\n\ts_nop 0\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
-    assert len(errs) == 1 and "another block" in errs[0]
-    n, errs = scan(".LBB0_3:\n\ts_nop 5\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+def test_writer_in_a_predecessor_block_is_flagged():
+    # fall-through predecessor
+    n, errs = scan("\tv_readfirstlane_b32 s8, v1\n.LBB0_3:\n\ts_nop 0\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+    assert len(errs) == 1 and "LBB0_3" in errs[0]
+    # branch predecessor only (the line before the label ends its block)
+    n, errs = scan("\tv_readfirstlane_b32 s9, v1\n\ts_cbranch_scc1 .LBB0_3\n\ts_endpgm\n"
+                   ".LBB0_3:\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+    assert len(errs) == 1 and "1 wait states" in errs[0]   # the branch itself
+    # the same with enough wait states on every path
+    n, errs = scan("\tv_readfirstlane_b32 s9, v1\n\ts_nop 3\n\ts_cbranch_scc1 .LBB0_3\n\ts_endpgm\n"
+                   ".LBB0_3:\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+    assert errs == []
+
+
+def test_one_bad_path_of_several_is_flagged():
+    text = ("\ts_mov_b32 s8, 0\n\ts_cbranch_scc0 .LBB0_4\n\tv_readfirstlane_b32 s8, v1\n"
+            ".LBB0_4:\n\ts_nop 0\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+    n, errs = scan(text)
+    assert len(errs) == 1 and "v_readfirstlane_b32 s8" in errs[0]
+
+
+def test_kernel_entry_and_loops():
+    # a path that starts at the kernel entry has no writer
+    n, errs = scan("kern:\n\ts_nop 0\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+    assert errs == []
+    # a loop whose back edge carries a VALU write of the base
+    n, errs = scan("\ts_mov_b64 s[8:9], 0\n.LBB0_1:\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n"
+                   "\tv_readfirstlane_b32 s8, v1\n\ts_cbranch_scc1 .LBB0_1\n\ts_endpgm\n")
+    assert len(errs) == 1
+
+
+def test_valu_write_of_m0_is_flagged():
+    n, errs = scan("\tv_readfirstlane_b32 m0, v3\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
+    assert len(errs) == 1
+    n, errs = scan("\ts_mov_b32 m0, s3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 v12, s[8:9]\n")
     assert errs == []
 
 
