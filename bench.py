@@ -591,6 +591,104 @@ def extra_ops(rk, W, args, x, y, lse2, ops, hip, sh, dev):
     return update
 
 
+TIMELINE_KINDS = {0: "whole tiles", 1: "narrow tiles", 2: "tail parts"}
+
+
+def timeline_report(rk, y, evict, desc: str) -> str:
+    """The tile launches of one lm-head call, one record per wave from
+    rl_debug_logprob_timeline (after the same cache eviction as the timed
+    operations), summarised as markdown."""
+    plain = lambda: rk.token_logprob(y.hidden, y.w_lm, y.target, y.inv_temperature)
+    stamped = lambda: rk.token_logprob_timeline(y.hidden, y.w_lm, y.target, y.inv_temperature)
+    for _ in range(2):
+        plain()
+        stamped()
+    # both entry points alternately, each call after the eviction, by events
+    ms = {"plain": [], "stamped": []}
+    for _ in range(5):
+        for name, f in (("plain", plain), ("stamped", stamped)):
+            evict()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            out = f()
+            e1.record()
+            torch.cuda.synchronize()
+            ms[name].append(e0.elapsed_time(e1))
+    lp, lse, rec = out                      # the last stamped call's
+    ref_lp, ref_lse = plain()
+    same = bool(torch.equal(lp, ref_lp) and torch.equal(lse, ref_lse))
+    return timeline_markdown(rec.cpu().numpy(), same, 2 * y.cfg.vocab * y.cfg.hidden, desc,
+                             float(np.median(ms["plain"])), float(np.median(ms["stamped"])))
+
+
+def timeline_markdown(r: np.ndarray, same: bool, wbytes: int, desc: str, plain_ms: float = None,
+                      stamped_ms: float = None) -> str:
+    """Markdown summary of timeline records (int64 [n, 8], 4 consecutive
+    records per workgroup; word layout in rl_kernels.h); plain_ms and
+    stamped_ms are the whole call's event times without and with the stamps."""
+    hw = r[:, 0] & 0xFFFFFFFF
+    xcc = (r[:, 0] >> 32) & 0xFF
+    kind = (r[:, 0] >> 40) & 0xFF
+    t_start, t_loop0, t_loop1, t_end = (r[:, i] for i in range(1, 5))
+    wait, cyc, nks = r[:, 5], r[:, 6], (r[:, 7] >> 32) & 0xFFFF
+    samples = np.maximum((r[:, 7] >> 48) & 0xFFFF, 1)
+    wait = wait / samples * nks          # the sampled stages' mean wait, over all stages
+    # HW_ID: CU id bits 11:8, shader array bit 12, shader engine bits 15:13
+    cu = xcc * 256 + ((hw >> 13) & 7) * 32 + ((hw >> 12) & 1) * 16 + ((hw >> 8) & 0xF)
+    t0 = int(t_start.min())
+    us = lambda t: (t - t0) * 0.01        # 100 MHz wall clock
+    q = lambda v: "/".join(f"{np.percentile(v, p):.1f}" for p in (10, 50, 90))
+    out = [f"# lm-head tile timeline: {desc}", "",
+           "One call of rl_debug_logprob_timeline (the tile launches of rl_token_logprob with per-wave "
+           "timestamps; the log-prob and lse it returned are "
+           f"{'bit-identical to' if same else 'NOT identical to'} rl_token_logprob's), after a 1 GiB read that "
+           "empties the caches.  Wall clock: s_memrealtime (100 MHz); cycles: s_memtime.  Per workgroup the "
+           "earliest start and the latest end of its 4 waves; waits and cycles averaged over the waves.  The stage-end "
+           "wait (loads of the next stage, then the barrier) is sampled in one stage of every 8.", "",
+           "| launch | workgroups | stages | first start - last end (us) | tile us p10/p50/p90 | "
+           "prologue us | loop us | epilogue us | ns per stage | stage-end wait share | clock (cycles per ns, GHz) |",
+           "|---|---:|---:|---|---|---|---|---|---:|---:|---:|"]
+    per_kind = {}
+    for k in sorted(set(kind.tolist())):
+        m = kind == k
+        n = int(m.sum()) // 4
+        g = lambda v: v[m].reshape(n, 4)
+        st, lo0, lo1, en = g(t_start).min(1), g(t_loop0).max(1), g(t_loop1).max(1), g(t_end).max(1)
+        wt, cy, ns = g(wait).mean(1), g(cyc).mean(1), g(nks)[:, 0]
+        wall_loop = (lo1 - lo0) * 10.0     # ns
+        per_kind[k] = (st, en, g(cu)[:, 0], g(xcc)[:, 0])
+        out.append(f"| {TIMELINE_KINDS.get(k, k)} | {n} | {int(np.median(ns))} | {us(st.min()):.1f} - {us(en.max()):.1f} "
+                   f"| {q((en - st) * 0.01)} | {q((lo0 - st) * 0.01)} | {q((lo1 - lo0) * 0.01)} "
+                   f"| {q((en - lo1) * 0.01)} | {np.median(wall_loop / ns):.0f} | {np.median(wt / cy):.3f} "
+                   f"| {np.median(cy / wall_loop):.3f} |")
+    out += ["", "Per CU (XCD, shader engine, CU): workgroups run one after another; the gap is the time from one "
+            "workgroup's end to the next one's start on the same CU, the idle tail the time from a CU's last end "
+            "to the launch's last end.", "",
+            "| launch | CUs used | workgroups per CU | gap us p10/p50/p90 | idle tail us p10/p50/p90 | "
+            "last end per XCD (us) |", "|---|---:|---|---|---|---|"]
+    for k, (st, en, c, x) in per_kind.items():
+        gaps, tails, counts = [], [], []
+        for cid in np.unique(c):
+            o = np.argsort(st[c == cid])
+            s1, e1 = st[c == cid][o], en[c == cid][o]
+            counts.append(len(o))
+            gaps += ((s1[1:] - e1[:-1]) * 0.01).tolist()
+            tails.append((en.max() - e1[-1]) * 0.01)
+        xe = " ".join(f"{us(en[x == i].max()):.0f}" for i in range(8) if (x == i).any())
+        hist = {v: counts.count(v) for v in sorted(set(counts))}
+        out.append(f"| {TIMELINE_KINDS.get(k, k)} | {len(counts)} | "
+                   f"{', '.join(f'{v}: {c_} CUs' for v, c_ in hist.items())} | {q(np.array(gaps)) if gaps else '-'} "
+                   f"| {q(np.array(tails))} | {xe} |")
+    span = us(t_end.max())
+    out += ["", f"All tile launches: {span:.1f} us from the first start to the last end; the weights "
+            f"({wbytes / 1e9:.3f} GB) over that span stream at {wbytes / (span * 1e-6) / 1e9:.0f} GB/s."]
+    if plain_ms is not None:
+        out += ["", f"Whole call by events (medians of 5, each after the eviction; both entry points "
+                f"alternately): rl_token_logprob {plain_ms * 1e3:.1f} us, rl_debug_logprob_timeline "
+                f"{stamped_ms * 1e3:.1f} us."]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -613,6 +711,9 @@ def main():
                          "which are timed after the step in a loop of their own")
     ap.add_argument("--no-extend", action="store_true",
                     help="skip the extend (prefill) of a refinement turn, timed after the step")
+    ap.add_argument("--timeline", default="",
+                    help="write a markdown summary of the headline lm-head's tile launches (per-wave timestamps "
+                         "from rl_debug_logprob_timeline) to this file")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy before the steps (outside the timed region) so a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -653,6 +754,10 @@ def main():
 
     head, t, (x, y, ops, lse2) = measure_workload(rk, W, args.workload, args, timer, dev, args.steps, args.warmup,
                                                   args.cpu_budget, keep=True)
+    if args.timeline and y is not None:
+        with open(args.timeline, "w") as f:
+            f.write(timeline_report(rk, y, evict, head["workload"]))
+        log(f"bench: tile timeline written to {args.timeline}")
     update = extra_ops(rk, W, args, x, y, lse2, ops, hip, stream.cuda_stream, dev)
     del x, y, ops, lse2
     torch.cuda.empty_cache()

@@ -80,7 +80,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 9
+#define RL_ABI_VERSION 10
 
 typedef enum {
     RL_OK = 0,
@@ -531,6 +531,39 @@ typedef struct {
 
 rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t hidden, int32_t vocab,
                                   int32_t every_stage, int32_t shrink_region, rl_bounds_report *report);
+
+/*
+ * Debug timeline of rl_token_logprob, to see where a tile's time goes: the
+ * same call (arguments, plan, outputs and arithmetic), with the tile
+ * launches (whole tiles, narrow tiles of a last round, hidden-dimension parts
+ * of tail tiles) built with timestamps.  Each wave of each of those
+ * workgroups writes one record of RL_TIMELINE_WORDS uint64 to `records`
+ * (device memory, 8-byte aligned, `capacity` records):
+ *   [0] HW_ID register | XCC id << 32 | launch (0 whole, 1 narrow,
+ *       2 tail part) << 40 | wave << 48
+ *   [1] wall clock when the workgroup starts   (s_memrealtime, 100 MHz)
+ *   [2] wall clock when its first stage has landed (the loop starts)
+ *   [3] wall clock at the end of the loop
+ *   [4] wall clock after the epilogue
+ *   [5] shader-clock cycles (s_memtime) spent in the stage-end waits (the
+ *       loads of the next stage, then the workgroup barrier) of the sampled
+ *       stages, those whose index is 3 mod 8
+ *   [6] shader-clock cycles of the loop
+ *   [7] workgroup index | hidden-dimension stages << 32 | sampled stages << 48
+ * Whole-tile workgroup b, wave w writes record 4 b + w; the narrow tiles and
+ * then the tail parts follow in the same way.  *num_records gets the number
+ * of records the call writes; with records == NULL only that number is
+ * computed (no launch, no other pointer checked).  A stamp makes the wave
+ * wait for the scalar read that returns it, so the sampled stages run a
+ * little slower than rl_token_logprob's.  Status: as rl_token_logprob, plus
+ * RL_ERR_NULL_POINTER for a NULL num_records, RL_ERR_WORKSPACE when capacity
+ * is short and RL_ERR_MISALIGNED for misaligned records.
+ */
+#define RL_TIMELINE_WORDS 8
+rl_status rl_debug_logprob_timeline(int64_t rows, int32_t hidden, int32_t vocab, const void *hidden_states,
+                                    const void *w_lm, const int32_t *target, float inv_temperature,
+                                    float *logprob, float *lse, void *workspace, size_t workspace_bytes,
+                                    uint64_t *records, int64_t capacity, int64_t *num_records, void *stream);
 
 #ifdef __cplusplus
 }

@@ -96,7 +96,7 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
            "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds",
-           "rl_token_logprob_noalloc"]
+           "rl_token_logprob_noalloc", "rl_debug_logprob_timeline"]
 
 
 def _load():
@@ -145,7 +145,10 @@ def _load():
     lib.rl_debug_logprob_bounds.argtypes = [I32, I64, I32, I32, I32, I32, ctypes.POINTER(BoundsReport)]
     lib.rl_token_logprob_noalloc.restype = ctypes.c_int
     lib.rl_token_logprob_noalloc.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P]
-    if lib.rl_abi_version() != 9:
+    lib.rl_debug_logprob_timeline.restype = ctypes.c_int
+    lib.rl_debug_logprob_timeline.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P, I64,
+                                              ctypes.POINTER(ctypes.c_int64), P]
+    if lib.rl_abi_version() != 10:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -566,6 +569,46 @@ def logprob_bounds(op: int, rows: int, hidden: int, vocab: int, every_stage: boo
     _check(_lib.rl_debug_logprob_bounds(op, rows, hidden, vocab, int(bool(every_stage)), shrink_region,
                                         ctypes.byref(rep)), "rl_debug_logprob_bounds")
     return rep
+
+
+TIMELINE_WORDS = 8
+
+
+def logprob_timeline_records(rows: int, hidden: int, vocab: int) -> int:
+    """Number of records rl_debug_logprob_timeline writes at these sizes."""
+    n = ctypes.c_int64(0)
+    _check(_lib.rl_debug_logprob_timeline(rows, hidden, vocab, None, None, None, 1.0, None, None, None, 0, None, 0,
+                                          ctypes.byref(n), None), "rl_debug_logprob_timeline")
+    return n.value
+
+
+@_on_call_stream
+def token_logprob_timeline(hidden: torch.Tensor, w_lm: torch.Tensor, target: torch.Tensor,
+                           inv_temperature: float = 1.0, stream=None):
+    """token_logprob through rl_debug_logprob_timeline: returns (logprob, lse,
+    records), records an int64 [n, TIMELINE_WORDS] device tensor holding the
+    per-wave timeline of the tile launches (word layout in rl_kernels.h)."""
+    _bf16_dev(hidden, "hidden")
+    _bf16_dev(w_lm, "w_lm")
+    _on_device(target, "target")
+    if target.dtype != torch.int32 or not target.is_contiguous():
+        raise TypeError("target must be a contiguous int32 tensor")
+    R, H = hidden.shape
+    V, H2 = w_lm.shape
+    if H2 != H or target.shape != (R,):
+        raise ValueError("shapes: hidden [R, H], w_lm [V, H], target [R]")
+    logprob = torch.empty(R, dtype=torch.float32, device=hidden.device)
+    lse = torch.empty(R, dtype=torch.float32, device=hidden.device)
+    need = token_logprob_workspace_size(R, H, V)
+    workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    cap = logprob_timeline_records(R, H, V)
+    records = torch.zeros((max(cap, 1), TIMELINE_WORDS), dtype=torch.int64, device=hidden.device)
+    n = ctypes.c_int64(0)
+    _check(_lib.rl_debug_logprob_timeline(R, H, V, _ptr(hidden), _ptr(w_lm), _ptr(target), float(inv_temperature),
+                                          _ptr(logprob), _ptr(lse), ctypes.c_void_p(workspace.data_ptr()),
+                                          workspace.numel(), ctypes.c_void_p(records.data_ptr()), cap,
+                                          ctypes.byref(n), _stream_handle(stream)), "rl_debug_logprob_timeline")
+    return logprob, lse, records[:n.value]
 
 
 def token_logprob_backward_workspace_size(rows: int, hidden: int, vocab: int) -> int:

@@ -430,6 +430,48 @@ rl_status rl_token_logprob(int64_t rows, int32_t hidden, int32_t vocab, const vo
     return RL_OK;
 }
 
+rl_status rl_debug_logprob_timeline(int64_t rows, int32_t hidden, int32_t vocab, const void *hidden_states,
+                                    const void *w_lm, const int32_t *target, float inv_temperature, float *logprob,
+                                    float *lse, void *workspace, size_t workspace_bytes, uint64_t *records,
+                                    int64_t capacity, int64_t *num_records, void *stream) {
+    g_last_error.clear();
+    if (!num_records) return set_error(RL_ERR_NULL_POINTER, "num_records is NULL");
+    rlk::LogprobPlan plan;
+    std::string err;
+    rl_status st = rlk::plan_logprob(rows, hidden, vocab, &plan, &err);
+    if (st != RL_OK) return set_error(st, err);
+    // one record per wave (4 per workgroup) of the whole-tile, narrow-tile
+    // and tail-part launches
+    const int64_t need =
+        (plan.n_dp_tiles + plan.narrow_tiles * plan.n_row_tiles + plan.n_tail_tiles * plan.tail_splits) * 4;
+    if (!records) {
+        *num_records = need;
+        return RL_OK;
+    }
+    st = rlk::check_logprob_args(plan, hidden_states, w_lm, target, inv_temperature, logprob, lse, &err);
+    if (st != RL_OK) return set_error(st, err);
+    if (capacity < need)
+        return set_error(RL_ERR_WORKSPACE, "records hold " + std::to_string(capacity) + " entries, the call writes " +
+                                               std::to_string(need));
+    if ((reinterpret_cast<uintptr_t>(records) & 7u) != 0)
+        return set_error(RL_ERR_MISALIGNED, "records are not 8-byte aligned");
+    if (rows == 0) {
+        *num_records = 0;
+        return RL_OK;
+    }
+    if (!workspace || workspace_bytes < plan.total_bytes)
+        return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(plan.total_bytes) +
+                                               " bytes, got " + std::to_string(workspace_bytes));
+    if (!aligned16(workspace)) return set_error(RL_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+    rlk::LogprobArgs a = rlk::logprob_args(plan, hidden_states, w_lm, target, inv_temperature, logprob, lse,
+                                           static_cast<unsigned char *>(workspace));
+    a.timeline = records;
+    const hipError_t e = rlk::launch_logprob(a, static_cast<hipStream_t>(stream), true);
+    if (e != hipSuccess) return hip_error(e, "launching token log-prob (timeline)");
+    *num_records = need;
+    return RL_OK;
+}
+
 static bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 namespace {

@@ -112,9 +112,18 @@ struct LogprobArgs {
     const float *inv_t_rows;
     float *logits;
     int64_t ld;
+    // debug timeline only (launch_logprob with timeline): kTimelineWords
+    // words per wave of every whole-tile, narrow-tile and tail-part
+    // workgroup, the launch's first record at timeline_base (set per launch)
+    uint64_t *timeline;
+    int64_t timeline_base;
 };
 
-hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream);
+constexpr int kTimelineWords = 8;
+
+// timeline: launch the tile kernels (whole, narrow, tail parts) built with
+// per-wave timeline records (same arithmetic and outputs)
+hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream, bool timeline = false);
 
 // Backward of the token log-prob with respect to the hidden rows, for one
 // chunk of rows at a time (the probabilities of a chunk live in the

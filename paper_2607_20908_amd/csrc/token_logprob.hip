@@ -179,9 +179,18 @@ __device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 
 // TM: 32-entry vocab blocks per wave; a tile spans 64 TM vocab entries (4:
 // the 256 x 256 tiles; 3: the narrow tiles of a last round, for the forward
 // (kNarrow) and the sampling head's logits (kLogits)).
-template <int WS, int MODE, int TM = 4>
+// TL: debug build with a timeline record per wave (forward modes only): wall
+// clock at the start, at the loop's start and end and after the epilogue,
+// shader-clock cycles of the loop, and the cycles of the stage-end wait in one
+// stage of every 8 (a sample: each stamp makes the wave wait for the scalar
+// read that returns it).  The same arithmetic as TL = false.
+template <int WS, int MODE, int TM = 4, bool TL = false>
 __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobArgs a) {
     static_assert(TM == 4 || MODE == kNarrow || MODE == kLogits, "narrow tiles: forward and logits only");
+    static_assert(!TL || MODE == kFwd || MODE == kNarrow || MODE == kPartialK, "timeline: forward tiles only");
+    [[maybe_unused]] uint64_t tl_start = 0, tl_loop0 = 0, tl_loop1 = 0, tl_c0 = 0, tl_c1 = 0, tl_wait = 0;
+    [[maybe_unused]] uint32_t tl_samples = 0;
+    if constexpr (TL) tl_start = __builtin_amdgcn_s_memrealtime();
     constexpr int VW = 64 * TM;                  // vocab entries per tile
     constexpr int WELEMS = VW * kK;              // bf16 elements of one weight stage
     constexpr int WBLK = VW / 32;                // 1 KB weight blocks per wave per stage
@@ -273,6 +282,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     if (WS == 3) issue_w(2);
     wait_vm<kBlocksPerWave + (WS == 3 ? 2 : 1) * WBLK>();   // stage 0 has landed
     barrier();
+    if constexpr (TL) {
+        tl_loop0 = __builtin_amdgcn_s_memrealtime();
+        tl_c0 = __builtin_amdgcn_s_memtime();
+    }
     read_frags(0, 0, 0);
     for (int ks = 0; ks < nks; ++ks) {
 #pragma unroll
@@ -288,9 +301,17 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         }
         // last k-step: stage ks+1 has landed (only the weights of stage ks+2
         // may still be in flight) and every wave is done reading stage ks
+        [[maybe_unused]] uint64_t tl_w0 = 0;
+        if constexpr (TL)
+            if ((ks & 7) == 3) tl_w0 = __builtin_amdgcn_s_memtime();
         wait_vm<(WS == 3 ? 1 : 0) * WBLK>();
         wait_lds();
         barrier();
+        if constexpr (TL)
+            if ((ks & 7) == 3) {
+                tl_wait += __builtin_amdgcn_s_memtime() - tl_w0;
+                ++tl_samples;
+            }
         // eight groups of: two global->LDS loads (hidden rows of stage ks+2
         // in groups 0-3, weights of stage ks+WS in groups 4-7), two MFMAs of
         // this k-step, one fragment read of stage ks+1 (kept in this order:
@@ -324,6 +345,28 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     wait_vm<0>();
     barrier();                                   // the reduction area aliases the weight ring
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (TL) {
+        tl_loop1 = __builtin_amdgcn_s_memrealtime();
+        tl_c1 = __builtin_amdgcn_s_memtime();
+    }
+    // the timeline record of this wave (lane 0 stores it)
+    [[maybe_unused]] auto tl_record = [&]() {
+        const uint64_t tl_end = __builtin_amdgcn_s_memrealtime();
+        const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);    // HW_ID
+        const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);  // XCC_ID
+        if (lane == 0) {
+            uint64_t *rec = a.timeline + (a.timeline_base + static_cast<int64_t>(blockIdx.x) * 4 + wave) * kTimelineWords;
+            const uint64_t kind = MODE == kFwd ? 0 : MODE == kNarrow ? 1 : 2;
+            rec[0] = hw | (static_cast<uint64_t>(xcc & 0xff) << 32) | (kind << 40) | (static_cast<uint64_t>(wave) << 48);
+            rec[1] = tl_start;
+            rec[2] = tl_loop0;
+            rec[3] = tl_loop1;
+            rec[4] = tl_end;
+            rec[5] = tl_wait;
+            rec[6] = tl_c1 - tl_c0;
+            rec[7] = blockIdx.x | (static_cast<uint64_t>(nks) << 32) | (static_cast<uint64_t>(tl_samples) << 48);
+        }
+    };
 
     if constexpr (MODE == kBwdProbs) {
         // acc[tm][tn][i]: vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4,
@@ -417,9 +460,11 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                                      acc[tm][tn][4 * q + 3]};
                     *reinterpret_cast<f32x4 *>(a.part + part_elem(blockIdx.x, wave, tm, tn, q, lane)) = v;
                 }
+        if constexpr (TL) tl_record();
         return;
     }
     fwd_epilogue<TM>(a, acc, v0, vt, rt, red);
+    if constexpr (TL) tl_record();
 }
 
 // Sums the hidden-dimension parts of the tail tiles (in a fixed order) and
@@ -550,17 +595,24 @@ __global__ __launch_bounds__(kThreads) void logprob_combine_row_kernel(LogprobAr
 
 }  // namespace
 
-hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
+hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream, bool timeline) {
     // whole tiles [0, dp_tiles)
     LogprobArgs d = a;
     d.tile_base = 0;
     d.tile_count = a.dp_tiles;
-    if (tile_weight_stages(a.n_row_tiles) == 3)
-        hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd>), dim3(static_cast<uint32_t>(d.tile_count)),
-                           dim3(kTileThreads), 0, stream, d);
-    else
-        hipLaunchKernelGGL((logprob_tile_kernel<2, kFwd>), dim3(static_cast<uint32_t>(d.tile_count)),
-                           dim3(kTileThreads), 0, stream, d);
+    d.timeline_base = 0;
+    const uint32_t whole = static_cast<uint32_t>(d.tile_count);
+    if (tile_weight_stages(a.n_row_tiles) == 3) {
+        if (timeline)
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd, 4, true>), dim3(whole), dim3(kTileThreads), 0, stream, d);
+        else
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kFwd>), dim3(whole), dim3(kTileThreads), 0, stream, d);
+    } else {
+        if (timeline)
+            hipLaunchKernelGGL((logprob_tile_kernel<2, kFwd, 4, true>), dim3(whole), dim3(kTileThreads), 0, stream, d);
+        else
+            hipLaunchKernelGGL((logprob_tile_kernel<2, kFwd>), dim3(whole), dim3(kTileThreads), 0, stream, d);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.narrow_tiles > 0) {
@@ -569,7 +621,13 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
         // ring applies)
         static_assert(kNarrowWidth == 64 * 3, "narrow tile width");
         const uint32_t blocks = static_cast<uint32_t>(a.narrow_tiles * a.n_row_tiles);
-        hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, a);
+        LogprobArgs n = a;
+        n.timeline_base = a.dp_tiles * 4;
+        if (timeline)
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3, true>), dim3(blocks), dim3(kTileThreads), 0, stream,
+                               n);
+        else
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, n);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -578,11 +636,21 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream) {
         LogprobArgs t = a;
         t.tile_base = a.dp_tiles;
         t.tile_count = a.tail_tiles;
+        t.timeline_base = (a.dp_tiles + a.narrow_tiles * a.n_row_tiles) * 4;
         const uint32_t parts = static_cast<uint32_t>(a.tail_tiles * a.splits);
-        if (tile_weight_stages(a.n_row_tiles) == 3)
-            hipLaunchKernelGGL((logprob_tile_kernel<3, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
-        else
-            hipLaunchKernelGGL((logprob_tile_kernel<2, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+        if (tile_weight_stages(a.n_row_tiles) == 3) {
+            if (timeline)
+                hipLaunchKernelGGL((logprob_tile_kernel<3, kPartialK, 4, true>), dim3(parts), dim3(kTileThreads), 0,
+                                   stream, t);
+            else
+                hipLaunchKernelGGL((logprob_tile_kernel<3, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+        } else {
+            if (timeline)
+                hipLaunchKernelGGL((logprob_tile_kernel<2, kPartialK, 4, true>), dim3(parts), dim3(kTileThreads), 0,
+                                   stream, t);
+            else
+                hipLaunchKernelGGL((logprob_tile_kernel<2, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+        }
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(logprob_tail_reduce_kernel, dim3(static_cast<uint32_t>(a.tail_tiles * 8)), dim3(128), 0,

@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 9
+    assert lib.rl_abi_version() == 10
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -607,3 +607,29 @@ def test_noalloc_validation_before_any_hip_call():
     # the 8B-class and 32B-class decode-step rows fit
     assert rk.token_logprob_workspace_size(512, 4096, 151936) <= rk.NOALLOC_SCRATCH_BYTES
     assert rk.token_logprob_workspace_size(256, 5120, 151936) <= rk.NOALLOC_SCRATCH_BYTES
+
+
+# ---------------------------------------------------------------- tile timeline (debug)
+def test_timeline_size_query_and_validation():
+    lib = rk.lib()
+    n = ctypes.c_int64(-1)
+    fake = ctypes.c_void_p(FAKE)
+    # size query: no pointer but num_records is looked at, nothing launched
+    for R, H, V in [(256, 5120, 151936), (512, 4096, 151936), (300, 128, 20000), (8, 256, 1024)]:
+        assert lib.rl_debug_logprob_timeline(R, H, V, None, None, None, 1.0, None, None, None, 0, None, 0,
+                                             ctypes.byref(n), None) == OK
+        assert n.value > 0 and n.value % 4 == 0
+        assert rk.logprob_timeline_records(R, H, V) == n.value
+    # one 256-row tile per 256 vocab entries: every tile covered once, whole or in parts
+    assert rk.logprob_timeline_records(256, 5120, 151936) >= 4 * 594
+    assert lib.rl_debug_logprob_timeline(256, 5120, 151936, None, None, None, 1.0, None, None, None, 0, None, 0,
+                                         None, None) == NULLP
+    assert lib.rl_debug_logprob_timeline(8, 96, 1024, None, None, None, 1.0, None, None, None, 0, None, 0,
+                                         ctypes.byref(n), None) == UNSUP
+    need = rk.logprob_timeline_records(8, 256, 1024)
+    ws = rk.token_logprob_workspace_size(8, 256, 1024)
+    args = (8, 256, 1024, fake, fake, fake, 1.0, fake, fake, fake, ws)
+    assert lib.rl_debug_logprob_timeline(*args, ctypes.c_void_p(FAKE), need - 1, ctypes.byref(n), None) == WSPACE
+    assert lib.rl_debug_logprob_timeline(*args, ctypes.c_void_p(FAKE + 4), need, ctypes.byref(n), None) == MISAL
+    assert lib.rl_debug_logprob_timeline(8, 256, 1024, fake, fake, None, 1.0, fake, fake, fake, ws,
+                                         ctypes.c_void_p(FAKE), need, ctypes.byref(n), None) == NULLP

@@ -98,3 +98,37 @@ def test_source_hash_covers_included_headers():
     assert names[0] == "token_logprob.hip"
     assert {"lds_stage.h", "tile_index.h", "kernels.h"} <= set(names)
     assert "decode_attn.hip" in bench._local_sources("decode_attn.hip")
+
+
+def test_timeline_markdown_on_synthetic_records():
+    # 8 XCDs x 32 CUs, two rounds of whole tiles, then 100 tail parts
+    cus = [(x, se, sh, c) for x in range(8) for se in range(4) for sh in range(2) for c in range(4)]
+    recs, b = [], 0
+
+    def word0(x, se, sh, c, w, kind):
+        return (c << 8) | (sh << 12) | (se << 13) | (w << 4) | (x << 32) | (kind << 40) | (w << 48)
+
+    for rnd in range(2):
+        for (x, se, sh, c) in cus:
+            st = rnd * 16000 + b % 7
+            for w in range(4):
+                recs.append([word0(x, se, sh, c, w, 0), st, st + 300, st + 15500, st + 15800, 62500, 2000000,
+                             b | (80 << 32) | (10 << 48)])
+            b += 1
+    for i, (x, se, sh, c) in enumerate(cus[:100]):
+        st = 32000
+        for w in range(4):
+            recs.append([word0(x, se, sh, c, w, 2), st, st + 300, st + 4000, st + 4100, 10000, 740000,
+                         i | (20 << 32) | (2 << 48)])
+    md = bench.timeline_markdown(np.array(recs, dtype=np.int64), True, 2 * 151936 * 5120, "synthetic")
+    assert "bit-identical" in md
+    # first table: workgroups, stages, tile duration 158 us, loop 152 us, 1900 ns per stage,
+    # wait share 0.25, 2e6 cycles over 152 us = 13.158 GHz
+    whole = [l for l in md.splitlines() if l.startswith("| whole tiles | 512")][0].split("|")
+    assert whole[3].strip() == "80" and whole[5].strip() == "158.0/158.0/158.0"
+    assert whole[9].strip() == "1900" and whole[10].strip() == "0.250" and whole[11].strip() == "13.158"
+    # per-CU table: 256 CUs with 2 tiles each, 100 CUs with one part
+    per_cu = [l for l in md.splitlines() if l.startswith("| whole tiles | 256")]
+    assert per_cu and "2: 256 CUs" in per_cu[0]
+    assert any(l.startswith("| tail parts | 100 |") and "1: 100 CUs" in l for l in md.splitlines())
+    assert "361.0 us from the first start" in md

@@ -196,3 +196,38 @@ def test_full_size_workloads(name, ntiles):
     say(f"logprob full-size {name}: logprob max-abs {e1:.3g}, lse max-abs {e2:.3g}")
     assert e1 <= LOGPROB_TOL and e2 <= LOGPROB_TOL
     assert torch.isfinite(lp).all() and torch.isfinite(lse).all()
+
+
+@pytest.mark.parametrize("R,H,V", [(256, 5120, 151936), (512, 4096, 151936), (300, 128, 20000)])
+def test_timeline_same_outputs_and_complete_records(R, H, V):
+    """rl_debug_logprob_timeline: the same log-prob and lse as rl_token_logprob
+    bit for bit (the instrumented kernels do the same arithmetic), and one
+    record per wave of every tile launch, with ordered timestamps.  The shapes:
+    32B-class rows (whole tiles + tail parts), 8B-class rows (whole tiles +
+    narrow last round) and a ragged small shape."""
+    say(f"timeline {R}x{H}x{V}")
+    x = W.make_logprob_inputs(W.LogprobConfig("t", R, H, V), dev())
+    lp0, lse0 = rk.token_logprob(x.hidden, x.w_lm, x.target, x.inv_temperature)
+    lp, lse, rec = rk.token_logprob_timeline(x.hidden, x.w_lm, x.target, x.inv_temperature)
+    torch.cuda.synchronize()
+    assert torch.equal(lp, lp0) and torch.equal(lse, lse0)
+    r = rec.cpu().numpy()
+    assert len(r) == rk.logprob_timeline_records(R, H, V)
+    kind, wave, blk = (r[:, 0] >> 40) & 0xFF, (r[:, 0] >> 48) & 0xFF, r[:, 7] & 0xFFFFFFFF
+    xcc = (r[:, 0] >> 32) & 0xFF
+    assert set(kind.tolist()) <= {0, 1, 2} and (xcc < 8).all()
+    # record 4 b + w of each launch is workgroup b, wave w
+    for k in set(kind.tolist()):
+        m = kind == k
+        n = int(m.sum())
+        assert n % 4 == 0
+        assert (blk[m] == np.arange(n) // 4).all() and (wave[m] == np.arange(n) % 4).all()
+    st, l0, l1, en = (r[:, i] for i in range(1, 5))
+    assert (st > 0).all() and (st <= l0).all() and (l0 <= l1).all() and (l1 <= en).all()
+    assert (r[:, 5] <= r[:, 6]).all() and (r[:, 6] > 0).all()     # stage-end waits within the loop's cycles
+    stages, samples = (r[:, 7] >> 32) & 0xFFFF, r[:, 7] >> 48
+    assert (stages > 0).all() and (samples == (stages + 4) // 8).all()   # stages 3, 11, 19, ... sampled
+    if R == 256:
+        assert {0, 2} <= set(kind.tolist())
+    if R == 512:
+        assert {0, 1} <= set(kind.tolist())
