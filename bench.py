@@ -642,11 +642,12 @@ def timeline_markdown(r: np.ndarray, same: bool, wbytes: int, desc: str, plain_m
            "One call of rl_debug_logprob_timeline (the tile launches of rl_token_logprob with per-wave "
            "timestamps; the log-prob and lse it returned are "
            f"{'bit-identical to' if same else 'NOT identical to'} rl_token_logprob's), after a 1 GiB read that "
-           "empties the caches.  Wall clock: s_memrealtime (100 MHz); cycles: s_memtime.  Per workgroup the "
+           "empties the caches.  Wall clock: s_memrealtime (100 MHz); cycles: s_memtime (its rate is not the shader "
+           "clock's: compare the MFMA-busy counters).  Per workgroup the "
            "earliest start and the latest end of its 4 waves; waits and cycles averaged over the waves.  The stage-end "
            "wait (loads of the next stage, then the barrier) is sampled in one stage of every 8.", "",
            "| launch | workgroups | stages | first start - last end (us) | tile us p10/p50/p90 | "
-           "prologue us | loop us | epilogue us | ns per stage | stage-end wait share | clock (cycles per ns, GHz) |",
+           "prologue us | loop us | epilogue us | ns per stage | stage-end wait share | s_memtime cycles per ns |",
            "|---|---:|---:|---|---|---|---|---|---:|---:|---:|"]
     per_kind = {}
     for k in sorted(set(kind.tolist())):

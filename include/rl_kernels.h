@@ -545,10 +545,11 @@ rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t hidden, int3
  *   [2] wall clock when its first stage has landed (the loop starts)
  *   [3] wall clock at the end of the loop
  *   [4] wall clock after the epilogue
- *   [5] shader-clock cycles (s_memtime) spent in the stage-end waits (the
+ *   [5] s_memtime cycles spent in the stage-end waits (the
  *       loads of the next stage, then the workgroup barrier) of the sampled
  *       stages, those whose index is 3 mod 8
- *   [6] shader-clock cycles of the loop
+ *   [6] s_memtime cycles of the loop (s_memtime counts at a rate of its
+ *       own, not the shader clock)
  *   [7] workgroup index | hidden-dimension stages << 32 | sampled stages << 48
  * Whole-tile workgroup b, wave w writes record 4 b + w; the narrow tiles and
  * then the tail parts follow in the same way.  *num_records gets the number

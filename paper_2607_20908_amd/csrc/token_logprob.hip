@@ -181,7 +181,7 @@ __device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 
 // (kNarrow) and the sampling head's logits (kLogits)).
 // TL: debug build with a timeline record per wave (forward modes only): wall
 // clock at the start, at the loop's start and end and after the epilogue,
-// shader-clock cycles of the loop, and the cycles of the stage-end wait in one
+// s_memtime cycles of the loop, and the cycles of the stage-end wait in one
 // stage of every 8 (a sample: each stamp makes the wave wait for the scalar
 // read that returns it).  The same arithmetic as TL = false.
 template <int WS, int MODE, int TM = 4, bool TL = false>
