@@ -16,11 +16,12 @@
 //      unit; the last also holds everything further below m, whose mass is
 //      at most 2^40 e^-64 < 1, i.e. 0) -> the bucket B where the ranked mass
 //      crosses T;
-//   2. gather the tokens of B (refined by 8-bit key digits first if B holds
-//      more than kCap of them), sort them by (key desc, id asc) in LDS and
-//      walk their masses to tau and k;
-//   3. per chunk of 2048 ids: nucleus mass and count of key-tau tokens;
-//      then the chunk holding the sample is rescanned in id order.
+//   2. per chunk of 2048 ids the mass of the buckets above B, and the tokens
+//      of B gathered, sorted by (key desc, id asc) in LDS and their masses
+//      walked to tau and k; if B holds more than kCap tokens, further passes
+//      refine it by 8-bit key digits first and recount each chunk's nucleus
+//      mass and key-tau tokens;
+//   3. the chunk holding the sample is rescanned in id order.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -85,7 +86,6 @@ struct SelShared {
         } chunk;                                    // (once the histograms are no longer read)
     } a;
     union {
-        uint32_t bcount[kBuckets];                  // tokens per bucket
         uint64_t cand[kCap];                        // (key << 32) | ~id of the candidates
     } b;
     uint32_t dcount[256];                           // tokens per key digit
@@ -123,9 +123,9 @@ __device__ uint64_t block_excl_scan(SelShared &sh, uint64_t v, uint64_t *excl) {
 }
 
 // Calls f(v, y_v) for the ids of float4 groups g0, g0 + step, ... below g1
-// (ids < V only), with four groups' loads in flight: the passes are bound by
+// (ids < V only), with DEPTH groups' loads in flight: the passes are bound by
 // how many bytes each CU keeps in flight against the HBM latency.
-template <typename F>
+template <int DEPTH, typename F>
 __device__ __forceinline__ void scan_groups(const float *y, int V, int g0, int g1, int step, F &&f) {
     auto visit = [&](const float4 q4, int g) {
         const float yy[4] = {q4.x, q4.y, q4.z, q4.w};
@@ -134,12 +134,12 @@ __device__ __forceinline__ void scan_groups(const float *y, int V, int g0, int g
             if (4 * g + e < V) f(4 * g + e, yy[e]);
     };
     int g = g0;
-    for (; g + 3 * step < g1; g += 4 * step) {
-        float4 q[4];
+    for (; g + (DEPTH - 1) * step < g1; g += DEPTH * step) {
+        float4 q[DEPTH];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) q[j] = *reinterpret_cast<const float4 *>(y + 4 * (g + j * step));
+        for (int j = 0; j < DEPTH; ++j) q[j] = *reinterpret_cast<const float4 *>(y + 4 * (g + j * step));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) visit(q[j], g + j * step);
+        for (int j = 0; j < DEPTH; ++j) visit(q[j], g + j * step);
     }
     for (; g < g1; g += step) visit(*reinterpret_cast<const float4 *>(y + 4 * g), g);
 }
@@ -199,7 +199,13 @@ __device__ void sort_and_walk(SelShared &sh, uint32_t ncand, uint64_t above, uin
     __syncthreads();
 }
 
-__global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
+// DEPTH: float4 loads in flight per lane in the passes; WPE: waves per SIMD
+// the build allows.  More than 256 rows: 8 waves per SIMD, so two rows share
+// a CU (the LDS fits two workgroups) and one row's serial steps overlap the
+// other's passes, at 64 registers and 4 loads per lane.  Up to 256 rows each
+// CU holds one row anyway, so its lanes keep 8 loads in flight instead.
+template <int DEPTH, int WPE>
+__global__ __launch_bounds__(kThreads, WPE) void sample_top_p_kernel(SampleArgs a) {
     __shared__ SelShared sh;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t r = blockIdx.x;
@@ -213,40 +219,31 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     for (int t = tid; t < a.n_partials; t += kThreads) m = fmaxf(m, a.pm[static_cast<int64_t>(t) * a.rows + r]);
     m = wave_max(m);
     if (lane == 0) sh.fred[wave] = m;
-    for (int i = tid; i < kBuckets; i += kThreads) {
-        sh.a.hist[i] = 0;
-        sh.b.bcount[i] = 0;
-    }
+    for (int i = tid; i < kBuckets; i += kThreads) sh.a.hist[i] = 0;
     __syncthreads();
     for (int w = 0; w < kWaves; ++w) m = fmaxf(m, sh.fred[w]);
 
-    // ---- pass 1: bucket masses and counts, and the total mass
-    uint64_t zloc = 0;
-    scan_groups(y, V, tid, nvec, kThreads, [&](int, float yv) {
-        const int b = bucket_of(yv, m);
+    // ---- pass 1: bucket masses (a bucket's token count is not needed: pass 2
+    // gathers the tokens of one bucket and counts them as it goes)
+    scan_groups<DEPTH>(y, V, tid, nvec, kThreads, [&](int, float yv) {
         const uint64_t q = qmass(yv, m);
-        if (q) {
-            atomicAdd(reinterpret_cast<unsigned long long *>(&sh.a.hist[b]), static_cast<unsigned long long>(q));
-            zloc += q;
-        }
-        atomicAdd(&sh.b.bcount[b], 1u);
+        if (q)
+            atomicAdd(reinterpret_cast<unsigned long long *>(&sh.a.hist[bucket_of(yv, m)]),
+                      static_cast<unsigned long long>(q));
     });
-    zloc = wave_sum_int(zloc);
-    if (lane == 0) sh.zsum[wave] = zloc;
     __syncthreads();
-    uint64_t Z = 0;
-    for (int w = 0; w < kWaves; ++w) Z += sh.zsum[w];
-    uint64_t T = a.top_p >= 1.f ? Z : static_cast<uint64_t>(ceil(static_cast<double>(a.top_p) * static_cast<double>(Z)));
-    if (T < 1) T = 1;
-    if (T > Z) T = Z;
 
-    // ---- the bucket where the ranked mass reaches T (buckets run from the max down)
+    // ---- the total mass Z (the histogram's sum) and the bucket where the
+    // ranked mass reaches T (buckets run from the max down)
     constexpr int kPer = kBuckets / kThreads;
     uint64_t mine = 0;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) mine += sh.a.hist[tid * kPer + j];
     uint64_t before;
-    block_excl_scan(sh, mine, &before);
+    const uint64_t Z = block_excl_scan(sh, mine, &before);
+    uint64_t T = a.top_p >= 1.f ? Z : static_cast<uint64_t>(ceil(static_cast<double>(a.top_p) * static_cast<double>(Z)));
+    if (T < 1) T = 1;
+    if (T > Z) T = Z;
     if (tid == 0) {                              // defaults, in range, for a degenerate row
         sh.part[0] = 0;
         sh.zsum[0] = kBuckets - 1;
@@ -262,34 +259,38 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     __syncthreads();
     uint64_t above = sh.part[0];
     const int B = static_cast<int>(sh.zsum[0]);
-    uint32_t ncand = sh.b.bcount[B];
-    __syncthreads();                             // histograms and counts are free from here
+    if (tid == 0) sh.ncand = 0;
+    __syncthreads();                             // the histogram is free from here
+
+    // ---- pass 2: per chunk of ids the mass of the buckets above B, and the
+    // tokens of B gathered for sorting (at most kCap of them stored; the
+    // counter keeps counting past kCap)
+    for (int c = wave; c < nchunks; c += kWaves) {
+        uint64_t ms = 0;
+        scan_groups<DEPTH>(y, V, c * (kChunk / 4) + lane, min(nvec, (c + 1) * (kChunk / 4)), 64, [&](int v, float yv) {
+            const int b = bucket_of(yv, m);
+            if (b < B) {
+                ms += qmass(yv, m);
+            } else if (b == B) {
+                const uint32_t slot = atomicAdd(&sh.ncand, 1u);
+                if (slot < kCap)
+                    sh.b.cand[slot] = (static_cast<uint64_t>(fkey(yv)) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(v));
+            }
+        });
+        ms = wave_sum_int(ms);
+        if (lane == 0) {
+            sh.a.chunk.mass[c] = ms;
+            sh.a.chunk.ties[c] = 0;
+        }
+    }
+    __syncthreads();
+    uint32_t ncand = sh.ncand;                   // tokens in bucket B
+    __syncthreads();
 
     uint32_t tau;
     uint64_t k;
     if (ncand <= kCap) {
-        // ---- fast path, one more pass: per chunk of ids the mass of the
-        // buckets above B, and the tokens of B gathered for sorting
-        if (tid == 0) sh.ncand = 0;
-        __syncthreads();
-        for (int c = wave; c < nchunks; c += kWaves) {
-            uint64_t ms = 0;
-            scan_groups(y, V, c * (kChunk / 4) + lane, min(nvec, (c + 1) * (kChunk / 4)), 64, [&](int v, float yv) {
-                const int b = bucket_of(yv, m);
-                if (b < B) {
-                    ms += qmass(yv, m);
-                } else if (b == B) {
-                    const uint32_t slot = atomicAdd(&sh.ncand, 1u);
-                    sh.b.cand[slot] = (static_cast<uint64_t>(fkey(yv)) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(v));
-                }
-            });
-            ms = wave_sum_int(ms);
-            if (lane == 0) {
-                sh.a.chunk.mass[c] = ms;
-                sh.a.chunk.ties[c] = 0;
-            }
-        }
-        __syncthreads();
+        // ---- fast path: sort the gathered tokens
         sort_and_walk(sh, ncand, above, T, m, &tau, &k);
         // the candidates complete the chunk masses (key above tau) and tie counts
         for (int i = tid; i < static_cast<int>(ncand); i += kThreads) {
@@ -319,7 +320,7 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
                 sh.dcount[i] = 0;
             }
             __syncthreads();
-            scan_groups(y, V, tid, nvec, kThreads, [&](int, float yv) {
+            scan_groups<DEPTH>(y, V, tid, nvec, kThreads, [&](int, float yv) {
                 const uint32_t kk = fkey(yv);
                 if (bucket_of(yv, m) == B && (shift == 32 || (kk >> shift) == prefix)) {
                     const int d = (kk >> s2) & 255;
@@ -354,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
         } else {
             if (tid == 0) sh.ncand = 0;
             __syncthreads();
-            scan_groups(y, V, tid, nvec, kThreads, [&](int v, float yv) {
+            scan_groups<DEPTH>(y, V, tid, nvec, kThreads, [&](int v, float yv) {
                 const uint32_t kk = fkey(yv);
                 if (bucket_of(yv, m) == B && (kk >> shift) == prefix) {
                     const uint32_t slot = atomicAdd(&sh.ncand, 1u);
@@ -368,7 +369,7 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
         for (int c = wave; c < nchunks; c += kWaves) {
             uint64_t ms = 0;
             uint32_t nt = 0;
-            scan_groups(y, V, c * (kChunk / 4) + lane, min(nvec, (c + 1) * (kChunk / 4)), 64, [&](int, float yv) {
+            scan_groups<DEPTH>(y, V, c * (kChunk / 4) + lane, min(nvec, (c + 1) * (kChunk / 4)), 64, [&](int, float yv) {
                 const uint32_t kk = fkey(yv);
                 if (kk > tau) ms += qmass(yv, m);
                 nt += kk == tau;
@@ -384,38 +385,58 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
     }
 
     const uint64_t qt = qmass(key_to_float(tau), m);
-    if (tid == 0) {
+    // ---- the nucleus mass per chunk of ids: its members above tau plus the
+    // key-tau tokens among the first k of them in id order; then the chunk
+    // where the running mass passes U = floor(u Z_N).  Wave 0, 64 chunks at
+    // a time, with wave scans of the tie counts and masses.
+    if (wave == 0) {
+        auto chunk_mass = [&](int c0, uint64_t tb, uint64_t *ti, uint64_t *tbx, uint64_t *mc) {
+            const int c = c0 + lane;
+            const uint64_t t = c < nchunks ? sh.a.chunk.ties[c] : 0;
+            *ti = wave_incl_scan(t, lane);
+            *tbx = tb + *ti - t;                                   // key-tau tokens in earlier chunks
+            const uint64_t inc = min(t, k > *tbx ? k - *tbx : 0);
+            *mc = c < nchunks ? sh.a.chunk.mass[c] + inc * qt : 0;
+        };
         uint64_t zn = 0, tb = 0;
-        for (int c = 0; c < nchunks; ++c) {
-            const uint64_t inc = min(static_cast<uint64_t>(sh.a.chunk.ties[c]), k > tb ? k - tb : 0);
-            zn += sh.a.chunk.mass[c] + inc * qt;
-            tb += sh.a.chunk.ties[c];
+        for (int c0 = 0; c0 < nchunks; c0 += 64) {
+            uint64_t ti, tbx, mc;
+            chunk_mass(c0, tb, &ti, &tbx, &mc);
+            zn += wave_sum_int(mc);
+            tb += __shfl(ti, 63, 64);
         }
         uint64_t U = static_cast<uint64_t>(floor(static_cast<double>(a.uniform[r]) * static_cast<double>(zn)));
         if (!(U < zn)) U = zn ? zn - 1 : 0;
-        // chunk holding the sample
         uint64_t cum = 0;
         tb = 0;
-        int cs = nchunks - 1;
+        int cs = -1;
         uint64_t tb_cs = 0, cum_cs = 0;
-        for (int c = 0; c < nchunks; ++c) {
-            const uint64_t inc = min(static_cast<uint64_t>(sh.a.chunk.ties[c]), k > tb ? k - tb : 0);
-            const uint64_t mc = sh.a.chunk.mass[c] + inc * qt;
-            if (cum + mc > U) {
-                cs = c;
-                tb_cs = tb;
-                cum_cs = cum;
+        for (int c0 = 0; c0 < nchunks; c0 += 64) {
+            uint64_t ti, tbx, mc;
+            chunk_mass(c0, tb, &ti, &tbx, &mc);
+            const uint64_t mi = wave_incl_scan(mc, lane);
+            const uint64_t hits = __ballot(c0 + lane < nchunks && cum + mi > U);   // the running mass passes U
+            if (hits) {
+                const int src = __builtin_ctzll(hits);
+                cs = c0 + src;
+                tb_cs = __shfl(tbx, src, 64);
+                cum_cs = cum + __shfl(mi - mc, src, 64);
                 break;
             }
-            cum += mc;
-            tb += sh.a.chunk.ties[c];
+            cum += __shfl(mi, 63, 64);
+            tb += __shfl(ti, 63, 64);
+        }
+        if (cs < 0) {                            // no chunk passes U (a row without mass)
+            cs = nchunks - 1;
             tb_cs = tb;
             cum_cs = cum;
         }
-        sh.part[0] = static_cast<uint64_t>(cs);
-        sh.part[1] = tb_cs;
-        sh.part[2] = U - min(U, cum_cs);
-        sh.part[3] = zn;
+        if (lane == 0) {
+            sh.part[0] = static_cast<uint64_t>(cs);
+            sh.part[1] = tb_cs;
+            sh.part[2] = U - min(U, cum_cs);
+            sh.part[3] = zn;
+        }
     }
     __syncthreads();
 
@@ -499,7 +520,12 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(SampleArgs a) {
 
 hipError_t launch_sample_top_p(const SampleArgs &a, hipStream_t stream) {
     if (a.rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(sample_top_p_kernel, dim3(static_cast<uint32_t>(a.rows)), dim3(kThreads), 0, stream, a);
+    if (a.rows > 256)
+        hipLaunchKernelGGL((sample_top_p_kernel<4, 8>), dim3(static_cast<uint32_t>(a.rows)), dim3(kThreads), 0, stream,
+                           a);
+    else
+        hipLaunchKernelGGL((sample_top_p_kernel<8, 4>), dim3(static_cast<uint32_t>(a.rows)), dim3(kThreads), 0, stream,
+                           a);
     return hipGetLastError();
 }
 
