@@ -231,3 +231,15 @@ def test_timeline_same_outputs_and_complete_records(R, H, V):
         assert {0, 2} <= set(kind.tolist())
     if R == 512:
         assert {0, 1} <= set(kind.tolist())
+
+
+def test_vocabulary_of_two_million():
+    """vocab = 2^21: 8192 vocabulary tiles, so each row's combine merges 8192
+    partial slots; targets include a masked row and the last id."""
+    rng = np.random.Generator(np.random.PCG64(2021))
+    R, H, V = 8, 64, 1 << 21
+    h, w = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.05)
+    t = rng.integers(0, V, R).astype(np.int32)
+    t[0], t[-1] = -1, V - 1
+    lp, _ = check(h, w, t, 1.0, "vocab 2^21")
+    assert lp[0] == 0.0

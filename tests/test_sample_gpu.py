@@ -221,3 +221,13 @@ def test_full_size_decode_shapes(name, nsample):
     say(f"sampling full-size {name}: oracle on {len(rows)} rows")
     got, _ = check(hb, wb, it, x.top_p, u, f"full-size {name} (rows recomputed)")
     assert np.array_equal(got, tok[idx].cpu().numpy()), "row subset differs from the full batch"
+
+
+def test_maximum_vocabulary():
+    """vocab = 2^21, the largest the sampling head takes: 1024 chunks of ids,
+    so the draw's chunk walk (64 chunks at a time) runs 16 rounds."""
+    rng = np.random.Generator(np.random.PCG64(21))
+    R, H, V = 3, 64, 1 << 21
+    hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), 0.3)
+    inv_t = np.array([1 / 0.7, 1.0, 1 / 0.2], np.float32)
+    check(hb, wb, inv_t, 0.9, rng.random(R, dtype=np.float32), "maximum vocabulary")
