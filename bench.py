@@ -690,6 +690,98 @@ def timeline_markdown(r: np.ndarray, same: bool, wbytes: int, desc: str, plain_m
     return "\n".join(out) + "\n"
 
 
+def decode_timeline_report(rk, x, evict, kv_layout: str, desc: str) -> str:
+    """The split kernel of one decode-attention call, one record per work item
+    from rl_debug_decode_timeline (after the same cache eviction as the timed
+    operations), summarised as markdown."""
+    c = x.cfg
+    args = (x.q, x.k_prefix, x.v_prefix, x.k_suffix, x.v_suffix, x.prefix_start, x.prefix_len, x.suffix_start,
+            x.suffix_len, c.group_size)
+    plain = lambda: rk.decode_attn(*args, scale=x.scale, return_lse=True, kv_layout=kv_layout)
+    stamped = lambda: rk.decode_attn_timeline(*args, scale=x.scale, kv_layout=kv_layout)
+    for _ in range(2):
+        plain()
+        stamped()
+    ms = {"plain": [], "stamped": []}
+    for _ in range(5):
+        for name, f in (("plain", plain), ("stamped", stamped)):
+            evict()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            res = f()
+            e1.record()
+            torch.cuda.synchronize()
+            ms[name].append(e0.elapsed_time(e1))
+    o, l, rec = res                         # the last stamped call's
+    ro, rl = plain()
+    same = bool(torch.equal(o.view(torch.int16), ro.view(torch.int16)) and torch.equal(l, rl))
+    return decode_timeline_markdown(rec.cpu().numpy(), same, 4 * c.head_dim, decode_bytes(x), desc,
+                                    float(np.median(ms["plain"])), float(np.median(ms["stamped"])))
+
+
+def decode_timeline_markdown(r: np.ndarray, same: bool, token_bytes: int, alg_bytes: int, desc: str,
+                             plain_ms: float = None, stamped_ms: float = None) -> str:
+    """Markdown summary of decode timeline records (int64 [n, 8], one per work
+    item; word layout in rl_kernels.h).  token_bytes: K and V bytes of one
+    token at one kv head; alg_bytes: the call's algorithmic bytes."""
+    hw = r[:, 0] & 0xFFFFFFFF
+    xcc = (r[:, 0] >> 32) & 0xFF
+    kind = (r[:, 0] >> 40) & 0xFF
+    rows = (r[:, 0] >> 48) & 0xFFFF
+    st, first, loop1, en = (r[:, i] for i in range(1, 5))
+    ntok, tiles = r[:, 5] & 0xFFFFFFFF, r[:, 5] >> 32
+    cu = xcc * 256 + ((hw >> 13) & 7) * 32 + ((hw >> 12) & 1) * 16 + ((hw >> 8) & 0xF)
+    t0 = int(st.min())
+    span = (int(en.max()) - t0) * 0.01
+    q = lambda v: "/".join(f"{np.percentile(v, p):.1f}" for p in (10, 50, 90)) if len(v) else "-"
+    out = [f"# Decode split kernel timeline: {desc}", "",
+           "One call of rl_debug_decode_timeline (rl_decode_attn with the split kernel built to leave one "
+           "record per work item; the output and lse it returned are "
+           f"{'bit-identical to' if same else 'NOT identical to'} rl_decode_attn's), after a 1 GiB read that "
+           "empties the caches.  Wall clock: s_memrealtime (100 MHz).  The work list runs in its planned order "
+           "(longest items first).", "",
+           "| items | query rows | count | KV tokens p10/p50/p90 | item us p10/p50/p90 | first tile us | "
+           "ns per 64-token tile | partials us | KV GB |",
+           "|---|---:|---:|---|---|---|---:|---|---:|"]
+    for k, name in ((0, "prefix"), (1, "suffix")):
+        m = kind == k
+        if not m.any():
+            continue
+        for rr in np.unique(rows[m]):
+            mm = m & (rows == rr)
+            loop_ns = (loop1[mm] - first[mm]) * 10.0
+            out.append(f"| {name} | {rr} | {int(mm.sum())} | {q(ntok[mm])} | {q((en[mm] - st[mm]) * 0.01)} | "
+                       f"{q((first[mm] - st[mm]) * 0.01)} | {np.median(loop_ns / np.maximum(tiles[mm], 1)):.0f} | "
+                       f"{q((en[mm] - loop1[mm]) * 0.01)} | {ntok[mm].sum() * token_bytes / 1e9:.3f} |")
+    # occupancy: items resident per CU over the span
+    ncu = len(np.unique(cu))
+    busy = (en - st).sum() * 0.01
+    events = np.concatenate([np.stack([st, np.ones_like(st)], 1), np.stack([en, -np.ones_like(en)], 1)])
+    events = events[np.lexsort((events[:, 1], events[:, 0]))]
+    resident = np.cumsum(events[:, 1])
+    times = (events[:, 0] - t0) * 0.01
+    # the last moment every CU still holds an item, from the per-CU last ends
+    cu_last = np.array([en[cu == c].max() for c in np.unique(cu)])
+    tails = (en.max() - cu_last) * 0.01
+    peak = int(resident.max())
+    out += ["", f"Span (first start to last end): {span:.1f} us over {ncu} CUs; the algorithmic "
+            f"{alg_bytes / 1e9:.3f} GB over the span stream at {alg_bytes / (span * 1e-6) / 1e9:.0f} GB/s.  "
+            f"Items resident at once: at most {peak} ({peak / ncu:.2f} per CU), on average "
+            f"{busy / span / ncu:.2f} per CU.  The last item starts at {(st.max() - t0) * 0.01:.1f} us; "
+            f"the CUs' idle tails (a CU's last end to the kernel's) are {q(tails)} us (p10/p50/p90).  "
+            f"Last end per XCD (us): "
+            + " ".join(f"{(en[xcc == i].max() - t0) * 0.01:.0f}" for i in range(8) if (xcc == i).any()) + "."]
+    late = int(np.argmax(en))
+    out += ["", f"The item that ends last: {'suffix' if kind[late] else 'prefix'}, {rows[late]} rows, "
+            f"{ntok[late]} tokens, started at {(st[late] - t0) * 0.01:.1f} us and took "
+            f"{(en[late] - st[late]) * 0.01:.1f} us."]
+    if plain_ms is not None:
+        out += ["", f"Whole call by events (medians of 5, each after the eviction; both entry points "
+                f"alternately): rl_decode_attn {plain_ms * 1e3:.1f} us, rl_debug_decode_timeline "
+                f"{stamped_ms * 1e3:.1f} us."]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -715,6 +807,9 @@ def main():
     ap.add_argument("--timeline", default="",
                     help="write a markdown summary of the headline lm-head's tile launches (per-wave timestamps "
                          "from rl_debug_logprob_timeline) to this file")
+    ap.add_argument("--decode-timeline", default="",
+                    help="write a markdown summary of the headline decode attention's split kernel (one record per "
+                         "work item from rl_debug_decode_timeline) to this file")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy before the steps (outside the timed region) so a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -755,6 +850,10 @@ def main():
 
     head, t, (x, y, ops, lse2) = measure_workload(rk, W, args.workload, args, timer, dev, args.steps, args.warmup,
                                                   args.cpu_budget, keep=True)
+    if args.decode_timeline and x is not None:
+        with open(args.decode_timeline, "w") as f:
+            f.write(decode_timeline_report(rk, x, evict, args.kv_layout, head["workload"]))
+        log(f"bench: decode timeline written to {args.decode_timeline}")
     if args.timeline and y is not None:
         with open(args.timeline, "w") as f:
             f.write(timeline_report(rk, y, evict, head["workload"]))

@@ -80,7 +80,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 10
+#define RL_ABI_VERSION 11
 
 typedef enum {
     RL_OK = 0,
@@ -565,6 +565,31 @@ rl_status rl_debug_logprob_timeline(int64_t rows, int32_t hidden, int32_t vocab,
                                     const void *w_lm, const int32_t *target, float inv_temperature,
                                     float *logprob, float *lse, void *workspace, size_t workspace_bytes,
                                     uint64_t *records, int64_t capacity, int64_t *num_records, void *stream);
+
+/*
+ * Debug timeline of rl_decode_attn, to see where the split kernel's time
+ * goes: the same call (arguments, plan, outputs and arithmetic), with the
+ * split kernel built to leave one record of RL_TIMELINE_WORDS uint64 per work
+ * item, item i at records + i * RL_TIMELINE_WORDS (device memory, 8-byte
+ * aligned, `capacity` records):
+ *   [0] HW_ID register | XCC id << 32 | kind (0 prefix item, 1 suffix item)
+ *       << 40 | query rows << 48
+ *   [1] wall clock when the item's workgroup starts   (s_memrealtime, 100 MHz)
+ *   [2] wall clock once its first KV tile is in LDS
+ *   [3] wall clock at the end of its loop over tiles
+ *   [4] wall clock after its partials are written
+ *   [5] KV tokens | tiles << 32
+ *   [6] work-item index
+ *   [7] s_memtime cycles of the loop
+ * *num_records gets the number of work items; with records == NULL only that
+ * number is computed (host-only planning; shape and lens are checked, no
+ * pointer).  Status: as rl_decode_attn, plus RL_ERR_NULL_POINTER for a NULL
+ * num_records, RL_ERR_WORKSPACE when capacity is short and
+ * RL_ERR_MISALIGNED for misaligned records.
+ */
+rl_status rl_debug_decode_timeline(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                                   const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
+                                   uint64_t *records, int64_t capacity, int64_t *num_records, void *stream);
 
 #ifdef __cplusplus
 }

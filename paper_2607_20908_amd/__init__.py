@@ -96,7 +96,7 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
            "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds",
-           "rl_token_logprob_noalloc", "rl_debug_logprob_timeline"]
+           "rl_token_logprob_noalloc", "rl_debug_logprob_timeline", "rl_debug_decode_timeline"]
 
 
 def _load():
@@ -145,10 +145,12 @@ def _load():
     lib.rl_debug_logprob_bounds.argtypes = [I32, I64, I32, I32, I32, I32, ctypes.POINTER(BoundsReport)]
     lib.rl_token_logprob_noalloc.restype = ctypes.c_int
     lib.rl_token_logprob_noalloc.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P]
+    lib.rl_debug_decode_timeline.restype = ctypes.c_int
+    lib.rl_debug_decode_timeline.argtypes = [P, P, P, P, ctypes.c_size_t, P, I64, ctypes.POINTER(ctypes.c_int64), P]
     lib.rl_debug_logprob_timeline.restype = ctypes.c_int
     lib.rl_debug_logprob_timeline.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P, I64,
                                               ctypes.POINTER(ctypes.c_int64), P]
-    if lib.rl_abi_version() != 10:
+    if lib.rl_abi_version() != 11:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -325,20 +327,9 @@ def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_suffix: torch.Tensor, 
                              workspace.numel(), _stream_handle(stream)), "rl_kv_append")
 
 
-@_on_call_stream
-def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
-                k_suffix: torch.Tensor, v_suffix: torch.Tensor,
-                prefix_start, prefix_len, suffix_start, suffix_len, group_size: int,
-                scale: Optional[float] = None, split_tokens: int = 0, return_lse: bool = False,
-                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-                workspace: Optional[torch.Tensor] = None, stream=None, kv_layout: str = "token"):
-    """Decode attention of P*G candidates over their prompt's prefix KV ++ own suffix KV.
-
-    q [P*G, Hq, D] bf16; k/v_prefix and k/v_suffix bf16 device tensors laid out
-    [rows, Hkv, D] (kv_layout="token") or [Hkv, rows, D] (kv_layout="head");
-    prefix_start/len [P], suffix_start/len [P*G] host integers.
-    Returns out [P*G, Hq, D] bf16 (and lse [P*G, Hq] fp32 natural log).
-    """
+def _decode_prepare(q, k_prefix, v_prefix, k_suffix, v_suffix, prefix_start, prefix_len, suffix_start, suffix_len,
+                    group_size, scale, split_tokens, return_lse, out, lse, workspace, kv_layout):
+    """Validation and marshalling shared by decode_attn and decode_attn_timeline."""
     for t, n in ((q, "q"), (k_prefix, "k_prefix"), (v_prefix, "v_prefix"),
                  (k_suffix, "k_suffix"), (v_suffix, "v_suffix")):
         _bf16_dev(t, n)
@@ -380,10 +371,53 @@ def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
                       k_suffix.data_ptr() if k_suffix.numel() else None,
                       v_suffix.data_ptr() if v_suffix.numel() else None,
                       out.data_ptr(), lse.data_ptr() if lse is not None else None)
+    return a, out, lse, workspace, ptrs
+
+
+@_on_call_stream
+def decode_attn(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
+                k_suffix: torch.Tensor, v_suffix: torch.Tensor,
+                prefix_start, prefix_len, suffix_start, suffix_len, group_size: int,
+                scale: Optional[float] = None, split_tokens: int = 0, return_lse: bool = False,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, stream=None, kv_layout: str = "token"):
+    """Decode attention of P*G candidates over their prompt's prefix KV ++ own suffix KV.
+
+    q [P*G, Hq, D] bf16; k/v_prefix and k/v_suffix bf16 device tensors laid out
+    [rows, Hkv, D] (kv_layout="token") or [Hkv, rows, D] (kv_layout="head");
+    prefix_start/len [P], suffix_start/len [P*G] host integers.
+    Returns out [P*G, Hq, D] bf16 (and lse [P*G, Hq] fp32 natural log).
+    """
+    a, out, lse, workspace, ptrs = _decode_prepare(q, k_prefix, v_prefix, k_suffix, v_suffix, prefix_start,
+                                                   prefix_len, suffix_start, suffix_len, group_size, scale,
+                                                   split_tokens, return_lse, out, lse, workspace, kv_layout)
     _check(_lib.rl_decode_attn(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(ptrs),
                                ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                _stream_handle(stream)), "rl_decode_attn")
     return (out, lse) if return_lse else out
+
+
+@_on_call_stream
+def decode_attn_timeline(q: torch.Tensor, k_prefix: torch.Tensor, v_prefix: torch.Tensor,
+                         k_suffix: torch.Tensor, v_suffix: torch.Tensor,
+                         prefix_start, prefix_len, suffix_start, suffix_len, group_size: int,
+                         scale: Optional[float] = None, split_tokens: int = 0,
+                         workspace: Optional[torch.Tensor] = None, stream=None, kv_layout: str = "token"):
+    """decode_attn through rl_debug_decode_timeline: returns (out, lse,
+    records), records an int64 [n_items, TIMELINE_WORDS] device tensor, one
+    timeline record per work item of the split kernel (layout in rl_kernels.h)."""
+    a, out, lse, workspace, ptrs = _decode_prepare(q, k_prefix, v_prefix, k_suffix, v_suffix, prefix_start,
+                                                   prefix_len, suffix_start, suffix_len, group_size, scale,
+                                                   split_tokens, True, None, None, workspace, kv_layout)
+    n = ctypes.c_int64(0)
+    _check(_lib.rl_debug_decode_timeline(ctypes.byref(a.shape), ctypes.byref(a.lens), None, None, 0, None, 0,
+                                         ctypes.byref(n), None), "rl_debug_decode_timeline")
+    records = torch.zeros((max(n.value, 1), TIMELINE_WORDS), dtype=torch.int64, device=q.device)
+    _check(_lib.rl_debug_decode_timeline(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(ptrs),
+                                         ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                         ctypes.c_void_p(records.data_ptr()), n.value, ctypes.byref(n),
+                                         _stream_handle(stream)), "rl_debug_decode_timeline")
+    return out, lse, records[:n.value]
 
 
 class _ExtendArgs:

@@ -289,18 +289,36 @@ rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_len
     return RL_OK;
 }
 
-rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *lens,
-                         const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
-                         void *stream) {
+namespace {
+// rl_decode_attn, and with num_records non-null rl_debug_decode_timeline:
+// the same call with the split kernel's timeline records in `records`.
+rl_status decode_call(const rl_decode_shape *shape, const rl_decode_lens *lens, const rl_decode_ptrs *ptrs,
+                      void *workspace, size_t workspace_bytes, void *stream, uint64_t *records, int64_t capacity,
+                      int64_t *num_records) {
     g_last_error.clear();
     rlk::DecodePlan &plan = g_plan;
     std::string err;
     rl_status st = rlk::plan_decode(shape, lens, &plan, &err, rlk::PlanDetail::kDevice);
     if (st != RL_OK) return set_error(st, err);
+    const int64_t n_items = static_cast<int64_t>(plan.dev_items.size());
+    if (num_records && !records) {
+        *num_records = n_items;
+        return RL_OK;
+    }
     st = rlk::check_decode_ptrs(plan, lens, ptrs, &err);
     if (st != RL_OK) return set_error(st, err);
+    if (num_records) {
+        if (capacity < n_items)
+            return set_error(RL_ERR_WORKSPACE, "records hold " + std::to_string(capacity) +
+                                                   " entries, the call writes " + std::to_string(n_items));
+        if ((reinterpret_cast<uintptr_t>(records) & 7u) != 0)
+            return set_error(RL_ERR_MISALIGNED, "records are not 8-byte aligned");
+    }
     const int64_t S = static_cast<int64_t>(plan.P) * plan.G;
-    if (S == 0) return RL_OK;
+    if (S == 0) {
+        if (num_records) *num_records = 0;
+        return RL_OK;
+    }
     if (!workspace || workspace_bytes < plan.total_bytes)
         return set_error(RL_ERR_WORKSPACE, "workspace needs " + std::to_string(plan.total_bytes) +
                                                " bytes, got " + std::to_string(workspace_bytes));
@@ -326,7 +344,7 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.pm = reinterpret_cast<float *>(ws + plan.off_m);
     a.pl = reinterpret_cast<float *>(ws + plan.off_l);
     a.pacc = reinterpret_cast<float *>(ws + plan.off_acc);
-    a.n_items = static_cast<int32_t>(plan.dev_items.size());
+    a.n_items = static_cast<int32_t>(n_items);
     a.P = plan.P;
     a.G = plan.G;
     a.Hq = plan.Hq;
@@ -339,8 +357,28 @@ rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *len
     a.suffix_rows = plan.suffix_rows;
     a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
     a.release = stage_release();
-    const hipError_t e = rlk::launch_decode(a, hs);
-    return stage_commit(hs, e != hipSuccess ? hip_error(e, "launching decode attention") : RL_OK, true);
+    a.timeline = records;
+    const hipError_t e = rlk::launch_decode(a, hs, num_records != nullptr);
+    st = stage_commit(hs, e != hipSuccess ? hip_error(e, "launching decode attention") : RL_OK, true);
+    if (st == RL_OK && num_records) *num_records = n_items;
+    return st;
+}
+}  // namespace
+
+rl_status rl_decode_attn(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                         const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
+                         void *stream) {
+    return decode_call(shape, lens, ptrs, workspace, workspace_bytes, stream, nullptr, 0, nullptr);
+}
+
+rl_status rl_debug_decode_timeline(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                                   const rl_decode_ptrs *ptrs, void *workspace, size_t workspace_bytes,
+                                   uint64_t *records, int64_t capacity, int64_t *num_records, void *stream) {
+    if (!num_records) {
+        g_last_error.clear();
+        return set_error(RL_ERR_NULL_POINTER, "num_records is NULL");
+    }
+    return decode_call(shape, lens, ptrs, workspace, workspace_bytes, stream, records, capacity, num_records);
 }
 
 rl_status rl_extend_attn_workspace_size(const rl_decode_shape *shape, const rl_extend_lens *lens,

@@ -74,10 +74,15 @@ __device__ __forceinline__ int v_off(int t, int c) {
 // Items of up to 16 rows split each tile's 4 sub-tiles over the 4 waves, items
 // of up to 32 rows over 2; those waves' partials are merged through LDS.
 // PF: tiles whose loads are in flight while a tile is computed (1 or 2).
-template <int D, int PF>
+// TL: debug build that leaves one timeline record per work item (wall clock
+// at the start, once the first tile is in LDS, at the loop's end and after
+// the partials; s_memtime cycles of the loop); the same arithmetic.
+template <int D, int PF, bool TL = false>
 __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitBlocksPerCU) void decode_split_kernel(
     DecodeArgs a) {
     using C = DCfg<D>;
+    [[maybe_unused]] uint64_t tl_start = 0, tl_first = 0, tl_loop1 = 0, tl_c0 = 0, tl_c1 = 0;
+    if constexpr (TL) tl_start = __builtin_amdgcn_s_memrealtime();
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::MAIN_BYTES + C::ML_BYTES];
     uint16_t *kv = reinterpret_cast<uint16_t *>(smem);
     float *red_acc = reinterpret_cast<float *>(smem);
@@ -270,11 +275,18 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
             __syncthreads();
         }
     };
+    auto tl_loop_start = [&]() {
+        if constexpr (TL) {
+            tl_first = __builtin_amdgcn_s_memrealtime();
+            tl_c0 = __builtin_amdgcn_s_memtime();
+        }
+    };
     if constexpr (PF == 1) {
         load_tile(0, kA, vA);
         store_tile(kA, vA);
         if (ntiles > 1) load_tile(1, kA, vA);
         __syncthreads();
+        tl_loop_start();
         for (int tile = 0; tile < ntiles; ++tile) step(tile, kA, vA);
     } else {
         // set A holds the odd tiles' loads, set B the even ones'
@@ -283,11 +295,35 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
         store_tile(kB, vB);
         load_tile(2, kB, vB);
         __syncthreads();
+        tl_loop_start();
         for (int tile = 0; tile < ntiles; tile += 2) {
             step(tile, kA, vA);
             if (tile + 1 < ntiles) step(tile + 1, kB, vB);
         }
     }
+    if constexpr (TL) {
+        tl_loop1 = __builtin_amdgcn_s_memrealtime();
+        tl_c1 = __builtin_amdgcn_s_memtime();
+    }
+    // the item's timeline record (thread 0 stores it once every wave is done)
+    [[maybe_unused]] auto tl_record = [&]() {
+        __syncthreads();
+        const uint64_t tl_end = __builtin_amdgcn_s_memrealtime();
+        const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);    // HW_ID
+        const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);  // XCC_ID
+        if (tid == 0) {
+            uint64_t *rec = a.timeline + static_cast<int64_t>(blockIdx.x) * kTimelineWords;
+            rec[0] = hw | (static_cast<uint64_t>(xcc & 0xff) << 32) | (static_cast<uint64_t>(is_suffix) << 40) |
+                     (static_cast<uint64_t>(rows) << 48);
+            rec[1] = tl_start;
+            rec[2] = tl_first;
+            rec[3] = tl_loop1;
+            rec[4] = tl_end;
+            rec[5] = static_cast<uint64_t>(ntok) | (static_cast<uint64_t>(ntiles) << 32);
+            rec[6] = blockIdx.x;
+            rec[7] = tl_c1 - tl_c0;
+        }
+    };
 
     // ---- the item's partials ------------------------------------------------
     l_run += __shfl_xor(l_run, 16, 64);
@@ -305,6 +341,7 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
                 a.pl[prow] = l_run;
             }
         }
+        if constexpr (TL) tl_record();
         return;
     }
     // Wt waves hold partials of the same rows over disjoint tokens: merge them
@@ -340,6 +377,7 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
             a.pl[prow] = L;
         }
     }
+    if constexpr (TL) tl_record();
 }
 
 // Merges, per (sequence s, query head h) row, the partials of the prompt's
@@ -460,12 +498,19 @@ __global__ __launch_bounds__(kThreads) void plan_fetch_kernel(const u32x4 *__res
 }
 
 template <int D>
-hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
+hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream, bool timeline) {
     if (a.n_items > 0) {
-        if (a.deep_prefetch)
-            hipLaunchKernelGGL((decode_split_kernel<D, 2>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
-        else
-            hipLaunchKernelGGL((decode_split_kernel<D, 1>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
+        if (a.deep_prefetch) {
+            if (timeline)
+                hipLaunchKernelGGL((decode_split_kernel<D, 2, true>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
+            else
+                hipLaunchKernelGGL((decode_split_kernel<D, 2>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
+        } else {
+            if (timeline)
+                hipLaunchKernelGGL((decode_split_kernel<D, 1, true>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
+            else
+                hipLaunchKernelGGL((decode_split_kernel<D, 1>), dim3(a.n_items), dim3(kThreads), 0, stream, a);
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -496,10 +541,10 @@ hipError_t launch_plan_fetch(const void *host_src, void *dst, size_t bytes, hipS
     return hipGetLastError();
 }
 
-hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream) {
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream, bool timeline) {
     switch (a.D) {
-        case 64: return launch_decode_d<64>(a, stream);
-        case 128: return launch_decode_d<128>(a, stream);
+        case 64: return launch_decode_d<64>(a, stream, timeline);
+        case 128: return launch_decode_d<128>(a, stream, timeline);
         default: return hipErrorInvalidValue;
     }
 }

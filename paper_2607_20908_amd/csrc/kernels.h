@@ -22,6 +22,10 @@ __device__ __forceinline__ void release_staging(const StageRelease &r) {
         __hip_atomic_store(r.flag, r.value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// uint64 words of one debug timeline record (a work item of the decode
+// split kernel, a wave of an lm-head tile kernel)
+constexpr int kTimelineWords = 8;
+
 struct DecodeArgs {
     const uint16_t *q;
     const uint16_t *k_prefix, *v_prefix, *k_suffix, *v_suffix;
@@ -37,9 +41,11 @@ struct DecodeArgs {
     int64_t prefix_rows, suffix_rows;
     float score_scale_log2;     // softmax_scale * log2(e)
     StageRelease release;       // stored by the combine kernel
+    uint64_t *timeline;         // debug timeline only: kTimelineWords words per work item
 };
 
-hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
+// timeline: the split kernel built with one timeline record per work item
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream, bool timeline = false);
 
 // Causal extend attention: one workgroup per ExtItem block of query rows.
 struct ExtendArgs {
@@ -118,8 +124,6 @@ struct LogprobArgs {
     uint64_t *timeline;
     int64_t timeline_base;
 };
-
-constexpr int kTimelineWords = 8;
 
 // timeline: launch the tile kernels (whole, narrow, tail parts) built with
 // per-wave timeline records (same arithmetic and outputs)

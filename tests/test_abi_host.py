@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 10
+    assert lib.rl_abi_version() == 11
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"
@@ -633,3 +633,34 @@ def test_timeline_size_query_and_validation():
     assert lib.rl_debug_logprob_timeline(*args, ctypes.c_void_p(FAKE + 4), need, ctypes.byref(n), None) == MISAL
     assert lib.rl_debug_logprob_timeline(8, 256, 1024, fake, fake, None, 1.0, fake, fake, fake, ws,
                                          ctypes.c_void_p(FAKE), need, ctypes.byref(n), None) == NULLP
+
+
+def test_decode_timeline_size_query_and_validation():
+    lib = rk.lib()
+    P, G, Hq, Hkv, D = 3, 8, 16, 2, 64
+    lp = np.array([700, 0, 193], np.int32)
+    ls = np.array([5, 0, 17, 64, 1, 65, 0, 30, 3, 9, 0, 2, 40, 1, 0, 12, 63, 0, 1, 2, 3, 4, 5, 6], np.int32)
+    ps = np.concatenate([[0], np.cumsum(lp)[:-1]]).astype(np.int64)
+    ss = np.concatenate([[0], np.cumsum(ls)[:-1]]).astype(np.int64)
+    a = rk._DecodeArgs(P, G, Hq, Hkv, D, 0.125, 0, ps, lp, ss, ls, int(lp.sum()), int(ls.sum()))
+    n = ctypes.c_int64(-1)
+    # size query: planning only, no pointer looked at
+    assert lib.rl_debug_decode_timeline(ctypes.byref(a.shape), ctypes.byref(a.lens), None, None, 0, None, 0,
+                                        ctypes.byref(n), None) == OK
+    items = rk.decode_plan(P, G, Hq, Hkv, D, ps, lp, ss, ls, int(lp.sum()), int(ls.sum()), scale=0.125)
+    assert n.value == len(items) > 0
+    assert lib.rl_debug_decode_timeline(ctypes.byref(a.shape), ctypes.byref(a.lens), None, None, 0, None, 0,
+                                        None, None) == NULLP
+    fake = ctypes.c_void_p(FAKE)
+    ptrs = rk.DecodePtrs(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    need = ctypes.c_size_t(0)
+    assert lib.rl_decode_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(need)) == OK
+    call = lambda rec, cap: lib.rl_debug_decode_timeline(ctypes.byref(a.shape), ctypes.byref(a.lens),
+                                                         ctypes.byref(ptrs), fake, need.value, rec, cap,
+                                                         ctypes.byref(n), None)
+    assert call(ctypes.c_void_p(FAKE), len(items) - 1) == WSPACE
+    assert call(ctypes.c_void_p(FAKE + 4), len(items)) == MISAL
+    bad = rk.DecodePtrs(FAKE, FAKE, FAKE, None, FAKE, FAKE, None)      # NULL k_suffix
+    assert lib.rl_debug_decode_timeline(ctypes.byref(a.shape), ctypes.byref(a.lens), ctypes.byref(bad), fake,
+                                        need.value, ctypes.c_void_p(FAKE), len(items), ctypes.byref(n),
+                                        None) == NULLP

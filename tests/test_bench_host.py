@@ -132,3 +132,26 @@ def test_timeline_markdown_on_synthetic_records():
     assert per_cu and "2: 256 CUs" in per_cu[0]
     assert any(l.startswith("| tail parts | 100 |") and "1: 100 CUs" in l for l in md.splitlines())
     assert "361.0 us from the first start" in md
+
+
+def test_decode_timeline_markdown_on_synthetic_records():
+    # 256 CUs; 256 prefix items (32 rows, 1024 tokens) then 512 suffix items (4 rows)
+    recs = []
+    for i in range(768):
+        kind, rows, ntok = (0, 32, 1024) if i < 256 else (1, 4, 512)
+        cu = i % 256
+        x, rest = cu // 32, cu % 32
+        se, sh, c = rest // 8, (rest // 4) % 2, rest % 4
+        st = (i // 256) * 4000
+        tiles = (ntok + 63) // 64
+        recs.append([(c << 8) | (sh << 12) | (se << 13) | (x << 32) | (kind << 40) | (rows << 48), st, st + 300,
+                     st + 300 + tiles * 200, st + 300 + tiles * 200 + 100, ntok | (tiles << 32), i, 0])
+    md = bench.decode_timeline_markdown(np.array(recs, dtype=np.int64), True, 512, 10 ** 9, "synthetic")
+    lines = md.splitlines()
+    pre = [l for l in lines if l.startswith("| prefix | 32 | 256 |")][0].split("|")
+    suf = [l for l in lines if l.startswith("| suffix | 4 | 512 |")][0].split("|")
+    # prefix item: 16 tiles x 2 us + 3 us first tile + 1 us partials = 36 us; 2000 ns per tile
+    assert pre[5].strip() == "36.0/36.0/36.0" and pre[7].strip() == "2000"
+    assert suf[5].strip() == "20.0/20.0/20.0"
+    assert "over 256 CUs" in md and "at most 256 (1.00 per CU)" in md
+    assert "The item that ends last: suffix" in md

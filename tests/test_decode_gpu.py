@@ -342,3 +342,42 @@ def test_full_size_workloads(name, layout):
     eo, el = max_abs(o, ro), max_abs(l, rl)
     say(f"decode full-size {name}: out max-abs {eo:.3g}, lse max-abs {el:.3g}")
     assert eo <= ATTN_OUT_TOL and el <= ATTN_LSE_TOL
+
+
+def _timeline_case(c, D, Hq, Hkv, layout, split=0):
+    """rl_debug_decode_timeline against rl_decode_attn on the same inputs: the
+    same output and lse bit for bit, and one record per work item of the plan,
+    in plan order, with its kind, rows and tokens and ordered timestamps."""
+    def kv(bits):
+        return to_dev(np.ascontiguousarray(np.transpose(bits, (1, 0, 2))) if layout == "head" else bits)
+    t = {k: kv(c[k]) for k in ("k_prefix", "v_prefix", "k_suffix", "v_suffix")}
+    q = to_dev(c["q"])
+    args = (q, t["k_prefix"], t["v_prefix"], t["k_suffix"], t["v_suffix"], c["prefix_start"], c["prefix_len"],
+            c["suffix_start"], c["suffix_len"], c["group_size"])
+    scale = 1.0 / math.sqrt(D)
+    o0, l0 = rk.decode_attn(*args, scale=scale, split_tokens=split, return_lse=True, kv_layout=layout)
+    o1, l1, rec = rk.decode_attn_timeline(*args, scale=scale, split_tokens=split, kv_layout=layout)
+    torch.cuda.synchronize()
+    assert torch.equal(o0.view(torch.int16), o1.view(torch.int16)) and torch.equal(l0, l1)
+    items = plan_of(c, Hq, Hkv, D, split)
+    r = rec.cpu().numpy()
+    assert len(r) == len(items)
+    assert (r[:, 6] == np.arange(len(items))).all()
+    assert (((r[:, 0] >> 40) & 0xFF) == items["kind"]).all()
+    assert (((r[:, 0] >> 48) & 0xFFFF) == items["row_count"]).all()
+    assert ((r[:, 5] & 0xFFFFFFFF) == items["tok_count"]).all()
+    assert ((r[:, 5] >> 32) == (items["tok_count"] + 63) // 64).all()
+    st, first, loop1, en = (r[:, i] for i in range(1, 5))
+    assert (st > 0).all() and (st <= first).all() and (first <= loop1).all() and (loop1 <= en).all()
+    assert (((r[:, 0] >> 32) & 0xFF) < 8).all()
+
+
+@pytest.mark.parametrize("layout", ["token", "head"])
+def test_timeline_same_outputs_and_records(layout):
+    # both split variants: narrow items (one tile in flight) and wide ones (two)
+    c = decode_host_case(3, 8, 16, 4, 128, [700, 0, 193], list(np.arange(24) * 37 % 300), seed=71, gap=2)
+    _timeline_case(c, 128, 16, 4, layout)
+    c = decode_host_case(3, 8, 16, 2, 64, [700, 0, 193],
+                         [5, 0, 17, 64, 1, 65, 0, 30, 3, 9, 0, 2, 40, 1, 0, 12, 63, 0, 1, 2, 3, 4, 5, 6], seed=72, gap=2)
+    assert set(plan_of(c, 16, 2, 64)["split_variant"]) == {1}
+    _timeline_case(c, 64, 16, 2, layout)
