@@ -352,8 +352,10 @@ rl_status rl_token_logprob_noalloc(int64_t rows, int32_t hidden, int32_t vocab,
  *   grad_hidden    device fp32 [rows, hidden], written (not accumulated)
  *
  * The workspace holds chunk_rows x vocab (padded to 256) bf16 probabilities
- * plus, when rows are few, fp32 partial sums of a vocabulary split; its size
- * depends on (rows, hidden, vocab) only.  w_lm must be finite.  rows == 0 is
+ * plus one fp32 section used in turn by the hidden-dimension parts of the
+ * last round of probability tiles (when that round would leave at least
+ * half of the CUs idle) and, when rows are few, by the partial sums of a
+ * vocabulary split; its size depends on (rows, hidden, vocab) only.  w_lm must be finite.  rows == 0 is
  * a valid no-op.  Status: as rl_token_logprob; hidden_states, w_lm and
  * grad_hidden 16-byte aligned, target, lse and grad_logprob 4-byte aligned.
  */

@@ -261,6 +261,37 @@ void replay_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegions &rg)
     });
 }
 
+// logprob_probs_tail_reduce_kernel: 8 workgroups of 128 threads per tail
+// tile of the backward's probability pass.
+void replay_probs_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegions &rg) {
+    rp.launch("logprob_probs_tail_reduce_kernel", t.tail_tiles * 8, [&](int64_t b, Replay::Lane &ln) {
+        const int64_t j = b >> 3;
+        const int wn = (b >> 2) & 1, tn = b & 3;
+        int64_t vt, rt;
+        tile_of_logical(t.tile_base + j, t.n_vocab_tiles, t.n_row_tiles, &vt, &rt);
+        for (int tid = 0; tid < 128; ++tid) {
+            ln.thread = tid;
+            const int wm = tid >> 6, lane = tid & 63, l32 = lane & 31, h2 = lane >> 5;
+            const int wave = wn * 2 + wm;
+            for (int sp = 0; sp < t.splits; ++sp)
+                for (int tm = 0; tm < 4; ++tm)
+                    for (int q = 0; q < 4; ++q)
+                        ln.check(rg.part, Replay::addr(t.part) + part_elem(j * t.splits + sp, wave, tm, tn, q, lane) * 4,
+                                 16, "tail part load");
+            const int row = wn * 128 + tn * 32 + l32;
+            const int64_t rr = rt * kRowTile + row;
+            if (rr < t.R) {
+                ln.check(rg.target, Replay::addr(t.target) + rr * 4, 4, "target load");
+                ln.check(rg.lse_in, Replay::addr(t.lse_in) + rr * 4, 4, "lse load");
+            }
+            const uint64_t pb = Replay::addr(t.probs) + probs_block(rt, t.n_vocab_tiles * 4LL, vt * 4 + wm * 2) * 2;
+            for (int tm = 0; tm < 4; ++tm)
+                for (int q = 0; q < 4; ++q)
+                    ln.check(rg.probs, pb + probs_store_off(tm, q, row, h2) * 2, 8, "probability store");
+        }
+    });
+}
+
 // The combine kernel launch_logprob picks for a.R rows.
 void replay_combine(Replay &rp, const LogprobArgs &a, const TileRegions &rg, int logprob_r, int lse_r) {
     const int kind = logprob_combine_kind(a.R);
@@ -440,19 +471,36 @@ extern "C" rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t h
         const uint64_t rows_pad = static_cast<uint64_t>(plan.chunk_row_tiles) * kRowTile;
         rg.probs = rp.section("workspace probabilities", ws, plan.off_probs,
                               rows_pad * static_cast<uint64_t>(plan.n_vsteps) * kHiddenStep * 2);
-        const int part = plan.splits > 1 ? rp.section("workspace split sums", ws, plan.off_part,
-                                                      static_cast<uint64_t>(plan.splits) * rows_pad * hidden * 4)
-                                         : dh;
+        // one section for the probability tail's parts and the GEMM's split
+        // sums (used one after the other within a chunk)
+        const bool has_part = plan.total_bytes > plan.off_part;
+        const int part = has_part ? rp.section("workspace tail parts and split sums", ws, plan.off_part,
+                                               plan.total_bytes - plan.off_part)
+                                  : -1;
+        rg.part = part;
+        const int gemm_out = plan.splits > 1 ? part : dh;
         for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
             LogprobArgs f;
             LogprobBwdArgs b;
             logprob_bwd_chunk_args(plan, c0, rp.ptr<uint16_t>(rg.hidden), rp.ptr<uint16_t>(rg.w),
                                    rp.ptr<int32_t>(rg.target), 1.f, rp.ptr<float>(rg.lse_in), rp.ptr<float>(grad),
                                    rp.ptr<float>(dh), rp.ptr<unsigned char>(ws), &f, &b);
-            replay_tile(rp, "logprob_tile_kernel<kBwdProbs>", kBwdProbs, 4, tile_weight_stages(f.n_row_tiles), f,
-                        static_cast<int64_t>(f.n_vocab_tiles) * f.n_row_tiles, rg);
-            replay_bwd_gemm(rp, b, rg.probs, rg.w, part);
-            replay_bwd_finish(rp, b, part, rg.w, rg.target, grad, dh);
+            // the launches of launch_logprob_probs, in order
+            LogprobArgs d = f;
+            d.tile_base = 0;
+            d.tile_count = f.dp_tiles;
+            replay_tile(rp, "logprob_tile_kernel<kBwdProbs>", kBwdProbs, 4, tile_weight_stages(f.n_row_tiles), d,
+                        d.tile_count, rg);
+            if (f.tail_tiles > 0) {
+                LogprobArgs t = f;
+                t.tile_base = f.dp_tiles;
+                t.tile_count = f.tail_tiles;
+                replay_tile(rp, "logprob_tile_kernel<kPartialK>", kPartialK, 4, tile_weight_stages(f.n_row_tiles), t,
+                            f.tail_tiles * f.splits, rg);
+                replay_probs_tail_reduce(rp, t, rg);
+            }
+            replay_bwd_gemm(rp, b, rg.probs, rg.w, gemm_out);
+            replay_bwd_finish(rp, b, gemm_out, rg.w, rg.target, grad, dh);
         }
     } else {
         return RL_ERR_INVALID_SHAPE;

@@ -94,11 +94,11 @@ struct LogprobArgs {
     int32_t H, V;
     int32_t n_vocab_tiles, n_row_tiles;
     float inv_temperature;
-    // forward only: logical tiles [0, dp_tiles) run whole; the tail_tiles
-    // after them run as `splits` parts of the hidden dimension each, whose
-    // fp32 accumulators go to part (256 x 256 floats per part, part
-    // j*splits + s of tail tile j) for the reduce kernel.  tile_base and
-    // tile_count are set per launch by launch_logprob.
+    // forward and backward probabilities: logical tiles [0, dp_tiles) run
+    // whole; the tail_tiles after them run as `splits` parts of the hidden
+    // dimension each, whose fp32 accumulators go to part (256 x 256 floats
+    // per part, part j*splits + s of tail tile j) for the reduce kernel.
+    // tile_base and tile_count are set per launch by the launch functions.
     int64_t dp_tiles, tail_tiles;
     int32_t splits;
     float *part;

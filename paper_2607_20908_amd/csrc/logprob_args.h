@@ -37,9 +37,9 @@ inline LogprobArgs logprob_args(const LogprobPlan &plan, const void *hidden_stat
     return a;
 }
 
-// The three launches of the backward's chunk starting at row c0: the
-// probability tile kernel (f), then the vocabulary GEMM and the finish
-// kernel (b).
+// The launches of the backward's chunk starting at row c0: the probability
+// pass (f: whole tiles, then, with a tail split, the tail tiles' parts and
+// their reduce), then the vocabulary GEMM and the finish kernel (b).
 inline void logprob_bwd_chunk_args(const LogprobBwdPlan &plan, int64_t c0, const uint16_t *hid, const uint16_t *w,
                                    const int32_t *target, float inv_temperature, const float *lse,
                                    const float *grad_logprob, float *grad_hidden, unsigned char *ws, LogprobArgs *f,
@@ -59,6 +59,11 @@ inline void logprob_bwd_chunk_args(const LogprobBwdPlan &plan, int64_t c0, const
     f->inv_temperature = inv_temperature;
     f->lse_in = lse + c0;
     f->probs = probs;
+    const TailSplit ts = bwd_probs_tail(plan, n);
+    f->dp_tiles = ts.dp_tiles;
+    f->tail_tiles = ts.tail_tiles;
+    f->splits = ts.splits;
+    f->part = reinterpret_cast<float *>(ws + plan.off_part);
     *b = LogprobBwdArgs{};
     b->w = w;
     b->target = target + c0;

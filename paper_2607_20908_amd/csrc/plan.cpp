@@ -454,6 +454,25 @@ rl_status check_extend_ptrs(const ExtendPlan &pl, const rl_decode_ptrs *ptrs, st
     return RL_OK;
 }
 
+TailSplit plan_tail_split(int64_t tiles, int64_t nks) {
+    TailSplit ts;
+    ts.dp_tiles = tiles;
+    const int64_t dp = tiles / kNumCUs * kNumCUs, tail = tiles - dp;
+    if (dp > 0 && tail > 0 && 2 * tail <= kNumCUs) {
+        const int64_t s = std::min<int64_t>(std::min<int64_t>(kMaxTailSplits, kNumCUs / tail), nks / 4);
+        if (s >= 2) {
+            ts.dp_tiles = dp;
+            ts.tail_tiles = tail;
+            ts.splits = static_cast<int32_t>(s);
+        }
+    }
+    return ts;
+}
+
+TailSplit bwd_probs_tail(const LogprobBwdPlan &plan, int64_t n) {
+    return plan_tail_split(plan.n_vocab_tiles * ceil_div(n, kRowTile), plan.H / kHiddenStep);
+}
+
 TileRounds plan_tile_rounds(int64_t rows, int32_t vocab) {
     // With at most 4 row tiles (the tiles of one vocab tile are neighbours in
     // launch order), the whole vocab tiles of the full rounds run as they are
@@ -499,23 +518,11 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
     if (pl.n_vocab_tiles * pl.n_row_tiles > INT32_MAX)
         return fail(err, RL_ERR_UNSUPPORTED, "too many rows x vocab tiles");
     if (rows == 0) return RL_OK;
-    // Whole rounds of tiles over the CUs run as they are.  A last round that
-    // would leave at least half of the CUs idle is split over the hidden
-    // dimension instead, as many ways as fit one round (up to 4, at least 4
-    // hidden steps per part), so that it takes a fraction of a tile's time.
-    const int64_t tiles = pl.n_vocab_tiles * pl.n_row_tiles;
-    const int64_t dp = tiles / kNumCUs * kNumCUs, tail = tiles - dp;
-    const int64_t nks = hidden / kHiddenStep;
-    pl.n_dp_tiles = tiles;
+    const TailSplit ts = plan_tail_split(pl.n_vocab_tiles * pl.n_row_tiles, hidden / kHiddenStep);
+    pl.n_dp_tiles = ts.dp_tiles;
+    pl.n_tail_tiles = ts.tail_tiles;
+    pl.tail_splits = ts.splits;
     pl.n_partials = pl.n_vocab_tiles;
-    if (dp > 0 && tail > 0 && 2 * tail <= kNumCUs) {
-        const int64_t s = std::min<int64_t>(std::min<int64_t>(kMaxTailSplits, kNumCUs / tail), nks / 4);
-        if (s >= 2) {
-            pl.n_dp_tiles = dp;
-            pl.n_tail_tiles = tail;
-            pl.tail_splits = static_cast<int32_t>(s);
-        }
-    }
     // A last round more than half full: narrow tiles, when they fit.
     if (pl.n_tail_tiles == 0) {
         const TileRounds tr = plan_tile_rounds(rows, vocab);
@@ -568,8 +575,16 @@ rl_status plan_logprob_bwd(int64_t rows, int32_t hidden, int32_t vocab, LogprobB
     size_t off = 0;
     pl.off_probs = off;
     off = align_up(off + rows_pad * static_cast<size_t>(pl.n_vsteps) * kHiddenStep * 2, 256);
+    // the GEMM's split sums and the probability tail's parts share one
+    // section: the reduce kernel has summed the parts before the GEMM writes
     pl.off_part = off;
-    if (pl.splits > 1) off = align_up(off + static_cast<size_t>(pl.splits) * rows_pad * hidden * 4, 256);
+    size_t part_bytes = pl.splits > 1 ? static_cast<size_t>(pl.splits) * rows_pad * hidden * 4 : 0;
+    for (const int64_t n : {pl.chunk_rows, rows % pl.chunk_rows}) {
+        if (n == 0) continue;
+        const TailSplit ts = bwd_probs_tail(pl, n);
+        part_bytes = std::max(part_bytes, static_cast<size_t>(ts.tail_tiles) * ts.splits * kVocabTile * kRowTile * 4);
+    }
+    if (part_bytes > 0) off = align_up(off + part_bytes, 256);
     pl.total_bytes = off;
     return RL_OK;
 }

@@ -103,6 +103,18 @@ rl_status check_decode_ptrs(const DecodePlan &plan, const rl_decode_lens *lens,
 // A last round of lm-head tiles that would leave at least half the CUs idle
 // is split over the hidden dimension into up to this many parts.
 constexpr int kMaxTailSplits = 4;
+
+// One pass of `tiles` 256 x 256 lm-head tiles over `nks` hidden steps: the
+// whole rounds over the CUs run as they are (logical tiles [0, dp_tiles)).
+// A last round that would leave at least half of the CUs idle runs as
+// `splits` hidden-dimension parts per tile instead, as many as fit one round
+// (up to kMaxTailSplits, at least 4 hidden steps per part), so that it takes
+// a fraction of a tile's time; tail_tiles = 0 when the last round runs whole.
+struct TailSplit {
+    int64_t dp_tiles = 0, tail_tiles = 0;
+    int32_t splits = 1;
+};
+TailSplit plan_tail_split(int64_t tiles, int64_t nks);
 // The tile kernels address a weight or hidden row of a tile as a 32-bit byte
 // offset from the tile's first row (255 rows of 2 * hidden bytes).
 constexpr int64_t kMaxHidden = 1 << 22;
@@ -163,8 +175,14 @@ struct LogprobBwdPlan {
     int32_t chunk_row_tiles = 0;     // 256-row tiles of a full chunk
     int32_t n_h_tiles = 0;           // 256-entry hidden tiles
     int32_t splits = 1, steps_per_split = 0;
+    // [off_part, total_bytes) holds, one after the other within a chunk, the
+    // hidden-dimension parts of the probability pass's tail tiles (summed
+    // before the GEMM starts) and the GEMM's split partial sums
     size_t off_probs = 0, off_part = 0, total_bytes = 0;
 };
+
+// The probability pass of the backward chunk of `n` rows: its tail split.
+TailSplit bwd_probs_tail(const LogprobBwdPlan &plan, int64_t n);
 
 rl_status plan_logprob_bwd(int64_t rows, int32_t hidden, int32_t vocab, LogprobBwdPlan *plan,
                            std::string *err);

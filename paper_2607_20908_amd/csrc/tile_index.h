@@ -114,11 +114,8 @@ RLK_HD TileCoord tile_coord(int mode, int tm, int64_t b, const LogprobArgs &a) {
         const int n = t.nks;
         t.kb = sp * n / a.splits;
         t.nks = (sp + 1) * n / a.splits - t.kb;
-    } else if (mode == kFwd || mode == kLogits) {
-        tile_of(b, a.tile_count, a.tile_base, a.n_vocab_tiles, a.n_row_tiles, &t.vt, &t.rt);
     } else {
-        tile_of(b, static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles, 0, a.n_vocab_tiles, a.n_row_tiles, &t.vt,
-                &t.rt);
+        tile_of(b, a.tile_count, a.tile_base, a.n_vocab_tiles, a.n_row_tiles, &t.vt, &t.rt);
     }
     t.v0 = t.vt * kVocabTile;
     return t;

@@ -142,6 +142,46 @@ __device__ __forceinline__ void write_partial(const LogprobArgs &a, int64_t vt, 
     a.pl[vt * a.R + rr] = l0 * fast_exp2(m0 - Mx) + l1 * fast_exp2(m1 - Mx);
 }
 
+// Backward epilogue of one 32-row column of a wave's 128 x 128 block, as one
+// lane holds it: z(tm)[i] is vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4
+// for tile row `row` of row tile rt.  p = exp(inv_T z - lse) (0 for masked
+// or invalid targets and past the vocabulary) goes to the blocked
+// probability buffer as bf16: the 4 consecutive entries i%4 are one 8-byte
+// store into vocab step vt*4 + wm*2 + tm/2, chunk (tm%2)*4 + i/4.
+template <class Z>
+__device__ __forceinline__ void probs_column(const LogprobArgs &a, Z z, int64_t v0, int64_t vt, int64_t rt, int wm,
+                                             int row, int h2) {
+    const float c2 = a.inv_temperature * kLog2e;
+    const int64_t vbase = v0 + wm * 128;
+    const int vlim = vbase + 128 <= a.V ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
+    uint16_t *pb = a.probs + probs_block(rt, a.n_vocab_tiles * 4LL, vt * 4 + wm * 2);
+    const int64_t rr = rt * kRowTile + row;
+    bool live = false;
+    float l2 = 0.f;
+    if (rr < a.R) {
+        const int32_t t = a.target[rr];
+        live = t >= 0 && t < a.V;
+        l2 = a.lse_in[rr] * kLog2e;
+    }
+#pragma unroll
+    for (int tm = 0; tm < 4; ++tm) {
+        const f32x16 zz = z(tm);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t w2[2];
+#pragma unroll
+            for (int e = 0; e < 4; e += 2) {
+                const int loc = tm * 32 + 8 * q + e;
+                const float p0 = live && loc < vlim ? fast_exp2(zz[4 * q + e] * c2 - l2) : 0.f;
+                const float p1 = live && loc + 1 < vlim ? fast_exp2(zz[4 * q + e + 1] * c2 - l2) : 0.f;
+                w2[e >> 1] = static_cast<uint32_t>(f32_to_bf16_bits(p0)) |
+                             (static_cast<uint32_t>(f32_to_bf16_bits(p1)) << 16);
+            }
+            *reinterpret_cast<uint2 *>(pb + probs_store_off(tm, q, row, h2)) = make_uint2(w2[0], w2[1]);
+        }
+    }
+}
+
 // Forward epilogue of one (64 TM) x 256 logit tile held in the registers of
 // the workgroup's 4 waves (acc[tm][tn][i] of wave (wm, wn), lane (h2, l32)
 // holds vocab v0 + wm*32*TM + tm*32 + 8*(i/4) + 4*h2 + i%4 for token row
@@ -369,41 +409,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     };
 
     if constexpr (MODE == kBwdProbs) {
-        // acc[tm][tn][i]: vocab v0 + wm*128 + tm*32 + 8*(i/4) + 4*h2 + i%4,
-        // row r0 + wn*128 + tn*32 + l32.  The 4 consecutive entries i%4 are one
-        // 8-byte store into vocab step vt*4 + wm*2 + tm/2, chunk (tm%2)*4 + i/4.
-        const float c2 = a.inv_temperature * kLog2e;
-        const int64_t vbase = v0 + wm * 128;
-        const int vlim = vbase + 128 <= a.V ? 128 : static_cast<int>(a.V - vbase) - 4 * h2;
-        uint16_t *pb = a.probs + probs_block(rt, a.n_vocab_tiles * 4LL, vt * 4 + wm * 2);
 #pragma unroll
         for (int tn = 0; tn < 4; ++tn) {
-            const int row = wn * 128 + tn * 32 + l32;
-            const int64_t rr = r0 + row;
-            bool live = false;
-            float l2 = 0.f;
-            if (rr < a.R) {
-                const int32_t t = a.target[rr];
-                live = t >= 0 && t < a.V;
-                l2 = a.lse_in[rr] * kLog2e;
-            }
-#pragma unroll
-            for (int tm = 0; tm < 4; ++tm) {
-                const f32x16 z = acc[tm][tn];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    uint32_t w2[2];
-#pragma unroll
-                    for (int e = 0; e < 4; e += 2) {
-                        const int loc = tm * 32 + 8 * q + e;
-                        const float p0 = live && loc < vlim ? fast_exp2(z[4 * q + e] * c2 - l2) : 0.f;
-                        const float p1 = live && loc + 1 < vlim ? fast_exp2(z[4 * q + e + 1] * c2 - l2) : 0.f;
-                        w2[e >> 1] = static_cast<uint32_t>(f32_to_bf16_bits(p0)) |
-                                     (static_cast<uint32_t>(f32_to_bf16_bits(p1)) << 16);
-                    }
-                    *reinterpret_cast<uint2 *>(pb + probs_store_off(tm, q, row, h2)) = make_uint2(w2[0], w2[1]);
-                }
-            }
+            probs_column(a, [&](int tm) -> const f32x16 & { return acc[tm][tn]; }, v0, vt, rt, wm,
+                         wn * 128 + tn * 32 + l32, h2);
             __builtin_amdgcn_sched_barrier(0);
         }
         return;
@@ -467,22 +476,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     if constexpr (TL) tl_record();
 }
 
-// Sums the hidden-dimension parts of the tail tiles (in a fixed order) and
-// runs the forward epilogue on the sums.  One workgroup of 2 waves per
-// (tail tile, 32-row column tn of row half wn): wave wm holds what lane (h2,
-// l32) of tile-kernel wave (wm, wn) held for that column, 8 workgroups per
-// tile, so the parts are read by many CUs at once.
-__global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a) {
-    __shared__ float red[2][32][2];
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t j = blockIdx.x >> 3;
-    const int wn = (blockIdx.x >> 2) & 1, tn = blockIdx.x & 3;
-    const int l32 = lane & 31, h2 = lane >> 5;
-    int64_t vt, rt;
-    tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
-    const int wave = wn * 2 + wm;                // the tile kernel's wave index
-    f32x16 z[4];
+// Sum, in part order, of the hidden-dimension parts of tail tile j (its
+// logical tile a.tile_base + j) that lane `lane` of tile-kernel wave `wave`
+// held in accumulators (0..3, tn).
+__device__ __forceinline__ void sum_parts(const LogprobArgs &a, int64_t j, int wave, int tn, int lane, f32x16 (&z)[4]) {
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm) z[tm] = f32x16{};
     for (int sp = 0; sp < a.splits; ++sp) {
@@ -499,6 +496,25 @@ __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) z[tm][4 * q + e] += v[tm][q][e];
     }
+}
+
+// The reduce kernels of a hidden-split tail: one workgroup of 2 waves per
+// (tail tile, 32-row column tn of row half wn), 8 workgroups per tile, so the
+// parts are read by many CUs at once.  Wave wm holds what lane (h2, l32) of
+// tile-kernel wave (wm, wn) held for that column.
+//
+// Forward: the forward epilogue on the sums.
+__global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a) {
+    __shared__ float red[2][32][2];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t j = blockIdx.x >> 3;
+    const int wn = (blockIdx.x >> 2) & 1, tn = blockIdx.x & 3;
+    const int l32 = lane & 31, h2 = lane >> 5;
+    int64_t vt, rt;
+    tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+    f32x16 z[4];
+    sum_parts(a, j, wn * 2 + wm, tn, lane, z);
     const int row = tn * 32 + l32;               // within the row half
     const int64_t rr = rt * kRowTile + wn * 128 + row;
     float mx, sum;
@@ -512,6 +528,21 @@ __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a)
         const int64_t r = rt * kRowTile + wn * 128 + tn * 32 + tid;
         if (r < a.R) write_partial(a, vt, r, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
     }
+}
+
+// Backward: the probabilities of the sums.
+__global__ __launch_bounds__(128) void logprob_probs_tail_reduce_kernel(LogprobArgs a) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t j = blockIdx.x >> 3;
+    const int wn = (blockIdx.x >> 2) & 1, tn = blockIdx.x & 3;
+    const int l32 = lane & 31, h2 = lane >> 5;
+    int64_t vt, rt;
+    tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
+    f32x16 z[4];
+    sum_parts(a, j, wn * 2 + wm, tn, lane, z);
+    probs_column(a, [&](int tm) -> const f32x16 & { return z[tm]; }, vt * kVocabTile, vt, rt, wm,
+                 wn * 128 + tn * 32 + l32, h2);
 }
 
 // Online log-sum-exp merge of (max, sum) partials, both in log2 units.
@@ -675,13 +706,32 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream, bool timelin
 }
 
 hipError_t launch_logprob_probs(const LogprobArgs &a, hipStream_t stream) {
-    const int64_t tiles = static_cast<int64_t>(a.n_vocab_tiles) * a.n_row_tiles;
-    if (tile_weight_stages(a.n_row_tiles) == 3)
-        hipLaunchKernelGGL((logprob_tile_kernel<3, kBwdProbs>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
-                           stream, a);
+    // whole tiles [0, dp_tiles), then the tail's hidden-dimension parts and
+    // their sums, which give the tail tiles' probabilities
+    LogprobArgs d = a;
+    d.tile_base = 0;
+    d.tile_count = a.dp_tiles;
+    const bool ws3 = tile_weight_stages(a.n_row_tiles) == 3;
+    if (ws3)
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kBwdProbs>), dim3(static_cast<uint32_t>(d.tile_count)),
+                           dim3(kTileThreads), 0, stream, d);
     else
-        hipLaunchKernelGGL((logprob_tile_kernel<2, kBwdProbs>), dim3(static_cast<uint32_t>(tiles)), dim3(kTileThreads), 0,
-                           stream, a);
+        hipLaunchKernelGGL((logprob_tile_kernel<2, kBwdProbs>), dim3(static_cast<uint32_t>(d.tile_count)),
+                           dim3(kTileThreads), 0, stream, d);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.tail_tiles == 0) return e;
+    LogprobArgs t = a;
+    t.tile_base = a.dp_tiles;
+    t.tile_count = a.tail_tiles;
+    const uint32_t parts = static_cast<uint32_t>(a.tail_tiles * a.splits);
+    if (ws3)
+        hipLaunchKernelGGL((logprob_tile_kernel<3, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+    else
+        hipLaunchKernelGGL((logprob_tile_kernel<2, kPartialK>), dim3(parts), dim3(kTileThreads), 0, stream, t);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(logprob_probs_tail_reduce_kernel, dim3(static_cast<uint32_t>(a.tail_tiles * 8)), dim3(128), 0,
+                       stream, t);
     return hipGetLastError();
 }
 

@@ -391,14 +391,22 @@ def test_logprob_backward_empty_is_noop():
 def test_logprob_backward_workspace_size():
     V = 151936
     vpad = -(-V // 256) * 256
-    # one chunk of probabilities (at most 16384 rows, padded to 256) in bf16
+    part = 256 * 256 * 4                 # one hidden-dimension part of a tail tile
+    # one chunk of probabilities (at most 16384 rows, padded to 256) in bf16;
+    # a full chunk has 594 x 64 tiles, whose last round of 128 tiles runs as
+    # 2 hidden-dimension parts each
     for R, H in [(262144, 5120), (16384, 5120), (20000, 4096)]:
         n = rk.token_logprob_backward_workspace_size(R, H, V)
-        assert n == 16384 * vpad * 2
-    # few rows: the vocabulary is split and fp32 partial sums follow
+        assert n == 16384 * vpad * 2 + 128 * 2 * part
+    # 8B-class rows: the vocabulary is split and fp32 partial sums follow
+    # (1188 tiles, a last round of 164 runs whole: no tail parts)
     n = rk.token_logprob_backward_workspace_size(512, 4096, V)
     probs = 512 * vpad * 2
     assert n > probs and (n - probs) % (512 * 4096 * 4) == 0
+    # 32B-class rows: the split sums (12 x 256 x 5120 fp32) and the tail
+    # parts (82 tiles x 3) share one section, as large as the larger
+    n = rk.token_logprob_backward_workspace_size(256, 5120, V)
+    assert n == 256 * vpad * 2 + max(12 * 256 * 5120 * 4, 82 * 3 * part)
     assert rk.token_logprob_backward_workspace_size(0, 64, 10) == 0
     with pytest.raises(rk.RLError):
         rk.token_logprob_backward_workspace_size(4, 100, 10)

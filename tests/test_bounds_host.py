@@ -30,7 +30,7 @@ V = 151936
 # (rows, hidden, vocab, every_stage)
 SHAPES = [
     (512, 4096, V, 0),        # 8B-class decode step: whole tiles + narrow last round; backward split 8 ways
-    (256, 5120, V, 0),        # 32B-class decode step
+    (256, 5120, V, 0),        # 32B-class decode step: 594 tiles, the last 82 split 3 ways
     (16384, 5120, V, 0),      # one full backward chunk, unsplit
     (262144, 5120, V, 0),     # policy pass: 16 backward chunks, one-thread-per-row combine
     (300, 128, 1000, 1),      # ragged rows and vocab
@@ -38,6 +38,7 @@ SHAPES = [
     (1, 64, 1, 1),            # one row, one vocab entry
     (4097, 192, 77777, 0),    # wave combine; ragged vocab tile
     (8000, 4096, 2500, 0),    # tail parts: 320 tiles, the last 64 split 4 ways over the hidden dimension
+    (300, 512, 40000, 1),     # tail parts: 314 tiles, the last 58 split 2 ways; ragged rows and vocab
 ]
 
 
@@ -54,9 +55,19 @@ def test_every_access_inside_its_allocation(op, rows, hidden, vocab, every):
 
 
 def test_backward_launch_count_per_chunk():
-    # three launches (probabilities, GEMM, finish) per 16384-row chunk
-    assert replay(1, 262144, 5120, V).launches == 3 * 16
+    # three launches (probabilities, GEMM, finish) per 16384-row chunk, and
+    # two more (tail tiles' hidden parts, their reduce) when the probability
+    # pass's last round is split: a full 5120-wide chunk has 594 x 64 tiles,
+    # a last round of 128
+    assert replay(1, 262144, 5120, V).launches == 5 * 16
     assert replay(1, 40000, 64, 700).launches == 3 * 3
+    # 32B-class rows: 594 tiles, the last 82 in 3 parts; 8B-class rows: 1188
+    # tiles, a last round of 164 runs whole
+    assert replay(1, 256, 5120, V).launches == 5
+    assert replay(1, 512, 4096, V).launches == 3
+    # the GPU parity tests' split-tail shapes
+    assert replay(1, 200, 1024, 75739).launches == 5
+    assert replay(1, 300, 512, 40000).launches == 5
 
 
 def test_forward_launches_follow_the_plan():
@@ -87,19 +98,24 @@ def test_shrunk_allocation_is_caught_forward(rows, hidden, vocab):
     assert n == 10
 
 
-@pytest.mark.parametrize("rows,hidden,vocab,splits", [(512, 4096, V, True), (16384, 5120, V, False),
-                                                      (300, 128, 1000, False), (300, 128, 20000, True)])
-def test_shrunk_allocation_is_caught_backward(rows, hidden, vocab, splits):
+# part: what the section after the probabilities holds (the GEMM's split
+# sums, the probability pass's tail parts, both, or nothing)
+@pytest.mark.parametrize("rows,hidden,vocab,part", [(512, 4096, V, "splits"), (16384, 5120, V, "tail"),
+                                                    (256, 5120, V, "both"), (300, 128, 1000, None),
+                                                    (300, 128, 20000, "splits")])
+def test_shrunk_allocation_is_caught_backward(rows, hidden, vocab, part):
     rep0 = replay(1, rows, hidden, vocab)
     for name, i in BWD_TIGHT.items():
         rep = replay(1, rows, hidden, vocab, shrink=i)
         assert rep.violations > 0, f"shrinking {name} went unnoticed"
     assert replay(1, rows, hidden, vocab, shrink=6).violations == 0   # the workspace's own extent
-    assert rep0.regions == (9 if splits else 8)
-    if splits:
-        # the split sums are padded to whole 256-row tiles: used to the last
-        # byte only when the rows fill their last tile
-        assert (replay(1, rows, hidden, vocab, shrink=8).violations > 0) == (rows % 256 == 0)
+    assert rep0.regions == (9 if part else 8)
+    if part:
+        # the section is as large as the larger user.  Tail parts fill it (256
+        # KB each).  The split sums are padded to whole 256-row tiles: used to
+        # the last byte only when the rows fill their last tile.
+        tight = part != "splits" or rows % 256 == 0
+        assert (replay(1, rows, hidden, vocab, shrink=8).violations > 0) == tight
 
 
 def test_invalid_arguments():

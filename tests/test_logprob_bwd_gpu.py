@@ -109,6 +109,14 @@ def test_ragged_shapes(R, H, V):
     case(R, H, V, seed=R + H + V, what=f"ragged")
 
 
+@pytest.mark.parametrize("R,H,V", [(200, 1024, 75739),   # 296 vocab tiles: 256 whole, the last 40 in 4 hidden parts
+                                   (300, 512, 40000)])   # 2 row tiles, 314 tiles: the last 58 in 2 hidden parts
+def test_split_tail(R, H, V):
+    # the probabilities of the last round's tiles come from the sum of their
+    # hidden-dimension parts (the host replay pins these launch plans)
+    case(R, H, V, seed=R + V, wstd=0.08, inv_T=1.0 / 0.7, mask_frac=0.05, what="split tail")
+
+
 def test_several_row_chunks():
     # 40000 rows, compared on every row: three chunks of probabilities
     # (16384, 16384, 7232), 64 row tiles in the full ones (two-stage ring)
