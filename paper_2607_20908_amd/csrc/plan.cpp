@@ -250,8 +250,51 @@ rl_status plan_decode(const rl_decode_shape *shape, const rl_decode_lens *lens,
                 key.swap(k2);
             }
         }
+        // --- one XCD per chunk ---------------------------------------------------
+        // A chunk of more than kMaxItemRows query rows (a wide prefix group)
+        // is served by g items of equal cost, neighbours after the sort, and
+        // neighbours land on different XCDs: each would fetch the chunk into
+        // its own L2.  Where kNumXcds such chunks of one cost follow each
+        // other, their items are transposed (item j of chunk k to window
+        // position j kNumXcds + k), so a chunk's items start on one XCD at
+        // about the same time and the later ones read it from that L2.  The
+        // window holds items of one cost, so the order stays longest first.
+        auto item_of = [&](size_t i) { return static_cast<uint32_t>(key[i] & 0xffffffffu); };
+        auto item_cost = [&](uint32_t x) {
+            const DevItem &d = tmp[x];
+            const int64_t M = (d.meta >> 15) & 1 ? r : Mp;
+            const int64_t rows = std::min<int64_t>(kMaxItemRows, M - static_cast<int64_t>(d.meta >> 24) * kMaxItemRows);
+            return static_cast<uint64_t>(d.meta & 0x7fff) * kv_bytes_per_tok +
+                   static_cast<uint64_t>(rows) * partial_bytes_per_row;
+        };
+        auto same_chunk = [&](uint32_t x, uint32_t y) {
+            return tmp[x].kv_row0 == tmp[y].kv_row0 && tmp[x].unit == tmp[y].unit &&
+                   (tmp[x].meta & 0x00ffffffu) == (tmp[y].meta & 0x00ffffffu);
+        };
+        const size_t n_sorted = key.size();
+        auto group_len = [&](size_t p) {
+            size_t g = 1;
+            while (p + g < n_sorted && same_chunk(item_of(p), item_of(p + g))) ++g;
+            return g;
+        };
+        std::vector<uint64_t> &win = pl.tmp_keys2;
+        for (size_t p = 0; p < n_sorted;) {
+            const size_t g = group_len(p);
+            bool ok = g >= 2 && p + kNumXcds * g <= n_sorted;
+            const uint64_t c0 = item_cost(item_of(p));
+            for (size_t i = p; ok && i < p + kNumXcds * g; ++i) ok = item_cost(item_of(i)) == c0;
+            for (int k = 0; ok && k < kNumXcds; ++k) ok = group_len(p + k * g) == g;
+            if (!ok) {
+                p += g;
+                continue;
+            }
+            win.assign(key.begin() + p, key.begin() + p + kNumXcds * g);
+            for (int k = 0; k < kNumXcds; ++k)
+                for (size_t j = 0; j < g; ++j) key[p + j * kNumXcds + k] = win[k * g + j];
+            p += kNumXcds * g;
+        }
         pl.dev_items.resize(key.size());
-        for (size_t i = 0; i < key.size(); ++i) pl.dev_items[i] = tmp[key[i] & 0xffffffffu];
+        for (size_t i = 0; i < key.size(); ++i) pl.dev_items[i] = tmp[item_of(i)];
         if (detail == PlanDetail::kDebug) {
             pl.items.resize(pl.dev_items.size());
             for (size_t i = 0; i < pl.dev_items.size(); ++i) {

@@ -27,6 +27,8 @@ constexpr int kRowTile = 256;
 constexpr int kHiddenStep = 64;
 // Compute units of an MI355X; the automatic split size is planned for them.
 constexpr int kNumCUs = 256;
+// XCDs: the hardware deals consecutive workgroups of a launch to them in turn.
+constexpr int kNumXcds = 8;
 constexpr float kLog2eHost = 1.4426950408889634f;
 
 // One split-K work item as the split kernel reads it (16 bytes; the work list

@@ -80,6 +80,32 @@ def test_workload_plans_cover_and_balance():
     assert (pre["row_count"] == 64).all() and sorted(set(pre["row_begin"])) == [0, 64]
 
 
+def test_row_blocks_of_a_chunk_share_an_xcd():
+    # workgroups go to the 8 XCDs in turn: the items of one wide prefix chunk
+    # are 8 launch positions apart, so they run on one XCD and share its L2
+    cfg = W.DECODE_CONFIGS["32b"]
+    items, _, _ = plan_for(cfg.num_prompts, cfg.group_size, cfg.num_q_heads, cfg.num_kv_heads,
+                           cfg.head_dim, np.full(16, 2048), W.suffix_lengths(cfg, 0))
+    pos = {}
+    for i, it in enumerate(items):
+        if it["kind"] == 0:
+            pos.setdefault((int(it["unit"]), int(it["kv_head"]), int(it["tok_begin"])), []).append(
+                (int(it["row_begin"]), i))
+    assert len(pos) == 16 * 8
+    for blocks in pos.values():
+        (rb0, i0), (rb1, i1) = sorted(blocks)
+        assert (rb0, rb1) == (0, 64) and i1 - i0 == 8, blocks
+    # three blocks per chunk (G*r = 192): 8 chunks of one cost at a time
+    items, _, _ = plan_for(4, 24, 64, 8, 128, np.full(4, 1024), np.full(96, 700))
+    pre = np.flatnonzero(items["kind"] == 0)
+    by_chunk = {}
+    for i in pre:
+        it = items[i]
+        by_chunk.setdefault((int(it["unit"]), int(it["kv_head"]), int(it["tok_begin"])), []).append(int(i))
+    full = [sorted(v) for v in by_chunk.values() if len(v) == 3]
+    assert full and all(np.all(np.diff(v) == 8) for v in full)
+
+
 @pytest.mark.parametrize("lengths", ["equal", "one_giant", "geometric", "zeros"])
 def test_skewed_lengths(lengths):
     P, G, Hq, Hkv = 4, 8, 64, 8
