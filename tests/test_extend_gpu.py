@@ -172,11 +172,19 @@ def test_full_size_turn(name, layout):
     x = W.make_extend_inputs(cfg, dev(), kv_layout=layout)
     d = x.dec
     say(f"extend full size {name} layout={layout}: {int(x.new_len.sum())} new tokens")
+    # outputs start as NaN: every new token's rows at every head must be
+    # written, so a work block missing from the launch shows up
+    out = torch.full(x.q.shape, float("nan"), dtype=torch.bfloat16, device=dev())
+    lse = torch.full(x.q.shape[:2], float("nan"), dtype=torch.float32, device=dev())
     out, lse = rk.extend_attn(x.q, d.k_prefix, d.v_prefix, d.k_suffix, d.v_suffix, d.prefix_start,
                               d.prefix_len, d.suffix_start, d.suffix_len, x.new_len, x.q_start,
-                              cfg.group_size, scale=d.scale, return_lse=True, kv_layout=layout)
+                              cfg.group_size, scale=d.scale, return_lse=True, out=out, lse=lse, kv_layout=layout)
     torch.cuda.synchronize()
-    assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
+    owned = torch.zeros(x.q.shape[0], dtype=torch.bool)
+    for s in range(cfg.num_seqs):
+        owned[int(x.q_start[s]):int(x.q_start[s]) + int(x.new_len[s])] = True
+    owned = owned.to(dev())
+    assert torch.isfinite(out[owned].float()).all() and torch.isfinite(lse[owned]).all()
     kp, vp, ks, vs = (W.bf16_bits(d.token_major(t)) for t in (d.k_prefix, d.v_prefix, d.k_suffix, d.v_suffix))
     rng = np.random.Generator(np.random.PCG64(3))
     S = cfg.num_seqs
