@@ -504,7 +504,8 @@ rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_len
 
 /*
  * Host-only replay of the global memory accesses that rl_token_logprob
- * (op = 0) or rl_token_logprob_backward (op = 1) would make for these sizes:
+ * (op = 0), rl_token_logprob_backward (op = 1) or rl_sample_top_p (op = 2)
+ * would make for these sizes:
  * every launch of the call, every workgroup and lane, with the kernel
  * arguments the entry point builds and the kernels' own index arithmetic;
  * each load and store is checked against the allocation (or workspace
@@ -518,7 +519,11 @@ rl_status rl_decode_plan_debug(const rl_decode_shape *shape, const rl_decode_len
  * w_lm, target, logprob, lse, workspace, and the workspace's partial max,
  * partial sum, target logit and tail part sections; op 1: hidden, w_lm,
  * target, lse, grad_logprob, grad_hidden, workspace, and the workspace's
- * probability and (split GEMMs only) split-sum sections.  Returns the plan's
+ * probability section and (when a tail or a GEMM is split) the section of
+ * tail parts and split sums; op 2: hidden, w_lm, inv_temperature, uniform,
+ * token, logprob, workspace, and the workspace's logits and row-maximum
+ * sections (the selection kernel's data-dependent reads are checked over
+ * the whole range it may touch).  Returns the plan's
  * status for invalid sizes, RL_ERR_NULL_POINTER for a NULL report and
  * RL_ERR_INVALID_SHAPE for an unknown op; otherwise RL_OK with the counts in
  * *report.

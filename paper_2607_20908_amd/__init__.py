@@ -597,8 +597,9 @@ def token_logprob_noalloc(hidden: torch.Tensor, w_lm: torch.Tensor, target: torc
 
 def logprob_bounds(op: int, rows: int, hidden: int, vocab: int, every_stage: bool = False,
                    shrink_region: int = -1) -> BoundsReport:
-    """Host replay of the global accesses of rl_token_logprob (op 0) or
-    rl_token_logprob_backward (op 1) at these sizes (no device access)."""
+    """Host replay of the global accesses of rl_token_logprob (op 0),
+    rl_token_logprob_backward (op 1) or rl_sample_top_p (op 2) at these
+    sizes (no device access)."""
     rep = BoundsReport()
     _check(_lib.rl_debug_logprob_bounds(op, rows, hidden, vocab, int(bool(every_stage)), shrink_region,
                                         ctypes.byref(rep)), "rl_debug_logprob_bounds")

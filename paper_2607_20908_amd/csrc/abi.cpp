@@ -704,42 +704,13 @@ rl_status rl_sample_top_p(int64_t rows, int32_t hidden, int32_t vocab, const voi
     unsigned char *ws = static_cast<unsigned char *>(workspace);
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     const uint16_t *hid = static_cast<const uint16_t *>(hidden_states);
-    float *logits = reinterpret_cast<float *>(ws + plan.off_logits);
-    float *pm = reinterpret_cast<float *>(ws + plan.off_pm);
     for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
-        const int64_t n = std::min(plan.chunk_rows, rows - c0);
-        rlk::LogprobArgs f{};
-        f.hidden = hid + c0 * hidden;
-        f.w = static_cast<const uint16_t *>(w_lm);
-        f.R = n;
-        f.H = hidden;
-        f.V = vocab;
-        f.n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
-        f.n_row_tiles = static_cast<int32_t>((n + rlk::kRowTile - 1) / rlk::kRowTile);
-        f.inv_temperature = 1.f;
-        f.inv_t_rows = inv_temperature + c0;
-        f.logits = logits;
-        f.ld = plan.ld;
-        f.pm = pm;
-        const rlk::TileRounds tr = rlk::plan_tile_rounds(n, vocab);
-        f.dp_tiles = tr.dp_tiles;
-        f.narrow_v0 = tr.narrow_v0;
-        f.narrow_tiles = tr.narrow_tiles;
-        f.narrow_slot0 = tr.narrow_slot0;
-        f.n_partials = tr.n_partials;
+        rlk::LogprobArgs f;
+        rlk::SampleArgs s;
+        rlk::sample_chunk_args(plan, c0, hid, static_cast<const uint16_t *>(w_lm), inv_temperature, top_p, uniform,
+                               token, logprob, ws, &f, &s);
         hipError_t e = rlk::launch_logits(f, hs);
         if (e != hipSuccess) return hip_error(e, "launching the sampling head (logits)");
-        rlk::SampleArgs s{};
-        s.logits = logits;
-        s.pm = pm;
-        s.uniform = uniform + c0;
-        s.token = token + c0;
-        s.logprob = logprob ? logprob + c0 : nullptr;
-        s.rows = n;
-        s.ld = plan.ld;
-        s.V = vocab;
-        s.n_partials = static_cast<int32_t>(tr.n_partials);
-        s.top_p = top_p;
         e = rlk::launch_sample_top_p(s, hs);
         if (e != hipSuccess) return hip_error(e, "launching the sampling head (selection)");
     }

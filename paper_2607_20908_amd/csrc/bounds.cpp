@@ -148,7 +148,7 @@ std::vector<int> stage_slots(const Replay &rp, int nks, int last_slot) {
 }
 
 struct TileRegions {
-    int hidden, w, target, pm, pl, zt, part, lse_in, probs;
+    int hidden, w, target, pm, pl, zt, part, lse_in, probs, inv_t, logits;
 };
 
 // logprob_tile_kernel<WS, MODE, TM> over `blocks` workgroups of 256 threads.
@@ -189,6 +189,21 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
             for (int lane = 0; lane < 64; ++lane) {
                 ln.thread = wave * 64 + lane;
                 const int l32 = lane & 31, h2 = lane >> 5;
+                if (mode == kLogits) {
+                    // the tempered logits of the wave's 32 TM vocab entries
+                    const int64_t vbase = tc.v0 + wm * 32 * TM;
+                    for (int tn = 0; tn < 4; ++tn) {
+                        const int64_t rr = r0 + wn * 128 + tn * 32 + l32;
+                        if (rr >= a.R) continue;
+                        ln.check(rg.inv_t, Replay::addr(a.inv_t_rows) + rr * 4, 4, "inverse temperature load");
+                        for (int tm = 0; tm < TM; ++tm)
+                            for (int q = 0; q < 4; ++q)
+                                ln.check(rg.logits,
+                                         Replay::addr(a.logits) + (rr * a.ld + vbase + 4 * h2 + tm * 32 + 8 * q) * 4,
+                                         16, "logits store");
+                    }
+                    continue;
+                }
                 if (mode == kPartialK) {
                     for (int tm = 0; tm < 4; ++tm)
                         for (int tn = 0; tn < 4; ++tn)
@@ -217,6 +232,12 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
                 }
             }
         }
+        if (mode == kLogits)
+            for (int tid = 0; tid < 256; ++tid) {
+                ln.thread = tid;
+                const int64_t rr = r0 + tid;
+                if (rr < a.R) ln.check(rg.pm, Replay::addr(a.pm) + (tc.vt * a.R + rr) * 4, 4, "row maximum store");
+            }
         if (mode == kFwd || mode == kNarrow)
             for (int tid = 0; tid < 256; ++tid) {
                 ln.thread = tid;
@@ -289,6 +310,25 @@ void replay_probs_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegion
                 for (int q = 0; q < 4; ++q)
                     ln.check(rg.probs, pb + probs_store_off(tm, q, row, h2) * 2, 8, "probability store");
         }
+    });
+}
+
+// sample_top_p_kernel: one workgroup per row.  Its reads of the row's logits
+// go to float4 groups below (V + 3) / 4 and to the drawn id (< V); which ones
+// depends on the data, so the replay checks the whole range the kernel may
+// touch: every group of the row, the row maxima of every partial slot, and
+// the per-row input and outputs.
+void replay_select(Replay &rp, const SampleArgs &s, int pm_r, int logits_r, int u_r, int tok_r, int lp_r) {
+    rp.launch("sample_top_p_kernel", s.rows, [&](int64_t r, Replay::Lane &ln) {
+        ln.thread = 0;
+        const int64_t nvec = (s.V + 3) / 4;
+        const uint64_t y = Replay::addr(s.logits) + static_cast<uint64_t>(r * s.ld) * 4;
+        for (int64_t g = 0; g < nvec; ++g) ln.check(logits_r, y + g * 16, 16, "logits load");
+        for (int64_t t = 0; t < s.n_partials; ++t)
+            ln.check(pm_r, Replay::addr(s.pm) + (t * s.rows + r) * 4, 4, "row maximum load");
+        ln.check(u_r, Replay::addr(s.uniform) + r * 4, 4, "uniform load");
+        ln.check(tok_r, Replay::addr(s.token) + r * 4, 4, "token store");
+        if (s.logprob) ln.check(lp_r, Replay::addr(s.logprob) + r * 4, 4, "log-prob store");
     });
 }
 
@@ -501,6 +541,39 @@ extern "C" rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t h
             }
             replay_bwd_gemm(rp, b, rg.probs, rg.w, gemm_out);
             replay_bwd_finish(rp, b, gemm_out, rg.w, rg.target, grad, dh);
+        }
+    } else if (op == 2) {
+        SamplePlan plan;
+        const rl_status st = plan_sample(rows, hidden, vocab, &plan, &err);
+        if (st != RL_OK) return st;
+        if (rows == 0) return RL_OK;
+        TileRegions rg{};
+        rg.hidden = rp.add("hidden", static_cast<uint64_t>(rows) * hidden * 2);
+        rg.w = rp.add("w_lm", static_cast<uint64_t>(vocab) * hidden * 2);
+        rg.inv_t = rp.add("inv_temperature", static_cast<uint64_t>(rows) * 4);
+        const int u = rp.add("uniform", static_cast<uint64_t>(rows) * 4);
+        const int tok = rp.add("token", static_cast<uint64_t>(rows) * 4);
+        const int lp = rp.add("logprob", static_cast<uint64_t>(rows) * 4);
+        const int ws = rp.add("workspace", plan.total_bytes);
+        const uint64_t rows_pad = static_cast<uint64_t>((plan.chunk_rows + kRowTile - 1) / kRowTile) * kRowTile;
+        rg.logits = rp.section("workspace logits", ws, plan.off_logits, rows_pad * plan.ld * 4);
+        rg.pm = rp.section("workspace row maxima", ws, plan.off_pm, static_cast<uint64_t>(plan.pm_slots) * plan.chunk_rows * 4);
+        for (int64_t c0 = 0; c0 < rows; c0 += plan.chunk_rows) {
+            LogprobArgs f;
+            SampleArgs s;
+            sample_chunk_args(plan, c0, rp.ptr<uint16_t>(rg.hidden), rp.ptr<uint16_t>(rg.w), rp.ptr<float>(rg.inv_t),
+                              0.9f, rp.ptr<float>(u), rp.ptr<int32_t>(tok), rp.ptr<float>(lp),
+                              rp.ptr<unsigned char>(ws), &f, &s);
+            // the launches of launch_logits and launch_sample_top_p, in order
+            LogprobArgs d = f;
+            d.tile_base = 0;
+            d.tile_count = f.dp_tiles;
+            if (d.tile_count > 0)
+                replay_tile(rp, "logprob_tile_kernel<kLogits>", kLogits, 4, tile_weight_stages(f.n_row_tiles), d,
+                            d.tile_count, rg);
+            if (f.narrow_tiles > 0)
+                replay_tile(rp, "logprob_tile_kernel<kLogits, 3>", kLogits, 3, 3, f, f.narrow_tiles * f.n_row_tiles, rg);
+            replay_select(rp, s, rg.pm, rg.logits, u, tok, lp);
         }
     } else {
         return RL_ERR_INVALID_SHAPE;

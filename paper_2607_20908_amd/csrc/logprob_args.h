@@ -82,4 +82,45 @@ inline void logprob_bwd_chunk_args(const LogprobBwdPlan &plan, int64_t c0, const
     b->inv_temperature = inv_temperature;
 }
 
+// The two launches of the sampling head's chunk starting at row c0: the
+// logits tile kernels (f: whole tiles, then the last round's narrow tiles if
+// any) and the selection kernel (s).
+inline void sample_chunk_args(const SamplePlan &plan, int64_t c0, const uint16_t *hid, const uint16_t *w,
+                              const float *inv_temperature, float top_p, const float *uniform, int32_t *token,
+                              float *logprob, unsigned char *ws, LogprobArgs *f, SampleArgs *s) {
+    const int64_t n = std::min(plan.chunk_rows, plan.R - c0);
+    float *logits = reinterpret_cast<float *>(ws + plan.off_logits);
+    float *pm = reinterpret_cast<float *>(ws + plan.off_pm);
+    *f = LogprobArgs{};
+    f->hidden = hid + c0 * plan.H;
+    f->w = w;
+    f->R = n;
+    f->H = plan.H;
+    f->V = plan.V;
+    f->n_vocab_tiles = static_cast<int32_t>(plan.n_vocab_tiles);
+    f->n_row_tiles = static_cast<int32_t>((n + kRowTile - 1) / kRowTile);
+    f->inv_temperature = 1.f;
+    f->inv_t_rows = inv_temperature + c0;
+    f->logits = logits;
+    f->ld = plan.ld;
+    f->pm = pm;
+    const TileRounds tr = plan_tile_rounds(n, plan.V);
+    f->dp_tiles = tr.dp_tiles;
+    f->narrow_v0 = tr.narrow_v0;
+    f->narrow_tiles = tr.narrow_tiles;
+    f->narrow_slot0 = tr.narrow_slot0;
+    f->n_partials = tr.n_partials;
+    *s = SampleArgs{};
+    s->logits = logits;
+    s->pm = pm;
+    s->uniform = uniform + c0;
+    s->token = token + c0;
+    s->logprob = logprob ? logprob + c0 : nullptr;
+    s->rows = n;
+    s->ld = plan.ld;
+    s->V = plan.V;
+    s->n_partials = static_cast<int32_t>(tr.n_partials);
+    s->top_p = top_p;
+}
+
 }  // namespace rlk

@@ -1,7 +1,8 @@
 """Host replay of the lm-head log-prob kernels' global accesses (no GPU).
 
-rl_debug_logprob_bounds replays every launch of rl_token_logprob (op 0) and
-rl_token_logprob_backward (op 1), workgroup by workgroup and lane by lane, with
+rl_debug_logprob_bounds replays every launch of rl_token_logprob (op 0),
+rl_token_logprob_backward (op 1) and rl_sample_top_p (op 2), workgroup by
+workgroup and lane by lane, with
 the arguments the entry points build and the kernels' own index functions, and
 checks each load and store against the allocation or workspace section it must
 fall in.  The shapes are the ones the bench and the parity tests run (the
@@ -120,7 +121,47 @@ def test_shrunk_allocation_is_caught_backward(rows, hidden, vocab, part):
 
 def test_invalid_arguments():
     rep = rk.BoundsReport()
-    assert _f(2, 8, 64, 100, 0, -1, ctypes.byref(rep)) == 2          # unknown op
+    assert _f(3, 8, 64, 100, 0, -1, ctypes.byref(rep)) == 2          # unknown op
     assert _f(0, 8, 96, 100, 0, -1, ctypes.byref(rep)) == 3          # hidden not a multiple of 64
     assert _f(1, 8, 64, 100, 0, -1, None) == 1
     assert replay(0, 0, 64, 100).launches == 0
+
+
+# ---------------------------------------------------------------- sampling head
+# (rows, hidden, vocab, every_stage)
+SAMPLE_SHAPES = [
+    (512, 4096, V, 0),        # 8B-class decode step: whole tiles + a narrow last round of 109 x 2 tiles
+    (256, 5120, V, 0),        # 32B-class decode step: the last 82 tiles as 110 narrow tiles
+    (300, 512, 51001, 1),     # 2 row tiles, narrow tiles ending past the vocabulary
+    (300, 128, 1000, 1),      # one round, ragged rows and vocab
+    (8192 + 300, 64, 300, 1), # two row chunks of logits
+    (3, 64, 1 << 21, 0),      # the largest vocabulary
+    (1, 64, 1, 1),            # one row, one vocab entry
+]
+
+
+@pytest.mark.parametrize("rows,hidden,vocab,every", SAMPLE_SHAPES)
+def test_sampling_accesses_inside_their_allocations(rows, hidden, vocab, every):
+    rep = replay(2, rows, hidden, vocab, every)
+    assert rep.accesses > 0 and rep.launches >= 2
+    assert rep.violations == 0, rep.first_violation.decode()
+
+
+def test_sampling_launches_follow_the_plan():
+    # per chunk of logits: whole tiles, (a narrow last round,) the selection
+    assert replay(2, 512, 4096, V).launches == 3
+    assert replay(2, 256, 5120, V).launches == 3
+    assert replay(2, 300, 128, 1000).launches == 2
+    assert replay(2, 8192 + 300, 64, 300).launches == 4
+
+
+SAMPLE_TIGHT = {"hidden": 0, "w_lm": 1, "inv_temperature": 2, "uniform": 3, "token": 4, "logprob": 5,
+                "row maxima": 8}
+
+
+@pytest.mark.parametrize("rows,hidden,vocab", [(512, 4096, V), (300, 128, 1000), (8192 + 300, 64, 300)])
+def test_shrunk_allocation_is_caught_sampling(rows, hidden, vocab):
+    assert replay(2, rows, hidden, vocab).regions == 9
+    for name, i in SAMPLE_TIGHT.items():
+        assert replay(2, rows, hidden, vocab, shrink=i).violations > 0, f"shrinking {name} went unnoticed"
+    assert replay(2, rows, hidden, vocab, shrink=6).violations == 0   # the workspace's own extent
