@@ -80,7 +80,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 11
+#define RL_ABI_VERSION 12
 
 typedef enum {
     RL_OK = 0,
@@ -538,6 +538,29 @@ typedef struct {
 
 rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t hidden, int32_t vocab,
                                   int32_t every_stage, int32_t shrink_region, rl_bounds_report *report);
+
+/*
+ * Host-only replay of the global memory accesses that rl_extend_attn would
+ * make for this shape and these lengths (Sec. 3, Structured Feedback and
+ * Iterative Refinement: the extend of a refinement turn): every work block
+ * of the plan, every lane, with the kernel arguments the entry point builds
+ * and the kernel's own index arithmetic; each query load, K/V tile load,
+ * output and lse store and the read of the block's work item is checked
+ * against its allocation, sized from the lengths (q and out [q_rows, Hq, D]
+ * bf16, lse [q_rows, Hq] fp32, the prefix and suffix K/V [rows, Hkv, D] bf16
+ * in shape->kv_layout, the workspace as rl_extend_attn_workspace_size
+ * gives it).  A block's tile loads are checked at the first and last tile of
+ * its prefix and of its suffix (each lane's address grows with the tile
+ * inside a range and the last tile of a range is the ragged one), or at
+ * every tile when every_stage != 0.  shrink_region as for
+ * rl_debug_logprob_bounds; regions: q, k_prefix, v_prefix, k_suffix,
+ * v_suffix, out, lse, workspace, and the workspace's work-list section.  No
+ * device access; for tests.  Returns the plan's status for invalid lengths,
+ * RL_ERR_NULL_POINTER for a NULL report; otherwise RL_OK with the counts in
+ * *report (all zero when the call has no work).
+ */
+rl_status rl_debug_extend_bounds(const rl_decode_shape *shape, const rl_extend_lens *lens, int32_t every_stage,
+                                 int32_t shrink_region, rl_bounds_report *report);
 
 /*
  * Debug timeline of rl_token_logprob, to see where a tile's time goes: the

@@ -96,7 +96,8 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_grpo_surrogate", "rl_token_logprob_backward_workspace_size", "rl_token_logprob_backward",
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
            "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds",
-           "rl_token_logprob_noalloc", "rl_debug_logprob_timeline", "rl_debug_decode_timeline"]
+           "rl_token_logprob_noalloc", "rl_debug_logprob_timeline", "rl_debug_decode_timeline",
+           "rl_debug_extend_bounds"]
 
 
 def _load():
@@ -143,6 +144,8 @@ def _load():
     lib.rl_extend_attn.argtypes = [P, P, P, P, SZ, P]
     lib.rl_debug_logprob_bounds.restype = ctypes.c_int
     lib.rl_debug_logprob_bounds.argtypes = [I32, I64, I32, I32, I32, I32, ctypes.POINTER(BoundsReport)]
+    lib.rl_debug_extend_bounds.restype = ctypes.c_int
+    lib.rl_debug_extend_bounds.argtypes = [P, P, I32, I32, ctypes.POINTER(BoundsReport)]
     lib.rl_token_logprob_noalloc.restype = ctypes.c_int
     lib.rl_token_logprob_noalloc.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P]
     lib.rl_debug_decode_timeline.restype = ctypes.c_int
@@ -150,7 +153,7 @@ def _load():
     lib.rl_debug_logprob_timeline.restype = ctypes.c_int
     lib.rl_debug_logprob_timeline.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P, I64,
                                               ctypes.POINTER(ctypes.c_int64), P]
-    if lib.rl_abi_version() != 11:
+    if lib.rl_abi_version() != 12:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 
@@ -603,6 +606,19 @@ def logprob_bounds(op: int, rows: int, hidden: int, vocab: int, every_stage: boo
     rep = BoundsReport()
     _check(_lib.rl_debug_logprob_bounds(op, rows, hidden, vocab, int(bool(every_stage)), shrink_region,
                                         ctypes.byref(rep)), "rl_debug_logprob_bounds")
+    return rep
+
+
+def extend_bounds(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix_len, new_len, q_start,
+                  prefix_rows, suffix_rows, q_rows, kv_layout: str = "token", every_stage: bool = False,
+                  shrink_region: int = -1) -> BoundsReport:
+    """Host replay of the global accesses of rl_extend_attn for these lengths
+    (no device access)."""
+    a = _ExtendArgs(P, G, Hq, Hkv, D, 1.0 / math.sqrt(D), prefix_start, prefix_len, suffix_start, suffix_len,
+                    new_len, q_start, prefix_rows, suffix_rows, q_rows, kv_layout)
+    rep = BoundsReport()
+    _check(_lib.rl_debug_extend_bounds(ctypes.byref(a.shape), ctypes.byref(a.lens), int(bool(every_stage)),
+                                       shrink_region, ctypes.byref(rep)), "rl_debug_extend_bounds")
     return rep
 
 

@@ -11,6 +11,7 @@
 
 #include "abi_error.h"
 #include "kernels.h"
+#include "extend_args.h"
 #include "logprob_args.h"
 #include "plan.h"
 #include "rl_kernels.h"
@@ -411,24 +412,7 @@ rl_status rl_extend_attn(const rl_decode_shape *shape, const rl_extend_lens *len
     const Section sec[1] = {{0, plan.items.data(), plan.items.size() * sizeof(rlk::ExtItem)}};
     st = stage_sections(sec, 1, plan.total_bytes, workspace, hs);
     if (st != RL_OK) return st;
-    rlk::ExtendArgs a{};
-    a.q = static_cast<const uint16_t *>(ptrs->q);
-    a.k_prefix = static_cast<const uint16_t *>(ptrs->k_prefix);
-    a.v_prefix = static_cast<const uint16_t *>(ptrs->v_prefix);
-    a.k_suffix = static_cast<const uint16_t *>(ptrs->k_suffix);
-    a.v_suffix = static_cast<const uint16_t *>(ptrs->v_suffix);
-    a.out = static_cast<uint16_t *>(ptrs->out);
-    a.lse = ptrs->lse;
-    a.items = static_cast<const rlk::ExtItem *>(workspace);
-    a.n_items = static_cast<int32_t>(plan.n_items);
-    a.Hq = plan.Hq;
-    a.Hkv = plan.Hkv;
-    a.r = plan.r;
-    a.D = plan.D;
-    a.kv_layout = plan.kv_layout;
-    a.prefix_rows = plan.prefix_rows;
-    a.suffix_rows = plan.suffix_rows;
-    a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
+    rlk::ExtendArgs a = rlk::extend_args(plan, *ptrs, workspace);
     a.release = stage_release();
     const hipError_t e = rlk::launch_extend(a, hs);
     return stage_commit(hs, e != hipSuccess ? hip_error(e, "launching extend attention") : RL_OK, true);

@@ -21,6 +21,8 @@
 #include <thread>
 #include <vector>
 
+#include "extend_args.h"
+#include "extend_index.h"
 #include "kernels.h"
 #include "logprob_args.h"
 #include "plan.h"
@@ -578,6 +580,95 @@ extern "C" rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t h
     } else {
         return RL_ERR_INVALID_SHAPE;
     }
+    rp.report(report);
+    return RL_OK;
+}
+
+// Host replay of rl_extend_attn's global accesses (see the header).
+extern "C" rl_status rl_debug_extend_bounds(const rl_decode_shape *shape, const rl_extend_lens *lens,
+                                            int32_t every_stage, int32_t shrink_region, rl_bounds_report *report) {
+    using namespace rlk;
+    if (!report) return RL_ERR_NULL_POINTER;
+    std::memset(report, 0, sizeof(*report));
+    std::string err;
+    ExtendPlan plan;
+    const rl_status st = plan_extend(shape, lens, &plan, &err, true);
+    if (st != RL_OK) return st;
+    if (plan.n_items == 0) return RL_OK;
+    Replay rp(every_stage != 0, shrink_region);
+    const int64_t D = plan.D, Hq = plan.Hq, Hkv = plan.Hkv;
+    const int q_r = rp.add("q", static_cast<uint64_t>(plan.q_rows) * Hq * D * 2);
+    const int kp_r = rp.add("k_prefix", static_cast<uint64_t>(plan.prefix_rows) * Hkv * D * 2);
+    const int vp_r = rp.add("v_prefix", static_cast<uint64_t>(plan.prefix_rows) * Hkv * D * 2);
+    const int ks_r = rp.add("k_suffix", static_cast<uint64_t>(plan.suffix_rows) * Hkv * D * 2);
+    const int vs_r = rp.add("v_suffix", static_cast<uint64_t>(plan.suffix_rows) * Hkv * D * 2);
+    const int out_r = rp.add("out", static_cast<uint64_t>(plan.q_rows) * Hq * D * 2);
+    const int lse_r = rp.add("lse", static_cast<uint64_t>(plan.q_rows) * Hq * 4);
+    const int ws_r = rp.add("workspace", plan.total_bytes);
+    const int items_r = rp.section("workspace work list", ws_r, 0, static_cast<uint64_t>(plan.n_items) * sizeof(ExtItem));
+    rl_decode_ptrs ptrs{};
+    ptrs.q = rp.ptr<void>(q_r);
+    ptrs.k_prefix = rp.ptr<void>(kp_r);
+    ptrs.v_prefix = rp.ptr<void>(vp_r);
+    ptrs.k_suffix = rp.ptr<void>(ks_r);
+    ptrs.v_suffix = rp.ptr<void>(vs_r);
+    ptrs.out = rp.ptr<void>(out_r);
+    ptrs.lse = rp.ptr<float>(lse_r);
+    const ExtendArgs a = extend_args(plan, ptrs, rp.ptr<void>(ws_r));
+    const int lpw = static_cast<int>(kExtTileTokens * D / 512 / kExtWaves);   // 1 KB loads per wave per tile
+    const int nkk = static_cast<int>(D / 16), ndt = static_cast<int>(D / 32);
+    rp.launch("extend_attn_kernel", plan.n_items, [&](int64_t b, Replay::Lane &ln) {
+        const ExtItem &it = plan.items[static_cast<size_t>(b)];
+        ln.thread = 0;
+        ln.check(items_r, Replay::addr(a.items) + b * sizeof(ExtItem), sizeof(ExtItem), "work item load");
+        const ExtGeom g = ext_geom(it, a.r);
+        const int64_t stride = ext_tok_stride(a, static_cast<int>(D));
+        const int64_t poff = ext_prefix_off(a, it, static_cast<int>(D));
+        const int64_t soff = ext_suffix_off(a, it, static_cast<int>(D));
+        // tiles replayed: all, or the first and last of the prefix and of the
+        // suffix (a lane's address grows with the tile inside a range, and
+        // the last tile of a range is the ragged one)
+        std::vector<int> tiles;
+        if (rp.every_stage()) {
+            for (int t = 0; t < g.ntiles; ++t) tiles.push_back(t);
+        } else {
+            for (int t : {0, g.np - 1, g.np, g.ntiles - 1})
+                if (t >= 0 && t < g.ntiles && (tiles.empty() || tiles.back() != t)) tiles.push_back(t);
+        }
+        for (int wave = 0; wave < kExtWaves; ++wave)
+            for (int lane = 0; lane < 64; ++lane) {
+                ln.thread = wave * 64 + lane;
+                const int l32 = lane & 31, h2 = lane >> 5;
+                const int row = wave * kExtRowsPerWave + l32;
+                if (row < g.rows) {
+                    const int u = it.row_begin + row;
+                    const int64_t qrow = ext_q_row(a, it, u);
+                    for (int kk = 0; kk < nkk; ++kk)
+                        ln.check(q_r, Replay::addr(a.q) + (qrow * D + h2 * 8 + kk * 16) * 2, 16, "query load");
+                    for (int dt = 0; dt < ndt; ++dt)
+                        for (int q4 = 0; q4 < 4; ++q4)
+                            ln.check(out_r, Replay::addr(a.out) + (qrow * D + 4 * h2 + 32 * dt + 8 * q4) * 2, 8,
+                                     "output store");
+                    if (h2 == 0) ln.check(lse_r, Replay::addr(a.lse) + qrow * 4, 4, "lse store");
+                }
+                for (int t : tiles) {
+                    const bool pre = t < g.np;
+                    const int tok0 = ext_tile_tok0(t, g.np), cnt = ext_tile_cnt(t, g.np, it.Lp, g.suf_ctx);
+                    const int64_t base = (pre ? poff : soff) + tok0 * stride;
+                    const uint64_t kb = Replay::addr(pre ? a.k_prefix : a.k_suffix) + base * 2;
+                    const uint64_t vb = Replay::addr(pre ? a.v_prefix : a.v_suffix) + base * 2;
+                    for (int j = 0; j < lpw; ++j) {
+                        const int e = (wave * lpw + j) * 64 + lane;
+                        const int tt = D == 128 ? ext_load_tok<128>(e) : ext_load_tok<64>(e);
+                        const int chk = D == 128 ? ext_load_chunk<128>(e) : ext_load_chunk<64>(e);
+                        const uint32_t off = cnt == kExtTileTokens ? ext_load_off_full(tt, stride, chk)
+                                                                   : ext_load_off(tt, cnt, stride, chk);
+                        ln.check(pre ? kp_r : ks_r, kb + off, 16, pre ? "prefix K tile load" : "suffix K tile load");
+                        ln.check(pre ? vp_r : vs_r, vb + off, 16, pre ? "prefix V tile load" : "suffix V tile load");
+                    }
+                }
+            }
+    });
     rp.report(report);
     return RL_OK;
 }

@@ -23,13 +23,14 @@
 // which keeps both fragment reads free of bank conflicts (64 banks) and lets
 // every direct load write 1 KB contiguously.
 #include "device_common.h"
+#include "extend_index.h"
 #include "kernels.h"
 #include "lds_stage.h"
 
 namespace rlk {
 namespace {
 
-constexpr int kBN = 64;        // KV tokens per tile
+constexpr int kBN = kExtTileTokens;   // KV tokens per tile
 constexpr int kStages = 4;     // LDS ring depth
 
 // NT: 32-row MFMA column tiles per wave; the workgroup's 256 rows take 8 / NT
@@ -46,24 +47,11 @@ struct ECfg {
     static_assert(LPW >= 1 && LPW * 512 * WAVES == TILE, "load split");
 };
 
-// Chunk swizzle of token row t.  D = 128: rows are 256 bytes (one window of
-// the 64 banks); the 16 rows a K-fragment pass reads and the 4 rows x 4 chunks
-// a V^T pass reads map to 16 distinct 16-byte slots.  D = 64: two 128-byte rows
-// share a window; the same holds with the row parity selecting the half.
-template <int D>
-__device__ __forceinline__ int swz(int t) {
-    if constexpr (D == 128) {
-        return ((t & 3) << 2) | ((t >> 2) & 3);
-    } else {
-        const int v = (t >> 1) & 7;
-        return ((v & 1) << 2) | (v >> 1);
-    }
-}
-
-// Element offset of (token t, dimension d) inside a K or V tile.
+// Element offset of (token t, dimension d) inside a K or V tile (chunks
+// swizzled by ext_swz).
 template <int D>
 __device__ __forceinline__ int kv_elem(int t, int d) {
-    return t * D + ((((d >> 3) ^ swz<D>(t))) << 3) + (d & 7);
+    return t * D + ((((d >> 3) ^ ext_swz<D>(t))) << 3) + (d & 7);
 }
 
 // Rows keep the max they exponentiate against until a new score exceeds it by
@@ -83,22 +71,15 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31, h2 = lane >> 5, l16 = lane & 15, g16 = (lane >> 4) & 1;
     const int r = a.r;
-    const int rows = min(kExtBlockRows, it.n * r - it.row_begin);
-    const int i_lo = it.row_begin / r;
-    const int i_hi = (it.row_begin + rows - 1) / r;
-    const int base_pos = it.Ls - it.n;            // suffix position of new token 0
-    const int suf_ctx = base_pos + i_hi + 1;      // suffix tokens the block reads
-    const int np = (it.Lp + kBN - 1) / kBN;
-    const int ntiles = np + (suf_ctx + kBN - 1) / kBN;
+    const ExtGeom gm = ext_geom(it, r);
+    const int rows = gm.rows, i_lo = gm.i_lo;
+    const int base_pos = gm.base_pos;             // suffix position of new token 0
+    const int suf_ctx = gm.suf_ctx;               // suffix tokens the block reads
+    const int np = gm.np, ntiles = gm.ntiles;
 
-    // token-major [rows, Hkv, D]: a kv head's rows are Hkv*D apart;
-    // head-major [Hkv, rows, D]: contiguous
-    const bool head_major = a.kv_layout == RL_KV_HEAD_MAJOR;
-    const int64_t tok_stride = head_major ? D : static_cast<int64_t>(a.Hkv) * D;
-    const int64_t poff = head_major ? (it.kh * a.prefix_rows + it.prefix_row0) * D
-                                    : (it.prefix_row0 * a.Hkv + it.kh) * D;
-    const int64_t soff = head_major ? (it.kh * a.suffix_rows + it.suffix_row0) * D
-                                    : (it.suffix_row0 * a.Hkv + it.kh) * D;
+    const int64_t tok_stride = ext_tok_stride(a, D);
+    const int64_t poff = ext_prefix_off(a, it, D);
+    const int64_t soff = ext_suffix_off(a, it, D);
     const uint16_t *kpre = it.Lp > 0 ? a.k_prefix + poff : nullptr;
     const uint16_t *vpre = it.Lp > 0 ? a.v_prefix + poff : nullptr;
     const uint16_t *ksuf = a.k_suffix + soff;
@@ -112,9 +93,8 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
         const int row = wave * 32 * NT + tn * 32 + l32;
         const bool ok = row < rows;
         const int u = it.row_begin + (ok ? row : rows - 1);
-        const int i = u / r, hr = u - i * r;
-        lim[tn] = base_pos + i;
-        const int64_t qoff = ((it.q_row0 + i) * a.Hq + it.kh * r + hr) * D + h2 * 8;
+        lim[tn] = base_pos + u / r;
+        const int64_t qoff = ext_q_row(a, it, u) * D + h2 * 8;
 #pragma unroll
         for (int kk = 0; kk < C::KK; ++kk)
             qf[tn][kk] = ok ? *reinterpret_cast<const bf16x8 *>(a.q + qoff + kk * 16) : bf16x8{};
@@ -133,13 +113,12 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
 #pragma unroll
     for (int j = 0; j < C::LPW; ++j) {
         const int e = (wave * C::LPW + j) * 64 + lane;
-        const int tt = e / C::CH, slot = e % C::CH;
-        ld_tok[j] = tt;
-        ld_chk[j] = (slot ^ swz<D>(tt)) << 3;
-        ld_off[j] = static_cast<uint32_t>((tt * tok_stride + ld_chk[j]) * 2);
+        ld_tok[j] = ext_load_tok<D>(e);
+        ld_chk[j] = ext_load_chunk<D>(e);
+        ld_off[j] = ext_load_off_full(ld_tok[j], tok_stride, ld_chk[j]);
     }
-    auto tile_tok0 = [&](int t) { return (t < np ? t : t - np) * kBN; };
-    auto tile_cnt = [&](int t) { return min(kBN, (t < np ? it.Lp : suf_ctx) - tile_tok0(t)); };
+    auto tile_tok0 = [&](int t) { return ext_tile_tok0(t, np); };
+    auto tile_cnt = [&](int t) { return ext_tile_cnt(t, np, it.Lp, suf_ctx); };
     const uint32_t ring_l = lds_addr(ring);
     auto issue = [&](int t) {
         const uint32_t kl = ring_l + (t % kStages) * (2 * C::TILE * 2);
@@ -157,7 +136,7 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
             uint32_t off[C::LPW];
 #pragma unroll
             for (int j = 0; j < C::LPW; ++j)
-                off[j] = static_cast<uint32_t>((min(ld_tok[j], cnt - 1) * tok_stride + ld_chk[j]) * 2);
+                off[j] = ext_load_off(ld_tok[j], cnt, tok_stride, ld_chk[j]);
 #pragma unroll
             for (int j = 0; j < C::LPW; ++j) load_lds16_s(kg, off[j], kl + (wave * C::LPW + j) * 1024);
 #pragma unroll
@@ -335,8 +314,7 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
         const int row = wave * 32 * NT + tn * 32 + l32;
         if (row < rows) {
             const int u = it.row_begin + row;
-            const int i = u / r, hr = u - i * r;
-            const int64_t orow = (it.q_row0 + i) * a.Hq + it.kh * r + hr;
+            const int64_t orow = ext_q_row(a, it, u);
             const float inv = 1.f / l;
             uint16_t *o = a.out + orow * D + 4 * h2;
 #pragma unroll
@@ -356,6 +334,7 @@ __global__ __launch_bounds__(64 * (8 / NT), 1) void extend_attn_kernel(ExtendArg
 // One 32-row column tile per wave, 8 waves: two waves per SIMD, so one
 // wave's softmax and LDS waits overlap the other's MFMAs.
 constexpr int kNT = 1;
+static_assert(ECfg<128, kNT>::WAVES == kExtWaves && 32 * kNT == kExtRowsPerWave, "launch geometry of the replay");
 
 template <int D>
 hipError_t launch_extend_d(const ExtendArgs &a, hipStream_t stream) {

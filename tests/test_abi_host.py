@@ -41,7 +41,7 @@ def test_one_hip_runtime_mapped():
 
 def test_status_strings_and_version():
     lib = rk.lib()
-    assert lib.rl_abi_version() == 11
+    assert lib.rl_abi_version() == 12
     for code, name in rk.STATUS_NAMES.items():
         assert lib.rl_status_string(code).decode() == name
     assert lib.rl_status_string(99).decode() == "RL_ERR_UNKNOWN"

@@ -165,3 +165,92 @@ def test_shrunk_allocation_is_caught_sampling(rows, hidden, vocab):
     for name, i in SAMPLE_TIGHT.items():
         assert replay(2, rows, hidden, vocab, shrink=i).violations > 0, f"shrinking {name} went unnoticed"
     assert replay(2, rows, hidden, vocab, shrink=6).violations == 0   # the workspace's own extent
+
+
+# ---------------------------------------------------------------- extend
+# rl_debug_extend_bounds replays rl_extend_attn: every work block of the plan,
+# every lane, with the arguments the entry point builds and the kernel's own
+# index functions (csrc/extend_index.h).
+import numpy as np  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+
+def _packed(lengths):
+    s = np.zeros(len(lengths), np.int64)
+    s[1:] = np.cumsum(np.asarray(lengths, np.int64))[:-1]
+    return s
+
+
+def _extend(P, G, Hq, Hkv, D, lp, ls, n, layout="head", every=False, shrink=-1, gap=0):
+    # sequences packed with `gap` unused rows after each one
+    lp, ls, n = (np.asarray(x, np.int32) for x in (lp, ls, n))
+    ps = _packed(lp + gap)
+    ss = _packed(ls + gap)
+    qs = _packed(n + gap)
+    return rk.extend_bounds(P, G, Hq, Hkv, D, ps, lp, ss, ls, n, qs, int((lp + gap).sum()), int((ls + gap).sum()),
+                            int((n + gap).sum()), kv_layout=layout, every_stage=every, shrink_region=shrink)
+
+
+def _workload(name):
+    cfg = W.DECODE_CONFIGS[name]
+    ls = W.suffix_lengths(cfg, 0)
+    return (cfg.num_prompts, cfg.group_size, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+            np.full(cfg.num_prompts, cfg.prefix_len, np.int32), ls, ls.copy())
+
+
+def _ragged(seed, P, G, Hq, Hkv, D):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    lp = rng.integers(0, 300, P)
+    lp[0] = 0                                     # a prompt without a prefix
+    ls = rng.integers(1, 400, P * G)
+    n = np.minimum(ls, rng.integers(0, 300, P * G))
+    if len(n) > 2:
+        n[1] = 0                                  # a candidate with no new tokens
+    n[-1] = ls[-1]                                # the last suffix read to its end
+    return P, G, Hq, Hkv, D, lp, ls, n
+
+
+EXTEND_CASES = [
+    ("longctx", "head", False), ("longctx", "token", False), ("8b", "head", False), ("32b", "head", False),
+]
+
+
+@pytest.mark.parametrize("name,layout,every", EXTEND_CASES)
+def test_extend_accesses_inside_their_allocations(name, layout, every):
+    rep = _extend(*_workload(name), layout=layout, every=every)
+    assert rep.accesses > 0 and rep.launches == 1 and rep.regions == 9
+    assert rep.violations == 0, rep.first_violation.decode()
+
+
+@pytest.mark.parametrize("case", [(1, 3, 2, 12, 4, 128), (2, 4, 3, 8, 8, 64), (3, 2, 5, 16, 2, 128),
+                                  (4, 1, 1, 128, 1, 128)],
+                         ids=["r3", "r1-D64", "r8", "G1-r128"])
+@pytest.mark.parametrize("layout", ["head", "token"])
+@pytest.mark.parametrize("gap", [0, 5])
+def test_extend_ragged_every_tile(case, layout, gap):
+    rep = _extend(*_ragged(*case), layout=layout, every=True, gap=gap)
+    assert rep.accesses > 0
+    assert rep.violations == 0, rep.first_violation.decode()
+
+
+EXTEND_TIGHT = {"q": 0, "k_prefix": 1, "v_prefix": 2, "k_suffix": 3, "v_suffix": 4, "out": 5, "lse": 6,
+                "work list": 8}
+
+
+@pytest.mark.parametrize("layout", ["head", "token"])
+def test_extend_shrunk_allocation_is_caught(layout):
+    args = _ragged(3, 2, 5, 16, 2, 128)
+    for name, i in EXTEND_TIGHT.items():
+        rep = _extend(*args, layout=layout, every=True, shrink=i)
+        assert rep.violations > 0, f"shrinking {name} went unnoticed"
+    assert _extend(*args, layout=layout, every=True, shrink=7).violations == 0   # the workspace's own extent
+
+
+def test_extend_bounds_arguments():
+    # no new tokens: no work, nothing replayed
+    rep = _extend(1, 2, 8, 8, 64, [10], [5, 6], [0, 0])
+    assert rep.launches == 0 and rep.accesses == 0
+    with pytest.raises(rk.RLError):
+        _extend(1, 2, 8, 8, 64, [10], [5, 6], [6, 0])     # more new tokens than the suffix holds
+    assert rk.lib().rl_debug_extend_bounds(None, None, 0, -1, None) == 1
