@@ -563,6 +563,29 @@ rl_status rl_debug_extend_bounds(const rl_decode_shape *shape, const rl_extend_l
                                  int32_t shrink_region, rl_bounds_report *report);
 
 /*
+ * Host-only replay of the global memory accesses that rl_decode_attn would
+ * make for this shape and these lengths (Sec. 2.2.1, Problem Setup: decode of
+ * a group of candidates over the prompt's shared prefix): the work list's
+ * upload, every work item of the split kernel (each tile's buffer descriptor,
+ * whose range bounds every lane's load of that tile, the item's query rows
+ * and its partial rows) and every (sequence, head) row of the combine (its
+ * unit tables, the partials it merges, its output row and lse), with the
+ * kernel arguments the entry point builds and the kernels' own index
+ * arithmetic.  Allocations are sized from the lengths: q and out [P*G, Hq, D]
+ * bf16, lse [P*G, Hq] fp32, the prefix and suffix K/V [rows, Hkv, D] bf16 in
+ * shape->kv_layout, the workspace as rl_decode_attn_workspace_size gives
+ * it.  shrink_region as for rl_debug_logprob_bounds; regions: q, k_prefix,
+ * v_prefix, k_suffix, v_suffix, out, lse, workspace, and the workspace's
+ * sections: work list and unit tables (the upload), work list, prefix units,
+ * suffix units, partial max, partial sum, partial values.  No device access;
+ * for tests.  Returns the plan's status for invalid lengths,
+ * RL_ERR_NULL_POINTER for a NULL report; otherwise RL_OK with the counts in
+ * *report (all zero when P*G = 0).
+ */
+rl_status rl_debug_decode_bounds(const rl_decode_shape *shape, const rl_decode_lens *lens, int32_t shrink_region,
+                                 rl_bounds_report *report);
+
+/*
  * Debug timeline of rl_token_logprob, to see where a tile's time goes: the
  * same call (arguments, plan, outputs and arithmetic), with the tile
  * launches (whole tiles, narrow tiles of a last round, hidden-dimension parts

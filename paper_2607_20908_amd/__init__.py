@@ -97,7 +97,7 @@ EXPORTS = ["rl_decode_attn_workspace_size", "rl_decode_attn", "rl_token_logprob_
            "rl_sample_top_p_workspace_size", "rl_sample_top_p", "rl_kv_append_workspace_size",
            "rl_kv_append", "rl_extend_attn_workspace_size", "rl_extend_attn", "rl_debug_logprob_bounds",
            "rl_token_logprob_noalloc", "rl_debug_logprob_timeline", "rl_debug_decode_timeline",
-           "rl_debug_extend_bounds"]
+           "rl_debug_extend_bounds", "rl_debug_decode_bounds"]
 
 
 def _load():
@@ -146,6 +146,8 @@ def _load():
     lib.rl_debug_logprob_bounds.argtypes = [I32, I64, I32, I32, I32, I32, ctypes.POINTER(BoundsReport)]
     lib.rl_debug_extend_bounds.restype = ctypes.c_int
     lib.rl_debug_extend_bounds.argtypes = [P, P, I32, I32, ctypes.POINTER(BoundsReport)]
+    lib.rl_debug_decode_bounds.restype = ctypes.c_int
+    lib.rl_debug_decode_bounds.argtypes = [P, P, I32, ctypes.POINTER(BoundsReport)]
     lib.rl_token_logprob_noalloc.restype = ctypes.c_int
     lib.rl_token_logprob_noalloc.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P]
     lib.rl_debug_decode_timeline.restype = ctypes.c_int
@@ -253,6 +255,18 @@ def decode_attn_workspace_size(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffi
     _check(_lib.rl_decode_attn_workspace_size(ctypes.byref(a.shape), ctypes.byref(a.lens),
                                               ctypes.byref(n)), "rl_decode_attn_workspace_size")
     return n.value
+
+
+def decode_bounds(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix_len, prefix_rows, suffix_rows,
+                  split_tokens: int = 0, kv_layout: str = "token", shrink_region: int = -1) -> "BoundsReport":
+    """Host replay of the global accesses of rl_decode_attn for these lengths
+    (no device access)."""
+    a = _DecodeArgs(P, G, Hq, Hkv, D, 1.0 / math.sqrt(D), split_tokens, prefix_start, prefix_len,
+                    suffix_start, suffix_len, prefix_rows, suffix_rows, kv_layout)
+    rep = BoundsReport()
+    _check(_lib.rl_debug_decode_bounds(ctypes.byref(a.shape), ctypes.byref(a.lens), shrink_region,
+                                       ctypes.byref(rep)), "rl_debug_decode_bounds")
+    return rep
 
 
 def decode_plan(P, G, Hq, Hkv, D, prefix_start, prefix_len, suffix_start, suffix_len,

@@ -11,6 +11,7 @@
 
 #include "abi_error.h"
 #include "kernels.h"
+#include "decode_args.h"
 #include "extend_args.h"
 #include "logprob_args.h"
 #include "plan.h"
@@ -331,32 +332,7 @@ rl_status decode_call(const rl_decode_shape *shape, const rl_decode_lens *lens, 
     st = stage_upload(plan, ws, hs);
     if (st != RL_OK) return st;
 
-    rlk::DecodeArgs a{};
-    a.q = static_cast<const uint16_t *>(ptrs->q);
-    a.k_prefix = static_cast<const uint16_t *>(ptrs->k_prefix);
-    a.v_prefix = static_cast<const uint16_t *>(ptrs->v_prefix);
-    a.k_suffix = static_cast<const uint16_t *>(ptrs->k_suffix);
-    a.v_suffix = static_cast<const uint16_t *>(ptrs->v_suffix);
-    a.out = static_cast<uint16_t *>(ptrs->out);
-    a.lse = ptrs->lse;
-    a.items = reinterpret_cast<const rlk::DevItem *>(ws + plan.off_items);
-    a.prefix_units = reinterpret_cast<const rlk::DevUnit *>(ws + plan.off_prefix_units);
-    a.suffix_units = reinterpret_cast<const rlk::DevUnit *>(ws + plan.off_suffix_units);
-    a.pm = reinterpret_cast<float *>(ws + plan.off_m);
-    a.pl = reinterpret_cast<float *>(ws + plan.off_l);
-    a.pacc = reinterpret_cast<float *>(ws + plan.off_acc);
-    a.n_items = static_cast<int32_t>(n_items);
-    a.P = plan.P;
-    a.G = plan.G;
-    a.Hq = plan.Hq;
-    a.Hkv = plan.Hkv;
-    a.r = plan.r;
-    a.D = plan.D;
-    a.kv_layout = plan.kv_layout;
-    a.deep_prefetch = plan.deep_prefetch;
-    a.prefix_rows = plan.prefix_rows;
-    a.suffix_rows = plan.suffix_rows;
-    a.score_scale_log2 = plan.scale * rlk::kLog2eHost;
+    rlk::DecodeArgs a = rlk::decode_args(plan, *ptrs, ws);
     a.release = stage_release();
     a.timeline = records;
     const hipError_t e = rlk::launch_decode(a, hs, num_records != nullptr);

@@ -21,6 +21,8 @@
 #include <thread>
 #include <vector>
 
+#include "decode_args.h"
+#include "decode_index.h"
 #include "extend_args.h"
 #include "extend_index.h"
 #include "kernels.h"
@@ -668,6 +670,118 @@ extern "C" rl_status rl_debug_extend_bounds(const rl_decode_shape *shape, const 
                     }
                 }
             }
+    });
+    rp.report(report);
+    return RL_OK;
+}
+
+// Host replay of rl_decode_attn's global accesses (see the header).
+extern "C" rl_status rl_debug_decode_bounds(const rl_decode_shape *shape, const rl_decode_lens *lens,
+                                            int32_t shrink_region, rl_bounds_report *report) {
+    using namespace rlk;
+    if (!report) return RL_ERR_NULL_POINTER;
+    std::memset(report, 0, sizeof(*report));
+    std::string err;
+    DecodePlan plan;
+    const rl_status st = plan_decode(shape, lens, &plan, &err, PlanDetail::kDevice);
+    if (st != RL_OK) return st;
+    const int64_t S = static_cast<int64_t>(plan.P) * plan.G;
+    if (S == 0) return RL_OK;
+    Replay rp(false, shrink_region);
+    const int64_t D = plan.D, Hq = plan.Hq, Hkv = plan.Hkv;
+    const int q_r = rp.add("q", static_cast<uint64_t>(S) * Hq * D * 2);
+    const int kp_r = rp.add("k_prefix", static_cast<uint64_t>(plan.prefix_rows) * Hkv * D * 2);
+    const int vp_r = rp.add("v_prefix", static_cast<uint64_t>(plan.prefix_rows) * Hkv * D * 2);
+    const int ks_r = rp.add("k_suffix", static_cast<uint64_t>(plan.suffix_rows) * Hkv * D * 2);
+    const int vs_r = rp.add("v_suffix", static_cast<uint64_t>(plan.suffix_rows) * Hkv * D * 2);
+    const int out_r = rp.add("out", static_cast<uint64_t>(S) * Hq * D * 2);
+    const int lse_r = rp.add("lse", static_cast<uint64_t>(S) * Hq * 4);
+    const int ws_r = rp.add("workspace", plan.total_bytes);
+    const int meta_r = rp.section("workspace work list and unit tables", ws_r, 0, plan.meta_bytes);
+    const int items_r = rp.section("workspace work list", ws_r, plan.off_items, plan.dev_items.size() * sizeof(DevItem));
+    const int pu_r = rp.section("workspace prefix units", ws_r, plan.off_prefix_units, plan.prefix_units.size() * sizeof(DevUnit));
+    const int su_r = rp.section("workspace suffix units", ws_r, plan.off_suffix_units, plan.suffix_units.size() * sizeof(DevUnit));
+    const uint64_t prow = static_cast<uint64_t>(plan.partial_rows);
+    const int pm_r = rp.section("workspace partial max", ws_r, plan.off_m, prow * 4);
+    const int pl_r = rp.section("workspace partial sum", ws_r, plan.off_l, prow * 4);
+    const int pa_r = rp.section("workspace partial values", ws_r, plan.off_acc, prow * D * 4);
+    rl_decode_ptrs ptrs{};
+    ptrs.q = rp.ptr<void>(q_r);
+    ptrs.k_prefix = rp.ptr<void>(kp_r);
+    ptrs.v_prefix = rp.ptr<void>(vp_r);
+    ptrs.k_suffix = rp.ptr<void>(ks_r);
+    ptrs.v_suffix = rp.ptr<void>(vs_r);
+    ptrs.out = rp.ptr<void>(out_r);
+    ptrs.lse = rp.ptr<float>(lse_r);
+    const DecodeArgs a = decode_args(plan, ptrs, rp.ptr<unsigned char>(ws_r));
+    // the work list and unit tables' upload: one copy of meta_bytes (16 bytes
+    // per thread) into the start of the workspace
+    rp.launch("plan_fetch_kernel", 1, [&](int64_t, Replay::Lane &ln) {
+        ln.thread = 0;
+        ln.check(meta_r, Replay::addr(a.items), 16, "work list upload (first)");
+        ln.check(meta_r, Replay::addr(a.items) + plan.meta_bytes - 16, 16, "work list upload (last)");
+    });
+    rp.launch("decode_split_kernel", a.n_items, [&](int64_t b, Replay::Lane &ln) {
+        const DevItem &it = plan.dev_items[static_cast<size_t>(b)];
+        ln.thread = 0;
+        ln.check(items_r, Replay::addr(a.items) + b * sizeof(DevItem), sizeof(DevItem), "work item load");
+        const int kh = dec_kh(it.meta);
+        const bool is_suffix = dec_is_suffix(it.meta);
+        const int row_begin = dec_row_begin(it.meta);
+        const int rows = dec_item_rows(dec_unit_rows(a, is_suffix), row_begin);
+        const int ntok = dec_ntok(it.meta);
+        const int64_t stride = dec_tok_stride(a, static_cast<int>(D));
+        const int64_t base = dec_kv_base(a, it, DecItem{kh, is_suffix}, static_cast<int>(D));
+        const uint64_t kg = Replay::addr(is_suffix ? a.k_suffix : a.k_prefix) + base * 2;
+        const uint64_t vg = Replay::addr(is_suffix ? a.v_suffix : a.v_prefix) + base * 2;
+        const int kr = is_suffix ? ks_r : kp_r, vr = is_suffix ? vs_r : vp_r;
+        // every tile's buffer descriptor lies inside its buffer (the hardware
+        // clamps each lane's offset to the descriptor's range); the loads past
+        // the last tile have empty ranges
+        const int ntiles = (ntok + kTileTokens - 1) / kTileTokens;
+        for (int t = 0; t < ntiles; ++t) {
+            const int t0 = t * kTileTokens;
+            const int64_t first = dec_tile_first(t0, ntok, stride);
+            const int range = dec_tile_range(t0, ntok, stride, static_cast<int>(D));
+            ln.check(kr, kg + first * 2, static_cast<uint64_t>(range), "K tile descriptor");
+            ln.check(vr, vg + first * 2, static_cast<uint64_t>(range), "V tile descriptor");
+        }
+        // the queries and the partials of the item's rows
+        for (int i = 0; i < rows; ++i) {
+            ln.thread = i;
+            const int64_t qoff = dec_q_off(a, it, DecItem{kh, is_suffix}, row_begin + i, static_cast<int>(D));
+            ln.check(q_r, Replay::addr(a.q) + qoff * 2, static_cast<uint64_t>(D) * 2, "query row load");
+            const int64_t pr = static_cast<int64_t>(it.partial_row0) + i;
+            ln.check(pa_r, Replay::addr(a.pacc) + pr * D * 4, static_cast<uint64_t>(D) * 4, "partial values store");
+            ln.check(pm_r, Replay::addr(a.pm) + pr * 4, 4, "partial max store");
+            ln.check(pl_r, Replay::addr(a.pl) + pr * 4, 4, "partial sum store");
+        }
+    });
+    const int64_t rows = S * Hq;
+    rp.launch("decode_combine_kernel", rows, [&](int64_t idx, Replay::Lane &ln) {
+        ln.thread = 0;
+        const int64_t s = idx / a.Hq;
+        const int h = static_cast<int>(idx % a.Hq);
+        const int64_t p = s / a.G;
+        const int g = static_cast<int>(s % a.G);
+        const int kh = h / a.r, hr = h % a.r;
+        ln.check(pu_r, Replay::addr(a.prefix_units) + p * sizeof(DevUnit), sizeof(DevUnit), "prefix unit load");
+        ln.check(su_r, Replay::addr(a.suffix_units) + s * sizeof(DevUnit), sizeof(DevUnit), "suffix unit load");
+        const DevUnit pu = plan.prefix_units[static_cast<size_t>(p)];
+        const DevUnit su = plan.suffix_units[static_cast<size_t>(s)];
+        const int64_t Mp = static_cast<int64_t>(a.G) * a.r;
+        const int pn = static_cast<int>(pu.nchunks);
+        const int n = pn + static_cast<int>(su.nchunks);
+        const int64_t pbase = dec_prefix_partial_base(pu, kh, Mp, g, a.r, hr);
+        const int64_t sbase = dec_suffix_partial_base(su, kh, a.r, hr);
+        for (int j = 0; j < n; ++j) {
+            const int64_t pr = dec_partial_row(pbase, sbase, Mp, pn, a.r, j);
+            ln.check(pm_r, Replay::addr(a.pm) + pr * 4, 4, "partial max load");
+            ln.check(pl_r, Replay::addr(a.pl) + pr * 4, 4, "partial sum load");
+            ln.check(pa_r, Replay::addr(a.pacc) + pr * D * 4, static_cast<uint64_t>(D) * 4, "partial values load");
+        }
+        ln.check(out_r, Replay::addr(a.out) + idx * D * 2, static_cast<uint64_t>(D) * 2, "output row store");
+        ln.check(lse_r, Replay::addr(a.lse) + idx * 4, 4, "lse store");
     });
     rp.report(report);
     return RL_OK;

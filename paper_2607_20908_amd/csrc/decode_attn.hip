@@ -19,6 +19,7 @@
 // (sequence, head) by log-sum-exp and writes the bf16 output and fp32 lse.
 #include <algorithm>
 
+#include "decode_index.h"
 #include "device_common.h"
 #include "kernels.h"
 
@@ -91,25 +92,20 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
     const DevItem it = a.items[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g4 = lane >> 4, l16 = lane & 15;
-    const int kh = (it.meta >> 16) & 255;
-    const bool is_suffix = (it.meta >> 15) & 1;
-    const int row_begin = static_cast<int>(it.meta >> 24) * kMaxItemRows;
-    const int M = is_suffix ? a.r : a.G * a.r;
-    const int rows = min(kMaxItemRows, M - row_begin);
+    const int kh = dec_kh(it.meta);
+    const bool is_suffix = dec_is_suffix(it.meta);
+    const int row_begin = dec_row_begin(it.meta);
+    const int M = dec_unit_rows(a, is_suffix);
+    const int rows = dec_item_rows(M, row_begin);
     const int n_ct = (rows + 15) >> 4;
     const int Wc = n_ct == 1 ? 1 : (n_ct == 2 ? 2 : 4);
     const int Wt = 4 / Wc;
     const int nst = kSubPerTile / Wt;            // sub-tiles per wave per tile
     const int wc = wave % Wc, wt = wave / Wc;
     const bool mine = wc < n_ct;                 // this wave has a column tile
-    const int ntok = static_cast<int>(it.meta & 0x7fff);
-    // token-major [rows, Hkv, D]: rows of one kv head are Hkv*D apart;
-    // head-major [Hkv, rows, D]: they are contiguous
-    const bool head_major = a.kv_layout == RL_KV_HEAD_MAJOR;
-    const int64_t nrows = is_suffix ? a.suffix_rows : a.prefix_rows;
-    const int64_t tok_stride = head_major ? D : static_cast<int64_t>(a.Hkv) * D;
-    const int64_t kv_row0 = it.kv_row0;
-    const int64_t base = head_major ? (kh * nrows + kv_row0) * D : (kv_row0 * a.Hkv + kh) * D;
+    const int ntok = dec_ntok(it.meta);
+    const int64_t tok_stride = dec_tok_stride(a, D);
+    const int64_t base = dec_kv_base(a, it, DecItem{kh, is_suffix}, D);
     const uint16_t *kg = (is_suffix ? a.k_suffix : a.k_prefix) + base;
     const uint16_t *vg = (is_suffix ? a.v_suffix : a.v_prefix) + base;
 
@@ -121,10 +117,7 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
         int64_t qoff = 0;
         if (ok) {
             const int ig = row_begin + i;            // row within the unit
-            int s, h;
-            if (is_suffix) { s = it.unit; h = kh * a.r + ig; }
-            else           { s = it.unit * a.G + ig / a.r; h = kh * a.r + ig % a.r; }
-            qoff = (static_cast<int64_t>(s) * a.Hq + h) * D;
+            qoff = dec_q_off(a, it, DecItem{kh, is_suffix}, ig, D);
         }
 #pragma unroll
         for (int kk = 0; kk < C::KK; ++kk) {
@@ -148,16 +141,14 @@ __global__ __launch_bounds__(kThreads, PF == 2 ? kSplitBlocksPerCUDeep : kSplitB
     uint32_t voff[C::LD];
 #pragma unroll
     for (int j = 0; j < C::LD; ++j) {
-        const int idx = tid + j * kThreads;
-        voff[j] = static_cast<uint32_t>((idx / C::CH) * tok_stride * 2 + (idx % C::CH) * 16);
+        voff[j] = dec_load_off(tid + j * kThreads, C::CH, tok_stride);
     }
     auto load_tile = [&](int tile, u32x4 (&kr)[C::LD], u32x4 (&vr)[C::LD]) {
         // a tile past the chunk gets an empty range: its loads touch no memory
         // and return zeros, so every step issues the same loads
         const int t0 = tile * kTileTokens;
-        const bool in = t0 < ntok;
-        const int64_t first = in ? static_cast<int64_t>(t0) * tok_stride : 0;
-        const int range = in ? static_cast<int>((static_cast<int64_t>(ntok - t0 - 1) * tok_stride + D) * 2) : 0;
+        const int64_t first = dec_tile_first(t0, ntok, tok_stride);
+        const int range = dec_tile_range(t0, ntok, tok_stride, D);
         const __amdgpu_buffer_rsrc_t rk =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(kg + first), 0, range, 0x00020000);
         const __amdgpu_buffer_rsrc_t rv =
@@ -411,11 +402,9 @@ __global__ __launch_bounds__(kThreads, NB == 4 ? 8 : 1) void decode_combine_kern
     const int pn = static_cast<int>(pu.nchunks);
     const int n = live ? pn + static_cast<int>(su.nchunks) : 0;
     // this kv head's partial rows of the prompt's prefix and the candidate's suffix
-    const int64_t pbase = pu.base + static_cast<int64_t>(kh) * pu.nchunks * Mp + g * a.r + hr;
-    const int64_t sbase = su.base + static_cast<int64_t>(kh) * su.nchunks * a.r + hr;
-    auto prow = [&](int j) -> int64_t {
-        return j < pn ? pbase + j * Mp : sbase + static_cast<int64_t>(j - pn) * a.r;
-    };
+    const int64_t pbase = dec_prefix_partial_base(pu, kh, Mp, g, a.r, hr);
+    const int64_t sbase = dec_suffix_partial_base(su, kh, a.r, hr);
+    auto prow = [&](int j) -> int64_t { return dec_partial_row(pbase, sbase, Mp, pn, a.r, j); };
     auto row_max = [](float v) {
 #pragma unroll
         for (int o = LPR / 2; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

@@ -254,3 +254,69 @@ def test_extend_bounds_arguments():
     with pytest.raises(rk.RLError):
         _extend(1, 2, 8, 8, 64, [10], [5, 6], [6, 0])     # more new tokens than the suffix holds
     assert rk.lib().rl_debug_extend_bounds(None, None, 0, -1, None) == 1
+
+
+# ---------------------------------------------------------------- decode
+# rl_debug_decode_bounds replays rl_decode_attn: the work list's upload, every
+# item of the split kernel (each tile's buffer descriptor, the item's query
+# and partial rows) and every row of the combine, through the kernels' own
+# index functions (csrc/decode_index.h).
+def _decode(P, G, Hq, Hkv, D, lp, ls, layout="head", split=0, gap=0, shrink=-1):
+    lp, ls = np.asarray(lp, np.int32), np.asarray(ls, np.int32)
+    return rk.decode_bounds(P, G, Hq, Hkv, D, _packed(lp + gap), lp, _packed(ls + gap), ls, int((lp + gap).sum()),
+                            int((ls + gap).sum()), split_tokens=split, kv_layout=layout, shrink_region=shrink)
+
+
+def _decode_workload(name):
+    cfg = W.DECODE_CONFIGS[name]
+    return (cfg.num_prompts, cfg.group_size, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+            np.full(cfg.num_prompts, cfg.prefix_len, np.int32), W.suffix_lengths(cfg, 0))
+
+
+def _decode_ragged(seed, P, G, Hq, Hkv, D):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    lp = rng.integers(1, 700, P)
+    lp[0] = 0 if P > 1 else lp[0]                 # a prompt without a prefix
+    return P, G, Hq, Hkv, D, lp, rng.integers(1, 900, P * G)
+
+
+@pytest.mark.parametrize("name", ["tiny", "8b", "32b", "longctx"])
+@pytest.mark.parametrize("layout", ["head", "token"])
+def test_decode_accesses_inside_their_allocations(name, layout):
+    rep = _decode(*_decode_workload(name), layout=layout)
+    assert rep.accesses > 0 and rep.launches == 3 and rep.regions == 15
+    assert rep.violations == 0, rep.first_violation.decode()
+
+
+@pytest.mark.parametrize("case", [(1, 3, 2, 12, 4, 128), (2, 4, 3, 8, 8, 64), (3, 2, 40, 64, 8, 128),
+                                  (4, 1, 1, 128, 1, 128)],
+                         ids=["r3", "r1-D64", "G40-r8-wide", "G1-r128"])
+@pytest.mark.parametrize("layout", ["head", "token"])
+@pytest.mark.parametrize("split,gap", [(0, 0), (48, 3)])
+def test_decode_ragged(case, layout, split, gap):
+    rep = _decode(*_decode_ragged(*case), layout=layout, split=split, gap=gap)
+    assert rep.accesses > 0
+    assert rep.violations == 0, rep.first_violation.decode()
+
+
+DECODE_TIGHT = {"q": 0, "k_prefix": 1, "v_prefix": 2, "k_suffix": 3, "v_suffix": 4, "out": 5, "lse": 6,
+                "work list and unit tables": 8, "work list": 9, "prefix units": 10, "suffix units": 11,
+                "partial max": 12, "partial sum": 13, "partial values": 14}
+
+
+@pytest.mark.parametrize("layout", ["head", "token"])
+def test_decode_shrunk_allocation_is_caught(layout):
+    args = _decode_ragged(3, 2, 40, 64, 8, 128)
+    args = args[:5] + (np.maximum(args[5], 1),) + args[6:]      # every prompt with a prefix
+    for name, i in DECODE_TIGHT.items():
+        rep = _decode(*args, layout=layout, split=48, shrink=i)
+        assert rep.violations > 0, f"shrinking {name} went unnoticed"
+    assert _decode(*args, layout=layout, split=48, shrink=7).violations == 0   # the workspace's own extent
+
+
+def test_decode_bounds_arguments():
+    rep = _decode(0, 4, 8, 8, 64, [], [])
+    assert rep.launches == 0 and rep.accesses == 0
+    with pytest.raises(rk.RLError):
+        _decode(1, 2, 8, 3, 64, [4], [5, 6])        # Hq not a multiple of Hkv
+    assert rk.lib().rl_debug_decode_bounds(None, None, -1, None) == 1
