@@ -623,10 +623,12 @@ def timeline_report(rk, y, evict, desc: str) -> str:
 
 def timeline_markdown(r: np.ndarray, same: bool, wbytes: int, desc: str, plain_ms: float = None,
                       stamped_ms: float = None) -> str:
-    """Markdown summary of timeline records (int64 [n, 8], 4 consecutive
-    records per workgroup; word layout in rl_kernels.h); plain_ms and
-    stamped_ms are the whole call's event times without and with the stamps."""
+    """Markdown summary of timeline records (int64 [n, 8], one per wave, the
+    waves of a workgroup consecutive; word layout in rl_kernels.h); plain_ms
+    and stamped_ms are the whole call's event times without and with the
+    stamps."""
     hw = r[:, 0] & 0xFFFFFFFF
+    wpg = int(((r[:, 0] >> 48) & 0xFF).max()) + 1    # waves per workgroup
     xcc = (r[:, 0] >> 32) & 0xFF
     kind = (r[:, 0] >> 40) & 0xFF
     t_start, t_loop0, t_loop1, t_end = (r[:, i] for i in range(1, 5))
@@ -644,7 +646,7 @@ def timeline_markdown(r: np.ndarray, same: bool, wbytes: int, desc: str, plain_m
            f"{'bit-identical to' if same else 'NOT identical to'} rl_token_logprob's), after a 1 GiB read that "
            "empties the caches.  Wall clock: s_memrealtime (100 MHz); cycles: s_memtime (its rate is not the shader "
            "clock's: compare the MFMA-busy counters).  Per workgroup the "
-           "earliest start and the latest end of its 4 waves; waits and cycles averaged over the waves.  The stage-end "
+           f"earliest start and the latest end of its {wpg} waves; waits and cycles averaged over the waves.  The stage-end "
            "wait (loads of the next stage, then the barrier) is sampled in one stage of every 8.", "",
            "| launch | workgroups | stages | first start - last end (us) | tile us p10/p50/p90 | "
            "prologue us | loop us | epilogue us | ns per stage | stage-end wait share | s_memtime cycles per ns |",
@@ -652,8 +654,8 @@ def timeline_markdown(r: np.ndarray, same: bool, wbytes: int, desc: str, plain_m
     per_kind = {}
     for k in sorted(set(kind.tolist())):
         m = kind == k
-        n = int(m.sum()) // 4
-        g = lambda v: v[m].reshape(n, 4)
+        n = int(m.sum()) // wpg
+        g = lambda v: v[m].reshape(n, wpg)
         st, lo0, lo1, en = g(t_start).min(1), g(t_loop0).max(1), g(t_loop1).max(1), g(t_end).max(1)
         wt, cy, ns = g(wait).mean(1), g(cyc).mean(1), g(nks)[:, 0]
         wall_loop = (lo1 - lo0) * 10.0     # ns

@@ -80,7 +80,7 @@
 extern "C" {
 #endif
 
-#define RL_ABI_VERSION 12
+#define RL_ABI_VERSION 13
 
 typedef enum {
     RL_OK = 0,
@@ -604,8 +604,9 @@ rl_status rl_debug_decode_bounds(const rl_decode_shape *shape, const rl_decode_l
  *   [6] s_memtime cycles of the loop (s_memtime counts at a rate of its
  *       own, not the shader clock)
  *   [7] workgroup index | hidden-dimension stages << 32 | sampled stages << 48
- * Whole-tile workgroup b, wave w writes record 4 b + w; the narrow tiles and
- * then the tail parts follow in the same way.  *num_records gets the number
+ * The tile workgroups have 8 waves: whole-tile workgroup b, wave w writes
+ * record 8 b + w; the narrow tiles and then the tail parts follow in the same
+ * way.  *num_records gets the number
  * of records the call writes; with records == NULL only that number is
  * computed (no launch, no other pointer checked).  A stamp makes the wave
  * wait for the scalar read that returns it, so the sampled stages run a

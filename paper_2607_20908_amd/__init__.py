@@ -155,7 +155,7 @@ def _load():
     lib.rl_debug_logprob_timeline.restype = ctypes.c_int
     lib.rl_debug_logprob_timeline.argtypes = [I64, I32, I32, P, P, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P, I64,
                                               ctypes.POINTER(ctypes.c_int64), P]
-    if lib.rl_abi_version() != 12:
+    if lib.rl_abi_version() != 13:
         raise ImportError("librlkern ABI version mismatch")
     return lib
 

@@ -16,6 +16,7 @@
 #include "logprob_args.h"
 #include "plan.h"
 #include "rl_kernels.h"
+#include "tile_index.h"
 
 namespace {
 
@@ -438,10 +439,10 @@ rl_status rl_debug_logprob_timeline(int64_t rows, int32_t hidden, int32_t vocab,
     std::string err;
     rl_status st = rlk::plan_logprob(rows, hidden, vocab, &plan, &err);
     if (st != RL_OK) return set_error(st, err);
-    // one record per wave (4 per workgroup) of the whole-tile, narrow-tile
-    // and tail-part launches
-    const int64_t need =
-        (plan.n_dp_tiles + plan.narrow_tiles * plan.n_row_tiles + plan.n_tail_tiles * plan.tail_splits) * 4;
+    // one record per wave (kTileWaves per workgroup) of the whole-tile,
+    // narrow-tile and tail-part launches
+    const int64_t need = (plan.n_dp_tiles + plan.narrow_tiles * plan.n_row_tiles +
+                          plan.n_tail_tiles * plan.tail_splits) * rlk::kTileWaves;
     if (!records) {
         *num_records = need;
         return RL_OK;

@@ -155,12 +155,13 @@ struct TileRegions {
     int hidden, w, target, pm, pl, zt, part, lse_in, probs, inv_t, logits;
 };
 
-// logprob_tile_kernel<WS, MODE, TM> over `blocks` workgroups of 256 threads.
+// logprob_tile_kernel<WS, MODE, TM> over `blocks` workgroups of kTileWaves
+// wave64s.
 void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const LogprobArgs &a, int64_t blocks,
                  const TileRegions &rg) {
     rp.launch(name, blocks, [&](int64_t b, Replay::Lane &ln) {
         const TileCoord tc = tile_coord(mode, TM, b, a);
-        const int VW = 64 * TM, WBLK = VW / 32;
+        const int VW = 64 * TM, WBLK = VW / 64, HBLK = 32 / kTileWaves;   // 1 KB blocks per wave per stage
         const int64_t H = a.H, r0 = tc.rt * kRowTile;
         const int wlast = stage_last(VW, a.V, tc.v0), hlast = stage_last(kRowTile, a.R, r0);
         ln.thread = 0;
@@ -172,7 +173,7 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
         const uint64_t hg = Replay::addr(a.hidden) + static_cast<uint64_t>(r0 * H) * 2;
         // the hidden rows of slots 0 .. nks + 1, the weights of 0 .. nks - 1 + WS
         const std::vector<int> hs = stage_slots(rp, tc.nks, tc.nks + 1), ws = stage_slots(rp, tc.nks, tc.nks - 1 + WS);
-        for (int wave = 0; wave < 4; ++wave)
+        for (int wave = 0; wave < kTileWaves; ++wave)
             for (int lane = 0; lane < 64; ++lane) {
                 ln.thread = wave * 64 + lane;
                 for (int j = 0; j < WBLK; ++j) {
@@ -180,24 +181,24 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
                     const uint32_t voff = stage_voff(row, wlast, H, stage_chunk(row, lane));
                     for (int slot : ws) ln.check(rg.w, wg + stage_k0(tc.kb, slot, tc.nks) * 2 + voff, 16, "weight stage load");
                 }
-                for (int j = 0; j < 8; ++j) {
-                    const int row = stage_row(wave * 8 + j, lane);
+                for (int j = 0; j < HBLK; ++j) {
+                    const int row = stage_row(wave * HBLK + j, lane);
                     const uint32_t voff = stage_voff(row, hlast, H, stage_chunk(row, lane));
                     for (int slot : hs) ln.check(rg.hidden, hg + stage_k0(tc.kb, slot, tc.nks) * 2 + voff, 16, "hidden stage load");
                 }
             }
         // epilogues
         const uint64_t tgt = Replay::addr(a.target);
-        for (int wave = 0; wave < 4; ++wave) {
-            const int wm = wave & 1, wn = wave >> 1;
+        for (int wave = 0; wave < kTileWaves; ++wave) {
+            const int wm = wave & 1, wn = wave >> 1;   // vocab half, 64-row quarter
             for (int lane = 0; lane < 64; ++lane) {
                 ln.thread = wave * 64 + lane;
                 const int l32 = lane & 31, h2 = lane >> 5;
                 if (mode == kLogits) {
                     // the tempered logits of the wave's 32 TM vocab entries
                     const int64_t vbase = tc.v0 + wm * 32 * TM;
-                    for (int tn = 0; tn < 4; ++tn) {
-                        const int64_t rr = r0 + wn * 128 + tn * 32 + l32;
+                    for (int tn = 0; tn < 2; ++tn) {
+                        const int64_t rr = r0 + wn * 64 + tn * 32 + l32;
                         if (rr >= a.R) continue;
                         ln.check(rg.inv_t, Replay::addr(a.inv_t_rows) + rr * 4, 4, "inverse temperature load");
                         for (int tm = 0; tm < TM; ++tm)
@@ -210,14 +211,14 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
                 }
                 if (mode == kPartialK) {
                     for (int tm = 0; tm < 4; ++tm)
-                        for (int tn = 0; tn < 4; ++tn)
+                        for (int tn = 0; tn < 2; ++tn)
                             for (int q = 0; q < 4; ++q)
-                                ln.check(rg.part, Replay::addr(a.part) + part_elem(b, wave, tm, tn, q, lane) * 4, 16,
-                                         "tail part store");
+                                ln.check(rg.part, Replay::addr(a.part) + part_elem(b, wm, wn * 2 + tn, tm, q, lane) * 4,
+                                         16, "tail part store");
                     continue;
                 }
-                for (int tn = 0; tn < 4; ++tn) {
-                    const int row = wn * 128 + tn * 32 + l32;
+                for (int tn = 0; tn < 2; ++tn) {
+                    const int row = wn * 64 + tn * 32 + l32;
                     const int64_t rr = r0 + row;
                     if (mode == kBwdProbs) {
                         if (rr < a.R) {
@@ -258,25 +259,24 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
 void replay_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegions &rg) {
     rp.launch("logprob_tail_reduce_kernel", t.tail_tiles * 8, [&](int64_t b, Replay::Lane &ln) {
         const int64_t j = b >> 3;
-        const int wn = (b >> 2) & 1, tn = b & 3;
+        const int rb = static_cast<int>(b & 7);
         int64_t vt, rt;
         tile_of_logical(t.tile_base + j, t.n_vocab_tiles, t.n_row_tiles, &vt, &rt);
         for (int tid = 0; tid < 128; ++tid) {
             ln.thread = tid;
             const int wm = tid >> 6, lane = tid & 63, l32 = lane & 31;
-            const int wave = wn * 2 + wm;
             for (int sp = 0; sp < t.splits; ++sp)
                 for (int tm = 0; tm < 4; ++tm)
                     for (int q = 0; q < 4; ++q)
-                        ln.check(rg.part, Replay::addr(t.part) + part_elem(j * t.splits + sp, wave, tm, tn, q, lane) * 4,
+                        ln.check(rg.part, Replay::addr(t.part) + part_elem(j * t.splits + sp, wm, rb, tm, q, lane) * 4,
                                  16, "tail part load");
-            const int64_t rr = rt * kRowTile + wn * 128 + tn * 32 + l32;
+            const int64_t rr = rt * kRowTile + rb * 32 + l32;
             if (rr < t.R) {
                 ln.check(rg.target, Replay::addr(t.target) + rr * 4, 4, "target load");
                 ln.check(rg.zt, Replay::addr(t.zt) + rr * 4, 4, "target logit store");
             }
             if (tid < 32) {
-                const int64_t r = rt * kRowTile + wn * 128 + tn * 32 + tid;
+                const int64_t r = rt * kRowTile + rb * 32 + tid;
                 if (r < t.R) {
                     ln.check(rg.pm, Replay::addr(t.pm) + (vt * t.R + r) * 4, 4, "partial max store");
                     ln.check(rg.pl, Replay::addr(t.pl) + (vt * t.R + r) * 4, 4, "partial sum store");
@@ -291,19 +291,18 @@ void replay_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegions &rg)
 void replay_probs_tail_reduce(Replay &rp, const LogprobArgs &t, const TileRegions &rg) {
     rp.launch("logprob_probs_tail_reduce_kernel", t.tail_tiles * 8, [&](int64_t b, Replay::Lane &ln) {
         const int64_t j = b >> 3;
-        const int wn = (b >> 2) & 1, tn = b & 3;
+        const int rb = static_cast<int>(b & 7);
         int64_t vt, rt;
         tile_of_logical(t.tile_base + j, t.n_vocab_tiles, t.n_row_tiles, &vt, &rt);
         for (int tid = 0; tid < 128; ++tid) {
             ln.thread = tid;
             const int wm = tid >> 6, lane = tid & 63, l32 = lane & 31, h2 = lane >> 5;
-            const int wave = wn * 2 + wm;
             for (int sp = 0; sp < t.splits; ++sp)
                 for (int tm = 0; tm < 4; ++tm)
                     for (int q = 0; q < 4; ++q)
-                        ln.check(rg.part, Replay::addr(t.part) + part_elem(j * t.splits + sp, wave, tm, tn, q, lane) * 4,
+                        ln.check(rg.part, Replay::addr(t.part) + part_elem(j * t.splits + sp, wm, rb, tm, q, lane) * 4,
                                  16, "tail part load");
-            const int row = wn * 128 + tn * 32 + l32;
+            const int row = rb * 32 + l32;
             const int64_t rr = rt * kRowTile + row;
             if (rr < t.R) {
                 ln.check(rg.target, Replay::addr(t.target) + rr * 4, 4, "target load");

@@ -22,6 +22,10 @@ RLK_HD int mini(int a, int b) { return a < b ? a : b; }
 // bf16 elements of one 256 x 64 stage of one operand (32 KB).
 constexpr int kStageElems = kVocabTile * kHiddenStep;
 
+// Wave64s per lm-head tile workgroup: wave w owns vocab half w & 1 (128
+// entries) and token rows 64 (w >> 1) .. 64 (w >> 1) + 63 of the tile.
+constexpr int kTileWaves = 8;
+
 // Element offset of 16-byte chunk c (0..7) of row `row` in a [rows][64] bf16
 // stage image.  Rows are 128 bytes, so two rows share one 256-byte window of
 // the 64 LDS banks; XOR-ing the chunk with row bits 1..3 gives the 16 rows
@@ -121,11 +125,13 @@ RLK_HD TileCoord tile_coord(int mode, int tm, int64_t b, const LogprobArgs &a) {
     return t;
 }
 
-// Element offset, from the tail part buffer, of what lane `lane` of tile
-// kernel wave `wave` holds in accumulator (tm, tn), 4-float group q, for part
-// `part`: each store writes 1 KB contiguously.
-RLK_HD int64_t part_elem(int64_t part, int wave, int tm, int tn, int q, int lane) {
-    return part * (kVocabTile * kRowTile) + (((wave * 16 + tm * 4 + tn) * 4 + q) * 64 + lane) * 4;
+// Element offset, from the tail part buffer, of the 32 x 32 accumulator
+// block of vocab half wm, 32-entry vocab block tm and 32-row block rb (token
+// rows 32 rb .. 32 rb + 31) of part `part`: 4-float group q of lane `lane`
+// in the MFMA's register layout, so each store writes 1 KB contiguously and
+// one block's 16 KB are contiguous.
+RLK_HD int64_t part_elem(int64_t part, int wm, int rb, int tm, int q, int lane) {
+    return part * (kVocabTile * kRowTile) + ((((rb * 2 + wm) * 4 + tm) * 4 + q) * 64 + lane) * 4;
 }
 
 // ---- blocked probabilities of the backward: for row tile rt and vocab

@@ -1,10 +1,11 @@
 // Fused lm-head token log-prob for gfx950.
 //
-// Tile kernel: one workgroup (4 wave64s, one per SIMD) computes the 256 x 256
+// Tile kernel: one workgroup (8 wave64s, two per SIMD) computes the 256 x 256
 // logit tile  Z^T = W_tile * hidden_tile^T  (vocab entries on the M side,
-// token rows on the N side); each wave owns 128 vocab x 128 rows as 4 x 4
-// MFMA 32x32x16 bf16 tiles whose fp32 accumulators live in the AGPRs.  Both
-// operands are hidden-contiguous.  The hidden dimension streams through two
+// token rows on the N side); each wave owns 128 vocab x 64 rows as 4 x 2
+// MFMA 32x32x16 bf16 tiles (fp32 accumulators: 128 registers), so while one
+// wave of a SIMD waits on LDS or issues loads the other keeps the matrix
+// core busy.  Both operands are hidden-contiguous.  The hidden dimension streams through two
 // LDS stages of 64 entries, filled by direct global->LDS loads (no register
 // staging): the loads for stage s+2 are issued right after the barrier that
 // frees stage s's buffer, interleaved with the MFMAs of stage s's last k-step,
@@ -34,9 +35,9 @@ constexpr int kK = kHiddenStep;                 // 64 hidden entries per LDS sta
 constexpr int kTileElems = kVocabTile * kK;     // bf16 elements per operand per stage
 constexpr int kHStages = 2;                     // hidden ring: 2 stages
 static_assert(kVocabTile == kRowTile, "square tiles assumed below");
-constexpr int kTileThreads = 256;               // 4 waves
-constexpr int kBlocksPerWave = kTileElems / 512 / 4;   // 1 KB load blocks per wave per operand per stage
-static_assert(kBlocksPerWave == 8, "staging layout");
+constexpr int kTileThreads = 64 * kTileWaves;  // 8 waves
+constexpr int kBlocksPerWave = kTileElems / 512 / kTileWaves;   // 1 KB hidden load blocks per wave per stage
+static_assert(kBlocksPerWave == 4, "staging layout");
 
 // WS: weight-ring depth.  With few row tiles the hidden rows stay in L2 and
 // only the weights stream from HBM; a third weight stage gives them two
@@ -183,14 +184,14 @@ __device__ __forceinline__ void probs_column(const LogprobArgs &a, Z z, int64_t 
 }
 
 // Forward epilogue of one (64 TM) x 256 logit tile held in the registers of
-// the workgroup's 4 waves (acc[tm][tn][i] of wave (wm, wn), lane (h2, l32)
+// the workgroup's 8 waves (acc[tm][tn][i] of wave (wm, wn), lane (h2, l32)
 // holds vocab v0 + wm*32*TM + tm*32 + 8*(i/4) + 4*h2 + i%4 for token row
-// r0 + wn*128 + tn*32 + l32): per token row the max and the sum of exp2 over
+// r0 + wn*64 + tn*32 + l32): per token row the max and the sum of exp2 over
 // the tile's vocab entries and, if the target falls in the tile, its logit.
 // The partial goes to slot `slot`.  `red` is 4 KB of LDS that the caller no
 // longer uses.
 template <int TM>
-__device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 (&acc)[TM][4], int64_t v0,
+__device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 (&acc)[TM][2], int64_t v0,
                                              int64_t slot, int64_t rt, float (*red)[kRowTile][2]) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -199,21 +200,22 @@ __device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 
     const int64_t r0 = rt * kRowTile;
     const int64_t vbase = v0 + wm * 32 * TM;
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-        const int row = wn * 128 + tn * 32 + l32;
+    for (int tn = 0; tn < 2; ++tn) {
+        const int row = wn * 64 + tn * 32 + l32;
         float mx, sum;
         row_partial<TM>(a, [&](int tm) -> const f32x16 & { return acc[tm][tn]; }, r0 + row, vbase, h2, mx, sum);
         if (h2 == 0) {
             red[wm][row][0] = mx;
             red[wm][row][1] = sum;
         }
-        // keep each row block's accumulator copies local: hoisting the reads
-        // of all four blocks would need 256 more VGPRs
+        // keep each row block's accumulator copies local
         __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
-    const int64_t rr = r0 + tid;                 // 256 threads, 256 rows
-    if (rr < a.R) write_partial(a, slot, rr, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
+    if (tid < kRowTile) {                        // one thread per row of the tile
+        const int64_t rr = r0 + tid;
+        if (rr < a.R) write_partial(a, slot, rr, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
+    }
 }
 
 // TM: 32-entry vocab blocks per wave; a tile spans 64 TM vocab entries (4:
@@ -233,7 +235,8 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     if constexpr (TL) tl_start = __builtin_amdgcn_s_memrealtime();
     constexpr int VW = 64 * TM;                  // vocab entries per tile
     constexpr int WELEMS = VW * kK;              // bf16 elements of one weight stage
-    constexpr int WBLK = VW / 32;                // 1 KB weight blocks per wave per stage
+    constexpr int WBLK = VW / 64;                // 1 KB weight blocks per wave per stage (= TM)
+    constexpr int HBLK = kBlocksPerWave;         // 1 KB hidden blocks per wave per stage
     // WS weight stages + 2 x 32 KB hidden stages; the epilogue's reduction
     // area reuses the weight ring once the loop is done
     __shared__ __attribute__((aligned(16))) uint16_t wring[WS * WELEMS];
@@ -242,7 +245,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;     // vocab half (32 TM entries), row half (128 rows)
+    const int wm = wave & 1, wn = wave >> 1;     // vocab half (32 TM entries), row quarter (64 rows)
     const int l32 = lane & 31, h2 = lane >> 5;
     const TileCoord tc = tile_coord(MODE, TM, blockIdx.x, a);
     const int64_t vt = uniform64(tc.vt), rt = uniform64(tc.rt), v0 = uniform64(tc.v0);   // vt: the tile's partial slot
@@ -250,8 +253,8 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     const int64_t r0 = rt * kRowTile;
     const int64_t H = a.H;
 
-    // ---- staging: each wave fills 2 TM blocks of 8 weight rows and 8 blocks
-    // of 8 hidden rows per stage.
+    // ---- staging: each wave fills TM blocks of 8 weight rows and 4 blocks
+    // of 8 hidden rows per stage (wave w: blocks w TM .. and 4 w ..).
     // Lane i of a block covers row 8*block + i/8 and LDS slot i%8 of that row,
     // which holds chunk (i%8) ^ swizzle(row), so the LDS image is op_off's.
     // Rows past the vocabulary / the batch re-read the last valid row.
@@ -280,15 +283,15 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     auto issue_h = [&](int slot) {
         const uint32_t st = hbuf_l(slot);
 #pragma unroll
-        for (int j = 0; j < kBlocksPerWave; ++j) issue_block(hg, hlast, st, slot, wave * kBlocksPerWave + j);
+        for (int j = 0; j < HBLK; ++j) issue_block(hg, hlast, st, slot, wave * HBLK + j);
     };
 
-    f32x16 acc[TM][4];
+    f32x16 acc[TM][2];
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = f32x16{};
-    bf16x8 fa[2][TM], fb[2][4];
+        for (int tn = 0; tn < 2; ++tn) acc[tm][tn] = f32x16{};
+    bf16x8 fa[2][TM], fb[2][2];
     auto read_frags = [&](int ks, int kq, int p) {
         const uint16_t *as = wbuf(ks);
         const uint16_t *bs = hbuf(ks);
@@ -297,13 +300,13 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         for (int i = 0; i < TM; ++i)
             fa[p][i] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 32 * TM + i * 32 + l32, c));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) fb[p][j] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + j * 32 + l32, c));
+        for (int j = 0; j < 2; ++j) fb[p][j] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 64 + j * 32 + l32, c));
     };
-    auto mfma16 = [&](int p) {
+    auto mfma_step = [&](int p) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < 2; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
     };
 
@@ -320,7 +323,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     issue_h(1);
     issue_w(1);
     if (WS == 3) issue_w(2);
-    wait_vm<kBlocksPerWave + (WS == 3 ? 2 : 1) * WBLK>();   // stage 0 has landed
+    wait_vm<HBLK + (WS == 3 ? 2 : 1) * WBLK>();   // stage 0 has landed
     barrier();
     if constexpr (TL) {
         tl_loop0 = __builtin_amdgcn_s_memrealtime();
@@ -331,13 +334,13 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 #pragma unroll
         for (int kq = 0; kq < kK / 16 - 1; ++kq) {
             read_frags(ks, kq + 1, (kq + 1) & 1);
-            mfma16(kq & 1);
+            mfma_step(kq & 1);
 #pragma unroll
-            for (int i = 0; i < TM + 4; ++i) {
+            for (int i = 0; i < TM + 2; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 4 * TM - (TM + 4), 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM - (TM + 2), 0);
         }
         // last k-step: stage ks+1 has landed (only the weights of stage ks+2
         // may still be in flight) and every wave is done reading stage ks
@@ -352,8 +355,8 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 tl_wait += __builtin_amdgcn_s_memtime() - tl_w0;
                 ++tl_samples;
             }
-        // eight groups of: two global->LDS loads (hidden rows of stage ks+2
-        // in groups 0-3, weights of stage ks+WS in groups 4-7), two MFMAs of
+        // eight groups of: one global->LDS load (hidden rows of stage ks+2
+        // in groups 0-3, weights of stage ks+WS in groups 4-7), one MFMA of
         // this k-step, one fragment read of stage ks+1 (kept in this order:
         // the loads are opaque to the scheduler)
         {
@@ -361,23 +364,15 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             const uint16_t *bs = hbuf(ks + 1);
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
-                if (g < 4) {
-                    issue_block(hg, hlast, hbuf_l(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g);
-                    issue_block(hg, hlast, hbuf_l(ks + 2), ks + 2, wave * kBlocksPerWave + 2 * g + 1);
-                } else {
-#pragma unroll
-                    for (int jj = 2 * (g - 4); jj < 2 * (g - 4) + 2; ++jj)
-                        if (jj < WBLK) issue_block(wg, wlast, wbuf_l(ks + WS), ks + WS, wave * WBLK + jj);
-                }
-#pragma unroll
-                for (int m = 2 * g; m < 2 * g + 2; ++m)
-                    if (m < 4 * TM)
-                        acc[m >> 2][m & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][m >> 2], fb[1][m & 3],
-                                                                                     acc[m >> 2][m & 3], 0, 0, 0);
+                if (g < HBLK) issue_block(hg, hlast, hbuf_l(ks + 2), ks + 2, wave * HBLK + g);
+                else if (g - HBLK < WBLK) issue_block(wg, wlast, wbuf_l(ks + WS), ks + WS, wave * WBLK + (g - HBLK));
+                if (g < 2 * TM)
+                    acc[g >> 1][g & 1] =
+                        __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][g >> 1], fb[1][g & 1], acc[g >> 1][g & 1], 0, 0, 0);
                 if (g < TM)
                     fa[0][g] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 32 * TM + g * 32 + l32, h2));
-                else if (g >= 4)
-                    fb[0][g - 4] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 128 + (g - 4) * 32 + l32, h2));
+                else if (g >= 4 && g < 6)
+                    fb[0][g - 4] = *reinterpret_cast<const bf16x8 *>(bs + op_off(wn * 64 + (g - 4) * 32 + l32, h2));
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -395,7 +390,8 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);    // HW_ID
         const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);  // XCC_ID
         if (lane == 0) {
-            uint64_t *rec = a.timeline + (a.timeline_base + static_cast<int64_t>(blockIdx.x) * 4 + wave) * kTimelineWords;
+            uint64_t *rec =
+                a.timeline + (a.timeline_base + static_cast<int64_t>(blockIdx.x) * kTileWaves + wave) * kTimelineWords;
             const uint64_t kind = MODE == kFwd ? 0 : MODE == kNarrow ? 1 : 2;
             rec[0] = hw | (static_cast<uint64_t>(xcc & 0xff) << 32) | (kind << 40) | (static_cast<uint64_t>(wave) << 48);
             rec[1] = tl_start;
@@ -410,21 +406,21 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 
     if constexpr (MODE == kBwdProbs) {
 #pragma unroll
-        for (int tn = 0; tn < 4; ++tn) {
+        for (int tn = 0; tn < 2; ++tn) {
             probs_column(a, [&](int tm) -> const f32x16 & { return acc[tm][tn]; }, v0, vt, rt, wm,
-                         wn * 128 + tn * 32 + l32, h2);
+                         wn * 64 + tn * 32 + l32, h2);
             __builtin_amdgcn_sched_barrier(0);
         }
         return;
     }
     if constexpr (MODE == kLogits) {
         // acc[tm][tn][i]: vocab v0 + wm*32*TM + tm*32 + 8*(i/4) + 4*h2 + i%4,
-        // row r0 + wn*128 + tn*32 + l32: 4 consecutive entries per store
+        // row r0 + wn*64 + tn*32 + l32: 4 consecutive entries per store
         const int64_t vbase = v0 + wm * 32 * TM;
         const int vlim = vbase + 32 * TM <= a.V ? 32 * TM : static_cast<int>(a.V - vbase) - 4 * h2;
 #pragma unroll
-        for (int tn = 0; tn < 4; ++tn) {
-            const int row = wn * 128 + tn * 32 + l32;
+        for (int tn = 0; tn < 2; ++tn) {
+            const int row = wn * 64 + tn * 32 + l32;
             const int64_t rr = r0 + row;
             const bool live = rr < a.R;
             const float it = live ? a.inv_t_rows[rr] : 0.f;
@@ -451,8 +447,10 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();
-        const int64_t rr = r0 + tid;
-        if (rr < a.R) a.pm[vt * a.R + rr] = fmaxf(red[0][tid][0], red[1][tid][0]);
+        if (tid < kRowTile) {
+            const int64_t rr = r0 + tid;
+            if (rr < a.R) a.pm[vt * a.R + rr] = fmaxf(red[0][tid][0], red[1][tid][0]);
+        }
         return;
     }
 
@@ -462,12 +460,12 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 #pragma unroll
         for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
-            for (int tn = 0; tn < 4; ++tn)
+            for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const f32x4 v = {acc[tm][tn][4 * q], acc[tm][tn][4 * q + 1], acc[tm][tn][4 * q + 2],
                                      acc[tm][tn][4 * q + 3]};
-                    *reinterpret_cast<f32x4 *>(a.part + part_elem(blockIdx.x, wave, tm, tn, q, lane)) = v;
+                    *reinterpret_cast<f32x4 *>(a.part + part_elem(blockIdx.x, wm, wn * 2 + tn, tm, q, lane)) = v;
                 }
         if constexpr (TL) tl_record();
         return;
@@ -477,9 +475,9 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
 }
 
 // Sum, in part order, of the hidden-dimension parts of tail tile j (its
-// logical tile a.tile_base + j) that lane `lane` of tile-kernel wave `wave`
-// held in accumulators (0..3, tn).
-__device__ __forceinline__ void sum_parts(const LogprobArgs &a, int64_t j, int wave, int tn, int lane, f32x16 (&z)[4]) {
+// logical tile a.tile_base + j): what lane `lane` held in the accumulators
+// (tm = 0..3) of vocab half wm and 32-row block rb.
+__device__ __forceinline__ void sum_parts(const LogprobArgs &a, int64_t j, int wm, int rb, int lane, f32x16 (&z)[4]) {
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm) z[tm] = f32x16{};
     for (int sp = 0; sp < a.splits; ++sp) {
@@ -488,7 +486,7 @@ __device__ __forceinline__ void sum_parts(const LogprobArgs &a, int64_t j, int w
         for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                v[tm][q] = *reinterpret_cast<const f32x4 *>(a.part + part_elem(j * a.splits + sp, wave, tm, tn, q, lane));
+                v[tm][q] = *reinterpret_cast<const f32x4 *>(a.part + part_elem(j * a.splits + sp, wm, rb, tm, q, lane));
 #pragma unroll
         for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
@@ -499,9 +497,9 @@ __device__ __forceinline__ void sum_parts(const LogprobArgs &a, int64_t j, int w
 }
 
 // The reduce kernels of a hidden-split tail: one workgroup of 2 waves per
-// (tail tile, 32-row column tn of row half wn), 8 workgroups per tile, so the
-// parts are read by many CUs at once.  Wave wm holds what lane (h2, l32) of
-// tile-kernel wave (wm, wn) held for that column.
+// (tail tile, 32-row block rb), 8 workgroups per tile, so the parts are read
+// by many CUs at once.  Wave wm holds what lane (h2, l32) of the tile
+// kernel's wave of vocab half wm held for that block.
 //
 // Forward: the forward epilogue on the sums.
 __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a) {
@@ -509,14 +507,13 @@ __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a)
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t j = blockIdx.x >> 3;
-    const int wn = (blockIdx.x >> 2) & 1, tn = blockIdx.x & 3;
+    const int rb = blockIdx.x & 7;
     const int l32 = lane & 31, h2 = lane >> 5;
     int64_t vt, rt;
     tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
     f32x16 z[4];
-    sum_parts(a, j, wn * 2 + wm, tn, lane, z);
-    const int row = tn * 32 + l32;               // within the row half
-    const int64_t rr = rt * kRowTile + wn * 128 + row;
+    sum_parts(a, j, wm, rb, lane, z);
+    const int64_t rr = rt * kRowTile + rb * 32 + l32;
     float mx, sum;
     row_partial<4>(a, [&](int tm) -> const f32x16 & { return z[tm]; }, rr, vt * kVocabTile + wm * 128, h2, mx, sum);
     if (h2 == 0) {
@@ -525,7 +522,7 @@ __global__ __launch_bounds__(128) void logprob_tail_reduce_kernel(LogprobArgs a)
     }
     __syncthreads();
     if (tid < 32) {
-        const int64_t r = rt * kRowTile + wn * 128 + tn * 32 + tid;
+        const int64_t r = rt * kRowTile + rb * 32 + tid;
         if (r < a.R) write_partial(a, vt, r, red[0][tid][0], red[0][tid][1], red[1][tid][0], red[1][tid][1]);
     }
 }
@@ -535,14 +532,13 @@ __global__ __launch_bounds__(128) void logprob_probs_tail_reduce_kernel(LogprobA
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t j = blockIdx.x >> 3;
-    const int wn = (blockIdx.x >> 2) & 1, tn = blockIdx.x & 3;
+    const int rb = blockIdx.x & 7;
     const int l32 = lane & 31, h2 = lane >> 5;
     int64_t vt, rt;
     tile_of_logical(a.tile_base + j, a.n_vocab_tiles, a.n_row_tiles, &vt, &rt);
     f32x16 z[4];
-    sum_parts(a, j, wn * 2 + wm, tn, lane, z);
-    probs_column(a, [&](int tm) -> const f32x16 & { return z[tm]; }, vt * kVocabTile, vt, rt, wm,
-                 wn * 128 + tn * 32 + l32, h2);
+    sum_parts(a, j, wm, rb, lane, z);
+    probs_column(a, [&](int tm) -> const f32x16 & { return z[tm]; }, vt * kVocabTile, vt, rt, wm, rb * 32 + l32, h2);
 }
 
 // Online log-sum-exp merge of (max, sum) partials, both in log2 units.
@@ -653,7 +649,7 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream, bool timelin
         static_assert(kNarrowWidth == 64 * 3, "narrow tile width");
         const uint32_t blocks = static_cast<uint32_t>(a.narrow_tiles * a.n_row_tiles);
         LogprobArgs n = a;
-        n.timeline_base = a.dp_tiles * 4;
+        n.timeline_base = a.dp_tiles * kTileWaves;
         if (timeline)
             hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3, true>), dim3(blocks), dim3(kTileThreads), 0, stream,
                                n);
@@ -667,7 +663,7 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream, bool timelin
         LogprobArgs t = a;
         t.tile_base = a.dp_tiles;
         t.tile_count = a.tail_tiles;
-        t.timeline_base = (a.dp_tiles + a.narrow_tiles * a.n_row_tiles) * 4;
+        t.timeline_base = (a.dp_tiles + a.narrow_tiles * a.n_row_tiles) * kTileWaves;
         const uint32_t parts = static_cast<uint32_t>(a.tail_tiles * a.splits);
         if (tile_weight_stages(a.n_row_tiles) == 3) {
             if (timeline)

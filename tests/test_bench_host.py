@@ -100,8 +100,10 @@ def test_source_hash_covers_included_headers():
     assert "decode_attn.hip" in bench._local_sources("decode_attn.hip")
 
 
-def test_timeline_markdown_on_synthetic_records():
-    # 8 XCDs x 32 CUs, two rounds of whole tiles, then 100 tail parts
+@pytest.mark.parametrize("waves", [4, 8])
+def test_timeline_markdown_on_synthetic_records(waves):
+    # 8 XCDs x 32 CUs, two rounds of whole tiles, then 100 tail parts; the
+    # waves per workgroup come from the records' wave field
     cus = [(x, se, sh, c) for x in range(8) for se in range(4) for sh in range(2) for c in range(4)]
     recs, b = [], 0
 
@@ -111,17 +113,17 @@ def test_timeline_markdown_on_synthetic_records():
     for rnd in range(2):
         for (x, se, sh, c) in cus:
             st = rnd * 16000 + b % 7
-            for w in range(4):
+            for w in range(waves):
                 recs.append([word0(x, se, sh, c, w, 0), st, st + 300, st + 15500, st + 15800, 62500, 2000000,
                              b | (80 << 32) | (10 << 48)])
             b += 1
     for i, (x, se, sh, c) in enumerate(cus[:100]):
         st = 32000
-        for w in range(4):
+        for w in range(waves):
             recs.append([word0(x, se, sh, c, w, 2), st, st + 300, st + 4000, st + 4100, 10000, 740000,
                          i | (20 << 32) | (2 << 48)])
     md = bench.timeline_markdown(np.array(recs, dtype=np.int64), True, 2 * 151936 * 5120, "synthetic")
-    assert "bit-identical" in md
+    assert "bit-identical" in md and f"its {waves} waves" in md
     # first table: workgroups, stages, tile duration 158 us, loop 152 us, 1900 ns per stage,
     # wait share 0.25, 2e6 cycles over 152 us = 13.158 GHz
     whole = [l for l in md.splitlines() if l.startswith("| whole tiles | 512")][0].split("|")

@@ -216,12 +216,12 @@ def test_timeline_same_outputs_and_complete_records(R, H, V):
     kind, wave, blk = (r[:, 0] >> 40) & 0xFF, (r[:, 0] >> 48) & 0xFF, r[:, 7] & 0xFFFFFFFF
     xcc = (r[:, 0] >> 32) & 0xFF
     assert set(kind.tolist()) <= {0, 1, 2} and (xcc < 8).all()
-    # record 4 b + w of each launch is workgroup b, wave w
+    # record 8 b + w of each launch is workgroup b, wave w (8 waves per tile workgroup)
     for k in set(kind.tolist()):
         m = kind == k
         n = int(m.sum())
-        assert n % 4 == 0
-        assert (blk[m] == np.arange(n) // 4).all() and (wave[m] == np.arange(n) % 4).all()
+        assert n % 8 == 0
+        assert (blk[m] == np.arange(n) // 8).all() and (wave[m] == np.arange(n) % 8).all()
     st, l0, l1, en = (r[:, i] for i in range(1, 5))
     assert (st > 0).all() and (st <= l0).all() and (l0 <= l1).all() and (l1 <= en).all()
     assert (r[:, 5] <= r[:, 6]).all() and (r[:, 6] > 0).all()     # stage-end waits within the loop's cycles
