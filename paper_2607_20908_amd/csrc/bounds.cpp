@@ -384,11 +384,12 @@ void replay_bwd_gemm(Replay &rp, const LogprobBwdArgs &a, int probs_r, int w_r, 
         }
         const int clast = bwd_clast(H, h0);
         const std::vector<int> as = stage_slots(rp, nks, nks + 1), bs = stage_slots(rp, nks, nks - 1 + WS);
-        for (int wave = 0; wave < 4; ++wave)
+        constexpr int BLK = 32 / kBwdGemmWaves;   // 1 KB blocks per wave per operand per stage
+        for (int wave = 0; wave < kBwdGemmWaves; ++wave)
             for (int lane = 0; lane < 64; ++lane) {
                 ln.thread = wave * 64 + lane;
-                for (int j = 0; j < 8; ++j) {
-                    const int blk = wave * 8 + j;
+                for (int j = 0; j < BLK; ++j) {
+                    const int blk = wave * BLK + j;
                     for (int slot : as)
                         ln.check(probs_r,
                                  Replay::addr(a.probs) + bwd_a_base(rt, a.n_vsteps, ks0, slot, nks, blk) * 2 +
@@ -411,13 +412,13 @@ void replay_bwd_gemm(Replay &rp, const LogprobBwdArgs &a, int probs_r, int w_r, 
         const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;
         const uint64_t out = Replay::addr(a.dpart) + bwd_out_base(split, rows_pad, rt, H, h0) * 4;
         const int64_t rlim = a.rows - static_cast<int64_t>(rt) * 256;
-        for (int wave = 0; wave < 4; ++wave) {
-            const int wm = wave & 1, wn = wave >> 1;
+        for (int wave = 0; wave < kBwdGemmWaves; ++wave) {
+            const int wm = wave & 1, wn = wave >> 1;   // row half, hidden quarter
             for (int lane = 0; lane < 64; ++lane) {
                 ln.thread = wave * 64 + lane;
                 const int l32 = lane & 31, h2 = lane >> 5;
-                for (int tn = 0; tn < 4; ++tn) {
-                    const int h = wn * 128 + tn * 32 + l32;
+                for (int tn = 0; tn < 2; ++tn) {
+                    const int h = wn * 64 + tn * 32 + l32;
                     if (h0 + h >= H) continue;
                     for (int tm = 0; tm < 4; ++tm)
                         for (int i = 0; i < 16; ++i) {

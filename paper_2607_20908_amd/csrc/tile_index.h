@@ -213,6 +213,9 @@ inline int64_t bwd_gemm_blocks(const LogprobBwdArgs &a) {
     return static_cast<int64_t>(a.n_row_tiles) * a.n_h_tiles * a.splits;
 }
 constexpr int kBwdFinishThreads = 256;
+// Wave64s per backward GEMM workgroup: wave w owns tile rows 128 (w & 1) ..
+// +127 and hidden entries 64 (w >> 1) .. +63 of its 256 x 256 output tile.
+constexpr int kBwdGemmWaves = 8;
 inline int64_t bwd_finish_blocks(const LogprobBwdArgs &a) {
     return (a.rows * (a.H / 4) + kBwdFinishThreads - 1) / kBwdFinishThreads;
 }

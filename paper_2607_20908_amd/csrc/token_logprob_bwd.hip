@@ -25,10 +25,11 @@
 namespace rlk {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;                   // finish kernel
 constexpr int kTileElems = 256 * 64;            // one stage of one operand, bf16 elements
-constexpr int kBlocksPerWave = kTileElems / 512 / 4;
-static_assert(kBlocksPerWave == 8, "staging layout");
+constexpr int kGemmThreads = 64 * kBwdGemmWaves;   // 8 waves, two per SIMD
+constexpr int kBlocksPerWave = kTileElems / 512 / kBwdGemmWaves;   // 1 KB blocks per wave per operand per stage
+static_assert(kBlocksPerWave == 4, "staging layout");
 
 // gfx950 transposing LDS read: in each group of 16 lanes, lane s supplies the
 // address of 4 consecutive bf16; seen as a 4 x 16 block whose row k holds the
@@ -40,16 +41,18 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const uint16_t *p) {
     return __builtin_bit_cast(bf16x4, v);
 }
 
-// S[rows, h] over one vocabulary range; one workgroup per 256 x 256 output
-// tile, each wave 128 rows x 128 hidden entries as 4 x 4 MFMA 32x32x16 tiles.
+// S[rows, h] over one vocabulary range; one workgroup of 8 waves (two per
+// SIMD) per 256 x 256 output tile, each wave 128 rows x 64 hidden entries as
+// 4 x 2 MFMA 32x32x16 tiles, so one wave of a SIMD issues its loads and LDS
+// reads while the other runs MFMAs.
 template <int WS>
-__global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBwdArgs a) {
+__global__ __launch_bounds__(kGemmThreads, 1) void logprob_bwd_gemm_kernel(LogprobBwdArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t bring[WS * kTileElems];   // W bands [64 v][256 h]
     __shared__ __attribute__((aligned(16))) uint16_t aring[2 * kTileElems];    // probabilities [256 rows][64 v]
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;     // row half, hidden half
+    const int wm = wave & 1, wn = wave >> 1;     // row half, hidden quarter
     const int l32 = lane & 31, h2 = lane >> 5;
     int split, ht, rt;
     gemm_tile_of(blockIdx.x, a.n_h_tiles, a.n_row_tiles, a.splits, &split, &ht, &rt);
@@ -92,24 +95,24 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
                      bring_l + ((slot % WS) * kTileElems + blk * 512) * 2);
     };
 
-    f32x16 acc[4][4];
+    f32x16 acc[4][2];
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < 4; ++tn) acc[tm][tn] = f32x16{};
+        for (int tn = 0; tn < 2; ++tn) acc[tm][tn] = f32x16{};
 
     // transposing-read address of this lane, relative to a band and k-step:
     // lanes 16q..16q+15 read rows 8 (q/2) + 4 e + s/4 at hidden entries
     // 16 (q%2) + 4 (s%4) of the 32-wide block j
     const int q = lane >> 4, s = lane & 15;
     const int brow = 8 * (q >> 1) + (s >> 2);
-    int boff[4];
+    int boff[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int hl = wn * 128 + j * 32 + 16 * (q & 1) + 4 * (s & 3);
+    for (int j = 0; j < 2; ++j) {
+        const int hl = wn * 64 + j * 32 + 16 * (q & 1) + 4 * (s & 3);
         boff[j] = band_off(brow, hl >> 3) + (hl & 7);
     }
-    bf16x8 fa[2][4], fb[2][4];
+    bf16x8 fa[2][4], fb[2][2];
     auto read_frags = [&](int ks, int kq, int p) {
         const uint16_t *as = abuf(ks);
         const uint16_t *bs = bbuf(ks) + kq * 16 * 256;
@@ -117,17 +120,17 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
 #pragma unroll
         for (int i = 0; i < 4; ++i) fa[p][i] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + i * 32 + l32, c));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < 2; ++j) {
             const bf16x4 lo = lds_read_tr16(bs + boff[j]);
             const bf16x4 hi = lds_read_tr16(bs + boff[j] + 4 * 256);
             fb[p][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         }
     };
-    auto mfma16 = [&](int p) {
+    auto mfma_step = [&](int p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < 2; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
     };
 
@@ -153,32 +156,25 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
 #pragma unroll
         for (int kq = 0; kq < 3; ++kq) {
             read_frags(ks, kq + 1, (kq + 1) & 1);
-            mfma16(kq & 1);
+            mfma_step(kq & 1);
         }
         wait_vm<(WS == 3 ? 1 : 0) * kBlocksPerWave>();
         wait_lds();
         barrier();
-        // two loads, two MFMAs of this k-step's last quarter and one fragment
-        // read of stage ks + 1 per group
+        // one load, one MFMA of this k-step's last quarter and one fragment
+        // read of stage ks + 1 per group (the B fragments in groups 4 and 5)
         {
             const uint16_t *as = abuf(ks + 1);
             const uint16_t *bs = bbuf(ks + 1);
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
-                if (g < 4) {
-                    issue_a(ks + 2, 2 * g);
-                    issue_a(ks + 2, 2 * g + 1);
-                } else {
-                    issue_b(ks + WS, 2 * (g - 4));
-                    issue_b(ks + WS, 2 * (g - 4) + 1);
-                }
-#pragma unroll
-                for (int m = 2 * g; m < 2 * g + 2; ++m)
-                    acc[m >> 2][m & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][m >> 2], fb[1][m & 3],
-                                                                                 acc[m >> 2][m & 3], 0, 0, 0);
+                if (g < 4) issue_a(ks + 2, g);
+                else issue_b(ks + WS, g - 4);
+                acc[g >> 1][g & 1] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][g >> 1], fb[1][g & 1], acc[g >> 1][g & 1], 0, 0, 0);
                 if (g < 4) {
                     fa[0][g] = *reinterpret_cast<const bf16x8 *>(as + op_off(wm * 128 + g * 32 + l32, h2));
-                } else {
+                } else if (g < 6) {
                     const bf16x4 lo = lds_read_tr16(bs + boff[g - 4]);
                     const bf16x4 hi = lds_read_tr16(bs + boff[g - 4] + 4 * 256);
                     fb[0][g - 4] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -190,13 +186,13 @@ __global__ __launch_bounds__(kThreads, 1) void logprob_bwd_gemm_kernel(LogprobBw
     wait_vm<0>();
 
     // ---- epilogue: acc[tm][tn][i] is S at row wm*128 + tm*32 + 8*(i/4) +
-    // 4*h2 + i%4 of the tile, hidden entry wn*128 + tn*32 + l32.
+    // 4*h2 + i%4 of the tile, hidden entry wn*64 + tn*32 + l32.
     const int64_t rows_pad = static_cast<int64_t>(a.n_row_tiles) * 256;
     float *out = a.dpart + bwd_out_base(split, rows_pad, rt, H, h0);
     const int64_t rlim = a.rows - static_cast<int64_t>(rt) * 256;
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-        const int h = wn * 128 + tn * 32 + l32;
+    for (int tn = 0; tn < 2; ++tn) {
+        const int h = wn * 64 + tn * 32 + l32;
         if (h0 + h >= H) continue;
 #pragma unroll
         for (int tm = 0; tm < 4; ++tm)
@@ -246,11 +242,11 @@ __global__ __launch_bounds__(kThreads) void logprob_bwd_finish_kernel(LogprobBwd
 hipError_t launch_logprob_bwd_gemm(const LogprobBwdArgs &a, hipStream_t stream) {
     const int64_t blocks = bwd_gemm_blocks(a);
     if (tile_weight_stages(a.n_row_tiles) == 3)
-        hipLaunchKernelGGL(logprob_bwd_gemm_kernel<3>, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream,
-                           a);
+        hipLaunchKernelGGL(logprob_bwd_gemm_kernel<3>, dim3(static_cast<uint32_t>(blocks)), dim3(kGemmThreads), 0,
+                           stream, a);
     else
-        hipLaunchKernelGGL(logprob_bwd_gemm_kernel<2>, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream,
-                           a);
+        hipLaunchKernelGGL(logprob_bwd_gemm_kernel<2>, dim3(static_cast<uint32_t>(blocks)), dim3(kGemmThreads), 0,
+                           stream, a);
     return hipGetLastError();
 }
 
