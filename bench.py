@@ -594,6 +594,14 @@ def extra_ops(rk, W, args, x, y, lse2, ops, hip, sh, dev):
 TIMELINE_KINDS = {0: "whole tiles", 1: "narrow tiles", 2: "tail parts"}
 
 
+def provenance(op: str) -> str:
+    """The command line that wrote a summary (as run from the repository
+    root) and the sha256 of the kernel sources it measured."""
+    argv = " ".join(["python3", "bench.py"] + [a if a else "''" for a in sys.argv[1:]])
+    return (f"\nCommand (on the MI355X box, from the repository root): `{argv}`\n\n"
+            f"Kernel sources: {op} sha256 {source_sha256(op)}\n")
+
+
 def timeline_report(rk, y, evict, desc: str) -> str:
     """The tile launches of one lm-head call, one record per wave from
     rl_debug_logprob_timeline (after the same cache eviction as the timed
@@ -855,10 +863,12 @@ def main():
     if args.decode_timeline and x is not None:
         with open(args.decode_timeline, "w") as f:
             f.write(decode_timeline_report(rk, x, evict, args.kv_layout, head["workload"]))
+            f.write(provenance("decode"))
         log(f"bench: decode timeline written to {args.decode_timeline}")
     if args.timeline and y is not None:
         with open(args.timeline, "w") as f:
             f.write(timeline_report(rk, y, evict, head["workload"]))
+            f.write(provenance("lmhead"))
         log(f"bench: tile timeline written to {args.timeline}")
     update = extra_ops(rk, W, args, x, y, lse2, ops, hip, stream.cuda_stream, dev)
     del x, y, ops, lse2

@@ -157,3 +157,12 @@ def test_decode_timeline_markdown_on_synthetic_records():
     assert suf[5].strip() == "20.0/20.0/20.0"
     assert "over 256 CUs" in md and "at most 256 (1.00 per CU)" in md
     assert "The item that ends last: suffix" in md
+
+
+def test_provenance_names_command_and_sources(monkeypatch):
+    """Summaries that bench.py writes itself record the command line and the
+    sha256 of the kernel sources they measured."""
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", "32b", "--also", "", "--timeline", "t.md"])
+    p = bench.provenance("lmhead")
+    assert "`python3 bench.py --workload 32b --also '' --timeline t.md`" in p
+    assert bench.source_sha256("lmhead") in p
