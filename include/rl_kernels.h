@@ -299,8 +299,9 @@ rl_status rl_kv_append(const rl_decode_shape *shape, const rl_kv_append_lens *le
  * at least half of the 256 CUs idle, those tiles run as 2-4 parts of the
  * hidden dimension and the workspace also holds their fp32 accumulators
  * (256 KB per part).  When it is more than half full and there are at most 4
- * row tiles, the vocabulary past the full rounds runs as tiles 192 entries
- * wide instead (if they fit in one round), each with its own partial slot.
+ * row tiles, the vocabulary past the full rounds runs as one round of tiles
+ * 128 or 192 entries wide instead (the narrower that fits; none if neither
+ * does), each with its own partial slot.
  */
 rl_status rl_token_logprob_workspace_size(int64_t rows, int32_t hidden, int32_t vocab,
                                           size_t *bytes);

@@ -171,8 +171,9 @@ void replay_tile(Replay &rp, const char *name, int mode, int TM, int WS, const L
         }
         const uint64_t wg = Replay::addr(a.w) + static_cast<uint64_t>(tc.v0 * H) * 2;
         const uint64_t hg = Replay::addr(a.hidden) + static_cast<uint64_t>(r0 * H) * 2;
-        // the hidden rows of slots 0 .. nks + 1, the weights of 0 .. nks - 1 + WS
-        const std::vector<int> hs = stage_slots(rp, tc.nks, tc.nks + 1), ws = stage_slots(rp, tc.nks, tc.nks - 1 + WS);
+        // the hidden rows of slots 0 .. nks - 1 + HS, the weights of 0 .. nks - 1 + WS
+        const std::vector<int> hs = stage_slots(rp, tc.nks, tc.nks - 1 + tile_hidden_stages(TM)),
+                               ws = stage_slots(rp, tc.nks, tc.nks - 1 + WS);
         for (int wave = 0; wave < kTileWaves; ++wave)
             for (int lane = 0; lane < 64; ++lane) {
                 ln.thread = wave * 64 + lane;
@@ -489,7 +490,8 @@ extern "C" rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t h
         d.tile_count = a.dp_tiles;
         replay_tile(rp, "logprob_tile_kernel<kFwd>", kFwd, 4, tile_weight_stages(a.n_row_tiles), d, d.tile_count, rg);
         if (a.narrow_tiles > 0)
-            replay_tile(rp, "logprob_tile_kernel<kNarrow>", kNarrow, 3, 3, a, a.narrow_tiles * a.n_row_tiles, rg);
+            replay_tile(rp, "logprob_tile_kernel<kNarrow>", kNarrow, a.narrow_tm, 3, a, a.narrow_tiles * a.n_row_tiles,
+                        rg);
         if (a.tail_tiles > 0) {
             LogprobArgs t = a;
             t.tile_base = a.dp_tiles;
@@ -576,7 +578,8 @@ extern "C" rl_status rl_debug_logprob_bounds(int32_t op, int64_t rows, int32_t h
                 replay_tile(rp, "logprob_tile_kernel<kLogits>", kLogits, 4, tile_weight_stages(f.n_row_tiles), d,
                             d.tile_count, rg);
             if (f.narrow_tiles > 0)
-                replay_tile(rp, "logprob_tile_kernel<kLogits, 3>", kLogits, 3, 3, f, f.narrow_tiles * f.n_row_tiles, rg);
+                replay_tile(rp, "logprob_tile_kernel<kLogits, narrow>", kLogits, f.narrow_tm, 3, f,
+                            f.narrow_tiles * f.n_row_tiles, rg);
             replay_select(rp, s, rg.pm, rg.logits, u, tok, lp);
         }
     } else {

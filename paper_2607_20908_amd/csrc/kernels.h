@@ -103,10 +103,12 @@ struct LogprobArgs {
     int32_t splits;
     float *part;
     int64_t tile_base, tile_count;
-    // forward only: the last round as narrow tiles of 192 vocab entries,
-    // narrow tile j covering [narrow_v0 + 192 j, + 192) with its partials in
-    // slot narrow_slot0 + j; the combine merges n_partials slots per row
+    // forward and logits only: the last round as narrow tiles of w = 64
+    // narrow_tm vocab entries (narrow_tm 2 or 3), narrow tile j covering
+    // [narrow_v0 + w j, + w) with its partials in slot narrow_slot0 + j; the
+    // combine merges n_partials slots per row
     int64_t narrow_v0, narrow_tiles, narrow_slot0, n_partials;
+    int32_t narrow_tm;
     // backward only: the forward's lse per row (input) and the probabilities
     // p = exp(inv_T z - lse) as bf16 in the blocked layout of
     // LogprobBwdArgs::probs (output); pm, pl, zt, logprob are then unused

@@ -33,6 +33,7 @@ inline LogprobArgs logprob_args(const LogprobPlan &plan, const void *hidden_stat
     a.narrow_v0 = plan.narrow_v0;
     a.narrow_tiles = plan.narrow_tiles;
     a.narrow_slot0 = plan.narrow_slot0;
+    a.narrow_tm = plan.narrow_tm;
     a.n_partials = plan.n_partials;
     return a;
 }
@@ -109,6 +110,7 @@ inline void sample_chunk_args(const SamplePlan &plan, int64_t c0, const uint16_t
     f->narrow_v0 = tr.narrow_v0;
     f->narrow_tiles = tr.narrow_tiles;
     f->narrow_slot0 = tr.narrow_slot0;
+    f->narrow_tm = tr.narrow_tm;
     f->n_partials = tr.n_partials;
     *s = SampleArgs{};
     s->logits = logits;

@@ -519,9 +519,9 @@ TailSplit bwd_probs_tail(const LogprobBwdPlan &plan, int64_t n) {
 TileRounds plan_tile_rounds(int64_t rows, int32_t vocab) {
     // With at most 4 row tiles (the tiles of one vocab tile are neighbours in
     // launch order), the whole vocab tiles of the full rounds run as they are
-    // and the rest of the vocabulary runs as one round of tiles 192 entries
-    // wide, if they fit on the CUs (a round of them takes about 3/4 of a
-    // round of whole tiles).
+    // and the rest of the vocabulary runs as one round of tiles 128 or 192
+    // entries wide, the narrower that fits on the CUs (a tile of either takes
+    // less time than a whole one, and every tile of the round runs at once).
     TileRounds tr;
     const int64_t nvt = ceil_div(vocab, kVocabTile), nrt = ceil_div(rows, kRowTile);
     const int64_t tiles = nvt * nrt;
@@ -530,13 +530,16 @@ TileRounds plan_tile_rounds(int64_t rows, int32_t vocab) {
     tr.n_partials = nvt;
     if (dp > 0 && tail > 0 && nrt <= kNarrowMaxRowTiles) {
         const int64_t vt0 = dp / nrt;
-        const int64_t n = ceil_div(vocab - vt0 * kVocabTile, kNarrowWidth);
-        if (n * nrt <= kNumCUs) {
+        for (int tm = kNarrowMinTM; tm <= kNarrowMaxTM; ++tm) {
+            const int64_t n = ceil_div(vocab - vt0 * kVocabTile, 64 * tm);
+            if (n * nrt > kNumCUs) continue;
             tr.dp_tiles = vt0 * nrt;
             tr.narrow_v0 = vt0 * kVocabTile;
             tr.narrow_tiles = n;
             tr.narrow_slot0 = vt0;
+            tr.narrow_tm = tm;
             tr.n_partials = vt0 + n;
+            break;
         }
     }
     return tr;
@@ -573,6 +576,7 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
         pl.narrow_v0 = tr.narrow_v0;
         pl.narrow_tiles = tr.narrow_tiles;
         pl.narrow_slot0 = tr.narrow_slot0;
+        pl.narrow_tm = tr.narrow_tm;
         pl.n_partials = tr.n_partials;
     }
     size_t off = 0;
@@ -644,7 +648,7 @@ rl_status plan_sample(int64_t rows, int32_t hidden, int32_t vocab, SamplePlan *p
     pl.V = vocab;
     pl.n_vocab_tiles = ceil_div(vocab, kVocabTile);
     // one tile of padding past the vocab tiles: a narrow last round's tiles
-    // (192 wide from a whole tile's edge) end at most 191 entries past V
+    // (128 or 192 wide from a whole tile's edge) end at most 191 entries past V
     pl.ld = (pl.n_vocab_tiles + 1) * kVocabTile;
     if (rows == 0) return RL_OK;
     pl.chunk_rows = std::min<int64_t>(rows, kSampleChunkRows);
@@ -653,7 +657,7 @@ rl_status plan_sample(int64_t rows, int32_t hidden, int32_t vocab, SamplePlan *p
     pl.off_logits = off;
     off = align_up(off + static_cast<size_t>(rows_pad) * pl.ld * 4, 256);
     // row-maximum slots: the whole tiles' and, per chunk, those of its narrow
-    // last round (at most 4/3 as many tiles cover the rest of the vocabulary)
+    // last round (at most twice as many tiles cover the rest of the vocabulary)
     pl.pm_slots = std::max(pl.n_vocab_tiles, plan_tile_rounds(pl.chunk_rows, vocab).n_partials);
     if (rows % pl.chunk_rows)
         pl.pm_slots = std::max(pl.pm_slots, plan_tile_rounds(rows % pl.chunk_rows, vocab).n_partials);

@@ -120,10 +120,11 @@ TailSplit plan_tail_split(int64_t tiles, int64_t nks);
 // The tile kernels address a weight or hidden row of a tile as a 32-bit byte
 // offset from the tile's first row (255 rows of 2 * hidden bytes).
 constexpr int64_t kMaxHidden = 1 << 22;
-// Narrow last-round tiles are this many vocab entries wide; they need every
-// row tile of a vocab tile next to each other in launch order, which holds
-// for at most kNarrowMaxRowTiles row tiles.
-constexpr int64_t kNarrowWidth = 192;
+// Narrow last-round tiles are 64 narrow_tm vocab entries wide, narrow_tm 2
+// or 3 (the narrower that fits one round); they need every row tile of a
+// vocab tile next to each other in launch order, which holds for at most
+// kNarrowMaxRowTiles row tiles.
+constexpr int kNarrowMinTM = 2, kNarrowMaxTM = 3;
 constexpr int64_t kNarrowMaxRowTiles = 4;
 
 struct LogprobPlan {
@@ -136,9 +137,10 @@ struct LogprobPlan {
     int64_t n_dp_tiles = 0, n_tail_tiles = 0;
     int32_t tail_splits = 1;
     // or: a last round more than half full runs as narrow_tiles tiles of
-    // kNarrowWidth vocab entries over [narrow_v0, V) (per row tile), their
+    // 64 narrow_tm vocab entries over [narrow_v0, V) (per row tile), their
     // partials in slots narrow_slot0.. after the whole tiles' slots
     int64_t narrow_v0 = 0, narrow_tiles = 0, narrow_slot0 = 0;
+    int32_t narrow_tm = 0;
     int64_t n_partials = 0;          // (max, sum) partial slots per row
     size_t off_m = 0, off_l = 0, off_zt = 0, off_part = 0, total_bytes = 0;
 };
@@ -148,12 +150,14 @@ rl_status plan_logprob(int64_t rows, int32_t hidden, int32_t vocab, LogprobPlan 
 
 // The tiles of one lm-head pass over `rows` rows: logical tiles [0,
 // dp_tiles) whole, then (when narrow_tiles > 0) the vocabulary from
-// narrow_v0 on as one round of kNarrowWidth-wide tiles per row tile, with
-// partial slots narrow_slot0.. ; n_partials slots per row in all.  Narrow
-// tiles are taken when the tiles leave a partial last round, there are at
-// most kNarrowMaxRowTiles row tiles and the narrow tiles fit in one round.
+// narrow_v0 on as one round of tiles 64 narrow_tm entries wide per row tile,
+// with partial slots narrow_slot0.. ; n_partials slots per row in all.
+// Narrow tiles are taken when the tiles leave a partial last round, there
+// are at most kNarrowMaxRowTiles row tiles and the narrow tiles fit in one
+// round; of the widths that fit, the narrowest (the most CUs busy).
 struct TileRounds {
     int64_t dp_tiles = 0, narrow_v0 = 0, narrow_tiles = 0, narrow_slot0 = 0, n_partials = 0;
+    int32_t narrow_tm = 0;
 };
 TileRounds plan_tile_rounds(int64_t rows, int32_t vocab);
 

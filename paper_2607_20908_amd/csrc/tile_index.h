@@ -95,8 +95,8 @@ struct TileCoord {
     int kb, nks;       // hidden steps [kb, kb + nks)
 };
 
-// TM: 32-entry vocab blocks per wave (4: 256 x 256 tiles; 3: the 192-wide
-// narrow tiles).  Narrow tile j covers vocab [narrow_v0 + j 64 TM, + 64 TM)
+// TM: 32-entry vocab blocks per wave (4: 256 x 256 tiles; 2, 3: the 128-
+// and 192-wide narrow tiles).  Narrow tile j covers vocab [narrow_v0 + j 64 TM, + 64 TM)
 // for row tile rt; the row tiles of one j are neighbours in launch order.
 // Part s of tail tile j covers hidden steps [s n / S, (s + 1) n / S).
 RLK_HD TileCoord tile_coord(int mode, int tm, int64_t b, const LogprobArgs &a) {
@@ -209,6 +209,11 @@ RLK_HD int64_t bwd_part_elem(int sp, int64_t rows_pad, int64_t r, int64_t H, int
 // to arrive (the whole 160 KB of LDS); with many row tiles two stages measure
 // better.
 inline int tile_weight_stages(int64_t n_row_tiles) { return n_row_tiles <= 8 ? 3 : 2; }
+// Hidden-row stages of the tile kernel with TM 32-entry vocab blocks per
+// wave: 2, or 3 for the 128-wide narrow tiles, whose short stages would not
+// cover the hidden rows' latency with one stage to arrive (and whose LDS has
+// room: 3 x 16 KB of weights + 3 x 32 KB of hidden rows).
+constexpr int tile_hidden_stages(int tm) { return tm == 2 ? 3 : 2; }
 inline int64_t bwd_gemm_blocks(const LogprobBwdArgs &a) {
     return static_cast<int64_t>(a.n_row_tiles) * a.n_h_tiles * a.splits;
 }

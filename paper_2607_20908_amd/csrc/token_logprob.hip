@@ -18,8 +18,9 @@
 // shuffle), picks out the target's logit when the target falls in the tile,
 // and writes one (max, sum) partial per (vocab tile, row).
 // A last round of tiles runs either as hidden-dimension parts summed by a
-// reduce kernel (at most half the CUs busy) or as tiles 192 vocab entries
-// wide (more than half busy, at most 4 row tiles), each with a partial slot
+// reduce kernel (at most half the CUs busy) or as tiles 128 or 192 vocab
+// entries wide (at most 4 row tiles; more than half busy in the forward, any
+// partial round for the sampling head's logits), each with a partial slot
 // of its own.
 // Combine kernel: per row, merge the partials of all slots into the
 // log-sum-exp and subtract it from the target logit.
@@ -33,7 +34,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kK = kHiddenStep;                 // 64 hidden entries per LDS stage
 constexpr int kTileElems = kVocabTile * kK;     // bf16 elements per operand per stage
-constexpr int kHStages = 2;                     // hidden ring: 2 stages
 static_assert(kVocabTile == kRowTile, "square tiles assumed below");
 constexpr int kTileThreads = 64 * kTileWaves;  // 8 waves
 constexpr int kBlocksPerWave = kTileElems / 512 / kTileWaves;   // 1 KB hidden load blocks per wave per stage
@@ -219,8 +219,8 @@ __device__ __forceinline__ void fwd_epilogue(const LogprobArgs &a, const f32x16 
 }
 
 // TM: 32-entry vocab blocks per wave; a tile spans 64 TM vocab entries (4:
-// the 256 x 256 tiles; 3: the narrow tiles of a last round, for the forward
-// (kNarrow) and the sampling head's logits (kLogits)).
+// the 256 x 256 tiles; 2, 3: the narrow tiles of a last round, for the
+// forward (kNarrow) and the sampling head's logits (kLogits)).
 // TL: debug build with a timeline record per wave (forward modes only): wall
 // clock at the start, at the loop's start and end and after the epilogue,
 // s_memtime cycles of the loop, and the cycles of the stage-end wait in one
@@ -237,10 +237,12 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     constexpr int WELEMS = VW * kK;              // bf16 elements of one weight stage
     constexpr int WBLK = VW / 64;                // 1 KB weight blocks per wave per stage (= TM)
     constexpr int HBLK = kBlocksPerWave;         // 1 KB hidden blocks per wave per stage
-    // WS weight stages + 2 x 32 KB hidden stages; the epilogue's reduction
+    constexpr int HS = tile_hidden_stages(TM);   // hidden-row stages
+    static_assert(HS == 2 || WS == 3, "a third hidden stage goes with the 3-stage weight ring");
+    // WS weight stages + HS x 32 KB hidden stages; the epilogue's reduction
     // area reuses the weight ring once the loop is done
     __shared__ __attribute__((aligned(16))) uint16_t wring[WS * WELEMS];
-    __shared__ __attribute__((aligned(16))) uint16_t hring[kHStages * kTileElems];
+    __shared__ __attribute__((aligned(16))) uint16_t hring[HS * kTileElems];
     float (*red)[kRowTile][2] = reinterpret_cast<float (*)[kRowTile][2]>(wring);   // [vocab half][row][m, l]
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -265,7 +267,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
     // Block j of stage `slot`'s buffer gets the data of stage min(slot, nks-1):
     // past the last stage the loads refill a buffer nobody reads any more.
     auto wbuf = [&](int ks) { return wring + (ks % WS) * WELEMS; };
-    auto hbuf = [&](int ks) { return hring + (ks & 1) * kTileElems; };
+    auto hbuf = [&](int ks) { return hring + (ks % HS) * kTileElems; };
     const uint32_t wring_l = lds_addr(wring), hring_l = lds_addr(hring);
     auto issue_block = [&](const uint16_t *g, int last, uint32_t st, int slot, int blk) {
         const int row = stage_row(blk, lane);
@@ -274,7 +276,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
         load_lds16_s(g + stage_k0(kb, slot, nks), stage_voff(row, last, H, stage_chunk(row, lane)), st + blk * 1024);
     };
     auto wbuf_l = [&](int ks) { return wring_l + (ks % WS) * (WELEMS * 2); };
-    auto hbuf_l = [&](int ks) { return hring_l + (ks & 1) * (kTileElems * 2); };
+    auto hbuf_l = [&](int ks) { return hring_l + (ks % HS) * (kTileElems * 2); };
     auto issue_w = [&](int slot) {
         const uint32_t st = wbuf_l(slot);
 #pragma unroll
@@ -310,20 +312,22 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
     };
 
-    // Stage ks lives in weight buffer ks % WS and hidden buffer ks % 2.  At
+    // Stage ks lives in weight buffer ks % WS and hidden buffer ks % HS.  At
     // the end of stage ks (once every wave is done reading it) the hidden rows
-    // of stage ks+2 and then the weights of stage ks+WS are issued, so the
-    // weights have WS-1 stages to arrive; the one wait per stage leaves only
-    // the newest weight stage in flight (WS = 3) or nothing (WS = 2).  Loads past the last stage
-    // refill a buffer nobody reads any more (so the loop body has no branch);
-    // the final wait makes sure none of them is still writing LDS when the
+    // of stage ks+HS and then the weights of stage ks+WS are issued, so they
+    // have HS-1 and WS-1 stages to arrive; the one wait per stage leaves only
+    // the newest stage in flight: the weights (HS = 2, WS = 3), both operands
+    // (HS = WS = 3) or nothing (WS = 2).  Loads past the last stage refill a
+    // buffer nobody reads any more (so the loop body has no branch); the
+    // final wait makes sure none of them is still writing LDS when the
     // epilogue starts.
     issue_h(0);
     issue_w(0);
     issue_h(1);
     issue_w(1);
+    if (HS == 3) issue_h(2);
     if (WS == 3) issue_w(2);
-    wait_vm<HBLK + (WS == 3 ? 2 : 1) * WBLK>();   // stage 0 has landed
+    wait_vm<(HS - 1) * HBLK + (WS - 1) * WBLK>();   // stage 0 has landed
     barrier();
     if constexpr (TL) {
         tl_loop0 = __builtin_amdgcn_s_memrealtime();
@@ -340,14 +344,14 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM - (TM + 2), 0);
+            if constexpr (TM > 2) __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM - (TM + 2), 0);
         }
-        // last k-step: stage ks+1 has landed (only the weights of stage ks+2
-        // may still be in flight) and every wave is done reading stage ks
+        // last k-step: stage ks+1 has landed (only stage ks+2's loads may
+        // still be in flight) and every wave is done reading stage ks
         [[maybe_unused]] uint64_t tl_w0 = 0;
         if constexpr (TL)
             if ((ks & 7) == 3) tl_w0 = __builtin_amdgcn_s_memtime();
-        wait_vm<(WS == 3 ? 1 : 0) * WBLK>();
+        wait_vm<(HS - 2) * HBLK + (WS - 2) * WBLK>();
         wait_lds();
         barrier();
         if constexpr (TL)
@@ -355,7 +359,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
                 tl_wait += __builtin_amdgcn_s_memtime() - tl_w0;
                 ++tl_samples;
             }
-        // eight groups of: one global->LDS load (hidden rows of stage ks+2
+        // eight groups of: one global->LDS load (hidden rows of stage ks+HS
         // in groups 0-3, weights of stage ks+WS in groups 4-7), one MFMA of
         // this k-step, one fragment read of stage ks+1 (kept in this order:
         // the loads are opaque to the scheduler)
@@ -364,7 +368,7 @@ __global__ __launch_bounds__(kTileThreads, 1) void logprob_tile_kernel(LogprobAr
             const uint16_t *bs = hbuf(ks + 1);
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
-                if (g < HBLK) issue_block(hg, hlast, hbuf_l(ks + 2), ks + 2, wave * HBLK + g);
+                if (g < HBLK) issue_block(hg, hlast, hbuf_l(ks + HS), ks + HS, wave * HBLK + g);
                 else if (g - HBLK < WBLK) issue_block(wg, wlast, wbuf_l(ks + WS), ks + WS, wave * WBLK + (g - HBLK));
                 if (g < 2 * TM)
                     acc[g >> 1][g & 1] =
@@ -643,18 +647,28 @@ hipError_t launch_logprob(const LogprobArgs &a, hipStream_t stream, bool timelin
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.narrow_tiles > 0) {
-        // the last round as narrow tiles, 192 vocab entries wide (the plan
-        // allows them only for at most 4 row tiles, so the 3-stage weight
-        // ring applies)
-        static_assert(kNarrowWidth == 64 * 3, "narrow tile width");
+        // the last round as narrow tiles, 128 or 192 vocab entries wide (the
+        // plan allows them only for at most 4 row tiles, so the 3-stage
+        // weight ring applies)
+        static_assert(kNarrowMinTM == 2 && kNarrowMaxTM == 3, "narrow tile widths");
         const uint32_t blocks = static_cast<uint32_t>(a.narrow_tiles * a.n_row_tiles);
         LogprobArgs n = a;
         n.timeline_base = a.dp_tiles * kTileWaves;
-        if (timeline)
-            hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3, true>), dim3(blocks), dim3(kTileThreads), 0, stream,
-                               n);
-        else
-            hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, n);
+        if (a.narrow_tm == 2) {
+            if (timeline)
+                hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 2, true>), dim3(blocks), dim3(kTileThreads), 0,
+                                   stream, n);
+            else
+                hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 2>), dim3(blocks), dim3(kTileThreads), 0, stream,
+                                   n);
+        } else {
+            if (timeline)
+                hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3, true>), dim3(blocks), dim3(kTileThreads), 0,
+                                   stream, n);
+            else
+                hipLaunchKernelGGL((logprob_tile_kernel<3, kNarrow, 3>), dim3(blocks), dim3(kTileThreads), 0, stream,
+                                   n);
+        }
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -747,9 +761,12 @@ hipError_t launch_logits(const LogprobArgs &a, hipStream_t stream) {
         if (e != hipSuccess) return e;
     }
     if (a.narrow_tiles > 0) {
-        static_assert(kNarrowWidth == 64 * 3, "narrow tile width");
+        static_assert(kNarrowMinTM == 2 && kNarrowMaxTM == 3, "narrow tile widths");
         const uint32_t blocks = static_cast<uint32_t>(a.narrow_tiles * a.n_row_tiles);
-        hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, a);
+        if (a.narrow_tm == 2)
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits, 2>), dim3(blocks), dim3(kTileThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL((logprob_tile_kernel<3, kLogits, 3>), dim3(blocks), dim3(kTileThreads), 0, stream, a);
     }
     return hipGetLastError();
 }

@@ -212,18 +212,23 @@ def tail_part_bytes(R, H, V, cus=256, max_splits=4):
     return tail * s * 256 * 256 * 4
 
 
-def narrow_tiles(R, H, V, cus=256, width=192):
+def narrow_tiles(R, H, V, cus=256, split=True):
     """(whole vocab tiles before the narrow region, narrow tiles per row
-    tile) when a last round of 256 x 256 tiles more than half full runs as
-    192-wide tiles (at most 4 row tiles, one round of them), else None."""
+    tile) when a partial last round of 256 x 256 tiles runs as one round of
+    128-wide tiles, or else 192-wide ones (at most 4 row tiles, the narrower
+    that fits), else None.  split: the forward, which splits a tail of at
+    most half a round over the hidden dimension instead when it can."""
     nrt = -(-R // 256)
     tiles = -(-V // 256) * nrt
     dp, tail = tiles // cus * cus, tiles % cus
-    if dp == 0 or tail == 0 or tail_part_bytes(R, H, V) or nrt > 4:
+    if dp == 0 or tail == 0 or (split and tail_part_bytes(R, H, V)) or nrt > 4:
         return None
     vt0 = dp // nrt
-    n = -(-(V - vt0 * 256) // width)
-    return (vt0, n) if n * nrt <= cus else None
+    for width in (128, 192):
+        n = -(-(V - vt0 * 256) // width)
+        if n * nrt <= cus:
+            return (vt0, n)
+    return None
 
 
 def test_logprob_workspace_size():
@@ -250,6 +255,11 @@ def test_logprob_workspace_size():
     assert narrow_tiles(1000, 512, 25500) == (64, 48)
     assert narrow_tiles(1200, 512, 20000) is None         # 5 row tiles
     assert narrow_tiles(200, 512, 55000) is None          # 215 tiles: no full round
+    # a tail too short in hidden steps to split: 44 tiles as 88 tiles 128 wide
+    assert narrow_tiles(256, 256, 76800) == (256, 88)
+    # the sampling head never splits: at 32B-class rows its 82-tile tail runs
+    # as 163 tiles 128 wide (20864 entries)
+    assert narrow_tiles(256, 5120, 151936, split=False) == (512, 163)
     # the 32B-class decode step (594 tiles: 2 rounds + 82) splits its tail
     # 3 ways; the 8B-class one (1188 tiles: 4 rounds + 164) does not split
     assert tail_part_bytes(256, 5120, 151936) == 82 * 3 * 256 * 256 * 4
@@ -467,6 +477,11 @@ def test_sample_workspace_size():
     assert narrow_tiles(512, 4096, V) == (512, 109)
     n = rk.sample_top_p_workspace_size(512, 4096, V)
     assert n >= 512 * ld * 4 + slots * 512 * 4 and n < 512 * ld * 4 + slots * 512 * 4 + 512
+    # at 256 rows, 163 tiles 128 wide: 512 + 163 slots
+    assert narrow_tiles(256, 5120, V, split=False) == (512, 163)
+    n = rk.sample_top_p_workspace_size(256, 5120, V)
+    slots = 512 + 163
+    assert n >= 256 * ld * 4 + slots * 256 * 4 and n < 256 * ld * 4 + slots * 256 * 4 + 512
     assert rk.sample_top_p_workspace_size(100000, 4096, V) == rk.sample_top_p_workspace_size(8192, 4096, V)
     assert rk.sample_top_p_workspace_size(0, 64, 10) == 0
 

@@ -40,6 +40,7 @@ SHAPES = [
     (4097, 192, 77777, 0),    # wave combine; ragged vocab tile
     (8000, 4096, 2500, 0),    # tail parts: 320 tiles, the last 64 split 4 ways over the hidden dimension
     (300, 512, 40000, 1),     # tail parts: 314 tiles, the last 58 split 2 ways; ragged rows and vocab
+    (256, 256, 76800, 1),     # too few hidden steps to split: the last 44 tiles as 88 narrow tiles 128 wide
 ]
 
 
@@ -131,7 +132,7 @@ def test_invalid_arguments():
 # (rows, hidden, vocab, every_stage)
 SAMPLE_SHAPES = [
     (512, 4096, V, 0),        # 8B-class decode step: whole tiles + a narrow last round of 109 x 2 tiles
-    (256, 5120, V, 0),        # 32B-class decode step: the last 82 tiles as 110 narrow tiles
+    (256, 5120, V, 0),        # 32B-class decode step: the last 82 tiles as 163 narrow tiles 128 wide
     (300, 512, 51001, 1),     # 2 row tiles, narrow tiles ending past the vocabulary
     (300, 128, 1000, 1),      # one round, ragged rows and vocab
     (8192 + 300, 64, 300, 1), # two row chunks of logits
@@ -159,7 +160,7 @@ SAMPLE_TIGHT = {"hidden": 0, "w_lm": 1, "inv_temperature": 2, "uniform": 3, "tok
                 "row maxima": 8}
 
 
-@pytest.mark.parametrize("rows,hidden,vocab", [(512, 4096, V), (300, 128, 1000), (8192 + 300, 64, 300)])
+@pytest.mark.parametrize("rows,hidden,vocab", [(512, 4096, V), (256, 5120, V), (300, 128, 1000), (8192 + 300, 64, 300)])
 def test_shrunk_allocation_is_caught_sampling(rows, hidden, vocab):
     assert replay(2, rows, hidden, vocab).regions == 9
     for name, i in SAMPLE_TIGHT.items():

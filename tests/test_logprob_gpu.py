@@ -79,13 +79,16 @@ def test_split_tail(R, H, V):
     assert lp[2] == 0 and np.isnan(lp[3])
 
 
-@pytest.mark.parametrize("R,H,V,vt0,n", [(300, 512, 51001, 128, 95),     # 2 row tiles, ragged rows
-                                         (600, 512, 35700, 85, 73),      # 3 row tiles: 255 whole tiles
-                                         (1000, 512, 25500, 64, 48)])    # 4 row tiles
-def test_narrow_last_round(R, H, V, vt0, n):
-    """A last round more than half full runs as tiles 192 entries wide over
-    vocab [256 vt0, V), each with its own partial slot; targets on both sides
-    of the boundary, on narrow-tile edges, in the ragged last narrow tile, a
+@pytest.mark.parametrize("R,H,V,vt0,n,width", [(300, 512, 51001, 128, 95, 192),     # 2 row tiles, ragged rows
+                                               (600, 512, 35700, 85, 73, 192),      # 3 row tiles: 255 whole tiles
+                                               (1000, 512, 25500, 64, 48, 192),     # 4 row tiles
+                                               (256, 256, 76800, 256, 88, 128),     # too few hidden steps to split
+                                               (400, 64, 40000, 128, 57, 128)])     # 2 row tiles, past the vocabulary
+def test_narrow_last_round(R, H, V, vt0, n, width):
+    """A partial last round that cannot be split over the hidden dimension
+    runs as tiles 128 (if they fit one round) or 192 entries wide over vocab
+    [256 vt0, V), each with its own partial slot; targets on both sides of
+    the boundary, on narrow-tile edges, in the ragged last narrow tile, a
     masked row and an invalid id go through it."""
     rng = np.random.Generator(np.random.PCG64(R * 11 + V))
     h = rand_bits(rng, (R, H))
@@ -93,7 +96,8 @@ def test_narrow_last_round(R, H, V, vt0, n):
     t = rng.integers(0, V, R).astype(np.int32)
     v0 = vt0 * 256
     t[: R // 3] = rng.integers(v0, V, R // 3)
-    edges = [v0 - 1, v0, v0 + 191, v0 + 192, v0 + 96, v0 + 95, v0 + 192 * (n - 1), V - 1, -1, V]
+    edges = [v0 - 1, v0, v0 + width - 1, v0 + width, v0 + width // 2, v0 + width // 2 - 1, v0 + width * (n - 1),
+             V - 1, -1, V]
     t[: len(edges)] = edges
     lp, lse = check(h, w, t, 1.0 / 0.9, f"narrow last round {R}x{H}x{V}")
     assert lp[8] == 0 and np.isnan(lp[9])

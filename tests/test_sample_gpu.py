@@ -92,7 +92,11 @@ def test_tiny_config():
                                               # narrow last rounds: 95 x 2 tiles 192 wide, the last
                                               # ending 64 entries past V (a multiple of 256); 48 x 4
                                               (300, 128, 50944, 0.3, 0.9),
-                                              (1000, 64, 25500, 0.3, 0.9)])
+                                              (1000, 64, 25500, 0.3, 0.9),
+                                              # 128 wide: 88 x 1 tiles; 57 x 2, the last ending 64
+                                              # entries past V
+                                              (256, 128, 76800, 0.3, 0.9),
+                                              (400, 64, 40000, 0.3, 0.9)])
 def test_shapes(R, H, V, wstd, top_p):
     rng = np.random.Generator(np.random.PCG64(R + H + V))
     hb, wb = rand_bits(rng, (R, H)), rand_bits(rng, (V, H), wstd)
